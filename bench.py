@@ -1,0 +1,230 @@
+"""Benchmark of one eviction pass over a whole batch on one MI355X.
+
+A step is the full hot path over every layer of the workload: window row statistics, per-token
+mean/dispersion, greedy selection and cache compaction (kv_window_mu_sigma, kv_mmr_select,
+kv_compact_cache), with every input already resident in HBM.  Default workload: 32 layers of a
+Mistral-7B-shaped cache (32 query / 8 kv heads, d=128, bf16), L=32768, W=32, B=64, quadratic
+lambda2 depth profile.
+
+Before every timed step a 512 MiB buffer is overwritten (outside the timed region) so that no part
+of the 2 GiB key cache is served from the 256 MB last-level cache.  Each step is timed with HIP
+events on the launch stream, per entry point and in total; rank 0 prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+WORKLOADS = ("mistral32_L32768_W32_B64", "mistral32_L8192_W32_B64", "mistral_layer_L4096_W32_B64")
+
+
+def make_workload(name: str):
+    from paper_2609_30738_amd import workloads as W
+    if name == "mistral32_L32768_W32_B64":
+        return W.mistral_pass_32k()
+    if name == "mistral32_L8192_W32_B64":
+        return W.mistral_pass_8k(64)
+    if name == "mistral_layer_L4096_W32_B64":
+        return W.mistral_layer()
+    raise SystemExit(f"unknown workload {name}; choose from {WORKLOADS}")
+
+
+def lambdas(wl):
+    """Per-problem coefficients from the library's depth-profile entry point."""
+    from paper_2609_30738_amd import _lib
+    l1 = _lib.depth_profile(wl.lam1.family, wl.lam1.params, wl.n_layers)
+    l2 = _lib.depth_profile(wl.lam2.family, wl.lam2.params, wl.n_layers)
+    idx = [wl.layer_of(p) for p in range(wl.n_prob)]
+    return l1[idx], l2[idx]
+
+
+def algorithmic_bytes(wl) -> dict:
+    """Bytes the method must move per pass: K once and Q_W once (scoring), the kept
+    rows of K and V read and written (compaction) and the admitted indices."""
+    e = 2 if wl.dtype == "bf16" else 4
+    lens = wl.lens.astype(np.int64)
+    n = wl.n_prob
+    keys = int(lens.sum()) * wl.h_kv * wl.d * e
+    queries = n * wl.w * wl.h_q * wl.d * e
+    kept = n * 2 * 2 * (wl.budget + wl.w) * wl.h_kv * wl.d * e
+    idx = n * 4 * wl.budget * wl.h_kv
+    return {"scoring": keys + queries, "total": keys + queries + kept + idx}
+
+
+def source_sha() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_30738_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was taken on the
+    current kernel sources (null otherwise)."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_sha") != source_sha():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(wl, packed_layers, n_layers_sample: int) -> dict:
+    """The CPU oracle, as it stands, on a bounded sample (the first layers), scaled to ms/pass."""
+    from oracle import evict, profiles
+    lam1 = profiles.layer_lambdas(wl.lam1.family, wl.lam1.params, wl.n_layers)
+    lam2 = profiles.layer_lambdas(wl.lam2.family, wl.lam2.params, wl.n_layers)
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    t0 = time.perf_counter()
+    for j, (q, k, v) in enumerate(packed_layers[:n_layers_sample]):
+        layer = wl.layer_of(j)
+        evict.evict_problem(q, k, v, wl.dtype, wl.scale, lam1[layer], lam2[layer], wl.budget)
+    dt = time.perf_counter() - t0
+    per_pass_ms = dt / n_layers_sample * wl.n_prob * 1e3
+    return {"value": round(per_pass_ms, 1), "unit": "ms", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{n_layers_sample} of {wl.n_prob} layers of {wl.name} "
+                      f"({dt:.1f} s), scaled to the full pass"}
+
+
+def main() -> None:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=WORKLOADS[0], choices=WORKLOADS)
+    ap.add_argument("--cpu-layers", type=int, default=3,
+                    help="layers of the oracle sample for the CPU baseline (0: skip)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="time kv_window_scores + kv_mu_sigma instead of kv_window_mu_sigma")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        raise SystemExit(2)
+
+    import torch
+    from paper_2609_30738_amd import _lib, api, workloads
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    torch.cuda.set_device(0)
+    _lib.lib()  # fail loudly if the library is missing
+
+    wl = make_workload(args.workload)
+    t_gen = time.perf_counter()
+    packed = workloads.draw_packed(wl)
+    lam1, lam2 = lambdas(wl)
+    inp = api.upload(wl.dtype, wl.h_q, wl.h_kv, wl.d, wl.w, packed.q_win, packed.k, packed.v,
+                     packed.lens, packed.tok_off, lam1, lam2)
+    out = api.allocate(inp, wl.budget)
+    gen_s = time.perf_counter() - t_gen
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+    b = inp.batch
+
+    names = ["scoring", "select", "compact"]
+
+    def step(evs):
+        evs[0].record(stream)
+        if args.unfused:
+            _lib.window_scores(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.ws)
+            _lib.mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
+                          out.sigma)
+        else:
+            _lib.window_mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum,
+                                 out.mu, out.sigma, out.ws)
+        evs[1].record(stream)
+        _lib.mmr_select(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2, wl.budget, 4,
+                        wl.w, out.sel_idx, None, None, None, out.ws)
+        evs[2].record(stream)
+        _lib.compact_cache(b, inp.k, inp.v, out.sel_idx, wl.budget, wl.w, out.k_out, out.v_out)
+        evs[3].record(stream)
+
+    def new_events():
+        return [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+
+    for _ in range(args.warmup):
+        flush.zero_()
+        step(new_events())
+    torch.cuda.synchronize()
+    print(f"# inputs drawn and uploaded in {gen_s:.1f} s; warmup done", file=sys.stderr,
+          flush=True)
+
+    all_events = []
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    for _ in range(args.steps):
+        flush.zero_()  # outside the events: evicts the key cache from the last-level cache
+        evs = new_events()
+        step(evs)
+        all_events.append(evs)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+
+    per = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(3)] for e in all_events])
+    step_ms = per.sum(axis=1)
+    ms = float(step_ms.mean())
+    mean_part = per.mean(axis=0)
+    ab = algorithmic_bytes(wl)
+    # dominant kernel: the scoring pass streams the whole key cache
+    dom = "window_mu_sigma" if not args.unfused else "window_scores+mu_sigma"
+    achieved = ab["scoring"] / (mean_part[0] * 1e-3) / 1e9
+    traffic = measured_traffic("window_mu_sigma", wl.name) if not args.unfused else None
+    line = {
+        "metric": "ms per 32-layer eviction pass at L=32k,W=32,B=64; HBM GB/s vs peak",
+        "value": round(ms, 4),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded; Mistral-7B-shaped cache, planted sink, near-duplicate "
+                "clusters and repeated passages)",
+        "config": {"workload": wl.name, "layers": wl.n_layers, "L": int(wl.seq_lens[0]),
+                   "W": wl.w, "B": wl.budget, "h_q": wl.h_q, "h_kv": wl.h_kv, "d": wl.d,
+                   "lambda2_profile": wl.lam2.family, "parallelism": "single GPU"},
+        "pass_GBps": round(ab["total"] / (ms * 1e-3) / 1e9, 1),
+        "pass_frac_of_hbm_peak": round(ab["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "breakdown_ms": {n: round(float(v), 4) for n, v in zip(names, mean_part)},
+        "step_ms_min_max": [round(float(step_ms.min()), 4), round(float(step_ms.max()), 4)],
+        "wall_s_timed_loop": round(wall, 3),
+        "roofline": {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic},
+    }
+    if args.cpu_layers > 0:
+        layers = []
+        for j in range(min(args.cpu_layers, wl.n_prob)):
+            L = int(packed.lens[j])
+            off = int(packed.tok_off[j]) * wl.h_kv * wl.d
+            n = L * wl.h_kv * wl.d
+            layers.append((packed.q_win[j], packed.k[off:off + n].reshape(wl.h_kv, L, wl.d),
+                           packed.v[off:off + n].reshape(wl.h_kv, L, wl.d)))
+        line["cpu_baseline"] = cpu_baseline(wl, layers, len(layers))
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

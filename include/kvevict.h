@@ -1,0 +1,169 @@
+/*
+ * kvevict.h -- C ABI of the diversity-aware, layer-wise KV-cache eviction path on AMD Instinct
+ * MI355X (gfx950).
+ *
+ * Method: "Beyond Mean Attention: Diversity-Aware, Layer-Wise Scoring for KV Cache Eviction".
+ * After prefill, for every layer and kv head, the last W queries (the observation window) attend to
+ * all L cached keys (section 3.1).  Each cached token i gets its mean attention mu_i (Eq. (1)) and
+ * its sample dispersion sigma_i over the window queries (Eq. (3)).  B tokens are then admitted
+ * greedily under s~_i + lambda2 corr(i, S), where s~ is the per-head normalised base score
+ * s_i = mu_i + lambda1 sigma_i and corr(i, S) the clamped maximum cosine of key i to the admitted
+ * keys (Eq. (2), (4), (5)); candidates are restricted to the top 4B base scores.  The per-layer
+ * coefficients come from a depth profile (section 3.3, Eq. (6)).  Finally the kept rows of K and V
+ * are compacted.
+ *
+ * Conventions shared by every entry point
+ *   - A "problem" is one layer of one sequence.  A batch holds n_prob problems; problem p has
+ *     context length L_p and its keys/values start at packed token offset tok_off[p].
+ *   - Every tensor pointer is a caller-owned DEVICE pointer unless its name ends in _host.  The
+ *     library never allocates or frees device memory; scratch comes from the caller's workspace.
+ *   - Calls are asynchronous: after host-side validation they enqueue kernels on `stream` (a
+ *     hipStream_t passed as void*, NULL = default stream) and return.  Device faults surface at the
+ *     caller's next synchronisation.
+ *   - On invalid arguments a call returns a negative KV_ERR_* code and launches nothing.  A launch
+ *     failure returns KV_ERR_LAUNCH (work enqueued before the failing launch may still run).
+ *   - Calls on one stream are ordered; calls that share output or workspace buffers must not run
+ *     concurrently on different streams.
+ *
+ * Layouts (row-major; e = element size: 4 for KV_F32, 2 for KV_BF16 = raw bfloat16 bits)
+ *   q_win   [n_prob][h_q][w][d]         window queries (positions L_p-w .. L_p-1); q-head h uses
+ *                                       kv-head h / (h_q / h_kv)
+ *   k, v    problem p at element offset tok_off[p]*h_kv*d, layout [h_kv][L_p][d] (keys after RoPE)
+ *   row_max, row_sum  [n_prob][h_q][w]  fp32
+ *   mu, sigma  problem p at tok_off[p]*h_kv, layout [h_kv][L_p], fp32
+ *   attn    problem p at tok_off[p]*h_q*w, layout [h_q][w][L_p], fp32
+ *   lambda1, lambda2  [n_prob] fp32
+ *   sel_idx, sel_score [n_prob][h_kv][budget]
+ *   cand_idx, cand_corr [n_prob][h_kv][cand_stride], cand_stride from kv_candidate_stride()
+ *   k_out, v_out [n_prob][h_kv][budget + keep_tail][d], same dtype as k and v
+ *
+ * Supported shapes: d in {64, 128}; 2 <= w; h_q % h_kv == 0; G*w <= 128 with G = h_q / h_kv;
+ * L_p >= w + 1 and L_p <= 2^24; 1 <= budget <= L_p - keep_tail; keep_tail in [0, L_p - 1].
+ */
+#ifndef KVEVICT_H
+#define KVEVICT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---------------------------------------------------------------------------- */
+#define KV_OK 0
+#define KV_ERR_NULL (-1)      /* a required pointer is NULL                                     */
+#define KV_ERR_SHAPE (-2)     /* head layout, window, length or candidate count not supported   */
+#define KV_ERR_DTYPE (-3)     /* dtype is neither KV_F32 nor KV_BF16                            */
+#define KV_ERR_BUDGET (-4)    /* budget < 1 or budget > L_p - keep_tail for some problem        */
+#define KV_ERR_WORKSPACE (-5) /* workspace smaller than kv_workspace_bytes() asks for           */
+#define KV_ERR_LAUNCH (-6)    /* a HIP launch or device query failed                            */
+#define KV_ERR_ARG (-7)       /* any other invalid argument (n_prob, profile family, params)    */
+
+/* ---- element types --------------------------------------------------------------------------- */
+#define KV_F32 0
+#define KV_BF16 1
+
+/* ---- depth-profile families (section 3.3) ----------------------------------------------------- */
+#define KV_PROFILE_GLOBAL 0   /* a(l) = a0                                   (1 parameter)      */
+#define KV_PROFILE_SEGMENTS 1 /* a(l) = a[floor(n_seg * l / n_layers)]       (n_seg parameters) */
+#define KV_PROFILE_CURVE 2    /* a(l) = c0 + c1 t + c2 t^2, t = l/(n_layers-1) (3 parameters)   */
+
+/* Shape of a batch of problems.  len_host/tok_off_host drive validation and grid sizing; the
+ * kernels read len_dev/tok_off_dev, which must hold the same values. */
+typedef struct kv_problem {
+  int32_t dtype;  /* KV_F32 or KV_BF16 (q_win, k and v share it)                             */
+  int32_t n_prob; /* number of problems, >= 1                                                */
+  int32_t h_q;    /* query heads                                                             */
+  int32_t h_kv;   /* key/value heads                                                         */
+  int32_t d;      /* head dimension                                                          */
+  int32_t w;      /* observation-window size |W|                                             */
+  const int32_t* len_host;     /* [n_prob] context lengths (host)                              */
+  const int64_t* tok_off_host; /* [n_prob] packed token offsets (host)                         */
+  const int32_t* len_dev;      /* [n_prob] same lengths (device)                               */
+  const int64_t* tok_off_dev;  /* [n_prob] same offsets (device)                               */
+} kv_problem;
+
+/* Human-readable text of a status code (static storage, never NULL). */
+const char* kv_strerror(int status);
+
+/* ABI version, currently 1. */
+int kv_version(void);
+
+/* Bytes of device workspace the calls below need for this batch (kv_window_scores,
+ * kv_window_mu_sigma and kv_mmr_select; kv_mu_sigma and kv_compact_cache need none).  Returns 0
+ * for invalid arguments.  The workspace must be 256-byte aligned; its contents need no
+ * initialisation and are not preserved between calls. */
+size_t kv_workspace_bytes(const kv_problem* pr, int32_t budget, int32_t cand_mult,
+                          int32_t keep_tail);
+
+/* Row stride of cand_idx / cand_corr: cand_mult * budget, or the largest candidate count
+ * max_p(L_p - keep_tail) when cand_mult == 0.  Returns 0 for invalid arguments. */
+int32_t kv_candidate_stride(const kv_problem* pr, int32_t budget, int32_t cand_mult,
+                            int32_t keep_tail);
+
+/* Observation-window logits and row-softmax statistics (section 3.1).
+ * For every problem p, q-head h and window row r (absolute position L_p - w + r), over the keys
+ * i <= L_p - w + r of kv-head h / G (causal mask), with l_i = scale * <q[p,h,r], k[p,g,i]>:
+ *   row_max[p,h,r] = max_i l_i,   row_sum[p,h,r] = sum_i exp(l_i - row_max[p,h,r]).
+ * scale is the softmax scale (1/sqrt(d) for scaled dot-product attention).  Logits are computed
+ * from the stored inputs with fp32 accumulation and never leave the chip.  Needs workspace. */
+int kv_window_scores(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                     float* row_max, float* row_sum, void* ws, size_t ws_bytes, void* stream);
+
+/* Per-token mean and dispersion of the window attention (Eq. (1), Eq. (3)).
+ * A[p,h,r,i] = exp(l - row_max) / row_sum (0 where masked), from the statistics of
+ * kv_window_scores.  The G query heads that share a kv head are averaged,
+ * a[r,i] = mean_h A[h,r,i]; then mu[i] = mean_r a[r,i] and
+ * sigma[i] = sqrt(sum_r (a[r,i] - mu[i])^2 / (w - 1)), for every position i < L_p.
+ * attn (nullable) receives A itself.  All fp32.  Needs no workspace. */
+int kv_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                const float* row_max, const float* row_sum, float* mu, float* sigma,
+                float* attn, void* stream);
+
+/* kv_window_scores followed by kv_mu_sigma (without attn): same results in one call.  Needs
+ * workspace. */
+int kv_window_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                       float* row_max, float* row_sum, float* mu, float* sigma, void* ws,
+                       size_t ws_bytes, void* stream);
+
+/* Greedy diversity-aware selection (Eq. (2), (4), (5); section 3.2), per problem p and kv head g:
+ *   candidates i in [0, n_cand), n_cand = L_p - keep_tail (the last keep_tail positions are always
+ *   kept and never compete);
+ *   s_i = mu_i + lambda1[p] * sigma_i (one fp32 rounding); s~_i = s_i / max(max_j s_j, 1e-12);
+ *   the candidate set P is the C = min(cand_mult * budget, n_cand) largest s (cand_mult = 0: all
+ *   n_cand), ties to the lower position;
+ *   then `budget` times: admit argmax_{i in P \ S} s~_i + lambda2[p] * corr_i (ties to the lower
+ *   position), where corr_i = max(0, max_{j in S} cos(k_i, k_j)) is a running maximum updated
+ *   against each newly admitted key; a zero key has cosine 0.
+ * Outputs: sel_idx[p,g,t] = position admitted at step t (admission order); sel_score (nullable) =
+ * its score s~ + lambda2 corr; cand_idx (nullable) = P in ascending position order, padded with -1;
+ * cand_corr (nullable) = each candidate's corr when it was admitted or, if never admitted, after the
+ * last step (padding 0).  Decisions are taken in fp32.  Needs workspace.
+ * Limit: C * d * e <= 131072 bytes (C <= 512 for bf16 keys of dimension 128). */
+int kv_mmr_select(const kv_problem* pr, const float* mu, const float* sigma, const void* k,
+                  const float* lambda1, const float* lambda2, int32_t budget, int32_t cand_mult,
+                  int32_t keep_tail, int32_t* sel_idx, float* sel_score, int32_t* cand_idx,
+                  float* cand_corr, void* ws, size_t ws_bytes, void* stream);
+
+/* Compacted cache (sections 1 and 3.1: each layer keeps `budget` entries plus the kept tail);
+ * budget <= 8192.
+ * For every problem and kv head, rows 0..budget-1 of k_out/v_out are the rows of k/v at the
+ * selected positions in ascending order, rows budget..budget+keep_tail-1 the last keep_tail
+ * positions.  Byte-exact copies.  A selected position outside [0, L_p) leaves its output row
+ * unwritten.  Needs no workspace. */
+int kv_compact_cache(const kv_problem* pr, const void* k, const void* v, const int32_t* sel_idx,
+                     int32_t budget, int32_t keep_tail, void* k_out, void* v_out, void* stream);
+
+/* Per-layer coefficients of a depth profile (section 3.3, Eq. (6)), host-only:
+ * lambda_out_host[l] = (float) sinh(a(l)) for l = 0..n_layers-1, a(l) given by `family` and the
+ * latent parameters `params_host` (n_params values).  Returns KV_ERR_ARG for an unknown family or
+ * a wrong parameter count, KV_ERR_NULL for NULL pointers. */
+int kv_depth_profile(int32_t family, const double* params_host, int32_t n_params,
+                     int32_t n_layers, float* lambda_out_host);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVEVICT_H */

@@ -1,0 +1,212 @@
+"""ctypes binding of libkvevict.so, with the same names as the C ABI (include/kvevict.h).
+
+Argument marshalling only: every function checks that tensors are contiguous device tensors,
+passes their addresses and the current HIP stream, and raises KvError on a negative status.  All
+computation happens in the library's gfx950 kernels.  Loading fails loudly if the library has not
+been built; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+KV_OK = 0
+KV_ERR_NULL = -1
+KV_ERR_SHAPE = -2
+KV_ERR_DTYPE = -3
+KV_ERR_BUDGET = -4
+KV_ERR_WORKSPACE = -5
+KV_ERR_LAUNCH = -6
+KV_ERR_ARG = -7
+
+KV_F32 = 0
+KV_BF16 = 1
+
+KV_PROFILE_GLOBAL = 0
+KV_PROFILE_SEGMENTS = 1
+KV_PROFILE_CURVE = 2
+PROFILE_FAMILIES = {"global": KV_PROFILE_GLOBAL, "segments": KV_PROFILE_SEGMENTS,
+                    "curve": KV_PROFILE_CURVE}
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvevict.so")
+
+SYMBOLS = ("kv_strerror", "kv_version", "kv_workspace_bytes", "kv_candidate_stride",
+           "kv_window_scores", "kv_mu_sigma", "kv_window_mu_sigma", "kv_mmr_select",
+           "kv_compact_cache", "kv_depth_profile")
+
+
+class KvError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {strerror(status)} (status {status})")
+
+
+class KvProblem(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("n_prob", ctypes.c_int32), ("h_q", ctypes.c_int32),
+                ("h_kv", ctypes.c_int32), ("d", ctypes.c_int32), ("w", ctypes.c_int32),
+                ("len_host", ctypes.c_void_p), ("tok_off_host", ctypes.c_void_p),
+                ("len_dev", ctypes.c_void_p), ("tok_off_dev", ctypes.c_void_p)]
+
+
+_LIB = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (raises if it has not been built)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        h = ctypes.CDLL(LIB_PATH)
+        vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        pr = ctypes.POINTER(KvProblem)
+        h.kv_strerror.argtypes = [ctypes.c_int]
+        h.kv_strerror.restype = ctypes.c_char_p
+        h.kv_version.argtypes = []
+        h.kv_version.restype = ctypes.c_int
+        h.kv_workspace_bytes.argtypes = [pr, i32, i32, i32]
+        h.kv_workspace_bytes.restype = sz
+        h.kv_candidate_stride.argtypes = [pr, i32, i32, i32]
+        h.kv_candidate_stride.restype = i32
+        h.kv_window_scores.argtypes = [pr, vp, vp, ctypes.c_float, vp, vp, vp, sz, vp]
+        h.kv_mu_sigma.argtypes = [pr, vp, vp, ctypes.c_float, vp, vp, vp, vp, vp, vp]
+        h.kv_window_mu_sigma.argtypes = [pr, vp, vp, ctypes.c_float, vp, vp, vp, vp, vp, sz, vp]
+        h.kv_mmr_select.argtypes = [pr, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, sz,
+                                    vp]
+        h.kv_compact_cache.argtypes = [pr, vp, vp, vp, i32, i32, vp, vp, vp]
+        h.kv_depth_profile.argtypes = [i32, ctypes.POINTER(ctypes.c_double), i32, i32,
+                                       ctypes.POINTER(ctypes.c_float)]
+        for name in ("kv_window_scores", "kv_mu_sigma", "kv_window_mu_sigma", "kv_mmr_select",
+                     "kv_compact_cache", "kv_depth_profile"):
+            getattr(h, name).restype = ctypes.c_int
+        _LIB = h
+    return _LIB
+
+
+def strerror(status: int) -> str:
+    return lib().kv_strerror(int(status)).decode()
+
+
+def version() -> int:
+    return int(lib().kv_version())
+
+
+def _check(status: int, where: str) -> None:
+    if status != KV_OK:
+        raise KvError(status, where)
+
+
+class Batch:
+    """Shape of a batch of problems (one problem = one layer of one sequence).
+
+    Holds the host lengths/offsets and their device copies and exposes the kv_problem struct.
+    """
+
+    def __init__(self, dtype: str, h_q: int, h_kv: int, d: int, w: int, lens: Sequence[int],
+                 tok_off: Optional[Sequence[int]] = None, device=None):
+        import torch
+        self.dtype_name = dtype
+        self.h_q, self.h_kv, self.d, self.w = int(h_q), int(h_kv), int(d), int(w)
+        self.lens_host = np.ascontiguousarray(np.asarray(lens, dtype=np.int32))
+        if tok_off is None:
+            off = np.zeros(len(self.lens_host), dtype=np.int64)
+            if len(off) > 1:
+                off[1:] = np.cumsum(self.lens_host.astype(np.int64))[:-1]
+        else:
+            off = np.asarray(tok_off, dtype=np.int64)
+        self.tok_off_host = np.ascontiguousarray(off)
+        dev = torch.device("cuda") if device is None else torch.device(device)
+        self.lens_dev = torch.from_numpy(self.lens_host).to(dev)
+        self.tok_off_dev = torch.from_numpy(self.tok_off_host).to(dev)
+        self.struct = KvProblem(KV_BF16 if dtype == "bf16" else KV_F32, len(self.lens_host),
+                                self.h_q, self.h_kv, self.d, self.w,
+                                self.lens_host.ctypes.data, self.tok_off_host.ctypes.data,
+                                self.lens_dev.data_ptr(), self.tok_off_dev.data_ptr())
+
+    @property
+    def n_prob(self) -> int:
+        return len(self.lens_host)
+
+    @property
+    def total_tokens(self) -> int:
+        return int(self.lens_host.astype(np.int64).sum())
+
+    def ref(self):
+        return ctypes.byref(self.struct)
+
+
+def _ptr(t) -> ctypes.c_void_p:
+    if t is None:
+        return ctypes.c_void_p(0)
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError("tensors passed to the library must be contiguous device tensors")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def workspace_bytes(batch: Batch, budget: int, cand_mult: int = 4,
+                    keep_tail: Optional[int] = None) -> int:
+    tail = batch.w if keep_tail is None else keep_tail
+    return int(lib().kv_workspace_bytes(batch.ref(), budget, cand_mult, tail))
+
+
+def candidate_stride(batch: Batch, budget: int, cand_mult: int = 4,
+                     keep_tail: Optional[int] = None) -> int:
+    tail = batch.w if keep_tail is None else keep_tail
+    return int(lib().kv_candidate_stride(batch.ref(), budget, cand_mult, tail))
+
+
+def window_scores(batch: Batch, q_win, k, scale: float, row_max, row_sum, ws,
+                  stream=None) -> None:
+    _check(lib().kv_window_scores(batch.ref(), _ptr(q_win), _ptr(k), float(scale), _ptr(row_max),
+                                  _ptr(row_sum), _ptr(ws), 0 if ws is None else ws.numel() *
+                                  ws.element_size(), _stream(stream)), "kv_window_scores")
+
+
+def mu_sigma(batch: Batch, q_win, k, scale: float, row_max, row_sum, mu, sigma, attn=None,
+             stream=None) -> None:
+    _check(lib().kv_mu_sigma(batch.ref(), _ptr(q_win), _ptr(k), float(scale), _ptr(row_max),
+                             _ptr(row_sum), _ptr(mu), _ptr(sigma), _ptr(attn), _stream(stream)),
+           "kv_mu_sigma")
+
+
+def window_mu_sigma(batch: Batch, q_win, k, scale: float, row_max, row_sum, mu, sigma, ws,
+                    stream=None) -> None:
+    _check(lib().kv_window_mu_sigma(batch.ref(), _ptr(q_win), _ptr(k), float(scale),
+                                    _ptr(row_max), _ptr(row_sum), _ptr(mu), _ptr(sigma), _ptr(ws),
+                                    0 if ws is None else ws.numel() * ws.element_size(),
+                                    _stream(stream)), "kv_window_mu_sigma")
+
+
+def mmr_select(batch: Batch, mu, sigma, k, lambda1, lambda2, budget: int, cand_mult: int,
+               keep_tail: int, sel_idx, sel_score=None, cand_idx=None, cand_corr=None, ws=None,
+               stream=None) -> None:
+    _check(lib().kv_mmr_select(batch.ref(), _ptr(mu), _ptr(sigma), _ptr(k), _ptr(lambda1),
+                               _ptr(lambda2), int(budget), int(cand_mult), int(keep_tail),
+                               _ptr(sel_idx), _ptr(sel_score), _ptr(cand_idx), _ptr(cand_corr),
+                               _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+                               _stream(stream)), "kv_mmr_select")
+
+
+def compact_cache(batch: Batch, k, v, sel_idx, budget: int, keep_tail: int, k_out, v_out,
+                  stream=None) -> None:
+    _check(lib().kv_compact_cache(batch.ref(), _ptr(k), _ptr(v), _ptr(sel_idx), int(budget),
+                                  int(keep_tail), _ptr(k_out), _ptr(v_out), _stream(stream)),
+           "kv_compact_cache")
+
+
+def depth_profile(family: str, params: Sequence[float], n_layers: int) -> np.ndarray:
+    """lambda per layer (float32) from a Global / Segments / Curve latent profile."""
+    fam = PROFILE_FAMILIES[family] if isinstance(family, str) else int(family)
+    p = (ctypes.c_double * len(params))(*[float(x) for x in params])
+    out = (ctypes.c_float * n_layers)()
+    _check(lib().kv_depth_profile(fam, p, len(params), int(n_layers), out), "kv_depth_profile")
+    return np.frombuffer(out, dtype=np.float32).copy()

@@ -1,0 +1,240 @@
+// C ABI of the eviction path: host-side validation, workspace sizing and dispatch to the gfx950
+// kernels.  Nothing here allocates device memory, keeps state between calls or launches anything
+// before every argument has been checked.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "kernels.h"
+#include "kvevict.h"
+
+namespace {
+
+constexpr int kMaxLen = 1 << 24;
+constexpr int kMaxGrid = 65535;
+constexpr int kMaxCompactBudget = 8192;
+constexpr size_t kWsAlign = 256;
+
+size_t align_up(size_t x) { return (x + kWsAlign - 1) & ~(kWsAlign - 1); }
+
+int elem_bytes(int dtype) { return dtype == KV_BF16 ? 2 : 4; }
+
+bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
+
+// Checks shared by every entry point; fills the launch shape.
+int check_problem(const kv_problem* pr, kv::Shape* s) {
+  if (!pr) return KV_ERR_NULL;
+  if (pr->dtype != KV_F32 && pr->dtype != KV_BF16) return KV_ERR_DTYPE;
+  if (pr->n_prob < 1 || pr->n_prob > kMaxGrid) return KV_ERR_ARG;
+  if (!pr->len_host || !pr->tok_off_host || !pr->len_dev || !pr->tok_off_dev) return KV_ERR_NULL;
+  if (pr->h_kv < 1 || pr->h_q < pr->h_kv || pr->h_q % pr->h_kv != 0 || pr->h_kv > kMaxGrid)
+    return KV_ERR_SHAPE;
+  if (pr->d != 64 && pr->d != 128) return KV_ERR_SHAPE;
+  if (pr->w < 2) return KV_ERR_SHAPE;
+  const int64_t rows = (int64_t)(pr->h_q / pr->h_kv) * pr->w;
+  if (rows > 128) return KV_ERR_SHAPE;
+  if (pr->w != 32 && rows > 64) return KV_ERR_SHAPE;
+  int max_len = 0;
+  for (int p = 0; p < pr->n_prob; ++p) {
+    const int L = pr->len_host[p];
+    if (L < pr->w + 1 || L > kMaxLen) return KV_ERR_SHAPE;
+    if (pr->tok_off_host[p] < 0) return KV_ERR_SHAPE;
+    if (L > max_len) max_len = L;
+  }
+  s->dtype = pr->dtype == KV_BF16 ? kv::kDtBf16 : kv::kDtF32;
+  s->n_prob = pr->n_prob;
+  s->h_q = pr->h_q;
+  s->h_kv = pr->h_kv;
+  s->d = pr->d;
+  s->w = pr->w;
+  s->max_len = max_len;
+  s->lens = pr->len_dev;
+  s->tok_off = pr->tok_off_dev;
+  if (s->max_chunks() > kMaxGrid) return KV_ERR_SHAPE;
+  return KV_OK;
+}
+
+int check_budget(const kv_problem* pr, int32_t budget, int32_t keep_tail) {
+  if (budget < 1) return KV_ERR_BUDGET;
+  for (int p = 0; p < pr->n_prob; ++p) {
+    const int L = pr->len_host[p];
+    if (keep_tail < 0 || keep_tail > L - 1) return KV_ERR_ARG;
+    if (budget > L - keep_tail) return KV_ERR_BUDGET;
+  }
+  return KV_OK;
+}
+
+int max_candidates(const kv_problem* pr, int32_t budget, int32_t cand_mult, int32_t keep_tail) {
+  int m = 0;
+  for (int p = 0; p < pr->n_prob; ++p) {
+    const int n_cand = pr->len_host[p] - keep_tail;
+    const int64_t c = cand_mult > 0 ? std::min<int64_t>((int64_t)cand_mult * budget, n_cand) : n_cand;
+    if (c > m) m = (int)c;
+  }
+  return m;
+}
+
+int launch_status(hipError_t e) { return e == hipSuccess ? KV_OK : KV_ERR_LAUNCH; }
+
+}  // namespace
+
+extern "C" {
+
+const char* kv_strerror(int status) {
+  switch (status) {
+    case KV_OK: return "success";
+    case KV_ERR_NULL: return "a required pointer is NULL";
+    case KV_ERR_SHAPE: return "unsupported head layout, window, length or candidate count";
+    case KV_ERR_DTYPE: return "unsupported dtype";
+    case KV_ERR_BUDGET: return "budget outside [1, L - keep_tail]";
+    case KV_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case KV_ERR_LAUNCH: return "HIP launch failed";
+    case KV_ERR_ARG: return "invalid argument";
+    default: return "unknown status";
+  }
+}
+
+int kv_version(void) { return 1; }
+
+size_t kv_workspace_bytes(const kv_problem* pr, int32_t budget, int32_t cand_mult,
+                          int32_t keep_tail) {
+  kv::Shape s;
+  if (check_problem(pr, &s) != KV_OK) return 0;
+  (void)budget;
+  (void)cand_mult;
+  (void)keep_tail;
+  return align_up(kv::window_stats_ws_bytes(s));
+}
+
+int32_t kv_candidate_stride(const kv_problem* pr, int32_t budget, int32_t cand_mult,
+                            int32_t keep_tail) {
+  kv::Shape s;
+  if (check_problem(pr, &s) != KV_OK || cand_mult < 0 || budget < 1) return 0;
+  if (check_budget(pr, budget, keep_tail) != KV_OK) return 0;
+  if (cand_mult > 0) {
+    const int64_t c = (int64_t)cand_mult * budget;
+    return c > INT32_MAX ? 0 : (int32_t)c;
+  }
+  return max_candidates(pr, budget, 0, keep_tail);
+}
+
+int kv_window_scores(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                     float* row_max, float* row_sum, void* ws, size_t ws_bytes, void* stream) {
+  kv::Shape s;
+  int st = check_problem(pr, &s);
+  if (st != KV_OK) return st;
+  if (!q_win || !k || !row_max || !row_sum) return KV_ERR_NULL;
+  if (!aligned16(q_win) || !aligned16(k)) return KV_ERR_ARG;
+  if (!std::isfinite(scale)) return KV_ERR_ARG;
+  const size_t need = align_up(kv::window_stats_ws_bytes(s));
+  if (ws_bytes < need || !ws || (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1)))
+    return KV_ERR_WORKSPACE;
+  return launch_status(kv::launch_window_stats(s, q_win, k, scale, ws, row_max, row_sum,
+                                               static_cast<hipStream_t>(stream)));
+}
+
+int kv_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                const float* row_max, const float* row_sum, float* mu, float* sigma, float* attn,
+                void* stream) {
+  kv::Shape s;
+  int st = check_problem(pr, &s);
+  if (st != KV_OK) return st;
+  if (!q_win || !k || !row_max || !row_sum || !mu || !sigma) return KV_ERR_NULL;
+  if (!aligned16(q_win) || !aligned16(k)) return KV_ERR_ARG;
+  if (!std::isfinite(scale)) return KV_ERR_ARG;
+  return launch_status(kv::launch_mu_sigma(s, q_win, k, scale, row_max, row_sum, mu, sigma, attn,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+int kv_window_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                       float* row_max, float* row_sum, float* mu, float* sigma, void* ws,
+                       size_t ws_bytes, void* stream) {
+  int st = kv_window_scores(pr, q_win, k, scale, row_max, row_sum, ws, ws_bytes, stream);
+  if (st != KV_OK) return st;
+  return kv_mu_sigma(pr, q_win, k, scale, row_max, row_sum, mu, sigma, nullptr, stream);
+}
+
+int kv_mmr_select(const kv_problem* pr, const float* mu, const float* sigma, const void* k,
+                  const float* lambda1, const float* lambda2, int32_t budget, int32_t cand_mult,
+                  int32_t keep_tail, int32_t* sel_idx, float* sel_score, int32_t* cand_idx,
+                  float* cand_corr, void* ws, size_t ws_bytes, void* stream) {
+  kv::Shape s;
+  int st = check_problem(pr, &s);
+  if (st != KV_OK) return st;
+  if (!mu || !sigma || !k || !lambda1 || !lambda2 || !sel_idx) return KV_ERR_NULL;
+  if (!aligned16(k)) return KV_ERR_ARG;
+  if (cand_mult < 0) return KV_ERR_ARG;
+  st = check_budget(pr, budget, keep_tail);
+  if (st != KV_OK) return st;
+  (void)ws;
+  (void)ws_bytes;
+  const int max_cand = max_candidates(pr, budget, cand_mult, keep_tail);
+  if (max_cand > kv::select_max_candidates(pr->d, elem_bytes(pr->dtype))) return KV_ERR_SHAPE;
+  kv::SelectArgs a;
+  a.mu = mu;
+  a.sigma = sigma;
+  a.k = k;
+  a.lambda1 = lambda1;
+  a.lambda2 = lambda2;
+  a.budget = budget;
+  a.cand_mult = cand_mult;
+  a.keep_tail = keep_tail;
+  a.cand_stride = kv_candidate_stride(pr, budget, cand_mult, keep_tail);
+  a.max_cand = max_cand;
+  a.sel_idx = sel_idx;
+  a.sel_score = sel_score;
+  a.cand_idx = cand_idx;
+  a.cand_corr = cand_corr;
+  if ((cand_idx || cand_corr) && a.cand_stride < 1) return KV_ERR_ARG;
+  return launch_status(kv::launch_mmr_select(s, a, static_cast<hipStream_t>(stream)));
+}
+
+int kv_compact_cache(const kv_problem* pr, const void* k, const void* v, const int32_t* sel_idx,
+                     int32_t budget, int32_t keep_tail, void* k_out, void* v_out, void* stream) {
+  kv::Shape s;
+  int st = check_problem(pr, &s);
+  if (st != KV_OK) return st;
+  if (!k || !v || !sel_idx || !k_out || !v_out) return KV_ERR_NULL;
+  if (!aligned16(k) || !aligned16(v) || !aligned16(k_out) || !aligned16(v_out)) return KV_ERR_ARG;
+  st = check_budget(pr, budget, keep_tail);
+  if (st != KV_OK) return st;
+  if (budget > kMaxCompactBudget) return KV_ERR_BUDGET;
+  return launch_status(kv::launch_compact(s, k, v, sel_idx, budget, keep_tail, k_out, v_out,
+                                          static_cast<hipStream_t>(stream)));
+}
+
+int kv_depth_profile(int32_t family, const double* params_host, int32_t n_params,
+                     int32_t n_layers, float* lambda_out_host) {
+  if (!params_host || !lambda_out_host) return KV_ERR_NULL;
+  if (n_layers < 1) return KV_ERR_ARG;
+  switch (family) {
+    case KV_PROFILE_GLOBAL:
+      if (n_params != 1) return KV_ERR_ARG;
+      break;
+    case KV_PROFILE_SEGMENTS:
+      if (n_params < 1 || n_params > n_layers) return KV_ERR_ARG;
+      break;
+    case KV_PROFILE_CURVE:
+      if (n_params != 3) return KV_ERR_ARG;
+      break;
+    default:
+      return KV_ERR_ARG;
+  }
+  for (int l = 0; l < n_layers; ++l) {
+    double a;
+    if (family == KV_PROFILE_GLOBAL) {
+      a = params_host[0];
+    } else if (family == KV_PROFILE_SEGMENTS) {
+      a = params_host[((int64_t)n_params * l) / n_layers];
+    } else {
+      const double t = n_layers == 1 ? 0.0 : (double)l / (double)(n_layers - 1);
+      a = params_host[0] + params_host[1] * t + params_host[2] * t * t;
+    }
+    lambda_out_host[l] = (float)std::sinh(a);
+  }
+  return KV_OK;
+}
+
+}  // extern "C"

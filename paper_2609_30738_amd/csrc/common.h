@@ -1,0 +1,110 @@
+// Device-side building blocks shared by the gfx950 kernels: element types, the 32x32 MFMA tile
+// and its operand fragments, wave-level reductions.
+//
+// MFMA tile conventions (v_mfma_f32_32x32x16_bf16 and v_mfma_f32_32x32x2_f32, wave64):
+//   operand fragments: lane l carries row/column (l % 32) of its operand and the K-half (l / 32);
+//     for bf16 one K step covers 16 elements, lane half h holds elements [16 s + 8 h, 16 s + 8 h + 8);
+//     for f32 one K step covers 2 elements; lane half h holds element h * (D / 2) + s, so every lane
+//     reads D / 2 contiguous floats.  A and B use the same K mapping, so every pairing of lanes sums
+//     a full dot product.
+//   accumulator: lane l, register j holds D[8 (j / 4) + 4 (l / 32) + (j % 4)][l % 32].
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kernels.h"
+
+namespace kv {
+
+typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8_t;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+template <int DT> struct Elem;
+template <> struct Elem<kDtF32> { typedef float T; };
+template <> struct Elem<kDtBf16> { typedef uint16_t T; };
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// Row of the 32x32 accumulator held by register j of lane l.
+__device__ __forceinline__ int acc_row(int j, int lane) { return 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3); }
+
+// All K-step fragments of one 32-wide operand slab (32 rows of D elements) for this lane.
+template <int DT, int D> struct Frags;
+
+template <int D> struct Frags<kDtBf16, D> {
+  static constexpr int NS = D / 16;
+  bf16x8_t v[NS];
+  // row: pointer to this lane's row (D elements), half: lane / 32
+  __device__ __forceinline__ void load_global(const uint16_t* row, int half) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      v[s] = *reinterpret_cast<const bf16x8_t*>(row + 16 * s + 8 * half);
+  }
+  __device__ __forceinline__ void load_lds(const uint16_t* row, int half) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      v[s] = *reinterpret_cast<const bf16x8_t*>(row + 16 * s + 8 * half);
+  }
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) v[s] = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+  }
+};
+
+template <int D> struct Frags<kDtF32, D> {
+  static constexpr int NS = D / 2;
+  float v[NS];
+  __device__ __forceinline__ void load_global(const float* row, int half) {
+    const float4* src = reinterpret_cast<const float4*>(row + half * (D / 2));
+#pragma unroll
+    for (int q = 0; q < NS / 4; ++q) {
+      float4 x = src[q];
+      v[4 * q + 0] = x.x;
+      v[4 * q + 1] = x.y;
+      v[4 * q + 2] = x.z;
+      v[4 * q + 3] = x.w;
+    }
+  }
+  __device__ __forceinline__ void load_lds(const float* row, int half) { load_global(row, half); }
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) v[s] = 0.f;
+  }
+};
+
+__device__ __forceinline__ f32x16_t mfma_step(bf16x8_t a, bf16x8_t b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x16_t mfma_step(float a, float b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+// acc = A * B^T over the full head dimension: A rows from `a`, B rows from `b`.
+template <int DT, int D>
+__device__ __forceinline__ f32x16_t mfma_tile(const Frags<DT, D>& a, const Frags<DT, D>& b) {
+  f32x16_t acc = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < Frags<DT, D>::NS; ++s) acc = mfma_step(a.v[s], b.v[s], acc);
+  return acc;
+}
+
+// Value of the lane l ^ 32 (the other K-half / the other 16 accumulator rows).
+__device__ __forceinline__ float swap_halves(float x) {
+  return __shfl_xor(x, 32, 64);
+}
+
+// Online-softmax pair merge in base-2 units: (m, z) represents z * 2^m.
+__device__ __forceinline__ void merge_mz(float& m, float& z, float m2, float z2) {
+  float mn = fmaxf(m, m2);
+  if (mn == -INFINITY) return;  // both empty
+  float a = (m == -INFINITY) ? 0.f : z * __builtin_amdgcn_exp2f(m - mn);
+  float b = (m2 == -INFINITY) ? 0.f : z2 * __builtin_amdgcn_exp2f(m2 - mn);
+  m = mn;
+  z = a + b;
+}
+
+}  // namespace kv

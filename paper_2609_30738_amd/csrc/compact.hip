@@ -1,0 +1,70 @@
+// Cache compaction (sections 1 and 3.1: each layer keeps B entries, plus the always-kept tail).
+//
+// One workgroup per (problem, kv head): the B admitted positions are sorted in LDS (bitonic sort
+// over the next power of two, padded with INT_MAX), then the kept rows of K and V are copied with
+// 16-byte vector loads and stores.  Rows are opaque bytes, so the copy is exact for every dtype.
+#include <limits.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace kv {
+
+namespace {
+constexpr int kThreads = 256;
+constexpr int kMaxSortedBudget = 8192;
+}  // namespace
+
+__global__ __launch_bounds__(kThreads) void compact_kernel(
+    const uint4* __restrict__ k, const uint4* __restrict__ v, const int32_t* __restrict__ sel_idx,
+    const int32_t* __restrict__ lens, const int64_t* __restrict__ tok_off, int h_kv,
+    int row_vecs, int budget, int keep_tail, uint4* __restrict__ k_out, uint4* __restrict__ v_out) {
+  __shared__ int32_t srt[kMaxSortedBudget];
+  const int g = blockIdx.x % h_kv, p = blockIdx.x / h_kv;
+  const int L = lens[p];
+  int n2 = 1;
+  while (n2 < budget) n2 <<= 1;
+  const int32_t* sel = sel_idx + ((size_t)p * h_kv + g) * budget;
+  for (int i = threadIdx.x; i < n2; i += kThreads) srt[i] = i < budget ? sel[i] : INT_MAX;
+  __syncthreads();
+  for (int size = 2; size <= n2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = threadIdx.x; i < n2; i += kThreads) {
+        const int j = i ^ stride;
+        if (j > i) {
+          const bool up = (i & size) == 0;
+          const int a = srt[i], b = srt[j];
+          if ((a > b) == up) {
+            srt[i] = b;
+            srt[j] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  const int rows = budget + keep_tail;
+  const size_t src_base = ((size_t)tok_off[p] * h_kv + (size_t)g * L) * row_vecs;
+  const size_t dst_base = ((size_t)p * h_kv + g) * rows * row_vecs;
+  for (int e = threadIdx.x; e < rows * row_vecs; e += kThreads) {
+    const int r = e / row_vecs, c = e % row_vecs;
+    const int pos = r < budget ? srt[r] : L - keep_tail + (r - budget);
+    if (pos < 0 || pos >= L) continue;  // invalid selection: leave the row unwritten
+    const size_t s = src_base + (size_t)pos * row_vecs + c;
+    k_out[dst_base + e] = k[s];
+    v_out[dst_base + e] = v[s];
+  }
+}
+
+hipError_t launch_compact(const Shape& s, const void* k, const void* v, const int32_t* sel_idx,
+                          int budget, int keep_tail, void* k_out, void* v_out, hipStream_t stream) {
+  if (budget > kMaxSortedBudget) return hipErrorInvalidValue;
+  const int elem = s.dtype == kDtBf16 ? 2 : 4;
+  const int row_vecs = s.d * elem / 16;
+  compact_kernel<<<dim3((unsigned)(s.n_prob * s.h_kv)), kThreads, 0, stream>>>(
+      static_cast<const uint4*>(k), static_cast<const uint4*>(v), sel_idx, s.lens, s.tok_off,
+      s.h_kv, row_vecs, budget, keep_tail, static_cast<uint4*>(k_out), static_cast<uint4*>(v_out));
+  return hipGetLastError();
+}
+
+}  // namespace kv

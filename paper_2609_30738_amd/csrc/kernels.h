@@ -1,0 +1,60 @@
+// Host-side launchers of the gfx950 kernels.  Arguments are validated by the C ABI layer before
+// any of these is called; every launcher only enqueues work on `stream` and reports launch errors.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace kv {
+
+constexpr int kDtF32 = 0;
+constexpr int kDtBf16 = 1;
+
+// Keys per work item of the window kernels (a multiple of 4 waves x 32 keys).
+constexpr int kWindowChunk = 1024;
+
+struct Shape {
+  int dtype;  // 0 = fp32, 1 = bf16
+  int n_prob, h_q, h_kv, d, w;
+  int max_len;                 // max_p L_p
+  const int32_t* lens;         // device [n_prob]
+  const int64_t* tok_off;      // device [n_prob]
+  int group() const { return h_q / h_kv; }
+  int rows() const { return group() * w; }
+  int row_blocks() const { return rows() <= 32 ? 1 : (rows() <= 64 ? 2 : 4); }
+  int max_chunks() const { return (max_len + kWindowChunk - 1) / kWindowChunk; }
+};
+
+// Workspace bytes of the split-L row statistics.
+size_t window_stats_ws_bytes(const Shape& s);
+
+hipError_t launch_window_stats(const Shape& s, const void* q_win, const void* k, float scale,
+                               void* ws, float* row_max, float* row_sum, hipStream_t stream);
+
+hipError_t launch_mu_sigma(const Shape& s, const void* q_win, const void* k, float scale,
+                           const float* row_max, const float* row_sum, float* mu, float* sigma,
+                           float* attn, hipStream_t stream);
+
+struct SelectArgs {
+  const float* mu;
+  const float* sigma;
+  const void* k;
+  const float* lambda1;
+  const float* lambda2;
+  int budget, cand_mult, keep_tail, cand_stride, max_cand;
+  int32_t* sel_idx;
+  float* sel_score;
+  int32_t* cand_idx;
+  float* cand_corr;
+};
+
+// Largest supported candidate count for a head dimension / element size.
+int select_max_candidates(int d, int elem_bytes);
+
+hipError_t launch_mmr_select(const Shape& s, const SelectArgs& a, hipStream_t stream);
+
+hipError_t launch_compact(const Shape& s, const void* k, const void* v, const int32_t* sel_idx,
+                          int budget, int keep_tail, void* k_out, void* v_out, hipStream_t stream);
+
+}  // namespace kv

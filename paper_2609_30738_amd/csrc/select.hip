@@ -1,0 +1,419 @@
+// Greedy diversity-aware admission (section 3.2, Eq. (2), (4), (5)) on gfx950.
+//
+// One workgroup of 256 threads per (problem, kv head):
+//   1. base scores s_i = fma(lambda1, sigma_i, mu_i) over the candidates [0, n_cand), their maximum
+//      (the normaliser, clamped at 1e-12), and the C-th largest score by a most-significant-digit
+//      radix select over order-preserving 32-bit keys (4 passes of 8 bits, wave-private LDS
+//      histograms filled with wave-aggregated increments);
+//   2. the candidate set P: every score above the threshold plus the lowest positions among those
+//      equal to it, compacted in ascending position order (ballot ranks inside a wave, LDS prefix
+//      across waves);
+//   3. B greedy steps.  Thread t owns candidates t, t + 256, ...: it keeps their keys in registers,
+//      their normalised score s~, running max-cosine and admitted flag.  Each step updates the
+//      running maxima against the last admitted key (read once from an LDS copy of the candidate
+//      keys), forms s~ + lambda2 * corr, and finds the (score, lowest slot) maximum with a wave
+//      shuffle reduction and one barrier; the per-wave winners are double-buffered so that one
+//      barrier per step suffices.
+#include <float.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace kv {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = 4;
+constexpr int kMaxCandBytes = 131072;  // LDS copy of the candidate keys
+
+__device__ __forceinline__ uint32_t order_key(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Add one to hist[digit] for every active lane, one LDS increment per distinct digit in the wave.
+__device__ __forceinline__ void wave_hist_add(uint32_t* hist, uint32_t digit, bool active) {
+  uint64_t pending = __ballot(active);
+  while (pending) {
+    const int leader = __ffsll((unsigned long long)pending) - 1;
+    const uint32_t dl = __shfl(digit, leader, 64);
+    const uint64_t same = __ballot(active && digit == dl);
+    if ((threadIdx.x & 63) == leader) atomicAdd(&hist[dl], (uint32_t)__popcll(same));
+    pending &= ~same;
+  }
+}
+
+// (score, slot) packed so that a larger value means a larger score, then a lower slot.
+__device__ __forceinline__ uint64_t pack_best(float score, int slot) {
+  return ((uint64_t)order_key(score) << 32) | (uint32_t)(0x7FFFFFFF - slot);
+}
+__device__ __forceinline__ int unpack_slot(uint64_t v) { return 0x7FFFFFFF - (int)(uint32_t)v; }
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint64_t o = __shfl_xor(v, off, 64);
+    v = o > v ? o : v;
+  }
+  return v;
+}
+__device__ __forceinline__ float wave_max_f(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+  return v;
+}
+
+// Key row of one candidate held in registers, and its dot product with a row in LDS.
+template <int DT, int D> struct KeyRow;
+
+template <int D> struct KeyRow<kDtBf16, D> {
+  typedef __bf16 __attribute__((ext_vector_type(2))) bf2;
+  bf2 v[D / 2];
+  __device__ __forceinline__ void load(const uint16_t* row) {
+    const uint4* src = reinterpret_cast<const uint4*>(row);
+#pragma unroll
+    for (int q = 0; q < D / 8; ++q) {
+      const uint4 x = src[q];
+      v[4 * q + 0] = __builtin_bit_cast(bf2, x.x);
+      v[4 * q + 1] = __builtin_bit_cast(bf2, x.y);
+      v[4 * q + 2] = __builtin_bit_cast(bf2, x.z);
+      v[4 * q + 3] = __builtin_bit_cast(bf2, x.w);
+    }
+  }
+  __device__ __forceinline__ void store(uint16_t* row) const {
+    uint4* dst = reinterpret_cast<uint4*>(row);
+#pragma unroll
+    for (int q = 0; q < D / 8; ++q)
+      dst[q] = make_uint4(__builtin_bit_cast(uint32_t, v[4 * q + 0]), __builtin_bit_cast(uint32_t, v[4 * q + 1]),
+                          __builtin_bit_cast(uint32_t, v[4 * q + 2]), __builtin_bit_cast(uint32_t, v[4 * q + 3]));
+  }
+  __device__ __forceinline__ float dot_lds(const uint16_t* row) const {
+    const uint4* src = reinterpret_cast<const uint4*>(row);
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < D / 8; ++q) {
+      const uint4 x = src[q];
+      acc[0] = __builtin_amdgcn_fdot2_f32_bf16(v[4 * q + 0], __builtin_bit_cast(bf2, x.x), acc[0], false);
+      acc[1] = __builtin_amdgcn_fdot2_f32_bf16(v[4 * q + 1], __builtin_bit_cast(bf2, x.y), acc[1], false);
+      acc[2] = __builtin_amdgcn_fdot2_f32_bf16(v[4 * q + 2], __builtin_bit_cast(bf2, x.z), acc[2], false);
+      acc[3] = __builtin_amdgcn_fdot2_f32_bf16(v[4 * q + 3], __builtin_bit_cast(bf2, x.w), acc[3], false);
+    }
+    return (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  }
+  __device__ __forceinline__ float sq_norm() const {
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < D / 2; ++i)
+      acc[i & 3] = __builtin_amdgcn_fdot2_f32_bf16(v[i], v[i], acc[i & 3], false);
+    return (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  }
+};
+
+template <int D> struct KeyRow<kDtF32, D> {
+  float v[D];
+  __device__ __forceinline__ void load(const float* row) {
+    const float4* src = reinterpret_cast<const float4*>(row);
+#pragma unroll
+    for (int q = 0; q < D / 4; ++q) {
+      const float4 x = src[q];
+      v[4 * q + 0] = x.x;
+      v[4 * q + 1] = x.y;
+      v[4 * q + 2] = x.z;
+      v[4 * q + 3] = x.w;
+    }
+  }
+  __device__ __forceinline__ void store(float* row) const {
+    float4* dst = reinterpret_cast<float4*>(row);
+#pragma unroll
+    for (int q = 0; q < D / 4; ++q) dst[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  }
+  __device__ __forceinline__ float dot_lds(const float* row) const {
+    const float4* src = reinterpret_cast<const float4*>(row);
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < D / 4; ++q) {
+      const float4 x = src[q];
+      acc[0] = fmaf(v[4 * q + 0], x.x, acc[0]);
+      acc[1] = fmaf(v[4 * q + 1], x.y, acc[1]);
+      acc[2] = fmaf(v[4 * q + 2], x.z, acc[2]);
+      acc[3] = fmaf(v[4 * q + 3], x.w, acc[3]);
+    }
+    return (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  }
+  __device__ __forceinline__ float sq_norm() const {
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < D; ++i) acc[i & 3] = fmaf(v[i], v[i], acc[i & 3]);
+    return (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  }
+};
+
+struct SelectShared {
+  uint32_t hist[kWaves][256];
+  uint32_t scan[256];
+  uint32_t wave_cnt[2][kWaves];
+  float wave_max[kWaves];
+  uint64_t best[2][kWaves];
+  uint32_t sel_threshold;
+  int sel_need;
+};
+
+}  // namespace
+
+template <int DT, int D, int CPT>
+__global__ __launch_bounds__(kThreads) void mmr_select_kernel(
+    const float* __restrict__ mu, const float* __restrict__ sigma,
+    const typename Elem<DT>::T* __restrict__ k, const int32_t* __restrict__ lens,
+    const int64_t* __restrict__ tok_off, const float* __restrict__ lambda1,
+    const float* __restrict__ lambda2, int h_kv, int budget, int cand_mult, int keep_tail,
+    int cand_stride, int32_t* __restrict__ sel_idx, float* __restrict__ sel_score,
+    int32_t* __restrict__ cand_idx, float* __restrict__ cand_corr) {
+  using T = typename Elem<DT>::T;
+  __shared__ SelectShared sh;
+  extern __shared__ __align__(16) unsigned char dyn[];  // [C] positions, [C] 1/|k|, [C][D] keys
+  const int g = blockIdx.x % h_kv, p = blockIdx.x / h_kv;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int L = lens[p];
+  const int n_cand = L - keep_tail;
+  const int C = cand_mult > 0 ? min(cand_mult * budget, n_cand) : n_cand;
+  const size_t base = (size_t)tok_off[p] * h_kv + (size_t)g * L;
+  const float* mu_g = mu + base;
+  const float* sg_g = sigma + base;
+  const T* kg = k + base * D;
+  const float lam1 = lambda1[p], lam2 = lambda2[p];
+  int32_t* cpos = reinterpret_cast<int32_t*>(dyn);
+  float* cinv = reinterpret_cast<float*>(dyn + (size_t)C * 4);
+  T* ckeys = reinterpret_cast<T*>(dyn + (((size_t)C * 8 + 15) & ~(size_t)15));
+
+  // ---- 1. normaliser and radix select of the C-th largest base score --------------------------
+  uint32_t prefix = 0, pmask = 0;
+  int need = C;
+  float local_max = -INFINITY;
+  const bool take_all = (C >= n_cand);
+  for (int pass = 0; pass < (take_all ? 1 : 4); ++pass) {
+    const int shift = 24 - 8 * pass;
+    for (int i = tid; i < kWaves * 256; i += kThreads) (&sh.hist[0][0])[i] = 0u;
+    __syncthreads();
+    const int n_iter = (n_cand + kThreads - 1) / kThreads;
+    for (int it = 0; it < n_iter; ++it) {
+      const int i = it * kThreads + tid;
+      const bool in = i < n_cand;
+      const float s = in ? fmaf(lam1, sg_g[i], mu_g[i]) : 0.f;
+      if (pass == 0 && in) local_max = fmaxf(local_max, s);
+      if (!take_all) {
+        const uint32_t key = order_key(s);
+        wave_hist_add(sh.hist[wave], (key >> shift) & 255u, in && (key & pmask) == prefix);
+      }
+    }
+    if (pass == 0) {
+      const float wm = wave_max_f(local_max);
+      if (lane == 0) sh.wave_max[wave] = wm;
+    }
+    __syncthreads();
+    if (take_all) break;
+    // suffix sums over bins (bin 255 = largest digit)
+    const uint32_t cnt = sh.hist[0][tid] + sh.hist[1][tid] + sh.hist[2][tid] + sh.hist[3][tid];
+    sh.scan[tid] = cnt;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {
+      const uint32_t add = (tid + off < 256) ? sh.scan[tid + off] : 0u;
+      __syncthreads();
+      sh.scan[tid] += add;
+      __syncthreads();
+    }
+    const uint32_t ge = sh.scan[tid];                               // count with digit >= tid
+    const uint32_t gt = (tid + 1 < 256) ? sh.scan[tid + 1] : 0u;    // count with digit > tid
+    if (ge >= (uint32_t)need && gt < (uint32_t)need) {
+      sh.sel_threshold = prefix | ((uint32_t)tid << shift);
+      sh.sel_need = need - (int)gt;
+    }
+    __syncthreads();
+    prefix = sh.sel_threshold;
+    need = sh.sel_need;
+    pmask |= 255u << shift;
+    __syncthreads();
+  }
+  float den = fmaxf(fmaxf(sh.wave_max[0], sh.wave_max[1]), fmaxf(sh.wave_max[2], sh.wave_max[3]));
+  den = fmaxf(den, 1e-12f);
+
+  // ---- 2. candidate positions in ascending order ----------------------------------------------
+  // key > threshold: taken; key == threshold: the `need` lowest positions are taken.
+  {
+    const uint32_t thr = prefix;
+    const int per_wave = (n_cand + kWaves - 1) / kWaves;
+    const int w0 = wave * per_wave, w1 = min(n_cand, w0 + per_wave);
+    uint32_t n_gt = 0, n_eq = 0;
+    for (int i0 = w0; i0 < w1; i0 += 64) {
+      const int i = i0 + lane;
+      uint32_t key = 0;
+      const bool in = i < w1;
+      if (in && !take_all) key = order_key(fmaf(lam1, sg_g[i], mu_g[i]));
+      n_gt += __popcll(__ballot(in && (take_all || key > thr)));
+      n_eq += __popcll(__ballot(in && !take_all && key == thr));
+    }
+    if (lane == 0) {
+      sh.wave_cnt[0][wave] = n_gt;
+      sh.wave_cnt[1][wave] = n_eq;
+    }
+    __syncthreads();
+    uint32_t out = 0, eq_before = 0;
+    for (int v = 0; v < wave; ++v) {
+      const uint32_t eq_v = sh.wave_cnt[1][v];
+      const uint32_t eq_taken = eq_before >= (uint32_t)need ? 0u : min(eq_v, (uint32_t)need - eq_before);
+      out += sh.wave_cnt[0][v] + eq_taken;
+      eq_before += eq_v;
+    }
+    const uint64_t lanes_below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    for (int i0 = w0; i0 < w1; i0 += 64) {
+      const int i = i0 + lane;
+      const bool in = i < w1;
+      uint32_t key = 0;
+      if (in && !take_all) key = order_key(fmaf(lam1, sg_g[i], mu_g[i]));
+      const bool is_gt = in && (take_all || key > thr);
+      const bool is_eq = in && !take_all && key == thr;
+      const uint64_t eqm = __ballot(is_eq);
+      const uint32_t eq_rank = eq_before + (uint32_t)__popcll(eqm & lanes_below);
+      const bool taken = is_gt || (is_eq && eq_rank < (uint32_t)need);
+      const uint64_t tm = __ballot(taken);
+      const uint32_t slot = out + (uint32_t)__popcll(tm & lanes_below);
+      if (taken && slot < (uint32_t)C) cpos[slot] = i;
+      out += (uint32_t)__popcll(tm);
+      eq_before += (uint32_t)__popcll(eqm);
+    }
+  }
+  __syncthreads();
+
+  // ---- 3. greedy admission -------------------------------------------------------------------
+  KeyRow<DT, D> key[CPT];
+  float st[CPT], corr[CPT], inv[CPT];
+  bool admitted[CPT];
+#pragma unroll
+  for (int q = 0; q < CPT; ++q) {
+    const int c = tid + q * kThreads;
+    admitted[q] = c >= C;  // slots beyond C never compete
+    corr[q] = 0.f;
+    st[q] = 0.f;
+    inv[q] = 0.f;
+    if (c < C) {
+      const int pos = cpos[c];
+      key[q].load(kg + (size_t)pos * D);
+      key[q].store(ckeys + (size_t)c * D);
+      const float n2 = key[q].sq_norm();
+      inv[q] = n2 > 0.f ? 1.f / sqrtf(n2) : 0.f;  // a zero key has cosine 0 to everything
+      cinv[c] = inv[q];
+      st[q] = fmaf(lam1, sg_g[pos], mu_g[pos]) / den;
+    }
+  }
+  __syncthreads();
+
+  int last = -1;
+  float last_inv = 0.f;
+  for (int t = 0; t < budget; ++t) {
+    uint64_t mine = 0;
+#pragma unroll
+    for (int q = 0; q < CPT; ++q) {
+      if (!admitted[q]) {
+        if (last >= 0) {
+          const float cs = key[q].dot_lds(ckeys + (size_t)last * D) * inv[q] * last_inv;
+          corr[q] = fmaxf(corr[q], cs);
+        }
+        float sc = fmaf(lam2, corr[q], st[q]);
+        if (!(sc > -INFINITY)) sc = -FLT_MAX;  // NaN or -inf still ranks above admitted slots
+        const uint64_t pk = pack_best(sc, tid + q * kThreads);
+        mine = pk > mine ? pk : mine;
+      }
+    }
+    const uint64_t wbest = wave_max_u64(mine);
+    if (lane == 0) sh.best[t & 1][wave] = wbest;
+    __syncthreads();
+    uint64_t b = sh.best[t & 1][0];
+#pragma unroll
+    for (int v = 1; v < kWaves; ++v) {
+      const uint64_t o = sh.best[t & 1][v];
+      b = o > b ? o : b;
+    }
+    last = min(max(unpack_slot(b), 0), C - 1);  // always a live slot: budget <= C
+#pragma unroll
+    for (int q = 0; q < CPT; ++q)
+      if (tid + q * kThreads == last) admitted[q] = true;
+    last_inv = cinv[last];
+    if (tid == 0) {
+      const size_t o = ((size_t)p * h_kv + g) * budget + t;
+      sel_idx[o] = cpos[last];
+      if (sel_score) {
+        const uint32_t kk = (uint32_t)(b >> 32);
+        const uint32_t u = (kk & 0x80000000u) ? (kk & 0x7FFFFFFFu) : ~kk;
+        sel_score[o] = __uint_as_float(u);
+      }
+    }
+  }
+
+  if (cand_idx || cand_corr) {
+    // corr after the last step includes the last admitted key
+#pragma unroll
+    for (int q = 0; q < CPT; ++q) {
+      if (!admitted[q]) {
+        const float cs = key[q].dot_lds(ckeys + (size_t)last * D) * inv[q] * last_inv;
+        corr[q] = fmaxf(corr[q], cs);
+      }
+    }
+    const size_t o = ((size_t)p * h_kv + g) * cand_stride;
+#pragma unroll
+    for (int q = 0; q < CPT; ++q) {
+      const int c = tid + q * kThreads;
+      if (c < cand_stride) {
+        if (cand_idx) cand_idx[o + c] = c < C ? cpos[c] : -1;
+        if (cand_corr) cand_corr[o + c] = c < C ? corr[q] : 0.f;
+      }
+    }
+    for (int c = tid + CPT * kThreads; c < cand_stride; c += kThreads) {
+      if (cand_idx) cand_idx[o + c] = -1;
+      if (cand_corr) cand_corr[o + c] = 0.f;
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+int select_max_candidates(int d, int elem_bytes) {
+  const int by_lds = kMaxCandBytes / (d * elem_bytes);
+  const int by_regs = 4 * kThreads;
+  return by_lds < by_regs ? by_lds : by_regs;
+}
+
+namespace {
+template <int DT, int D, int CPT>
+hipError_t select_dispatch(const Shape& s, const SelectArgs& a, hipStream_t st) {
+  using T = typename Elem<DT>::T;
+  const size_t dyn = (((size_t)a.max_cand * 8 + 15) & ~(size_t)15) + (size_t)a.max_cand * D * sizeof(T);
+  auto kern = mmr_select_kernel<DT, D, CPT>;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+  if (e != hipSuccess) return e;
+  kern<<<dim3((unsigned)(s.n_prob * s.h_kv)), kThreads, dyn, st>>>(
+      a.mu, a.sigma, static_cast<const T*>(a.k), s.lens, s.tok_off, a.lambda1, a.lambda2, s.h_kv,
+      a.budget, a.cand_mult, a.keep_tail, a.cand_stride, a.sel_idx, a.sel_score, a.cand_idx,
+      a.cand_corr);
+  return hipGetLastError();
+}
+
+template <int DT, int D>
+hipError_t select_cpt(const Shape& s, const SelectArgs& a, hipStream_t st) {
+  // only the candidates-per-thread counts that the LDS key copy allows are instantiated
+  constexpr int kMaxCand = kMaxCandBytes / (D * (int)sizeof(typename Elem<DT>::T));
+  const int cpt = (a.max_cand + kThreads - 1) / kThreads;
+  if (cpt <= 1) return select_dispatch<DT, D, 1>(s, a, st);
+  if constexpr (kMaxCand > kThreads) {
+    if (cpt <= 2) return select_dispatch<DT, D, 2>(s, a, st);
+  }
+  if constexpr (kMaxCand > 2 * kThreads) return select_dispatch<DT, D, 4>(s, a, st);
+  return hipErrorInvalidValue;
+}
+}  // namespace
+
+hipError_t launch_mmr_select(const Shape& s, const SelectArgs& a, hipStream_t stream) {
+  if (s.dtype == kDtBf16)
+    return s.d == 64 ? select_cpt<kDtBf16, 64>(s, a, stream) : select_cpt<kDtBf16, 128>(s, a, stream);
+  return s.d == 64 ? select_cpt<kDtF32, 64>(s, a, stream) : select_cpt<kDtF32, 128>(s, a, stream);
+}
+
+}  // namespace kv

@@ -31,7 +31,9 @@ bf16 tensors are returned as their raw uint16 bit patterns (round-to-nearest-eve
 """
 from __future__ import annotations
 
+import concurrent.futures
 import dataclasses
+import os
 from typing import List, Optional, Sequence, Tuple
 
 import numpy as np
@@ -181,11 +183,22 @@ def ragged_batch(run: str = "both", n_seq: int = 8, n_layers: int = 32,
 # Drawing
 # --------------------------------------------------------------------------------------------
 
-def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    """Round fp32 to bf16 (nearest, ties to even) and return the uint16 bit patterns."""
-    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    r = ((b >> 16) & 1) + np.uint32(0x7FFF)
-    return ((b + r) >> 16).astype(np.uint16)
+def f32_to_bf16_bits(x: np.ndarray, out: Optional[np.ndarray] = None,
+                     inplace: bool = False) -> np.ndarray:
+    """Round fp32 to bf16 (nearest, ties to even) and return the uint16 bit patterns.
+
+    With inplace=True the float32 input is used as scratch (its contents are destroyed)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    b = x.view(np.uint32) if inplace else x.view(np.uint32).copy()
+    r = b >> np.uint32(16)
+    r &= np.uint32(1)
+    r += np.uint32(0x7FFF)
+    b += r
+    b >>= np.uint32(16)
+    if out is None:
+        return b.astype(np.uint16)
+    np.copyto(out, b.reshape(out.shape), casting="unsafe")
+    return out
 
 
 def _unit_orthogonal(rng: np.random.Generator, u: np.ndarray, n: int) -> np.ndarray:
@@ -214,7 +227,8 @@ def _place(rng: np.random.Generator, lo: int, hi: int, lengths: Sequence[int]) -
 
 def _planted_keys(rng, q_group: np.ndarray, scale: float, L: int, w: int, lay: Layout,
                   n_clusters: int, k: np.ndarray) -> None:
-    """Overwrite rows of one kv-head's keys k[L, d] (float32) with the planted structure."""
+    """Overwrite rows of one kv-head's keys k[L, d] (float32) with the planted structure (computed
+    in float64, stored rounded)."""
     d = k.shape[1]
     u = q_group.sum(axis=0)
     u /= np.linalg.norm(u)
@@ -247,14 +261,20 @@ def _planted_keys(rng, q_group: np.ndarray, scale: float, L: int, w: int, lay: L
             k[s1:s1 + n] = toks + NOISE_REL * rms * rng.standard_normal((n, d))
 
 
-def _random_values(rng: np.random.Generator, shape) -> np.ndarray:
+def _random_values(rng: np.random.Generator, shape, out: Optional[np.ndarray] = None) -> np.ndarray:
     """Random bf16 bit patterns: random sign and mantissa, exponent in [2^-7, 2^2]."""
     n = int(np.prod(shape))
-    raw = rng.integers(0, 1 << 16, size=n, dtype=np.uint16)
-    mant = raw & np.uint16(0x7F)
-    sign = (raw >> np.uint16(15)) << np.uint16(15)
-    expo = (np.uint16(120) + (raw >> np.uint16(7)) % np.uint16(10)) << np.uint16(7)
-    return (sign | expo | mant).reshape(shape)
+    raw = np.frombuffer(rng.bytes(2 * n), dtype=np.uint16).copy()
+    expo = raw >> np.uint16(7)
+    expo %= np.uint16(10)
+    expo += np.uint16(120)
+    expo <<= np.uint16(7)
+    raw &= np.uint16(0x807F)  # sign and mantissa
+    raw |= expo
+    if out is None:
+        return raw.reshape(shape)
+    np.copyto(out, raw.reshape(out.shape))
+    return out
 
 
 @dataclasses.dataclass
@@ -265,29 +285,39 @@ class ProblemInputs:
     v: np.ndarray      # [h_kv, L, d]
 
 
-def draw_problem(wl: Workload, p: int) -> ProblemInputs:
-    """Draw the inputs of problem p (deterministic in (config_id, sequence, layer))."""
+def draw_problem(wl: Workload, p: int, k_out: Optional[np.ndarray] = None,
+                 v_out: Optional[np.ndarray] = None) -> ProblemInputs:
+    """Draw the inputs of problem p (deterministic in (config_id, sequence, layer)).
+
+    k_out / v_out (optional, [h_kv, L, d] in the stored dtype) receive K and V directly."""
     s, layer = wl.seq_of(p), wl.layer_of(p)
     L = int(wl.seq_lens[s])
     rng = np.random.default_rng([wl.config_id, s, layer])
     d, w, h_q, h_kv = wl.d, wl.w, wl.h_q, wl.h_kv
     g_sz = h_q // h_kv
-    q = (rng.standard_normal((h_q, w, d), dtype=np.float32) / np.float32(np.sqrt(d)))
-    k = (rng.standard_normal((h_kv, L, d), dtype=np.float32) / np.float32(np.sqrt(d)))
+    q = rng.standard_normal((h_q, w, d), dtype=np.float32)
+    q /= np.float32(np.sqrt(d))
+    k = rng.standard_normal((h_kv, L, d), dtype=np.float32)
+    k /= np.float32(np.sqrt(d))
     lay = wl.layout
     n_clusters = lay.n_clusters
     if lay.cluster_density is not None:
         n_clusters = int(np.floor(lay.cluster_density * L / lay.cluster_size))
     for g in range(h_kv):
         qg = q[g * g_sz:(g + 1) * g_sz].reshape(-1, d).astype(np.float64)
-        kg = k[g].astype(np.float64)
-        _planted_keys(rng, qg, wl.scale, L, w, lay, n_clusters, kg)
-        k[g] = kg.astype(np.float32)
+        _planted_keys(rng, qg, wl.scale, L, w, lay, n_clusters, k[g])
     if wl.dtype == F32:
         v = rng.standard_normal((h_kv, L, d), dtype=np.float32)
+        if k_out is not None:
+            np.copyto(k_out, k)
+            k = k_out
+        if v_out is not None:
+            np.copyto(v_out, v)
+            v = v_out
         return ProblemInputs(q, k, v)
-    v = _random_values(rng, (h_kv, L, d))
-    return ProblemInputs(f32_to_bf16_bits(q), f32_to_bf16_bits(k), v)
+    v = _random_values(rng, (h_kv, L, d), v_out)
+    kb = f32_to_bf16_bits(k, k_out, inplace=True)
+    return ProblemInputs(f32_to_bf16_bits(q), kb, v)
 
 
 @dataclasses.dataclass
@@ -300,8 +330,10 @@ class PackedInputs:
     tok_off: np.ndarray  # int64 [n_prob]
 
 
-def draw_packed(wl: Workload, problems: Optional[Sequence[int]] = None) -> PackedInputs:
-    """Draw and pack the given problems (default: all) of a workload."""
+def draw_packed(wl: Workload, problems: Optional[Sequence[int]] = None,
+                threads: Optional[int] = None) -> PackedInputs:
+    """Draw and pack the given problems (default: all) of a workload (problems are independent
+    and drawn in parallel threads; the result does not depend on the thread count)."""
     probs = list(range(wl.n_prob)) if problems is None else list(problems)
     lens = np.asarray([wl.seq_lens[wl.seq_of(p)] for p in probs], dtype=np.int32)
     off = np.zeros(len(probs), dtype=np.int64)
@@ -312,13 +344,22 @@ def draw_packed(wl: Workload, problems: Optional[Sequence[int]] = None) -> Packe
     k = np.empty(total, dtype=elt)
     v = np.empty(total, dtype=elt)
     q = np.empty((len(probs), wl.h_q, wl.w, wl.d), dtype=elt)
-    for j, p in enumerate(probs):
-        pi = draw_problem(wl, p)
+
+    def one(j: int) -> None:
         n = int(lens[j]) * wl.h_kv * wl.d
         base = int(off[j]) * wl.h_kv * wl.d
-        k[base:base + n] = pi.k.reshape(-1)
-        v[base:base + n] = pi.v.reshape(-1)
+        shape = (wl.h_kv, int(lens[j]), wl.d)
+        pi = draw_problem(wl, probs[j], k[base:base + n].reshape(shape),
+                          v[base:base + n].reshape(shape))
         q[j] = pi.q_win
+
+    workers = max(1, min(len(probs), threads if threads else min(16, os.cpu_count() or 1)))
+    if workers == 1:
+        for j in range(len(probs)):
+            one(j)
+    else:
+        with concurrent.futures.ThreadPoolExecutor(workers) as ex:
+            list(ex.map(one, range(len(probs))))
     return PackedInputs(q, k, v, lens, off)
 
 

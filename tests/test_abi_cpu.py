@@ -1,0 +1,165 @@
+"""The C ABI library on the host: it loads, exports every symbol the header declares, rejects bad
+arguments before launching anything, and evaluates the depth profiles (a host-only call).
+
+No test here launches a kernel: every call with device pointers fails validation first (the
+pointers are host addresses that are never dereferenced).
+"""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import profiles
+from paper_2609_30738_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kvevict.h")
+
+
+def test_library_exports_every_declared_symbol():
+    text = open(HEADER).read()
+    declared = set(re.findall(r"\b(kv_[a-z_]+)\s*\(", text))
+    assert declared == set(_lib.SYMBOLS)
+    h = _lib.lib()
+    for name in declared:
+        assert hasattr(h, name), name
+
+
+def test_version_and_strerror():
+    assert _lib.version() == 1
+    for code in range(-7, 1):
+        assert _lib.strerror(code) and _lib.strerror(code) != "unknown status"
+    assert _lib.strerror(-99) == "unknown status"
+
+
+# ------------------------------------------------------------------------------------------------
+# validation (host pointers stand in for device pointers; nothing is launched)
+# ------------------------------------------------------------------------------------------------
+
+class HostProblem:
+    def __init__(self, dtype=_lib.KV_BF16, h_q=32, h_kv=8, d=128, w=32, lens=(4096,)):
+        self.lens = np.asarray(lens, dtype=np.int32)
+        self.off = np.zeros(len(lens), dtype=np.int64)
+        self.off[1:] = np.cumsum(self.lens)[:-1]
+        self.s = _lib.KvProblem(dtype, len(lens), h_q, h_kv, d, w, self.lens.ctypes.data,
+                                self.off.ctypes.data, self.lens.ctypes.data, self.off.ctypes.data)
+
+    def ref(self):
+        return ctypes.byref(self.s)
+
+
+BUF = np.zeros(1 << 16, dtype=np.float32)  # 16-byte aligned host block used as a stand-in pointer
+P = ctypes.c_void_p(BUF.ctypes.data)
+NULL = ctypes.c_void_p(0)
+
+
+def window_scores(pr, q=P, k=P, rm=P, rs=P, ws=P, ws_bytes=0, scale=0.088):
+    return _lib.lib().kv_window_scores(pr, q, k, scale, rm, rs, ws, ws_bytes, NULL)
+
+
+def mmr_select(pr, budget=64, cand_mult=4, keep_tail=32, sel=P):
+    return _lib.lib().kv_mmr_select(pr, P, P, P, P, P, budget, cand_mult, keep_tail, sel, NULL,
+                                    NULL, NULL, NULL, 0, NULL)
+
+
+def compact(pr, budget=64, keep_tail=32, k=P):
+    return _lib.lib().kv_compact_cache(pr, k, P, P, budget, keep_tail, P, P, NULL)
+
+
+@pytest.mark.parametrize("kwargs,code", [
+    (dict(dtype=7), _lib.KV_ERR_DTYPE),
+    (dict(h_q=30, h_kv=8), _lib.KV_ERR_SHAPE),
+    (dict(h_q=4, h_kv=8), _lib.KV_ERR_SHAPE),
+    (dict(d=96), _lib.KV_ERR_SHAPE),
+    (dict(w=1), _lib.KV_ERR_SHAPE),
+    (dict(h_q=64, h_kv=8), _lib.KV_ERR_SHAPE),          # G*w = 256 > 128
+    (dict(h_q=32, h_kv=8, w=24), _lib.KV_ERR_SHAPE),     # w != 32 needs G*w <= 64
+    (dict(lens=(32,)), _lib.KV_ERR_SHAPE),               # L < w + 1
+    (dict(lens=(4096, 20)), _lib.KV_ERR_SHAPE),
+    (dict(lens=(1 << 25,)), _lib.KV_ERR_SHAPE),
+])
+def test_problem_validation(kwargs, code):
+    pr = HostProblem(**kwargs)
+    assert window_scores(pr.ref()) == code
+    assert _lib.lib().kv_workspace_bytes(pr.ref(), 64, 4, 32) == 0
+
+
+def test_null_pointers():
+    pr = HostProblem()
+    assert _lib.lib().kv_window_scores(None, P, P, 0.1, P, P, P, 1 << 30, NULL) == _lib.KV_ERR_NULL
+    assert window_scores(pr.ref(), q=NULL) == _lib.KV_ERR_NULL
+    assert window_scores(pr.ref(), rs=NULL) == _lib.KV_ERR_NULL
+    assert mmr_select(pr.ref(), sel=NULL) == _lib.KV_ERR_NULL
+    assert compact(pr.ref(), k=NULL) == _lib.KV_ERR_NULL
+    pr.s.len_dev = None
+    assert window_scores(pr.ref()) == _lib.KV_ERR_NULL
+
+
+def test_workspace_checks():
+    pr = HostProblem()
+    need = _lib.lib().kv_workspace_bytes(pr.ref(), 64, 4, 32)
+    assert need > 0 and need % 256 == 0
+    assert window_scores(pr.ref(), ws_bytes=need - 1) == _lib.KV_ERR_WORKSPACE
+    assert window_scores(pr.ref(), ws=NULL, ws_bytes=need) == _lib.KV_ERR_WORKSPACE
+    odd = ctypes.c_void_p(BUF.ctypes.data + 16)  # 16-byte but not 256-byte aligned
+    assert window_scores(pr.ref(), ws=odd, ws_bytes=need) == _lib.KV_ERR_WORKSPACE
+
+
+def test_misaligned_and_nonfinite_arguments():
+    pr = HostProblem()
+    odd = ctypes.c_void_p(BUF.ctypes.data + 4)
+    assert window_scores(pr.ref(), k=odd) == _lib.KV_ERR_ARG
+    assert window_scores(pr.ref(), scale=float("nan")) == _lib.KV_ERR_ARG
+    assert compact(pr.ref(), k=odd) == _lib.KV_ERR_ARG
+
+
+def test_budget_and_candidate_checks():
+    pr = HostProblem(lens=(4096, 100))
+    assert mmr_select(pr.ref(), budget=0) == _lib.KV_ERR_BUDGET
+    assert mmr_select(pr.ref(), budget=69) == _lib.KV_ERR_BUDGET      # 100 - 32 = 68 candidates
+    assert mmr_select(pr.ref(), keep_tail=-1) == _lib.KV_ERR_ARG
+    assert mmr_select(pr.ref(), keep_tail=100) == _lib.KV_ERR_ARG
+    assert mmr_select(pr.ref(), cand_mult=-1) == _lib.KV_ERR_ARG
+    assert mmr_select(pr.ref(), budget=64, cand_mult=0) == _lib.KV_ERR_SHAPE  # 4064 > 512
+    assert mmr_select(pr.ref(), budget=64, cand_mult=16) == _lib.KV_ERR_SHAPE  # 1024 > 512
+    assert compact(pr.ref(), budget=69) == _lib.KV_ERR_BUDGET
+    big = HostProblem(lens=(20000,))
+    assert compact(big.ref(), budget=9000) == _lib.KV_ERR_BUDGET
+    assert _lib.lib().kv_candidate_stride(pr.ref(), 64, 4, 32) == 256
+    assert _lib.lib().kv_candidate_stride(pr.ref(), 16, 0, 32) == 4064
+    assert _lib.lib().kv_candidate_stride(pr.ref(), 0, 4, 32) == 0
+
+
+# ------------------------------------------------------------------------------------------------
+# depth profiles (host-only entry point) against the oracle
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("family,params,n_layers", [
+    ("global", [math.asinh(-0.15)], 32),
+    ("global", [0.0], 1),
+    ("segments", [math.asinh(-1.0), math.asinh(-0.5), math.asinh(-1.2)], 32),
+    ("segments", [0.3, -0.2], 32),
+    ("segments", [0.1 * i for i in range(8)], 32),
+    ("curve", [-1.47190, 6.19355, -6.0], 32),
+    ("curve", [0.5, -1.0, 0.25], 7),
+    ("curve", [0.5, -1.0, 0.25], 1),
+])
+def test_depth_profile_matches_oracle(family, params, n_layers):
+    got = _lib.depth_profile(family, params, n_layers)
+    ref = np.array(profiles.layer_lambdas(family, params, n_layers))
+    np.testing.assert_allclose(got, ref.astype(np.float32), rtol=2 ** -23, atol=0)
+
+
+def test_depth_profile_errors():
+    h = _lib.lib()
+    p = (ctypes.c_double * 3)(0.1, 0.2, 0.3)
+    out = (ctypes.c_float * 32)()
+    assert h.kv_depth_profile(9, p, 1, 32, out) == _lib.KV_ERR_ARG
+    assert h.kv_depth_profile(_lib.KV_PROFILE_CURVE, p, 2, 32, out) == _lib.KV_ERR_ARG
+    assert h.kv_depth_profile(_lib.KV_PROFILE_GLOBAL, p, 3, 32, out) == _lib.KV_ERR_ARG
+    assert h.kv_depth_profile(_lib.KV_PROFILE_SEGMENTS, p, 3, 2, out) == _lib.KV_ERR_ARG
+    assert h.kv_depth_profile(_lib.KV_PROFILE_GLOBAL, None, 1, 32, out) == _lib.KV_ERR_NULL
+    assert h.kv_depth_profile(_lib.KV_PROFILE_GLOBAL, p, 1, 0, out) == _lib.KV_ERR_ARG

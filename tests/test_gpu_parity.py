@@ -1,0 +1,103 @@
+"""GPU parity: every C-ABI entry point against the CPU oracle on seeded synthetic inputs.
+
+Sizes span several key chunks and MFMA tiles with ragged tails; the full-size workloads run in the
+benchmark's launch configuration (all layers in one batch) and are checked on sampled problems.
+"""
+import numpy as np
+import pytest
+
+from paper_2609_30738_amd import workloads
+from tests import gpu_cases
+
+pytestmark = pytest.mark.gpu
+
+
+def _all(run, heads=None):
+    reports = []
+    for j in range(len(run.problems)):
+        reports += gpu_cases.check_problem(run, j, heads)
+    print("  ", gpu_cases.summarize(reports), flush=True)
+    return reports
+
+
+def test_tiny_f32_unfused_with_attention():
+    """fp32 path, 2 query heads on 1 kv head, d=64, W=8 (general window reduction)."""
+    reports = _all(gpu_cases.run_gpu(workloads.tiny_f32(), want_attn=True))
+    assert all(r.candidates_equal for r in reports)
+
+
+def test_tiny_f32_fused_exact_greedy_over_all_candidates():
+    """cand_mult = 0: the greedy runs over every prefix position."""
+    _all(gpu_cases.run_gpu(workloads.tiny_f32(), fused=True, cand_mult=0))
+
+
+@pytest.mark.parametrize("keep_tail", [0, 3])
+def test_tiny_f32_keep_tail(keep_tail):
+    _all(gpu_cases.run_gpu(workloads.tiny_f32(), keep_tail=keep_tail))
+
+
+def test_mistral_layer_unfused():
+    """One Mistral-7B layer, bf16, L=4096, W=32, B=64, lambda1=0.3, lambda2=-0.8."""
+    reports = _all(gpu_cases.run_gpu(workloads.mistral_layer()))
+    assert sum(r.exact_steps for r in reports) >= 0.9 * sum(r.steps for r in reports)
+
+
+def test_mistral_layer_fused_with_attention_short_context():
+    """Ragged context (L=1337: partial chunk and partial tile) with the attention output."""
+    wl = workloads.mistral_layer()
+    wl.seq_lens = [1337]
+    _all(gpu_cases.run_gpu(wl, want_attn=True))
+
+
+@pytest.mark.parametrize("budget", [32, 64, 128])
+def test_segments_profile_budget_sweep_scaled(budget):
+    """Three-segment lambda2 over 3 layers (one per segment), L=2048, B in {32, 64, 128}."""
+    wl = workloads.mistral_pass_8k(budget=budget, n_layers=3, L=2048)
+    _all(gpu_cases.run_gpu(wl, fused=True))
+
+
+def test_curve_profile_scaled():
+    """Quadratic lambda2 profile with passages repeated twice, 4 layers of L=6000."""
+    wl = workloads.mistral_pass_32k(n_layers=4, L=6000, n_clusters=16, n_passages=4)
+    _all(gpu_cases.run_gpu(wl, fused=True))
+
+
+@pytest.mark.parametrize("run", ["dispersion_only", "redundancy_only", "both"])
+def test_ragged_batch_scaled(run):
+    """Three sequences of different lengths x 2 layers, B=128, the three term-ablation runs."""
+    wl = workloads.ragged_batch(run, n_seq=3, n_layers=2, len_range=(700, 3100))
+    _all(gpu_cases.run_gpu(wl, fused=True))
+
+
+def test_compaction_of_oracle_selection():
+    """kv_compact_cache fed with the oracle's admissions reproduces the oracle's compacted rows."""
+    import torch
+    from oracle import evict
+    from paper_2609_30738_amd import _lib, api
+    wl = workloads.mistral_layer()
+    wl.seq_lens = [900]
+    print(f"[gpu case] compaction {wl.name} L=900", flush=True)
+    pk = workloads.draw_packed(wl)
+    q, k, v = pk.q_win[0], pk.k.reshape(wl.h_kv, 900, wl.d), pk.v.reshape(wl.h_kv, 900, wl.d)
+    res = evict.evict_problem(q, k, v, wl.dtype, wl.scale, 0.3, -0.8, wl.budget)
+    sel = np.array([res.heads[g].trace.selected for g in range(wl.h_kv)], dtype=np.int32)
+    inp = api.upload(wl.dtype, wl.h_q, wl.h_kv, wl.d, wl.w, pk.q_win, pk.k, pk.v, pk.lens,
+                     pk.tok_off, [0.3], [-0.8])
+    rows = wl.budget + wl.w
+    k_out = torch.empty(wl.h_kv * rows * wl.d, dtype=inp.k.dtype, device=inp.k.device)
+    v_out = torch.empty_like(k_out)
+    _lib.compact_cache(inp.batch, inp.k, inp.v, api.to_device(sel.reshape(-1)), wl.budget, wl.w,
+                       k_out, v_out)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(api.to_host_bits(k_out).reshape(res.k_out.shape), res.k_out)
+    np.testing.assert_array_equal(api.to_host_bits(v_out).reshape(res.v_out.shape), res.v_out)
+
+
+def test_deterministic_repeat():
+    """Two runs on the same inputs give bitwise-identical outputs (no races in the reductions)."""
+    wl = workloads.mistral_pass_32k(n_layers=2, L=5000, n_clusters=16, n_passages=4)
+    a = gpu_cases.run_gpu(wl, fused=True)
+    b = gpu_cases.run_gpu(wl, fused=True, packed=a.packed)
+    for name in ("row_max", "row_sum", "mu", "sigma", "sel_idx", "sel_score", "cand_idx",
+                 "cand_corr", "k_out", "v_out"):
+        np.testing.assert_array_equal(a.host[name], b.host[name], err_msg=name)
