@@ -3,6 +3,7 @@
 // before every argument has been checked.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -105,7 +106,7 @@ size_t kv_workspace_bytes(const kv_problem* pr, int32_t budget, int32_t cand_mul
   (void)budget;
   (void)cand_mult;
   (void)keep_tail;
-  return align_up(kv::window_stats_ws_bytes(s));
+  return align_up(std::max(kv::window_stats_ws_bytes(s), kv::fused_ws_bytes(s)));
 }
 
 int32_t kv_candidate_stride(const kv_problem* pr, int32_t budget, int32_t cand_mult,
@@ -151,9 +152,31 @@ int kv_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float sc
 int kv_window_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float scale,
                        float* row_max, float* row_sum, float* mu, float* sigma, void* ws,
                        size_t ws_bytes, void* stream) {
-  int st = kv_window_scores(pr, q_win, k, scale, row_max, row_sum, ws, ws_bytes, stream);
+  kv::Shape s;
+  int st = check_problem(pr, &s);
   if (st != KV_OK) return st;
-  return kv_mu_sigma(pr, q_win, k, scale, row_max, row_sum, mu, sigma, nullptr, stream);
+  if (!q_win || !k || !row_max || !row_sum || !mu || !sigma) return KV_ERR_NULL;
+  if (!aligned16(q_win) || !aligned16(k)) return KV_ERR_ARG;
+  if (!std::isfinite(scale)) return KV_ERR_ARG;
+  const size_t need = align_up(std::max(kv::window_stats_ws_bytes(s), kv::fused_ws_bytes(s)));
+  if (ws_bytes < need || !ws || (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1)))
+    return KV_ERR_WORKSPACE;
+  int64_t items = 0;
+  for (int p = 0; p < pr->n_prob; ++p)
+    items += (int64_t)pr->h_kv * ((pr->len_host[p] + kv::kFusedChunk - 1) / kv::kFusedChunk);
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (items <= INT32_MAX) {
+    bool used = false;
+    const hipError_t e = kv::launch_window_mu_sigma_fused(s, q_win, k, scale, (int)items, ws,
+                                                          row_max, row_sum, mu, sigma, &used, hs);
+    if (e != hipSuccess) return KV_ERR_LAUNCH;
+    if (used) return KV_OK;
+  }
+  // shapes the single-pass kernel does not cover: row statistics, then a second pass over K
+  st = launch_status(kv::launch_window_stats(s, q_win, k, scale, ws, row_max, row_sum, hs));
+  if (st != KV_OK) return st;
+  return launch_status(kv::launch_mu_sigma(s, q_win, k, scale, row_max, row_sum, mu, sigma,
+                                           nullptr, hs));
 }
 
 int kv_mmr_select(const kv_problem* pr, const float* mu, const float* sigma, const void* k,
@@ -183,6 +206,7 @@ int kv_mmr_select(const kv_problem* pr, const float* mu, const float* sigma, con
   a.keep_tail = keep_tail;
   a.cand_stride = kv_candidate_stride(pr, budget, cand_mult, keep_tail);
   a.max_cand = max_cand;
+  a.max_cand_all = max_candidates(pr, budget, 0, keep_tail);
   a.sel_idx = sel_idx;
   a.sel_score = sel_score;
   a.cand_idx = cand_idx;

@@ -13,6 +13,8 @@ constexpr int kDtBf16 = 1;
 
 // Keys per work item of the window kernels (a multiple of 4 waves x 32 keys).
 constexpr int kWindowChunk = 1024;
+// Keys per work item of the single-pass window kernel (16 waves x 32 keys).
+constexpr int kFusedChunk = 512;
 
 struct Shape {
   int dtype;  // 0 = fp32, 1 = bf16
@@ -36,6 +38,15 @@ hipError_t launch_mu_sigma(const Shape& s, const void* q_win, const void* k, flo
                            const float* row_max, const float* row_sum, float* mu, float* sigma,
                            float* attn, hipStream_t stream);
 
+// Single-pass row statistics + mu/sigma (bf16, w = 32, G in {1, 2, 4}, scale > 0).  Sets *used to
+// false (and enqueues nothing) when the shape or the device cannot run it; the caller then runs the
+// two-pass kernels.  total_items = sum_p h_kv * ceil(L_p / kFusedChunk).
+size_t fused_ws_bytes(const Shape& s);
+hipError_t launch_window_mu_sigma_fused(const Shape& s, const void* q_win, const void* k,
+                                        float scale, int total_items, void* ws, float* row_max,
+                                        float* row_sum, float* mu, float* sigma, bool* used,
+                                        hipStream_t stream);
+
 struct SelectArgs {
   const float* mu;
   const float* sigma;
@@ -43,6 +54,7 @@ struct SelectArgs {
   const float* lambda1;
   const float* lambda2;
   int budget, cand_mult, keep_tail, cand_stride, max_cand;
+  int max_cand_all;  // max_p (L_p - keep_tail): every position that competes for a candidate slot
   int32_t* sel_idx;
   float* sel_score;
   int32_t* cand_idx;

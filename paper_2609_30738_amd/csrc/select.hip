@@ -4,17 +4,20 @@
 //   1. base scores s_i = fma(lambda1, sigma_i, mu_i) over the candidates [0, n_cand), their maximum
 //      (the normaliser, clamped at 1e-12), and the C-th largest score by a most-significant-digit
 //      radix select over order-preserving 32-bit keys (4 passes of 8 bits, wave-private LDS
-//      histograms filled with wave-aggregated increments);
+//      histograms filled with LDS atomics); the keys are staged in LDS once with
+//      coalesced loads when they fit (up to 34816 candidates), otherwise recomputed per pass;
 //   2. the candidate set P: every score above the threshold plus the lowest positions among those
 //      equal to it, compacted in ascending position order (ballot ranks inside a wave, LDS prefix
 //      across waves);
 //   3. B greedy steps.  Thread t owns candidates t, t + 256, ...: it keeps their keys in registers,
 //      their normalised score s~, running max-cosine and admitted flag.  Each step updates the
-//      running maxima against the last admitted key (read once from an LDS copy of the candidate
-//      keys), forms s~ + lambda2 * corr, and finds the (score, lowest slot) maximum with a wave
-//      shuffle reduction and one barrier; the per-wave winners are double-buffered so that one
-//      barrier per step suffices.
+//      running maxima against the last admitted key (read from an LDS copy of the candidate keys),
+//      forms s~ + lambda2 * corr, and finds the (score, lowest slot) maximum: a DPP / permlane
+//      maximum and a ballot inside each wave, then one barrier; the per-wave winners are
+//      double-buffered so that one barrier per step suffices.
 #include <float.h>
+
+#include <algorithm>
 
 #include "common.h"
 #include "kernels.h"
@@ -25,23 +28,25 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
-constexpr int kMaxCandBytes = 131072;  // LDS copy of the candidate keys
+constexpr int kMaxCandBytes = 131072;        // LDS copy of the candidate keys
+constexpr int kMaxStagedKeyBytes = 139264;  // LDS copy of every candidate's score key (34816)
 
 __device__ __forceinline__ uint32_t order_key(float x) {
   const uint32_t u = __float_as_uint(x);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Add one to hist[digit] for every active lane, one LDS increment per distinct digit in the wave.
+// Add one to hist[digit] for every active lane.  The digit of the first active lane is counted
+// with one ballot and a single LDS add (the common case: most scores share their leading digits);
+// lanes with other digits use LDS atomics, which handle scattered digits without conflicts.
 __device__ __forceinline__ void wave_hist_add(uint32_t* hist, uint32_t digit, bool active) {
-  uint64_t pending = __ballot(active);
-  while (pending) {
-    const int leader = __ffsll((unsigned long long)pending) - 1;
-    const uint32_t dl = __shfl(digit, leader, 64);
-    const uint64_t same = __ballot(active && digit == dl);
-    if ((threadIdx.x & 63) == leader) atomicAdd(&hist[dl], (uint32_t)__popcll(same));
-    pending &= ~same;
-  }
+  const uint64_t act = __ballot(active);
+  if (act == 0) return;
+  const int leader = __ffsll((unsigned long long)act) - 1;
+  const uint32_t dl = __builtin_amdgcn_readlane(digit, leader);
+  const uint64_t same = __ballot(active && digit == dl);
+  if ((int)(threadIdx.x & 63) == leader) atomicAdd(&hist[dl], (uint32_t)__popcll(same));
+  if (active && digit != dl) atomicAdd(&hist[digit], 1u);
 }
 
 // (score, slot) packed so that a larger value means a larger score, then a lower slot.
@@ -57,10 +62,35 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
   }
   return v;
 }
+// Maximum over the 64 lanes, in every lane: quad and row steps with DPP, then permlane swaps
+// between rows and between the wave's halves.
 __device__ __forceinline__ float wave_max_f(float v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
-  return v;
+#define KV_DPPF(x, CTRL) __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), CTRL, 0xF, 0xF, false))
+  v = fmaxf(v, KV_DPPF(v, 0xB1));   // quad_perm [1,0,3,2]
+  v = fmaxf(v, KV_DPPF(v, 0x4E));   // quad_perm [2,3,0,1]
+  v = fmaxf(v, KV_DPPF(v, 0x124));  // row_ror:4
+  v = fmaxf(v, KV_DPPF(v, 0x128));  // row_ror:8
+#undef KV_DPPF
+  auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+  auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
+}
+
+// (score, slot) of the best candidate of the wave, ties to the lowest slot.
+__device__ __forceinline__ uint64_t wave_best(float score, int slot) {
+  const float wm = wave_max_f(score);
+  const uint64_t tied = __ballot(score == wm);
+  int best = __builtin_amdgcn_readlane(slot, __ffsll((unsigned long long)tied) - 1);
+  if (__popcll(tied) > 1) {  // exact tie between lanes: lowest slot among them
+    uint64_t rest = tied;
+    while (rest) {
+      const int l = __ffsll((unsigned long long)rest) - 1;
+      best = min(best, __builtin_amdgcn_readlane(slot, l));
+      rest &= rest - 1;
+    }
+  }
+  return pack_best(wm, best);
 }
 
 // Key row of one candidate held in registers, and its dot product with a row in LDS.
@@ -160,17 +190,19 @@ struct SelectShared {
 
 }  // namespace
 
-template <int DT, int D, int CPT>
+template <int DT, int D, int CPT, bool STAGED>
 __global__ __launch_bounds__(kThreads) void mmr_select_kernel(
     const float* __restrict__ mu, const float* __restrict__ sigma,
     const typename Elem<DT>::T* __restrict__ k, const int32_t* __restrict__ lens,
     const int64_t* __restrict__ tok_off, const float* __restrict__ lambda1,
     const float* __restrict__ lambda2, int h_kv, int budget, int cand_mult, int keep_tail,
-    int cand_stride, int32_t* __restrict__ sel_idx, float* __restrict__ sel_score,
+    int cand_stride, int max_cand, int32_t* __restrict__ sel_idx, float* __restrict__ sel_score,
     int32_t* __restrict__ cand_idx, float* __restrict__ cand_corr) {
   using T = typename Elem<DT>::T;
   __shared__ SelectShared sh;
-  extern __shared__ __align__(16) unsigned char dyn[];  // [C] positions, [C] 1/|k|, [C][D] keys
+  // dynamic LDS: [max_cand] positions, [max_cand] 1/|k|, then a region that first holds the
+  // order-preserving keys of every candidate score (STAGED) and then the candidates' key rows
+  extern __shared__ __align__(16) unsigned char dyn[];
   const int g = blockIdx.x % h_kv, p = blockIdx.x / h_kv;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = lens[p];
@@ -182,35 +214,78 @@ __global__ __launch_bounds__(kThreads) void mmr_select_kernel(
   const T* kg = k + base * D;
   const float lam1 = lambda1[p], lam2 = lambda2[p];
   int32_t* cpos = reinterpret_cast<int32_t*>(dyn);
-  float* cinv = reinterpret_cast<float*>(dyn + (size_t)C * 4);
-  T* ckeys = reinterpret_cast<T*>(dyn + (((size_t)C * 8 + 15) & ~(size_t)15));
+  float* cinv = reinterpret_cast<float*>(dyn + (size_t)max_cand * 4);
+  unsigned char* region = dyn + (((size_t)max_cand * 8 + 15) & ~(size_t)15);
+  uint32_t* skeys = reinterpret_cast<uint32_t*>(region);
+  T* ckeys = reinterpret_cast<T*>(region);
+  const bool take_all = (C >= n_cand);
 
-  // ---- 1. normaliser and radix select of the C-th largest base score --------------------------
+  // ---- 0. base scores s_i = mu_i + lambda1 sigma_i (one rounding) and their maximum -----------
+  float local_max = -INFINITY;
+  if constexpr (STAGED) {
+    // mu / sigma rows start at a multiple of 4 floats only if base is; stage element-wise until
+    // the first aligned index, then 4 per lane with several loads in flight
+    const int head = (int)((4 - (base & 3)) & 3) < n_cand ? (int)((4 - (base & 3)) & 3) : n_cand;
+    if (tid < head) {
+      const float sv = fmaf(lam1, sg_g[tid], mu_g[tid]);
+      local_max = fmaxf(local_max, sv);
+      skeys[tid] = order_key(sv);
+    }
+    const int n4 = (n_cand - head) / 4;
+    const float4* mu4 = reinterpret_cast<const float4*>(mu_g + head);
+    const float4* sg4 = reinterpret_cast<const float4*>(sg_g + head);
+#pragma unroll 4
+    for (int v = tid; v < n4; v += kThreads) {
+      const float4 m = mu4[v], sgv = sg4[v];
+      const float s0 = fmaf(lam1, sgv.x, m.x), s1 = fmaf(lam1, sgv.y, m.y);
+      const float s2 = fmaf(lam1, sgv.z, m.z), s3 = fmaf(lam1, sgv.w, m.w);
+      local_max = fmaxf(fmaxf(local_max, fmaxf(s0, s1)), fmaxf(s2, s3));
+      const int i = head + 4 * v;
+      skeys[i] = order_key(s0);
+      skeys[i + 1] = order_key(s1);
+      skeys[i + 2] = order_key(s2);
+      skeys[i + 3] = order_key(s3);
+    }
+    for (int i = head + 4 * n4 + tid; i < n_cand; i += kThreads) {
+      const float sv = fmaf(lam1, sg_g[i], mu_g[i]);
+      local_max = fmaxf(local_max, sv);
+      skeys[i] = order_key(sv);
+    }
+    __syncthreads();
+  } else {
+    for (int i = tid; i < n_cand; i += kThreads) local_max = fmaxf(local_max, fmaf(lam1, sg_g[i], mu_g[i]));
+  }
+  auto key_at = [&](int i) -> uint32_t {
+    if constexpr (STAGED) return skeys[i];
+    else return order_key(fmaf(lam1, sg_g[i], mu_g[i]));
+  };
+  {
+    const float wm = wave_max_f(local_max);
+    if (lane == 0) sh.wave_max[wave] = wm;
+  }
+
+  // ---- 1. the C-th largest key: most-significant-digit radix select ---------------------------
   uint32_t prefix = 0, pmask = 0;
   int need = C;
-  float local_max = -INFINITY;
-  const bool take_all = (C >= n_cand);
-  for (int pass = 0; pass < (take_all ? 1 : 4); ++pass) {
+  for (int pass = 0; pass < (take_all ? 0 : 4); ++pass) {
     const int shift = 24 - 8 * pass;
     for (int i = tid; i < kWaves * 256; i += kThreads) (&sh.hist[0][0])[i] = 0u;
     __syncthreads();
-    const int n_iter = (n_cand + kThreads - 1) / kThreads;
+    const int n_iter = (n_cand + 4 * kThreads - 1) / (4 * kThreads);
     for (int it = 0; it < n_iter; ++it) {
-      const int i = it * kThreads + tid;
-      const bool in = i < n_cand;
-      const float s = in ? fmaf(lam1, sg_g[i], mu_g[i]) : 0.f;
-      if (pass == 0 && in) local_max = fmaxf(local_max, s);
-      if (!take_all) {
-        const uint32_t key = order_key(s);
-        wave_hist_add(sh.hist[wave], (key >> shift) & 255u, in && (key & pmask) == prefix);
+      uint32_t kk[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {  // four independent reads in flight
+        const int i = (4 * it + q) * kThreads + tid;
+        kk[q] = i < n_cand ? key_at(i) : 0u;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = (4 * it + q) * kThreads + tid;
+        wave_hist_add(sh.hist[wave], (kk[q] >> shift) & 255u, i < n_cand && (kk[q] & pmask) == prefix);
       }
     }
-    if (pass == 0) {
-      const float wm = wave_max_f(local_max);
-      if (lane == 0) sh.wave_max[wave] = wm;
-    }
     __syncthreads();
-    if (take_all) break;
     // suffix sums over bins (bin 255 = largest digit)
     const uint32_t cnt = sh.hist[0][tid] + sh.hist[1][tid] + sh.hist[2][tid] + sh.hist[3][tid];
     sh.scan[tid] = cnt;
@@ -221,8 +296,8 @@ __global__ __launch_bounds__(kThreads) void mmr_select_kernel(
       sh.scan[tid] += add;
       __syncthreads();
     }
-    const uint32_t ge = sh.scan[tid];                               // count with digit >= tid
-    const uint32_t gt = (tid + 1 < 256) ? sh.scan[tid + 1] : 0u;    // count with digit > tid
+    const uint32_t ge = sh.scan[tid];                             // count with digit >= tid
+    const uint32_t gt = (tid + 1 < 256) ? sh.scan[tid + 1] : 0u;  // count with digit > tid
     if (ge >= (uint32_t)need && gt < (uint32_t)need) {
       sh.sel_threshold = prefix | ((uint32_t)tid << shift);
       sh.sel_need = need - (int)gt;
@@ -233,6 +308,7 @@ __global__ __launch_bounds__(kThreads) void mmr_select_kernel(
     pmask |= 255u << shift;
     __syncthreads();
   }
+  __syncthreads();
   float den = fmaxf(fmaxf(sh.wave_max[0], sh.wave_max[1]), fmaxf(sh.wave_max[2], sh.wave_max[3]));
   den = fmaxf(den, 1e-12f);
 
@@ -243,13 +319,19 @@ __global__ __launch_bounds__(kThreads) void mmr_select_kernel(
     const int per_wave = (n_cand + kWaves - 1) / kWaves;
     const int w0 = wave * per_wave, w1 = min(n_cand, w0 + per_wave);
     uint32_t n_gt = 0, n_eq = 0;
-    for (int i0 = w0; i0 < w1; i0 += 64) {
-      const int i = i0 + lane;
-      uint32_t key = 0;
-      const bool in = i < w1;
-      if (in && !take_all) key = order_key(fmaf(lam1, sg_g[i], mu_g[i]));
-      n_gt += __popcll(__ballot(in && (take_all || key > thr)));
-      n_eq += __popcll(__ballot(in && !take_all && key == thr));
+    for (int i0 = w0; i0 < w1; i0 += 256) {
+      uint32_t kk[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = i0 + 64 * q + lane;
+        kk[q] = (i < w1 && !take_all) ? key_at(i) : 0u;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const bool in = i0 + 64 * q + lane < w1;
+        n_gt += __popcll(__ballot(in && (take_all || kk[q] > thr)));
+        n_eq += __popcll(__ballot(in && !take_all && kk[q] == thr));
+      }
     }
     if (lane == 0) {
       sh.wave_cnt[0][wave] = n_gt;
@@ -264,24 +346,31 @@ __global__ __launch_bounds__(kThreads) void mmr_select_kernel(
       eq_before += eq_v;
     }
     const uint64_t lanes_below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    for (int i0 = w0; i0 < w1; i0 += 64) {
-      const int i = i0 + lane;
-      const bool in = i < w1;
-      uint32_t key = 0;
-      if (in && !take_all) key = order_key(fmaf(lam1, sg_g[i], mu_g[i]));
-      const bool is_gt = in && (take_all || key > thr);
-      const bool is_eq = in && !take_all && key == thr;
-      const uint64_t eqm = __ballot(is_eq);
-      const uint32_t eq_rank = eq_before + (uint32_t)__popcll(eqm & lanes_below);
-      const bool taken = is_gt || (is_eq && eq_rank < (uint32_t)need);
-      const uint64_t tm = __ballot(taken);
-      const uint32_t slot = out + (uint32_t)__popcll(tm & lanes_below);
-      if (taken && slot < (uint32_t)C) cpos[slot] = i;
-      out += (uint32_t)__popcll(tm);
-      eq_before += (uint32_t)__popcll(eqm);
+    for (int i0 = w0; i0 < w1; i0 += 256) {
+      uint32_t kk[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = i0 + 64 * q + lane;
+        kk[q] = (i < w1 && !take_all) ? key_at(i) : 0u;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {  // blocks of 64 in ascending position order
+        const int i = i0 + 64 * q + lane;
+        const bool in = i < w1;
+        const bool is_gt = in && (take_all || kk[q] > thr);
+        const bool is_eq = in && !take_all && kk[q] == thr;
+        const uint64_t eqm = __ballot(is_eq);
+        const uint32_t eq_rank = eq_before + (uint32_t)__popcll(eqm & lanes_below);
+        const bool taken = is_gt || (is_eq && eq_rank < (uint32_t)need);
+        const uint64_t tm = __ballot(taken);
+        const uint32_t slot = out + (uint32_t)__popcll(tm & lanes_below);
+        if (taken && slot < (uint32_t)C) cpos[slot] = i;
+        out += (uint32_t)__popcll(tm);
+        eq_before += (uint32_t)__popcll(eqm);
+      }
     }
   }
-  __syncthreads();
+  __syncthreads();  // the staged score keys are dead from here on: the region takes key rows
 
   // ---- 3. greedy admission -------------------------------------------------------------------
   KeyRow<DT, D> key[CPT];
@@ -309,7 +398,8 @@ __global__ __launch_bounds__(kThreads) void mmr_select_kernel(
   int last = -1;
   float last_inv = 0.f;
   for (int t = 0; t < budget; ++t) {
-    uint64_t mine = 0;
+    float my_score = -INFINITY;  // admitted slots rank below every live score
+    int my_slot = 0x7FFFFFFF;
 #pragma unroll
     for (int q = 0; q < CPT; ++q) {
       if (!admitted[q]) {
@@ -319,11 +409,13 @@ __global__ __launch_bounds__(kThreads) void mmr_select_kernel(
         }
         float sc = fmaf(lam2, corr[q], st[q]);
         if (!(sc > -INFINITY)) sc = -FLT_MAX;  // NaN or -inf still ranks above admitted slots
-        const uint64_t pk = pack_best(sc, tid + q * kThreads);
-        mine = pk > mine ? pk : mine;
+        if (sc > my_score) {  // q ascending: ties keep the lower slot
+          my_score = sc;
+          my_slot = tid + q * kThreads;
+        }
       }
     }
-    const uint64_t wbest = wave_max_u64(mine);
+    const uint64_t wbest = wave_best(my_score, my_slot);
     if (lane == 0) sh.best[t & 1][wave] = wbest;
     __syncthreads();
     uint64_t b = sh.best[t & 1][0];
@@ -381,19 +473,29 @@ int select_max_candidates(int d, int elem_bytes) {
 }
 
 namespace {
-template <int DT, int D, int CPT>
-hipError_t select_dispatch(const Shape& s, const SelectArgs& a, hipStream_t st) {
+template <int DT, int D, int CPT, bool STAGED>
+hipError_t select_launch(const Shape& s, const SelectArgs& a, hipStream_t st) {
   using T = typename Elem<DT>::T;
-  const size_t dyn = (((size_t)a.max_cand * 8 + 15) & ~(size_t)15) + (size_t)a.max_cand * D * sizeof(T);
-  auto kern = mmr_select_kernel<DT, D, CPT>;
+  const size_t region = std::max((size_t)a.max_cand * D * sizeof(T),
+                                 STAGED ? (size_t)a.max_cand_all * 4 : (size_t)0);
+  const size_t dyn = (((size_t)a.max_cand * 8 + 15) & ~(size_t)15) + region;
+  auto kern = mmr_select_kernel<DT, D, CPT, STAGED>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
   if (e != hipSuccess) return e;
   kern<<<dim3((unsigned)(s.n_prob * s.h_kv)), kThreads, dyn, st>>>(
       a.mu, a.sigma, static_cast<const T*>(a.k), s.lens, s.tok_off, a.lambda1, a.lambda2, s.h_kv,
-      a.budget, a.cand_mult, a.keep_tail, a.cand_stride, a.sel_idx, a.sel_score, a.cand_idx,
-      a.cand_corr);
+      a.budget, a.cand_mult, a.keep_tail, a.cand_stride, a.max_cand, a.sel_idx, a.sel_score,
+      a.cand_idx, a.cand_corr);
   return hipGetLastError();
+}
+
+// Score keys are staged in LDS when every problem's candidates fit next to the key rows.
+template <int DT, int D, int CPT>
+hipError_t select_dispatch(const Shape& s, const SelectArgs& a, hipStream_t st) {
+  if ((size_t)a.max_cand_all * 4 <= (size_t)kMaxStagedKeyBytes)
+    return select_launch<DT, D, CPT, true>(s, a, st);
+  return select_launch<DT, D, CPT, false>(s, a, st);
 }
 
 template <int DT, int D>
