@@ -49,7 +49,7 @@ def lambdas(wl):
 
 
 def algorithmic_bytes(wl) -> dict:
-    """Bytes the method must move per pass (see DESIGN.md): K once and Q_W once (scoring), the kept
+    """Bytes the method must move per pass: K once and Q_W once (scoring), the kept
     rows of K and V read and written (compaction) and the admitted indices."""
     e = 2 if wl.dtype == "bf16" else 4
     lens = wl.lens.astype(np.int64)
@@ -105,6 +105,18 @@ def cpu_baseline(wl, packed_layers, n_layers_sample: int) -> dict:
                       f"({dt:.1f} s), scaled to the full pass"}
 
 
+def copy_probe(torch, mib: int) -> None:
+    """A plain copy of known size: each launch reads and writes exactly mib MiB of HBM."""
+    n = mib << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n, "launches": 3}), flush=True)
+
+
 def main() -> None:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -115,6 +127,9 @@ def main() -> None:
                     help="layers of the oracle sample for the CPU baseline (0: skip)")
     ap.add_argument("--unfused", action="store_true",
                     help="time kv_window_scores + kv_mu_sigma instead of kv_window_mu_sigma")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run a plain device copy of this many MiB three times (the known-size "
+                         "kernel that scales the HBM byte counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
@@ -126,6 +141,9 @@ def main() -> None:
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
     torch.cuda.set_device(0)
+    if args.copy_probe_mib > 0:
+        copy_probe(torch, args.copy_probe_mib)
+        return
     _lib.lib()  # fail loudly if the library is missing
 
     wl = make_workload(args.workload)

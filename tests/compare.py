@@ -17,7 +17,9 @@ import numpy as np
 
 from oracle import evict
 
-# fp32 error model of the GPU path ("tolerances")
+# fp32 error model of the GPU path: statistics within 1e-5 relative (sigma with a floor of
+# 1e-6 mu, since sigma is formed from values of size mu), cosines within 2e-6 absolute, and the
+# scores built from them within the sum of their parts.
 MU_RTOL = 1e-5
 SIGMA_RTOL = 1e-5
 SIGMA_MU_FLOOR = 1e-6
