@@ -161,14 +161,17 @@ int kv_window_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, f
   const size_t need = align_up(std::max(kv::window_stats_ws_bytes(s), kv::fused_ws_bytes(s)));
   if (ws_bytes < need || !ws || (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1)))
     return KV_ERR_WORKSPACE;
-  int64_t items = 0;
-  for (int p = 0; p < pr->n_prob; ++p)
+  int64_t items = 0, stat_elems = 0;
+  for (int p = 0; p < pr->n_prob; ++p) {
     items += (int64_t)pr->h_kv * ((pr->len_host[p] + kv::kFusedChunk - 1) / kv::kFusedChunk);
+    stat_elems = std::max(stat_elems, (pr->tok_off_host[p] + pr->len_host[p]) * pr->h_kv);
+  }
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (items <= INT32_MAX) {
     bool used = false;
-    const hipError_t e = kv::launch_window_mu_sigma_fused(s, q_win, k, scale, (int)items, ws,
-                                                          row_max, row_sum, mu, sigma, &used, hs);
+    const hipError_t e = kv::launch_window_mu_sigma_fused(s, q_win, k, scale, (int)items,
+                                                          stat_elems, ws, row_max, row_sum, mu,
+                                                          sigma, &used, hs);
     if (e != hipSuccess) return KV_ERR_LAUNCH;
     if (used) return KV_OK;
   }

@@ -2,30 +2,40 @@
 // (section 3.1, Eq. (1), Eq. (3)) reading every cached key once, for bf16 caches with w = 32.
 //
 // The row normaliser of a window query needs every key of its (problem, kv head) "unit" before any
-// token's attention can be formed.  Instead of a second pass over K, each work item keeps its logits
-// in registers while the units' statistics are combined across workgroups:
+// token's attention can be formed.  Each workgroup therefore keeps the keys it has scored on chip
+// until its unit's normalisers are known, and forms the attention from them a second time:
 //
-//   work item = (unit, chunk of 512 keys); 16 waves x one MFMA tile of 32 keys; rows = G*32 window
-//   rows of the kv group (row block b = query head b of the group, row = window position r);
-//   1. logits D[key][row] = K Q^T with v_mfma_f32_32x32x16_bf16, keys as the M dimension so that a
-//      lane holds one window row and 16 keys (queries from LDS, keys straight from HBM into operand
-//      registers; the next item's queries are requested into the other LDS buffer right after the
-//      MFMAs, its keys right after this item's partials are published, so both stream in during
-//      the unit barrier and the final reduction);
-//   2. workgroup row maximum m and, after e = 2^(t - m) in place, row sum z: in-lane over 16 keys,
-//      one permlane32 swap for the other 16, then across waves in LDS; (m, z) is published to the
-//      unit's partial slot with a write-through store;
-//   3. unit barrier: the last workgroup of a unit to publish its partial merges all of them into
-//      b = M + log2 Z per row (and the row_max / row_sum outputs) and raises the unit's flag; the
-//      others poll the flag.  Exchanged data uses system-scope (write-through, cache-bypassing)
-//      accesses ordered by s_waitcnt, so no L2 write-back or invalidation is needed; the grid is
-//      launched cooperatively so every workgroup is resident, and a unit spans at most one grid;
-//   4. a = e * 2^(m - b) / G summed over the group's heads gives the window row means a[r] of the
-//      lane's 16 keys; a per-wave 32 x 32 LDS transpose gives each lane one key and 16 rows, so the
-//      mean over r and the two-pass sample variance are in-lane plus one permlane32 swap.
+//   item = 256 keys of one unit (8 waves x one 32-key MFMA tile).  Items are dealt round-robin to
+//   the persistent workgroups, so a unit's items run side by side on many workgroups.  Each
+//   workgroup pipelines its items through four register slots:
 //
-// Work items are dealt round-robin (item i -> workgroup i % grid), units in order, so a unit's
-// items are resident together and the barrier cannot deadlock.  Every wait is bounded.
+//     iteration i:  phase 1 of item i     logits D[key][row] = K Q^T (v_mfma_f32_32x32x16_bf16, keys
+//                                         as M so that a lane holds one window row), per-wave row
+//                                         maximum m and sum z of 2^(t - m), merged over the waves;
+//                                         the item's partial (m, z) per row is stored for its unit
+//                                         (write-through store, nothing waited for);
+//                   phase 2 of item i-2   the unit's normalisers b = M + log2 Z are known by now:
+//                                         logits again with keys as N (a lane holds one key),
+//                                         a = 2^(t - b) summed over the group's heads, then the mean
+//                                         and the two-pass sample variance over the window rows;
+//                   keys of item i+2 are requested into the slot item i-2 has just released.
+//
+//   Eight of a unit's items (chosen so that the role rotates over the workgroups) merge it, one
+//   slice of R/8 window rows each: they poll every item's partial of their rows (initialised to a
+//   NaN sentinel), combine them and store the normalisers and the row_max / row_sum outputs of
+//   those rows.  Every workgroup
+//   requests the normalisers of an item's unit one iteration after publishing the item's partial
+//   and waits for them one iteration later.
+//   Exchanged values use device-scope accesses, which bypass the per-XCD caches; every wait is
+//   bounded.
+//
+// Deadlock freedom: in every iteration a workgroup publishes its item's partial (and merges, if it
+// is a merger) before it waits for any normaliser, and it only waits for the units of earlier
+// items.  When each workgroup holds at most three items of any unit (checked at launch), every
+// partial of a unit is published before anyone waits for that unit.  The grid is launched
+// cooperatively so that every workgroup is resident.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -33,32 +43,57 @@ namespace kv {
 
 namespace {
 
-constexpr int kWaves = 16;
+constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
-constexpr int kTiles = 1;
-constexpr int kMaxSpins = 1 << 22;
-constexpr unsigned kFinPending = 0x7FC0DEADu;  // NaN pattern: final row value not published yet
+constexpr int kItemKeys = kWaves * 32;  // keys per item
+static_assert(kItemKeys == kFusedChunk, "an item is one chunk");
+constexpr int kSlots = 4;   // register slots of key tiles per wave
+constexpr int kLag = 2;     // phase 2 of an item runs kLag iterations after its phase 1
+constexpr int kQBufs = 4;   // query / normaliser buffers (items i-2 .. i+1)
+constexpr int kMergers = kWaves;  // row slices of a unit's merge (one wave's rows each)
+constexpr int kMaxLocalItems = 800;  // items per workgroup (their descriptors sit in LDS)
+constexpr int kMaxSpins = 1 << 16;     // polls of another workgroup's value (about 1 us each)
+constexpr int kMaxLdsSpins = 1 << 24;  // polls of the workgroup's own counter
+constexpr int kMaxProbs = 4096;        // problems the descriptor builder scans in LDS
+constexpr unsigned kPending = 0x7FC0DEADu;  // NaN pattern: value not published yet
 
-struct FusedArgs {
+// One item: (unit = p * h_kv + g, chunk index within the unit, L_p, stat_base) with
+// stat_base = tok_off[p] * h_kv + g * L_p, the element offset of the unit's mu / sigma row (the
+// unit's keys start at element stat_base * d).  stat_base < 2^31 is checked at launch.
+typedef int4 ItemDesc;
+
+struct PipeArgs {
   const uint16_t* q_win;
   const uint16_t* k;
-  const int32_t* lens;
-  const int64_t* tok_off;
-  int n_prob, h_q, h_kv;
-  float c;  // softmax scale * log2(e)
+  const ItemDesc* desc;  // [total_items]
+  int G;                 // query heads per kv head
+  float c;               // softmax scale * log2(e)
   float* row_max;
   float* row_sum;
   float* mu;
   float* sigma;
-  float2* part;       // [n_units][max_chunks][ROWS]
-  float* fin;         // [n_units][ROWS]
-  int* cnt;           // [n_units]
-  int* flag;          // [n_units]
-  int* item_prefix;   // [n_prob + 1]
-  int* status;        // [1]
-  int max_chunks;
+  float2* part;  // [n_units][max_items][ROWS]
+  float* fin;    // [n_units][ROWS]
+  int* status;
+  int max_items;
   int total_items;
 };
+
+struct Item {
+  int unit, c, L, n, sbase;  // n = items of the unit
+};
+
+__device__ __forceinline__ int sread(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+__device__ __forceinline__ Item unpack(const ItemDesc& d) {
+  Item it;
+  it.unit = sread(d.x);
+  it.c = sread(d.y);
+  it.L = sread(d.z);
+  it.sbase = sread(d.w);
+  it.n = (it.L + kItemKeys - 1) / kItemKeys;
+  return it;
+}
 
 __device__ __forceinline__ float sum_halves(float x) {  // x + x of lane ^ 32
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -70,353 +105,478 @@ __device__ __forceinline__ float max_halves(float x) {  // max(x, x of lane ^ 32
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
-// Coherent (write-through / cache-bypassing) accesses for data exchanged between workgroups.
-__device__ __forceinline__ void publish_f2(float2* p, float2 v) {
-  __hip_atomic_store(reinterpret_cast<unsigned long long*>(p), __builtin_bit_cast(unsigned long long, v),
-                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+// Device-scope accesses for values exchanged between workgroups.
+__device__ __forceinline__ void put_u64(void* p, unsigned long long v) {
+  __hip_atomic_store(reinterpret_cast<unsigned long long*>(p), v, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ float2 fetch_f2(const float2* p) {
-  return __builtin_bit_cast(float2, __hip_atomic_load(reinterpret_cast<const unsigned long long*>(p),
-                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM));
+__device__ __forceinline__ unsigned long long get_u64(const void* p) {
+  return __hip_atomic_load(reinterpret_cast<const unsigned long long*>(p), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void publish_f(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+__device__ __forceinline__ void put_u32(void* p, unsigned v) {
+  __hip_atomic_store(reinterpret_cast<unsigned*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ float fetch_f(const float* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+__device__ __forceinline__ unsigned get_u32(const void* p) {
+  return __hip_atomic_load(reinterpret_cast<const unsigned*>(p), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
 }
 
-struct Item {
-  int p, g, c, L, nch, unit;
+// Merge (m2, z2) into (m, z); base-2 units, z relative to 2^m, m = -inf for "no key".
+__device__ __forceinline__ void merge_into(float& m, float& z, float m2, float z2) {
+  const float mn = fmaxf(m, m2);
+  if (mn == -INFINITY) return;
+  const float a = (m == -INFINITY) ? 0.f : z * __builtin_amdgcn_exp2f(m - mn);
+  const float b = (m2 == -INFINITY) ? 0.f : z2 * __builtin_amdgcn_exp2f(m2 - mn);
+  m = mn;
+  z = a + b;
+}
+
+template <int D, int NB> struct Geo {
+  static constexpr int R = NB * 32;         // window rows of a unit (G heads x 32)
+  static constexpr int NS = D / 16;         // MFMA K steps
+  static constexpr int CH = D * 2 / 16;     // 16-byte chunks of a query row
+  static constexpr int QELEMS = R * D;      // bf16 elements of one query buffer
+  static constexpr int QCHUNKS = R * CH;
+  static constexpr int QPT = (QCHUNKS + kThreads - 1) / kThreads;  // staging loads per thread
+  static constexpr int RW = R / kWaves;  // rows whose partials a wave merges (lanes 0 .. RW-1)
+  static constexpr int LG = 64 / RW;     // lane groups of a wave in a unit merge
+  // 16-byte chunk `ch` of query row `row` sits at chunk ch ^ (row % CH) of the row in LDS, so that
+  // a fragment read of 16 consecutive rows touches 16 different chunks (all banks).
+  __device__ static int qslot(int row, int ch) { return row * CH + (ch ^ (row % CH)); }
 };
 
-__device__ __forceinline__ Item decode_item(const FusedArgs& a, int item) {
-  // problem: largest p with item_prefix[p] <= item
-  int lo = 0, hi = a.n_prob;  // item_prefix[0] = 0 <= item < item_prefix[n_prob]
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (a.item_prefix[mid] <= item) lo = mid;
-    else hi = mid;
-  }
-  // every field is the same for the whole workgroup: keep them in scalar registers
-  Item it;
-  it.p = __builtin_amdgcn_readfirstlane(lo);
-  it.L = __builtin_amdgcn_readfirstlane(a.lens[it.p]);
-  it.nch = (it.L + kFusedChunk - 1) / kFusedChunk;
-  const int local = __builtin_amdgcn_readfirstlane(item - a.item_prefix[it.p]);
-  it.g = local / it.nch;
-  it.c = local % it.nch;
-  it.unit = it.p * a.h_kv + it.g;
-  return it;
-}
-
-// Query rows of one unit in LDS: row pitch CHUNKS + 1 sixteen-byte slots (the pad slot shifts
-// consecutive rows by four banks, so a fragment read of 16 rows is conflict-free and every K-step
-// offset is an immediate).  Filled by direct-to-LDS loads, one contiguous kilobyte per wave
-// instruction; a lane whose slot is a pad loads its row's first chunk again.
-template <int D> struct QPitch {
-  static constexpr int CHUNKS = D * 2 / 16;
-  static constexpr int SLOTS = CHUNKS + 1;
-};
-
-// Issued by waves first_wave .. kWaves-1 only.
 template <int D, int NB>
-__device__ __forceinline__ void request_queries(const FusedArgs& a, const Item& it, uint16_t* qbuf,
-                                                int first_wave) {
-  constexpr int CHUNKS = QPitch<D>::CHUNKS, SLOTS = QPitch<D>::SLOTS;
-  constexpr int ROWS = NB * 32;
-  constexpr int PER_WAVE_INSTR = 64;  // 16-byte slots per wave instruction
-  constexpr int N_INSTR = (ROWS * SLOTS + PER_WAVE_INSTR - 1) / PER_WAVE_INSTR;
-  const int G = a.h_q / a.h_kv;
-  const uint16_t* qg = a.q_win + ((size_t)it.p * a.h_q + (size_t)it.g * G) * 32 * D;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int gi = wave - first_wave; gi >= 0 && gi < N_INSTR; gi += kWaves - first_wave) {
-    const int slot_lin = gi * PER_WAVE_INSTR + lane;  // LDS 16-byte slot written by this lane
-    int m = slot_lin / SLOTS, q = slot_lin % SLOTS;
-    if (q == CHUNKS) q = 0;               // pad slot
-    if (m >= ROWS) m = ROWS - 1, q = 0;   // beyond the last row (inside the buffer's tail)
-    __builtin_amdgcn_global_load_lds(qg + (size_t)m * D + q * 8, qbuf + gi * PER_WAVE_INSTR * 8,
-                                     16, 0, 0);
+__global__ __launch_bounds__(kThreads, 1) void window_mu_sigma_fused_kernel(PipeArgs a) {
+  using Gm = Geo<D, NB>;
+  constexpr int R = Gm::R, NS = Gm::NS, CH = Gm::CH, QPT = Gm::QPT;
+  constexpr int RW = Gm::RW, LG = Gm::LG;
+  __shared__ __align__(16) uint16_t qbuf[kQBufs][Gm::QELEMS];
+  __shared__ __align__(16) float2 red[2][kWaves][R];  // per-wave (m, z) of the last two items
+  __shared__ __align__(16) float2 mrg[kWaves][RW];    // unit merge: per-wave partial results
+  __shared__ __align__(16) float bsh[kQBufs][R];      // normalisers of the items in phase 2
+  __shared__ __align__(16) ItemDesc dsh[kMaxLocalItems];  // this workgroup's items, in order
+  __shared__ int qcnt, rcnt, dcnt, bcnt;  // wave-to-wave ordering, see below
+  __shared__ int s_fail;  // a wait timed out: every later wait is skipped, outputs become NaN
+
+  const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
+  const int wave = sread(threadIdx.x >> 6);
+  const int grid = gridDim.x, wg = blockIdx.x;
+  const int n_local = wg < a.total_items ? (a.total_items - wg + grid - 1) / grid : 0;
+  const float inv_g = 1.f / (float)a.G;
+  const float c = a.c;
+  const int mrow = wave * RW + (lane % RW);  // row this lane publishes / polls (lanes < RW)
+  if (n_local == 0) return;
+  if (threadIdx.x == 0) bcnt = 0, s_fail = 0;
+  auto failed = [&]() {
+    return __hip_atomic_load(&s_fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) != 0;
+  };
+  auto fail = [&](int bit) {
+    __hip_atomic_store(&s_fail, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    atomicOr(a.status, bit);
+  };
+  auto exists = [&](int n) { return n >= 0 && n < n_local; };
+  auto item_of = [&](int n) { return unpack(dsh[n]); };
+
+  bf16x8_t slot[kSlots][NS];
+  bf16x8_t qst[QPT];
+  float bq = 0.f;  // this lane's polled normaliser (kept in one register throughout)
+
+  // ---- loads ---------------------------------------------------------------------------------
+  // keys of this wave's tile of an item: a wave-uniform base and this lane's offset (its key
+  // clamped into the unit; the lane half selects the 8 elements of each K step)
+  auto load_keys = [&](bf16x8_t (&t)[NS], const uint16_t* base, int off) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) t[s] = *reinterpret_cast<const bf16x8_t*>(base + off + 16 * s);
+  };
+  auto load_item_keys = [&](bf16x8_t (&t)[NS], int n) {
+    if (exists(n)) {
+      const Item it = item_of(n);
+      const int t0 = it.c * kItemKeys + wave * 32;
+      load_keys(t, a.k + (size_t)(it.sbase + t0) * D, min(l32, it.L - 1 - t0) * D + 8 * half);
+    } else {
+      load_keys(t, a.k, 8 * half);  // keeps the number of loads per iteration fixed
+    }
+  };
+  // the unit's query rows are contiguous (heads g G .. g G + G - 1 of problem p)
+  auto load_queries = [&](int n) {
+    const uint16_t* qg = a.q_win + (size_t)(exists(n) ? item_of(n).unit : 0) * R * D;
+#pragma unroll
+    for (int j = 0; j < QPT; ++j) {
+      const int ch = min((int)threadIdx.x + j * kThreads, Gm::QCHUNKS - 1);
+      qst[j] = *reinterpret_cast<const bf16x8_t*>(qg + 8 * ch);
+    }
+  };
+  auto store_queries = [&](uint16_t* qb) {
+#pragma unroll
+    for (int j = 0; j < QPT; ++j) {
+      const int ch = threadIdx.x + j * kThreads;
+      if (ch < Gm::QCHUNKS)
+        *reinterpret_cast<bf16x8_t*>(qb + Gm::qslot(ch / CH, ch % CH) * 8) = qst[j];
+    }
+  };
+  // query fragments of head b (window rows b*32 + l32), all K steps
+  auto read_q = [&](bf16x8_t (&qf)[NS], const uint16_t* qb, int b) {
+    const int row = b * 32 + l32;
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+      qf[s] = *reinterpret_cast<const bf16x8_t*>(qb + Gm::qslot(row, 2 * s + half) * 8);
+  };
+
+  // ---- phase 1: logits (keys as M), per-wave row maximum and sum -> red[wave] ----------------
+  auto phase1 = [&](const bf16x8_t (&t)[NS], const uint16_t* qb, const Item& it, int buf) {
+    const int t0 = it.c * kItemKeys + wave * 32;
+    const bool edge = t0 + 31 > it.L - 32;
+    // window row l32 sees keys <= min(L - 1, L - 32 + l32); the key of register j is
+    // t0 + acc_row(j, lane) = t0 + 4 half + 8 (j / 4) + (j % 4)
+    const int thr = min(it.L - 1, it.L - 32 + l32) - t0 - 4 * half;
+    bf16x8_t qf[NS];
+    read_q(qf, qb, 0);
+#pragma unroll 1
+    for (int b = 0; b < NB; ++b) {
+      f32x16_t d = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < NS; ++s) d = mfma_step(t[s], qf[s], d);
+      if (b + 1 < NB) read_q(qf, qb, b + 1);  // the next head's fragments arrive meanwhile
+      if (edge) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          if (8 * (j >> 2) + (j & 3) > thr) d[j] = -INFINITY;
+      }
+      float mx[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) mx[u] = fmaxf(fmaxf(d[4 * u], d[4 * u + 1]), fmaxf(d[4 * u + 2], d[4 * u + 3]));
+      const float m = max_halves(fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3])));
+      const float ms = (m == -INFINITY) ? 0.f : m * c;
+      float zs[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        zs[u] = __builtin_amdgcn_exp2f(fmaf(d[4 * u], c, -ms));
+#pragma unroll
+        for (int v = 1; v < 4; ++v) zs[u] += __builtin_amdgcn_exp2f(fmaf(d[4 * u + v], c, -ms));
+      }
+      const float z = sum_halves((zs[0] + zs[1]) + (zs[2] + zs[3]));
+      if (half == 0) red[buf][wave][b * 32 + l32] = make_float2(m == -INFINITY ? -INFINITY : ms, z);
+    }
+  };
+
+  // ---- phase 2: attention from the unit's normalisers (keys as N), mean and dispersion --------
+  auto phase2 = [&](const bf16x8_t (&t)[NS], const uint16_t* qb, const float* bs, const Item& it) {
+    const int t0 = it.c * kItemKeys + wave * 32;
+    const int key = t0 + l32;
+    const bool edge = t0 + 31 > it.L - 32;
+    // window row r = acc_row(j, lane) = 4 half + 8 (j / 4) + (j % 4) sees the key iff
+    // key <= L - 32 + r
+    const int thr = key - (it.L - 32) - 4 * half;
+    float ab[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) ab[j] = 0.f;
+#pragma unroll 1
+    for (int b = 0; b < NB; ++b) {
+      f32x16_t d = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      bf16x8_t qf[NS];
+      read_q(qf, qb, b);
+#pragma unroll
+      for (int s = 0; s < NS; ++s) d = mfma_step(qf[s], t[s], d);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        // window rows 8 q + 4 half + 0..3 of query head b
+        const float4 bv = *reinterpret_cast<const float4*>(bs + b * 32 + 8 * q + 4 * half);
+        const float bb[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int j = 4 * q + u;
+          float e = __builtin_amdgcn_exp2f(fmaf(d[j], c, -bb[u]));
+          if (edge && 8 * q + u < thr) e = 0.f;
+          ab[j] += e;
+        }
+      }
+    }
+    // ab[j] = G a[r][key] for the window rows r = acc_row(j, lane); the other 16 are in lane ^ 32
+    float sp[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) sp[u] = (ab[u] + ab[u + 4]) + (ab[u + 8] + ab[u + 12]);
+    const float mean = sum_halves((sp[0] + sp[1]) + (sp[2] + sp[3])) * (inv_g * (1.f / 32.f));
+    float vp[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const float dl = fmaf(ab[j], inv_g, -mean);
+      vp[j & 3] = fmaf(dl, dl, vp[j & 3]);
+    }
+    const float var = sum_halves((vp[0] + vp[1]) + (vp[2] + vp[3])) * (1.f / 31.f);
+    if (key < it.L) {
+      const float bad = failed() ? __builtin_nanf("") : 0.f;  // a timed-out wait poisons the output
+      float* dst = half == 0 ? a.mu : a.sigma;
+      const float val = half == 0 ? mean : __builtin_amdgcn_sqrtf(var);
+      (dst + (it.sbase + t0))[l32] = val + bad;
+    }
+  };
+
+  // ---- unit merge of one row slice: the workgroup's waves split the unit's items --------------
+  //      lane = lane group lg x slice row; wave w, lane group lg take the items w + 8 (lg + LG k)
+  auto merge_slice = [&](const Item& it, int slice) {
+    const int lr = lane % RW, lg = lane / RW;
+    const int row = slice * RW + lr;
+    const float2* col = a.part + (size_t)it.unit * a.max_items * R + row;
+    float m = -INFINITY, z = 0.f;
+    constexpr int kBatch = 4;
+#pragma unroll 1
+    for (int c0 = wave + kWaves * lg; c0 < it.n; c0 += kBatch * kWaves * LG) {
+      unsigned long long v[kBatch];
+#pragma unroll
+      for (int q = 0; q < kBatch; ++q)
+        v[q] = get_u64(col + (size_t)min(c0 + q * kWaves * LG, it.n - 1) * R);
+#pragma unroll
+      for (int q = 0; q < kBatch; ++q) {
+        const int cq = c0 + q * kWaves * LG;
+        if (cq >= it.n) continue;
+        int spins = 0;
+        while ((unsigned)(v[q] & 0xFFFFFFFFu) == kPending && !failed()) {
+          if (++spins > kMaxSpins) {
+            fail(1);
+            break;
+          }
+          __builtin_amdgcn_s_sleep(2);
+          v[q] = get_u64(col + (size_t)cq * R);
+        }
+        const float2 f = __builtin_bit_cast(float2, v[q]);
+        merge_into(m, z, f.x, f.y);
+      }
+    }
+#pragma unroll
+    for (int off = RW; off < 64; off <<= 1) merge_into(m, z, __shfl_xor(m, off), __shfl_xor(z, off));
+    if (lane < RW) mrg[wave][lr] = make_float2(m, z);
+    __syncthreads();
+    if (wave == 0 && lane < RW) {
+      float mm = -INFINITY, zz = 0.f;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) merge_into(mm, zz, mrg[w][lr].x, mrg[w][lr].y);
+      put_u32(a.fin + (size_t)it.unit * R + row, __float_as_uint(mm + __builtin_log2f(zz)));
+      const size_t ri = (size_t)it.unit * R + row;  // = (p h_q + g G + head) * 32 + r
+      a.row_max[ri] = mm * kLn2;
+      a.row_sum[ri] = zz;
+    }
+    __syncthreads();
+  };
+
+  // ---- wave-to-wave ordering through LDS counters (each wave adds 1 per event) ----------------
+  //   qcnt: query buffers written (Q of item n is complete when qcnt >= 8 (n + 1))
+  //   rcnt: phase-1 row statistics written (item n's in red when rcnt >= 8 (n + 1))
+  //   dcnt: iterations finished (iteration n done by every wave when dcnt >= 8 (n + 1))
+  //   bcnt: normalisers delivered (item n's in bsh when bcnt >= 8 (n + 1))
+  auto bump = [&](int* ctr) {
+    if (lane == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+  };
+  auto await = [&](int* ctr, int need) {
+    int spins = 0;
+    while (__hip_atomic_load(ctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < need && !failed()) {
+      if (++spins > kMaxLdsSpins) {
+        fail(4);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  };
+
+  // ---- the item's partial over the waves (this wave's rows), max first then the rescaled sum --
+  auto item_partial = [&](int buf, float& m, float& z) {
+    float2 v[kWaves];
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) v[w] = red[buf][w][mrow];
+    m = v[0].x;
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) m = fmaxf(m, v[w].x);
+    z = 0.f;
+    if (m != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) z = fmaf(v[w].y, __builtin_amdgcn_exp2f(v[w].x - m), z);
+    }
+  };
+
+  // ---- prologue: item descriptors, queries of item 0 into LDS, keys of items 0 and 1 ----------
+  for (int j = threadIdx.x; j < n_local; j += kThreads) dsh[j] = a.desc[(size_t)wg + (size_t)j * grid];
+  if (threadIdx.x == 0) qcnt = 0, rcnt = 0, dcnt = 0;
+  __syncthreads();
+  load_queries(0);
+  store_queries(qbuf[0]);
+  bump(&qcnt);
+  load_queries(1);
+  load_item_keys(slot[0], 0);
+  load_item_keys(slot[1], 1);
+
+  auto step = [&](auto sc, int i) {
+    constexpr int S1 = decltype(sc)::value;            // slot of item i (phase 1)
+    constexpr int S2 = (S1 + kSlots - kLag) % kSlots;  // slot of item i - 2, then of item i + 2
+    const int n2 = i - kLag;                           // item of phase 2
+    const bool has1 = exists(i), has2 = exists(n2);
+    Item it1, it2;
+    if (has1) it1 = item_of(i);
+    if (has2) it2 = item_of(n2);
+
+    // (a) phase 1 of item i, once its queries are in LDS and red[i & 1] is free again
+    if (has1) {
+      await(&qcnt, kWaves * (i + 1));
+      await(&dcnt, kWaves * (i - 1));
+      phase1(slot[S1], qbuf[i % kQBufs], it1, i & 1);
+    }
+    bump(&rcnt);
+
+    // (b) item i's partial of this wave's rows, published for its unit; the last kMergers items
+    //     of a unit then merge one row slice each (slice s by item max(0, n - kMergers + s))
+    if (has1) {
+      await(&rcnt, kWaves * (i + 1));
+      if (lane < RW) {
+        float m, z;
+        item_partial(i & 1, m, z);
+        float2* dst = a.part + ((size_t)it1.unit * a.max_items + it1.c) * R + mrow;
+        put_u64(dst, __builtin_bit_cast(unsigned long long, make_float2(m, z)));
+      }
+      // The last kMergers items of a unit merge; with fewer items than slices item 0 takes the
+      // surplus slices.  A workgroup's items of one unit lie grid items apart and the grid holds at
+      // least min(n, kMergers) workgroups, so no workgroup merges for a unit before holding all its
+      // own items of that unit.
+      const int first = it1.n - kMergers;
+      if (it1.c >= first) {
+        const int s_lo = it1.c == 0 ? 0 : it1.c - first;
+        const int s_hi = it1.c - first;
+#pragma unroll 1
+        for (int sl = s_lo; sl <= s_hi; ++sl) merge_slice(it1, sl);
+      }
+    }
+
+    // (c) this wave's rows of item i - 2's normalisers (requested in the previous iteration) into
+    //     LDS; phase 2 of item i - 2 once every wave has delivered its rows
+    if (has2) {
+      if (lane < RW) {
+        int spins = 0;
+        while (__float_as_uint(bq) == kPending && !failed()) {
+          if (++spins > kMaxSpins) {
+            fail(2);
+            break;
+          }
+          __builtin_amdgcn_s_sleep(2);
+          bq = __uint_as_float(get_u32(a.fin + (size_t)it2.unit * R + mrow));
+        }
+        bsh[n2 % kQBufs][mrow] = bq;
+      }
+      bump(&bcnt);
+      await(&bcnt, kWaves * (n2 + 1));
+      phase2(slot[S2], qbuf[n2 % kQBufs], bsh[n2 % kQBufs], it2);
+    }
+
+    // (d) queries of item i + 1 into LDS (their buffer was last used by item i - 3, whose phase 2
+    //     every wave has finished once iteration i - 1 is done)
+    if (exists(i + 1)) {
+      await(&dcnt, kWaves * i);
+      store_queries(qbuf[(i + 1) % kQBufs]);
+    }
+    bump(&qcnt);
+
+    // (e) this wave's rows of item i - 1's normalisers, the queries of item i + 2, then the keys
+    //     of item i + 2 into the released slot.  Vector loads of a wave complete in order: what
+    //     is waited for sooner is requested first.  The key loads are issued unconditionally so
+    //     that every iteration issues the same number of them and the waits before phase 1 only
+    //     cover the keys of the item they need.
+    if (exists(i - 1) && lane < RW)
+      bq = __uint_as_float(get_u32(a.fin + (size_t)item_of(i - 1).unit * R + mrow));
+    load_queries(i + 2);
+    load_item_keys(slot[S2], i + 2);
+    bump(&dcnt);
+  };
+
+  for (int i0 = 0; i0 < n_local + kLag; i0 += kSlots) {
+    step(std::integral_constant<int, 0>{}, i0 + 0);
+    step(std::integral_constant<int, 1>{}, i0 + 1);
+    step(std::integral_constant<int, 2>{}, i0 + 2);
+    step(std::integral_constant<int, 3>{}, i0 + 3);
   }
+}
+
+// Item descriptors, sentinel-initialised partials and normalisers, cleared status.  Every block
+// scans the per-problem item counts itself (n_prob <= kMaxProbs).
+__global__ __launch_bounds__(256) void fused_init_kernel(const int32_t* __restrict__ lens,
+                                                         const int64_t* __restrict__ tok_off,
+                                                         int n_prob, int h_kv, int total_items,
+                                                         int max_items, int rows, ItemDesc* desc,
+                                                         unsigned* part, unsigned* fin, int* status) {
+  __shared__ int pre[kMaxProbs + 1];
+  __shared__ int wsum[4];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  // exclusive prefix of h_kv * ceil(L_p / kItemKeys) over the problems
+  int carry = 0;
+  for (int base = 0; base < n_prob; base += 256) {
+    const int p = base + threadIdx.x;
+    const int v = p < n_prob ? h_kv * ((lens[p] + kItemKeys - 1) / kItemKeys) : 0;
+    int x = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(x, off, 64);
+      if (lane >= off) x += y;
+    }
+    if (lane == 63) wsum[w] = x;
+    __syncthreads();
+    int before = carry;
+    for (int q = 0; q < w; ++q) before += wsum[q];
+    if (p < n_prob) pre[p] = before + x - v;
+    const int total = carry + wsum[0] + wsum[1] + wsum[2] + wsum[3];
+    __syncthreads();
+    carry = total;
+  }
+  if (threadIdx.x == 0) pre[n_prob] = carry;
+  __syncthreads();
+  const int tid = blockIdx.x * blockDim.x + threadIdx.x, nthr = gridDim.x * blockDim.x;
+  for (int q = tid; q < total_items; q += nthr) {
+    int lo = 0, hi = n_prob;  // largest p with pre[p] <= q
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (pre[mid] <= q) lo = mid;
+      else hi = mid;
+    }
+    const int L = lens[lo];
+    const int nip = (L + kItemKeys - 1) / kItemKeys;
+    const int local = q - pre[lo];
+    const int g = local / nip, ci = local % nip;
+    const long long sbase = (long long)tok_off[lo] * h_kv + (long long)g * L;
+    desc[q] = make_int4(lo * h_kv + g, ci, L, (int)sbase);
+  }
+  const int n_units = n_prob * h_kv;
+  const size_t n_part = (size_t)n_units * max_items * rows;  // float2 entries; mark the m word
+  for (size_t e = tid; e < n_part; e += nthr) part[2 * e] = kPending;
+  for (int e = tid; e < n_units * rows; e += nthr) fin[e] = kPending;
+  if (tid == 0) status[0] = 0;
 }
 
 }  // namespace
-
-template <int D, int NB>
-__global__ __launch_bounds__(kThreads, 1) void window_mu_sigma_fused_kernel(FusedArgs a) {
-  constexpr int ROWS = NB * 32;
-  constexpr int SLOTS = QPitch<D>::SLOTS;
-  constexpr int QBUF = ((ROWS * SLOTS + 63) / 64) * 64 * 8;  // elements, whole wave instructions
-  constexpr int NS = D / 16;                                 // MFMA K steps
-  constexpr int PARTS = kThreads / ROWS;                     // slices of a unit's chunks
-  constexpr int TP = 33;                                     // transpose tile pitch (floats)
-  __shared__ __align__(16) uint16_t qbuf[2][QBUF];
-  __shared__ __align__(16) float red[kWaves][ROWS];
-  __shared__ __align__(16) float srow[ROWS];  // workgroup row max, then 2^(m - b) / G
-  // per-wave 32x32 transpose tiles of the finalisation; the last workgroup's merge reuses them
-  __shared__ __align__(16) float xt[kWaves * 32 * TP];
-  static_assert(kWaves * 32 * TP >= 2 * PARTS * ROWS, "merge scratch must fit in the tiles");
-  __shared__ int s_last;
-
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
-  const int G = a.h_q / a.h_kv;
-  const float inv_g = 1.f / (float)G;
-
-  int item = blockIdx.x;
-  if (item >= a.total_items) return;
-  Item it = decode_item(a, item);
-  Frags<kDtBf16, D> kf;
-  auto key_row = [&](const Item& x) {
-    const int64_t off = (int64_t)__builtin_amdgcn_readfirstlane((int)(a.tok_off[x.p] & 0xFFFFFFFF)) |
-                        ((int64_t)__builtin_amdgcn_readfirstlane((int)(a.tok_off[x.p] >> 32)) << 32);
-    const uint16_t* kg = a.k + ((size_t)off * a.h_kv + (size_t)x.g * x.L) * D;
-    const int key = min(x.c * kFusedChunk + wave * 32 + l32, x.L - 1);
-    return kg + (size_t)key * D;
-  };
-  request_queries<D, NB>(a, it, qbuf[0], 0);
-  kf.load_global(key_row(it), half);
-
-  for (int iter = 0; item < a.total_items; ++iter, item += gridDim.x) {
-    const int nxt = item + gridDim.x;
-    const bool has_next = nxt < a.total_items;
-    const Item nx = has_next ? decode_item(a, nxt) : it;
-    const uint16_t* qb = qbuf[iter & 1];
-    __builtin_amdgcn_s_waitcnt(0);  // this item's queries (direct-to-LDS) and keys have landed
-    __syncthreads();
-
-    // ---- 1. logits D[key][row]: lane = window row b*32 + (lane % 32), 16 keys per lane ----------
-    f32x16_t acc[NB];
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      f32x16_t d = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      const uint16_t* qrow = qb + ((b * 32 + l32) * SLOTS + half) * 8;
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const bf16x8_t qa = *reinterpret_cast<const bf16x8_t*>(qrow + 16 * s);
-        d = mfma_step(kf.v[s], qa, d);
-      }
-      acc[b] = d;
-    }
-
-    // ---- causal / ragged mask: row r = lane % 32 sees keys <= L - 32 + r -----------------------
-    const int t0 = it.c * kFusedChunk + wave * 32;
-    if (t0 + 31 > it.L - 32) {
-      const int lim = min(it.L - 1, it.L - 32 + l32);
-#pragma unroll
-      for (int b = 0; b < NB; ++b)
-#pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if (t0 + acc_row(j, lane) > lim) acc[b][j] = -INFINITY;
-    }
-
-    // ---- 2a. workgroup row maximum (in-lane over 16 keys, the other 16 in lane ^ 32) ----------
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      float m = acc[b][0];
-#pragma unroll
-      for (int j = 1; j < 16; ++j) m = fmaxf(m, acc[b][j]);
-      m = max_halves(m);
-      if (half == 0) red[wave][b * 32 + l32] = m;
-    }
-    __syncthreads();
-    if (threadIdx.x < ROWS) {
-      float m = red[0][threadIdx.x];
-#pragma unroll
-      for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red[w][threadIdx.x]);
-      srow[threadIdx.x] = m * a.c;  // in base-2 logit units (c > 0)
-    }
-    __syncthreads();
-
-    // ---- 2b. e = 2^(t - m) in place and workgroup row sum ------------------------------------
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const float mm = srow[b * 32 + l32];
-      float z = 0.f;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const float e = __builtin_amdgcn_exp2f(fmaf(acc[b][j], a.c, -mm));
-        acc[b][j] = e;
-        z += e;
-      }
-      z = sum_halves(z);
-      if (half == 0) red[wave][b * 32 + l32] = z;
-    }
-    __syncthreads();
-    const size_t ubase = (size_t)it.unit * a.max_chunks * ROWS;
-    if (threadIdx.x < ROWS) {
-      float z = 0.f;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) z += red[w][threadIdx.x];
-      publish_f2(a.part + ubase + (size_t)it.c * ROWS + threadIdx.x, make_float2(srow[threadIdx.x], z));
-      __builtin_amdgcn_s_waitcnt(0);  // the partial has reached memory before the counter moves
-    }
-    __syncthreads();
-
-    // ---- 3. unit barrier ------------------------------------------------------------------------
-    if (threadIdx.x == 0) {
-      const int old = __hip_atomic_fetch_add(&a.cnt[it.unit], 1, __ATOMIC_RELAXED,
-                                             __HIP_MEMORY_SCOPE_AGENT);
-      s_last = (old == it.nch - 1);
-    }
-    __syncthreads();
-    // The next item's queries and keys stream in while this unit's statistics are combined and
-    // finalised.  They are issued after the publish (so that its wait covers only the partial
-    // store), and the waves that poll for the unit's final values issue theirs only after the
-    // poll: vector loads of a wave complete in order, so a poll behind a prefetch would wait for it.
-    constexpr int kPollWaves = (ROWS + 63) / 64;
-    if (has_next && wave >= kPollWaves) {
-      request_queries<D, NB>(a, nx, qbuf[(iter + 1) & 1], kPollWaves);
-      kf.load_global(key_row(nx), half);
-    }
-    if (s_last) {
-      // merge every partial of the unit: PARTS slices per row, loads issued in batches of 8
-      float2* comb = reinterpret_cast<float2*>(xt);
-      const int row = threadIdx.x % ROWS, part = threadIdx.x / ROWS;
-      float M = -INFINITY, Z = 0.f;
-      for (int ch0 = part; ch0 < it.nch; ch0 += 8 * PARTS) {
-        float2 o[8];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const int ch = ch0 + q * PARTS;
-          o[q] = ch < it.nch ? fetch_f2(a.part + ubase + (size_t)ch * ROWS + row)
-                             : make_float2(-INFINITY, 0.f);
-        }
-#pragma unroll
-        for (int q = 0; q < 8; ++q) merge_mz(M, Z, o[q].x, o[q].y);
-      }
-      comb[part * ROWS + row] = make_float2(M, Z);
-      __syncthreads();
-      if (threadIdx.x < ROWS) {
-        float2 r = comb[threadIdx.x];
-#pragma unroll
-        for (int q = 1; q < PARTS; ++q) merge_mz(r.x, r.y, comb[q * ROWS + threadIdx.x].x, comb[q * ROWS + threadIdx.x].y);
-        const float bfin = r.x + log2f(r.y);
-        publish_f(a.fin + (size_t)it.unit * ROWS + threadIdx.x, bfin);
-        const int hl = threadIdx.x / 32, rr = threadIdx.x % 32;
-        const size_t ri = ((size_t)it.p * a.h_q + (size_t)it.g * G + hl) * 32 + rr;
-        a.row_max[ri] = r.x * kLn2;
-        a.row_sum[ri] = r.y;
-        srow[threadIdx.x] = __builtin_amdgcn_exp2f(srow[threadIdx.x] - bfin) * inv_g;
-      }
-    } else if (threadIdx.x < ROWS) {
-      // each row polls its own final value; the init kernel set it to a NaN sentinel
-      const float* fp = a.fin + (size_t)it.unit * ROWS + threadIdx.x;
-      float bfin = fetch_f(fp);
-      int spins = 0;
-      while (__float_as_uint(bfin) == kFinPending) {
-        if (++spins > kMaxSpins) {
-          atomicOr(a.status, 1);
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-        bfin = fetch_f(fp);
-      }
-      srow[threadIdx.x] = __builtin_amdgcn_exp2f(srow[threadIdx.x] - bfin) * inv_g;
-    }
-    if (has_next && wave < kPollWaves) kf.load_global(key_row(nx), half);
-    __syncthreads();
-
-    // ---- 4. group mean over heads, then mean and dispersion over the window --------------------
-    float abar[16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j) abar[j] = 0.f;
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const float al = srow[b * 32 + l32];
-#pragma unroll
-      for (int j = 0; j < 16; ++j) abar[j] = fmaf(acc[b][j], al, abar[j]);
-    }
-    // transpose through LDS: tile[key][r], this lane holds r = lane % 32 of keys acc_row(j, lane)
-    float* tile = xt + wave * 32 * TP;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) tile[acc_row(j, lane) * TP + l32] = abar[j];
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    float v[16];
-    float s = 0.f;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      v[i] = tile[l32 * TP + 16 * half + i];  // key l32, rows 16 half .. 16 half + 15
-      s += v[i];
-    }
-    const float mean = sum_halves(s) * (1.f / 32.f);
-    float var = 0.f;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const float dl = v[i] - mean;
-      var = fmaf(dl, dl, var);
-    }
-    var = sum_halves(var) * (1.f / 31.f);
-    const int64_t toff = (int64_t)__builtin_amdgcn_readfirstlane((int)(a.tok_off[it.p] & 0xFFFFFFFF)) |
-                         ((int64_t)__builtin_amdgcn_readfirstlane((int)(a.tok_off[it.p] >> 32)) << 32);
-    const size_t stat_base = (size_t)toff * a.h_kv + (size_t)it.g * it.L;
-    const int key = t0 + l32;
-    if (key < it.L) {
-      if (half == 0) a.mu[stat_base + key] = mean;
-      else a.sigma[stat_base + key] = sqrtf(var);
-    }
-    it = nx;
-  }
-}
-
-// Zero the unit counters and flags and lay out the work items (exclusive prefix over problems).
-__global__ __launch_bounds__(1024) void fused_init_kernel(const int32_t* __restrict__ lens, int n_prob,
-                                                          int h_kv, int n_units, int rows, int* cnt,
-                                                          unsigned* fin, int* item_prefix, int* status) {
-  __shared__ int part[1024];
-  for (int u = threadIdx.x; u < n_units; u += blockDim.x) cnt[u] = 0;
-  for (int i = threadIdx.x; i < n_units * rows; i += blockDim.x) fin[i] = kFinPending;
-  if (threadIdx.x == 0) status[0] = 0;
-  const int per = (n_prob + 1023) / 1024;
-  const int lo = threadIdx.x * per, hi = min(n_prob, lo + per);
-  int s = 0;
-  for (int p = lo; p < hi; ++p) s += h_kv * ((lens[p] + kFusedChunk - 1) / kFusedChunk);
-  part[threadIdx.x] = s;
-  __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    const int add = threadIdx.x >= off ? part[threadIdx.x - off] : 0;
-    __syncthreads();
-    part[threadIdx.x] += add;
-    __syncthreads();
-  }
-  int run = part[threadIdx.x] - s;  // exclusive prefix of this thread's range
-  for (int p = lo; p < hi; ++p) {
-    item_prefix[p] = run;
-    run += h_kv * ((lens[p] + kFusedChunk - 1) / kFusedChunk);
-  }
-  if (threadIdx.x == 1023) item_prefix[n_prob] = part[1023];
-}
 
 // ------------------------------------------------------------------------------------------------
 size_t fused_ws_bytes(const Shape& s) {
   const size_t n_units = (size_t)s.n_prob * s.h_kv;
   const size_t rows = (size_t)s.group() * 32;
-  const size_t max_chunks = (s.max_len + kFusedChunk - 1) / kFusedChunk;
-  size_t b = n_units * max_chunks * rows * sizeof(float2);
+  const size_t max_items = (s.max_len + kItemKeys - 1) / kItemKeys;
+  size_t b = n_units * max_items * sizeof(ItemDesc);  // bounds the number of items
+  b += n_units * max_items * rows * sizeof(float2);
   b += n_units * rows * sizeof(float);
-  b += 2 * n_units * sizeof(int);
-  b += (s.n_prob + 1) * sizeof(int) + sizeof(int);
+  b += 256;
   return b;
 }
 
 bool fused_shape_ok(const Shape& s, float scale) {
   const int G = s.group();
   return s.dtype == kDtBf16 && s.w == 32 && (s.d == 64 || s.d == 128) && (G == 1 || G == 2 || G == 4) &&
-         scale > 0.f;
+         scale > 0.f && s.n_prob <= kMaxProbs;
 }
 
 namespace {
 int g_resident[64] = {0};  // co-resident workgroups of the fused kernel per device and shape
 
 template <int D, int NB>
-hipError_t fused_dispatch(const FusedArgs& base, int total_items, bool* used, hipStream_t st) {
+hipError_t fused_dispatch(const PipeArgs& base, int total_items, bool* used, hipStream_t st) {
   auto kern = window_mu_sigma_fused_kernel<D, NB>;
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  const int slot = ((dev & 15) << 2) | ((D == 128) << 1) | (NB == 4);
-  int& res = g_resident[slot & 63];
+  const int key = ((dev & 7) << 3) | ((D == 128) << 2) | (NB == 4 ? 2 : (NB == 2 ? 1 : 0));
+  int& res = g_resident[key & 63];
   if (res == 0) {
     int per_cu = 0, cus = 0;
     e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kern),
@@ -427,11 +587,13 @@ hipError_t fused_dispatch(const FusedArgs& base, int total_items, bool* used, hi
     res = per_cu * cus;
   }
   const int grid = min(total_items, res);
-  if (grid <= 0 || base.max_chunks > grid) {  // every unit must fit in one grid of items
+  // a workgroup may hold at most three items of one unit (the deadlock argument above), and its
+  // item descriptors must fit in LDS
+  if (grid <= 0 || base.max_items > 3 * grid || (total_items + grid - 1) / grid > kMaxLocalItems) {
     *used = false;
     return hipSuccess;
   }
-  FusedArgs args = base;
+  PipeArgs args = base;
   args.total_items = total_items;
   void* params[] = {&args};
   e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kern), dim3(grid), dim3(kThreads),
@@ -442,44 +604,38 @@ hipError_t fused_dispatch(const FusedArgs& base, int total_items, bool* used, hi
 }  // namespace
 
 hipError_t launch_window_mu_sigma_fused(const Shape& s, const void* q_win, const void* k,
-                                        float scale, int total_items, void* ws, float* row_max,
-                                        float* row_sum, float* mu, float* sigma, bool* used,
-                                        hipStream_t stream) {
+                                        float scale, int total_items, int64_t stat_elems, void* ws,
+                                        float* row_max, float* row_sum, float* mu, float* sigma,
+                                        bool* used, hipStream_t stream) {
   *used = false;
-  if (!fused_shape_ok(s, scale)) return hipSuccess;
+  if (!fused_shape_ok(s, scale) || stat_elems >= INT32_MAX) return hipSuccess;
   const int n_units = s.n_prob * s.h_kv;
   const int rows = s.group() * 32;
-  const int max_chunks = (s.max_len + kFusedChunk - 1) / kFusedChunk;
+  const int max_items = (s.max_len + kItemKeys - 1) / kItemKeys;
   char* p = static_cast<char*>(ws);
-  FusedArgs a;
+  PipeArgs a;
+  ItemDesc* desc = reinterpret_cast<ItemDesc*>(p);
+  a.desc = desc;
+  p += (size_t)n_units * max_items * sizeof(ItemDesc);
   a.part = reinterpret_cast<float2*>(p);
-  p += (size_t)n_units * max_chunks * rows * sizeof(float2);
+  p += (size_t)n_units * max_items * rows * sizeof(float2);
   a.fin = reinterpret_cast<float*>(p);
   p += (size_t)n_units * rows * sizeof(float);
-  a.cnt = reinterpret_cast<int*>(p);
-  p += (size_t)n_units * sizeof(int);
-  a.flag = reinterpret_cast<int*>(p);
-  p += (size_t)n_units * sizeof(int);
-  a.item_prefix = reinterpret_cast<int*>(p);
-  p += (size_t)(s.n_prob + 1) * sizeof(int);
   a.status = reinterpret_cast<int*>(p);
   a.q_win = static_cast<const uint16_t*>(q_win);
   a.k = static_cast<const uint16_t*>(k);
-  a.lens = s.lens;
-  a.tok_off = s.tok_off;
-  a.n_prob = s.n_prob;
-  a.h_q = s.h_q;
-  a.h_kv = s.h_kv;
+  a.G = s.group();
   a.c = scale * kLog2e;
   a.row_max = row_max;
   a.row_sum = row_sum;
   a.mu = mu;
   a.sigma = sigma;
-  a.max_chunks = max_chunks;
+  a.max_items = max_items;
   a.total_items = total_items;
-  fused_init_kernel<<<1, 1024, 0, stream>>>(s.lens, s.n_prob, s.h_kv, n_units, rows, a.cnt,
-                                            reinterpret_cast<unsigned*>(a.fin), a.item_prefix,
-                                            a.status);
+  fused_init_kernel<<<512, 256, 0, stream>>>(s.lens, s.tok_off, s.n_prob, s.h_kv, total_items,
+                                             max_items, rows, desc,
+                                             reinterpret_cast<unsigned*>(a.part),
+                                             reinterpret_cast<unsigned*>(a.fin), a.status);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int G = s.group();
