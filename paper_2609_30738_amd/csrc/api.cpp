@@ -79,6 +79,20 @@ int max_candidates(const kv_problem* pr, int32_t budget, int32_t cand_mult, int3
 
 int launch_status(hipError_t e) { return e == hipSuccess ? KV_OK : KV_ERR_LAUNCH; }
 
+// Segment plan of the streaming window kernels for this batch.
+kv::StreamPlan stream_plan_of(const kv_problem* pr, const kv::Shape& s) {
+  int64_t total = 0;
+  for (int p = 0; p < pr->n_prob; ++p) total += (int64_t)pr->h_kv * pr->len_host[p];
+  return kv::stream_plan(s, total);
+}
+
+// Workspace of the window entry points: the larger of the chunked and the streaming layouts.
+size_t window_ws_bytes(const kv_problem* pr, const kv::Shape& s) {
+  size_t b = kv::window_stats_ws_bytes(s);
+  if (kv::stream_shape_ok(s, 1.f)) b = std::max(b, kv::stream_ws_bytes(s, stream_plan_of(pr, s)));
+  return align_up(b);
+}
+
 }  // namespace
 
 extern "C" {
@@ -106,7 +120,7 @@ size_t kv_workspace_bytes(const kv_problem* pr, int32_t budget, int32_t cand_mul
   (void)budget;
   (void)cand_mult;
   (void)keep_tail;
-  return align_up(std::max(kv::window_stats_ws_bytes(s), kv::fused_ws_bytes(s)));
+  return window_ws_bytes(pr, s);
 }
 
 int32_t kv_candidate_stride(const kv_problem* pr, int32_t budget, int32_t cand_mult,
@@ -129,11 +143,18 @@ int kv_window_scores(const kv_problem* pr, const void* q_win, const void* k, flo
   if (!q_win || !k || !row_max || !row_sum) return KV_ERR_NULL;
   if (!aligned16(q_win) || !aligned16(k)) return KV_ERR_ARG;
   if (!std::isfinite(scale)) return KV_ERR_ARG;
-  const size_t need = align_up(kv::window_stats_ws_bytes(s));
-  if (ws_bytes < need || !ws || (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1)))
+  if (ws_bytes < window_ws_bytes(pr, s) || !ws ||
+      (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1)))
     return KV_ERR_WORKSPACE;
-  return launch_status(kv::launch_window_stats(s, q_win, k, scale, ws, row_max, row_sum,
-                                               static_cast<hipStream_t>(stream)));
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (kv::stream_shape_ok(s, scale)) {
+    const kv::StreamPlan plan = stream_plan_of(pr, s);
+    st = launch_status(kv::launch_stream_stats(s, plan, q_win, k, scale, ws, hs));
+    if (st != KV_OK) return st;
+    return launch_status(kv::launch_combine_partials(s, ws, plan.seg_keys, plan.max_segs,
+                                                     s.group() * 32, row_max, row_sum, hs));
+  }
+  return launch_status(kv::launch_window_stats(s, q_win, k, scale, ws, row_max, row_sum, hs));
 }
 
 int kv_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float scale,
@@ -145,8 +166,13 @@ int kv_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float sc
   if (!q_win || !k || !row_max || !row_sum || !mu || !sigma) return KV_ERR_NULL;
   if (!aligned16(q_win) || !aligned16(k)) return KV_ERR_ARG;
   if (!std::isfinite(scale)) return KV_ERR_ARG;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (kv::stream_shape_ok(s, scale) && !attn)
+    return launch_status(kv::launch_stream_mu_sigma(s, stream_plan_of(pr, s), q_win, k, scale,
+                                                    nullptr, row_max, row_sum, nullptr, nullptr,
+                                                    mu, sigma, hs));
   return launch_status(kv::launch_mu_sigma(s, q_win, k, scale, row_max, row_sum, mu, sigma, attn,
-                                           static_cast<hipStream_t>(stream)));
+                                           hs));
 }
 
 int kv_window_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float scale,
@@ -158,24 +184,19 @@ int kv_window_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, f
   if (!q_win || !k || !row_max || !row_sum || !mu || !sigma) return KV_ERR_NULL;
   if (!aligned16(q_win) || !aligned16(k)) return KV_ERR_ARG;
   if (!std::isfinite(scale)) return KV_ERR_ARG;
-  const size_t need = align_up(std::max(kv::window_stats_ws_bytes(s), kv::fused_ws_bytes(s)));
-  if (ws_bytes < need || !ws || (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1)))
+  if (ws_bytes < window_ws_bytes(pr, s) || !ws ||
+      (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1)))
     return KV_ERR_WORKSPACE;
-  int64_t items = 0, stat_elems = 0;
-  for (int p = 0; p < pr->n_prob; ++p) {
-    items += (int64_t)pr->h_kv * ((pr->len_host[p] + kv::kFusedChunk - 1) / kv::kFusedChunk);
-    stat_elems = std::max(stat_elems, (pr->tok_off_host[p] + pr->len_host[p]) * pr->h_kv);
-  }
   hipStream_t hs = static_cast<hipStream_t>(stream);
-  if (items <= INT32_MAX) {
-    bool used = false;
-    const hipError_t e = kv::launch_window_mu_sigma_fused(s, q_win, k, scale, (int)items,
-                                                          stat_elems, ws, row_max, row_sum, mu,
-                                                          sigma, &used, hs);
-    if (e != hipSuccess) return KV_ERR_LAUNCH;
-    if (used) return KV_OK;
+  if (kv::stream_shape_ok(s, scale)) {
+    // segment partials, then normalisers, row statistics and mu / sigma in one more pass
+    const kv::StreamPlan plan = stream_plan_of(pr, s);
+    st = launch_status(kv::launch_stream_stats(s, plan, q_win, k, scale, ws, hs));
+    if (st != KV_OK) return st;
+    return launch_status(kv::launch_stream_mu_sigma(s, plan, q_win, k, scale, ws, nullptr,
+                                                    nullptr, row_max, row_sum, mu, sigma, hs));
   }
-  // shapes the single-pass kernel does not cover: row statistics, then a second pass over K
+  // other shapes: chunked row statistics, then a second pass over K
   st = launch_status(kv::launch_window_stats(s, q_win, k, scale, ws, row_max, row_sum, hs));
   if (st != KV_OK) return st;
   return launch_status(kv::launch_mu_sigma(s, q_win, k, scale, row_max, row_sum, mu, sigma,

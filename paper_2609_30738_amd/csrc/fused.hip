@@ -20,20 +20,22 @@
 //                                         and the two-pass sample variance over the window rows;
 //                   keys of item i+2 are requested into the slot item i-2 has just released.
 //
-//   Eight of a unit's items (chosen so that the role rotates over the workgroups) merge it, one
-//   slice of R/8 window rows each: they poll every item's partial of their rows (initialised to a
-//   NaN sentinel), combine them and store the normalisers and the row_max / row_sum outputs of
-//   those rows.  Every workgroup
-//   requests the normalisers of an item's unit one iteration after publishing the item's partial
-//   and waits for them one iteration later.
-//   Exchanged values use device-scope accesses, which bypass the per-XCD caches; every wait is
-//   bounded.
+//   The merge is spread over the unit's items: the last M = min(n, R, grid) of its n items own the
+//   window rows r = c - (n - M) (mod M) each.  One iteration after publishing item c, its
+//   workgroup polls every item's partial of the rows it owns (initialised to a NaN sentinel),
+//   combines them and stores those rows' normalisers and row_max / row_sum outputs.  The
+//   normalisers of item i - 2's unit are requested at the end of iteration i - 1 and waited for
+//   in iteration i.  Exchanged values use device-scope accesses, which bypass the per-XCD caches;
+//   every wait is bounded.
 //
-// Deadlock freedom: in every iteration a workgroup publishes its item's partial (and merges, if it
-// is a merger) before it waits for any normaliser, and it only waits for the units of earlier
-// items.  When each workgroup holds at most three items of any unit (checked at launch), every
-// partial of a unit is published before anyone waits for that unit.  The grid is launched
-// cooperatively so that every workgroup is resident.
+// Deadlock freedom (n <= grid, checked at launch, so that a workgroup holds at most one item of
+// a unit and the items of a unit lie in consecutive iterations of the workgroups): iteration j of
+// every workgroup publishes item j, then merges for item j - 1, then waits for item j - 2's unit.
+// Take the smallest iteration j at which some workgroup waits.  The other items of item j - 1's
+// unit lie at iterations <= j of their workgroups, all already published; the owners of item
+// j - 2's rows lie at iterations <= j - 1 and have merged by iteration j, before their own wait.
+// So every wait at iteration j ends.  The grid is launched cooperatively so that every workgroup
+// is resident.
 #include <type_traits>
 
 #include "common.h"
@@ -50,10 +52,8 @@ static_assert(kItemKeys == kFusedChunk, "an item is one chunk");
 constexpr int kSlots = 4;   // register slots of key tiles per wave
 constexpr int kLag = 2;     // phase 2 of an item runs kLag iterations after its phase 1
 constexpr int kQBufs = 4;   // query / normaliser buffers (items i-2 .. i+1)
-constexpr int kMergers = kWaves;  // row slices of a unit's merge (one wave's rows each)
-constexpr int kMaxLocalItems = 800;  // items per workgroup (their descriptors sit in LDS)
+constexpr int kMaxLocalItems = 760;  // items per workgroup (their descriptors sit in LDS)
 constexpr int kMaxSpins = 1 << 16;     // polls of another workgroup's value (about 1 us each)
-constexpr int kMaxLdsSpins = 1 << 24;  // polls of the workgroup's own counter
 constexpr int kMaxProbs = 4096;        // problems the descriptor builder scans in LDS
 constexpr unsigned kPending = 0x7FC0DEADu;  // NaN pattern: value not published yet
 
@@ -139,8 +139,7 @@ template <int D, int NB> struct Geo {
   static constexpr int QELEMS = R * D;      // bf16 elements of one query buffer
   static constexpr int QCHUNKS = R * CH;
   static constexpr int QPT = (QCHUNKS + kThreads - 1) / kThreads;  // staging loads per thread
-  static constexpr int RW = R / kWaves;  // rows whose partials a wave merges (lanes 0 .. RW-1)
-  static constexpr int LG = 64 / RW;     // lane groups of a wave in a unit merge
+  static constexpr int RPL = (R + 63) / 64;  // window rows per lane when a wave covers all rows
   // 16-byte chunk `ch` of query row `row` sits at chunk ch ^ (row % CH) of the row in LDS, so that
   // a fragment read of 16 consecutive rows touches 16 different chunks (all banks).
   __device__ static int qslot(int row, int ch) { return row * CH + (ch ^ (row % CH)); }
@@ -150,13 +149,12 @@ template <int D, int NB>
 __global__ __launch_bounds__(kThreads, 1) void window_mu_sigma_fused_kernel(PipeArgs a) {
   using Gm = Geo<D, NB>;
   constexpr int R = Gm::R, NS = Gm::NS, CH = Gm::CH, QPT = Gm::QPT;
-  constexpr int RW = Gm::RW, LG = Gm::LG;
+  constexpr int RPL = Gm::RPL;
   __shared__ __align__(16) uint16_t qbuf[kQBufs][Gm::QELEMS];
   __shared__ __align__(16) float2 red[2][kWaves][R];  // per-wave (m, z) of the last two items
-  __shared__ __align__(16) float2 mrg[kWaves][RW];    // unit merge: per-wave partial results
-  __shared__ __align__(16) float bsh[kQBufs][R];      // normalisers of the items in phase 2
+  __shared__ __align__(16) float bsw[kWaves][R];      // each wave's copy of its phase-2 normalisers
   __shared__ __align__(16) ItemDesc dsh[kMaxLocalItems];  // this workgroup's items, in order
-  __shared__ int qcnt, rcnt, dcnt, bcnt;  // wave-to-wave ordering, see below
+  __shared__ int rcnt;  // phase-1 arrivals: the wave that raises it to 8 (n + 1) is item n's last
   __shared__ int s_fail;  // a wait timed out: every later wait is skipped, outputs become NaN
 
   const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
@@ -165,9 +163,8 @@ __global__ __launch_bounds__(kThreads, 1) void window_mu_sigma_fused_kernel(Pipe
   const int n_local = wg < a.total_items ? (a.total_items - wg + grid - 1) / grid : 0;
   const float inv_g = 1.f / (float)a.G;
   const float c = a.c;
-  const int mrow = wave * RW + (lane % RW);  // row this lane publishes / polls (lanes < RW)
   if (n_local == 0) return;
-  if (threadIdx.x == 0) bcnt = 0, s_fail = 0;
+  if (threadIdx.x == 0) s_fail = 0;
   auto failed = [&]() {
     return __hip_atomic_load(&s_fail, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) != 0;
   };
@@ -180,7 +177,12 @@ __global__ __launch_bounds__(kThreads, 1) void window_mu_sigma_fused_kernel(Pipe
 
   bf16x8_t slot[kSlots][NS];
   bf16x8_t qst[QPT];
-  float bq = 0.f;  // this lane's polled normaliser (kept in one register throughout)
+  float bq[RPL];  // this lane's polled normalisers, rows lane + 64 k (kept in registers throughout)
+#pragma unroll
+  for (int k = 0; k < RPL; ++k) bq[k] = 0.f;
+  unsigned long long pm[2] = {0ull, 0ull};  // partials requested for the next merge
+  float out_val = 0.f;  // this lane's mu (lanes 0-31) or sigma (lanes 32-63) of the last phase 2
+  int out_idx = -1;     // its element index, -1 for none
 
   // ---- loads ---------------------------------------------------------------------------------
   // keys of this wave's tile of an item: a wave-uniform base and this lane's offset (its key
@@ -271,27 +273,32 @@ __global__ __launch_bounds__(kThreads, 1) void window_mu_sigma_fused_kernel(Pipe
     float ab[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) ab[j] = 0.f;
+    // the causal mask only cuts into a unit's last tile: the other tiles take the unmasked loop
+    auto accumulate = [&](auto masked) {
 #pragma unroll 1
-    for (int b = 0; b < NB; ++b) {
-      f32x16_t d = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      bf16x8_t qf[NS];
-      read_q(qf, qb, b);
+      for (int b = 0; b < NB; ++b) {
+        f32x16_t d = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        bf16x8_t qf[NS];
+        read_q(qf, qb, b);
 #pragma unroll
-      for (int s = 0; s < NS; ++s) d = mfma_step(qf[s], t[s], d);
+        for (int s = 0; s < NS; ++s) d = mfma_step(qf[s], t[s], d);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        // window rows 8 q + 4 half + 0..3 of query head b
-        const float4 bv = *reinterpret_cast<const float4*>(bs + b * 32 + 8 * q + 4 * half);
-        const float bb[4] = {bv.x, bv.y, bv.z, bv.w};
+        for (int q = 0; q < 4; ++q) {
+          // window rows 8 q + 4 half + 0..3 of query head b
+          const float4 bv = *reinterpret_cast<const float4*>(bs + b * 32 + 8 * q + 4 * half);
+          const float bb[4] = {bv.x, bv.y, bv.z, bv.w};
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int j = 4 * q + u;
-          float e = __builtin_amdgcn_exp2f(fmaf(d[j], c, -bb[u]));
-          if (edge && 8 * q + u < thr) e = 0.f;
-          ab[j] += e;
+          for (int u = 0; u < 4; ++u) {
+            const int j = 4 * q + u;
+            float e = __builtin_amdgcn_exp2f(fmaf(d[j], c, -bb[u]));
+            if (decltype(masked)::value && 8 * q + u < thr) e = 0.f;
+            ab[j] += e;
+          }
         }
       }
-    }
+    };
+    if (edge) accumulate(std::true_type{});
+    else accumulate(std::false_type{});
     // ab[j] = G a[r][key] for the window rows r = acc_row(j, lane); the other 16 are in lane ^ 32
     float sp[4];
 #pragma unroll
@@ -304,85 +311,58 @@ __global__ __launch_bounds__(kThreads, 1) void window_mu_sigma_fused_kernel(Pipe
       vp[j & 3] = fmaf(dl, dl, vp[j & 3]);
     }
     const float var = sum_halves((vp[0] + vp[1]) + (vp[2] + vp[3])) * (1.f / 31.f);
-    if (key < it.L) {
-      const float bad = failed() ? __builtin_nanf("") : 0.f;  // a timed-out wait poisons the output
-      float* dst = half == 0 ? a.mu : a.sigma;
-      const float val = half == 0 ? mean : __builtin_amdgcn_sqrtf(var);
-      (dst + (it.sbase + t0))[l32] = val + bad;
-    }
+    // the store is issued at the end of the iteration, after the loads the next one waits for
+    const float bad = failed() ? __builtin_nanf("") : 0.f;  // a timed-out wait poisons the output
+    out_val = (half == 0 ? mean : __builtin_amdgcn_sqrtf(var)) + bad;
+    out_idx = key < it.L ? it.sbase + key : -1;
   };
 
-  // ---- unit merge of one row slice: the workgroup's waves split the unit's items --------------
-  //      lane = lane group lg x slice row; wave w, lane group lg take the items w + 8 (lg + LG k)
-  auto merge_slice = [&](const Item& it, int slice) {
-    const int lr = lane % RW, lg = lane / RW;
-    const int row = slice * RW + lr;
-    const float2* col = a.part + (size_t)it.unit * a.max_items * R + row;
-    float m = -INFINITY, z = 0.f;
-    constexpr int kBatch = 4;
+  // ---- merge of the rows an item owns (one wave): lane k takes the partials of items k + 64 q;
+  //      pm holds the first row's partials of items lane and lane + 64, requested earlier ----------
+  auto owns_rows = [&](const Item& it) { return it.c >= it.n - min(min(it.n, R), grid); };
+  auto merge_rows = [&](const Item& it, const unsigned long long (&pm)[2]) {
+    const int M = min(min(it.n, R), grid);
+    const int r0 = it.c - (it.n - M);
 #pragma unroll 1
-    for (int c0 = wave + kWaves * lg; c0 < it.n; c0 += kBatch * kWaves * LG) {
-      unsigned long long v[kBatch];
-#pragma unroll
-      for (int q = 0; q < kBatch; ++q)
-        v[q] = get_u64(col + (size_t)min(c0 + q * kWaves * LG, it.n - 1) * R);
-#pragma unroll
-      for (int q = 0; q < kBatch; ++q) {
-        const int cq = c0 + q * kWaves * LG;
-        if (cq >= it.n) continue;
-        int spins = 0;
-        while ((unsigned)(v[q] & 0xFFFFFFFFu) == kPending && !failed()) {
-          if (++spins > kMaxSpins) {
-            fail(1);
-            break;
+    for (int row = r0; row < R; row += M) {
+      const float2* col = a.part + (size_t)it.unit * a.max_items * R + row;
+      float m = -INFINITY, z = 0.f;
+#pragma unroll 1
+      for (int q = 0; q * 64 < it.n; ++q) {
+        const int k = q * 64 + lane;
+        unsigned long long v;
+        if (row == r0 && q < 2) v = q == 0 ? pm[0] : pm[1];
+        else v = get_u64(col + (size_t)min(k, it.n - 1) * R);
+        if (k < it.n) {
+          int spins = 0;
+          while ((unsigned)(v & 0xFFFFFFFFu) == kPending && !failed()) {
+            if (++spins > kMaxSpins) {
+              fail(1);
+              break;
+            }
+            __builtin_amdgcn_s_sleep(2);
+            v = get_u64(col + (size_t)k * R);
           }
-          __builtin_amdgcn_s_sleep(2);
-          v[q] = get_u64(col + (size_t)cq * R);
+          const float2 f = __builtin_bit_cast(float2, v);
+          merge_into(m, z, f.x, f.y);
         }
-        const float2 f = __builtin_bit_cast(float2, v[q]);
-        merge_into(m, z, f.x, f.y);
       }
-    }
 #pragma unroll
-    for (int off = RW; off < 64; off <<= 1) merge_into(m, z, __shfl_xor(m, off), __shfl_xor(z, off));
-    if (lane < RW) mrg[wave][lr] = make_float2(m, z);
-    __syncthreads();
-    if (wave == 0 && lane < RW) {
-      float mm = -INFINITY, zz = 0.f;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) merge_into(mm, zz, mrg[w][lr].x, mrg[w][lr].y);
-      put_u32(a.fin + (size_t)it.unit * R + row, __float_as_uint(mm + __builtin_log2f(zz)));
-      const size_t ri = (size_t)it.unit * R + row;  // = (p h_q + g G + head) * 32 + r
-      a.row_max[ri] = mm * kLn2;
-      a.row_sum[ri] = zz;
-    }
-    __syncthreads();
-  };
-
-  // ---- wave-to-wave ordering through LDS counters (each wave adds 1 per event) ----------------
-  //   qcnt: query buffers written (Q of item n is complete when qcnt >= 8 (n + 1))
-  //   rcnt: phase-1 row statistics written (item n's in red when rcnt >= 8 (n + 1))
-  //   dcnt: iterations finished (iteration n done by every wave when dcnt >= 8 (n + 1))
-  //   bcnt: normalisers delivered (item n's in bsh when bcnt >= 8 (n + 1))
-  auto bump = [&](int* ctr) {
-    if (lane == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-  };
-  auto await = [&](int* ctr, int need) {
-    int spins = 0;
-    while (__hip_atomic_load(ctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < need && !failed()) {
-      if (++spins > kMaxLdsSpins) {
-        fail(4);
-        break;
+      for (int off = 1; off < 64; off <<= 1) merge_into(m, z, __shfl_xor(m, off), __shfl_xor(z, off));
+      if (lane == 0) {
+        const size_t ri = (size_t)it.unit * R + row;  // = (p h_q + g G + head) * 32 + r
+        put_u32(a.fin + ri, __float_as_uint(m + __builtin_log2f(z)));
+        a.row_max[ri] = m * kLn2;
+        a.row_sum[ri] = z;
       }
-      __builtin_amdgcn_s_sleep(1);
     }
   };
 
-  // ---- the item's partial over the waves (this wave's rows), max first then the rescaled sum --
-  auto item_partial = [&](int buf, float& m, float& z) {
+  // ---- the item's partial of one row over the waves, max first then the rescaled sum ----------
+  auto item_partial = [&](int buf, int row, float& m, float& z) {
     float2 v[kWaves];
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) v[w] = red[buf][w][mrow];
+    for (int w = 0; w < kWaves; ++w) v[w] = red[buf][w][row];
     m = v[0].x;
 #pragma unroll
     for (int w = 1; w < kWaves; ++w) m = fmaxf(m, v[w].x);
@@ -395,11 +375,10 @@ __global__ __launch_bounds__(kThreads, 1) void window_mu_sigma_fused_kernel(Pipe
 
   // ---- prologue: item descriptors, queries of item 0 into LDS, keys of items 0 and 1 ----------
   for (int j = threadIdx.x; j < n_local; j += kThreads) dsh[j] = a.desc[(size_t)wg + (size_t)j * grid];
-  if (threadIdx.x == 0) qcnt = 0, rcnt = 0, dcnt = 0;
+  if (threadIdx.x == 0) rcnt = 0;
   __syncthreads();
   load_queries(0);
   store_queries(qbuf[0]);
-  bump(&qcnt);
   load_queries(1);
   load_item_keys(slot[0], 0);
   load_item_keys(slot[1], 1);
@@ -413,75 +392,84 @@ __global__ __launch_bounds__(kThreads, 1) void window_mu_sigma_fused_kernel(Pipe
     if (has1) it1 = item_of(i);
     if (has2) it2 = item_of(n2);
 
-    // (a) phase 1 of item i, once its queries are in LDS and red[i & 1] is free again
-    if (has1) {
-      await(&qcnt, kWaves * (i + 1));
-      await(&dcnt, kWaves * (i - 1));
-      phase1(slot[S1], qbuf[i % kQBufs], it1, i & 1);
-    }
-    bump(&rcnt);
+    // (a) once every wave has finished iteration i - 1, the queries of item i (stored there) are
+    //     complete and the buffer of item i + 1 (last read by item i - 3) and red[i & 1] (last read
+    //     for item i - 2) are free: store the queries of item i + 1, then phase 1 of item i
+    __syncthreads();
+    if (exists(i + 1)) store_queries(qbuf[(i + 1) % kQBufs]);
+    if (has1) phase1(slot[S1], qbuf[i % kQBufs], it1, i & 1);
 
-    // (b) item i's partial of this wave's rows, published for its unit; the last kMergers items
-    //     of a unit then merge one row slice each (slice s by item max(0, n - kMergers + s))
+    // (b) the last wave to finish phase 1 of item i forms the item's partial of every row and
+    //     publishes it for its unit; the others go on at once
     if (has1) {
-      await(&rcnt, kWaves * (i + 1));
-      if (lane < RW) {
-        float m, z;
-        item_partial(i & 1, m, z);
-        float2* dst = a.part + ((size_t)it1.unit * a.max_items + it1.c) * R + mrow;
-        put_u64(dst, __builtin_bit_cast(unsigned long long, make_float2(m, z)));
-      }
-      // The last kMergers items of a unit merge; with fewer items than slices item 0 takes the
-      // surplus slices.  A workgroup's items of one unit lie grid items apart and the grid holds at
-      // least min(n, kMergers) workgroups, so no workgroup merges for a unit before holding all its
-      // own items of that unit.
-      const int first = it1.n - kMergers;
-      if (it1.c >= first) {
-        const int s_lo = it1.c == 0 ? 0 : it1.c - first;
-        const int s_hi = it1.c - first;
-#pragma unroll 1
-        for (int sl = s_lo; sl <= s_hi; ++sl) merge_slice(it1, sl);
-      }
-    }
-
-    // (c) this wave's rows of item i - 2's normalisers (requested in the previous iteration) into
-    //     LDS; phase 2 of item i - 2 once every wave has delivered its rows
-    if (has2) {
-      if (lane < RW) {
-        int spins = 0;
-        while (__float_as_uint(bq) == kPending && !failed()) {
-          if (++spins > kMaxSpins) {
-            fail(2);
-            break;
+      int old = 0;
+      if (lane == 0)
+        old = __hip_atomic_fetch_add(&rcnt, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
+      old = sread(old);
+      if (old == kWaves * i + kWaves - 1) {
+#pragma unroll
+        for (int k = 0; k < RPL; ++k) {
+          const int row = lane + 64 * k;
+          if (row < R) {
+            float m, z;
+            item_partial(i & 1, row, m, z);
+            float2* dst = a.part + ((size_t)it1.unit * a.max_items + it1.c) * R + row;
+            put_u64(dst, __builtin_bit_cast(unsigned long long, make_float2(m, z)));
           }
-          __builtin_amdgcn_s_sleep(2);
-          bq = __uint_as_float(get_u32(a.fin + (size_t)it2.unit * R + mrow));
         }
-        bsh[n2 % kQBufs][mrow] = bq;
       }
-      bump(&bcnt);
-      await(&bcnt, kWaves * (n2 + 1));
-      phase2(slot[S2], qbuf[n2 % kQBufs], bsh[n2 % kQBufs], it2);
     }
 
-    // (d) queries of item i + 1 into LDS (their buffer was last used by item i - 3, whose phase 2
-    //     every wave has finished once iteration i - 1 is done)
-    if (exists(i + 1)) {
-      await(&dcnt, kWaves * i);
-      store_queries(qbuf[(i + 1) % kQBufs]);
+    // (b') the rows item i - 1 owns, merged by one wave (rotating with the iteration)
+    if (exists(i - 1) && wave == ((i - 1) & (kWaves - 1))) {
+      const Item itm = item_of(i - 1);
+      if (owns_rows(itm)) merge_rows(itm, pm);
     }
-    bump(&qcnt);
 
-    // (e) this wave's rows of item i - 1's normalisers, the queries of item i + 2, then the keys
-    //     of item i + 2 into the released slot.  Vector loads of a wave complete in order: what
-    //     is waited for sooner is requested first.  The key loads are issued unconditionally so
-    //     that every iteration issues the same number of them and the waits before phase 1 only
-    //     cover the keys of the item they need.
-    if (exists(i - 1) && lane < RW)
-      bq = __uint_as_float(get_u32(a.fin + (size_t)item_of(i - 1).unit * R + mrow));
+    // (c) item i - 2's normalisers (requested in the previous iteration) into this wave's LDS
+    //     row, then phase 2 of item i - 2
+    if (has2) {
+#pragma unroll
+      for (int k = 0; k < RPL; ++k) {
+        const int row = lane + 64 * k;
+        if (row < R) {
+          int spins = 0;
+          while (__float_as_uint(bq[k]) == kPending && !failed()) {
+            if (++spins > kMaxSpins) {
+              fail(2);
+              break;
+            }
+            __builtin_amdgcn_s_sleep(2);
+            bq[k] = __uint_as_float(get_u32(a.fin + (size_t)it2.unit * R + row));
+          }
+          bsw[wave][row] = bq[k];
+        }
+      }
+      phase2(slot[S2], qbuf[n2 % kQBufs], bsw[wave], it2);
+    }
+
+    // (d) the queries of item i + 2, the first partials of item i's next merge, item i - 1's
+    //     normalisers, then the keys of item i + 2 into the released slot.  Vector memory
+    //     operations of a wave complete in order: what is waited for sooner is requested first,
+    //     and this iteration's output store goes last.  Every load is issued unconditionally
+    //     (clamped addresses) so that every iteration issues the same number of them and the
+    //     waits before phase 1 only cover the keys of the item they need.
     load_queries(i + 2);
+    {
+      const Item itp = item_of(exists(i) ? i : 0);
+      const int M = min(min(itp.n, R), grid);
+      const int r0 = max(0, itp.c - (itp.n - M));
+      const float2* col = a.part + (size_t)itp.unit * a.max_items * R + r0;
+      pm[0] = get_u64(col + (size_t)min(lane, itp.n - 1) * R);
+      pm[1] = get_u64(col + (size_t)min(lane + 64, itp.n - 1) * R);
+      const Item itf = item_of(exists(i - 1) ? i - 1 : 0);
+#pragma unroll
+      for (int k = 0; k < RPL; ++k)
+        bq[k] = __uint_as_float(get_u32(a.fin + (size_t)itf.unit * R + min(lane + 64 * k, R - 1)));
+    }
     load_item_keys(slot[S2], i + 2);
-    bump(&dcnt);
+    if (out_idx >= 0) (half == 0 ? a.mu : a.sigma)[out_idx] = out_val;
+    out_idx = -1;
   };
 
   for (int i0 = 0; i0 < n_local + kLag; i0 += kSlots) {
@@ -587,9 +575,9 @@ hipError_t fused_dispatch(const PipeArgs& base, int total_items, bool* used, hip
     res = per_cu * cus;
   }
   const int grid = min(total_items, res);
-  // a workgroup may hold at most three items of one unit (the deadlock argument above), and its
-  // item descriptors must fit in LDS
-  if (grid <= 0 || base.max_items > 3 * grid || (total_items + grid - 1) / grid > kMaxLocalItems) {
+  // a unit may have at most one item per workgroup (the deadlock argument above), and a
+  // workgroup's item descriptors must fit in LDS
+  if (grid <= 0 || base.max_items > grid || (total_items + grid - 1) / grid > kMaxLocalItems) {
     *used = false;
     return hipSuccess;
   }

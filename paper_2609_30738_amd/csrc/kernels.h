@@ -48,6 +48,33 @@ hipError_t launch_window_mu_sigma_fused(const Shape& s, const void* q_win, const
                                         float* row_max, float* row_sum, float* mu, float* sigma,
                                         bool* used, hipStream_t stream);
 
+// Streaming two-pass row statistics + mu/sigma (bf16, w = 32, G in {1, 2, 4}, scale > 0): every
+// unit is cut
+// into segments of seg_keys keys (a multiple of 256), one workgroup each, sized so that a batch
+// fills the chip about once; the segment partials (m, z) per window row live in the workspace,
+// [n_units][max_segs][32 G] float2.
+struct StreamPlan {
+  int seg_keys;
+  int max_segs;
+};
+bool stream_shape_ok(const Shape& s, float scale);
+StreamPlan stream_plan(const Shape& s, int64_t total_keys);  // total_keys = sum_p h_kv L_p
+size_t stream_ws_bytes(const Shape& s, const StreamPlan& plan);
+// Pass 1: segment partials into ws.
+hipError_t launch_stream_stats(const Shape& s, const StreamPlan& plan, const void* q_win,
+                               const void* k, float scale, void* ws, hipStream_t stream);
+// Pass 2: normalisers from the partials in ws (then also row_max_out / row_sum_out), or, with
+// ws == nullptr, from row_max_in / row_sum_in; mu / sigma out.
+hipError_t launch_stream_mu_sigma(const Shape& s, const StreamPlan& plan, const void* q_win,
+                                  const void* k, float scale, const void* ws,
+                                  const float* row_max_in, const float* row_sum_in,
+                                  float* row_max_out, float* row_sum_out, float* mu, float* sigma,
+                                  hipStream_t stream);
+// row_max / row_sum from chunk partials [n_units][max_chunks][rows_pad] of chunk_keys keys each.
+hipError_t launch_combine_partials(const Shape& s, const void* part, int chunk_keys,
+                                   int max_chunks, int rows_pad, float* row_max, float* row_sum,
+                                   hipStream_t stream);
+
 struct SelectArgs {
   const float* mu;
   const float* sigma;

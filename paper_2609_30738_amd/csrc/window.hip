@@ -360,6 +360,16 @@ hipError_t mu_sigma_nb(const Shape& s, const void* q, const void* k, float scale
 
 }  // namespace
 
+hipError_t launch_combine_partials(const Shape& s, const void* part, int chunk_keys,
+                                   int max_chunks, int rows_pad, float* row_max, float* row_sum,
+                                   hipStream_t stream) {
+  const int64_t rows = (int64_t)s.n_prob * s.h_q * s.w;
+  combine_stats_kernel<<<(unsigned)((rows + kThreads - 1) / kThreads), kThreads, 0, stream>>>(
+      static_cast<const float2*>(part), s.lens, s.n_prob, s.h_q, s.h_kv, s.w, rows_pad, chunk_keys,
+      max_chunks, row_max, row_sum);
+  return hipGetLastError();
+}
+
 hipError_t launch_window_stats(const Shape& s, const void* q_win, const void* k, float scale,
                                void* ws, float* row_max, float* row_sum, hipStream_t stream) {
   if (s.dtype == kDtBf16)
