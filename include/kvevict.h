@@ -121,10 +121,9 @@ int kv_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float sc
                 const float* row_max, const float* row_sum, float* mu, float* sigma,
                 float* attn, void* stream);
 
-/* kv_window_scores followed by kv_mu_sigma (without attn): same results in one call.  For bf16
- * caches with w = 32, G in {1, 2, 4}, scale > 0 and L_p <= 131072 the keys are read once (the
- * logits stay on chip while each unit's row statistics are combined); other shapes run the two
- * passes.  Needs workspace. */
+/* kv_window_scores followed by kv_mu_sigma (without attn): same results in one call.  The
+ * normalisers go from the first pass to the second through the workspace, without a round trip
+ * through row_max / row_sum.  Needs workspace. */
 int kv_window_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float scale,
                        float* row_max, float* row_sum, float* mu, float* sigma, void* ws,
                        size_t ws_bytes, void* stream);

@@ -13,8 +13,6 @@ constexpr int kDtBf16 = 1;
 
 // Keys per work item of the window kernels (a multiple of 4 waves x 32 keys).
 constexpr int kWindowChunk = 1024;
-// Keys per work item of the single-pass window kernel (8 waves x 32 keys).
-constexpr int kFusedChunk = 256;
 
 struct Shape {
   int dtype;  // 0 = fp32, 1 = bf16
@@ -37,16 +35,6 @@ hipError_t launch_window_stats(const Shape& s, const void* q_win, const void* k,
 hipError_t launch_mu_sigma(const Shape& s, const void* q_win, const void* k, float scale,
                            const float* row_max, const float* row_sum, float* mu, float* sigma,
                            float* attn, hipStream_t stream);
-
-// Single-pass row statistics + mu/sigma (bf16, w = 32, G in {1, 2, 4}, scale > 0).  Sets *used to
-// false (and enqueues nothing) when the shape or the device cannot run it; the caller then runs the
-// two-pass kernels.  total_items = sum_p h_kv * ceil(L_p / kFusedChunk); stat_elems = the extent
-// of mu / sigma, max_p (tok_off[p] + L_p) * h_kv.
-size_t fused_ws_bytes(const Shape& s);
-hipError_t launch_window_mu_sigma_fused(const Shape& s, const void* q_win, const void* k,
-                                        float scale, int total_items, int64_t stat_elems, void* ws,
-                                        float* row_max, float* row_sum, float* mu, float* sigma,
-                                        bool* used, hipStream_t stream);
 
 // Streaming two-pass row statistics + mu/sigma (bf16, w = 32, G in {1, 2, 4}, scale > 0): every
 // unit is cut

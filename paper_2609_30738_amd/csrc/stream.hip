@@ -33,7 +33,8 @@ namespace {
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
 constexpr int kTileKeys = 32;
-constexpr int kSlots = 3;  // register slots of key tiles per wave (two tiles in flight)
+constexpr int kSlots = 3;  // register slots of key tiles per wave (kSlots - 1 tiles in flight)
+static_assert(kSlots == 3 || kSlots == 4, "the tile loop is unrolled for three or four slots");
 
 struct StreamArgs {
   const uint16_t* q_win;
@@ -131,8 +132,8 @@ __global__ __launch_bounds__(kThreads, 1) void stats_stream_kernel(StreamArgs a)
     e_run[b] = 0.f;
   }
   bf16x8_t slot[kSlots][NS];
-  load_tile<D>(slot[0], kg, tile_key(0), L, l32, half);
-  load_tile<D>(slot[1], kg, tile_key(1), L, l32, half);
+#pragma unroll
+  for (int q = 0; q + 1 < kSlots; ++q) load_tile<D>(slot[q], kg, tile_key(q), L, l32, half);
   __syncthreads();
 
   auto tile = [&](const bf16x8_t (&t)[NS], int t0) __attribute__((always_inline)) {
@@ -204,16 +205,17 @@ __global__ __launch_bounds__(kThreads, 1) void stats_stream_kernel(StreamArgs a)
 
   auto step = [&](auto sc, int j) __attribute__((always_inline)) {
     constexpr int S = decltype(sc)::value;
-    constexpr int SN = (S + 2) % kSlots;
-    // tile j + 2 into the slot tile j - 1 released (unconditional: a fixed number of loads per
-    // step keeps every wait on exactly the tile it needs)
-    load_tile<D>(slot[SN], kg, tile_key(j + 2), L, l32, half);
+    constexpr int SN = (S + kSlots - 1) % kSlots;
+    // tile j + kSlots - 1 into the slot tile j - 1 released (unconditional: a fixed number of
+    // loads per step keeps every wait on exactly the tile it needs)
+    load_tile<D>(slot[SN], kg, tile_key(j + kSlots - 1), L, l32, half);
     if (j < my_tiles) tile(slot[S], tile_key(j));
   };
   for (int j0 = 0; j0 < my_tiles; j0 += kSlots) {
     step(std::integral_constant<int, 0>{}, j0);
     step(std::integral_constant<int, 1>{}, j0 + 1);
     step(std::integral_constant<int, 2>{}, j0 + 2);
+    if constexpr (kSlots > 3) step(std::integral_constant<int, 3 % kSlots>{}, j0 + 3);
   }
 
   // (max, sum relative to it) of this lane's keys; lanes l and l ^ 32 hold the same rows
@@ -282,8 +284,8 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
   auto tile_key = [&](int j) { return k0 + (j * kWaves + wave) * kTileKeys; };
 
   bf16x8_t slot[kSlots][NS];
-  load_tile<D>(slot[0], kg, tile_key(0), L, l32, half);
-  load_tile<D>(slot[1], kg, tile_key(1), L, l32, half);
+#pragma unroll
+  for (int q = 0; q + 1 < kSlots; ++q) load_tile<D>(slot[q], kg, tile_key(q), L, l32, half);
   __syncthreads();
 
   auto tile = [&](const bf16x8_t (&t)[NS], int t0) __attribute__((always_inline)) {
@@ -336,14 +338,15 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
 
   auto step = [&](auto sc, int j) __attribute__((always_inline)) {
     constexpr int S = decltype(sc)::value;
-    constexpr int SN = (S + 2) % kSlots;
-    load_tile<D>(slot[SN], kg, tile_key(j + 2), L, l32, half);
+    constexpr int SN = (S + kSlots - 1) % kSlots;
+    load_tile<D>(slot[SN], kg, tile_key(j + kSlots - 1), L, l32, half);
     if (j < my_tiles) tile(slot[S], tile_key(j));
   };
   for (int j0 = 0; j0 < my_tiles; j0 += kSlots) {
     step(std::integral_constant<int, 0>{}, j0);
     step(std::integral_constant<int, 1>{}, j0 + 1);
     step(std::integral_constant<int, 2>{}, j0 + 2);
+    if constexpr (kSlots > 3) step(std::integral_constant<int, 3 % kSlots>{}, j0 + 3);
   }
 }
 

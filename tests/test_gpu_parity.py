@@ -69,6 +69,42 @@ def test_ragged_batch_scaled(run):
     _all(gpu_cases.run_gpu(wl, fused=True))
 
 
+def _plant_rising_keys(wl, pk, plants):
+    """Per kv group, keys along head 0's mean query direction (orthogonal to the other heads'
+    mean directions) with window logits of about alpha nats at the given positions of problem 0."""
+    from oracle import evict
+    q = evict.decode(pk.q_win[0], wl.dtype).astype(np.float64)  # [h_q, w, d]
+    L = int(pk.lens[0])
+    G = wl.h_q // wl.h_kv
+    k = pk.k[: wl.h_kv * L * wl.d].reshape(wl.h_kv, L, wl.d)
+    for g in range(wl.h_kv):
+        dirs = [q[g * G + h].mean(axis=0) for h in range(G)]
+        u = dirs[0].copy()
+        basis = []
+        for v in dirs[1:]:
+            for b_ in basis:
+                v = v - (v @ b_) * b_
+            basis.append(v / np.linalg.norm(v))
+        for b_ in basis:
+            u = u - (u @ b_) * b_
+        u /= np.linalg.norm(u)
+        nu = float((q[g * G] @ u).mean())
+        for pos, alpha in plants:
+            k[g, pos] = workloads.f32_to_bf16_bits((alpha / (wl.scale * nu) * u).astype(np.float32))
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_rising_logits_move_the_running_offset(fused):
+    """Keys whose logits rise far above the earlier ones, in later tiles and segments of the unit:
+    about 9 nats (kept against the running offset), 40 nats (a rebase) and 100 nats (2^x of the
+    difference overflows; a rebase).  Row statistics, mu and sigma must still match."""
+    wl = workloads.mistral_layer()
+    wl.seq_lens = [5000]
+    pk = workloads.draw_packed(wl)
+    _plant_rising_keys(wl, pk, [(777, 9.0), (2222, 40.0), (4444, 100.0)])
+    _all(gpu_cases.run_gpu(wl, fused=fused, packed=pk))
+
+
 def test_compaction_of_oracle_selection():
     """kv_compact_cache fed with the oracle's admissions reproduces the oracle's compacted rows."""
     import torch
