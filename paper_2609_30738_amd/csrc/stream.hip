@@ -141,9 +141,9 @@ __global__ __launch_bounds__(kThreads, 1) void stats_stream_kernel(StreamArgs a)
     // segment.  The key of register j is t0 + 4 half + 8 (j / 4) + (j % 4).
     const bool edge = t0 + 31 >= min(k1, L - 31);
     const int thr = min(k1 - 1, L - 32 + l32) - t0 - 4 * half;
-    // the running statistics of head b sit in m_run[0] / z_run[0] during its turn (the arrays
-    // rotate by one head per turn, so that the loop indexes registers statically)
-#pragma unroll 1
+    // heads one after another: the scheduling barrier at the end of each keeps the compiler from
+    // hoisting the next head's fragment reads (registers stay at one head's worth)
+#pragma unroll
     for (int b = 0; b < NB; ++b) {
       bf16x8_t qf[NS];
       read_qfrags<D, NB>(qf, qs, b, l32, half);
@@ -155,7 +155,7 @@ __global__ __launch_bounds__(kThreads, 1) void stats_stream_kernel(StreamArgs a)
         for (int j = 0; j < 16; ++j)
           if (8 * (j >> 2) + (j & 3) > thr) d[j] = -INFINITY;
       }
-      const float mo = m_run[0];
+      const float mo = m_run[b];
       float ex[16];
 #pragma unroll
       for (int j = 0; j < 16; ++j) ex[j] = __builtin_amdgcn_exp2f(fmaf(d[j], c, -mo));
@@ -170,8 +170,8 @@ __global__ __launch_bounds__(kThreads, 1) void stats_stream_kernel(StreamArgs a)
       }
       const float zt = (zs[0] + zs[1]) + (zs[2] + zs[3]);
       if (zt <= 4294967296.f) {
-        z_run[0] += zt;
-        e_run[0] = __uint_as_float(max(__float_as_uint(e_run[0]), max(max(es[0], es[1]), max(es[2], es[3]))));
+        z_run[b] += zt;
+        e_run[b] = __uint_as_float(max(__float_as_uint(e_run[b]), max(max(es[0], es[1]), max(es[2], es[3]))));
       } else {
         // first tile of the lane, a larger logit or an overflow (also NaN from -inf - -inf):
         // rebase on the larger of the offset and the tile's maximum logit
@@ -182,24 +182,15 @@ __global__ __launch_bounds__(kThreads, 1) void stats_stream_kernel(StreamArgs a)
         const float mn = fmaxf(mo, tm);
         if (mn != -INFINITY) {
           const float keep = mo == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mo - mn);
-          float z = z_run[0] * keep;
+          float z = z_run[b] * keep;
 #pragma unroll
           for (int j = 0; j < 16; ++j) z += __builtin_amdgcn_exp2f(fmaf(d[j], c, -mn));
-          m_run[0] = mn;
-          z_run[0] = z;
-          e_run[0] = fmaxf(e_run[0] * keep, tm == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(tm - mn));
+          m_run[b] = mn;
+          z_run[b] = z;
+          e_run[b] = fmaxf(e_run[b] * keep, tm == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(tm - mn));
         }
       }
-      const float m0 = m_run[0], z0 = z_run[0], e0 = e_run[0];
-#pragma unroll
-      for (int q = 0; q + 1 < NB; ++q) {
-        m_run[q] = m_run[q + 1];
-        z_run[q] = z_run[q + 1];
-        e_run[q] = e_run[q + 1];
-      }
-      m_run[NB - 1] = m0;
-      z_run[NB - 1] = z0;
-      e_run[NB - 1] = e0;
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
@@ -297,7 +288,7 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
 #pragma unroll
     for (int j = 0; j < 16; ++j) ab[j] = 0.f;
     auto accumulate = [&](auto masked) __attribute__((always_inline)) {
-#pragma unroll 1
+#pragma unroll
       for (int b = 0; b < NB; ++b) {
         bf16x8_t qf[NS];
         read_qfrags<D, NB>(qf, qs, b, l32, half);
@@ -317,6 +308,7 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
             ab[j] += e;
           }
         }
+        __builtin_amdgcn_sched_barrier(0);  // one head at a time, as in pass 1
       }
     };
     if (edge) accumulate(std::true_type{});
