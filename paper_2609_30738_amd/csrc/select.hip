@@ -1,6 +1,7 @@
 // Greedy diversity-aware admission (section 3.2, Eq. (2), (4), (5)) on gfx950.
 //
-// One workgroup of 256 threads per (problem, kv head):
+// One workgroup per (problem, kv head): 1024 threads for bf16 keys (one candidate per thread), 256
+// for fp32 keys (up to four per thread, whose key rows need more registers):
 //   1. base scores s_i = fma(lambda1, sigma_i, mu_i) over the candidates [0, n_cand), their maximum
 //      (the normaliser, clamped at 1e-12), and the C-th largest score by a most-significant-digit
 //      radix select over order-preserving 32-bit keys (4 passes of 8 bits, wave-private LDS
@@ -9,7 +10,7 @@
 //   2. the candidate set P: every score above the threshold plus the lowest positions among those
 //      equal to it, compacted in ascending position order (ballot ranks inside a wave, LDS prefix
 //      across waves);
-//   3. B greedy steps.  Thread t owns candidates t, t + 256, ...: it keeps their keys in registers,
+//   3. B greedy steps.  Thread t owns candidates t, t + NT, ...: it keeps their keys in registers,
 //      their normalised score s~, running max-cosine and admitted flag.  Each step updates the
 //      running maxima against the last admitted key (read from an LDS copy of the candidate keys),
 //      forms s~ + lambda2 * corr, and finds the (score, lowest slot) maximum: a DPP / permlane
@@ -26,10 +27,9 @@ namespace kv {
 
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = 4;
 constexpr int kMaxCandBytes = 131072;        // LDS copy of the candidate keys
 constexpr int kMaxStagedKeyBytes = 139264;  // LDS copy of every candidate's score key (34816)
+constexpr size_t kLdsBytes = 163840;        // LDS of one CU
 
 __device__ __forceinline__ uint32_t order_key(float x) {
   const uint32_t u = __float_as_uint(x);
@@ -178,20 +178,20 @@ template <int D> struct KeyRow<kDtF32, D> {
   }
 };
 
-struct SelectShared {
-  uint32_t hist[kWaves][256];
+template <int NW> struct SelectShared {
+  uint32_t hist[NW][256];
   uint32_t scan[256];
-  uint32_t wave_cnt[2][kWaves];
-  float wave_max[kWaves];
-  uint64_t best[2][kWaves];
+  uint32_t wave_cnt[2][NW];
+  float wave_max[NW];
+  uint64_t best[2][NW];
   uint32_t sel_threshold;
   int sel_need;
 };
 
 }  // namespace
 
-template <int DT, int D, int CPT, bool STAGED>
-__global__ __launch_bounds__(kThreads) void mmr_select_kernel(
+template <int DT, int D, int NT, int CPT, bool STAGED>
+__global__ __launch_bounds__(NT) void mmr_select_kernel(
     const float* __restrict__ mu, const float* __restrict__ sigma,
     const typename Elem<DT>::T* __restrict__ k, const int32_t* __restrict__ lens,
     const int64_t* __restrict__ tok_off, const float* __restrict__ lambda1,
@@ -199,7 +199,9 @@ __global__ __launch_bounds__(kThreads) void mmr_select_kernel(
     int cand_stride, int max_cand, int32_t* __restrict__ sel_idx, float* __restrict__ sel_score,
     int32_t* __restrict__ cand_idx, float* __restrict__ cand_corr) {
   using T = typename Elem<DT>::T;
-  __shared__ SelectShared sh;
+  constexpr int kThreads = NT, kWaves = NT / 64;
+  static_assert(NT >= 256, "one thread per histogram bin");
+  __shared__ SelectShared<kWaves> sh;
   // dynamic LDS: [max_cand] positions, [max_cand] 1/|k|, then a region that first holds the
   // order-preserving keys of every candidate score (STAGED) and then the candidates' key rows
   extern __shared__ __align__(16) unsigned char dyn[];
@@ -286,21 +288,28 @@ __global__ __launch_bounds__(kThreads) void mmr_select_kernel(
       }
     }
     __syncthreads();
-    // suffix sums over bins (bin 255 = largest digit)
-    const uint32_t cnt = sh.hist[0][tid] + sh.hist[1][tid] + sh.hist[2][tid] + sh.hist[3][tid];
-    sh.scan[tid] = cnt;
+    // suffix sums over bins (bin 255 = largest digit); thread tid < 256 holds bin tid
+    const bool bin = tid < 256;
+    if (bin) {
+      uint32_t cnt = 0;
+#pragma unroll
+      for (int v = 0; v < kWaves; ++v) cnt += sh.hist[v][tid];
+      sh.scan[tid] = cnt;
+    }
     __syncthreads();
     for (int off = 1; off < 256; off <<= 1) {
-      const uint32_t add = (tid + off < 256) ? sh.scan[tid + off] : 0u;
+      const uint32_t add = (bin && tid + off < 256) ? sh.scan[tid + off] : 0u;
       __syncthreads();
-      sh.scan[tid] += add;
+      if (bin) sh.scan[tid] += add;
       __syncthreads();
     }
-    const uint32_t ge = sh.scan[tid];                             // count with digit >= tid
-    const uint32_t gt = (tid + 1 < 256) ? sh.scan[tid + 1] : 0u;  // count with digit > tid
-    if (ge >= (uint32_t)need && gt < (uint32_t)need) {
-      sh.sel_threshold = prefix | ((uint32_t)tid << shift);
-      sh.sel_need = need - (int)gt;
+    if (bin) {
+      const uint32_t ge = sh.scan[tid];                             // count with digit >= tid
+      const uint32_t gt = (tid + 1 < 256) ? sh.scan[tid + 1] : 0u;  // count with digit > tid
+      if (ge >= (uint32_t)need && gt < (uint32_t)need) {
+        sh.sel_threshold = prefix | ((uint32_t)tid << shift);
+        sh.sel_need = need - (int)gt;
+      }
     }
     __syncthreads();
     prefix = sh.sel_threshold;
@@ -309,7 +318,9 @@ __global__ __launch_bounds__(kThreads) void mmr_select_kernel(
     __syncthreads();
   }
   __syncthreads();
-  float den = fmaxf(fmaxf(sh.wave_max[0], sh.wave_max[1]), fmaxf(sh.wave_max[2], sh.wave_max[3]));
+  float den = sh.wave_max[0];
+#pragma unroll
+  for (int v = 1; v < kWaves; ++v) den = fmaxf(den, sh.wave_max[v]);
   den = fmaxf(den, 1e-12f);
 
   // ---- 2. candidate positions in ascending order ----------------------------------------------
@@ -397,45 +408,52 @@ __global__ __launch_bounds__(kThreads) void mmr_select_kernel(
 
   int last = -1;
   float last_inv = 0.f;
+  // only the waves that own candidate slots take part; the others just keep step with the
+  // barrier (sleeping there instead of taking issue slots from the live waves)
+  const int live_waves = min(kWaves, (C + 63) / 64);
+  const bool live = wave < live_waves;
   for (int t = 0; t < budget; ++t) {
-    float my_score = -INFINITY;  // admitted slots rank below every live score
-    int my_slot = 0x7FFFFFFF;
+    if (live) {
+      float my_score = -INFINITY;  // admitted slots rank below every live score
+      int my_slot = 0x7FFFFFFF;
 #pragma unroll
-    for (int q = 0; q < CPT; ++q) {
-      if (!admitted[q]) {
-        if (last >= 0) {
-          const float cs = key[q].dot_lds(ckeys + (size_t)last * D) * inv[q] * last_inv;
-          corr[q] = fmaxf(corr[q], cs);
-        }
-        float sc = fmaf(lam2, corr[q], st[q]);
-        if (!(sc > -INFINITY)) sc = -FLT_MAX;  // NaN or -inf still ranks above admitted slots
-        if (sc > my_score) {  // q ascending: ties keep the lower slot
-          my_score = sc;
-          my_slot = tid + q * kThreads;
+      for (int q = 0; q < CPT; ++q) {
+        if (!admitted[q]) {
+          if (last >= 0) {
+            const float cs = key[q].dot_lds(ckeys + (size_t)last * D) * inv[q] * last_inv;
+            corr[q] = fmaxf(corr[q], cs);
+          }
+          float sc = fmaf(lam2, corr[q], st[q]);
+          if (!(sc > -INFINITY)) sc = -FLT_MAX;  // NaN or -inf still ranks above admitted slots
+          if (sc > my_score) {  // q ascending: ties keep the lower slot
+            my_score = sc;
+            my_slot = tid + q * kThreads;
+          }
         }
       }
+      const uint64_t wbest = wave_best(my_score, my_slot);
+      if (lane == 0) sh.best[t & 1][wave] = wbest;
     }
-    const uint64_t wbest = wave_best(my_score, my_slot);
-    if (lane == 0) sh.best[t & 1][wave] = wbest;
     __syncthreads();
-    uint64_t b = sh.best[t & 1][0];
+    if (live) {
+      uint64_t b = sh.best[t & 1][0];
+      for (int v = 1; v < live_waves; ++v) {
+        const uint64_t o = sh.best[t & 1][v];
+        b = o > b ? o : b;
+      }
+      last = min(max(unpack_slot(b), 0), C - 1);  // always a live slot: budget <= C
 #pragma unroll
-    for (int v = 1; v < kWaves; ++v) {
-      const uint64_t o = sh.best[t & 1][v];
-      b = o > b ? o : b;
-    }
-    last = min(max(unpack_slot(b), 0), C - 1);  // always a live slot: budget <= C
-#pragma unroll
-    for (int q = 0; q < CPT; ++q)
-      if (tid + q * kThreads == last) admitted[q] = true;
-    last_inv = cinv[last];
-    if (tid == 0) {
-      const size_t o = ((size_t)p * h_kv + g) * budget + t;
-      sel_idx[o] = cpos[last];
-      if (sel_score) {
-        const uint32_t kk = (uint32_t)(b >> 32);
-        const uint32_t u = (kk & 0x80000000u) ? (kk & 0x7FFFFFFFu) : ~kk;
-        sel_score[o] = __uint_as_float(u);
+      for (int q = 0; q < CPT; ++q)
+        if (tid + q * kThreads == last) admitted[q] = true;
+      last_inv = cinv[last];
+      if (tid == 0) {
+        const size_t o = ((size_t)p * h_kv + g) * budget + t;
+        sel_idx[o] = cpos[last];
+        if (sel_score) {
+          const uint32_t kk = (uint32_t)(b >> 32);
+          const uint32_t u = (kk & 0x80000000u) ? (kk & 0x7FFFFFFFu) : ~kk;
+          sel_score[o] = __uint_as_float(u);
+        }
       }
     }
   }
@@ -468,47 +486,59 @@ __global__ __launch_bounds__(kThreads) void mmr_select_kernel(
 // ------------------------------------------------------------------------------------------------
 int select_max_candidates(int d, int elem_bytes) {
   const int by_lds = kMaxCandBytes / (d * elem_bytes);
-  const int by_regs = 4 * kThreads;
+  const int by_regs = elem_bytes == 2 ? 1024 : 4 * 256;  // candidate slots of the workgroup
   return by_lds < by_regs ? by_lds : by_regs;
 }
 
 namespace {
-template <int DT, int D, int CPT, bool STAGED>
+template <int DT, int D, int NT, int CPT, bool STAGED>
 hipError_t select_launch(const Shape& s, const SelectArgs& a, hipStream_t st) {
   using T = typename Elem<DT>::T;
   const size_t region = std::max((size_t)a.max_cand * D * sizeof(T),
                                  STAGED ? (size_t)a.max_cand_all * 4 : (size_t)0);
   const size_t dyn = (((size_t)a.max_cand * 8 + 15) & ~(size_t)15) + region;
-  auto kern = mmr_select_kernel<DT, D, CPT, STAGED>;
+  auto kern = mmr_select_kernel<DT, D, NT, CPT, STAGED>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
   if (e != hipSuccess) return e;
-  kern<<<dim3((unsigned)(s.n_prob * s.h_kv)), kThreads, dyn, st>>>(
+  kern<<<dim3((unsigned)(s.n_prob * s.h_kv)), NT, dyn, st>>>(
       a.mu, a.sigma, static_cast<const T*>(a.k), s.lens, s.tok_off, a.lambda1, a.lambda2, s.h_kv,
       a.budget, a.cand_mult, a.keep_tail, a.cand_stride, a.max_cand, a.sel_idx, a.sel_score,
       a.cand_idx, a.cand_corr);
   return hipGetLastError();
 }
 
-// Score keys are staged in LDS when every problem's candidates fit next to the key rows.
-template <int DT, int D, int CPT>
+// Score keys are staged in LDS when every problem's candidates fit next to the key rows (and the
+// whole workgroup's LDS stays within the 160 KiB of a CU).
+template <int DT, int D, int NT, int CPT>
 hipError_t select_dispatch(const Shape& s, const SelectArgs& a, hipStream_t st) {
-  if ((size_t)a.max_cand_all * 4 <= (size_t)kMaxStagedKeyBytes)
-    return select_launch<DT, D, CPT, true>(s, a, st);
-  return select_launch<DT, D, CPT, false>(s, a, st);
+  using T = typename Elem<DT>::T;
+  const size_t rows = (size_t)a.max_cand * D * sizeof(T);
+  const size_t staged = (((size_t)a.max_cand * 8 + 15) & ~(size_t)15) +
+                        std::max(rows, (size_t)a.max_cand_all * 4) + sizeof(SelectShared<NT / 64>);
+  if ((size_t)a.max_cand_all * 4 <= (size_t)kMaxStagedKeyBytes && staged <= kLdsBytes)
+    return select_launch<DT, D, NT, CPT, true>(s, a, st);
+  return select_launch<DT, D, NT, CPT, false>(s, a, st);
 }
 
 template <int DT, int D>
 hipError_t select_cpt(const Shape& s, const SelectArgs& a, hipStream_t st) {
-  // only the candidates-per-thread counts that the LDS key copy allows are instantiated
   constexpr int kMaxCand = kMaxCandBytes / (D * (int)sizeof(typename Elem<DT>::T));
-  const int cpt = (a.max_cand + kThreads - 1) / kThreads;
-  if (cpt <= 1) return select_dispatch<DT, D, 1>(s, a, st);
-  if constexpr (kMaxCand > kThreads) {
-    if (cpt <= 2) return select_dispatch<DT, D, 2>(s, a, st);
+  if constexpr (DT == kDtBf16) {
+    // bf16 key rows fit the registers of 16 waves: one candidate per thread of 1024
+    static_assert(kMaxCand <= 1024, "one candidate per thread");
+    return select_dispatch<DT, D, 1024, 1>(s, a, st);
+  } else {
+    // only the candidates-per-thread counts that the LDS key copy allows are instantiated
+    constexpr int kNT = 256;
+    const int cpt = (a.max_cand + kNT - 1) / kNT;
+    if (cpt <= 1) return select_dispatch<DT, D, kNT, 1>(s, a, st);
+    if constexpr (kMaxCand > kNT) {
+      if (cpt <= 2) return select_dispatch<DT, D, kNT, 2>(s, a, st);
+    }
+    if constexpr (kMaxCand > 2 * kNT) return select_dispatch<DT, D, kNT, 4>(s, a, st);
+    return hipErrorInvalidValue;
   }
-  if constexpr (kMaxCand > 2 * kThreads) return select_dispatch<DT, D, 4>(s, a, st);
-  return hipErrorInvalidValue;
 }
 }  // namespace
 
