@@ -8,11 +8,13 @@ lambda2 depth profile.
 
 Before every timed step a 512 MiB buffer is overwritten (outside the timed region) so that no part
 of the 2 GiB key cache is served from the 256 MB last-level cache.  Each step is timed with HIP
-events on the launch stream, per entry point and in total.  A second timed loop runs the scoring
+events on the launch stream, per entry point and in total (`value`: the whole batch in one launch
+per entry point).  A second timed loop runs the scoring
 as its two separate entry points (kv_window_scores: the first streaming pass over the keys and
 the merge of its segment partials; kv_mu_sigma: the second pass) so that each kernel's duration
-is measured live; the roofline entry describes the first pass, the dominant kernel.  One JSON
-line is printed.
+is measured live; the roofline entry describes the first pass, the dominant kernel.  A third loop
+times the per-layer schedule: the scoring launched once per layer, then one batched selection and
+compaction.  One JSON line is printed.
 """
 from __future__ import annotations
 
@@ -75,10 +77,14 @@ def mfma_flops(wl) -> float:
     return 2.0 * float(lens.sum()) * wl.h_q * wl.w * wl.d
 
 
-def source_sha() -> str:
+# sources that define each profiled kernel: its traffic record stays valid while they are unchanged
+KERNEL_SOURCES = {"stats_stream": ("stream.hip", "common.h")}
+
+
+def source_sha(kernel: str) -> str:
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2609_30738_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in KERNEL_SOURCES[kernel]:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
@@ -86,13 +92,13 @@ def source_sha() -> str:
 
 def measured_traffic(kernel: str, workload: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it was taken on the
-    current kernel sources (null otherwise)."""
+    current sources of the kernel (null otherwise)."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("source_sha") != source_sha():
+    if rec.get("source_sha") != source_sha(kernel):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -228,6 +234,35 @@ def main() -> None:
     kern = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(2)] for e in kernel_events])
     k_stats, k_mu = (float(x) for x in kern.mean(axis=0))
 
+    # the per-layer schedule: the scoring launched layer by layer (as a model would after each
+    # layer's prefill, into the same output buffers), then one batched selection and compaction
+    layer_batches = [_lib.Batch(wl.dtype, wl.h_q, wl.h_kv, wl.d, wl.w, [int(b.lens_host[p])],
+                                [int(b.tok_off_host[p])]) for p in range(b.n_prob)]
+    rows = wl.h_q * wl.w
+
+    def layered_step(evs):
+        evs[0].record(stream)
+        for p, lb in enumerate(layer_batches):
+            _lib.window_mu_sigma(lb, inp.q_win[p], inp.k, inp.scale,
+                                 out.row_max[p * rows:(p + 1) * rows],
+                                 out.row_sum[p * rows:(p + 1) * rows], out.mu, out.sigma, out.ws)
+        evs[1].record(stream)
+        _lib.mmr_select(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2, wl.budget, 4,
+                        wl.w, out.sel_idx, None, None, None, out.ws)
+        _lib.compact_cache(b, inp.k, inp.v, out.sel_idx, wl.budget, wl.w, out.k_out, out.v_out)
+        evs[2].record(stream)
+
+    layer_events = []
+    for it in range(args.warmup + args.steps):
+        flush.zero_()
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        layered_step(evs)
+        if it >= args.warmup:
+            layer_events.append(evs)
+    torch.cuda.synchronize()
+    lay = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(2)] for e in layer_events])
+    lay_score, lay_rest = (float(x) for x in lay.mean(axis=0))
+
     per = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(3)] for e in all_events])
     step_ms = per.sum(axis=1)
     ms = float(step_ms.mean())
@@ -260,6 +295,9 @@ def main() -> None:
         "breakdown_ms": {n: round(float(v), 4) for n, v in zip(names, mean_part)},
         "step_ms_min_max": [round(float(step_ms.min()), 4), round(float(step_ms.max()), 4)],
         "wall_s_timed_loop": round(wall, 3),
+        "per_layer_schedule_ms": {"total": round(lay_score + lay_rest, 4),
+                                  "scoring (32 launches of kv_window_mu_sigma)": round(lay_score, 4),
+                                  "select+compact (batched)": round(lay_rest, 4)},
         "per_kernel_ms": {"stats_stream+combine (kv_window_scores)": round(k_stats, 4),
                           "mu_sigma_stream (kv_mu_sigma)": round(k_mu, 4),
                           "mmr_select": round(float(mean_part[1]), 4),

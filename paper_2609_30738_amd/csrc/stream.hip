@@ -89,11 +89,13 @@ __device__ __forceinline__ void read_qfrags(bf16x8_t (&qf)[D / 16], const uint16
     qf[s] = *reinterpret_cast<const bf16x8_t*>(qs + Gm::qslot(row, 2 * s + half) * 8);
 }
 
-// keys of this wave's tile starting at key t0 of the unit (lane key clamped into the unit)
+// keys of this wave's tile starting at key t0 of the unit; a lane's key is clamped to the last key
+// of the segment (kend - 1), so that the prefetches past the segment's last tile re-read one row
+// instead of the next segment
 template <int D>
-__device__ __forceinline__ void load_tile(bf16x8_t (&t)[D / 16], const uint16_t* kg, int t0, int L,
-                                          int l32, int half) {
-  const uint16_t* row = kg + (size_t)min(t0 + l32, L - 1) * D + 8 * half;
+__device__ __forceinline__ void load_tile(bf16x8_t (&t)[D / 16], const uint16_t* kg, int t0,
+                                          int kend, int l32, int half) {
+  const uint16_t* row = kg + (size_t)min(t0 + l32, kend - 1) * D + 8 * half;
 #pragma unroll
   for (int s = 0; s < D / 16; ++s) t[s] = *reinterpret_cast<const bf16x8_t*>(row + 16 * s);
 }
@@ -133,7 +135,7 @@ __global__ __launch_bounds__(kThreads, 1) void stats_stream_kernel(StreamArgs a)
   }
   bf16x8_t slot[kSlots][NS];
 #pragma unroll
-  for (int q = 0; q + 1 < kSlots; ++q) load_tile<D>(slot[q], kg, tile_key(q), L, l32, half);
+  for (int q = 0; q + 1 < kSlots; ++q) load_tile<D>(slot[q], kg, tile_key(q), k1, l32, half);
   __syncthreads();
 
   auto tile = [&](const bf16x8_t (&t)[NS], int t0) __attribute__((always_inline)) {
@@ -199,7 +201,7 @@ __global__ __launch_bounds__(kThreads, 1) void stats_stream_kernel(StreamArgs a)
     constexpr int SN = (S + kSlots - 1) % kSlots;
     // tile j + kSlots - 1 into the slot tile j - 1 released (unconditional: a fixed number of
     // loads per step keeps every wait on exactly the tile it needs)
-    load_tile<D>(slot[SN], kg, tile_key(j + kSlots - 1), L, l32, half);
+    load_tile<D>(slot[SN], kg, tile_key(j + kSlots - 1), k1, l32, half);
     if (j < my_tiles) tile(slot[S], tile_key(j));
   };
   for (int j0 = 0; j0 < my_tiles; j0 += kSlots) {
@@ -276,7 +278,7 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
 
   bf16x8_t slot[kSlots][NS];
 #pragma unroll
-  for (int q = 0; q + 1 < kSlots; ++q) load_tile<D>(slot[q], kg, tile_key(q), L, l32, half);
+  for (int q = 0; q + 1 < kSlots; ++q) load_tile<D>(slot[q], kg, tile_key(q), k1, l32, half);
   __syncthreads();
 
   auto tile = [&](const bf16x8_t (&t)[NS], int t0) __attribute__((always_inline)) {
@@ -331,7 +333,7 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
   auto step = [&](auto sc, int j) __attribute__((always_inline)) {
     constexpr int S = decltype(sc)::value;
     constexpr int SN = (S + kSlots - 1) % kSlots;
-    load_tile<D>(slot[SN], kg, tile_key(j + kSlots - 1), L, l32, half);
+    load_tile<D>(slot[SN], kg, tile_key(j + kSlots - 1), k1, l32, half);
     if (j < my_tiles) tile(slot[S], tile_key(j));
   };
   for (int j0 = 0; j0 < my_tiles; j0 += kSlots) {
