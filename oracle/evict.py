@@ -110,12 +110,29 @@ def f32(x):
     return np.float32(x)
 
 
-def base_scores(mu: np.ndarray, sigma: np.ndarray, lam1: float) -> np.ndarray:
-    """s_i = mu_i + lambda1 sigma_i (Eq. (2) without the set term), formed in fp32 (one rounding)."""
-    mu32 = mu.astype(np.float32).astype(np.float64)
+def base_scores(mu: np.ndarray, sigma: np.ndarray, lam1: float, w_mu: float = 1.0) -> np.ndarray:
+    """s_i = w_mu mu_i + lambda1 sigma_i (Eq. (2) without the set term), formed in fp32: the weighted
+    mean rounded to fp32, then one rounding of the sum.  w_mu = 1 is the paper's score; w_mu = 0
+    drops the mean (the "dispersion & Corr" rule of the term ablation, section 4)."""
+    mu32 = mu.astype(np.float32)
+    if w_mu != 1.0:
+        mu32 = (mu32.astype(np.float64) * float(f32(w_mu))).astype(np.float32)
     sg32 = sigma.astype(np.float32).astype(np.float64)
     lam = float(f32(lam1))
-    return (mu32 + lam * sg32).astype(np.float32)
+    return (mu32.astype(np.float64) + lam * sg32).astype(np.float32)
+
+
+def max_pool(s: np.ndarray, n_cand: int, pool: int) -> np.ndarray:
+    """Max-pooling of the base scores along the candidate positions (the pooling of the mean-attention
+    baselines that section 3.1 keeps): s'_i = max of s_j over |j - i| <= (pool - 1) / 2 and
+    0 <= j < n_cand, i.e. positions outside the candidate range count as -inf.  pool is odd."""
+    if pool % 2 != 1 or pool < 1:
+        raise ValueError("the pooling window must be odd")
+    h = pool // 2
+    out = np.empty(n_cand, dtype=np.float32)
+    for i in range(n_cand):
+        out[i] = s[max(0, i - h):min(n_cand, i + h + 1)].max()
+    return out
 
 
 def normalised_scores(s: np.ndarray, n_cand: int) -> np.ndarray:
@@ -236,9 +253,13 @@ def candidate_count(n_cand: int, budget: int, cand_mult: int) -> int:
 
 
 def select_head(mu_g: np.ndarray, sigma_g: np.ndarray, k_g: np.ndarray, lam1: float, lam2: float,
-                budget: int, n_cand: int, cand_mult: int = 4) -> HeadResult:
-    """Selection for one kv head: base score, normalisation, top-C restriction, greedy MMR."""
-    s = base_scores(mu_g[:n_cand], sigma_g[:n_cand], lam1)
+                budget: int, n_cand: int, cand_mult: int = 4, pool: int = 1,
+                w_mu: float = 1.0) -> HeadResult:
+    """Selection for one kv head: base score (optionally max-pooled), normalisation, top-C
+    restriction, greedy MMR."""
+    s = base_scores(mu_g[:n_cand], sigma_g[:n_cand], lam1, w_mu)
+    if pool > 1:
+        s = max_pool(s, n_cand, pool)
     s_t = normalised_scores(s, n_cand)
     n_keep = candidate_count(n_cand, budget, cand_mult)
     cand = top_candidates(s, n_cand, n_keep)
@@ -254,11 +275,12 @@ def select_head(mu_g: np.ndarray, sigma_g: np.ndarray, k_g: np.ndarray, lam1: fl
 
 def evict_problem(q_win, k, v, dtype: str, scale: float, lam1: float, lam2: float, budget: int,
                   cand_mult: int = 4, keep_tail: Optional[int] = None, heads=None,
-                  want_attn: bool = False) -> ProblemResult:
+                  want_attn: bool = False, pool: int = 1, w_mu: float = 1.0) -> ProblemResult:
     """Whole path for one problem (one layer of one sequence).
 
     q_win [h_q, W, d], k and v [h_kv, L, d] as stored (fp32 or bf16 bits).  `heads` restricts the
-    selection to some kv heads (statistics are still returned for all of them).
+    selection to some kv heads (statistics are still returned for all of them).  pool / w_mu:
+    see max_pool and base_scores.
     """
     qd = decode(q_win, dtype)
     kd = decode(k, dtype)
@@ -284,7 +306,8 @@ def evict_problem(q_win, k, v, dtype: str, scale: float, lam1: float, lam2: floa
     results = []
     for g in range(h_kv):
         if g in sel_heads:
-            results.append(select_head(mu[g], sigma[g], kd[g], lam1, lam2, budget, n_cand, cand_mult))
+            results.append(select_head(mu[g], sigma[g], kd[g], lam1, lam2, budget, n_cand, cand_mult,
+                                       pool, w_mu))
         else:
             results.append(None)
     res = ProblemResult(row_max, row_sum, mu, sigma, results, attn=attn)

@@ -346,6 +346,62 @@ def test_ties_go_to_lower_position():
 # Compaction
 # ------------------------------------------------------------------------------------------------
 
+# ------------------------------------------------------------------------------------------------
+# Max-pooling of the base score and the mean-free score (NEXT items of the hot path)
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("pool", [1, 3, 5, 7, 31])
+def test_max_pool_matches_scipy_filter(pool):
+    """The pooled score equals scipy's 1-D maximum filter with the outside counted as -inf."""
+    from scipy.ndimage import maximum_filter1d
+    s = _rand(300, 21).astype(np.float32)
+    ref = maximum_filter1d(s.astype(np.float64), size=pool, mode="constant", cval=-np.inf)
+    np.testing.assert_array_equal(evict.max_pool(s, 300, pool), ref.astype(np.float32))
+
+
+def test_max_pool_spreads_a_spike_and_stops_at_the_candidate_range():
+    s = np.zeros(20, dtype=np.float32)
+    s[10] = 5.0
+    s[19] = 9.0                     # outside the candidate range [0, 18)
+    out = evict.max_pool(s, 18, 5)
+    assert list(np.flatnonzero(out == 5.0)) == [8, 9, 10, 11, 12]
+    assert out.max() == 5.0 and len(out) == 18
+    with pytest.raises(ValueError):
+        evict.max_pool(s, 18, 4)
+
+
+def test_pooled_selection_with_zero_lambdas_is_top_b_of_the_pooled_mean():
+    """lambda1 = lambda2 = 0 with pooling: the admissions are the B largest pooled means (ties to
+    the lower position), found here by a sort of the brute-force window maxima."""
+    rng = np.random.default_rng(7)
+    n, B, pool = 60, 9, 5
+    mu = rng.random(n).astype(np.float32)
+    k = rng.standard_normal((n, 8))
+    res = evict.select_head(mu, np.zeros(n), k, 0.0, 0.0, B, n, cand_mult=0, pool=pool)
+    pooled = [max(mu[max(0, i - 2):min(n, i + 3)]) for i in range(n)]
+    want = sorted(range(n), key=lambda i: (-pooled[i], i))[:B]
+    assert res.trace.selected == want
+
+
+def test_mean_free_score_with_lambda1_one_is_sigma():
+    """w_mu = 0, lambda1 = 1: the base score is sigma itself (rounded to fp32)."""
+    rng = np.random.default_rng(8)
+    mu, sg = rng.random(50), rng.random(50)
+    np.testing.assert_array_equal(evict.base_scores(mu, sg, 1.0, w_mu=0.0), sg.astype(np.float32))
+    np.testing.assert_array_equal(evict.base_scores(mu, sg, 0.4, w_mu=1.0),
+                                  evict.base_scores(mu, sg, 0.4))
+
+
+def test_mean_free_selection_with_lambda2_zero_is_top_b_by_sigma():
+    rng = np.random.default_rng(9)
+    n, B = 40, 6
+    mu, sg = rng.random(n), rng.random(n)
+    res = evict.select_head(mu, sg, rng.standard_normal((n, 4)), 0.7, 0.0, B, n, cand_mult=0,
+                            w_mu=0.0)
+    want = sorted(range(n), key=lambda i: (-float(np.float32(sg[i])), i))[:B]
+    assert res.trace.selected == want
+
+
 def test_compaction_keeps_sorted_selection_then_tail():
     L, d = 40, 4
     k = np.arange(L * d, dtype=np.uint16).reshape(L, d)
