@@ -147,6 +147,30 @@ int kv_mmr_select(const kv_problem* pr, const float* mu, const float* sigma, con
                   int32_t keep_tail, int32_t* sel_idx, float* sel_score, int32_t* cand_idx,
                   float* cand_corr, void* ws, size_t ws_bytes, void* stream);
 
+/* Scoring options of kv_mmr_select_ex.  NULL options mean {pool = 1, w_mu = 1}, which is exactly
+ * kv_mmr_select.
+ *   pool: odd window, 1 <= pool <= 63, of a max-pool over positions applied to the base score
+ *     before normalisation and the top-C restriction (the pooling that the mean-attention baselines
+ *     apply and that the paper keeps in its scoring, section 3.1):
+ *     s'_i = max_{j in [i - pool/2, i + pool/2] and [0, n_cand)} s_j.  The normaliser
+ *     max_j s'_j equals max_j s_j.
+ *   w_mu: weight of mu in the base score, s_i = w_mu * mu_i + lambda1 * sigma_i, with w_mu * mu_i
+ *     rounded to fp32 first (exact for w_mu = 1).  w_mu = 0 is the mean-free "dispersion and
+ *     redundancy" rule of the term ablation (section 4.3, Table 3).
+ * An even, non-positive or too large pool, or a non-finite w_mu, returns KV_ERR_ARG. */
+typedef struct kv_select_opts {
+  int32_t pool;
+  float w_mu;
+} kv_select_opts;
+
+/* kv_mmr_select with scoring options (opts nullable, see kv_select_opts); every other argument,
+ * output and limit as in kv_mmr_select. */
+int kv_mmr_select_ex(const kv_problem* pr, const float* mu, const float* sigma, const void* k,
+                     const float* lambda1, const float* lambda2, int32_t budget, int32_t cand_mult,
+                     int32_t keep_tail, const kv_select_opts* opts, int32_t* sel_idx,
+                     float* sel_score, int32_t* cand_idx, float* cand_corr, void* ws,
+                     size_t ws_bytes, void* stream);
+
 /* Compacted cache (sections 1 and 3.1: each layer keeps `budget` entries plus the kept tail);
  * budget <= 8192.
  * For every problem and kv head, rows 0..budget-1 of k_out/v_out are the rows of k/v at the

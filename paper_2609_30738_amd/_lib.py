@@ -35,7 +35,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvevict.
 
 SYMBOLS = ("kv_strerror", "kv_version", "kv_workspace_bytes", "kv_candidate_stride",
            "kv_window_scores", "kv_mu_sigma", "kv_window_mu_sigma", "kv_mmr_select",
-           "kv_compact_cache", "kv_depth_profile")
+           "kv_mmr_select_ex", "kv_compact_cache", "kv_depth_profile")
 
 
 class KvError(RuntimeError):
@@ -49,6 +49,10 @@ class KvProblem(ctypes.Structure):
                 ("h_kv", ctypes.c_int32), ("d", ctypes.c_int32), ("w", ctypes.c_int32),
                 ("len_host", ctypes.c_void_p), ("tok_off_host", ctypes.c_void_p),
                 ("len_dev", ctypes.c_void_p), ("tok_off_dev", ctypes.c_void_p)]
+
+
+class KvSelectOpts(ctypes.Structure):
+    _fields_ = [("pool", ctypes.c_int32), ("w_mu", ctypes.c_float)]
 
 
 _LIB = None
@@ -76,11 +80,13 @@ def lib() -> ctypes.CDLL:
         h.kv_window_mu_sigma.argtypes = [pr, vp, vp, ctypes.c_float, vp, vp, vp, vp, vp, sz, vp]
         h.kv_mmr_select.argtypes = [pr, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, sz,
                                     vp]
+        h.kv_mmr_select_ex.argtypes = [pr, vp, vp, vp, vp, vp, i32, i32, i32,
+                                       ctypes.POINTER(KvSelectOpts), vp, vp, vp, vp, vp, sz, vp]
         h.kv_compact_cache.argtypes = [pr, vp, vp, vp, i32, i32, vp, vp, vp]
         h.kv_depth_profile.argtypes = [i32, ctypes.POINTER(ctypes.c_double), i32, i32,
                                        ctypes.POINTER(ctypes.c_float)]
         for name in ("kv_window_scores", "kv_mu_sigma", "kv_window_mu_sigma", "kv_mmr_select",
-                     "kv_compact_cache", "kv_depth_profile"):
+                     "kv_mmr_select_ex", "kv_compact_cache", "kv_depth_profile"):
             getattr(h, name).restype = ctypes.c_int
         _LIB = h
     return _LIB
@@ -194,6 +200,22 @@ def mmr_select(batch: Batch, mu, sigma, k, lambda1, lambda2, budget: int, cand_m
                                _ptr(sel_idx), _ptr(sel_score), _ptr(cand_idx), _ptr(cand_corr),
                                _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
                                _stream(stream)), "kv_mmr_select")
+
+
+def mmr_select_ex(batch: Batch, mu, sigma, k, lambda1, lambda2, budget: int, cand_mult: int,
+                  keep_tail: int, sel_idx, sel_score=None, cand_idx=None, cand_corr=None, ws=None,
+                  pool: Optional[int] = None, w_mu: Optional[float] = None, stream=None) -> None:
+    """kv_mmr_select_ex; options are passed as NULL when both pool and w_mu are None."""
+    opts = None
+    if pool is not None or w_mu is not None:
+        opts = ctypes.byref(KvSelectOpts(1 if pool is None else int(pool),
+                                         1.0 if w_mu is None else float(w_mu)))
+    _check(lib().kv_mmr_select_ex(batch.ref(), _ptr(mu), _ptr(sigma), _ptr(k), _ptr(lambda1),
+                                  _ptr(lambda2), int(budget), int(cand_mult), int(keep_tail), opts,
+                                  _ptr(sel_idx), _ptr(sel_score), _ptr(cand_idx),
+                                  _ptr(cand_corr), _ptr(ws),
+                                  0 if ws is None else ws.numel() * ws.element_size(),
+                                  _stream(stream)), "kv_mmr_select_ex")
 
 
 def compact_cache(batch: Batch, k, v, sel_idx, budget: int, keep_tail: int, k_out, v_out,

@@ -1,8 +1,8 @@
 """Device plumbing around the C ABI: upload inputs, allocate outputs, run one eviction pass.
 
 Torch is used only for device memory and streams; every step of the pass is one of the library's
-entry points (kv_window_scores + kv_mu_sigma or kv_window_mu_sigma, kv_mmr_select,
-kv_compact_cache).
+entry points (kv_window_scores + kv_mu_sigma or kv_window_mu_sigma, kv_mmr_select or
+kv_mmr_select_ex, kv_compact_cache).
 """
 from __future__ import annotations
 
@@ -97,8 +97,12 @@ def allocate(inp: DeviceInputs, budget: int, cand_mult: int = 4, keep_tail: Opti
 
 
 def run_pass(inp: DeviceInputs, out: PassOutputs, budget: int, cand_mult: int = 4,
-             keep_tail: Optional[int] = None, fused: bool = True, stream=None) -> None:
-    """One whole eviction pass over the batch, enqueued on `stream` (default: current stream)."""
+             keep_tail: Optional[int] = None, fused: bool = True, pool: int = 1, w_mu: float = 1.0,
+             stream=None) -> None:
+    """One whole eviction pass over the batch, enqueued on `stream` (default: current stream).
+
+    pool / w_mu: scoring options of kv_mmr_select_ex (max-pool window, weight of mu); the
+    defaults are the paper's score and call kv_mmr_select."""
     b = inp.batch
     tail = b.w if keep_tail is None else keep_tail
     if fused and out.attn is None:
@@ -109,6 +113,12 @@ def run_pass(inp: DeviceInputs, out: PassOutputs, budget: int, cand_mult: int = 
                            stream)
         _lib.mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
                       out.sigma, out.attn, stream)
-    _lib.mmr_select(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2, budget, cand_mult,
-                    tail, out.sel_idx, out.sel_score, out.cand_idx, out.cand_corr, out.ws, stream)
+    if pool == 1 and w_mu == 1.0:
+        _lib.mmr_select(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2, budget, cand_mult,
+                        tail, out.sel_idx, out.sel_score, out.cand_idx, out.cand_corr, out.ws,
+                        stream)
+    else:
+        _lib.mmr_select_ex(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2, budget,
+                           cand_mult, tail, out.sel_idx, out.sel_score, out.cand_idx,
+                           out.cand_corr, out.ws, pool=pool, w_mu=w_mu, stream=stream)
     _lib.compact_cache(b, inp.k, inp.v, out.sel_idx, budget, tail, out.k_out, out.v_out, stream)

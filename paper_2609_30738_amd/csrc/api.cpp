@@ -16,6 +16,7 @@ namespace {
 constexpr int kMaxLen = 1 << 24;
 constexpr int kMaxGrid = 65535;
 constexpr int kMaxCompactBudget = 8192;
+constexpr int kMaxPool = 63;  // widest max-pool window of kv_mmr_select_ex
 constexpr size_t kWsAlign = 256;
 
 size_t align_up(size_t x) { return (x + kWsAlign - 1) & ~(kWsAlign - 1); }
@@ -207,12 +208,24 @@ int kv_mmr_select(const kv_problem* pr, const float* mu, const float* sigma, con
                   const float* lambda1, const float* lambda2, int32_t budget, int32_t cand_mult,
                   int32_t keep_tail, int32_t* sel_idx, float* sel_score, int32_t* cand_idx,
                   float* cand_corr, void* ws, size_t ws_bytes, void* stream) {
+  return kv_mmr_select_ex(pr, mu, sigma, k, lambda1, lambda2, budget, cand_mult, keep_tail, nullptr,
+                          sel_idx, sel_score, cand_idx, cand_corr, ws, ws_bytes, stream);
+}
+
+int kv_mmr_select_ex(const kv_problem* pr, const float* mu, const float* sigma, const void* k,
+                     const float* lambda1, const float* lambda2, int32_t budget, int32_t cand_mult,
+                     int32_t keep_tail, const kv_select_opts* opts, int32_t* sel_idx,
+                     float* sel_score, int32_t* cand_idx, float* cand_corr, void* ws,
+                     size_t ws_bytes, void* stream) {
   kv::Shape s;
   int st = check_problem(pr, &s);
   if (st != KV_OK) return st;
   if (!mu || !sigma || !k || !lambda1 || !lambda2 || !sel_idx) return KV_ERR_NULL;
   if (!aligned16(k)) return KV_ERR_ARG;
   if (cand_mult < 0) return KV_ERR_ARG;
+  const int32_t pool = opts ? opts->pool : 1;
+  const float w_mu = opts ? opts->w_mu : 1.f;
+  if (pool < 1 || pool > kMaxPool || pool % 2 == 0 || !std::isfinite(w_mu)) return KV_ERR_ARG;
   st = check_budget(pr, budget, keep_tail);
   if (st != KV_OK) return st;
   (void)ws;
@@ -225,6 +238,8 @@ int kv_mmr_select(const kv_problem* pr, const float* mu, const float* sigma, con
   a.k = k;
   a.lambda1 = lambda1;
   a.lambda2 = lambda2;
+  a.pool = pool;
+  a.w_mu = w_mu;
   a.budget = budget;
   a.cand_mult = cand_mult;
   a.keep_tail = keep_tail;

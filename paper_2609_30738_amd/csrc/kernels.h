@@ -69,6 +69,8 @@ struct SelectArgs {
   const void* k;
   const float* lambda1;
   const float* lambda2;
+  int pool;     // odd max-pool window over the candidate positions (1: none)
+  float w_mu;   // weight of mu in the base score (1: the paper's score)
   int budget, cand_mult, keep_tail, cand_stride, max_cand;
   int max_cand_all;  // max_p (L_p - keep_tail): every position that competes for a candidate slot
   int32_t* sel_idx;

@@ -2,7 +2,8 @@
 //
 // One workgroup per (problem, kv head): 1024 threads for bf16 keys (one candidate per thread), 256
 // for fp32 keys (up to four per thread, whose key rows need more registers):
-//   1. base scores s_i = fma(lambda1, sigma_i, mu_i) over the candidates [0, n_cand), their maximum
+//   1. base scores s_i = fma(lambda1, sigma_i, w_mu mu_i) over the candidates [0, n_cand) (optionally
+//      max-pooled over an odd window of positions, the outside of [0, n_cand) ignored), their maximum
 //      (the normaliser, clamped at 1e-12), and the C-th largest score by a most-significant-digit
 //      radix select over order-preserving 32-bit keys (4 passes of 8 bits, wave-private LDS
 //      histograms filled with LDS atomics); the keys are staged in LDS once with
@@ -195,7 +196,8 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
     const float* __restrict__ mu, const float* __restrict__ sigma,
     const typename Elem<DT>::T* __restrict__ k, const int32_t* __restrict__ lens,
     const int64_t* __restrict__ tok_off, const float* __restrict__ lambda1,
-    const float* __restrict__ lambda2, int h_kv, int budget, int cand_mult, int keep_tail,
+    const float* __restrict__ lambda2, int pool_h, float w_mu, int h_kv, int budget, int cand_mult,
+    int keep_tail,
     int cand_stride, int max_cand, int32_t* __restrict__ sel_idx, float* __restrict__ sel_score,
     int32_t* __restrict__ cand_idx, float* __restrict__ cand_corr) {
   using T = typename Elem<DT>::T;
@@ -229,7 +231,7 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
     // the first aligned index, then 4 per lane with several loads in flight
     const int head = (int)((4 - (base & 3)) & 3) < n_cand ? (int)((4 - (base & 3)) & 3) : n_cand;
     if (tid < head) {
-      const float sv = fmaf(lam1, sg_g[tid], mu_g[tid]);
+      const float sv = fmaf(lam1, sg_g[tid], w_mu * mu_g[tid]);
       local_max = fmaxf(local_max, sv);
       skeys[tid] = order_key(sv);
     }
@@ -239,8 +241,8 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
 #pragma unroll 4
     for (int v = tid; v < n4; v += kThreads) {
       const float4 m = mu4[v], sgv = sg4[v];
-      const float s0 = fmaf(lam1, sgv.x, m.x), s1 = fmaf(lam1, sgv.y, m.y);
-      const float s2 = fmaf(lam1, sgv.z, m.z), s3 = fmaf(lam1, sgv.w, m.w);
+      const float s0 = fmaf(lam1, sgv.x, w_mu * m.x), s1 = fmaf(lam1, sgv.y, w_mu * m.y);
+      const float s2 = fmaf(lam1, sgv.z, w_mu * m.z), s3 = fmaf(lam1, sgv.w, w_mu * m.w);
       local_max = fmaxf(fmaxf(local_max, fmaxf(s0, s1)), fmaxf(s2, s3));
       const int i = head + 4 * v;
       skeys[i] = order_key(s0);
@@ -249,17 +251,26 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
       skeys[i + 3] = order_key(s3);
     }
     for (int i = head + 4 * n4 + tid; i < n_cand; i += kThreads) {
-      const float sv = fmaf(lam1, sg_g[i], mu_g[i]);
+      const float sv = fmaf(lam1, sg_g[i], w_mu * mu_g[i]);
       local_max = fmaxf(local_max, sv);
       skeys[i] = order_key(sv);
     }
     __syncthreads();
   } else {
-    for (int i = tid; i < n_cand; i += kThreads) local_max = fmaxf(local_max, fmaf(lam1, sg_g[i], mu_g[i]));
+    for (int i = tid; i < n_cand; i += kThreads)
+      local_max = fmaxf(local_max, fmaf(lam1, sg_g[i], w_mu * mu_g[i]));
   }
-  auto key_at = [&](int i) -> uint32_t {
+  // key of the (pooled) score at position i; pooling keeps the maximum, which is also the maximum
+  // of the order-preserving keys
+  auto raw_key = [&](int i) -> uint32_t {
     if constexpr (STAGED) return skeys[i];
-    else return order_key(fmaf(lam1, sg_g[i], mu_g[i]));
+    else return order_key(fmaf(lam1, sg_g[i], w_mu * mu_g[i]));
+  };
+  auto key_at = [&](int i) -> uint32_t {
+    if (pool_h == 0) return raw_key(i);
+    uint32_t kmax = 0u;
+    for (int j = max(0, i - pool_h); j <= min(n_cand - 1, i + pool_h); ++j) kmax = max(kmax, raw_key(j));
+    return kmax;
   };
   {
     const float wm = wave_max_f(local_max);
@@ -401,7 +412,10 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
       const float n2 = key[q].sq_norm();
       inv[q] = n2 > 0.f ? 1.f / sqrtf(n2) : 0.f;  // a zero key has cosine 0 to everything
       cinv[c] = inv[q];
-      st[q] = fmaf(lam1, sg_g[pos], mu_g[pos]) / den;
+      float sv = fmaf(lam1, sg_g[pos], w_mu * mu_g[pos]);
+      for (int j = max(0, pos - pool_h); j <= min(n_cand - 1, pos + pool_h); ++j)
+        sv = fmaxf(sv, fmaf(lam1, sg_g[j], w_mu * mu_g[j]));
+      st[q] = sv / den;
     }
   }
   __syncthreads();
@@ -502,7 +516,8 @@ hipError_t select_launch(const Shape& s, const SelectArgs& a, hipStream_t st) {
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
   if (e != hipSuccess) return e;
   kern<<<dim3((unsigned)(s.n_prob * s.h_kv)), NT, dyn, st>>>(
-      a.mu, a.sigma, static_cast<const T*>(a.k), s.lens, s.tok_off, a.lambda1, a.lambda2, s.h_kv,
+      a.mu, a.sigma, static_cast<const T*>(a.k), s.lens, s.tok_off, a.lambda1, a.lambda2,
+      a.pool / 2, a.w_mu, s.h_kv,
       a.budget, a.cand_mult, a.keep_tail, a.cand_stride, a.max_cand, a.sel_idx, a.sel_score,
       a.cand_idx, a.cand_corr);
   return hipGetLastError();

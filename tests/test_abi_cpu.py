@@ -133,6 +133,23 @@ def test_budget_and_candidate_checks():
     assert _lib.lib().kv_candidate_stride(pr.ref(), 0, 4, 32) == 0
 
 
+def test_select_option_checks():
+    pr = HostProblem()
+
+    def sel_ex(pool, w_mu, budget=64):
+        opts = _lib.KvSelectOpts(pool, w_mu)
+        return _lib.lib().kv_mmr_select_ex(pr.ref(), P, P, P, P, P, budget, 4, 32,
+                                           ctypes.byref(opts), P, NULL, NULL, NULL, NULL, 0, NULL)
+    for pool in (0, -1, 2, 8, 65):
+        assert sel_ex(pool, 1.0) == _lib.KV_ERR_ARG, pool
+    assert sel_ex(3, float("nan")) == _lib.KV_ERR_ARG
+    assert sel_ex(3, float("inf")) == _lib.KV_ERR_ARG
+    # valid options, invalid budget: the budget check still answers (nothing is launched)
+    assert sel_ex(63, 0.0, budget=0) == _lib.KV_ERR_BUDGET
+    assert _lib.lib().kv_mmr_select_ex(pr.ref(), P, P, P, P, P, 0, 4, 32, None, P, NULL, NULL,
+                                       NULL, NULL, 0, NULL) == _lib.KV_ERR_BUDGET
+
+
 # ------------------------------------------------------------------------------------------------
 # depth profiles (host-only entry point) against the oracle
 # ------------------------------------------------------------------------------------------------

@@ -105,6 +105,34 @@ def test_rising_logits_move_the_running_offset(fused):
     _all(gpu_cases.run_gpu(wl, fused=fused, packed=pk))
 
 
+@pytest.mark.parametrize("pool", [3, 7, 31])
+def test_max_pooled_scores(pool):
+    """kv_mmr_select_ex with a max-pool over positions (the window stops at the end of the
+    candidate range): two ragged sequences x 2 layers, B=64."""
+    wl = workloads.ragged_batch("both", n_seq=2, n_layers=2, len_range=(700, 3100))
+    wl.budget = 64
+    _all(gpu_cases.run_gpu(wl, fused=True, pool=pool))
+
+
+def test_max_pooled_scores_fp32_keep_all():
+    """fp32 keys (256-thread select), every position a candidate (keep_tail = 0) and pool 5."""
+    _all(gpu_cases.run_gpu(workloads.tiny_f32(), fused=True, keep_tail=0, pool=5))
+
+
+@pytest.mark.parametrize("lam_run", ["dispersion_only", "both"])
+def test_mean_free_score(lam_run):
+    """w_mu = 0: the score without the mean term (dispersion and redundancy only)."""
+    wl = workloads.ragged_batch(lam_run, n_seq=2, n_layers=2, len_range=(700, 3100))
+    _all(gpu_cases.run_gpu(wl, fused=True, w_mu=0.0))
+
+
+def test_mean_free_max_pooled_unfused():
+    """w_mu = 0.5 and pool 9 together, through the two-call scoring path."""
+    wl = workloads.mistral_layer()
+    wl.seq_lens = [3000]
+    _all(gpu_cases.run_gpu(wl, fused=False, w_mu=0.5, pool=9))
+
+
 def test_compaction_of_oracle_selection():
     """kv_compact_cache fed with the oracle's admissions reproduces the oracle's compacted rows."""
     import torch
