@@ -13,7 +13,9 @@ fixed by a clear margin from a near-tie where several answers are correct.
 Readings of points the paper leaves open (each used below where it applies):
   R1  grouped-query attention: the G query heads that share a kv head are averaged,
       a[r, i] = mean_h A[h, r, i]; the mean (Eq. (1)) and the sample standard deviation (Eq. (3)) are
-      then taken over the W window rows, and selection is per kv head.
+      then taken over the W window rows, and selection is per kv head.  The other reading (R1b,
+      all_rows=True below) takes the mean and the sample standard deviation over all G W
+      (head, row) attention values of the group; the mean is the same under both readings.
   R2  causal mask: window row r sits at position L - W + r and attends to keys 0 .. L - W + r.
   R3  the softmax scale is an explicit argument (1/sqrt(d) for scaled dot-product attention).
   R4  candidates are the positions [0, L - keep_tail); the last keep_tail positions (the window by
@@ -87,14 +89,21 @@ def window_attention(logits: np.ndarray) -> np.ndarray:
     return np.exp(logits - m[..., None]) / z[..., None]
 
 
-def token_statistics(attn: np.ndarray, h_kv: int):
-    """Mean mu_i (Eq. (1)) and sample dispersion sigma_i (Eq. (3)) per kv head, following R1.
+def token_statistics(attn: np.ndarray, h_kv: int, all_rows: bool = False):
+    """Mean mu_i (Eq. (1)) and sample dispersion sigma_i (Eq. (3)) per kv head, following R1
+    (all_rows=False) or R1b (all_rows=True).
 
-    attn [h_q, W, L] -> mu, sigma [h_kv, L].  sigma divides by W - 1 and is computed in two passes
-    (mean first, then the squared deviations from it).
+    attn [h_q, W, L] -> mu, sigma [h_kv, L].  sigma divides by n - 1 (n = W, or G W under R1b) and
+    is computed in two passes (mean first, then the squared deviations from it).
     """
     h_q, w, L = attn.shape
     group = h_q // h_kv
+    if all_rows:
+        x = attn.reshape(h_kv, group * w, L)
+        n = group * w
+        mu = x.sum(axis=1) / n
+        dev = x - mu[:, None, :]
+        return mu, np.sqrt((dev * dev).sum(axis=1) / (n - 1))
     a = attn.reshape(h_kv, group, w, L).sum(axis=1) / group
     mu = a.sum(axis=1) / w
     dev = a - mu[:, None, :]
@@ -275,12 +284,13 @@ def select_head(mu_g: np.ndarray, sigma_g: np.ndarray, k_g: np.ndarray, lam1: fl
 
 def evict_problem(q_win, k, v, dtype: str, scale: float, lam1: float, lam2: float, budget: int,
                   cand_mult: int = 4, keep_tail: Optional[int] = None, heads=None,
-                  want_attn: bool = False, pool: int = 1, w_mu: float = 1.0) -> ProblemResult:
+                  want_attn: bool = False, pool: int = 1, w_mu: float = 1.0,
+                  sigma_all_rows: bool = False) -> ProblemResult:
     """Whole path for one problem (one layer of one sequence).
 
     q_win [h_q, W, d], k and v [h_kv, L, d] as stored (fp32 or bf16 bits).  `heads` restricts the
     selection to some kv heads (statistics are still returned for all of them).  pool / w_mu:
-    see max_pool and base_scores.
+    see max_pool and base_scores; sigma_all_rows: the R1b reading of token_statistics.
     """
     qd = decode(q_win, dtype)
     kd = decode(k, dtype)
@@ -301,7 +311,7 @@ def evict_problem(q_win, k, v, dtype: str, scale: float, lam1: float, lam2: floa
         a = window_attention(lg)
         if want_attn:
             attn[hs] = a
-        mu[g:g + 1], sigma[g:g + 1] = token_statistics(a, 1)
+        mu[g:g + 1], sigma[g:g + 1] = token_statistics(a, 1, sigma_all_rows)
     sel_heads = range(h_kv) if heads is None else heads
     results = []
     for g in range(h_kv):

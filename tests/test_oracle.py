@@ -127,6 +127,50 @@ def test_gqa_identical_group_heads_reduce_to_single_head():
     np.testing.assert_allclose(grouped[1], single[1], rtol=1e-12)
 
 
+def test_all_rows_dispersion_against_statistics_module():
+    """Reading R1b: the mean and the sample standard deviation over all G W (head, row) values."""
+    rng = np.random.default_rng(31)
+    attn = rng.random((6, 5, 7))  # 6 query heads, 5 rows, 7 tokens; 3 kv heads of 2
+    mu, sigma = evict.token_statistics(attn, 3, all_rows=True)
+    for g in range(3):
+        for i in range(7):
+            vals = [attn[h, r, i] for h in (2 * g, 2 * g + 1) for r in range(5)]
+            assert mu[g, i] == pytest.approx(statistics.mean(vals), rel=1e-13)
+            assert sigma[g, i] == pytest.approx(statistics.stdev(vals), rel=1e-11)
+
+
+def test_all_rows_dispersion_single_head_and_identical_heads():
+    """G = 1: both readings coincide.  G identical heads: the sum of squared deviations over the
+    G W values is G times the one over W rows, so sigma_all^2 (G W - 1) = G (W - 1) sigma^2, and
+    the means agree."""
+    q1 = _rand((1, 6, 8), 32)
+    k = _rand((1, 30, 8), 33, 2.0)
+    a1 = evict.window_attention(evict.window_logits(q1, k, 0.35))
+    np.testing.assert_array_equal(evict.token_statistics(a1, 1, all_rows=True)[1],
+                                  evict.token_statistics(a1, 1)[1])
+    G, w = 4, 6
+    a4 = evict.window_attention(evict.window_logits(np.repeat(q1, G, axis=0), k, 0.35))
+    mu_g, sg_g = evict.token_statistics(a4, 1)
+    mu_a, sg_a = evict.token_statistics(a4, 1, all_rows=True)
+    np.testing.assert_allclose(mu_a, mu_g, rtol=1e-14)
+    np.testing.assert_allclose(sg_a ** 2 * (G * w - 1), G * (w - 1) * sg_g ** 2, rtol=1e-12)
+
+
+def test_all_rows_dispersion_law_of_total_variance():
+    """sum_{h,r} (A - mu)^2 = sum_{h,r} (A_hr - a_r)^2 + G sum_r (a_r - mu)^2 with a_r the group
+    mean of row r: ties the two readings together on unequal heads."""
+    q = _rand((4, 5, 8), 34)
+    k = _rand((1, 25, 8), 35, 2.0)
+    attn = evict.window_attention(evict.window_logits(q, k, 0.4))
+    G, w = 4, 5
+    _, sg_g = evict.token_statistics(attn, 1)
+    _, sg_a = evict.token_statistics(attn, 1, all_rows=True)
+    a_r = attn.mean(axis=0)
+    within = ((attn - a_r[None]) ** 2).sum(axis=(0, 1))
+    np.testing.assert_allclose(sg_a[0] ** 2 * (G * w - 1), within + G * (w - 1) * sg_g[0] ** 2,
+                               rtol=1e-11)
+
+
 def test_causal_mask_window_tokens():
     """Window row r sees keys up to L - W + r (reading R2): the last key gets attention only from
     the last row, so its mean is A[last row, L-1] / W."""
