@@ -128,6 +128,28 @@ int kv_window_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, f
                        float* row_max, float* row_sum, float* mu, float* sigma, void* ws,
                        size_t ws_bytes, void* stream);
 
+/* Which window values the dispersion sigma of kv_mu_sigma_ex / kv_window_mu_sigma_ex runs over.
+ * The paper defines Eq. (3) for one attention head and does not say how the G query heads that
+ * share a kv head enter it:
+ *   KV_SIGMA_GROUP_MEAN: the w rows of the group-mean attention a[r,i] = mean_h A[h,r,i], divisor
+ *     w - 1 (the reading kv_mu_sigma and kv_window_mu_sigma use);
+ *   KV_SIGMA_ALL_ROWS: all G w values A[h,r,i] of the group, divisor G w - 1.
+ * mu is the same under both; for G = 1 so is sigma. */
+#define KV_SIGMA_GROUP_MEAN 0
+#define KV_SIGMA_ALL_ROWS 1
+
+/* kv_mu_sigma with the dispersion taken over `sigma_rows` (KV_SIGMA_*; any other value returns
+ * KV_ERR_ARG).  Every other argument, output and rule as in kv_mu_sigma. */
+int kv_mu_sigma_ex(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                   const float* row_max, const float* row_sum, int32_t sigma_rows, float* mu,
+                   float* sigma, float* attn, void* stream);
+
+/* kv_window_mu_sigma with the dispersion taken over `sigma_rows` (KV_SIGMA_*; any other value
+ * returns KV_ERR_ARG).  Every other argument, output and rule as in kv_window_mu_sigma. */
+int kv_window_mu_sigma_ex(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                          int32_t sigma_rows, float* row_max, float* row_sum, float* mu,
+                          float* sigma, void* ws, size_t ws_bytes, void* stream);
+
 /* Greedy diversity-aware selection (Eq. (2), (4), (5); section 3.2), per problem p and kv head g:
  *   candidates i in [0, n_cand), n_cand = L_p - keep_tail (the last keep_tail positions are always
  *   kept and never compete);

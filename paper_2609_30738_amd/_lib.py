@@ -22,6 +22,10 @@ KV_ERR_WORKSPACE = -5
 KV_ERR_LAUNCH = -6
 KV_ERR_ARG = -7
 
+KV_SIGMA_GROUP_MEAN = 0
+KV_SIGMA_ALL_ROWS = 1
+SIGMA_ROWS = {"group_mean": KV_SIGMA_GROUP_MEAN, "all_rows": KV_SIGMA_ALL_ROWS}
+
 KV_F32 = 0
 KV_BF16 = 1
 
@@ -34,8 +38,9 @@ PROFILE_FAMILIES = {"global": KV_PROFILE_GLOBAL, "segments": KV_PROFILE_SEGMENTS
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvevict.so")
 
 SYMBOLS = ("kv_strerror", "kv_version", "kv_workspace_bytes", "kv_candidate_stride",
-           "kv_window_scores", "kv_mu_sigma", "kv_window_mu_sigma", "kv_mmr_select",
-           "kv_mmr_select_ex", "kv_compact_cache", "kv_depth_profile")
+           "kv_window_scores", "kv_mu_sigma", "kv_mu_sigma_ex", "kv_window_mu_sigma",
+           "kv_window_mu_sigma_ex", "kv_mmr_select", "kv_mmr_select_ex", "kv_compact_cache",
+           "kv_depth_profile")
 
 
 class KvError(RuntimeError):
@@ -78,6 +83,9 @@ def lib() -> ctypes.CDLL:
         h.kv_window_scores.argtypes = [pr, vp, vp, ctypes.c_float, vp, vp, vp, sz, vp]
         h.kv_mu_sigma.argtypes = [pr, vp, vp, ctypes.c_float, vp, vp, vp, vp, vp, vp]
         h.kv_window_mu_sigma.argtypes = [pr, vp, vp, ctypes.c_float, vp, vp, vp, vp, vp, sz, vp]
+        h.kv_mu_sigma_ex.argtypes = [pr, vp, vp, ctypes.c_float, vp, vp, i32, vp, vp, vp, vp]
+        h.kv_window_mu_sigma_ex.argtypes = [pr, vp, vp, ctypes.c_float, i32, vp, vp, vp, vp, vp,
+                                            sz, vp]
         h.kv_mmr_select.argtypes = [pr, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, sz,
                                     vp]
         h.kv_mmr_select_ex.argtypes = [pr, vp, vp, vp, vp, vp, i32, i32, i32,
@@ -85,8 +93,9 @@ def lib() -> ctypes.CDLL:
         h.kv_compact_cache.argtypes = [pr, vp, vp, vp, i32, i32, vp, vp, vp]
         h.kv_depth_profile.argtypes = [i32, ctypes.POINTER(ctypes.c_double), i32, i32,
                                        ctypes.POINTER(ctypes.c_float)]
-        for name in ("kv_window_scores", "kv_mu_sigma", "kv_window_mu_sigma", "kv_mmr_select",
-                     "kv_mmr_select_ex", "kv_compact_cache", "kv_depth_profile"):
+        for name in ("kv_window_scores", "kv_mu_sigma", "kv_mu_sigma_ex", "kv_window_mu_sigma",
+                     "kv_window_mu_sigma_ex", "kv_mmr_select", "kv_mmr_select_ex",
+                     "kv_compact_cache", "kv_depth_profile"):
             getattr(h, name).restype = ctypes.c_int
         _LIB = h
     return _LIB
@@ -190,6 +199,28 @@ def window_mu_sigma(batch: Batch, q_win, k, scale: float, row_max, row_sum, mu, 
                                     _ptr(row_max), _ptr(row_sum), _ptr(mu), _ptr(sigma), _ptr(ws),
                                     0 if ws is None else ws.numel() * ws.element_size(),
                                     _stream(stream)), "kv_window_mu_sigma")
+
+
+def _sigma_rows(sigma_rows) -> int:
+    return SIGMA_ROWS[sigma_rows] if isinstance(sigma_rows, str) else int(sigma_rows)
+
+
+def mu_sigma_ex(batch: Batch, q_win, k, scale: float, row_max, row_sum, sigma_rows, mu, sigma,
+                attn=None, stream=None) -> None:
+    """kv_mu_sigma_ex; sigma_rows is "group_mean", "all_rows" or a KV_SIGMA_* value."""
+    _check(lib().kv_mu_sigma_ex(batch.ref(), _ptr(q_win), _ptr(k), float(scale), _ptr(row_max),
+                                _ptr(row_sum), _sigma_rows(sigma_rows), _ptr(mu), _ptr(sigma),
+                                _ptr(attn), _stream(stream)), "kv_mu_sigma_ex")
+
+
+def window_mu_sigma_ex(batch: Batch, q_win, k, scale: float, sigma_rows, row_max, row_sum, mu,
+                       sigma, ws, stream=None) -> None:
+    """kv_window_mu_sigma_ex; sigma_rows is "group_mean", "all_rows" or a KV_SIGMA_* value."""
+    _check(lib().kv_window_mu_sigma_ex(batch.ref(), _ptr(q_win), _ptr(k), float(scale),
+                                       _sigma_rows(sigma_rows), _ptr(row_max), _ptr(row_sum),
+                                       _ptr(mu), _ptr(sigma), _ptr(ws),
+                                       0 if ws is None else ws.numel() * ws.element_size(),
+                                       _stream(stream)), "kv_window_mu_sigma_ex")
 
 
 def mmr_select(batch: Batch, mu, sigma, k, lambda1, lambda2, budget: int, cand_mult: int,

@@ -98,21 +98,31 @@ def allocate(inp: DeviceInputs, budget: int, cand_mult: int = 4, keep_tail: Opti
 
 def run_pass(inp: DeviceInputs, out: PassOutputs, budget: int, cand_mult: int = 4,
              keep_tail: Optional[int] = None, fused: bool = True, pool: int = 1, w_mu: float = 1.0,
-             stream=None) -> None:
+             sigma_rows: str = "group_mean", stream=None) -> None:
     """One whole eviction pass over the batch, enqueued on `stream` (default: current stream).
 
-    pool / w_mu: scoring options of kv_mmr_select_ex (max-pool window, weight of mu); the
-    defaults are the paper's score and call kv_mmr_select."""
+    pool / w_mu: scoring options of kv_mmr_select_ex (max-pool window, weight of mu);
+    sigma_rows: the dispersion reading of kv_mu_sigma_ex / kv_window_mu_sigma_ex.  The defaults
+    call the plain entry points."""
     b = inp.batch
     tail = b.w if keep_tail is None else keep_tail
+    plain = sigma_rows == "group_mean"
     if fused and out.attn is None:
-        _lib.window_mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
-                             out.sigma, out.ws, stream)
+        if plain:
+            _lib.window_mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
+                                 out.sigma, out.ws, stream)
+        else:
+            _lib.window_mu_sigma_ex(b, inp.q_win, inp.k, inp.scale, sigma_rows, out.row_max,
+                                    out.row_sum, out.mu, out.sigma, out.ws, stream)
     else:
         _lib.window_scores(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.ws,
                            stream)
-        _lib.mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
-                      out.sigma, out.attn, stream)
+        if plain:
+            _lib.mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
+                          out.sigma, out.attn, stream)
+        else:
+            _lib.mu_sigma_ex(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, sigma_rows,
+                             out.mu, out.sigma, out.attn, stream)
     if pool == 1 and w_mu == 1.0:
         _lib.mmr_select(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2, budget, cand_mult,
                         tail, out.sel_idx, out.sel_score, out.cand_idx, out.cand_corr, out.ws,

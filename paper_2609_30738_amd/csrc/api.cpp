@@ -161,30 +161,48 @@ int kv_window_scores(const kv_problem* pr, const void* q_win, const void* k, flo
 int kv_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float scale,
                 const float* row_max, const float* row_sum, float* mu, float* sigma, float* attn,
                 void* stream) {
+  return kv_mu_sigma_ex(pr, q_win, k, scale, row_max, row_sum, KV_SIGMA_GROUP_MEAN, mu, sigma,
+                        attn, stream);
+}
+
+int kv_mu_sigma_ex(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                   const float* row_max, const float* row_sum, int32_t sigma_rows, float* mu,
+                   float* sigma, float* attn, void* stream) {
   kv::Shape s;
   int st = check_problem(pr, &s);
   if (st != KV_OK) return st;
   if (!q_win || !k || !row_max || !row_sum || !mu || !sigma) return KV_ERR_NULL;
   if (!aligned16(q_win) || !aligned16(k)) return KV_ERR_ARG;
   if (!std::isfinite(scale)) return KV_ERR_ARG;
+  if (sigma_rows != KV_SIGMA_GROUP_MEAN && sigma_rows != KV_SIGMA_ALL_ROWS) return KV_ERR_ARG;
+  const bool all = sigma_rows == KV_SIGMA_ALL_ROWS;
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (kv::stream_shape_ok(s, scale) && !attn)
     return launch_status(kv::launch_stream_mu_sigma(s, stream_plan_of(pr, s), q_win, k, scale,
                                                     nullptr, row_max, row_sum, nullptr, nullptr,
-                                                    mu, sigma, hs));
+                                                    mu, sigma, all, hs));
   return launch_status(kv::launch_mu_sigma(s, q_win, k, scale, row_max, row_sum, mu, sigma, attn,
-                                           hs));
+                                           all, hs));
 }
 
 int kv_window_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float scale,
                        float* row_max, float* row_sum, float* mu, float* sigma, void* ws,
                        size_t ws_bytes, void* stream) {
+  return kv_window_mu_sigma_ex(pr, q_win, k, scale, KV_SIGMA_GROUP_MEAN, row_max, row_sum, mu,
+                               sigma, ws, ws_bytes, stream);
+}
+
+int kv_window_mu_sigma_ex(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                          int32_t sigma_rows, float* row_max, float* row_sum, float* mu,
+                          float* sigma, void* ws, size_t ws_bytes, void* stream) {
   kv::Shape s;
   int st = check_problem(pr, &s);
   if (st != KV_OK) return st;
   if (!q_win || !k || !row_max || !row_sum || !mu || !sigma) return KV_ERR_NULL;
   if (!aligned16(q_win) || !aligned16(k)) return KV_ERR_ARG;
   if (!std::isfinite(scale)) return KV_ERR_ARG;
+  if (sigma_rows != KV_SIGMA_GROUP_MEAN && sigma_rows != KV_SIGMA_ALL_ROWS) return KV_ERR_ARG;
+  const bool all = sigma_rows == KV_SIGMA_ALL_ROWS;
   if (ws_bytes < window_ws_bytes(pr, s) || !ws ||
       (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1)))
     return KV_ERR_WORKSPACE;
@@ -195,13 +213,13 @@ int kv_window_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, f
     st = launch_status(kv::launch_stream_stats(s, plan, q_win, k, scale, ws, hs));
     if (st != KV_OK) return st;
     return launch_status(kv::launch_stream_mu_sigma(s, plan, q_win, k, scale, ws, nullptr,
-                                                    nullptr, row_max, row_sum, mu, sigma, hs));
+                                                    nullptr, row_max, row_sum, mu, sigma, all, hs));
   }
   // other shapes: chunked row statistics, then a second pass over K
   st = launch_status(kv::launch_window_stats(s, q_win, k, scale, ws, row_max, row_sum, hs));
   if (st != KV_OK) return st;
   return launch_status(kv::launch_mu_sigma(s, q_win, k, scale, row_max, row_sum, mu, sigma,
-                                           nullptr, hs));
+                                           nullptr, all, hs));
 }
 
 int kv_mmr_select(const kv_problem* pr, const float* mu, const float* sigma, const void* k,

@@ -34,7 +34,7 @@ hipError_t launch_window_stats(const Shape& s, const void* q_win, const void* k,
 
 hipError_t launch_mu_sigma(const Shape& s, const void* q_win, const void* k, float scale,
                            const float* row_max, const float* row_sum, float* mu, float* sigma,
-                           float* attn, hipStream_t stream);
+                           float* attn, bool sigma_all, hipStream_t stream);
 
 // Streaming two-pass row statistics + mu/sigma (bf16, w = 32, G in {1, 2, 4}, scale > 0): every
 // unit is cut
@@ -57,7 +57,7 @@ hipError_t launch_stream_mu_sigma(const Shape& s, const StreamPlan& plan, const 
                                   const void* k, float scale, const void* ws,
                                   const float* row_max_in, const float* row_sum_in,
                                   float* row_max_out, float* row_sum_out, float* mu, float* sigma,
-                                  hipStream_t stream);
+                                  bool sigma_all, hipStream_t stream);
 // row_max / row_sum from chunk partials [n_units][max_chunks][rows_pad] of chunk_keys keys each.
 hipError_t launch_combine_partials(const Shape& s, const void* part, int chunk_keys,
                                    int max_chunks, int rows_pad, float* row_max, float* row_sum,

@@ -19,7 +19,9 @@
 //     b = M + log2 Z (segment 0 also writes row_max / row_sum), or takes them from given
 //     row_max / row_sum; then logits again with keys as N (a lane holds one key),
 //     a = 2^(t - b) summed over the group's heads, the mean and the two-pass sample variance over
-//     the 32 window rows, stored as mu / sigma.
+//     the 32 window rows, stored as mu / sigma.  With `sigma_all` the variance runs over all G x 32
+//     (head, row) values instead: every head's mean and squared deviations over its 32 rows, merged
+//     across heads with the pairwise update of Chan, Golub and LeVeque.
 #include <algorithm>
 #include <type_traits>
 
@@ -51,6 +53,7 @@ struct StreamArgs {
   float* row_sum_out;
   float* mu;
   float* sigma;
+  int sigma_all;          // pass 2: dispersion over all G x 32 (head, row) values
 };
 
 template <int D, int NB> struct SGeo {
@@ -233,7 +236,7 @@ __global__ __launch_bounds__(kThreads, 1) void stats_stream_kernel(StreamArgs a)
 // ------------------------------------------------------------------------------------------------
 // Pass 2
 // ------------------------------------------------------------------------------------------------
-template <int D, int NB>
+template <int D, int NB, bool ALL>
 __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs a) {
   using Gm = SGeo<D, NB>;
   constexpr int R = Gm::R, NS = Gm::NS;
@@ -289,9 +292,11 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
     float ab[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) ab[j] = 0.f;
+    float h_mean = 0.f, h_m2 = 0.f;  // ALL: running mean and squared deviations of the heads so far
     auto accumulate = [&](auto masked) __attribute__((always_inline)) {
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
+        float eb[16];
         bf16x8_t qf[NS];
         read_qfrags<D, NB>(qf, qs, b, l32, half);
         f32x16_t d = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -308,6 +313,28 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
             float e = __builtin_amdgcn_exp2f(fmaf(d[j], c, -bb[u]));
             if (decltype(masked)::value && 8 * q + u < thr) e = 0.f;
             ab[j] += e;
+            eb[j] = e;
+          }
+        }
+        if constexpr (ALL) {
+          float hs[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int j = 0; j < 16; ++j) hs[j & 3] += eb[j];
+          const float mb = sum_halves((hs[0] + hs[1]) + (hs[2] + hs[3])) * (1.f / 32.f);
+          float hv[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            const float dl = eb[j] - mb;
+            hv[j & 3] = fmaf(dl, dl, hv[j & 3]);
+          }
+          const float m2b = sum_halves((hv[0] + hv[1]) + (hv[2] + hv[3]));
+          if (b == 0) {
+            h_mean = mb;
+            h_m2 = m2b;
+          } else {  // b heads of 32 rows merged with one more
+            const float dl = mb - h_mean;
+            h_mean = fmaf(dl, 1.f / (float)(b + 1), h_mean);
+            h_m2 += fmaf(dl * dl, 32.f * (float)b / (float)(b + 1), m2b);
           }
         }
         __builtin_amdgcn_sched_barrier(0);  // one head at a time, as in pass 1
@@ -320,13 +347,18 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
 #pragma unroll
     for (int u = 0; u < 4; ++u) sp[u] = (ab[u] + ab[u + 4]) + (ab[u + 8] + ab[u + 12]);
     const float mean = sum_halves((sp[0] + sp[1]) + (sp[2] + sp[3])) * (inv_g * (1.f / 32.f));
-    float vp[4] = {0.f, 0.f, 0.f, 0.f};
+    float var;
+    if constexpr (ALL) {
+      var = h_m2 * (1.f / (float)(NB * 32 - 1));
+    } else {
+      float vp[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const float dl = fmaf(ab[j], inv_g, -mean);
-      vp[j & 3] = fmaf(dl, dl, vp[j & 3]);
+      for (int j = 0; j < 16; ++j) {
+        const float dl = fmaf(ab[j], inv_g, -mean);
+        vp[j & 3] = fmaf(dl, dl, vp[j & 3]);
+      }
+      var = sum_halves((vp[0] + vp[1]) + (vp[2] + vp[3])) * (1.f / 31.f);
     }
-    const float var = sum_halves((vp[0] + vp[1]) + (vp[2] + vp[3])) * (1.f / 31.f);
     if (key < k1) (half == 0 ? a.mu : a.sigma)[stat_base + key] = half == 0 ? mean : __builtin_amdgcn_sqrtf(var);
   };
 
@@ -349,7 +381,8 @@ hipError_t stream_dispatch(const Shape& s, const StreamArgs& args, bool pass1, h
   const int max_segs = args.max_segs;
   const dim3 grid(max_segs, s.h_kv, s.n_prob);
   if (pass1) stats_stream_kernel<D, NB><<<grid, kThreads, 0, st>>>(args);
-  else mu_sigma_stream_kernel<D, NB><<<grid, kThreads, 0, st>>>(args);
+  else if (args.sigma_all) mu_sigma_stream_kernel<D, NB, true><<<grid, kThreads, 0, st>>>(args);
+  else mu_sigma_stream_kernel<D, NB, false><<<grid, kThreads, 0, st>>>(args);
   return hipGetLastError();
 }
 
@@ -416,7 +449,7 @@ hipError_t launch_stream_mu_sigma(const Shape& s, const StreamPlan& plan, const 
                                   const void* k, float scale, const void* ws,
                                   const float* row_max_in, const float* row_sum_in,
                                   float* row_max_out, float* row_sum_out, float* mu, float* sigma,
-                                  hipStream_t stream) {
+                                  bool sigma_all, hipStream_t stream) {
   StreamArgs a = base_args(s, plan, q_win, k, scale);
   a.part = const_cast<float2*>(static_cast<const float2*>(ws));
   a.row_max = row_max_in;
@@ -425,6 +458,7 @@ hipError_t launch_stream_mu_sigma(const Shape& s, const StreamPlan& plan, const 
   a.row_sum_out = row_sum_out;
   a.mu = mu;
   a.sigma = sigma;
+  a.sigma_all = sigma_all ? 1 : 0;
   return stream_launch(s, a, false, stream);
 }
 

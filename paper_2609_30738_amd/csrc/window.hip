@@ -13,6 +13,7 @@
 //     lane and M block), A = 2^(t - b) with b = row_max*log2(e) + log2(row_sum); for w = 32 every
 //     M block is one query head, so the group mean, the mean over the window and the two-pass sample
 //     variance are in-lane sums plus one exchange with lane ^ 32.  Other windows reduce through LDS.
+//     With `sigma_all` the variance runs over all G w (head, row) values of the group.
 #include "common.h"
 #include "kernels.h"
 
@@ -169,7 +170,7 @@ __global__ __launch_bounds__(kThreads) void combine_stats_kernel(
 // ------------------------------------------------------------------------------------------------
 // Pass 2: attention, group mean, mean and sample dispersion over the window
 // ------------------------------------------------------------------------------------------------
-template <int DT, int D, int NB, bool W32>
+template <int DT, int D, int NB, bool W32, bool ALL>
 __global__ __launch_bounds__(kThreads) void mu_sigma_kernel(
     const typename Elem<DT>::T* __restrict__ q_win, const typename Elem<DT>::T* __restrict__ k,
     const int32_t* __restrict__ lens, const int64_t* __restrict__ tok_off, int h_q, int h_kv, int w,
@@ -223,11 +224,13 @@ __global__ __launch_bounds__(kThreads) void mu_sigma_kernel(
     float abar[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) abar[j] = 0.f;
+    float h_mean = 0.f, h_m2 = 0.f;  // W32 && ALL: running mean / squared deviations over heads
 #pragma unroll 1
     for (int b = 0; b < NB; ++b) {
       Frags<DT, D> qf;
       qf.load_lds(q_lds + (b * 32 + l32) * PITCH, half);
       const f32x16_t acc = mfma_tile<DT, D>(qf, kf);  // D[row][key]
+      float ah[16];
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const int m = b * 32 + acc_row(j, lane);
@@ -240,7 +243,26 @@ __global__ __launch_bounds__(kThreads) void mu_sigma_kernel(
           abar[j] += a;
         else
           red[wave][m][l32] = a;  // every (row, key) of the tile is held by exactly one lane
+        ah[j] = a;
         if (attn_g && key_ok && m < R) attn_g[(size_t)m * L + key] = a;
+      }
+      if constexpr (W32 && ALL) {
+        // head b (rows b*32 .. b*32+31, all real when b < G) merged into the running moments with
+        // the pairwise update of Chan, Golub and LeVeque
+        if (b < G) {
+          float hs = 0.f;
+#pragma unroll
+          for (int j = 0; j < 16; ++j) hs += ah[j];
+          const float mb = (hs + swap_halves(hs)) * (1.f / 32.f);
+          float hv = 0.f;
+#pragma unroll
+          for (int j = 0; j < 16; ++j) hv = fmaf(ah[j] - mb, ah[j] - mb, hv);
+          const float m2b = hv + swap_halves(hv);
+          const float dl = mb - h_mean;
+          const float fb = (float)b;
+          h_mean = fmaf(dl, 1.f / (fb + 1.f), h_mean);
+          h_m2 += fmaf(dl * dl, 32.f * fb / (fb + 1.f), m2b);
+        }
       }
     }
     if constexpr (W32) {
@@ -259,6 +281,7 @@ __global__ __launch_bounds__(kThreads) void mu_sigma_kernel(
         v += dlt * dlt;
       }
       v = (v + swap_halves(v)) * inv_w1;
+      if constexpr (ALL) v = h_m2 / (float)(R - 1);
       if (half == 0 && key_ok) {
         mu[stat_base + key] = mean;
         sigma[stat_base + key] = sqrtf(v);
@@ -268,7 +291,18 @@ __global__ __launch_bounds__(kThreads) void mu_sigma_kernel(
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      if (half == 0 && key_ok) {
+      if (ALL && half == 0 && key_ok) {
+        float s = 0.f;
+        for (int m = 0; m < R; ++m) s += red[wave][m][l32];
+        const float mean = s / (float)R;
+        float v = 0.f;
+        for (int m = 0; m < R; ++m) {
+          const float dlt = red[wave][m][l32] - mean;
+          v += dlt * dlt;
+        }
+        mu[stat_base + key] = mean;
+        sigma[stat_base + key] = sqrtf(v / (float)(R - 1));
+      } else if (half == 0 && key_ok) {
         float s = 0.f;
         for (int r = 0; r < w; ++r) {
           float ab = 0.f;
@@ -323,10 +357,11 @@ hipError_t stats_dispatch(const Shape& s, const void* q, const void* k, float sc
 template <int DT, int D, int NB, bool W32>
 hipError_t mu_sigma_dispatch(const Shape& s, const void* q, const void* k, float scale,
                              const float* row_max, const float* row_sum, float* mu,
-                             float* sigma, float* attn, hipStream_t st) {
+                             float* sigma, float* attn, bool all, hipStream_t st) {
   using T = typename Elem<DT>::T;
   const dim3 grid(s.max_chunks(), s.h_kv, s.n_prob);
-  mu_sigma_kernel<DT, D, NB, W32><<<grid, kThreads, 0, st>>>(
+  auto kern = all ? mu_sigma_kernel<DT, D, NB, W32, true> : mu_sigma_kernel<DT, D, NB, W32, false>;
+  kern<<<grid, kThreads, 0, st>>>(
       static_cast<const T*>(q), static_cast<const T*>(k), s.lens, s.tok_off, s.h_q, s.h_kv, s.w,
       scale * kLog2e, kWindowChunk, row_max, row_sum, mu, sigma, attn);
   return hipGetLastError();
@@ -345,17 +380,18 @@ hipError_t stats_nb(const Shape& s, const void* q, const void* k, float scale, v
 template <int DT, int D>
 hipError_t mu_sigma_nb(const Shape& s, const void* q, const void* k, float scale,
                        const float* rm, const float* rs, float* mu, float* sg, float* attn,
-                       hipStream_t st) {
+                       bool all, hipStream_t st) {
   const int nb = s.row_blocks();
   if (s.w == 32) {
     switch (nb) {
-      case 1: return mu_sigma_dispatch<DT, D, 1, true>(s, q, k, scale, rm, rs, mu, sg, attn, st);
-      case 2: return mu_sigma_dispatch<DT, D, 2, true>(s, q, k, scale, rm, rs, mu, sg, attn, st);
-      default: return mu_sigma_dispatch<DT, D, 4, true>(s, q, k, scale, rm, rs, mu, sg, attn, st);
+      case 1: return mu_sigma_dispatch<DT, D, 1, true>(s, q, k, scale, rm, rs, mu, sg, attn, all, st);
+      case 2: return mu_sigma_dispatch<DT, D, 2, true>(s, q, k, scale, rm, rs, mu, sg, attn, all, st);
+      default: return mu_sigma_dispatch<DT, D, 4, true>(s, q, k, scale, rm, rs, mu, sg, attn, all, st);
     }
   }
-  if (nb == 1) return mu_sigma_dispatch<DT, D, 1, false>(s, q, k, scale, rm, rs, mu, sg, attn, st);
-  return mu_sigma_dispatch<DT, D, 2, false>(s, q, k, scale, rm, rs, mu, sg, attn, st);
+  if (nb == 1)
+    return mu_sigma_dispatch<DT, D, 1, false>(s, q, k, scale, rm, rs, mu, sg, attn, all, st);
+  return mu_sigma_dispatch<DT, D, 2, false>(s, q, k, scale, rm, rs, mu, sg, attn, all, st);
 }
 
 }  // namespace
@@ -381,14 +417,15 @@ hipError_t launch_window_stats(const Shape& s, const void* q_win, const void* k,
 
 hipError_t launch_mu_sigma(const Shape& s, const void* q_win, const void* k, float scale,
                            const float* row_max, const float* row_sum, float* mu, float* sigma,
-                           float* attn, hipStream_t stream) {
+                           float* attn, bool sigma_all, hipStream_t stream) {
+  const bool all = sigma_all;
   if (s.dtype == kDtBf16)
     return s.d == 64
-               ? mu_sigma_nb<kDtBf16, 64>(s, q_win, k, scale, row_max, row_sum, mu, sigma, attn, stream)
-               : mu_sigma_nb<kDtBf16, 128>(s, q_win, k, scale, row_max, row_sum, mu, sigma, attn, stream);
+               ? mu_sigma_nb<kDtBf16, 64>(s, q_win, k, scale, row_max, row_sum, mu, sigma, attn, all, stream)
+               : mu_sigma_nb<kDtBf16, 128>(s, q_win, k, scale, row_max, row_sum, mu, sigma, attn, all, stream);
   return s.d == 64
-             ? mu_sigma_nb<kDtF32, 64>(s, q_win, k, scale, row_max, row_sum, mu, sigma, attn, stream)
-             : mu_sigma_nb<kDtF32, 128>(s, q_win, k, scale, row_max, row_sum, mu, sigma, attn, stream);
+             ? mu_sigma_nb<kDtF32, 64>(s, q_win, k, scale, row_max, row_sum, mu, sigma, attn, all, stream)
+             : mu_sigma_nb<kDtF32, 128>(s, q_win, k, scale, row_max, row_sum, mu, sigma, attn, all, stream);
 }
 
 }  // namespace kv

@@ -35,16 +35,18 @@ class GpuRun:
     host: Dict[str, np.ndarray]
     pool: int = 1
     w_mu: float = 1.0
+    sigma_rows: str = "group_mean"
 
 
 def run_gpu(wl: workloads.Workload, problems: Optional[Sequence[int]] = None, *, fused: bool = False,
             want_attn: bool = False, cand_mult: int = 4, keep_tail: Optional[int] = None,
             budget: Optional[int] = None, packed: Optional[workloads.PackedInputs] = None,
-            pool: int = 1, w_mu: float = 1.0) -> GpuRun:
+            pool: int = 1, w_mu: float = 1.0, sigma_rows: str = "group_mean") -> GpuRun:
     import torch
     probs = list(range(wl.n_prob)) if problems is None else list(problems)
     print(f"[gpu case] {wl.name} problems={len(probs)} fused={fused} attn={want_attn} "
-          f"cand_mult={cand_mult} keep_tail={keep_tail} pool={pool} w_mu={w_mu}", flush=True)
+          f"cand_mult={cand_mult} keep_tail={keep_tail} pool={pool} w_mu={w_mu} "
+          f"sigma_rows={sigma_rows}", flush=True)
     sys.stdout.flush()
     if packed is None:
         packed = workloads.draw_packed(wl, probs)
@@ -54,14 +56,15 @@ def run_gpu(wl: workloads.Workload, problems: Optional[Sequence[int]] = None, *,
     inp = api.upload(wl.dtype, wl.h_q, wl.h_kv, wl.d, wl.w, packed.q_win, packed.k, packed.v,
                      packed.lens, packed.tok_off, lam1, lam2)
     out = api.allocate(inp, B, cand_mult, tail, want_candidates=True, want_attn=want_attn)
-    api.run_pass(inp, out, B, cand_mult, tail, fused=fused, pool=pool, w_mu=w_mu)
+    api.run_pass(inp, out, B, cand_mult, tail, fused=fused, pool=pool, w_mu=w_mu,
+                 sigma_rows=sigma_rows)
     torch.cuda.synchronize()
     host = {name: api.to_host_bits(getattr(out, name)) for name in
             ("row_max", "row_sum", "mu", "sigma", "sel_idx", "sel_score", "cand_idx", "cand_corr",
              "k_out", "v_out")}
     if want_attn:
         host["attn"] = api.to_host_bits(out.attn)
-    return GpuRun(wl, probs, packed, lam1, lam2, B, cand_mult, tail, host, pool, w_mu)
+    return GpuRun(wl, probs, packed, lam1, lam2, B, cand_mult, tail, host, pool, w_mu, sigma_rows)
 
 
 def problem_arrays(run: GpuRun, j: int):
@@ -86,7 +89,7 @@ def check_problem(run: GpuRun, j: int, heads: Optional[Sequence[int]] = None,
     res = evict.evict_problem(q, k, None, wl.dtype, wl.scale, float(run.lam1[j]),
                               float(run.lam2[j]), run.budget, run.cand_mult, run.keep_tail,
                               heads=heads, want_attn="attn" in run.host, pool=run.pool,
-                              w_mu=run.w_mu)
+                              w_mu=run.w_mu, sigma_all_rows=run.sigma_rows == "all_rows")
     H = run.host
     rows = wl.h_q * wl.w
     compare.assert_row_stats(H["row_max"][j * rows:(j + 1) * rows].reshape(wl.h_q, wl.w),

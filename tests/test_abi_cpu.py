@@ -150,6 +150,21 @@ def test_select_option_checks():
                                        NULL, NULL, 0, NULL) == _lib.KV_ERR_BUDGET
 
 
+def test_sigma_rows_checks():
+    pr = HostProblem()
+    lib = _lib.lib()
+    for bad in (-1, 2, 7):
+        assert lib.kv_mu_sigma_ex(pr.ref(), P, P, 0.08, P, P, bad, P, P, NULL,
+                                  NULL) == _lib.KV_ERR_ARG
+        assert lib.kv_window_mu_sigma_ex(pr.ref(), P, P, 0.08, bad, P, P, P, P, P, 1 << 30,
+                                         NULL) == _lib.KV_ERR_ARG
+    # valid reading, other errors still reported first
+    assert lib.kv_mu_sigma_ex(pr.ref(), P, P, 0.08, P, P, _lib.KV_SIGMA_ALL_ROWS, NULL, P, NULL,
+                              NULL) == _lib.KV_ERR_NULL
+    assert lib.kv_window_mu_sigma_ex(pr.ref(), P, P, 0.08, _lib.KV_SIGMA_ALL_ROWS, P, P, P, P, P,
+                                     0, NULL) == _lib.KV_ERR_WORKSPACE
+
+
 # ------------------------------------------------------------------------------------------------
 # depth profiles (host-only entry point) against the oracle
 # ------------------------------------------------------------------------------------------------

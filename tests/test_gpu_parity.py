@@ -133,6 +133,30 @@ def test_mean_free_max_pooled_unfused():
     _all(gpu_cases.run_gpu(wl, fused=False, w_mu=0.5, pool=9))
 
 
+@pytest.mark.parametrize("fused", [True, False])
+def test_dispersion_over_all_group_rows(fused):
+    """KV_SIGMA_ALL_ROWS, 4 query heads per kv head: streaming pass 2 (fused) and the generic
+    w = 32 kernel with the attention output (unfused), L = 3000."""
+    wl = workloads.mistral_layer()
+    wl.seq_lens = [3000]
+    _all(gpu_cases.run_gpu(wl, fused=fused, want_attn=not fused, sigma_rows="all_rows"))
+
+
+@pytest.mark.parametrize("sigma_rows", ["group_mean", "all_rows"])
+def test_three_query_heads_per_kv_head(sigma_rows):
+    """G = 3 (w = 32): 96 window rows in four 32-row blocks, the last one padding; generic
+    kernels, both dispersion readings, L = 2100."""
+    wl = workloads.mistral_layer()
+    wl.h_q, wl.h_kv = 12, 4
+    wl.seq_lens = [2100]
+    _all(gpu_cases.run_gpu(wl, fused=True, sigma_rows=sigma_rows))
+
+
+def test_dispersion_over_all_group_rows_general_window():
+    """KV_SIGMA_ALL_ROWS through the LDS reduction of other window sizes (fp32, G = 2, w = 8)."""
+    _all(gpu_cases.run_gpu(workloads.tiny_f32(), fused=True, sigma_rows="all_rows"))
+
+
 def test_compaction_of_oracle_selection():
     """kv_compact_cache fed with the oracle's admissions reproduces the oracle's compacted rows."""
     import torch
