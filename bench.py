@@ -217,22 +217,40 @@ def main() -> None:
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
 
+    def timed(*calls):
+        """Mean ms of each call over `steps` iterations (after `warmup`), cache flushed before
+        every iteration, HIP events between the calls on the launch stream."""
+        rows_ = []
+        for it in range(args.warmup + args.steps):
+            flush.zero_()
+            evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
+            evs[0].record(stream)
+            for c, fn in enumerate(calls):
+                fn()
+                evs[c + 1].record(stream)
+            if it >= args.warmup:
+                rows_.append(evs)
+        torch.cuda.synchronize()
+        t = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(len(calls))] for e in rows_])
+        return [float(x) for x in t.mean(axis=0)]
+
     # per kernel: the two scoring passes through their own entry points, events between them
     # (warm-up first: a kernel's first launch also loads its code)
-    kernel_events = []
-    for it in range(args.warmup + args.steps):
-        flush.zero_()
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-        evs[0].record(stream)
-        _lib.window_scores(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.ws)
-        evs[1].record(stream)
-        _lib.mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu, out.sigma)
-        evs[2].record(stream)
-        if it >= args.warmup:
-            kernel_events.append(evs)
-    torch.cuda.synchronize()
-    kern = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(2)] for e in kernel_events])
-    k_stats, k_mu = (float(x) for x in kern.mean(axis=0))
+    k_stats, k_mu = timed(
+        lambda: _lib.window_scores(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum,
+                                   out.ws),
+        lambda: _lib.mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
+                              out.sigma))
+
+    # scoring options on the same workload: dispersion over all (head, row) values, a max-pooled
+    # base score, the mean-free score
+    v_all, v_pool, v_free = timed(
+        lambda: _lib.window_mu_sigma_ex(b, inp.q_win, inp.k, inp.scale, "all_rows", out.row_max,
+                                        out.row_sum, out.mu, out.sigma, out.ws),
+        lambda: _lib.mmr_select_ex(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2,
+                                   wl.budget, 4, wl.w, out.sel_idx, ws=out.ws, pool=7),
+        lambda: _lib.mmr_select_ex(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2,
+                                   wl.budget, 4, wl.w, out.sel_idx, ws=out.ws, w_mu=0.0))
 
     # the per-layer schedule: the scoring launched layer by layer (as a model would after each
     # layer's prefill, into the same output buffers), then one batched selection and compaction
@@ -302,6 +320,9 @@ def main() -> None:
                           "mu_sigma_stream (kv_mu_sigma)": round(k_mu, 4),
                           "mmr_select": round(float(mean_part[1]), 4),
                           "compact": round(float(mean_part[2]), 4)},
+        "options_ms": {"kv_window_mu_sigma_ex (sigma over all G*W rows)": round(v_all, 4),
+                       "kv_mmr_select_ex (pool 7)": round(v_pool, 4),
+                       "kv_mmr_select_ex (w_mu 0)": round(v_free, 4)},
         "mfma_tflops": {"stats_stream": round(flops / (k_stats * 1e-3) / 1e12, 1),
                         "mu_sigma_stream": round(flops / (k_mu * 1e-3) / 1e12, 1),
                         "peak_bf16_dense": MFMA_PEAK_TFLOPS},

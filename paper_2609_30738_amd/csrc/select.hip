@@ -185,6 +185,7 @@ template <int NW> struct SelectShared {
   uint32_t wave_cnt[2][NW];
   float wave_max[NW];
   uint64_t best[2][NW];
+  uint32_t halo[2][32];  // raw keys left of a pooling chunk (pool_h <= 31)
   uint32_t sel_threshold;
   int sel_need;
 };
@@ -260,17 +261,52 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
     for (int i = tid; i < n_cand; i += kThreads)
       local_max = fmaxf(local_max, fmaf(lam1, sg_g[i], w_mu * mu_g[i]));
   }
-  // key of the (pooled) score at position i; pooling keeps the maximum, which is also the maximum
-  // of the order-preserving keys
-  auto raw_key = [&](int i) -> uint32_t {
-    if constexpr (STAGED) return skeys[i];
-    else return order_key(fmaf(lam1, sg_g[i], w_mu * mu_g[i]));
-  };
+  // Max-pooling keeps the largest score of the window, whose key is also the largest key.
+  if constexpr (STAGED) {
+    if (pool_h > 0) {
+      // In place, a chunk of kPer * kThreads positions at a time: pooled keys of the chunk go to
+      // registers, the raw keys of its last pool_h positions to a halo that the next chunk reads
+      // instead of the (by then overwritten) chunk, then the chunk is overwritten.
+      constexpr int kPer = 8, kChunk = kPer * kThreads;
+      for (int c0 = 0, c = 0; c0 < n_cand; c0 += kChunk, ++c) {
+        const int c1 = min(n_cand, c0 + kChunk);
+        const uint32_t* halo_in = sh.halo[c & 1];  // positions c0 - pool_h .. c0 - 1
+        uint32_t pk[kPer];
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+          const int i = c0 + q * kThreads + tid;
+          uint32_t m = 0u;
+          if (i < c1) {
+            const int j1 = min(n_cand - 1, i + pool_h);
+            for (int j = max(0, i - pool_h); j <= j1; ++j)
+              m = max(m, j < c0 ? halo_in[j - (c0 - pool_h)] : skeys[j]);
+          }
+          pk[q] = m;
+        }
+        if (tid < pool_h && c1 < n_cand) sh.halo[(c + 1) & 1][tid] = skeys[c1 - pool_h + tid];
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+          const int i = c0 + q * kThreads + tid;
+          if (i < c1) skeys[i] = pk[q];
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // key of the (pooled) score at position i
   auto key_at = [&](int i) -> uint32_t {
-    if (pool_h == 0) return raw_key(i);
-    uint32_t kmax = 0u;
-    for (int j = max(0, i - pool_h); j <= min(n_cand - 1, i + pool_h); ++j) kmax = max(kmax, raw_key(j));
-    return kmax;
+    if constexpr (STAGED) {
+      return skeys[i];
+    } else {
+      uint32_t kmax = order_key(fmaf(lam1, sg_g[i], w_mu * mu_g[i]));
+      if (pool_h > 0) {
+        const int j1 = min(n_cand - 1, i + pool_h);
+        for (int j = max(0, i - pool_h); j <= j1; ++j)
+          kmax = max(kmax, order_key(fmaf(lam1, sg_g[j], w_mu * mu_g[j])));
+      }
+      return kmax;
+    }
   };
   {
     const float wm = wave_max_f(local_max);

@@ -70,3 +70,15 @@ def test_ragged_8x32_both_terms():
     run = gpu_cases.run_gpu(workloads.ragged_batch("both"), fused=True)
     _properties(run)
     _sampled(run, [0, 37, 100, 255], [3])
+
+
+@pytest.mark.parametrize("pool", [1, 5])
+def test_long_context_select_from_global_scores(pool):
+    """L = 40000 > the 34816 candidate scores the selection stages in LDS: the score keys are
+    re-formed from mu / sigma in HBM on every pass (and pooled there), 2 layers."""
+    wl = workloads.mistral_layer()
+    wl.seq_lens = [40000]
+    wl.n_layers = 2
+    run = gpu_cases.run_gpu(wl, fused=True, pool=pool)
+    _properties(run)
+    _sampled(run, [0, 1], [1, 6])

@@ -114,6 +114,21 @@ def test_max_pooled_scores(pool):
     _all(gpu_cases.run_gpu(wl, fused=True, pool=pool))
 
 
+def test_max_pooled_scores_across_pooling_chunks():
+    """bf16 keys, L = 20000: the in-place pooling of the staged keys runs in three chunks of
+    8192 positions, so windows straddle chunk ends (pool 31)."""
+    wl = workloads.mistral_layer()
+    wl.seq_lens = [20000]
+    _all(gpu_cases.run_gpu(wl, fused=True, pool=31), heads=[0, 3, 7])
+
+
+def test_max_pooled_scores_fp32_chunks():
+    """fp32 keys (256 threads, chunks of 2048 positions), L = 5000, pool 9."""
+    wl = workloads.tiny_f32()
+    wl.seq_lens = [5000]
+    _all(gpu_cases.run_gpu(wl, fused=True, pool=9))
+
+
 def test_max_pooled_scores_fp32_keep_all():
     """fp32 keys (256-thread select), every position a candidate (keep_tail = 0) and pool 5."""
     _all(gpu_cases.run_gpu(workloads.tiny_f32(), fused=True, keep_tail=0, pool=5))
