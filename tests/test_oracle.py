@@ -15,7 +15,7 @@ import pytest
 import torch
 from hypothesis import given, settings, strategies as st
 
-from oracle import evict, profiles
+from oracle import budgets, evict, profiles
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -518,3 +518,37 @@ def test_profile_rejects_bad_arguments():
         profiles.latent("nope", [1.0], 0, 32)
     with pytest.raises(ValueError):
         profiles.latent("global", [1.0], 32, 32)
+
+
+# ------------------------------------------------------------------------------------------------
+# Depth-decreasing budgets at a fixed total (reading R26)
+# ------------------------------------------------------------------------------------------------
+
+def test_pyramid_budgets_hand_worked():
+    """B = 10, beta = 5, 4 layers: B_min = 2, B_max = 18, real budgets 18, 12.67, 7.33, 2, rounded
+    away from 10: 18, 13, 7, 2."""
+    assert budgets.pyramid_budgets(10, 4, 5.0) == [18, 13, 7, 2]
+
+
+def test_pyramid_budgets_benchmark_shape():
+    """B = 64 over 32 layers with beta = 20: from 125 down to 3, total 2048, and the largest
+    top-4B candidate set 4 * 125 = 500."""
+    b = budgets.pyramid_budgets(64, 32, 20.0)
+    assert b[0] == 125 and b[-1] == 3 and sum(b) == 2048
+
+
+@settings(max_examples=300, deadline=None)
+@given(st.integers(1, 300), st.integers(1, 48), st.sampled_from([1.0, 1.5, 2.0, 5.0, 20.0, 1e9]))
+def test_pyramid_budgets_invariants(B, n, beta):
+    """Same total as the uniform allocation, non-increasing with depth, mirror-symmetric about B,
+    within [B_min, B_max], and uniform for beta = 1 or a single layer."""
+    b = budgets.pyramid_budgets(B, n, beta)
+    assert len(b) == n and sum(b) == n * B
+    assert all(x >= y for x, y in zip(b, b[1:]))
+    assert all(b[i] + b[n - 1 - i] == 2 * B for i in range(n))
+    b_min = max(1, math.floor(B / beta))
+    assert all(b_min <= x <= 2 * B - b_min for x in b)
+    if beta == 1.0 or n == 1:
+        assert b == [B] * n
+    if n > 1:
+        assert b[0] == 2 * B - b_min and b[-1] == b_min
