@@ -244,6 +244,20 @@ def main() -> None:
 
     # scoring options on the same workload: dispersion over all (head, row) values, a max-pooled
     # base score, the mean-free score
+    # depth-decreasing budgets at the same total (B = 64 per layer on average, beta = 20): the
+    # rows are strided by the largest budget
+    sched = _lib.pyramid_budgets(wl.budget, wl.n_layers, 20.0)
+    pyr = _lib.Budgets([int(sched[wl.layer_of(p)]) for p in range(wl.n_prob)])
+    b_max = pyr.max
+    sel_pyr = torch.empty(wl.n_prob * wl.h_kv * b_max, dtype=torch.int32, device="cuda")
+    kv_rows = wl.n_prob * wl.h_kv * (b_max + wl.w) * wl.d
+    k_pyr = torch.empty(kv_rows, dtype=inp.k.dtype, device="cuda")
+    v_pyr = torch.empty(kv_rows, dtype=inp.v.dtype, device="cuda")
+    v_pyr_sel, v_pyr_cmp = timed(
+        lambda: _lib.mmr_select_ex(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2, b_max, 4,
+                                   wl.w, sel_pyr, ws=out.ws, budgets=pyr),
+        lambda: _lib.compact_cache_ex(b, inp.k, inp.v, sel_pyr, b_max, wl.w, pyr, k_pyr, v_pyr))
+
     v_all, v_pool, v_free = timed(
         lambda: _lib.window_mu_sigma_ex(b, inp.q_win, inp.k, inp.scale, "all_rows", out.row_max,
                                         out.row_sum, out.mu, out.sigma, out.ws),
@@ -322,7 +336,10 @@ def main() -> None:
                           "compact": round(float(mean_part[2]), 4)},
         "options_ms": {"kv_window_mu_sigma_ex (sigma over all G*W rows)": round(v_all, 4),
                        "kv_mmr_select_ex (pool 7)": round(v_pool, 4),
-                       "kv_mmr_select_ex (w_mu 0)": round(v_free, 4)},
+                       "kv_mmr_select_ex (w_mu 0)": round(v_free, 4),
+                       "kv_mmr_select_ex (depth-decreasing budgets, beta 20, "
+                       f"{int(sched[0])}..{int(sched[-1])})": round(v_pyr_sel, 4),
+                       "kv_compact_cache_ex (same budgets)": round(v_pyr_cmp, 4)},
         "mfma_tflops": {"stats_stream": round(flops / (k_stats * 1e-3) / 1e12, 1),
                         "mu_sigma_stream": round(flops / (k_mu * 1e-3) / 1e12, 1),
                         "peak_bf16_dense": MFMA_PEAK_TFLOPS},

@@ -169,8 +169,8 @@ int kv_mmr_select(const kv_problem* pr, const float* mu, const float* sigma, con
                   int32_t keep_tail, int32_t* sel_idx, float* sel_score, int32_t* cand_idx,
                   float* cand_corr, void* ws, size_t ws_bytes, void* stream);
 
-/* Scoring options of kv_mmr_select_ex.  NULL options mean {pool = 1, w_mu = 1}, which is exactly
- * kv_mmr_select.
+/* Scoring and budget options of kv_mmr_select_ex.  NULL options mean {pool = 1, w_mu = 1, no
+ * per-problem budgets}, which is exactly kv_mmr_select.
  *   pool: odd window, 1 <= pool <= 63, of a max-pool over positions applied to the base score
  *     before normalisation and the top-C restriction (the pooling that the mean-attention baselines
  *     apply and that the paper keeps in its scoring, section 3.1):
@@ -179,10 +179,19 @@ int kv_mmr_select(const kv_problem* pr, const float* mu, const float* sigma, con
  *   w_mu: weight of mu in the base score, s_i = w_mu * mu_i + lambda1 * sigma_i, with w_mu * mu_i
  *     rounded to fp32 first (exact for w_mu = 1).  w_mu = 0 is the mean-free "dispersion and
  *     redundancy" rule of the term ablation (section 4.3, Table 3).
+ *   budget_host / budget_dev: per-problem budgets B_p (n_prob int32 values, the same values in
+ *     host and device memory; both NULL for the uniform `budget`).  The budgets of a depth schedule
+ *     such as kv_pyramid_budgets (section 3.1: the runs use budgets that fall with depth at a fixed
+ *     total).  Each B_p must satisfy 1 <= B_p <= budget and B_p <= L_p - keep_tail (else
+ *     KV_ERR_BUDGET); `budget` stays the row stride of sel_idx / sel_score, and problem p runs B_p
+ *     greedy steps, C_p = min(cand_mult * B_p, n_cand) candidates, and pads steps B_p .. budget-1
+ *     with sel_idx = -1 and sel_score = 0.  One array without the other returns KV_ERR_NULL.
  * An even, non-positive or too large pool, or a non-finite w_mu, returns KV_ERR_ARG. */
 typedef struct kv_select_opts {
   int32_t pool;
   float w_mu;
+  const int32_t* budget_host;
+  const int32_t* budget_dev;
 } kv_select_opts;
 
 /* kv_mmr_select with scoring options (opts nullable, see kv_select_opts); every other argument,
@@ -201,6 +210,25 @@ int kv_mmr_select_ex(const kv_problem* pr, const float* mu, const float* sigma, 
  * unwritten.  Needs no workspace. */
 int kv_compact_cache(const kv_problem* pr, const void* k, const void* v, const int32_t* sel_idx,
                      int32_t budget, int32_t keep_tail, void* k_out, void* v_out, void* stream);
+
+/* kv_compact_cache with per-problem budgets (budget_host / budget_dev as in kv_select_opts; both
+ * NULL is exactly kv_compact_cache).  The block of every (problem, kv head) keeps its stride of
+ * budget + keep_tail rows; rows 0..B_p-1 are the rows of the first B_p selected positions in
+ * ascending order, rows B_p..B_p+keep_tail-1 the last keep_tail positions, and the rows after them
+ * are not written. */
+int kv_compact_cache_ex(const kv_problem* pr, const void* k, const void* v,
+                        const int32_t* sel_idx, int32_t budget, int32_t keep_tail,
+                        const int32_t* budget_host, const int32_t* budget_dev, void* k_out,
+                        void* v_out, void* stream);
+
+/* Per-layer budgets that fall with depth at the total of a uniform `budget` (section 3.1: the runs
+ * use such an allocation; the paper prints no schedule), host-only.  With
+ * B_min = max(1, floor(budget / beta)) and B_max = 2 budget - B_min, layer l gets the linear
+ * value B_max - l (B_max - B_min) / (n_layers - 1) rounded away from `budget` (up above it, down
+ * below it), so the layers sum to exactly n_layers * budget; one layer gets `budget`.
+ * budgets_host receives n_layers values.  beta >= 1 (beta = 1: uniform).  KV_ERR_NULL for a NULL
+ * output, KV_ERR_ARG for budget < 1, n_layers < 1 or beta < 1 or not finite. */
+int kv_pyramid_budgets(int32_t budget, int32_t n_layers, double beta, int32_t* budgets_host);
 
 /* Per-layer coefficients of a depth profile (section 3.3, Eq. (6)), host-only:
  * lambda_out_host[l] = (float) sinh(a(l)) for l = 0..n_layers-1, a(l) given by `family` and the

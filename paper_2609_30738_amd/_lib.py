@@ -40,7 +40,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvevict.
 SYMBOLS = ("kv_strerror", "kv_version", "kv_workspace_bytes", "kv_candidate_stride",
            "kv_window_scores", "kv_mu_sigma", "kv_mu_sigma_ex", "kv_window_mu_sigma",
            "kv_window_mu_sigma_ex", "kv_mmr_select", "kv_mmr_select_ex", "kv_compact_cache",
-           "kv_depth_profile")
+           "kv_compact_cache_ex", "kv_pyramid_budgets", "kv_depth_profile")
 
 
 class KvError(RuntimeError):
@@ -57,7 +57,8 @@ class KvProblem(ctypes.Structure):
 
 
 class KvSelectOpts(ctypes.Structure):
-    _fields_ = [("pool", ctypes.c_int32), ("w_mu", ctypes.c_float)]
+    _fields_ = [("pool", ctypes.c_int32), ("w_mu", ctypes.c_float),
+                ("budget_host", ctypes.c_void_p), ("budget_dev", ctypes.c_void_p)]
 
 
 _LIB = None
@@ -91,11 +92,14 @@ def lib() -> ctypes.CDLL:
         h.kv_mmr_select_ex.argtypes = [pr, vp, vp, vp, vp, vp, i32, i32, i32,
                                        ctypes.POINTER(KvSelectOpts), vp, vp, vp, vp, vp, sz, vp]
         h.kv_compact_cache.argtypes = [pr, vp, vp, vp, i32, i32, vp, vp, vp]
+        h.kv_compact_cache_ex.argtypes = [pr, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp]
+        h.kv_pyramid_budgets.argtypes = [i32, i32, ctypes.c_double, ctypes.POINTER(ctypes.c_int32)]
         h.kv_depth_profile.argtypes = [i32, ctypes.POINTER(ctypes.c_double), i32, i32,
                                        ctypes.POINTER(ctypes.c_float)]
         for name in ("kv_window_scores", "kv_mu_sigma", "kv_mu_sigma_ex", "kv_window_mu_sigma",
                      "kv_window_mu_sigma_ex", "kv_mmr_select", "kv_mmr_select_ex",
-                     "kv_compact_cache", "kv_depth_profile"):
+                     "kv_compact_cache", "kv_compact_cache_ex", "kv_pyramid_budgets",
+                     "kv_depth_profile"):
             getattr(h, name).restype = ctypes.c_int
         _LIB = h
     return _LIB
@@ -151,6 +155,24 @@ class Batch:
 
     def ref(self):
         return ctypes.byref(self.struct)
+
+
+class Budgets:
+    """Per-problem budgets B_p: the host values and their device copy (budget_host / budget_dev of
+    kv_select_opts and kv_compact_cache_ex)."""
+
+    def __init__(self, values: Sequence[int], device=None):
+        import torch
+        self.host = np.ascontiguousarray(np.asarray(values, dtype=np.int32))
+        dev = torch.device("cuda") if device is None else torch.device(device)
+        self.dev = torch.from_numpy(self.host).to(dev)
+
+    @property
+    def max(self) -> int:
+        return int(self.host.max())
+
+    def pointers(self):
+        return ctypes.c_void_p(self.host.ctypes.data), ctypes.c_void_p(self.dev.data_ptr())
 
 
 def _ptr(t) -> ctypes.c_void_p:
@@ -235,12 +257,15 @@ def mmr_select(batch: Batch, mu, sigma, k, lambda1, lambda2, budget: int, cand_m
 
 def mmr_select_ex(batch: Batch, mu, sigma, k, lambda1, lambda2, budget: int, cand_mult: int,
                   keep_tail: int, sel_idx, sel_score=None, cand_idx=None, cand_corr=None, ws=None,
-                  pool: Optional[int] = None, w_mu: Optional[float] = None, stream=None) -> None:
-    """kv_mmr_select_ex; options are passed as NULL when both pool and w_mu are None."""
+                  pool: Optional[int] = None, w_mu: Optional[float] = None,
+                  budgets: Optional[Budgets] = None, stream=None) -> None:
+    """kv_mmr_select_ex; options are passed as NULL when pool, w_mu and budgets are all None.
+    With `budgets`, `budget` is the row stride of sel_idx / sel_score."""
     opts = None
-    if pool is not None or w_mu is not None:
+    if pool is not None or w_mu is not None or budgets is not None:
+        bh, bd = budgets.pointers() if budgets is not None else (None, None)
         opts = ctypes.byref(KvSelectOpts(1 if pool is None else int(pool),
-                                         1.0 if w_mu is None else float(w_mu)))
+                                         1.0 if w_mu is None else float(w_mu), bh, bd))
     _check(lib().kv_mmr_select_ex(batch.ref(), _ptr(mu), _ptr(sigma), _ptr(k), _ptr(lambda1),
                                   _ptr(lambda2), int(budget), int(cand_mult), int(keep_tail), opts,
                                   _ptr(sel_idx), _ptr(sel_score), _ptr(cand_idx),
@@ -254,6 +279,22 @@ def compact_cache(batch: Batch, k, v, sel_idx, budget: int, keep_tail: int, k_ou
     _check(lib().kv_compact_cache(batch.ref(), _ptr(k), _ptr(v), _ptr(sel_idx), int(budget),
                                   int(keep_tail), _ptr(k_out), _ptr(v_out), _stream(stream)),
            "kv_compact_cache")
+
+
+def compact_cache_ex(batch: Batch, k, v, sel_idx, budget: int, keep_tail: int,
+                     budgets: Optional[Budgets], k_out, v_out, stream=None) -> None:
+    bh, bd = budgets.pointers() if budgets is not None else (None, None)
+    _check(lib().kv_compact_cache_ex(batch.ref(), _ptr(k), _ptr(v), _ptr(sel_idx), int(budget),
+                                     int(keep_tail), bh, bd, _ptr(k_out), _ptr(v_out),
+                                     _stream(stream)), "kv_compact_cache_ex")
+
+
+def pyramid_budgets(budget: int, n_layers: int, beta: float) -> np.ndarray:
+    """Depth-decreasing per-layer budgets at the total of a uniform `budget` (int32)."""
+    out = (ctypes.c_int32 * n_layers)()
+    _check(lib().kv_pyramid_budgets(int(budget), int(n_layers), float(beta), out),
+           "kv_pyramid_budgets")
+    return np.frombuffer(out, dtype=np.int32).copy()
 
 
 def depth_profile(family: str, params: Sequence[float], n_layers: int) -> np.ndarray:

@@ -2,7 +2,7 @@
 
 Torch is used only for device memory and streams; every step of the pass is one of the library's
 entry points (kv_window_scores + kv_mu_sigma or kv_window_mu_sigma, kv_mmr_select or
-kv_mmr_select_ex, kv_compact_cache).
+kv_mmr_select_ex, kv_compact_cache or kv_compact_cache_ex), or their _ex variants.
 """
 from __future__ import annotations
 
@@ -98,12 +98,14 @@ def allocate(inp: DeviceInputs, budget: int, cand_mult: int = 4, keep_tail: Opti
 
 def run_pass(inp: DeviceInputs, out: PassOutputs, budget: int, cand_mult: int = 4,
              keep_tail: Optional[int] = None, fused: bool = True, pool: int = 1, w_mu: float = 1.0,
-             sigma_rows: str = "group_mean", stream=None) -> None:
+             sigma_rows: str = "group_mean", budgets: Optional[_lib.Budgets] = None,
+             stream=None) -> None:
     """One whole eviction pass over the batch, enqueued on `stream` (default: current stream).
 
     pool / w_mu: scoring options of kv_mmr_select_ex (max-pool window, weight of mu);
-    sigma_rows: the dispersion reading of kv_mu_sigma_ex / kv_window_mu_sigma_ex.  The defaults
-    call the plain entry points."""
+    sigma_rows: the dispersion reading of kv_mu_sigma_ex / kv_window_mu_sigma_ex; budgets:
+    per-problem budgets (then `budget` is the row stride and must be at least their maximum).  The
+    defaults call the plain entry points."""
     b = inp.batch
     tail = b.w if keep_tail is None else keep_tail
     plain = sigma_rows == "group_mean"
@@ -123,12 +125,16 @@ def run_pass(inp: DeviceInputs, out: PassOutputs, budget: int, cand_mult: int = 
         else:
             _lib.mu_sigma_ex(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, sigma_rows,
                              out.mu, out.sigma, out.attn, stream)
-    if pool == 1 and w_mu == 1.0:
+    if pool == 1 and w_mu == 1.0 and budgets is None:
         _lib.mmr_select(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2, budget, cand_mult,
                         tail, out.sel_idx, out.sel_score, out.cand_idx, out.cand_corr, out.ws,
                         stream)
+        _lib.compact_cache(b, inp.k, inp.v, out.sel_idx, budget, tail, out.k_out, out.v_out,
+                           stream)
     else:
         _lib.mmr_select_ex(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2, budget,
                            cand_mult, tail, out.sel_idx, out.sel_score, out.cand_idx,
-                           out.cand_corr, out.ws, pool=pool, w_mu=w_mu, stream=stream)
-    _lib.compact_cache(b, inp.k, inp.v, out.sel_idx, budget, tail, out.k_out, out.v_out, stream)
+                           out.cand_corr, out.ws, pool=pool, w_mu=w_mu, budgets=budgets,
+                           stream=stream)
+        _lib.compact_cache_ex(b, inp.k, inp.v, out.sel_idx, budget, tail, budgets, out.k_out,
+                              out.v_out, stream)

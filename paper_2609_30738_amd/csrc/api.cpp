@@ -68,11 +68,26 @@ int check_budget(const kv_problem* pr, int32_t budget, int32_t keep_tail) {
   return KV_OK;
 }
 
-int max_candidates(const kv_problem* pr, int32_t budget, int32_t cand_mult, int32_t keep_tail) {
+// Per-problem budgets (both arrays or neither): every B_p in [1, budget] and <= L_p - keep_tail.
+int check_budgets(const kv_problem* pr, int32_t budget, int32_t keep_tail, const int32_t* b_host,
+                  const int32_t* b_dev) {
+  if (!b_host && !b_dev) return KV_OK;
+  if (!b_host || !b_dev) return KV_ERR_NULL;
+  for (int p = 0; p < pr->n_prob; ++p) {
+    const int32_t b = b_host[p];
+    if (b < 1 || b > budget || b > pr->len_host[p] - keep_tail) return KV_ERR_BUDGET;
+  }
+  return KV_OK;
+}
+
+// Largest candidate count of the batch (budget of problem p: b_host[p], or `budget`).
+int max_candidates(const kv_problem* pr, int32_t budget, int32_t cand_mult, int32_t keep_tail,
+                   const int32_t* b_host = nullptr) {
   int m = 0;
   for (int p = 0; p < pr->n_prob; ++p) {
     const int n_cand = pr->len_host[p] - keep_tail;
-    const int64_t c = cand_mult > 0 ? std::min<int64_t>((int64_t)cand_mult * budget, n_cand) : n_cand;
+    const int64_t b = b_host ? b_host[p] : budget;
+    const int64_t c = cand_mult > 0 ? std::min<int64_t>((int64_t)cand_mult * b, n_cand) : n_cand;
     if (c > m) m = (int)c;
   }
   return m;
@@ -243,12 +258,16 @@ int kv_mmr_select_ex(const kv_problem* pr, const float* mu, const float* sigma, 
   if (cand_mult < 0) return KV_ERR_ARG;
   const int32_t pool = opts ? opts->pool : 1;
   const float w_mu = opts ? opts->w_mu : 1.f;
+  const int32_t* b_host = opts ? opts->budget_host : nullptr;
+  const int32_t* b_dev = opts ? opts->budget_dev : nullptr;
   if (pool < 1 || pool > kMaxPool || pool % 2 == 0 || !std::isfinite(w_mu)) return KV_ERR_ARG;
   st = check_budget(pr, budget, keep_tail);
   if (st != KV_OK) return st;
+  st = check_budgets(pr, budget, keep_tail, b_host, b_dev);
+  if (st != KV_OK) return st;
   (void)ws;
   (void)ws_bytes;
-  const int max_cand = max_candidates(pr, budget, cand_mult, keep_tail);
+  const int max_cand = max_candidates(pr, budget, cand_mult, keep_tail, b_host);
   if (max_cand > kv::select_max_candidates(pr->d, elem_bytes(pr->dtype))) return KV_ERR_SHAPE;
   kv::SelectArgs a;
   a.mu = mu;
@@ -259,6 +278,7 @@ int kv_mmr_select_ex(const kv_problem* pr, const float* mu, const float* sigma, 
   a.pool = pool;
   a.w_mu = w_mu;
   a.budget = budget;
+  a.budgets = b_dev;
   a.cand_mult = cand_mult;
   a.keep_tail = keep_tail;
   a.cand_stride = kv_candidate_stride(pr, budget, cand_mult, keep_tail);
@@ -274,6 +294,14 @@ int kv_mmr_select_ex(const kv_problem* pr, const float* mu, const float* sigma, 
 
 int kv_compact_cache(const kv_problem* pr, const void* k, const void* v, const int32_t* sel_idx,
                      int32_t budget, int32_t keep_tail, void* k_out, void* v_out, void* stream) {
+  return kv_compact_cache_ex(pr, k, v, sel_idx, budget, keep_tail, nullptr, nullptr, k_out, v_out,
+                             stream);
+}
+
+int kv_compact_cache_ex(const kv_problem* pr, const void* k, const void* v,
+                        const int32_t* sel_idx, int32_t budget, int32_t keep_tail,
+                        const int32_t* budget_host, const int32_t* budget_dev, void* k_out,
+                        void* v_out, void* stream) {
   kv::Shape s;
   int st = check_problem(pr, &s);
   if (st != KV_OK) return st;
@@ -281,9 +309,31 @@ int kv_compact_cache(const kv_problem* pr, const void* k, const void* v, const i
   if (!aligned16(k) || !aligned16(v) || !aligned16(k_out) || !aligned16(v_out)) return KV_ERR_ARG;
   st = check_budget(pr, budget, keep_tail);
   if (st != KV_OK) return st;
+  st = check_budgets(pr, budget, keep_tail, budget_host, budget_dev);
+  if (st != KV_OK) return st;
   if (budget > kMaxCompactBudget) return KV_ERR_BUDGET;
-  return launch_status(kv::launch_compact(s, k, v, sel_idx, budget, keep_tail, k_out, v_out,
-                                          static_cast<hipStream_t>(stream)));
+  return launch_status(kv::launch_compact(s, k, v, sel_idx, budget, budget_dev, keep_tail, k_out,
+                                          v_out, static_cast<hipStream_t>(stream)));
+}
+
+int kv_pyramid_budgets(int32_t budget, int32_t n_layers, double beta, int32_t* budgets_host) {
+  if (!budgets_host) return KV_ERR_NULL;
+  if (budget < 1 || n_layers < 1 || !(beta >= 1.0) || !std::isfinite(beta)) return KV_ERR_ARG;
+  if (n_layers == 1) {
+    budgets_host[0] = budget;
+    return KV_OK;
+  }
+  const int64_t b_min = std::max<int64_t>(1, (int64_t)std::floor((double)budget / beta));
+  const int64_t b_max = 2 * (int64_t)budget - b_min, span = b_max - b_min, n1 = n_layers - 1;
+  for (int64_t l = 0; l < n_layers; ++l) {
+    // the linear budget of layer l rounded away from `budget`; layers l and n-1-l sum to 2 budget
+    int64_t b;
+    if (2 * l < n1) b = b_max - (l * span) / n1;
+    else if (2 * l == n1) b = budget;
+    else b = b_min + ((n1 - l) * span) / n1;
+    budgets_host[l] = (int32_t)b;
+  }
+  return KV_OK;
 }
 
 int kv_depth_profile(int32_t family, const double* params_host, int32_t n_params,

@@ -72,6 +72,7 @@ struct SelectArgs {
   int pool;     // odd max-pool window over the candidate positions (1: none)
   float w_mu;   // weight of mu in the base score (1: the paper's score)
   int budget, cand_mult, keep_tail, cand_stride, max_cand;
+  const int32_t* budgets;  // per-problem budgets (device, nullable): B_p <= budget, the row stride
   int max_cand_all;  // max_p (L_p - keep_tail): every position that competes for a candidate slot
   int32_t* sel_idx;
   float* sel_score;
@@ -85,6 +86,7 @@ int select_max_candidates(int d, int elem_bytes);
 hipError_t launch_mmr_select(const Shape& s, const SelectArgs& a, hipStream_t stream);
 
 hipError_t launch_compact(const Shape& s, const void* k, const void* v, const int32_t* sel_idx,
-                          int budget, int keep_tail, void* k_out, void* v_out, hipStream_t stream);
+                          int budget, const int32_t* budgets, int keep_tail, void* k_out,
+                          void* v_out, hipStream_t stream);
 
 }  // namespace kv

@@ -197,8 +197,8 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
     const float* __restrict__ mu, const float* __restrict__ sigma,
     const typename Elem<DT>::T* __restrict__ k, const int32_t* __restrict__ lens,
     const int64_t* __restrict__ tok_off, const float* __restrict__ lambda1,
-    const float* __restrict__ lambda2, int pool_h, float w_mu, int h_kv, int budget, int cand_mult,
-    int keep_tail,
+    const float* __restrict__ lambda2, int pool_h, float w_mu, int h_kv, int budget,
+    const int32_t* __restrict__ budgets, int cand_mult, int keep_tail,
     int cand_stride, int max_cand, int32_t* __restrict__ sel_idx, float* __restrict__ sel_score,
     int32_t* __restrict__ cand_idx, float* __restrict__ cand_corr) {
   using T = typename Elem<DT>::T;
@@ -212,7 +212,8 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = lens[p];
   const int n_cand = L - keep_tail;
-  const int C = cand_mult > 0 ? min(cand_mult * budget, n_cand) : n_cand;
+  const int bp = budgets ? budgets[p] : budget;  // this problem's budget; `budget` is the row stride
+  const int C = cand_mult > 0 ? min(cand_mult * bp, n_cand) : n_cand;
   const size_t base = (size_t)tok_off[p] * h_kv + (size_t)g * L;
   const float* mu_g = mu + base;
   const float* sg_g = sigma + base;
@@ -462,7 +463,7 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
   // barrier (sleeping there instead of taking issue slots from the live waves)
   const int live_waves = min(kWaves, (C + 63) / 64);
   const bool live = wave < live_waves;
-  for (int t = 0; t < budget; ++t) {
+  for (int t = 0; t < bp; ++t) {
     if (live) {
       float my_score = -INFINITY;  // admitted slots rank below every live score
       int my_slot = 0x7FFFFFFF;
@@ -491,7 +492,7 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
         const uint64_t o = sh.best[t & 1][v];
         b = o > b ? o : b;
       }
-      last = min(max(unpack_slot(b), 0), C - 1);  // always a live slot: budget <= C
+      last = min(max(unpack_slot(b), 0), C - 1);  // always a live slot: bp <= C
 #pragma unroll
       for (int q = 0; q < CPT; ++q)
         if (tid + q * kThreads == last) admitted[q] = true;
@@ -506,6 +507,13 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
         }
       }
     }
+  }
+
+  // steps beyond this problem's budget: padding
+  for (int t = bp + tid; t < budget; t += kThreads) {
+    const size_t o = ((size_t)p * h_kv + g) * budget + t;
+    sel_idx[o] = -1;
+    if (sel_score) sel_score[o] = 0.f;
   }
 
   if (cand_idx || cand_corr) {
@@ -554,7 +562,7 @@ hipError_t select_launch(const Shape& s, const SelectArgs& a, hipStream_t st) {
   kern<<<dim3((unsigned)(s.n_prob * s.h_kv)), NT, dyn, st>>>(
       a.mu, a.sigma, static_cast<const T*>(a.k), s.lens, s.tok_off, a.lambda1, a.lambda2,
       a.pool / 2, a.w_mu, s.h_kv,
-      a.budget, a.cand_mult, a.keep_tail, a.cand_stride, a.max_cand, a.sel_idx, a.sel_score,
+      a.budget, a.budgets, a.cand_mult, a.keep_tail, a.cand_stride, a.max_cand, a.sel_idx, a.sel_score,
       a.cand_idx, a.cand_corr);
   return hipGetLastError();
 }

@@ -165,6 +165,48 @@ def test_sigma_rows_checks():
                                      0, NULL) == _lib.KV_ERR_WORKSPACE
 
 
+def test_per_problem_budget_checks():
+    pr = HostProblem(lens=(4096, 100))
+    lib = _lib.lib()
+
+    def sel_ex(values, budget=64, keep_tail=32, dev=True):
+        b = np.asarray(values, dtype=np.int32)
+        opts = _lib.KvSelectOpts(1, 1.0, b.ctypes.data, P.value if dev else None)
+        return lib.kv_mmr_select_ex(pr.ref(), P, P, P, P, P, budget, 4, keep_tail,
+                                    ctypes.byref(opts), P, NULL, NULL, NULL, NULL, 0, NULL)
+
+    def compact_ex(values, budget=64, keep_tail=32, host=True):
+        b = np.asarray(values, dtype=np.int32)
+        return lib.kv_compact_cache_ex(pr.ref(), P, P, P, budget, keep_tail,
+                                       ctypes.c_void_p(b.ctypes.data) if host else NULL, P, P, P,
+                                       NULL)
+    assert sel_ex([64, 0]) == _lib.KV_ERR_BUDGET
+    assert sel_ex([65, 10]) == _lib.KV_ERR_BUDGET           # above the stride
+    assert sel_ex([64, 69], budget=64) == _lib.KV_ERR_BUDGET  # 100 - 32 = 68 candidates
+    assert sel_ex([64, 10], dev=False) == _lib.KV_ERR_NULL
+    assert compact_ex([64, 0]) == _lib.KV_ERR_BUDGET
+    assert compact_ex([64, 10], host=False) == _lib.KV_ERR_NULL
+
+
+@pytest.mark.parametrize("budget,n_layers,beta", [(64, 32, 20.0), (10, 4, 5.0), (128, 32, 20.0),
+                                                  (7, 1, 3.0), (50, 9, 1.0), (1, 5, 2.0),
+                                                  (300, 47, 1.5)])
+def test_pyramid_budgets_match_oracle(budget, n_layers, beta):
+    from oracle import budgets
+    assert _lib.pyramid_budgets(budget, n_layers, beta).tolist() == \
+        budgets.pyramid_budgets(budget, n_layers, beta)
+
+
+def test_pyramid_budget_errors():
+    lib = _lib.lib()
+    out = (ctypes.c_int32 * 4)()
+    assert lib.kv_pyramid_budgets(0, 4, 2.0, out) == _lib.KV_ERR_ARG
+    assert lib.kv_pyramid_budgets(8, 0, 2.0, out) == _lib.KV_ERR_ARG
+    assert lib.kv_pyramid_budgets(8, 4, 0.5, out) == _lib.KV_ERR_ARG
+    assert lib.kv_pyramid_budgets(8, 4, float("nan"), out) == _lib.KV_ERR_ARG
+    assert lib.kv_pyramid_budgets(8, 4, 2.0, None) == _lib.KV_ERR_NULL
+
+
 # ------------------------------------------------------------------------------------------------
 # depth profiles (host-only entry point) against the oracle
 # ------------------------------------------------------------------------------------------------

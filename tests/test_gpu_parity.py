@@ -172,6 +172,26 @@ def test_dispersion_over_all_group_rows_general_window():
     _all(gpu_cases.run_gpu(workloads.tiny_f32(), fused=True, sigma_rows="all_rows"))
 
 
+def test_depth_decreasing_budgets():
+    """Per-problem budgets from the depth schedule (B = 64 over 4 layers, beta = 20: 125, 85, 43,
+    3), two sequences x 4 layers of L = 3000 and 2200: ragged greedy lengths, candidate counts and
+    compacted blocks, padded steps."""
+    from oracle import budgets
+    wl = workloads.mistral_pass_8k(n_layers=4, L=3000)
+    wl.n_seq, wl.seq_lens = 2, [3000, 2200]
+    sched = budgets.pyramid_budgets(64, 4, 20.0)
+    assert sched == [125, 85, 43, 3]
+    per_prob = [sched[wl.layer_of(p)] for p in range(wl.n_prob)]
+    _all(gpu_cases.run_gpu(wl, fused=True, budgets=per_prob))
+
+
+def test_depth_decreasing_budgets_fp32_with_options():
+    """fp32 keys (256-thread select), budgets 40 and 16 in one batch, with pool 3 and w_mu 0.5."""
+    wl = workloads.tiny_f32()
+    wl.n_seq, wl.seq_lens = 2, [512, 700]
+    _all(gpu_cases.run_gpu(wl, fused=True, budgets=[40, 16], pool=3, w_mu=0.5))
+
+
 def test_compaction_of_oracle_selection():
     """kv_compact_cache fed with the oracle's admissions reproduces the oracle's compacted rows."""
     import torch
