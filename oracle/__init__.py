@@ -9,5 +9,7 @@ Modules
   evict     -- window attention, mean/dispersion statistics, base score, normalisation, top-4B
                candidate restriction, greedy MMR admission and cache compaction (sections 3.1, 3.2)
   profiles  -- per-layer coefficients from the Global / Segments / Curve depth profiles (section 3.3)
+  budgets   -- per-layer budgets that fall with depth at the total of a uniform budget (section 3.1)
+  decode    -- attention of a generated token over the compacted cache (section 4.3)
 """
-from . import evict, profiles  # noqa: F401
+from . import budgets, decode, evict, profiles  # noqa: F401

@@ -552,3 +552,44 @@ def test_pyramid_budgets_invariants(B, n, beta):
         assert b == [B] * n
     if n > 1:
         assert b[0] == 2 * B - b_min and b[-1] == b_min
+
+
+# ------------------------------------------------------------------------------------------------
+# Decode attention over the compacted cache
+# ------------------------------------------------------------------------------------------------
+
+def test_decode_attention_against_sdpa():
+    """GQA decode (8 query heads on 2 kv heads, one query token) against torch's scaled dot-product
+    attention in float64 with the kv heads repeated per group."""
+    from oracle import decode
+    rng = np.random.default_rng(41)
+    q = rng.standard_normal((8, 16))
+    k = rng.standard_normal((2, 37, 16))
+    v = rng.standard_normal((2, 37, 16))
+    o = decode.decode_attention(q, k, v, 0.3)
+    kt = torch.from_numpy(np.repeat(k, 4, axis=0))
+    vt = torch.from_numpy(np.repeat(v, 4, axis=0))
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q)[:, None, :], kt, vt, scale=0.3)[:, 0, :].numpy()
+    np.testing.assert_allclose(o, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_decode_attention_special_cases():
+    """Identical keys average the values; one row returns its value; a key far along the query
+    returns (nearly) its value; appending k_new / v_new equals attending over the longer cache."""
+    from oracle import decode
+    rng = np.random.default_rng(42)
+    q = rng.standard_normal((2, 8))
+    v = rng.standard_normal((1, 10, 8))
+    k_same = np.tile(rng.standard_normal(8), (1, 10, 1))
+    np.testing.assert_allclose(decode.decode_attention(q, k_same, v, 0.5),
+                               np.tile(v[0].mean(axis=0), (2, 1)), rtol=1e-13)
+    np.testing.assert_allclose(decode.decode_attention(q, k_same[:, :1], v[:, :1], 0.5),
+                               np.tile(v[0, 0], (2, 1)), rtol=1e-15)
+    k = rng.standard_normal((1, 10, 8)) * 0.01
+    k[0, 6] = 400.0 * q[0] / np.linalg.norm(q[0])
+    o = decode.decode_attention(q[:1], k, v, 1.0)
+    np.testing.assert_allclose(o[0], v[0, 6], rtol=1e-9, atol=1e-9)
+    k2 = rng.standard_normal((1, 10, 8))
+    a = decode.decode_attention(q, k2[:, :9], v[:, :9], 0.4, k2[:, 9], v[:, 9])
+    np.testing.assert_array_equal(a, decode.decode_attention(q, k2, v, 0.4))
