@@ -211,15 +211,50 @@ int kv_mmr_select_ex(const kv_problem* pr, const float* mu, const float* sigma, 
 int kv_compact_cache(const kv_problem* pr, const void* k, const void* v, const int32_t* sel_idx,
                      int32_t budget, int32_t keep_tail, void* k_out, void* v_out, void* stream);
 
-/* kv_compact_cache with per-problem budgets (budget_host / budget_dev as in kv_select_opts; both
- * NULL is exactly kv_compact_cache).  The block of every (problem, kv head) keeps its stride of
- * budget + keep_tail rows; rows 0..B_p-1 are the rows of the first B_p selected positions in
- * ascending order, rows B_p..B_p+keep_tail-1 the last keep_tail positions, and the rows after them
- * are not written. */
+/* kv_compact_cache with per-problem budgets and a chosen block size (budget_host / budget_dev as
+ * in kv_select_opts; both NULL with out_rows = 0 is exactly kv_compact_cache).  The block of every
+ * (problem, kv head) in k_out / v_out has out_rows rows (0: budget + keep_tail; otherwise at least
+ * budget + keep_tail, else KV_ERR_ARG), so that rows for generated tokens can follow the kept ones
+ * (kv_decode_attention appends there).  Rows 0..B_p-1 are the rows of the first B_p selected
+ * positions in ascending order, rows B_p..B_p+keep_tail-1 the last keep_tail positions, and the
+ * rows after them are not written. */
 int kv_compact_cache_ex(const kv_problem* pr, const void* k, const void* v,
                         const int32_t* sel_idx, int32_t budget, int32_t keep_tail,
-                        const int32_t* budget_host, const int32_t* budget_dev, void* k_out,
-                        void* v_out, void* stream);
+                        const int32_t* budget_host, const int32_t* budget_dev, int32_t out_rows,
+                        void* k_out, void* v_out, void* stream);
+
+/* A batch of caches for decoding: problem p (one layer of one sequence) holds, for every kv head
+ * g, a block of row_stride rows of d elements starting at row (p * h_kv + g) * row_stride of the
+ * K and V buffers, of which rows 0..len_p-1 are in use (the layout kv_compact_cache_ex writes, with
+ * len_p = B_p + keep_tail).  len_host / len_dev: n_prob lengths in host and device memory. */
+typedef struct kv_cache_batch {
+  int32_t dtype; /* KV_F32 or KV_BF16: caches, queries and new rows */
+  int32_t n_prob;
+  int32_t h_q;
+  int32_t h_kv;
+  int32_t d;
+  int32_t row_stride;
+  const int32_t* len_host;
+  const int32_t* len_dev;
+} kv_cache_batch;
+
+/* Bytes of device workspace kv_decode_attention needs for this batch (0 if none; 256-byte
+ * alignment).  Returns 0 for invalid arguments as well. */
+size_t kv_decode_workspace_bytes(const kv_cache_batch* cb);
+
+/* Attention of one generated token per problem over its cache (section 4.3: after eviction the
+ * model generates against the kept rows of every layer):
+ *   out[p,h,:] = sum_r softmax_r(scale <q[p,h], k[p,g,r]>) v[p,g,r,:],  g = h / (h_q / h_kv),
+ * over the rows r < len_p, plus the token's own row when k_new / v_new are given: then
+ * k_new[p,g,:] / v_new[p,g,:] are also written into row len_p of every block (len_p < row_stride
+ * required), so the next call passes len_p + 1.
+ * q [n_prob, h_q, d] and k_new / v_new [n_prob, h_kv, d] in the cache dtype; out fp32
+ * [n_prob, h_q, d].  Logits, softmax and the weighted sum in fp32.  k_new and v_new both or
+ * neither (KV_ERR_NULL).  h_q / h_kv <= 8, d in {64, 128}, every len_p >= 1 (or >= 0 with a new
+ * row) and <= row_stride, else KV_ERR_SHAPE.  Needs the workspace of kv_decode_workspace_bytes. */
+int kv_decode_attention(const kv_cache_batch* cb, const void* q, void* k_cache, void* v_cache,
+                        const void* k_new, const void* v_new, float scale, float* out, void* ws,
+                        size_t ws_bytes, void* stream);
 
 /* Per-layer budgets that fall with depth at the total of a uniform `budget` (section 3.1: the runs
  * use such an allocation; the paper prints no schedule), host-only.  With

@@ -40,7 +40,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvevict.
 SYMBOLS = ("kv_strerror", "kv_version", "kv_workspace_bytes", "kv_candidate_stride",
            "kv_window_scores", "kv_mu_sigma", "kv_mu_sigma_ex", "kv_window_mu_sigma",
            "kv_window_mu_sigma_ex", "kv_mmr_select", "kv_mmr_select_ex", "kv_compact_cache",
-           "kv_compact_cache_ex", "kv_pyramid_budgets", "kv_depth_profile")
+           "kv_compact_cache_ex", "kv_decode_workspace_bytes", "kv_decode_attention",
+           "kv_pyramid_budgets", "kv_depth_profile")
 
 
 class KvError(RuntimeError):
@@ -54,6 +55,12 @@ class KvProblem(ctypes.Structure):
                 ("h_kv", ctypes.c_int32), ("d", ctypes.c_int32), ("w", ctypes.c_int32),
                 ("len_host", ctypes.c_void_p), ("tok_off_host", ctypes.c_void_p),
                 ("len_dev", ctypes.c_void_p), ("tok_off_dev", ctypes.c_void_p)]
+
+
+class KvCacheBatch(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("n_prob", ctypes.c_int32), ("h_q", ctypes.c_int32),
+                ("h_kv", ctypes.c_int32), ("d", ctypes.c_int32), ("row_stride", ctypes.c_int32),
+                ("len_host", ctypes.c_void_p), ("len_dev", ctypes.c_void_p)]
 
 
 class KvSelectOpts(ctypes.Structure):
@@ -92,14 +99,18 @@ def lib() -> ctypes.CDLL:
         h.kv_mmr_select_ex.argtypes = [pr, vp, vp, vp, vp, vp, i32, i32, i32,
                                        ctypes.POINTER(KvSelectOpts), vp, vp, vp, vp, vp, sz, vp]
         h.kv_compact_cache.argtypes = [pr, vp, vp, vp, i32, i32, vp, vp, vp]
-        h.kv_compact_cache_ex.argtypes = [pr, vp, vp, vp, i32, i32, vp, vp, vp, vp, vp]
+        h.kv_compact_cache_ex.argtypes = [pr, vp, vp, vp, i32, i32, vp, vp, i32, vp, vp, vp]
+        cb = ctypes.POINTER(KvCacheBatch)
+        h.kv_decode_workspace_bytes.argtypes = [cb]
+        h.kv_decode_workspace_bytes.restype = sz
+        h.kv_decode_attention.argtypes = [cb, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp, sz, vp]
         h.kv_pyramid_budgets.argtypes = [i32, i32, ctypes.c_double, ctypes.POINTER(ctypes.c_int32)]
         h.kv_depth_profile.argtypes = [i32, ctypes.POINTER(ctypes.c_double), i32, i32,
                                        ctypes.POINTER(ctypes.c_float)]
         for name in ("kv_window_scores", "kv_mu_sigma", "kv_mu_sigma_ex", "kv_window_mu_sigma",
                      "kv_window_mu_sigma_ex", "kv_mmr_select", "kv_mmr_select_ex",
-                     "kv_compact_cache", "kv_compact_cache_ex", "kv_pyramid_budgets",
-                     "kv_depth_profile"):
+                     "kv_compact_cache", "kv_compact_cache_ex", "kv_decode_attention",
+                     "kv_pyramid_budgets", "kv_depth_profile"):
             getattr(h, name).restype = ctypes.c_int
         _LIB = h
     return _LIB
@@ -282,11 +293,57 @@ def compact_cache(batch: Batch, k, v, sel_idx, budget: int, keep_tail: int, k_ou
 
 
 def compact_cache_ex(batch: Batch, k, v, sel_idx, budget: int, keep_tail: int,
-                     budgets: Optional[Budgets], k_out, v_out, stream=None) -> None:
+                     budgets: Optional[Budgets], k_out, v_out, out_rows: int = 0,
+                     stream=None) -> None:
     bh, bd = budgets.pointers() if budgets is not None else (None, None)
     _check(lib().kv_compact_cache_ex(batch.ref(), _ptr(k), _ptr(v), _ptr(sel_idx), int(budget),
-                                     int(keep_tail), bh, bd, _ptr(k_out), _ptr(v_out),
-                                     _stream(stream)), "kv_compact_cache_ex")
+                                     int(keep_tail), bh, bd, int(out_rows), _ptr(k_out),
+                                     _ptr(v_out), _stream(stream)), "kv_compact_cache_ex")
+
+
+class CacheBatch:
+    """Shape of a batch of caches for decoding (kv_cache_batch): per-problem lengths on the host
+    and the device.  `advance()` adds one row to every length (after a call that appended)."""
+
+    def __init__(self, dtype: str, h_q: int, h_kv: int, d: int, row_stride: int,
+                 lens: Sequence[int], device=None):
+        import torch
+        self.dtype_name = dtype
+        self.h_q, self.h_kv, self.d, self.row_stride = int(h_q), int(h_kv), int(d), int(row_stride)
+        self.lens_host = np.ascontiguousarray(np.asarray(lens, dtype=np.int32))
+        self._dev = torch.device("cuda") if device is None else torch.device(device)
+        self._sync()
+
+    def _sync(self):
+        import torch
+        self.lens_dev = torch.from_numpy(self.lens_host).to(self._dev)
+        self.struct = KvCacheBatch(KV_BF16 if self.dtype_name == "bf16" else KV_F32,
+                                   len(self.lens_host), self.h_q, self.h_kv, self.d,
+                                   self.row_stride, self.lens_host.ctypes.data,
+                                   self.lens_dev.data_ptr())
+
+    def advance(self):
+        self.lens_host = self.lens_host + 1
+        self._sync()
+
+    @property
+    def n_prob(self) -> int:
+        return len(self.lens_host)
+
+    def ref(self):
+        return ctypes.byref(self.struct)
+
+
+def decode_workspace_bytes(cb: CacheBatch) -> int:
+    return int(lib().kv_decode_workspace_bytes(cb.ref()))
+
+
+def decode_attention(cb: CacheBatch, q, k_cache, v_cache, k_new, v_new, scale: float, out,
+                     ws=None, stream=None) -> None:
+    _check(lib().kv_decode_attention(cb.ref(), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_new),
+                                     _ptr(v_new), float(scale), _ptr(out), _ptr(ws),
+                                     0 if ws is None else ws.numel() * ws.element_size(),
+                                     _stream(stream)), "kv_decode_attention")
 
 
 def pyramid_budgets(budget: int, n_layers: int, beta: float) -> np.ndarray:

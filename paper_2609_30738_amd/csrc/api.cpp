@@ -16,6 +16,7 @@ namespace {
 constexpr int kMaxLen = 1 << 24;
 constexpr int kMaxGrid = 65535;
 constexpr int kMaxCompactBudget = 8192;
+constexpr float kLog2eF = 1.4426950408889634f;  // log2(e): kernels take logits in base 2
 constexpr int kMaxPool = 63;  // widest max-pool window of kv_mmr_select_ex
 constexpr size_t kWsAlign = 256;
 
@@ -294,14 +295,14 @@ int kv_mmr_select_ex(const kv_problem* pr, const float* mu, const float* sigma, 
 
 int kv_compact_cache(const kv_problem* pr, const void* k, const void* v, const int32_t* sel_idx,
                      int32_t budget, int32_t keep_tail, void* k_out, void* v_out, void* stream) {
-  return kv_compact_cache_ex(pr, k, v, sel_idx, budget, keep_tail, nullptr, nullptr, k_out, v_out,
-                             stream);
+  return kv_compact_cache_ex(pr, k, v, sel_idx, budget, keep_tail, nullptr, nullptr, 0, k_out,
+                             v_out, stream);
 }
 
 int kv_compact_cache_ex(const kv_problem* pr, const void* k, const void* v,
                         const int32_t* sel_idx, int32_t budget, int32_t keep_tail,
-                        const int32_t* budget_host, const int32_t* budget_dev, void* k_out,
-                        void* v_out, void* stream) {
+                        const int32_t* budget_host, const int32_t* budget_dev, int32_t out_rows,
+                        void* k_out, void* v_out, void* stream) {
   kv::Shape s;
   int st = check_problem(pr, &s);
   if (st != KV_OK) return st;
@@ -312,8 +313,80 @@ int kv_compact_cache_ex(const kv_problem* pr, const void* k, const void* v,
   st = check_budgets(pr, budget, keep_tail, budget_host, budget_dev);
   if (st != KV_OK) return st;
   if (budget > kMaxCompactBudget) return KV_ERR_BUDGET;
-  return launch_status(kv::launch_compact(s, k, v, sel_idx, budget, budget_dev, keep_tail, k_out,
-                                          v_out, static_cast<hipStream_t>(stream)));
+  if (out_rows == 0) out_rows = budget + keep_tail;
+  if (out_rows < budget + keep_tail) return KV_ERR_ARG;
+  return launch_status(kv::launch_compact(s, k, v, sel_idx, budget, budget_dev, keep_tail,
+                                          out_rows, k_out, v_out,
+                                          static_cast<hipStream_t>(stream)));
+}
+
+namespace {
+
+int check_cache_batch(const kv_cache_batch* cb) {
+  if (!cb) return KV_ERR_NULL;
+  if (cb->dtype != KV_F32 && cb->dtype != KV_BF16) return KV_ERR_DTYPE;
+  if (cb->n_prob < 1 || cb->n_prob > kMaxGrid) return KV_ERR_ARG;
+  if (!cb->len_host || !cb->len_dev) return KV_ERR_NULL;
+  if (cb->h_kv < 1 || cb->h_kv > kMaxGrid || cb->h_q < cb->h_kv || cb->h_q % cb->h_kv != 0 ||
+      cb->h_q / cb->h_kv > 8)
+    return KV_ERR_SHAPE;
+  if (cb->d != 64 && cb->d != 128) return KV_ERR_SHAPE;
+  if (cb->row_stride < 1 || cb->row_stride > kMaxLen) return KV_ERR_SHAPE;
+  for (int p = 0; p < cb->n_prob; ++p)
+    if (cb->len_host[p] < 0 || cb->len_host[p] > cb->row_stride) return KV_ERR_SHAPE;
+  return KV_OK;
+}
+
+kv::DecodePlan decode_plan_of(const kv_cache_batch* cb) {
+  int max_len = 0;
+  for (int p = 0; p < cb->n_prob; ++p) max_len = std::max(max_len, (int)cb->len_host[p]);
+  return kv::decode_plan(cb->n_prob, cb->h_kv, max_len);
+}
+
+}  // namespace
+
+size_t kv_decode_workspace_bytes(const kv_cache_batch* cb) {
+  if (check_cache_batch(cb) != KV_OK) return 0;
+  return align_up(kv::decode_ws_bytes(cb->n_prob, cb->h_q, cb->d, decode_plan_of(cb)));
+}
+
+int kv_decode_attention(const kv_cache_batch* cb, const void* q, void* k_cache, void* v_cache,
+                        const void* k_new, const void* v_new, float scale, float* out, void* ws,
+                        size_t ws_bytes, void* stream) {
+  int st = check_cache_batch(cb);
+  if (st != KV_OK) return st;
+  if (!q || !k_cache || !v_cache || !out) return KV_ERR_NULL;
+  if ((k_new == nullptr) != (v_new == nullptr)) return KV_ERR_NULL;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) ||
+      (k_new && (!aligned16(k_new) || !aligned16(v_new))))
+    return KV_ERR_ARG;
+  if (!std::isfinite(scale)) return KV_ERR_ARG;
+  for (int p = 0; p < cb->n_prob; ++p) {
+    const int len = cb->len_host[p];
+    if (k_new ? len >= cb->row_stride : len < 1) return KV_ERR_SHAPE;
+  }
+  const kv::DecodePlan plan = decode_plan_of(cb);
+  if (plan.n_split > kMaxGrid) return KV_ERR_SHAPE;
+  const size_t need = align_up(kv::decode_ws_bytes(cb->n_prob, cb->h_q, cb->d, plan));
+  if (need > 0 && (ws_bytes < need || !ws || (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1))))
+    return KV_ERR_WORKSPACE;
+  kv::DecodeArgs a;
+  a.q = q;
+  a.k = k_cache;
+  a.v = v_cache;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.lens = cb->len_dev;
+  a.h_q = cb->h_q;
+  a.h_kv = cb->h_kv;
+  a.row_stride = cb->row_stride;
+  a.c = scale * kLog2eF;
+  a.split_rows = plan.split_rows;
+  a.n_split = plan.n_split;
+  a.out = out;
+  a.part = static_cast<float*>(ws);
+  return launch_status(kv::launch_decode(cb->dtype == KV_BF16 ? kv::kDtBf16 : kv::kDtF32, cb->d,
+                                         cb->n_prob, a, static_cast<hipStream_t>(stream)));
 }
 
 int kv_pyramid_budgets(int32_t budget, int32_t n_layers, double beta, int32_t* budgets_host) {

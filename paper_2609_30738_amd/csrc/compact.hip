@@ -3,7 +3,7 @@
 // One workgroup per (problem, kv head): the B_p admitted positions (B_p = the problem's own budget,
 // or the uniform B) are sorted in LDS (bitonic sort over the next power of two, padded with
 // INT_MAX), then the kept rows of K and V are copied with 16-byte vector loads and stores into rows
-// 0 .. B_p + keep_tail - 1 of the unit's block of B + keep_tail rows.  Rows are opaque bytes, so the
+// 0 .. B_p + keep_tail - 1 of the unit's block of out_rows rows.  Rows are opaque bytes, so the
 // copy is exact for every dtype.
 #include <limits.h>
 
@@ -20,7 +20,7 @@ constexpr int kMaxSortedBudget = 8192;
 __global__ __launch_bounds__(kThreads) void compact_kernel(
     const uint4* __restrict__ k, const uint4* __restrict__ v, const int32_t* __restrict__ sel_idx,
     const int32_t* __restrict__ lens, const int64_t* __restrict__ tok_off, int h_kv,
-    int row_vecs, int budget, const int32_t* __restrict__ budgets, int keep_tail,
+    int row_vecs, int budget, const int32_t* __restrict__ budgets, int keep_tail, int out_rows,
     uint4* __restrict__ k_out, uint4* __restrict__ v_out) {
   __shared__ int32_t srt[kMaxSortedBudget];
   const int g = blockIdx.x % h_kv, p = blockIdx.x / h_kv;
@@ -49,7 +49,7 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(
   }
   const int rows = bp + keep_tail;
   const size_t src_base = ((size_t)tok_off[p] * h_kv + (size_t)g * L) * row_vecs;
-  const size_t dst_base = ((size_t)p * h_kv + g) * (budget + keep_tail) * row_vecs;
+  const size_t dst_base = ((size_t)p * h_kv + g) * out_rows * row_vecs;
   for (int e = threadIdx.x; e < rows * row_vecs; e += kThreads) {
     const int r = e / row_vecs, c = e % row_vecs;
     const int pos = r < bp ? srt[r] : L - keep_tail + (r - bp);
@@ -61,14 +61,14 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(
 }
 
 hipError_t launch_compact(const Shape& s, const void* k, const void* v, const int32_t* sel_idx,
-                          int budget, const int32_t* budgets, int keep_tail, void* k_out,
-                          void* v_out, hipStream_t stream) {
+                          int budget, const int32_t* budgets, int keep_tail, int out_rows,
+                          void* k_out, void* v_out, hipStream_t stream) {
   if (budget > kMaxSortedBudget) return hipErrorInvalidValue;
   const int elem = s.dtype == kDtBf16 ? 2 : 4;
   const int row_vecs = s.d * elem / 16;
   compact_kernel<<<dim3((unsigned)(s.n_prob * s.h_kv)), kThreads, 0, stream>>>(
       static_cast<const uint4*>(k), static_cast<const uint4*>(v), sel_idx, s.lens, s.tok_off,
-      s.h_kv, row_vecs, budget, budgets, keep_tail, static_cast<uint4*>(k_out),
+      s.h_kv, row_vecs, budget, budgets, keep_tail, out_rows, static_cast<uint4*>(k_out),
       static_cast<uint4*>(v_out));
   return hipGetLastError();
 }

@@ -86,7 +86,28 @@ int select_max_candidates(int d, int elem_bytes);
 hipError_t launch_mmr_select(const Shape& s, const SelectArgs& a, hipStream_t stream);
 
 hipError_t launch_compact(const Shape& s, const void* k, const void* v, const int32_t* sel_idx,
-                          int budget, const int32_t* budgets, int keep_tail, void* k_out,
-                          void* v_out, hipStream_t stream);
+                          int budget, const int32_t* budgets, int keep_tail, int out_rows,
+                          void* k_out, void* v_out, hipStream_t stream);
+
+// Decode attention over a compacted cache (decode.hip).
+struct DecodeArgs {
+  const void* q;      // [n_prob][h_q][d]
+  void* k;            // [n_prob][h_kv][row_stride][d]; row len_p is written when k_new is set
+  void* v;
+  const void* k_new;  // [n_prob][h_kv][d] or null
+  const void* v_new;
+  const int32_t* lens;
+  int h_q, h_kv, row_stride;
+  float c;            // softmax scale * log2(e)
+  int split_rows, n_split;
+  float* out;         // [n_prob][h_q][d]
+  float* part;        // [n_prob][h_q][n_split][d + 2] when n_split > 1
+};
+struct DecodePlan {
+  int n_split, split_rows;
+};
+DecodePlan decode_plan(int n_prob, int h_kv, int max_len);
+size_t decode_ws_bytes(int n_prob, int h_q, int d, const DecodePlan& plan);
+hipError_t launch_decode(int dtype, int d, int n_prob, const DecodeArgs& a, hipStream_t stream);
 
 }  // namespace kv

@@ -27,6 +27,9 @@ Recipe (per problem = one (sequence, layer), seed ``[config_id, sequence, layer]
   * values are random bf16 numbers (random sign and mantissa, exponent 2^-7..2^2): they are only ever
     gathered, never used in arithmetic.
 
+Decode over compacted caches (draw_decode): queries, keys, values and the new token's key/value
+~ N(0, 1), a few rows of every block's keys scaled by 4 (dominant rows), scale 1/sqrt(d).
+
 bf16 tensors are returned as their raw uint16 bit patterns (round-to-nearest-even from fp32).
 """
 from __future__ import annotations
@@ -367,3 +370,51 @@ def all_workloads() -> List[Workload]:
     return [tiny_f32(), mistral_layer(), mistral_pass_8k(32), mistral_pass_8k(64),
             mistral_pass_8k(128), mistral_pass_32k(), ragged_batch("dispersion_only"),
             ragged_batch("redundancy_only"), ragged_batch("both")]
+
+
+# --------------------------------------------------------------------------------------------
+# Decode over compacted caches
+# --------------------------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class DecodeInputs:
+    """A batch of caches in the block layout of kv_cache_batch plus one generated token each.
+
+    q [n_prob, h_q, d]; k, v [n_prob, h_kv, row_stride, d] (every row filled, rows >= len too);
+    k_new, v_new [n_prob, h_kv, d]; bf16 as uint16 bit patterns."""
+    dtype: str
+    h_q: int
+    h_kv: int
+    d: int
+    row_stride: int
+    lens: np.ndarray
+    q: np.ndarray
+    k: np.ndarray
+    v: np.ndarray
+    k_new: np.ndarray
+    v_new: np.ndarray
+
+    @property
+    def scale(self) -> float:
+        return float(1.0 / np.sqrt(self.d))
+
+
+def draw_decode(dtype: str, h_q: int, h_kv: int, d: int, row_stride: int, lens: Sequence[int],
+                seed: int = 0, peak_rows: int = 4) -> DecodeInputs:
+    """Random queries, keys and values ~ N(0, 1); in every block `peak_rows` rows of K are scaled
+    by 4 so that the softmax has a few dominant rows, as attention to kept heavy hitters does."""
+    rng = np.random.default_rng([7, seed])
+    n = len(lens)
+    k = rng.standard_normal((n, h_kv, row_stride, d)).astype(np.float32)
+    for p in range(n):
+        for g in range(h_kv):
+            rows = rng.integers(0, max(1, int(lens[p])), peak_rows)
+            k[p, g, rows] *= 4.0
+    v = rng.standard_normal((n, h_kv, row_stride, d)).astype(np.float32)
+    q = rng.standard_normal((n, h_q, d)).astype(np.float32)
+    k_new = rng.standard_normal((n, h_kv, d)).astype(np.float32)
+    v_new = rng.standard_normal((n, h_kv, d)).astype(np.float32)
+    if dtype == BF16:
+        k, v, q, k_new, v_new = (f32_to_bf16_bits(x) for x in (k, v, q, k_new, v_new))
+    return DecodeInputs(dtype, h_q, h_kv, d, row_stride, np.asarray(lens, dtype=np.int32), q, k,
+                        v, k_new, v_new)

@@ -178,8 +178,8 @@ def test_per_problem_budget_checks():
     def compact_ex(values, budget=64, keep_tail=32, host=True):
         b = np.asarray(values, dtype=np.int32)
         return lib.kv_compact_cache_ex(pr.ref(), P, P, P, budget, keep_tail,
-                                       ctypes.c_void_p(b.ctypes.data) if host else NULL, P, P, P,
-                                       NULL)
+                                       ctypes.c_void_p(b.ctypes.data) if host else NULL, P, 0, P,
+                                       P, NULL)
     assert sel_ex([64, 0]) == _lib.KV_ERR_BUDGET
     assert sel_ex([65, 10]) == _lib.KV_ERR_BUDGET           # above the stride
     assert sel_ex([64, 69], budget=64) == _lib.KV_ERR_BUDGET  # 100 - 32 = 68 candidates
@@ -205,6 +205,47 @@ def test_pyramid_budget_errors():
     assert lib.kv_pyramid_budgets(8, 4, 0.5, out) == _lib.KV_ERR_ARG
     assert lib.kv_pyramid_budgets(8, 4, float("nan"), out) == _lib.KV_ERR_ARG
     assert lib.kv_pyramid_budgets(8, 4, 2.0, None) == _lib.KV_ERR_NULL
+
+
+def _cache_batch(dtype=_lib.KV_BF16, h_q=32, h_kv=8, d=128, stride=100, lens=(96, 50)):
+    ln = np.asarray(lens, dtype=np.int32)
+    cb = _lib.KvCacheBatch(dtype, len(lens), h_q, h_kv, d, stride, ln.ctypes.data, ln.ctypes.data)
+    return cb, ln
+
+
+def test_decode_checks():
+    lib = _lib.lib()
+
+    def call(cb, q=P, kn=P, vn=P, scale=0.08, ws=P, ws_bytes=1 << 30):
+        return lib.kv_decode_attention(ctypes.byref(cb), q, P, P, kn, vn, scale, P, ws, ws_bytes,
+                                       NULL)
+    for kw, code in [(dict(dtype=5), _lib.KV_ERR_DTYPE), (dict(h_q=30), _lib.KV_ERR_SHAPE),
+                     (dict(h_q=72, h_kv=8), _lib.KV_ERR_SHAPE), (dict(d=96), _lib.KV_ERR_SHAPE),
+                     (dict(lens=(101,)), _lib.KV_ERR_SHAPE), (dict(lens=(-1,)), _lib.KV_ERR_SHAPE)]:
+        cb, keep = _cache_batch(**kw)
+        assert call(cb) == code, kw
+        assert lib.kv_decode_workspace_bytes(ctypes.byref(cb)) == 0
+    cb, keep = _cache_batch(lens=(100,))
+    assert call(cb) == _lib.KV_ERR_SHAPE                     # no room to append
+    cb, keep = _cache_batch(lens=(0,))
+    assert call(cb, kn=NULL, vn=NULL) == _lib.KV_ERR_SHAPE   # nothing to attend to
+    cb, keep = _cache_batch()
+    assert call(cb, kn=NULL) == _lib.KV_ERR_NULL
+    assert call(cb, q=NULL) == _lib.KV_ERR_NULL
+    assert call(cb, q=ctypes.c_void_p(BUF.ctypes.data + 4)) == _lib.KV_ERR_ARG
+    assert call(cb, scale=float("inf")) == _lib.KV_ERR_ARG
+    # a long cache with few units splits its rows and needs a workspace
+    big, keep = _cache_batch(stride=40000, lens=(30000,))
+    need = lib.kv_decode_workspace_bytes(ctypes.byref(big))
+    assert need > 0 and need % 256 == 0
+    assert call(big, ws_bytes=need - 256) == _lib.KV_ERR_WORKSPACE
+    assert call(big, ws=NULL, ws_bytes=need) == _lib.KV_ERR_WORKSPACE
+
+
+def test_compact_block_size_check():
+    pr = HostProblem()
+    assert _lib.lib().kv_compact_cache_ex(pr.ref(), P, P, P, 64, 32, NULL, NULL, 95, P, P,
+                                          NULL) == _lib.KV_ERR_ARG
 
 
 # ------------------------------------------------------------------------------------------------
