@@ -137,4 +137,4 @@ def run_pass(inp: DeviceInputs, out: PassOutputs, budget: int, cand_mult: int = 
                            out.cand_corr, out.ws, pool=pool, w_mu=w_mu, budgets=budgets,
                            stream=stream)
         _lib.compact_cache_ex(b, inp.k, inp.v, out.sel_idx, budget, tail, budgets, out.k_out,
-                              out.v_out, stream)
+                              out.v_out, stream=stream)
