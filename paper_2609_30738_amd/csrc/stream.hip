@@ -2,19 +2,20 @@
 // passes over the keys, each a plain stream from HBM with no communication between workgroups.
 //
 //   Work item: one segment of `seg_keys` consecutive keys of one (problem, kv head) unit, 512
-//   threads = 8 waves.  The unit's R = 32 G window rows are staged in LDS once; every wave streams
-//   32-key tiles (tile j of the segment goes to wave j % 8) straight from HBM into MFMA operand
-//   registers, two tiles ahead of the one it computes.
+//   threads = 8 waves.  Every lane holds the MFMA fragments of its window rows of all G heads of
+//   the unit in registers for the whole segment.  Each wave streams 32-key tiles (tile j of the
+//   segment goes to wave j % 8) from HBM into a private two-tile ring in LDS with direct-to-LDS,
+//   non-temporal loads: every load instruction covers 1 KiB of consecutive key bytes (four 256-byte
+//   rows at d = 128), and each lane picks the 16-byte chunk that lands at its LDS position, so the
+//   tile is stored with its chunks XOR-swizzled by row (chunk c of row r at slot c ^ (r mod CH)).
+//   The MFMA operand reads of 16 consecutive rows then touch 16 different chunk slots (all banks).
+//   While a tile is computed, the next two are in flight.
 //
 //   stats_stream_kernel (pass 1): logits D[key][row] = K Q^T with keys as the MFMA M dimension, so
-//     a lane holds one window row and 16 keys of each tile.  Every lane keeps, for its rows, a
-//     running offset m, the sum z of 2^(t - m) and the largest term e = 2^(t_max - m)
-//     (t = logit * scale * log2 e).  A tile is summed against the running offset directly; only
-//     when that sum is not below 2^32 (the first tile, a larger logit, an overflow) is the tile's
-//     maximum logit taken and the lane rebased on it, so the common tile needs no maximum of the
-//     logits, only one of its exponentials.  At the end every lane converts to the row maximum
-//     m + log2 e and the sum z / e relative to it; the lanes, then the waves, are merged and the
-//     segment's (max, sum) per row goes to the workspace.
+//     a lane holds one window row and 16 keys of each tile.  Every lane keeps, per head, the exact
+//     running maximum m of t = logit * scale * log2 e and the sum z of 2^(t - m), rescaled when m
+//     grows (online softmax).  At the end the lanes, then the waves, are merged and the segment's
+//     (max, sum) per row goes to the workspace.
 //   mu_sigma_stream_kernel (pass 2): merges the segment partials of its unit into the normalisers
 //     b = M + log2 Z (segment 0 also writes row_max / row_sum), or takes them from given
 //     row_max / row_sum; then logits again with keys as N (a lane holds one key),
@@ -22,6 +23,9 @@
 //     the 32 window rows, stored as mu / sigma.  With `sigma_all` the variance runs over all G x 32
 //     (head, row) values instead: every head's mean and squared deviations over its 32 rows, merged
 //     across heads with the pairwise update of Chan, Golub and LeVeque.
+//
+//   Tiles with a masked key (the causal triangle of the window, keys past the segment end) take a
+//   separate, guarded path; every other tile runs without masks or branches.
 #include <algorithm>
 #include <type_traits>
 
@@ -35,8 +39,6 @@ namespace {
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
 constexpr int kTileKeys = 32;
-constexpr int kSlots = 3;  // register slots of key tiles per wave (kSlots - 1 tiles in flight)
-static_assert(kSlots == 3 || kSlots == 4, "the tile loop is unrolled for three or four slots");
 
 struct StreamArgs {
   const uint16_t* q_win;
@@ -57,50 +59,110 @@ struct StreamArgs {
 };
 
 template <int D, int NB> struct SGeo {
-  static constexpr int R = NB * 32;       // window rows of a unit (G heads x 32)
-  static constexpr int NS = D / 16;       // MFMA K steps
-  static constexpr int CH = D * 2 / 16;   // 16-byte chunks of a query row
-  // chunk `ch` of query row `row` sits at chunk ch ^ (row % CH) of the row in LDS, so that a
-  // fragment read of 16 consecutive rows touches 16 different chunks (all banks)
-  __device__ static int qslot(int row, int ch) { return row * CH + (ch ^ (row % CH)); }
+  static constexpr int R = NB * 32;          // window rows of a unit (G heads x 32)
+  static constexpr int NS = D / 16;          // MFMA K steps
+  static constexpr int CH = D * 2 / 16;      // 16-byte chunks of a key row
+  static constexpr int TE = kTileKeys * D;   // elements of a tile
+  static constexpr int NDMA = TE * 2 / 1024; // 1 KiB load instructions per tile
+  // LDS slot (in 16-byte chunks) of chunk `ch` of tile row `row`
+  __device__ static int slot_of(int row, int ch) { return row * CH + (ch ^ (row % CH)); }
 };
+
+typedef const __attribute__((address_space(1))) void* gptr_t;
+typedef __attribute__((address_space(3))) void* lptr_t;
+
+// s_waitcnt vmcnt(N): at most N vector memory operations of this wave still outstanding.  Vector
+// memory operations complete in issue order, so this waits for everything issued before the last N.
+template <int N> __device__ __forceinline__ void wait_vmem() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// maximum of three values (NaN-propagating, no canonicalisation of the operands)
+__device__ __forceinline__ float fmax3(float a, float b, float c) {
+  return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+}
 
 __device__ __forceinline__ float sum_halves(float x) {  // x + x of lane ^ 32
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// The unit's window rows (heads g G .. g G + G - 1 of problem p, contiguous in q_win) into LDS.
-template <int D, int NB>
-__device__ __forceinline__ void stage_unit_queries(const uint16_t* __restrict__ qg, uint16_t* qs) {
+// Per-wave key stream of one segment: a two-tile ring in LDS filled by direct-to-LDS loads.
+template <int D, int NB> struct KeyStream {
   using Gm = SGeo<D, NB>;
-  for (int e = threadIdx.x; e < Gm::R * Gm::CH; e += kThreads) {
-    const int row = e / Gm::CH, ch = e % Gm::CH;
-    *reinterpret_cast<bf16x8_t*>(qs + Gm::qslot(row, ch) * 8) =
-        *reinterpret_cast<const bf16x8_t*>(qg + 8 * e);
+  uint16_t* ring;       // this wave's two tiles
+  const uint16_t* kg;   // keys of the unit
+  int k0, k1, wave, lane;
+
+  __device__ int tile_key(int j) const { return k0 + (j * kWaves + wave) * kTileKeys; }
+
+  // tile j into ring slot j & 1; rows past the segment end re-read its last key
+  __device__ __forceinline__ void issue(int j) const {
+    const int t0 = tile_key(j);
+    uint16_t* dst = ring + (j & 1) * Gm::TE;
+#pragma unroll
+    for (int i = 0; i < Gm::NDMA; ++i) {
+      const int pos = 64 * i + lane;  // LDS chunk slot written by this lane
+      const int row = pos / Gm::CH;
+      const int ch = (pos % Gm::CH) ^ (row % Gm::CH);
+      const uint16_t* src = kg + (size_t)min(t0 + row, k1 - 1) * D + ch * 8;
+      // aux 2: non-temporal (the keys are read once per pass)
+      __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)(dst + i * 512), 16, 0, 2);
+    }
   }
-}
 
-// query fragments of head b (window rows b*32 + l32), all K steps
+  // MFMA operand fragments of tile j (lane: row l32, K half `half`), once its loads have landed
+  __device__ __forceinline__ void read(bf16x8_t (&a)[Gm::NS], int j, int l32, int half) const {
+    const uint16_t* src = ring + (j & 1) * Gm::TE;
+#pragma unroll
+    for (int s = 0; s < Gm::NS; ++s)
+      a[s] = *reinterpret_cast<const bf16x8_t*>(src + Gm::slot_of(l32, 2 * s + half) * 8);
+  }
+
+  // Wait for tile j (tile j + 1, if issued, may stay in flight), copy it into registers and hand
+  // its slot to tile j + 2.  STORES: vector memory stores the caller issues per tile, after the
+  // tile's computation; the tile's loads are then followed by the stores of tiles j - 2 and j - 1
+  // and the loads of tile j + 1.
+  template <int STORES>
+  __device__ __forceinline__ void next(bf16x8_t (&a)[Gm::NS], int j, int my_tiles, int l32,
+                                       int half) const {
+    if (j + 1 < my_tiles) wait_vmem<Gm::NDMA + 2 * STORES>();
+    else wait_vmem<0>();
+    read(a, j, l32, half);
+    wait_lds();
+    if (j + 2 < my_tiles) issue(j + 2);
+  }
+};
+
+// the unit's window-row fragments of every head (head b, rows b * 32 + l32), all K steps
 template <int D, int NB>
-__device__ __forceinline__ void read_qfrags(bf16x8_t (&qf)[D / 16], const uint16_t* qs, int b,
-                                            int l32, int half) {
-  using Gm = SGeo<D, NB>;
-  const int row = b * 32 + l32;
+__device__ __forceinline__ void load_queries(bf16x8_t (&q)[NB][D / 16], const uint16_t* qg, int l32,
+                                             int half) {
 #pragma unroll
-  for (int s = 0; s < Gm::NS; ++s)
-    qf[s] = *reinterpret_cast<const bf16x8_t*>(qs + Gm::qslot(row, 2 * s + half) * 8);
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s)
+      q[b][s] = *reinterpret_cast<const bf16x8_t*>(qg + (size_t)(b * 32 + l32) * D + 16 * s + 8 * half);
 }
 
-// keys of this wave's tile starting at key t0 of the unit; a lane's key is clamped to the last key
-// of the segment (kend - 1), so that the prefetches past the segment's last tile re-read one row
-// instead of the next segment
-template <int D>
-__device__ __forceinline__ void load_tile(bf16x8_t (&t)[D / 16], const uint16_t* kg, int t0,
-                                          int kend, int l32, int half) {
-  const uint16_t* row = kg + (size_t)min(t0 + l32, kend - 1) * D + 8 * half;
+// An empty use of every query register: the compiler waits for the query loads here, once,
+// instead of at the first MFMA of the tile loop, where its wait would also cover the key tiles in
+// flight.
+template <int D, int NB>
+__device__ __forceinline__ void hold_until_loaded(bf16x8_t (&q)[NB][D / 16]) {
 #pragma unroll
-  for (int s = 0; s < D / 16; ++s) t[s] = *reinterpret_cast<const bf16x8_t*>(row + 16 * s);
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) asm volatile("" ::"v"(q[b][s]));
+}
+
+template <int NS>
+__device__ __forceinline__ f32x16_t chain(const bf16x8_t (&x)[NS], const bf16x8_t (&y)[NS]) {
+  f32x16_t d = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < NS; ++s) d = mfma_step(x[s], y[s], d);
+  return d;
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -110,7 +172,7 @@ template <int D, int NB>
 __global__ __launch_bounds__(kThreads, 1) void stats_stream_kernel(StreamArgs a) {
   using Gm = SGeo<D, NB>;
   constexpr int R = Gm::R, NS = Gm::NS;
-  __shared__ __align__(16) uint16_t qs[R * D];
+  __shared__ __align__(16) uint16_t ring[kWaves][2 * Gm::TE];
   __shared__ float2 red[kWaves][R];
 
   const int seg = blockIdx.x, g = blockIdx.y, p = blockIdx.z;
@@ -123,104 +185,79 @@ __global__ __launch_bounds__(kThreads, 1) void stats_stream_kernel(StreamArgs a)
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const float c = a.c;
 
-  stage_unit_queries<D, NB>(a.q_win + ((size_t)p * a.h_q + (size_t)g * G) * 32 * D, qs);
-  const uint16_t* kg = a.k + ((size_t)a.tok_off[p] * a.h_kv + (size_t)g * L) * D;
+  KeyStream<D, NB> ks{ring[wave], a.k + ((size_t)a.tok_off[p] * a.h_kv + (size_t)g * L) * D, k0, k1,
+                      wave, lane};
   const int n_tiles = (k1 - k0 + kTileKeys - 1) / kTileKeys;
   const int my_tiles = n_tiles > wave ? (n_tiles - wave + kWaves - 1) / kWaves : 0;
-  auto tile_key = [&](int j) { return k0 + (j * kWaves + wave) * kTileKeys; };
+  // the query loads go first: vector memory operations complete in issue order, so the waits on
+  // key tiles below also cover them
+  bf16x8_t q[NB][NS];
+  load_queries<D, NB>(q, a.q_win + ((size_t)p * a.h_q + (size_t)g * G) * 32 * D, l32, half);
+  if (my_tiles > 0) ks.issue(0);
+  if (my_tiles > 1) ks.issue(1);
+  hold_until_loaded<D, NB>(q);
 
-  float m_run[NB], z_run[NB], e_run[NB];
+  float m_run[NB], z_run[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
     m_run[b] = -INFINITY;
     z_run[b] = 0.f;
-    e_run[b] = 0.f;
   }
-  bf16x8_t slot[kSlots][NS];
+  // a tile is interior when none of its keys is masked: t0 + 31 < min(k1, L - 31)
+  const int kedge = min(k1, L - 31);
+  for (int j = 0; j < my_tiles; ++j) {
+    bf16x8_t kt[NS];
+    ks.template next<0>(kt, j, my_tiles, l32, half);
+    const int t0 = ks.tile_key(j);
+    if (t0 + 31 < kedge) {
 #pragma unroll
-  for (int q = 0; q + 1 < kSlots; ++q) load_tile<D>(slot[q], kg, tile_key(q), k1, l32, half);
-  __syncthreads();
-
-  auto tile = [&](const bf16x8_t (&t)[NS], int t0) __attribute__((always_inline)) {
-    // window row l32 of every head sees keys <= L - 32 + l32; keys >= k1 belong to the next
-    // segment.  The key of register j is t0 + 4 half + 8 (j / 4) + (j % 4).
-    const bool edge = t0 + 31 >= min(k1, L - 31);
-    const int thr = min(k1 - 1, L - 32 + l32) - t0 - 4 * half;
-    // heads one after another: the scheduling barrier at the end of each keeps the compiler from
-    // hoisting the next head's fragment reads (registers stay at one head's worth)
+      for (int b = 0; b < NB; ++b) {
+        const f32x16_t d = chain<NS>(kt, q[b]);
+        float mx = fmax3(fmax3(fmax3(d[0], d[1], d[2]), d[3], d[4]), d[5], d[6]);
+        mx = fmax3(fmax3(mx, d[7], d[8]), d[9], d[10]);
+        mx = fmax3(fmax3(mx, d[11], d[12]), d[13], d[14]);
+        const float mn = __builtin_elementwise_maximum(m_run[b], __builtin_elementwise_maximum(mx, d[15]) * c);
+        const float keep = __builtin_amdgcn_exp2f(m_run[b] - mn);  // 0 on the lane's first tile
+        float ex[16];
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      bf16x8_t qf[NS];
-      read_qfrags<D, NB>(qf, qs, b, l32, half);
-      f32x16_t d = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        for (int jj = 0; jj < 16; ++jj) ex[jj] = __builtin_amdgcn_exp2f(fmaf(d[jj], c, -mn));
+        float zs[4];
 #pragma unroll
-      for (int s = 0; s < NS; ++s) d = mfma_step(t[s], qf[s], d);
-      if (edge) {
-#pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if (8 * (j >> 2) + (j & 3) > thr) d[j] = -INFINITY;
+        for (int u = 0; u < 4; ++u) zs[u] = (ex[4 * u] + ex[4 * u + 1]) + (ex[4 * u + 2] + ex[4 * u + 3]);
+        z_run[b] = fmaf(z_run[b], keep, (zs[0] + zs[1]) + (zs[2] + zs[3]));
+        m_run[b] = mn;
       }
-      const float mo = m_run[b];
-      float ex[16];
+    } else {
+      // window row l32 of every head sees keys <= L - 32 + l32; keys >= k1 belong to the next
+      // segment.  The key of register jj is t0 + 4 half + 8 (jj / 4) + (jj % 4).
+      const int thr = min(k1 - 1, L - 32 + l32) - t0 - 4 * half;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) ex[j] = __builtin_amdgcn_exp2f(fmaf(d[j], c, -mo));
-      // the terms are not negative: their bit patterns order like their values
-      float zs[4];
-      unsigned es[4];
+      for (int b = 0; b < NB; ++b) {
+        f32x16_t d = chain<NS>(kt, q[b]);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        zs[u] = (ex[4 * u] + ex[4 * u + 1]) + (ex[4 * u + 2] + ex[4 * u + 3]);
-        es[u] = max(max(__float_as_uint(ex[4 * u]), __float_as_uint(ex[4 * u + 1])),
-                    max(__float_as_uint(ex[4 * u + 2]), __float_as_uint(ex[4 * u + 3])));
-      }
-      const float zt = (zs[0] + zs[1]) + (zs[2] + zs[3]);
-      if (zt <= 4294967296.f) {
-        z_run[b] += zt;
-        e_run[b] = __uint_as_float(max(__float_as_uint(e_run[b]), max(max(es[0], es[1]), max(es[2], es[3]))));
-      } else {
-        // first tile of the lane, a larger logit or an overflow (also NaN from -inf - -inf):
-        // rebase on the larger of the offset and the tile's maximum logit
+        for (int jj = 0; jj < 16; ++jj)
+          if (8 * (jj >> 2) + (jj & 3) > thr) d[jj] = -INFINITY;
         float mx = d[0];
 #pragma unroll
-        for (int j = 1; j < 16; ++j) mx = fmaxf(mx, d[j]);
-        const float tm = mx * c;
-        const float mn = fmaxf(mo, tm);
+        for (int jj = 1; jj < 16; ++jj) mx = fmaxf(mx, d[jj]);
+        const float mn = fmaxf(m_run[b], mx * c);
         if (mn != -INFINITY) {
-          const float keep = mo == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mo - mn);
+          const float keep = m_run[b] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[b] - mn);
           float z = z_run[b] * keep;
 #pragma unroll
-          for (int j = 0; j < 16; ++j) z += __builtin_amdgcn_exp2f(fmaf(d[j], c, -mn));
-          m_run[b] = mn;
+          for (int jj = 0; jj < 16; ++jj) z += __builtin_amdgcn_exp2f(fmaf(d[jj], c, -mn));
           z_run[b] = z;
-          e_run[b] = fmaxf(e_run[b] * keep, tm == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(tm - mn));
+          m_run[b] = mn;
         }
       }
-      __builtin_amdgcn_sched_barrier(0);
     }
-  };
-
-  auto step = [&](auto sc, int j) __attribute__((always_inline)) {
-    constexpr int S = decltype(sc)::value;
-    constexpr int SN = (S + kSlots - 1) % kSlots;
-    // tile j + kSlots - 1 into the slot tile j - 1 released (unconditional: a fixed number of
-    // loads per step keeps every wait on exactly the tile it needs)
-    load_tile<D>(slot[SN], kg, tile_key(j + kSlots - 1), k1, l32, half);
-    if (j < my_tiles) tile(slot[S], tile_key(j));
-  };
-  for (int j0 = 0; j0 < my_tiles; j0 += kSlots) {
-    step(std::integral_constant<int, 0>{}, j0);
-    step(std::integral_constant<int, 1>{}, j0 + 1);
-    step(std::integral_constant<int, 2>{}, j0 + 2);
-    if constexpr (kSlots > 3) step(std::integral_constant<int, 3 % kSlots>{}, j0 + 3);
   }
+  wait_vmem<0>();  // no load into the ring may outlive the workgroup
 
-  // (max, sum relative to it) of this lane's keys; lanes l and l ^ 32 hold the same rows
-  // (different keys); then the waves
+  // lanes l and l ^ 32 hold the same rows (different keys); then the waves
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    const bool any = e_run[b] > 0.f;
-    float m = any ? m_run[b] + __builtin_log2f(e_run[b]) : -INFINITY;
-    float z = any ? z_run[b] / e_run[b] : 0.f;
+    float m = m_run[b], z = z_run[b];
     merge_mz(m, z, swap_halves(m), swap_halves(z));
     if (half == 0) red[wave][b * 32 + l32] = make_float2(m, z);
   }
@@ -240,7 +277,7 @@ template <int D, int NB, bool ALL>
 __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs a) {
   using Gm = SGeo<D, NB>;
   constexpr int R = Gm::R, NS = Gm::NS;
-  __shared__ __align__(16) uint16_t qs[R * D];
+  __shared__ __align__(16) uint16_t ring[kWaves][2 * Gm::TE];
   __shared__ __align__(16) float bsh[R];
 
   const int seg = blockIdx.x, g = blockIdx.y, p = blockIdx.z;
@@ -254,7 +291,18 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
   const float c = a.c;
   const float inv_g = 1.f / (float)G;
 
-  stage_unit_queries<D, NB>(a.q_win + ((size_t)p * a.h_q + (size_t)g * G) * 32 * D, qs);
+  KeyStream<D, NB> ks{ring[wave], a.k + ((size_t)a.tok_off[p] * a.h_kv + (size_t)g * L) * D, k0, k1,
+                      wave, lane};
+  const int n_tiles = (k1 - k0 + kTileKeys - 1) / kTileKeys;
+  const int my_tiles = n_tiles > wave ? (n_tiles - wave + kWaves - 1) / kWaves : 0;
+  // the query loads go first: vector memory operations complete in issue order, so the waits on
+  // key tiles below also cover them
+  bf16x8_t q[NB][NS];
+  load_queries<D, NB>(q, a.q_win + ((size_t)p * a.h_q + (size_t)g * G) * 32 * D, l32, half);
+  if (my_tiles > 0) ks.issue(0);
+  if (my_tiles > 1) ks.issue(1);
+  hold_until_loaded<D, NB>(q);
+
   if (threadIdx.x < R) {
     const size_t ri = ((size_t)p * a.h_q + (size_t)g * G) * 32 + threadIdx.x;
     float bv;
@@ -262,7 +310,7 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
       const int n_seg = (L + a.seg_keys - 1) / a.seg_keys;
       const float2* src = a.part + ((size_t)p * a.h_kv + g) * a.max_segs * R + threadIdx.x;
       float M = -INFINITY, Z = 0.f;
-      for (int q = 0; q < n_seg; ++q) merge_mz(M, Z, src[(size_t)q * R].x, src[(size_t)q * R].y);
+      for (int qq = 0; qq < n_seg; ++qq) merge_mz(M, Z, src[(size_t)qq * R].x, src[(size_t)qq * R].y);
       bv = M + __builtin_log2f(Z);
       if (seg == 0) {
         a.row_max_out[ri] = M * kLn2;
@@ -273,75 +321,57 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
     }
     bsh[threadIdx.x] = bv;
   }
-  const uint16_t* kg = a.k + ((size_t)a.tok_off[p] * a.h_kv + (size_t)g * L) * D;
-  const size_t stat_base = (size_t)a.tok_off[p] * a.h_kv + (size_t)g * L;
-  const int n_tiles = (k1 - k0 + kTileKeys - 1) / kTileKeys;
-  const int my_tiles = n_tiles > wave ? (n_tiles - wave + kWaves - 1) / kWaves : 0;
-  auto tile_key = [&](int j) { return k0 + (j * kWaves + wave) * kTileKeys; };
-
-  bf16x8_t slot[kSlots][NS];
-#pragma unroll
-  for (int q = 0; q + 1 < kSlots; ++q) load_tile<D>(slot[q], kg, tile_key(q), k1, l32, half);
   __syncthreads();
+  const size_t stat_base = (size_t)a.tok_off[p] * a.h_kv + (size_t)g * L;
 
-  auto tile = [&](const bf16x8_t (&t)[NS], int t0) __attribute__((always_inline)) {
+  auto tile = [&](const bf16x8_t (&kt)[NS], int t0, auto masked) __attribute__((always_inline)) {
     const int key = t0 + l32;
     // window row r = 4 half + 8 (j / 4) + (j % 4) of every head sees the key iff key <= L - 32 + r
-    const bool edge = t0 + 31 > L - 32;
     const int thr = key - (L - 32) - 4 * half;
     float ab[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) ab[j] = 0.f;
     float h_mean = 0.f, h_m2 = 0.f;  // ALL: running mean and squared deviations of the heads so far
-    auto accumulate = [&](auto masked) __attribute__((always_inline)) {
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        float eb[16];
-        bf16x8_t qf[NS];
-        read_qfrags<D, NB>(qf, qs, b, l32, half);
-        f32x16_t d = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int b = 0; b < NB; ++b) {
+      float eb[16];
+      const f32x16_t d = chain<NS>(q[b], kt);
 #pragma unroll
-        for (int s = 0; s < NS; ++s) d = mfma_step(qf[s], t[s], d);
+      for (int qq = 0; qq < 4; ++qq) {
+        // window rows 8 qq + 4 half + 0..3 of query head b
+        const float4 bv = *reinterpret_cast<const float4*>(bsh + b * 32 + 8 * qq + 4 * half);
+        const float bb[4] = {bv.x, bv.y, bv.z, bv.w};
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          // window rows 8 q + 4 half + 0..3 of query head b
-          const float4 bv = *reinterpret_cast<const float4*>(bsh + b * 32 + 8 * q + 4 * half);
-          const float bb[4] = {bv.x, bv.y, bv.z, bv.w};
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int j = 4 * q + u;
-            float e = __builtin_amdgcn_exp2f(fmaf(d[j], c, -bb[u]));
-            if (decltype(masked)::value && 8 * q + u < thr) e = 0.f;
-            ab[j] += e;
-            eb[j] = e;
-          }
+        for (int u = 0; u < 4; ++u) {
+          const int j = 4 * qq + u;
+          float e = __builtin_amdgcn_exp2f(fmaf(d[j], c, -bb[u]));
+          if (decltype(masked)::value && 8 * qq + u < thr) e = 0.f;
+          ab[j] += e;
+          eb[j] = e;
         }
-        if constexpr (ALL) {
-          float hs[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int j = 0; j < 16; ++j) hs[j & 3] += eb[j];
-          const float mb = sum_halves((hs[0] + hs[1]) + (hs[2] + hs[3])) * (1.f / 32.f);
-          float hv[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const float dl = eb[j] - mb;
-            hv[j & 3] = fmaf(dl, dl, hv[j & 3]);
-          }
-          const float m2b = sum_halves((hv[0] + hv[1]) + (hv[2] + hv[3]));
-          if (b == 0) {
-            h_mean = mb;
-            h_m2 = m2b;
-          } else {  // b heads of 32 rows merged with one more
-            const float dl = mb - h_mean;
-            h_mean = fmaf(dl, 1.f / (float)(b + 1), h_mean);
-            h_m2 += fmaf(dl * dl, 32.f * (float)b / (float)(b + 1), m2b);
-          }
-        }
-        __builtin_amdgcn_sched_barrier(0);  // one head at a time, as in pass 1
       }
-    };
-    if (edge) accumulate(std::true_type{});
-    else accumulate(std::false_type{});
+      if constexpr (ALL) {
+        float hs[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < 16; ++j) hs[j & 3] += eb[j];
+        const float mb = sum_halves((hs[0] + hs[1]) + (hs[2] + hs[3])) * (1.f / 32.f);
+        float hv[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const float dl = eb[j] - mb;
+          hv[j & 3] = fmaf(dl, dl, hv[j & 3]);
+        }
+        const float m2b = sum_halves((hv[0] + hv[1]) + (hv[2] + hv[3]));
+        if (b == 0) {
+          h_mean = mb;
+          h_m2 = m2b;
+        } else {  // b heads of 32 rows merged with one more
+          const float dl = mb - h_mean;
+          h_mean = fmaf(dl, 1.f / (float)(b + 1), h_mean);
+          h_m2 += fmaf(dl * dl, 32.f * (float)b / (float)(b + 1), m2b);
+        }
+      }
+    }
     // ab[j] = G a[r][key] for the window rows r = acc_row(j, lane); the other 16 are in lane ^ 32
     float sp[4];
 #pragma unroll
@@ -362,18 +392,14 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
     if (key < k1) (half == 0 ? a.mu : a.sigma)[stat_base + key] = half == 0 ? mean : __builtin_amdgcn_sqrtf(var);
   };
 
-  auto step = [&](auto sc, int j) __attribute__((always_inline)) {
-    constexpr int S = decltype(sc)::value;
-    constexpr int SN = (S + kSlots - 1) % kSlots;
-    load_tile<D>(slot[SN], kg, tile_key(j + kSlots - 1), k1, l32, half);
-    if (j < my_tiles) tile(slot[S], tile_key(j));
-  };
-  for (int j0 = 0; j0 < my_tiles; j0 += kSlots) {
-    step(std::integral_constant<int, 0>{}, j0);
-    step(std::integral_constant<int, 1>{}, j0 + 1);
-    step(std::integral_constant<int, 2>{}, j0 + 2);
-    if constexpr (kSlots > 3) step(std::integral_constant<int, 3 % kSlots>{}, j0 + 3);
+  for (int j = 0; j < my_tiles; ++j) {
+    bf16x8_t kt[NS];
+    ks.template next<1>(kt, j, my_tiles, l32, half);  // one mu / sigma store per tile
+    const int t0 = ks.tile_key(j);
+    if (t0 + 31 > L - 32) tile(kt, t0, std::true_type{});
+    else tile(kt, t0, std::false_type{});
   }
+  wait_vmem<0>();  // no load into the ring may outlive the workgroup
 }
 
 template <int D, int NB>
