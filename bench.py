@@ -145,6 +145,8 @@ def main() -> None:
     ap.add_argument("--workload", default=WORKLOADS[0], choices=WORKLOADS)
     ap.add_argument("--cpu-layers", type=int, default=3,
                     help="layers of the oracle sample for the CPU baseline (0: skip)")
+    ap.add_argument("--flush", choices=("read", "write"), default="read",
+                    help="how the last-level cache is emptied before each timed step")
     ap.add_argument("--unfused", action="store_true",
                     help="time kv_window_scores + kv_mu_sigma instead of kv_window_mu_sigma")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -174,7 +176,15 @@ def main() -> None:
                      packed.lens, packed.tok_off, lam1, lam2)
     out = api.allocate(inp, wl.budget)
     gen_s = time.perf_counter() - t_gen
-    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    # evicts the key cache from the 256 MB last-level cache before every timed step: a read of
+    # 512 MiB (a write would leave dirty lines whose write-back lands in the timed region)
+    flush_buf = torch.ones(128 << 20, dtype=torch.float32, device="cuda")
+
+    def flush():
+        if args.flush == "write":
+            flush_buf.fill_(1.0)
+        else:
+            flush_buf.amax()
     stream = torch.cuda.current_stream()
     b = inp.batch
 
@@ -200,7 +210,7 @@ def main() -> None:
         return [torch.cuda.Event(enable_timing=True) for _ in range(4)]
 
     for _ in range(args.warmup):
-        flush.zero_()
+        flush()
         step(new_events())
     torch.cuda.synchronize()
     print(f"# inputs drawn and uploaded in {gen_s:.1f} s; warmup done", file=sys.stderr,
@@ -210,7 +220,7 @@ def main() -> None:
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     for _ in range(args.steps):
-        flush.zero_()  # outside the events: evicts the key cache from the last-level cache
+        flush()  # outside the events
         evs = new_events()
         step(evs)
         all_events.append(evs)
@@ -222,7 +232,7 @@ def main() -> None:
         every iteration, HIP events between the calls on the launch stream."""
         rows_ = []
         for it in range(args.warmup + args.steps):
-            flush.zero_()
+            flush()
             evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
             evs[0].record(stream)
             for c, fn in enumerate(calls):
@@ -286,7 +296,7 @@ def main() -> None:
 
     layer_events = []
     for it in range(args.warmup + args.steps):
-        flush.zero_()
+        flush()
         evs = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
         layered_step(evs)
         if it >= args.warmup:
@@ -327,6 +337,7 @@ def main() -> None:
         "breakdown_ms": {n: round(float(v), 4) for n, v in zip(names, mean_part)},
         "step_ms_min_max": [round(float(step_ms.min()), 4), round(float(step_ms.max()), 4)],
         "wall_s_timed_loop": round(wall, 3),
+        "cache_flush": f"{args.flush} of 512 MiB before every timed step",
         "per_layer_schedule_ms": {"total": round(lay_score + lay_rest, 4),
                                   "scoring (32 launches of kv_window_mu_sigma)": round(lay_score, 4),
                                   "select+compact (batched)": round(lay_rest, 4)},
