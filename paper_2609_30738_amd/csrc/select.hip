@@ -336,24 +336,27 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
       }
     }
     __syncthreads();
-    // suffix sums over bins (bin 255 = largest digit); thread tid < 256 holds bin tid
+    // suffix sums over bins (bin 255 = largest digit); thread tid < 256 (waves 0..3) holds bin
+    // tid: a suffix scan inside each wave, then the totals of the waves above it
     const bool bin = tid < 256;
+    uint32_t cnt = 0, suf = 0;
     if (bin) {
-      uint32_t cnt = 0;
 #pragma unroll
       for (int v = 0; v < kWaves; ++v) cnt += sh.hist[v][tid];
-      sh.scan[tid] = cnt;
+      suf = cnt;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t o = __shfl_down(suf, off, 64);
+        if (lane + off < 64) suf += o;
+      }
+      if (lane == 0) sh.scan[wave] = suf;
     }
     __syncthreads();
-    for (int off = 1; off < 256; off <<= 1) {
-      const uint32_t add = (bin && tid + off < 256) ? sh.scan[tid + off] : 0u;
-      __syncthreads();
-      if (bin) sh.scan[tid] += add;
-      __syncthreads();
-    }
     if (bin) {
-      const uint32_t ge = sh.scan[tid];                             // count with digit >= tid
-      const uint32_t gt = (tid + 1 < 256) ? sh.scan[tid + 1] : 0u;  // count with digit > tid
+      uint32_t above = 0;
+      for (int v = wave + 1; v < 4; ++v) above += sh.scan[v];
+      const uint32_t ge = suf + above;  // count with digit >= tid
+      const uint32_t gt = ge - cnt;     // count with digit > tid
       if (ge >= (uint32_t)need && gt < (uint32_t)need) {
         sh.sel_threshold = prefix | ((uint32_t)tid << shift);
         sh.sel_need = need - (int)gt;

@@ -329,8 +329,6 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
     // window row r = 4 half + 8 (j / 4) + (j % 4) of every head sees the key iff key <= L - 32 + r
     const int thr = key - (L - 32) - 4 * half;
     float ab[16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j) ab[j] = 0.f;
     float h_mean = 0.f, h_m2 = 0.f;  // ALL: running mean and squared deviations of the heads so far
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
@@ -346,7 +344,7 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
           const int j = 4 * qq + u;
           float e = __builtin_amdgcn_exp2f(fmaf(d[j], c, -bb[u]));
           if (decltype(masked)::value && 8 * qq + u < thr) e = 0.f;
-          ab[j] += e;
+          ab[j] = b == 0 ? e : ab[j] + e;
           eb[j] = e;
         }
       }
