@@ -279,6 +279,7 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
   constexpr int R = Gm::R, NS = Gm::NS;
   __shared__ __align__(16) uint16_t ring[kWaves][2 * Gm::TE];
   __shared__ __align__(16) float bsh[R];
+  __shared__ float2 mz_part[kThreads / R][R];
 
   const int seg = blockIdx.x, g = blockIdx.y, p = blockIdx.z;
   const int L = a.lens[p];
@@ -303,14 +304,36 @@ __global__ __launch_bounds__(kThreads, 1) void mu_sigma_stream_kernel(StreamArgs
   if (my_tiles > 1) ks.issue(1);
   hold_until_loaded<D, NB>(q);
 
+  // Normalisers of the unit's rows.  From segment partials: thread (row, part) merges segments
+  // part, part + P, ... of its row (four loads in flight), then one thread per row merges the P
+  // results in a fixed order.
+  constexpr int P = kThreads / R;
+  const size_t ri0 = ((size_t)p * a.h_q + (size_t)g * G) * 32;
+  if (a.part) {
+    const int n_seg = (L + a.seg_keys - 1) / a.seg_keys;
+    const int row = threadIdx.x % R, pt = threadIdx.x / R;
+    const float2* src = a.part + ((size_t)p * a.h_kv + g) * a.max_segs * R + row;
+    float M = -INFINITY, Z = 0.f;
+    for (int q0 = pt; q0 < n_seg; q0 += 4 * P) {
+      float2 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int qq = q0 + u * P;
+        v[u] = qq < n_seg ? src[(size_t)qq * R] : make_float2(-INFINITY, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) merge_mz(M, Z, v[u].x, v[u].y);
+    }
+    mz_part[pt][row] = make_float2(M, Z);
+  }
+  __syncthreads();
   if (threadIdx.x < R) {
-    const size_t ri = ((size_t)p * a.h_q + (size_t)g * G) * 32 + threadIdx.x;
+    const size_t ri = ri0 + threadIdx.x;
     float bv;
     if (a.part) {
-      const int n_seg = (L + a.seg_keys - 1) / a.seg_keys;
-      const float2* src = a.part + ((size_t)p * a.h_kv + g) * a.max_segs * R + threadIdx.x;
-      float M = -INFINITY, Z = 0.f;
-      for (int qq = 0; qq < n_seg; ++qq) merge_mz(M, Z, src[(size_t)qq * R].x, src[(size_t)qq * R].y);
+      float M = mz_part[0][threadIdx.x].x, Z = mz_part[0][threadIdx.x].y;
+#pragma unroll
+      for (int pt = 1; pt < P; ++pt) merge_mz(M, Z, mz_part[pt][threadIdx.x].x, mz_part[pt][threadIdx.x].y);
       bv = M + __builtin_log2f(Z);
       if (seg == 0) {
         a.row_max_out[ri] = M * kLn2;

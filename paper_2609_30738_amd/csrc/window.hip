@@ -159,9 +159,13 @@ __global__ __launch_bounds__(kThreads) void combine_stats_kernel(
   const int n_chunks = (lens[p] + chunk_keys - 1) / chunk_keys;
   float M = -INFINITY, Z = 0.f;
   const float2* src = partial + ((size_t)p * h_kv + g) * max_chunks * rows_pad + m;
-  for (int ch = 0; ch < n_chunks; ++ch) {
-    const float2 o = src[(size_t)ch * rows_pad];
-    merge_mz(M, Z, o.x, o.y);
+  for (int ch0 = 0; ch0 < n_chunks; ch0 += 4) {  // four loads in flight
+    float2 o[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      o[u] = ch0 + u < n_chunks ? src[(size_t)(ch0 + u) * rows_pad] : make_float2(-INFINITY, 0.f);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) merge_mz(M, Z, o[u].x, o[u].y);
   }
   row_max[idx] = M * kLn2;
   row_sum[idx] = Z;
