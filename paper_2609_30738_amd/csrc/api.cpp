@@ -166,7 +166,10 @@ int kv_window_scores(const kv_problem* pr, const void* q_win, const void* k, flo
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (kv::stream_shape_ok(s, scale)) {
     const kv::StreamPlan plan = stream_plan_of(pr, s);
-    st = launch_status(kv::launch_stream_stats(s, plan, q_win, k, scale, ws, hs));
+    if (plan.max_segs == 1)  // one segment per unit: pass 1 writes the row statistics itself
+      return launch_status(kv::launch_stream_stats(s, plan, q_win, k, scale, nullptr, row_max,
+                                                   row_sum, hs));
+    st = launch_status(kv::launch_stream_stats(s, plan, q_win, k, scale, ws, nullptr, nullptr, hs));
     if (st != KV_OK) return st;
     return launch_status(kv::launch_combine_partials(s, ws, plan.seg_keys, plan.max_segs,
                                                      s.group() * 32, row_max, row_sum, hs));
@@ -226,7 +229,7 @@ int kv_window_mu_sigma_ex(const kv_problem* pr, const void* q_win, const void* k
   if (kv::stream_shape_ok(s, scale)) {
     // segment partials, then normalisers, row statistics and mu / sigma in one more pass
     const kv::StreamPlan plan = stream_plan_of(pr, s);
-    st = launch_status(kv::launch_stream_stats(s, plan, q_win, k, scale, ws, hs));
+    st = launch_status(kv::launch_stream_stats(s, plan, q_win, k, scale, ws, nullptr, nullptr, hs));
     if (st != KV_OK) return st;
     return launch_status(kv::launch_stream_mu_sigma(s, plan, q_win, k, scale, ws, nullptr,
                                                     nullptr, row_max, row_sum, mu, sigma, all, hs));

@@ -48,9 +48,11 @@ struct StreamPlan {
 bool stream_shape_ok(const Shape& s, float scale);
 StreamPlan stream_plan(const Shape& s, int64_t total_keys);  // total_keys = sum_p h_kv L_p
 size_t stream_ws_bytes(const Shape& s, const StreamPlan& plan);
-// Pass 1: segment partials into ws.
+// Pass 1: segment partials into ws or, with ws == nullptr (only when plan.max_segs == 1), the
+// row statistics into row_max / row_sum.
 hipError_t launch_stream_stats(const Shape& s, const StreamPlan& plan, const void* q_win,
-                               const void* k, float scale, void* ws, hipStream_t stream);
+                               const void* k, float scale, void* ws, float* row_max,
+                               float* row_sum, hipStream_t stream);
 // Pass 2: normalisers from the partials in ws (then also row_max_out / row_sum_out), or, with
 // ws == nullptr, from row_max_in / row_sum_in; mu / sigma out.
 hipError_t launch_stream_mu_sigma(const Shape& s, const StreamPlan& plan, const void* q_win,

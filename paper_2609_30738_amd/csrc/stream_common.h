@@ -1,0 +1,233 @@
+// Building blocks of the streaming window kernels (pass 1 in stream_stats.hip, pass 2 in
+// stream_mu_sigma.hip): the argument block, the tile geometry, the per-wave key stream into LDS
+// and small wave-level helpers.
+//
+// Streaming window statistics for bf16 caches with w = 32 (section 3.1, Eq. (1), Eq. (3)): two
+// passes over the keys, each a plain stream from HBM with no communication between workgroups.
+//
+//   Work item: one segment of `seg_keys` consecutive keys of one (problem, kv head) unit, 512
+//   threads = 8 waves.  Every lane holds the MFMA fragments of its window rows of all G heads of
+//   the unit in registers for the whole segment.  Each wave streams 32-key tiles (tile j of the
+//   segment goes to wave j % 8) from HBM into a private two-tile ring in LDS with direct-to-LDS,
+//   non-temporal loads: every load instruction covers 1 KiB of consecutive key bytes (four 256-byte
+//   rows at d = 128), and each lane picks the 16-byte chunk that lands at its LDS position, so the
+//   tile is stored with its chunks XOR-swizzled by row (chunk c of row r at slot c ^ (r mod CH)).
+//   The MFMA operand reads of 16 consecutive rows then touch 16 different chunk slots (all banks).
+//   While a tile is computed, the next two are in flight.
+//
+//   stats_stream_kernel (pass 1): logits D[key][row] = K Q^T with keys as the MFMA M dimension, so
+//     a lane holds one window row and 16 keys of each tile.  Every lane keeps, per head, the exact
+//     running maximum m of t = logit * scale * log2 e and the sum z of 2^(t - m), rescaled when m
+//     grows (online softmax).  At the end the lanes, then the waves, are merged and the segment's
+//     (max, sum) per row goes to the workspace.
+//   mu_sigma_stream_kernel (pass 2): merges the segment partials of its unit into the normalisers
+//     b = M + log2 Z (segment 0 also writes row_max / row_sum), or takes them from given
+//     row_max / row_sum; then logits again with keys as N (a lane holds one key),
+//     a = 2^(t - b) summed over the group's heads, the mean and the two-pass sample variance over
+//     the 32 window rows, stored as mu / sigma.  With `sigma_all` the variance runs over all G x 32
+//     (head, row) values instead: every head's mean and squared deviations over its 32 rows, merged
+//     across heads with the pairwise update of Chan, Golub and LeVeque.
+//
+//   Tiles with a masked key (the causal triangle of the window, keys past the segment end) take a
+//   separate, guarded path; every other tile runs without masks or branches.
+#pragma once
+
+#include <algorithm>
+#include <type_traits>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace kv {
+namespace stream {
+
+constexpr int kWaves = 8;
+constexpr int kThreads = kWaves * 64;
+constexpr int kTileKeys = 32;
+
+struct StreamArgs {
+  const uint16_t* q_win;
+  const uint16_t* k;
+  const int32_t* lens;
+  const int64_t* tok_off;
+  int h_q, h_kv;
+  float c;  // softmax scale * log2(e)
+  int seg_keys, max_segs;
+  float2* part;           // [n_units][max_segs][R] segment partials (m, z), base 2; pass 1 with
+                          // part == nullptr (one segment per unit) writes row_max_out / row_sum_out
+  const float* row_max;   // pass 2 from given statistics (part == nullptr)
+  const float* row_sum;
+  float* row_max_out;     // pass 2 from partials: written by segment 0
+  float* row_sum_out;
+  float* mu;
+  float* sigma;
+  int sigma_all;          // pass 2: dispersion over all G x 32 (head, row) values
+};
+
+template <int D, int NB> struct SGeo {
+  static constexpr int R = NB * 32;          // window rows of a unit (G heads x 32)
+  static constexpr int NS = D / 16;          // MFMA K steps
+  static constexpr int CH = D * 2 / 16;      // 16-byte chunks of a key row
+  static constexpr int TE = kTileKeys * D;   // elements of a tile
+  static constexpr int NDMA = TE * 2 / 1024; // 1 KiB load instructions per tile
+  // LDS slot (in 16-byte chunks) of chunk `ch` of tile row `row`
+  __device__ static int slot_of(int row, int ch) { return row * CH + (ch ^ (row % CH)); }
+};
+
+typedef const __attribute__((address_space(1))) void* gptr_t;
+typedef __attribute__((address_space(3))) void* lptr_t;
+
+// s_waitcnt vmcnt(N): at most N vector memory operations of this wave still outstanding.  Vector
+// memory operations complete in issue order, so this waits for everything issued before the last N.
+template <int N> __device__ __forceinline__ void wait_vmem() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ void wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// maximum of three values (NaN-propagating, no canonicalisation of the operands)
+__device__ __forceinline__ float fmax3(float a, float b, float c) {
+  return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+}
+
+__device__ __forceinline__ float sum_halves(float x) {  // x + x of lane ^ 32
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// s_waitcnt vmcnt(later NDMA + (stores ? TS : 0)) for a run-time later in [0, 3]
+template <int NDMA, int TS>
+__device__ __forceinline__ void wait_vmem_tiles(int later, bool stores) {
+  if (stores) {
+    switch (later) {
+      case 0: wait_vmem<TS>(); break;
+      case 1: wait_vmem<NDMA + TS>(); break;
+      case 2: wait_vmem<2 * NDMA + TS>(); break;
+      default: wait_vmem<3 * NDMA + TS>(); break;
+    }
+  } else {
+    switch (later) {
+      case 0: wait_vmem<0>(); break;
+      case 1: wait_vmem<NDMA>(); break;
+      case 2: wait_vmem<2 * NDMA>(); break;
+      default: wait_vmem<3 * NDMA>(); break;
+    }
+  }
+}
+
+// Per-wave key stream of one segment: a ring of S tiles in LDS filled by direct-to-LDS loads.
+// Tile j of the wave (keys k0 + (j NW + wave) 32 ..) goes to slot j mod S.
+template <int D, int NB, int NW, int S> struct KeyStream {
+  using Gm = SGeo<D, NB>;
+  static_assert(S == 2 || S == 4, "ring of 2 or 4 tiles");
+  uint16_t* ring;       // this wave's S tiles
+  const uint16_t* kg;   // keys of the unit
+  int k0, k1, wave, lane;
+
+  __device__ int tile_key(int j) const { return k0 + (j * NW + wave) * kTileKeys; }
+
+  // tile j into its slot; rows past the segment end re-read its last key
+  __device__ __forceinline__ void issue(int j) const {
+    const int t0 = tile_key(j);
+    uint16_t* dst = ring + (j & (S - 1)) * Gm::TE;
+#pragma unroll
+    for (int i = 0; i < Gm::NDMA; ++i) {
+      const int pos = 64 * i + lane;  // LDS chunk slot written by this lane
+      const int row = pos / Gm::CH;
+      const int ch = (pos % Gm::CH) ^ (row % Gm::CH);
+      const uint16_t* src = kg + (size_t)min(t0 + row, k1 - 1) * D + ch * 8;
+      // aux 2: non-temporal (the keys are read once per pass)
+      __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)(dst + i * 512), 16, 0, 2);
+    }
+  }
+
+  // the first min(S, my_tiles) tiles
+  __device__ __forceinline__ void prologue(int my_tiles) const {
+#pragma unroll
+    for (int j = 0; j < S; ++j)
+      if (j < my_tiles) issue(j);
+  }
+
+  // MFMA operand fragments of tile j (lane: row l32, K half `half`), once its loads have landed
+  __device__ __forceinline__ void read(bf16x8_t (&a)[Gm::NS], int j, int l32, int half) const {
+    const uint16_t* src = ring + (j & (S - 1)) * Gm::TE;
+#pragma unroll
+    for (int s = 0; s < Gm::NS; ++s)
+      a[s] = *reinterpret_cast<const bf16x8_t*>(src + Gm::slot_of(l32, 2 * s + half) * 8);
+  }
+
+  // Wait for tile j, copy it into registers and hand its slot to tile j + S.  After tile j's loads
+  // the wave has issued the loads of the (up to S - 1) tiles after it and, from tile S on, the
+  // STORES vector memory stores per tile of the S tiles before it (the caller's, issued after each
+  // tile's computation); those may stay in flight.
+  template <int STORES>
+  __device__ __forceinline__ void next(bf16x8_t (&a)[Gm::NS], int j, int my_tiles, int l32,
+                                       int half) const {
+    wait_vmem_tiles<Gm::NDMA, STORES * S>(min(S - 1, my_tiles - 1 - j), STORES > 0 && j >= S);
+    read(a, j, l32, half);
+    wait_lds();
+    if (j + S < my_tiles) issue(j + S);
+  }
+};
+
+// the unit's window-row fragments of every head (head b, rows b * 32 + l32), all K steps
+template <int D, int NB>
+__device__ __forceinline__ void load_queries(bf16x8_t (&q)[NB][D / 16], const uint16_t* qg, int l32,
+                                             int half) {
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s)
+      q[b][s] = *reinterpret_cast<const bf16x8_t*>(qg + (size_t)(b * 32 + l32) * D + 16 * s + 8 * half);
+}
+
+// An empty use of every query register: the compiler waits for the query loads here, once,
+// instead of at the first MFMA of the tile loop, where its wait would also cover the key tiles in
+// flight.
+template <int D, int NB>
+__device__ __forceinline__ void hold_until_loaded(bf16x8_t (&q)[NB][D / 16]) {
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) asm volatile("" ::"v"(q[b][s]));
+}
+
+template <int NS>
+__device__ __forceinline__ f32x16_t chain(const bf16x8_t (&x)[NS], const bf16x8_t (&y)[NS]) {
+  f32x16_t d = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < NS; ++s) d = mfma_step(x[s], y[s], d);
+  return d;
+}
+
+
+inline StreamArgs base_args(const Shape& s, const StreamPlan& plan, const void* q_win, const void* k,
+                     float scale) {
+  StreamArgs a{};
+  a.q_win = static_cast<const uint16_t*>(q_win);
+  a.k = static_cast<const uint16_t*>(k);
+  a.lens = s.lens;
+  a.tok_off = s.tok_off;
+  a.h_q = s.h_q;
+  a.h_kv = s.h_kv;
+  a.c = scale * kLog2e;
+  a.seg_keys = plan.seg_keys;
+  a.max_segs = plan.max_segs;
+  return a;
+}
+
+// Launch of either pass for the unit shape of `s` (d in {64, 128}, G in {1, 2, 4}).
+template <template <int, int> class Launch>
+hipError_t launch_for_shape(const Shape& s, const StreamArgs& args, hipStream_t st) {
+  const int G = s.group();
+  if (s.d == 128) {
+    if (G == 4) return Launch<128, 4>::run(s, args, st);
+    if (G == 2) return Launch<128, 2>::run(s, args, st);
+    return Launch<128, 1>::run(s, args, st);
+  }
+  if (G == 4) return Launch<64, 4>::run(s, args, st);
+  if (G == 2) return Launch<64, 2>::run(s, args, st);
+  return Launch<64, 1>::run(s, args, st);
+}
+
+}  // namespace stream
+}  // namespace kv

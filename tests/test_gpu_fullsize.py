@@ -82,3 +82,20 @@ def test_long_context_select_from_global_scores(pool):
     run = gpu_cases.run_gpu(wl, fused=True, pool=pool)
     _properties(run)
     _sampled(run, [0, 1], [1, 6])
+
+
+def test_32_layers_L8192_unfused_one_segment_per_unit():
+    """kv_window_scores, then kv_mu_sigma from its row statistics, on the whole 32-layer batch:
+    every unit is one segment, so the first pass writes the row statistics itself."""
+    run = gpu_cases.run_gpu(workloads.mistral_pass_8k(64), fused=False)
+    _properties(run)
+    _sampled(run, [0, 15, 31], [1, 6])
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_one_layer_of_the_32k_pass_alone(fused):
+    """One layer of the L=32768 workload launched by itself, as in the per-layer schedule: 32
+    segments of 1024 keys per unit, whose partials the second pass (or the combine) merges."""
+    run = gpu_cases.run_gpu(workloads.mistral_pass_32k(), problems=[16], fused=fused)
+    _properties(run)
+    _sampled(run, [0], [0, 3, 7])
