@@ -269,6 +269,29 @@ def main() -> None:
                                    wl.w, sel_pyr, ws=out.ws, budgets=pyr),
         lambda: _lib.compact_cache_ex(b, inp.k, inp.v, sel_pyr, b_max, wl.w, pyr, k_pyr, v_pyr))
 
+    # generation after eviction: one decode step (one token per layer, every query head) over the
+    # compacted B + W rows, and for contrast over the uncompacted L rows of the same layers
+    # (the attention the eviction saves on every generated token)
+    q_dec = torch.randn(wl.n_prob * wl.h_q * wl.d, device="cuda").to(inp.k.dtype)
+    o_dec = torch.empty(wl.n_prob * wl.h_q * wl.d, dtype=torch.float32, device="cuda")
+    cb_kept = _lib.CacheBatch(wl.dtype, wl.h_q, wl.h_kv, wl.d, wl.budget + wl.w,
+                              [wl.budget + wl.w] * wl.n_prob)
+    uniform = bool(np.all(packed.lens == packed.lens[0]))
+    cb_full = _lib.CacheBatch(wl.dtype, wl.h_q, wl.h_kv, wl.d, int(packed.lens[0]),
+                              [int(packed.lens[0])] * wl.n_prob) if uniform else None
+
+    def dec_ws(cb):
+        nb = _lib.decode_workspace_bytes(cb)
+        return torch.empty(max(nb, 256), dtype=torch.uint8, device="cuda") if nb else None
+    ws_kept = dec_ws(cb_kept)
+    ws_full = dec_ws(cb_full) if uniform else None
+    dec_calls = [lambda: _lib.decode_attention(cb_kept, q_dec, out.k_out, out.v_out, None, None,
+                                               inp.scale, o_dec, ws_kept)]
+    if uniform:
+        dec_calls.append(lambda: _lib.decode_attention(cb_full, q_dec, inp.k, inp.v, None, None,
+                                                       inp.scale, o_dec, ws_full))
+    v_dec = timed(*dec_calls)
+
     v_all, v_pool, v_free = timed(
         lambda: _lib.window_mu_sigma_ex(b, inp.q_win, inp.k, inp.scale, "all_rows", out.row_max,
                                         out.row_sum, out.mu, out.sigma, out.ws),
@@ -352,6 +375,10 @@ def main() -> None:
                        "kv_mmr_select_ex (depth-decreasing budgets, beta 20, "
                        f"{int(sched[0])}..{int(sched[-1])})": round(v_pyr_sel, 4),
                        "kv_compact_cache_ex (same budgets)": round(v_pyr_cmp, 4)},
+        "decode_step_ms": {f"over the compacted cache ({wl.budget + wl.w} rows per kv head)":
+                           round(v_dec[0], 4),
+                           f"over the full cache ({int(packed.lens[0])} rows per kv head)":
+                           round(v_dec[1], 4) if uniform else None},
         "mfma_tflops": {"stats_stream": round(flops / (k_stats * 1e-3) / 1e12, 1),
                         "mu_sigma_stream": round(flops / (k_mu * 1e-3) / 1e12, 1),
                         "peak_bf16_dense": MFMA_PEAK_TFLOPS},
