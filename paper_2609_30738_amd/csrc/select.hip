@@ -184,7 +184,7 @@ template <int NW> struct SelectShared {
   uint32_t scan[256];
   uint32_t wave_cnt[2][NW];
   float wave_max[NW];
-  uint64_t best[2][NW];
+  uint4 best[2][NW];  // per wave and step parity: the packed (score, slot) pair, 1 / |k|
   uint32_t halo[2][32];  // raw keys left of a pooling chunk (pool_h <= 31)
   uint32_t sel_threshold;
   int sel_need;
@@ -462,6 +462,10 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
 
   int last = -1;
   float last_inv = 0.f;
+  // the greedy trace (admitted slot and score key per step) reuses the radix histograms: at most
+  // C <= 2 NT steps (2 NT = 128 NW words each)
+  uint32_t* trace_slot = &sh.hist[0][0];
+  uint32_t* trace_key = &sh.hist[0][0] + kWaves * 128;
   // only the waves that own candidate slots take part; the others just keep step with the
   // barrier (sleeping there instead of taking issue slots from the live waves)
   const int live_waves = min(kWaves, (C + 63) / 64);
@@ -486,29 +490,56 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
         }
       }
       const uint64_t wbest = wave_best(my_score, my_slot);
-      if (lane == 0) sh.best[t & 1][wave] = wbest;
+      // the wave's best slot is owned by one of its lanes (slot = tid + q NT): its 1 / |k| rides
+      // along, so that no lookup follows the barrier
+      const int bslot = unpack_slot(wbest);
+      float binv = 0.f;
+#pragma unroll
+      for (int q = 0; q < CPT; ++q) {
+        const uint32_t v = __builtin_amdgcn_readlane(__float_as_uint(inv[q]), bslot & 63);
+        if ((bslot - q * kThreads) >> 6 == wave) binv = __uint_as_float(v);
+      }
+      if (lane == 0)
+        sh.best[t & 1][wave] = make_uint4((uint32_t)wbest, (uint32_t)(wbest >> 32), __float_as_uint(binv), 0u);
     }
     __syncthreads();
     if (live) {
-      uint64_t b = sh.best[t & 1][0];
-      for (int v = 1; v < live_waves; ++v) {
-        const uint64_t o = sh.best[t & 1][v];
-        b = o > b ? o : b;
+      // the live waves' records (score key, slot, 1 / |k|), four reads in flight at a time
+      uint64_t b = 0;
+      float bi = 0.f;
+      for (int v0 = 0; v0 < live_waves; v0 += 4) {
+        uint4 r[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          r[u] = v0 + u < live_waves ? sh.best[t & 1][v0 + u] : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const uint64_t o = ((uint64_t)r[u].y << 32) | r[u].x;
+          if (o > b) {
+            b = o;
+            bi = __uint_as_float(r[u].z);
+          }
+        }
       }
       last = min(max(unpack_slot(b), 0), C - 1);  // always a live slot: bp <= C
 #pragma unroll
       for (int q = 0; q < CPT; ++q)
         if (tid + q * kThreads == last) admitted[q] = true;
-      last_inv = cinv[last];
-      if (tid == 0) {
-        const size_t o = ((size_t)p * h_kv + g) * budget + t;
-        sel_idx[o] = cpos[last];
-        if (sel_score) {
-          const uint32_t kk = (uint32_t)(b >> 32);
-          const uint32_t u = (kk & 0x80000000u) ? (kk & 0x7FFFFFFFu) : ~kk;
-          sel_score[o] = __uint_as_float(u);
-        }
+      last_inv = bi;
+      if (tid == 0) {  // the step's record; written out after the last step
+        trace_slot[t] = (uint32_t)last;
+        trace_key[t] = (uint32_t)(b >> 32);
       }
+    }
+  }
+  __syncthreads();
+  for (int t = tid; t < bp; t += kThreads) {
+    const size_t o = ((size_t)p * h_kv + g) * budget + t;
+    sel_idx[o] = cpos[trace_slot[t]];
+    if (sel_score) {
+      const uint32_t kk = trace_key[t];
+      const uint32_t u = (kk & 0x80000000u) ? (kk & 0x7FFFFFFFu) : ~kk;
+      sel_score[o] = __uint_as_float(u);
     }
   }
 
