@@ -67,15 +67,17 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
 // between rows and between the wave's halves.
 __device__ __forceinline__ float wave_max_f(float v) {
 #define KV_DPPF(x, CTRL) __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), CTRL, 0xF, 0xF, false))
-  v = fmaxf(v, KV_DPPF(v, 0xB1));   // quad_perm [1,0,3,2]
-  v = fmaxf(v, KV_DPPF(v, 0x4E));   // quad_perm [2,3,0,1]
-  v = fmaxf(v, KV_DPPF(v, 0x124));  // row_ror:4
-  v = fmaxf(v, KV_DPPF(v, 0x128));  // row_ror:8
-#undef KV_DPPF
+#define KV_MAX(a, b) __builtin_elementwise_maximum(a, b)  // no operand canonicalisation
+  v = KV_MAX(v, KV_DPPF(v, 0xB1));   // quad_perm [1,0,3,2]
+  v = KV_MAX(v, KV_DPPF(v, 0x4E));   // quad_perm [2,3,0,1]
+  v = KV_MAX(v, KV_DPPF(v, 0x124));  // row_ror:4
+  v = KV_MAX(v, KV_DPPF(v, 0x128));  // row_ror:8
   auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  v = fmaxf(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
+  v = KV_MAX(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
   auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return fmaxf(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
+  return KV_MAX(__uint_as_float(r32[0]), __uint_as_float(r32[1]));
+#undef KV_MAX
+#undef KV_DPPF
 }
 
 // (score, slot) of the best candidate of the wave, ties to the lowest slot.
@@ -508,13 +510,13 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
       uint64_t b = 0;
       float bi = 0.f;
       for (int v0 = 0; v0 < live_waves; v0 += 4) {
+        // records past the live waves are read (v0 + 3 < NW) but never win
         uint4 r[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-          r[u] = v0 + u < live_waves ? sh.best[t & 1][v0 + u] : make_uint4(0u, 0u, 0u, 0u);
+        for (int u = 0; u < 4; ++u) r[u] = sh.best[t & 1][v0 + u];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const uint64_t o = ((uint64_t)r[u].y << 32) | r[u].x;
+          const uint64_t o = v0 + u < live_waves ? ((uint64_t)r[u].y << 32) | r[u].x : 0ull;
           if (o > b) {
             b = o;
             bi = __uint_as_float(r[u].z);
