@@ -80,12 +80,15 @@ __device__ __forceinline__ float wave_max_f(float v) {
 #undef KV_DPPF
 }
 
-// (score, slot) of the best candidate of the wave, ties to the lowest slot.
+// (score, slot) of the best candidate of the wave, ties to the lowest slot.  With one candidate
+// per lane (slots ascending with the lane) the lowest tied lane holds the lowest slot.
+template <bool ONE_PER_LANE>
 __device__ __forceinline__ uint64_t wave_best(float score, int slot) {
   const float wm = wave_max_f(score);
   const uint64_t tied = __ballot(score == wm);
   int best = __builtin_amdgcn_readlane(slot, __ffsll((unsigned long long)tied) - 1);
-  if (__popcll(tied) > 1) {  // exact tie between lanes: lowest slot among them
+  if (!ONE_PER_LANE && wm > -INFINITY && __popcll(tied) > 1) {
+    // exact tie between lanes: lowest slot among them (a wave with no live slot left ties at -inf)
     uint64_t rest = tied;
     while (rest) {
       const int l = __ffsll((unsigned long long)rest) - 1;
@@ -491,7 +494,7 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
           }
         }
       }
-      const uint64_t wbest = wave_best(my_score, my_slot);
+      const uint64_t wbest = wave_best<CPT == 1>(my_score, my_slot);
       // the wave's best slot is owned by one of its lanes (slot = tid + q NT): its 1 / |k| rides
       // along, so that no lookup follows the barrier
       const int bslot = unpack_slot(wbest);
