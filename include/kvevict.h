@@ -38,7 +38,9 @@
  *   k_out, v_out [n_prob][h_kv][budget + keep_tail][d], same dtype as k and v
  *
  * Supported shapes: d in {64, 128}; 2 <= w; h_q % h_kv == 0; G*w <= 128 with G = h_q / h_kv;
- * L_p >= w + 1 and L_p <= 2^24; 1 <= budget <= L_p - keep_tail; keep_tail in [0, L_p - 1].
+ * L_p >= w + 1 and L_p <= 2^24; 1 <= budget <= L_p - keep_tail (with per-problem budgets B_p,
+ * each B_p <= L_p - keep_tail and `budget` only bounds them as the row stride); keep_tail in
+ * [0, L_p - 1].
  */
 #ifndef KVEVICT_H
 #define KVEVICT_H

@@ -59,12 +59,14 @@ int check_problem(const kv_problem* pr, kv::Shape* s) {
   return KV_OK;
 }
 
-int check_budget(const kv_problem* pr, int32_t budget, int32_t keep_tail) {
+// The uniform budget (per_problem = false), or the row stride of per-problem budgets, which may
+// exceed a short problem's candidates (its own B_p is checked by check_budgets).
+int check_budget(const kv_problem* pr, int32_t budget, int32_t keep_tail, bool per_problem = false) {
   if (budget < 1) return KV_ERR_BUDGET;
   for (int p = 0; p < pr->n_prob; ++p) {
     const int L = pr->len_host[p];
     if (keep_tail < 0 || keep_tail > L - 1) return KV_ERR_ARG;
-    if (budget > L - keep_tail) return KV_ERR_BUDGET;
+    if (!per_problem && budget > L - keep_tail) return KV_ERR_BUDGET;
   }
   return KV_OK;
 }
@@ -144,7 +146,8 @@ int32_t kv_candidate_stride(const kv_problem* pr, int32_t budget, int32_t cand_m
                             int32_t keep_tail) {
   kv::Shape s;
   if (check_problem(pr, &s) != KV_OK || cand_mult < 0 || budget < 1) return 0;
-  if (check_budget(pr, budget, keep_tail) != KV_OK) return 0;
+  // `budget` may be the row stride of per-problem budgets: no bound by the candidates here
+  if (check_budget(pr, budget, keep_tail, true) != KV_OK) return 0;
   if (cand_mult > 0) {
     const int64_t c = (int64_t)cand_mult * budget;
     return c > INT32_MAX ? 0 : (int32_t)c;
@@ -265,7 +268,7 @@ int kv_mmr_select_ex(const kv_problem* pr, const float* mu, const float* sigma, 
   const int32_t* b_host = opts ? opts->budget_host : nullptr;
   const int32_t* b_dev = opts ? opts->budget_dev : nullptr;
   if (pool < 1 || pool > kMaxPool || pool % 2 == 0 || !std::isfinite(w_mu)) return KV_ERR_ARG;
-  st = check_budget(pr, budget, keep_tail);
+  st = check_budget(pr, budget, keep_tail, b_host != nullptr || b_dev != nullptr);
   if (st != KV_OK) return st;
   st = check_budgets(pr, budget, keep_tail, b_host, b_dev);
   if (st != KV_OK) return st;
@@ -311,7 +314,7 @@ int kv_compact_cache_ex(const kv_problem* pr, const void* k, const void* v,
   if (st != KV_OK) return st;
   if (!k || !v || !sel_idx || !k_out || !v_out) return KV_ERR_NULL;
   if (!aligned16(k) || !aligned16(v) || !aligned16(k_out) || !aligned16(v_out)) return KV_ERR_ARG;
-  st = check_budget(pr, budget, keep_tail);
+  st = check_budget(pr, budget, keep_tail, budget_host != nullptr || budget_dev != nullptr);
   if (st != KV_OK) return st;
   st = check_budgets(pr, budget, keep_tail, budget_host, budget_dev);
   if (st != KV_OK) return st;

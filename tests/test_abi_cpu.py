@@ -186,6 +186,13 @@ def test_per_problem_budget_checks():
     assert sel_ex([64, 10], dev=False) == _lib.KV_ERR_NULL
     assert compact_ex([64, 0]) == _lib.KV_ERR_BUDGET
     assert compact_ex([64, 10], host=False) == _lib.KV_ERR_NULL
+    # the row stride may exceed a short problem's 68 candidates when every B_p fits: validation
+    # passes (no GPU here, so the launch itself is what fails); the uniform budget may not
+    assert sel_ex([96, 10], budget=96) == _lib.KV_ERR_LAUNCH
+    assert compact_ex([96, 10], budget=96) == _lib.KV_ERR_LAUNCH
+    assert lib.kv_mmr_select(pr.ref(), P, P, P, P, P, 96, 4, 32, P, NULL, NULL, NULL, NULL, 0,
+                             NULL) == _lib.KV_ERR_BUDGET
+    assert lib.kv_candidate_stride(pr.ref(), 96, 4, 32) == 384
 
 
 @pytest.mark.parametrize("budget,n_layers,beta", [(64, 32, 20.0), (10, 4, 5.0), (128, 32, 20.0),

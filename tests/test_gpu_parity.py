@@ -224,3 +224,16 @@ def test_deterministic_repeat():
     for name in ("row_max", "row_sum", "mu", "sigma", "sel_idx", "sel_score", "cand_idx",
                  "cand_corr", "k_out", "v_out"):
         np.testing.assert_array_equal(a.host[name], b.host[name], err_msg=name)
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_short_contexts_near_the_window(fused):
+    """Contexts of 33, 64, 65, 95 and 287 keys in one bf16 batch with per-problem budgets: one
+    candidate, partial tiles, the causal triangle of the window across two tiles, tiles with no
+    unmasked key for some rows."""
+    wl = workloads.Workload(
+        "short_contexts_W32", 1, workloads.BF16, 32, 8, 128, 32, 64, 5, 1, [33, 64, 65, 95, 287],
+        workloads.Layout(cluster_density=0.02),
+        workloads.ProfileSpec(workloads.PROFILE_GLOBAL, (float(np.arcsinh(0.3)),)),
+        workloads.ProfileSpec(workloads.PROFILE_GLOBAL, (float(np.arcsinh(-0.8)),)))
+    _all(gpu_cases.run_gpu(wl, fused=fused, budgets=[1, 8, 8, 16, 64]))
