@@ -137,6 +137,67 @@ def copy_probe(torch, mib: int) -> None:
     print(json.dumps({"copy_probe_bytes": n, "launches": 3}), flush=True)
 
 
+def config_passes(torch, args) -> None:
+    """One JSON line per workload of the other configurations: the same batched pass (scoring,
+    selection, compaction), timed the same way (cache read-flushed before every step, HIP events),
+    with its algorithmic bytes per second.  The ragged batch times its three coefficient runs over
+    one scoring."""
+    from paper_2609_30738_amd import _lib, api, workloads as W
+    flush_buf = torch.ones(128 << 20, dtype=torch.float32, device="cuda")
+    cases = [W.mistral_layer()] + [W.mistral_pass_8k(b) for b in (32, 64, 128)]
+    ragged = [W.ragged_batch(r) for r in ("dispersion_only", "redundancy_only", "both")]
+    stream = torch.cuda.current_stream()
+
+    def run(wl, packed, lam_runs):
+        inp = api.upload(wl.dtype, wl.h_q, wl.h_kv, wl.d, wl.w, packed.q_win, packed.k, packed.v,
+                         packed.lens, packed.tok_off, *lam_runs[0])
+        out = api.allocate(inp, wl.budget)
+        b = inp.batch
+        lam_dev = [(torch.from_numpy(np.asarray(l1, np.float32)).cuda(),
+                    torch.from_numpy(np.asarray(l2, np.float32)).cuda()) for l1, l2 in lam_runs]
+        rows = []
+        for it in range(args.warmup + args.steps):
+            flush_buf.amax()
+            evs = [torch.cuda.Event(enable_timing=True) for _ in range(2 + len(lam_dev))]
+            evs[0].record(stream)
+            _lib.window_mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
+                                 out.sigma, out.ws)
+            evs[1].record(stream)
+            for r, (l1, l2) in enumerate(lam_dev):
+                _lib.mmr_select(b, out.mu, out.sigma, inp.k, l1, l2, wl.budget, 4, wl.w,
+                                out.sel_idx, None, None, None, out.ws)
+                _lib.compact_cache(b, inp.k, inp.v, out.sel_idx, wl.budget, wl.w, out.k_out,
+                                   out.v_out)
+                evs[2 + r].record(stream)
+            if it >= args.warmup:
+                rows.append(evs)
+        torch.cuda.synchronize()
+        t = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(len(e) - 1)] for e in rows])
+        return t.mean(axis=0), algorithmic_bytes(wl)
+
+    for wl in cases:
+        packed = W.draw_packed(wl)
+        parts, ab = run(wl, packed, [lambdas(wl)])
+        ms = float(parts.sum())
+        print(json.dumps({"config": wl.name, "ms_per_pass": round(ms, 4),
+                          "scoring_ms": round(float(parts[0]), 4),
+                          "select_compact_ms": round(float(parts[1]), 4),
+                          "algorithmic_bytes": ab["total"],
+                          "GBps": round(ab["total"] / (ms * 1e-3) / 1e9, 1)}), flush=True)
+    packed = W.draw_packed(ragged[0])  # the three runs share their inputs
+    parts, ab = run(ragged[0], packed, [lambdas(wl) for wl in ragged])
+    print(json.dumps({"config": ragged[0].name.replace("_dispersion_only", ""),
+                      "total_tokens_per_layer": int(packed.lens.sum() // ragged[0].n_layers),
+                      "scoring_ms": round(float(parts[0]), 4),
+                      "select_compact_ms_per_run": {r: round(float(x), 4) for r, x in
+                                                    zip(("dispersion_only", "redundancy_only",
+                                                         "both"), parts[1:])},
+                      "ms_per_pass_both": round(float(parts[0] + parts[3]), 4),
+                      "algorithmic_bytes": ab["total"],
+                      "GBps_both": round(ab["total"] / (float(parts[0] + parts[3]) * 1e-3) / 1e9, 1)}),
+          flush=True)
+
+
 def main() -> None:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -149,6 +210,9 @@ def main() -> None:
                     help="how the last-level cache is emptied before each timed step")
     ap.add_argument("--unfused", action="store_true",
                     help="time kv_window_scores + kv_mu_sigma instead of kv_window_mu_sigma")
+    ap.add_argument("--configs", action="store_true",
+                    help="only time the pass on the other workloads (one layer, the 8k sweep over B, "
+                         "the ragged batch), one JSON line each")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB three times (the known-size "
                          "kernel that scales the HBM byte counters) and exit")
@@ -165,6 +229,10 @@ def main() -> None:
     torch.cuda.set_device(0)
     if args.copy_probe_mib > 0:
         copy_probe(torch, args.copy_probe_mib)
+        return
+    if args.configs:
+        _lib.lib()
+        config_passes(torch, args)
         return
     _lib.lib()  # fail loudly if the library is missing
 
