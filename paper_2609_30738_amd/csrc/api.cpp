@@ -230,8 +230,11 @@ int kv_window_mu_sigma_ex(const kv_problem* pr, const void* q_win, const void* k
     return KV_ERR_WORKSPACE;
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (kv::stream_shape_ok(s, scale)) {
-    // segment partials, then normalisers, row statistics and mu / sigma in one more pass
     const kv::StreamPlan plan = stream_plan_of(pr, s);
+    if (plan.max_segs == 1)  // every unit one segment: both passes of a unit in one workgroup
+      return launch_status(kv::launch_stream_window(s, plan, q_win, k, scale, row_max, row_sum, mu,
+                                                    sigma, all, hs));
+    // segment partials, then normalisers, row statistics and mu / sigma in one more pass
     st = launch_status(kv::launch_stream_stats(s, plan, q_win, k, scale, ws, nullptr, nullptr, hs));
     if (st != KV_OK) return st;
     return launch_status(kv::launch_stream_mu_sigma(s, plan, q_win, k, scale, ws, nullptr,

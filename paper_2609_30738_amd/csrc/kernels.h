@@ -60,6 +60,11 @@ hipError_t launch_stream_mu_sigma(const Shape& s, const StreamPlan& plan, const 
                                   const float* row_max_in, const float* row_sum_in,
                                   float* row_max_out, float* row_sum_out, float* mu, float* sigma,
                                   bool sigma_all, hipStream_t stream);
+// Both passes in one launch when every unit is one segment (plan.max_segs == 1): row_max /
+// row_sum and mu / sigma out, no workspace.
+hipError_t launch_stream_window(const Shape& s, const StreamPlan& plan, const void* q_win,
+                                const void* k, float scale, float* row_max, float* row_sum,
+                                float* mu, float* sigma, bool sigma_all, hipStream_t stream);
 // row_max / row_sum from chunk partials [n_units][max_chunks][rows_pad] of chunk_keys keys each.
 hipError_t launch_combine_partials(const Shape& s, const void* part, int chunk_keys,
                                    int max_chunks, int rows_pad, float* row_max, float* row_sum,

@@ -2,7 +2,7 @@
 // normalisers of a unit from the pass-1 partials, then per key the group-mean attention of the
 // window rows, its mean mu and sample standard deviation sigma.  The design shared with pass 1 is
 // described in stream_common.h.
-#include "stream_common.h"
+#include "stream_passes.h"
 
 namespace kv {
 namespace stream {
@@ -83,80 +83,8 @@ __global__ __launch_bounds__(NW * 64, 1) void mu_sigma_stream_kernel(StreamArgs 
   }
   __syncthreads();
   const size_t stat_base = (size_t)a.tok_off[p] * a.h_kv + (size_t)g * L;
-  auto tile = [&](const bf16x8_t (&kt)[NS], int t0, auto masked) __attribute__((always_inline)) {
-    const int key = t0 + l32;
-    // window row r = 4 half + 8 (j / 4) + (j % 4) of every head sees the key iff key <= L - 32 + r
-    const int thr = key - (L - 32) - 4 * half;
-    float ab[16];
-    float h_mean = 0.f, h_m2 = 0.f;  // ALL: running mean and squared deviations of the heads so far
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      float eb[16];
-      const f32x16_t d = chain<NS>(q[b], kt);
-#pragma unroll
-      for (int qq = 0; qq < 4; ++qq) {
-        // window rows 8 qq + 4 half + 0..3 of query head b (read per tile: the registers hold
-        // the queries, the tile and the logit blocks)
-        const float4 bv = *reinterpret_cast<const float4*>(bsh + b * 32 + 8 * qq + 4 * half);
-        const float bb[4] = {bv.x, bv.y, bv.z, bv.w};
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int j = 4 * qq + u;
-          float e = __builtin_amdgcn_exp2f(fmaf(d[j], c, -bb[u]));
-          if (decltype(masked)::value && 8 * qq + u < thr) e = 0.f;
-          ab[j] = b == 0 ? e : ab[j] + e;
-          eb[j] = e;
-        }
-      }
-      if constexpr (ALL) {
-        float hs[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int j = 0; j < 16; ++j) hs[j & 3] += eb[j];
-        const float mb = sum_halves((hs[0] + hs[1]) + (hs[2] + hs[3])) * (1.f / 32.f);
-        float hv[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const float dl = eb[j] - mb;
-          hv[j & 3] = fmaf(dl, dl, hv[j & 3]);
-        }
-        const float m2b = sum_halves((hv[0] + hv[1]) + (hv[2] + hv[3]));
-        if (b == 0) {
-          h_mean = mb;
-          h_m2 = m2b;
-        } else {  // b heads of 32 rows merged with one more
-          const float dl = mb - h_mean;
-          h_mean = fmaf(dl, 1.f / (float)(b + 1), h_mean);
-          h_m2 += fmaf(dl * dl, 32.f * (float)b / (float)(b + 1), m2b);
-        }
-      }
-    }
-    // ab[j] = G a[r][key] for the window rows r = acc_row(j, lane); the other 16 are in lane ^ 32
-    float sp[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) sp[u] = (ab[u] + ab[u + 4]) + (ab[u + 8] + ab[u + 12]);
-    const float mean = sum_halves((sp[0] + sp[1]) + (sp[2] + sp[3])) * (inv_g * (1.f / 32.f));
-    float var;
-    if constexpr (ALL) {
-      var = h_m2 * (1.f / (float)(NB * 32 - 1));
-    } else {
-      float vp[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const float dl = fmaf(ab[j], inv_g, -mean);
-        vp[j & 3] = fmaf(dl, dl, vp[j & 3]);
-      }
-      var = sum_halves((vp[0] + vp[1]) + (vp[2] + vp[3])) * (1.f / 31.f);
-    }
-    if (key < k1) (half == 0 ? a.mu : a.sigma)[stat_base + key] = half == 0 ? mean : __builtin_amdgcn_sqrtf(var);
-  };
-
-  for (int j = 0; j < my_tiles; ++j) {
-    bf16x8_t kt[NS];
-    ks.template next<1>(kt, j, my_tiles, l32, half);  // one mu / sigma store per tile
-    const int t0 = ks.tile_key(j);
-    if (t0 + 31 > L - 32) tile(kt, t0, std::true_type{});
-    else tile(kt, t0, std::false_type{});
-  }
+  mu_sigma_tiles<D, NB, ALL, NW, S>(ks, q, bsh, my_tiles, k1, L, c, inv_g, a.mu + stat_base,
+                                    a.sigma + stat_base, l32, half);
   wait_vmem<0>();  // no load into the ring may outlive the workgroup
 }
 

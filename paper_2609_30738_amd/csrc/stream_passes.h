@@ -1,0 +1,189 @@
+// Per-segment loops of the two streaming passes (section 3.1, Eq. (1); section 3.2, Eq. (3)),
+// shared by the pass kernels (stream_stats.hip, stream_mu_sigma.hip) and by the kernel that runs
+// both passes over a whole unit in one workgroup (stream_window.hip).  The tile geometry and the
+// key stream are described in stream_common.h.
+#pragma once
+
+#include "stream_common.h"
+
+namespace kv {
+namespace stream {
+
+// Pass 1 over the wave's tiles of a segment [k0, k1) of a unit with L keys: for every head, the
+// running maximum m of t = logit * c and the sum z of 2^(t - m) over the keys the lane's window
+// row sees (online softmax; base 2).  Interior tiles run without masks or branches; a tile with a
+// masked key (the causal triangle of the window, keys past the segment end) takes a guarded path.
+template <int D, int NB, int NW, int S>
+__device__ __forceinline__ void stats_tiles(const KeyStream<D, NB, NW, S>& ks,
+                                            const bf16x8_t (&q)[NB][D / 16], int my_tiles, int k1,
+                                            int L, float c, int l32, int half, float (&m_run)[NB],
+                                            float (&z_run)[NB]) {
+  constexpr int NS = D / 16;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    m_run[b] = -INFINITY;
+    z_run[b] = 0.f;
+  }
+  // a tile is interior when none of its keys is masked: t0 + 31 < min(k1, L - 31)
+  const int kedge = min(k1, L - 31);
+  for (int j = 0; j < my_tiles; ++j) {
+    bf16x8_t kt[NS];
+    ks.template next<0>(kt, j, my_tiles, l32, half);
+    const int t0 = ks.tile_key(j);
+    if (t0 + 31 < kedge) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const f32x16_t d = chain<NS>(kt, q[b]);
+        float mx = fmax3(fmax3(fmax3(d[0], d[1], d[2]), d[3], d[4]), d[5], d[6]);
+        mx = fmax3(fmax3(mx, d[7], d[8]), d[9], d[10]);
+        mx = fmax3(fmax3(mx, d[11], d[12]), d[13], d[14]);
+        const float mn = __builtin_elementwise_maximum(m_run[b], __builtin_elementwise_maximum(mx, d[15]) * c);
+        const float keep = __builtin_amdgcn_exp2f(m_run[b] - mn);  // 0 on the lane's first tile
+        float ex[16];
+#pragma unroll
+        for (int jj = 0; jj < 16; ++jj) ex[jj] = __builtin_amdgcn_exp2f(fmaf(d[jj], c, -mn));
+        float zs[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) zs[u] = (ex[4 * u] + ex[4 * u + 1]) + (ex[4 * u + 2] + ex[4 * u + 3]);
+        z_run[b] = fmaf(z_run[b], keep, (zs[0] + zs[1]) + (zs[2] + zs[3]));
+        m_run[b] = mn;
+      }
+    } else {
+      // window row l32 of every head sees keys <= L - 32 + l32; keys >= k1 belong to the next
+      // segment.  The key of register jj is t0 + 4 half + 8 (jj / 4) + (jj % 4).
+      const int thr = min(k1 - 1, L - 32 + l32) - t0 - 4 * half;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        f32x16_t d = chain<NS>(kt, q[b]);
+#pragma unroll
+        for (int jj = 0; jj < 16; ++jj)
+          if (8 * (jj >> 2) + (jj & 3) > thr) d[jj] = -INFINITY;
+        float mx = d[0];
+#pragma unroll
+        for (int jj = 1; jj < 16; ++jj) mx = fmaxf(mx, d[jj]);
+        const float mn = fmaxf(m_run[b], mx * c);
+        if (mn != -INFINITY) {
+          const float keep = m_run[b] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[b] - mn);
+          float z = z_run[b] * keep;
+#pragma unroll
+          for (int jj = 0; jj < 16; ++jj) z += __builtin_amdgcn_exp2f(fmaf(d[jj], c, -mn));
+          z_run[b] = z;
+          m_run[b] = mn;
+        }
+      }
+    }
+  }
+}
+
+// Lanes l and l ^ 32 hold the same rows (different keys): merge them and put the wave's (m, z) of
+// unit row b * 32 + l32 into red[b * 32 + l32].  The caller merges the waves after a barrier.
+template <int NB>
+__device__ __forceinline__ void stats_to_lds(const float (&m_run)[NB], const float (&z_run)[NB],
+                                             float2* red, int l32, int half) {
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    float m = m_run[b], z = z_run[b];
+    merge_mz(m, z, swap_halves(m), swap_halves(z));
+    if (half == 0) red[b * 32 + l32] = make_float2(m, z);
+  }
+}
+
+// (m, z) of one row over the NW waves' entries red[w * R + row], merged in wave order
+template <int NW, int R>
+__device__ __forceinline__ float2 merge_waves(const float2* red, int row) {
+  float2 v = red[row];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) merge_mz(v.x, v.y, red[w * R + row].x, red[w * R + row].y);
+  return v;
+}
+
+// Pass 2 over the wave's tiles of a segment: logits again with keys as the MFMA N dimension (a
+// lane holds one key), a = 2^(t - b) with the row normalisers b = M + log2 Z read from bsh, summed
+// over the group's heads, then the mean and the two-pass sample variance over the 32 window rows,
+// stored as mu / sigma (mu_u, sigma_u: the unit's rows).  With ALL the variance runs over all
+// G x 32 (head, row) values: every head's mean and squared deviations over its 32 rows, merged
+// across heads with the pairwise update of Chan, Golub and LeVeque.
+template <int D, int NB, bool ALL, int NW, int S>
+__device__ __forceinline__ void mu_sigma_tiles(const KeyStream<D, NB, NW, S>& ks,
+                                               const bf16x8_t (&q)[NB][D / 16], const float* bsh,
+                                               int my_tiles, int k1, int L, float c, float inv_g,
+                                               float* mu_u, float* sigma_u, int l32, int half) {
+  constexpr int NS = D / 16;
+  auto tile = [&](const bf16x8_t (&kt)[NS], int t0, auto masked) __attribute__((always_inline)) {
+    const int key = t0 + l32;
+    // window row r = 4 half + 8 (j / 4) + (j % 4) of every head sees the key iff key <= L - 32 + r
+    const int thr = key - (L - 32) - 4 * half;
+    float ab[16];
+    float h_mean = 0.f, h_m2 = 0.f;  // ALL: running mean and squared deviations of the heads so far
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      float eb[16];
+      const f32x16_t d = chain<NS>(q[b], kt);
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq) {
+        // window rows 8 qq + 4 half + 0..3 of query head b (read per tile: the registers hold
+        // the queries, the tile and the logit blocks)
+        const float4 bv = *reinterpret_cast<const float4*>(bsh + b * 32 + 8 * qq + 4 * half);
+        const float bb[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int j = 4 * qq + u;
+          float e = __builtin_amdgcn_exp2f(fmaf(d[j], c, -bb[u]));
+          if (decltype(masked)::value && 8 * qq + u < thr) e = 0.f;
+          ab[j] = b == 0 ? e : ab[j] + e;
+          eb[j] = e;
+        }
+      }
+      if constexpr (ALL) {
+        float hs[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < 16; ++j) hs[j & 3] += eb[j];
+        const float mb = sum_halves((hs[0] + hs[1]) + (hs[2] + hs[3])) * (1.f / 32.f);
+        float hv[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const float dl = eb[j] - mb;
+          hv[j & 3] = fmaf(dl, dl, hv[j & 3]);
+        }
+        const float m2b = sum_halves((hv[0] + hv[1]) + (hv[2] + hv[3]));
+        if (b == 0) {
+          h_mean = mb;
+          h_m2 = m2b;
+        } else {  // b heads of 32 rows merged with one more
+          const float dl = mb - h_mean;
+          h_mean = fmaf(dl, 1.f / (float)(b + 1), h_mean);
+          h_m2 += fmaf(dl * dl, 32.f * (float)b / (float)(b + 1), m2b);
+        }
+      }
+    }
+    // ab[j] = G a[r][key] for the window rows r = acc_row(j, lane); the other 16 are in lane ^ 32
+    float sp[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) sp[u] = (ab[u] + ab[u + 4]) + (ab[u + 8] + ab[u + 12]);
+    const float mean = sum_halves((sp[0] + sp[1]) + (sp[2] + sp[3])) * (inv_g * (1.f / 32.f));
+    float var;
+    if constexpr (ALL) {
+      var = h_m2 * (1.f / (float)(NB * 32 - 1));
+    } else {
+      float vp[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const float dl = fmaf(ab[j], inv_g, -mean);
+        vp[j & 3] = fmaf(dl, dl, vp[j & 3]);
+      }
+      var = sum_halves((vp[0] + vp[1]) + (vp[2] + vp[3])) * (1.f / 31.f);
+    }
+    if (key < k1) (half == 0 ? mu_u : sigma_u)[key] = half == 0 ? mean : __builtin_amdgcn_sqrtf(var);
+  };
+
+  for (int j = 0; j < my_tiles; ++j) {
+    bf16x8_t kt[NS];
+    ks.template next<1>(kt, j, my_tiles, l32, half);  // one mu / sigma store per tile
+    const int t0 = ks.tile_key(j);
+    if (t0 + 31 > L - 32) tile(kt, t0, std::true_type{});
+    else tile(kt, t0, std::false_type{});
+  }
+}
+
+}  // namespace stream
+}  // namespace kv

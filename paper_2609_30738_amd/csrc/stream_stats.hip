@@ -1,7 +1,7 @@
 // Streaming window statistics, pass 1 (section 3.1): per segment of a unit's keys, the running
 // maximum and the sum of exponentials of every window row's logits.  The design shared with pass 2
 // is described in stream_common.h.
-#include "stream_common.h"
+#include "stream_passes.h"
 
 namespace kv {
 namespace stream {
@@ -39,74 +39,13 @@ __global__ __launch_bounds__(NW * 64, 1) void stats_stream_kernel(StreamArgs a) 
   hold_until_loaded<D, NB>(q);
 
   float m_run[NB], z_run[NB];
-#pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    m_run[b] = -INFINITY;
-    z_run[b] = 0.f;
-  }
-  // a tile is interior when none of its keys is masked: t0 + 31 < min(k1, L - 31)
-  const int kedge = min(k1, L - 31);
-  for (int j = 0; j < my_tiles; ++j) {
-    bf16x8_t kt[NS];
-    ks.template next<0>(kt, j, my_tiles, l32, half);
-    const int t0 = ks.tile_key(j);
-    if (t0 + 31 < kedge) {
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const f32x16_t d = chain<NS>(kt, q[b]);
-        float mx = fmax3(fmax3(fmax3(d[0], d[1], d[2]), d[3], d[4]), d[5], d[6]);
-        mx = fmax3(fmax3(mx, d[7], d[8]), d[9], d[10]);
-        mx = fmax3(fmax3(mx, d[11], d[12]), d[13], d[14]);
-        const float mn = __builtin_elementwise_maximum(m_run[b], __builtin_elementwise_maximum(mx, d[15]) * c);
-        const float keep = __builtin_amdgcn_exp2f(m_run[b] - mn);  // 0 on the lane's first tile
-        float ex[16];
-#pragma unroll
-        for (int jj = 0; jj < 16; ++jj) ex[jj] = __builtin_amdgcn_exp2f(fmaf(d[jj], c, -mn));
-        float zs[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) zs[u] = (ex[4 * u] + ex[4 * u + 1]) + (ex[4 * u + 2] + ex[4 * u + 3]);
-        z_run[b] = fmaf(z_run[b], keep, (zs[0] + zs[1]) + (zs[2] + zs[3]));
-        m_run[b] = mn;
-      }
-    } else {
-      // window row l32 of every head sees keys <= L - 32 + l32; keys >= k1 belong to the next
-      // segment.  The key of register jj is t0 + 4 half + 8 (jj / 4) + (jj % 4).
-      const int thr = min(k1 - 1, L - 32 + l32) - t0 - 4 * half;
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        f32x16_t d = chain<NS>(kt, q[b]);
-#pragma unroll
-        for (int jj = 0; jj < 16; ++jj)
-          if (8 * (jj >> 2) + (jj & 3) > thr) d[jj] = -INFINITY;
-        float mx = d[0];
-#pragma unroll
-        for (int jj = 1; jj < 16; ++jj) mx = fmaxf(mx, d[jj]);
-        const float mn = fmaxf(m_run[b], mx * c);
-        if (mn != -INFINITY) {
-          const float keep = m_run[b] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[b] - mn);
-          float z = z_run[b] * keep;
-#pragma unroll
-          for (int jj = 0; jj < 16; ++jj) z += __builtin_amdgcn_exp2f(fmaf(d[jj], c, -mn));
-          z_run[b] = z;
-          m_run[b] = mn;
-        }
-      }
-    }
-  }
+  stats_tiles<D, NB, NW, S>(ks, q, my_tiles, k1, L, c, l32, half, m_run, z_run);
   wait_vmem<0>();  // no load into the ring may outlive the workgroup
 
-  // lanes l and l ^ 32 hold the same rows (different keys); then the waves
-#pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    float m = m_run[b], z = z_run[b];
-    merge_mz(m, z, swap_halves(m), swap_halves(z));
-    if (half == 0) red[wave][b * 32 + l32] = make_float2(m, z);
-  }
+  stats_to_lds<NB>(m_run, z_run, red[wave], l32, half);
   __syncthreads();
   if (threadIdx.x < R) {
-    float2 v = red[0][threadIdx.x];
-#pragma unroll
-    for (int w = 1; w < NW; ++w) merge_mz(v.x, v.y, red[w][threadIdx.x].x, red[w][threadIdx.x].y);
+    const float2 v = merge_waves<NW, R>(&red[0][0], threadIdx.x);
     if (a.part) {
       a.part[(((size_t)p * a.h_kv + g) * a.max_segs + seg) * R + threadIdx.x] = v;
     } else {  // every unit is one segment: the row statistics themselves

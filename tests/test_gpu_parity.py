@@ -237,3 +237,27 @@ def test_short_contexts_near_the_window(fused):
         workloads.ProfileSpec(workloads.PROFILE_GLOBAL, (float(np.arcsinh(0.3)),)),
         workloads.ProfileSpec(workloads.PROFILE_GLOBAL, (float(np.arcsinh(-0.8)),)))
     _all(gpu_cases.run_gpu(wl, fused=fused, budgets=[1, 8, 8, 16, 64]))
+
+
+def _one_segment_per_unit(wl) -> bool:
+    """Whether the streaming plan gives every unit a single segment (both passes of a unit then
+    run in one workgroup): about one segment per compute unit, 1024 keys at least, in whole
+    256-key steps, never longer than the longest context."""
+    total = int(wl.lens.astype(np.int64).sum()) * wl.h_kv
+    seg = max(1024, -(-(-(-total // 256)) // 256) * 256)
+    seg = min(seg, -(-int(wl.lens.max()) // 256) * 256)
+    return seg >= int(wl.lens.max())
+
+
+@pytest.mark.parametrize("sigma_rows", ["group_mean", "all_rows"])
+def test_both_passes_in_one_workgroup_ragged(sigma_rows):
+    """256 units of 1024, 1000, 700 and 513 keys (8 layers of 4 sequences): each unit is one
+    segment, so the fused entry point runs pass 1, the normalisers and pass 2 of a unit in one
+    workgroup; ragged tails, whole tiles and the window's causal triangle."""
+    wl = workloads.Workload(
+        "one_segment_units_W32", 1, workloads.BF16, 32, 8, 128, 32, 32, 4, 8, [1024, 1000, 700, 513],
+        workloads.Layout(cluster_density=0.02),
+        workloads.ProfileSpec(workloads.PROFILE_GLOBAL, (float(np.arcsinh(0.3)),)),
+        workloads.ProfileSpec(workloads.PROFILE_GLOBAL, (float(np.arcsinh(-0.8)),)))
+    assert wl.n_prob * wl.h_kv == 256 and _one_segment_per_unit(wl)
+    _all(gpu_cases.run_gpu(wl, fused=True, sigma_rows=sigma_rows))
