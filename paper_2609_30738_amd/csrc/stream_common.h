@@ -1,6 +1,7 @@
 // Building blocks of the streaming window kernels (pass 1 in stream_stats.hip, pass 2 in
-// stream_mu_sigma.hip): the argument block, the tile geometry, the per-wave key stream into LDS
-// and small wave-level helpers.
+// stream_mu_sigma.hip, both passes of a unit in one workgroup in stream_window.hip; the passes'
+// per-segment loops in stream_passes.h): the argument block, the tile geometry, the per-wave key
+// stream into LDS and small wave-level helpers.
 //
 // Streaming window statistics for bf16 caches with w = 32 (section 3.1, Eq. (1), Eq. (3)): two
 // passes over the keys, each a plain stream from HBM with no communication between workgroups.

@@ -63,3 +63,10 @@ def test_committed_traffic_records_name_their_kernel():
         assert rec["source_files"] == list(bench.KERNEL_SOURCES[kernel])
         assert rec["algorithmic_bytes_per_launch"] == bench.algorithmic_bytes(
             workloads.mistral_pass_32k())["stats_pass" if kernel == "stats_stream" else "mu_sigma_pass"]
+
+
+def test_source_hash_ignores_comments_only():
+    code = bench._code_only('int a; // note\n/* block\n note */ int b;\nconst char* s = "a // b";\n\n')
+    assert code == 'int a;\n int b;\nconst char* s = "a // b";'
+    assert bench._code_only("x = 1;  // one\n") == bench._code_only("// header\nx = 1;\n")
+    assert bench._code_only("x = 1;\n") != bench._code_only("x = 2;\n")
