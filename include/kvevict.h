@@ -124,8 +124,9 @@ int kv_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float sc
                 float* attn, void* stream);
 
 /* kv_window_scores followed by kv_mu_sigma (without attn): same results in one call.  The
- * normalisers go from the first pass to the second through the workspace, without a round trip
- * through row_max / row_sum.  Needs workspace. */
+ * normalisers go from the first pass to the second without a round trip through row_max /
+ * row_sum: inside one workgroup when a batch is large enough for every (problem, kv head) to be
+ * scored by one workgroup, else through the workspace.  Needs workspace (always validated). */
 int kv_window_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float scale,
                        float* row_max, float* row_sum, float* mu, float* sigma, void* ws,
                        size_t ws_bytes, void* stream);
