@@ -126,7 +126,11 @@ int kv_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float sc
 /* kv_window_scores followed by kv_mu_sigma (without attn): same results in one call.  The
  * normalisers go from the first pass to the second without a round trip through row_max /
  * row_sum: inside one workgroup when a batch is large enough for every (problem, kv head) to be
- * scored by one workgroup, else through the workspace.  Needs workspace (always validated). */
+ * scored by one workgroup, else through the workspace (in one launch when the batch fits the chip
+ * at once; a workgroup then polls the workspace for the other segments of its (problem, kv head)
+ * and, if they are late, computes their partials itself; the environment variable
+ * KVEVICT_SPIN_LIMIT sets the number of polls, 0 taking that path at once).  Needs workspace
+ * (always validated); calls that overlap on one workspace race. */
 int kv_window_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float scale,
                        float* row_max, float* row_sum, float* mu, float* sigma, void* ws,
                        size_t ws_bytes, void* stream);

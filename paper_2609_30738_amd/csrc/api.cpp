@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdlib>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -97,6 +98,18 @@ int max_candidates(const kv_problem* pr, int32_t budget, int32_t cand_mult, int3
 }
 
 int launch_status(hipError_t e) { return e == hipSuccess ? KV_OK : KV_ERR_LAUNCH; }
+
+// Polls a workgroup of the one-launch window path makes for its unit's other segments before it
+// computes their partials itself: the default, or KVEVICT_SPIN_LIMIT (0 takes that path at once).
+uint32_t spin_limit() {
+  const char* e = std::getenv("KVEVICT_SPIN_LIMIT");
+  if (e && *e) {
+    char* end = nullptr;
+    const unsigned long v = std::strtoul(e, &end, 10);
+    if (end && *end == '\0') return (uint32_t)std::min<unsigned long>(v, 1ul << 30);
+  }
+  return kv::kDefaultSpinLimit;
+}
 
 // Segment plan of the streaming window kernels for this batch.
 kv::StreamPlan stream_plan_of(const kv_problem* pr, const kv::Shape& s) {
@@ -234,6 +247,11 @@ int kv_window_mu_sigma_ex(const kv_problem* pr, const void* q_win, const void* k
     if (plan.max_segs == 1)  // every unit one segment: both passes of a unit in one workgroup
       return launch_status(kv::launch_stream_window(s, plan, q_win, k, scale, row_max, row_sum, mu,
                                                     sigma, all, hs));
+    // several segments per unit: one cooperative launch if the grid fits the chip at once
+    bool launched = false;
+    st = launch_status(kv::launch_stream_window_coop(s, plan, q_win, k, scale, ws, row_max, row_sum,
+                                                     mu, sigma, all, spin_limit(), hs, &launched));
+    if (st != KV_OK || launched) return st;
     // segment partials, then normalisers, row statistics and mu / sigma in one more pass
     st = launch_status(kv::launch_stream_stats(s, plan, q_win, k, scale, ws, nullptr, nullptr, hs));
     if (st != KV_OK) return st;

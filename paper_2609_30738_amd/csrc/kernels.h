@@ -48,6 +48,7 @@ struct StreamPlan {
 bool stream_shape_ok(const Shape& s, float scale);
 StreamPlan stream_plan(const Shape& s, int64_t total_keys);  // total_keys = sum_p h_kv L_p
 size_t stream_ws_bytes(const Shape& s, const StreamPlan& plan);
+size_t stream_counter_offset(const Shape& s, const StreamPlan& plan);  // counters after the partials
 // Pass 1: segment partials into ws or, with ws == nullptr (only when plan.max_segs == 1), the
 // row statistics into row_max / row_sum.
 hipError_t launch_stream_stats(const Shape& s, const StreamPlan& plan, const void* q_win,
@@ -65,6 +66,15 @@ hipError_t launch_stream_mu_sigma(const Shape& s, const StreamPlan& plan, const 
 hipError_t launch_stream_window(const Shape& s, const StreamPlan& plan, const void* q_win,
                                 const void* k, float scale, float* row_max, float* row_sum,
                                 float* mu, float* sigma, bool sigma_all, hipStream_t stream);
+// Both passes in one launch when units span several segments: partials and per-unit arrival
+// counters in ws; a workgroup polls at most spin_limit times for its unit's other segments before
+// it computes their partials itself.  Sets *launched = false (and launches nothing) if the grid
+// does not fit the chip at once; the caller then takes the two-launch path.
+hipError_t launch_stream_window_coop(const Shape& s, const StreamPlan& plan, const void* q_win,
+                                     const void* k, float scale, void* ws, float* row_max,
+                                     float* row_sum, float* mu, float* sigma, bool sigma_all,
+                                     uint32_t spin_limit, hipStream_t stream, bool* launched);
+constexpr uint32_t kDefaultSpinLimit = 4096;  // polls (each a device-coherent load and a short sleep)
 // row_max / row_sum from chunk partials [n_units][max_chunks][rows_pad] of chunk_keys keys each.
 hipError_t launch_combine_partials(const Shape& s, const void* part, int chunk_keys,
                                    int max_chunks, int rows_pad, float* row_max, float* row_sum,

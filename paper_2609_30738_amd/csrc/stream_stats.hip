@@ -86,8 +86,14 @@ StreamPlan stream_plan(const Shape& s, int64_t total_keys) {
   return plan;
 }
 
+size_t stream_counter_offset(const Shape& s, const StreamPlan& plan) {
+  const size_t part = (size_t)s.n_prob * s.h_kv * plan.max_segs * s.group() * 32 * sizeof(float2);
+  return (part + 255) & ~(size_t)255;
+}
+
 size_t stream_ws_bytes(const Shape& s, const StreamPlan& plan) {
-  return (size_t)s.n_prob * s.h_kv * plan.max_segs * s.group() * 32 * sizeof(float2);
+  // segment partials, then one arrival counter per unit (both passes in one launch)
+  return stream_counter_offset(s, plan) + (size_t)s.n_prob * s.h_kv * sizeof(uint32_t);
 }
 
 hipError_t launch_stream_stats(const Shape& s, const StreamPlan& plan, const void* q_win,

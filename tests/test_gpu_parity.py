@@ -261,3 +261,19 @@ def test_both_passes_in_one_workgroup_ragged(sigma_rows):
         workloads.ProfileSpec(workloads.PROFILE_GLOBAL, (float(np.arcsinh(-0.8)),)))
     assert wl.n_prob * wl.h_kv == 256 and _one_segment_per_unit(wl)
     _all(gpu_cases.run_gpu(wl, fused=True, sigma_rows=sigma_rows))
+
+
+@pytest.mark.parametrize("sigma_rows", ["group_mean", "all_rows"])
+def test_segments_computed_by_a_waiting_workgroup(sigma_rows, monkeypatch):
+    """Units of 4096 keys in 4 segments (one Mistral-shaped layer): both passes run in one launch,
+    and a workgroup that stops waiting for its unit's other segments computes their partials
+    itself.  A poll limit of 0, set from the host, sends every workgroup down that path: the
+    results match the oracle and are bit-identical to those of the default path."""
+    wl = workloads.mistral_layer()
+    monkeypatch.delenv("KVEVICT_SPIN_LIMIT", raising=False)
+    ref = gpu_cases.run_gpu(wl, fused=True, sigma_rows=sigma_rows)
+    monkeypatch.setenv("KVEVICT_SPIN_LIMIT", "0")
+    run = gpu_cases.run_gpu(wl, fused=True, sigma_rows=sigma_rows)
+    for name in ("row_max", "row_sum", "mu", "sigma", "sel_idx", "k_out", "v_out"):
+        assert np.array_equal(run.host[name], ref.host[name]), name
+    _all(run)
