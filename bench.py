@@ -436,9 +436,10 @@ def main() -> None:
     ab = algorithmic_bytes(wl)
     flops = mfma_flops(wl)
     # The dominant kernel is the scoring kernel of the timed pass (kv_window_mu_sigma with every
-    # unit one segment: both passes of a unit in one workgroup).  What it must move: K and Q_W
-    # once, the row statistics and mu / sigma out; its second read of K is overhead, and shows in
-    # `traffic`.  roofline_passes gives the same view of the two passes run as separate launches.
+    # unit one segment: both passes of a unit in one workgroup).  What the method must move for it
+    # is K and Q_W once; its second read of K and its outputs (row statistics, mu and sigma) are
+    # overhead of the design, and show in `traffic`.  roofline_passes gives the same view of the
+    # two passes run as separate launches.
     def roofline(kernel, alg, kms):
         achieved = alg / (kms * 1e-3) / 1e9
         return {"kernel": kernel, "bound": "hbm", "achieved": round(achieved, 1),
@@ -446,9 +447,9 @@ def main() -> None:
                 "traffic": measured_traffic(kernel, wl.name),
                 "algorithmic_bytes_per_launch": alg, "ms_per_launch": round(kms, 4)}
     dominant = roofline("stats_stream+mu_sigma_stream" if args.unfused else "window_stream",
-                        ab["mu_sigma_pass"], float(mean_part[0]))
-    passes = [roofline("stats_stream", ab["stats_pass"], k_stats),
-              roofline("mu_sigma_stream", ab["mu_sigma_pass"], k_mu)]
+                        ab["scoring"], float(mean_part[0]))
+    passes = [roofline("stats_stream", ab["scoring"], k_stats),
+              roofline("mu_sigma_stream", ab["scoring"], k_mu)]
     line = {
         "metric": "ms per 32-layer eviction pass at L=32k,W=32,B=64; HBM GB/s vs peak",
         "value": round(ms, 4),

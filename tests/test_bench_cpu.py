@@ -27,6 +27,7 @@ def test_algorithmic_bytes_of_the_benchmark_workload():
     assert ab["mu_sigma_pass"] == pass2 == 2_223_243_264
     kept = units * 2 * 2 * (B + W) * d * e  # K and V rows kept, read and written
     assert ab["total"] == units * (L * d * e + G * W * d * e) + kept + units * B * 4
+    assert ab["scoring"] == units * (L * d * e + G * W * d * e) == 2_155_872_256
     assert bench.mfma_flops(wl) == 2.0 * 32 * L * 32 * W * d
 
 
@@ -62,7 +63,7 @@ def test_committed_traffic_records_name_their_kernel():
         assert rec["kernel"].startswith(kernel)
         assert rec["source_files"] == list(bench.KERNEL_SOURCES[kernel])
         assert rec["algorithmic_bytes_per_launch"] == bench.algorithmic_bytes(
-            workloads.mistral_pass_32k())["stats_pass" if kernel == "stats_stream" else "mu_sigma_pass"]
+            workloads.mistral_pass_32k())["scoring"]
 
 
 def test_source_hash_ignores_comments_only():
