@@ -277,3 +277,34 @@ def test_segments_computed_by_a_waiting_workgroup(sigma_rows, monkeypatch):
     for name in ("row_max", "row_sum", "mu", "sigma", "sel_idx", "k_out", "v_out"):
         assert np.array_equal(run.host[name], ref.host[name]), name
     _all(run)
+
+
+def _shape_workload(h_q, h_kv, d, n_seq, n_layers, lens, budget=16):
+    return workloads.Workload(
+        f"bf16_hq{h_q}_hkv{h_kv}_d{d}_W32", 1, workloads.BF16, h_q, h_kv, d, 32, budget, n_seq,
+        n_layers, list(lens), workloads.Layout(cluster_density=0.02),
+        workloads.ProfileSpec(workloads.PROFILE_GLOBAL, (float(np.arcsinh(0.3)),)),
+        workloads.ProfileSpec(workloads.PROFILE_GLOBAL, (float(np.arcsinh(-0.8)),)))
+
+
+STREAM_SHAPES = [(8, 8, 64), (16, 8, 128), (8, 2, 64), (16, 8, 64), (8, 8, 128)]
+
+
+@pytest.mark.parametrize("h_q,h_kv,d", STREAM_SHAPES)
+@pytest.mark.parametrize("fused", [True, False])
+def test_stream_shapes_several_segments(h_q, h_kv, d, fused):
+    """bf16, W = 32, every head layout and head size the streaming kernels take (G = 1, 2, 4;
+    d = 64, 128), units of 3000 and 2100 keys in several segments: both passes in one launch
+    (fused) or as the two entry points."""
+    wl = _shape_workload(h_q, h_kv, d, 2, 2, [3000, 2100])
+    _all(gpu_cases.run_gpu(wl, fused=fused))
+
+
+@pytest.mark.parametrize("h_q,h_kv,d", STREAM_SHAPES)
+def test_stream_shapes_one_segment_per_unit(h_q, h_kv, d):
+    """The same layouts with 256 units of at most 1024 keys: each unit is one segment, so both
+    passes of a unit run in one workgroup."""
+    n_prob = 256 // h_kv
+    wl = _shape_workload(h_q, h_kv, d, 2, n_prob // 2, [1024, 777])
+    assert _one_segment_per_unit(wl)
+    _all(gpu_cases.run_gpu(wl, fused=True))
