@@ -308,3 +308,28 @@ def test_stream_shapes_one_segment_per_unit(h_q, h_kv, d):
     wl = _shape_workload(h_q, h_kv, d, 2, n_prob // 2, [1024, 777])
     assert _one_segment_per_unit(wl)
     _all(gpu_cases.run_gpu(wl, fused=True))
+
+
+def test_segments_merged_by_the_second_launch():
+    """192 units of 5000 keys in two segments each: 384 workgroups do not fit the chip at once, so
+    the fused entry point takes two launches, the second merging the first's segment partials
+    from the workspace."""
+    wl = _shape_workload(32, 8, 128, 3, 8, [5000, 5000, 5000], budget=32)
+    total = int(wl.lens.sum()) * wl.h_kv
+    seg = min(max(1024, -(-(-(-total // 256)) // 256) * 256), -(-int(wl.lens.max()) // 256) * 256)
+    n_seg = -(-int(wl.lens.max()) // seg)
+    assert n_seg == 2 and n_seg * wl.n_prob * wl.h_kv > 256
+    _all(gpu_cases.run_gpu(wl, fused=True))
+
+
+@pytest.mark.parametrize("h_q,h_kv,d", STREAM_SHAPES)
+def test_stream_shapes_late_segments_computed_by_the_waiting_workgroup(h_q, h_kv, d, monkeypatch):
+    """Every head layout and head size with a poll limit of 0: each workgroup computes the other
+    segments' partials itself; the results are bit-identical to the default path's."""
+    wl = _shape_workload(h_q, h_kv, d, 2, 2, [3000, 2100])
+    monkeypatch.delenv("KVEVICT_SPIN_LIMIT", raising=False)
+    ref = gpu_cases.run_gpu(wl, fused=True)
+    monkeypatch.setenv("KVEVICT_SPIN_LIMIT", "0")
+    run = gpu_cases.run_gpu(wl, fused=True)
+    for name in ("row_max", "row_sum", "mu", "sigma", "sel_idx", "k_out", "v_out"):
+        assert np.array_equal(run.host[name], ref.host[name]), name
