@@ -218,6 +218,16 @@ int kv_mmr_select_ex(const kv_problem* pr, const float* mu, const float* sigma, 
 int kv_compact_cache(const kv_problem* pr, const void* k, const void* v, const int32_t* sel_idx,
                      int32_t budget, int32_t keep_tail, void* k_out, void* v_out, void* stream);
 
+/* kv_mmr_select (default scoring, no optional outputs) followed by kv_compact_cache, in one launch
+ * (section 3.2, Eq. (2), (4), (5); sections 1 and 3.1): sel_idx [n_prob][h_kv][budget] as from
+ * kv_mmr_select, k_out / v_out [n_prob][h_kv][budget + keep_tail][d] as from kv_compact_cache
+ * with the same sel_idx; budget <= 8192.  k, v, k_out, v_out 16-byte aligned.  The workspace
+ * (ws, ws_bytes) is that of kv_mmr_select.  Returns the codes of both calls. */
+int kv_mmr_select_compact(const kv_problem* pr, const float* mu, const float* sigma, const void* k,
+                          const void* v, const float* lambda1, const float* lambda2,
+                          int32_t budget, int32_t cand_mult, int32_t keep_tail, int32_t* sel_idx,
+                          void* k_out, void* v_out, void* ws, size_t ws_bytes, void* stream);
+
 /* kv_compact_cache with per-problem budgets and a chosen block size (budget_host / budget_dev as
  * in kv_select_opts; both NULL with out_rows = 0 is exactly kv_compact_cache).  The block of every
  * (problem, kv head) in k_out / v_out has out_rows rows (0: budget + keep_tail; otherwise at least

@@ -39,9 +39,9 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvevict.
 
 SYMBOLS = ("kv_strerror", "kv_version", "kv_workspace_bytes", "kv_candidate_stride",
            "kv_window_scores", "kv_mu_sigma", "kv_mu_sigma_ex", "kv_window_mu_sigma",
-           "kv_window_mu_sigma_ex", "kv_mmr_select", "kv_mmr_select_ex", "kv_compact_cache",
-           "kv_compact_cache_ex", "kv_decode_workspace_bytes", "kv_decode_attention",
-           "kv_pyramid_budgets", "kv_depth_profile")
+           "kv_window_mu_sigma_ex", "kv_mmr_select", "kv_mmr_select_ex", "kv_mmr_select_compact",
+           "kv_compact_cache", "kv_compact_cache_ex", "kv_decode_workspace_bytes",
+           "kv_decode_attention", "kv_pyramid_budgets", "kv_depth_profile")
 
 
 class KvError(RuntimeError):
@@ -96,6 +96,8 @@ def lib() -> ctypes.CDLL:
                                             sz, vp]
         h.kv_mmr_select.argtypes = [pr, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, sz,
                                     vp]
+        h.kv_mmr_select_compact.argtypes = [pr, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp,
+                                            vp, sz, vp]
         h.kv_mmr_select_ex.argtypes = [pr, vp, vp, vp, vp, vp, i32, i32, i32,
                                        ctypes.POINTER(KvSelectOpts), vp, vp, vp, vp, vp, sz, vp]
         h.kv_compact_cache.argtypes = [pr, vp, vp, vp, i32, i32, vp, vp, vp]
@@ -264,6 +266,16 @@ def mmr_select(batch: Batch, mu, sigma, k, lambda1, lambda2, budget: int, cand_m
                                _ptr(sel_idx), _ptr(sel_score), _ptr(cand_idx), _ptr(cand_corr),
                                _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
                                _stream(stream)), "kv_mmr_select")
+
+
+def mmr_select_compact(batch: Batch, mu, sigma, k, v, lambda1, lambda2, budget: int,
+                       cand_mult: int, keep_tail: int, sel_idx, k_out, v_out, ws=None,
+                       stream=None) -> None:
+    _check(lib().kv_mmr_select_compact(batch.ref(), _ptr(mu), _ptr(sigma), _ptr(k), _ptr(v),
+                                       _ptr(lambda1), _ptr(lambda2), int(budget), int(cand_mult),
+                                       int(keep_tail), _ptr(sel_idx), _ptr(k_out), _ptr(v_out),
+                                       _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+                                       _stream(stream)), "kv_mmr_select_compact")
 
 
 def mmr_select_ex(batch: Batch, mu, sigma, k, lambda1, lambda2, budget: int, cand_mult: int,

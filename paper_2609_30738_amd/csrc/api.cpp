@@ -125,6 +125,58 @@ size_t window_ws_bytes(const kv_problem* pr, const kv::Shape& s) {
   return align_up(b);
 }
 
+// Selection, and with k_out / v_out the compaction of the selected rows, in one launch.
+int mmr_select_impl(const kv_problem* pr, const float* mu, const float* sigma, const void* k,
+                    const void* v, const float* lambda1, const float* lambda2, int32_t budget,
+                    int32_t cand_mult, int32_t keep_tail, const kv_select_opts* opts,
+                    int32_t* sel_idx, float* sel_score, int32_t* cand_idx, float* cand_corr,
+                    void* k_out, void* v_out, void* stream) {
+  kv::Shape s;
+  int st = check_problem(pr, &s);
+  if (st != KV_OK) return st;
+  if (!mu || !sigma || !k || !lambda1 || !lambda2 || !sel_idx) return KV_ERR_NULL;
+  if (!aligned16(k)) return KV_ERR_ARG;
+  if (k_out && (!aligned16(v) || !aligned16(k_out) || !aligned16(v_out))) return KV_ERR_ARG;
+  if (cand_mult < 0) return KV_ERR_ARG;
+  const int32_t pool = opts ? opts->pool : 1;
+  const float w_mu = opts ? opts->w_mu : 1.f;
+  const int32_t* b_host = opts ? opts->budget_host : nullptr;
+  const int32_t* b_dev = opts ? opts->budget_dev : nullptr;
+  if (pool < 1 || pool > kMaxPool || pool % 2 == 0 || !std::isfinite(w_mu)) return KV_ERR_ARG;
+  st = check_budget(pr, budget, keep_tail, b_host != nullptr || b_dev != nullptr);
+  if (st != KV_OK) return st;
+  st = check_budgets(pr, budget, keep_tail, b_host, b_dev);
+  if (st != KV_OK) return st;
+  if (k_out && budget > kMaxCompactBudget) return KV_ERR_BUDGET;
+  const int max_cand = max_candidates(pr, budget, cand_mult, keep_tail, b_host);
+  if (max_cand > kv::select_max_candidates(pr->d, elem_bytes(pr->dtype))) return KV_ERR_SHAPE;
+  kv::SelectArgs a;
+  a.mu = mu;
+  a.sigma = sigma;
+  a.k = k;
+  a.lambda1 = lambda1;
+  a.lambda2 = lambda2;
+  a.pool = pool;
+  a.w_mu = w_mu;
+  a.budget = budget;
+  a.budgets = b_dev;
+  a.cand_mult = cand_mult;
+  a.keep_tail = keep_tail;
+  a.cand_stride = kv_candidate_stride(pr, budget, cand_mult, keep_tail);
+  a.max_cand = max_cand;
+  a.max_cand_all = max_candidates(pr, budget, 0, keep_tail);
+  a.sel_idx = sel_idx;
+  a.sel_score = sel_score;
+  a.cand_idx = cand_idx;
+  a.cand_corr = cand_corr;
+  a.v = v;
+  a.k_out = k_out;
+  a.v_out = v_out;
+  a.out_rows = budget + keep_tail;
+  if ((cand_idx || cand_corr) && a.cand_stride < 1) return KV_ERR_ARG;
+  return launch_status(kv::launch_mmr_select(s, a, static_cast<hipStream_t>(stream)));
+}
+
 }  // namespace
 
 extern "C" {
@@ -278,46 +330,21 @@ int kv_mmr_select_ex(const kv_problem* pr, const float* mu, const float* sigma, 
                      int32_t keep_tail, const kv_select_opts* opts, int32_t* sel_idx,
                      float* sel_score, int32_t* cand_idx, float* cand_corr, void* ws,
                      size_t ws_bytes, void* stream) {
-  kv::Shape s;
-  int st = check_problem(pr, &s);
-  if (st != KV_OK) return st;
-  if (!mu || !sigma || !k || !lambda1 || !lambda2 || !sel_idx) return KV_ERR_NULL;
-  if (!aligned16(k)) return KV_ERR_ARG;
-  if (cand_mult < 0) return KV_ERR_ARG;
-  const int32_t pool = opts ? opts->pool : 1;
-  const float w_mu = opts ? opts->w_mu : 1.f;
-  const int32_t* b_host = opts ? opts->budget_host : nullptr;
-  const int32_t* b_dev = opts ? opts->budget_dev : nullptr;
-  if (pool < 1 || pool > kMaxPool || pool % 2 == 0 || !std::isfinite(w_mu)) return KV_ERR_ARG;
-  st = check_budget(pr, budget, keep_tail, b_host != nullptr || b_dev != nullptr);
-  if (st != KV_OK) return st;
-  st = check_budgets(pr, budget, keep_tail, b_host, b_dev);
-  if (st != KV_OK) return st;
   (void)ws;
   (void)ws_bytes;
-  const int max_cand = max_candidates(pr, budget, cand_mult, keep_tail, b_host);
-  if (max_cand > kv::select_max_candidates(pr->d, elem_bytes(pr->dtype))) return KV_ERR_SHAPE;
-  kv::SelectArgs a;
-  a.mu = mu;
-  a.sigma = sigma;
-  a.k = k;
-  a.lambda1 = lambda1;
-  a.lambda2 = lambda2;
-  a.pool = pool;
-  a.w_mu = w_mu;
-  a.budget = budget;
-  a.budgets = b_dev;
-  a.cand_mult = cand_mult;
-  a.keep_tail = keep_tail;
-  a.cand_stride = kv_candidate_stride(pr, budget, cand_mult, keep_tail);
-  a.max_cand = max_cand;
-  a.max_cand_all = max_candidates(pr, budget, 0, keep_tail);
-  a.sel_idx = sel_idx;
-  a.sel_score = sel_score;
-  a.cand_idx = cand_idx;
-  a.cand_corr = cand_corr;
-  if ((cand_idx || cand_corr) && a.cand_stride < 1) return KV_ERR_ARG;
-  return launch_status(kv::launch_mmr_select(s, a, static_cast<hipStream_t>(stream)));
+  return mmr_select_impl(pr, mu, sigma, k, nullptr, lambda1, lambda2, budget, cand_mult, keep_tail,
+                         opts, sel_idx, sel_score, cand_idx, cand_corr, nullptr, nullptr, stream);
+}
+
+int kv_mmr_select_compact(const kv_problem* pr, const float* mu, const float* sigma, const void* k,
+                          const void* v, const float* lambda1, const float* lambda2,
+                          int32_t budget, int32_t cand_mult, int32_t keep_tail, int32_t* sel_idx,
+                          void* k_out, void* v_out, void* ws, size_t ws_bytes, void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  if (!v || !k_out || !v_out) return KV_ERR_NULL;
+  return mmr_select_impl(pr, mu, sigma, k, v, lambda1, lambda2, budget, cand_mult, keep_tail,
+                         nullptr, sel_idx, nullptr, nullptr, nullptr, k_out, v_out, stream);
 }
 
 int kv_compact_cache(const kv_problem* pr, const void* k, const void* v, const int32_t* sel_idx,

@@ -3,11 +3,12 @@
 // One workgroup per (problem, kv head): the B_p admitted positions (B_p = the problem's own budget,
 // or the uniform B) are sorted in LDS (bitonic sort over the next power of two, padded with
 // INT_MAX), then the kept rows of K and V are copied with 16-byte vector loads and stores into rows
-// 0 .. B_p + keep_tail - 1 of the unit's block of out_rows rows.  Rows are opaque bytes, so the
-// copy is exact for every dtype.
+// 0 .. B_p + keep_tail - 1 of the unit's block of out_rows rows (compact_rows.h).  Rows are opaque
+// bytes, so the copy is exact for every dtype.
 #include <limits.h>
 
 #include "common.h"
+#include "compact_rows.h"
 #include "kernels.h"
 
 namespace kv {
@@ -31,33 +32,10 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(
   const int32_t* sel = sel_idx + ((size_t)p * h_kv + g) * budget;
   for (int i = threadIdx.x; i < n2; i += kThreads) srt[i] = i < bp ? sel[i] : INT_MAX;
   __syncthreads();
-  for (int size = 2; size <= n2; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = threadIdx.x; i < n2; i += kThreads) {
-        const int j = i ^ stride;
-        if (j > i) {
-          const bool up = (i & size) == 0;
-          const int a = srt[i], b = srt[j];
-          if ((a > b) == up) {
-            srt[i] = b;
-            srt[j] = a;
-          }
-        }
-      }
-      __syncthreads();
-    }
-  }
-  const int rows = bp + keep_tail;
-  const size_t src_base = ((size_t)tok_off[p] * h_kv + (size_t)g * L) * row_vecs;
-  const size_t dst_base = ((size_t)p * h_kv + g) * out_rows * row_vecs;
-  for (int e = threadIdx.x; e < rows * row_vecs; e += kThreads) {
-    const int r = e / row_vecs, c = e % row_vecs;
-    const int pos = r < bp ? srt[r] : L - keep_tail + (r - bp);
-    if (pos < 0 || pos >= L) continue;  // invalid selection: leave the row unwritten
-    const size_t s = src_base + (size_t)pos * row_vecs + c;
-    k_out[dst_base + e] = k[s];
-    v_out[dst_base + e] = v[s];
-  }
+  sort_positions(srt, n2, threadIdx.x, kThreads);
+  copy_kept_rows(k, v, srt, bp, keep_tail, L, row_vecs,
+                 ((size_t)tok_off[p] * h_kv + (size_t)g * L) * row_vecs,
+                 ((size_t)p * h_kv + g) * out_rows * row_vecs, k_out, v_out, threadIdx.x, kThreads);
 }
 
 hipError_t launch_compact(const Shape& s, const void* k, const void* v, const int32_t* sel_idx,

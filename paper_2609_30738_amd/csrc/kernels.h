@@ -95,6 +95,12 @@ struct SelectArgs {
   float* sel_score;
   int32_t* cand_idx;
   float* cand_corr;
+  // optional compaction after the selection (k_out == nullptr: none): K, V rows of the admitted
+  // positions in position order, then the last keep_tail rows, into blocks of out_rows rows
+  const void* v = nullptr;
+  void* k_out = nullptr;
+  void* v_out = nullptr;
+  int out_rows = 0;
 };
 
 // Largest supported candidate count for a head dimension / element size.

@@ -22,6 +22,7 @@
 #include <algorithm>
 
 #include "common.h"
+#include "compact_rows.h"
 #include "kernels.h"
 
 namespace kv {
@@ -195,6 +196,15 @@ template <int NW> struct SelectShared {
   int sel_need;
 };
 
+// Compaction after the selection (k_out == nullptr: none); K, V, outputs as 16-byte vectors.
+struct CompactOut {
+  const uint4* k;
+  const uint4* v;
+  uint4* k_out;
+  uint4* v_out;
+  int out_rows;
+};
+
 }  // namespace
 
 template <int DT, int D, int NT, int CPT, bool STAGED>
@@ -205,7 +215,7 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
     const float* __restrict__ lambda2, int pool_h, float w_mu, int h_kv, int budget,
     const int32_t* __restrict__ budgets, int cand_mult, int keep_tail,
     int cand_stride, int max_cand, int32_t* __restrict__ sel_idx, float* __restrict__ sel_score,
-    int32_t* __restrict__ cand_idx, float* __restrict__ cand_corr) {
+    int32_t* __restrict__ cand_idx, float* __restrict__ cand_corr, CompactOut co) {
   using T = typename Elem<DT>::T;
   constexpr int kThreads = NT, kWaves = NT / 64;
   static_assert(NT >= 256, "one thread per histogram bin");
@@ -578,6 +588,22 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
       if (cand_corr) cand_corr[o + c] = 0.f;
     }
   }
+
+  if (co.k_out) {
+    // the unit's compacted rows: the admitted positions sorted in the key-row region (dead once
+    // the last candidate has read it), then the rows copied as in compact.hip
+    int32_t* srt = reinterpret_cast<int32_t*>(region);
+    int n2 = 1;
+    while (n2 < bp) n2 <<= 1;
+    __syncthreads();
+    for (int i = tid; i < n2; i += kThreads) srt[i] = i < bp ? cpos[trace_slot[i]] : INT_MAX;
+    __syncthreads();
+    sort_positions(srt, n2, tid, kThreads);
+    constexpr int kRowVecs = D * (int)sizeof(T) / 16;
+    copy_kept_rows(co.k, co.v, srt, bp, keep_tail, L, kRowVecs, base * kRowVecs,
+                   ((size_t)p * h_kv + g) * co.out_rows * kRowVecs, co.k_out, co.v_out, tid,
+                   kThreads);
+  }
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -602,7 +628,9 @@ hipError_t select_launch(const Shape& s, const SelectArgs& a, hipStream_t st) {
       a.mu, a.sigma, static_cast<const T*>(a.k), s.lens, s.tok_off, a.lambda1, a.lambda2,
       a.pool / 2, a.w_mu, s.h_kv,
       a.budget, a.budgets, a.cand_mult, a.keep_tail, a.cand_stride, a.max_cand, a.sel_idx, a.sel_score,
-      a.cand_idx, a.cand_corr);
+      a.cand_idx, a.cand_corr,
+      CompactOut{static_cast<const uint4*>(a.k), static_cast<const uint4*>(a.v),
+                 static_cast<uint4*>(a.k_out), static_cast<uint4*>(a.v_out), a.out_rows});
   return hipGetLastError();
 }
 

@@ -285,3 +285,18 @@ def test_depth_profile_errors():
     assert h.kv_depth_profile(_lib.KV_PROFILE_SEGMENTS, p, 3, 2, out) == _lib.KV_ERR_ARG
     assert h.kv_depth_profile(_lib.KV_PROFILE_GLOBAL, None, 1, 32, out) == _lib.KV_ERR_NULL
     assert h.kv_depth_profile(_lib.KV_PROFILE_GLOBAL, p, 1, 0, out) == _lib.KV_ERR_ARG
+
+
+def test_select_compact_checks():
+    """kv_mmr_select_compact validates like kv_mmr_select followed by kv_compact_cache."""
+    lib = _lib.lib()
+    pr = HostProblem(lens=(4096,))
+    p = ctypes.c_void_p(256)
+    args = lambda **kw: [pr.ref(), kw.get("mu", p), p, kw.get("k", p), kw.get("v", p), p, p,
+                         kw.get("budget", 64), 4, 32, p, kw.get("k_out", p), kw.get("v_out", p),
+                         None, 0, None]
+    assert lib.kv_mmr_select_compact(*args(v=None)) == _lib.KV_ERR_NULL
+    assert lib.kv_mmr_select_compact(*args(k_out=None)) == _lib.KV_ERR_NULL
+    assert lib.kv_mmr_select_compact(*args(mu=None)) == _lib.KV_ERR_NULL
+    assert lib.kv_mmr_select_compact(*args(v=ctypes.c_void_p(258))) == _lib.KV_ERR_ARG
+    assert lib.kv_mmr_select_compact(*args(budget=0)) == _lib.KV_ERR_BUDGET

@@ -333,3 +333,44 @@ def test_stream_shapes_late_segments_computed_by_the_waiting_workgroup(h_q, h_kv
     run = gpu_cases.run_gpu(wl, fused=True)
     for name in ("row_max", "row_sum", "mu", "sigma", "sel_idx", "k_out", "v_out"):
         assert np.array_equal(run.host[name], ref.host[name]), name
+
+
+@pytest.mark.parametrize("case", ["mistral_layer", "pass_8k_B128_scaled", "tiny_f32", "tiny_f32_no_tail"])
+def test_select_and_compact_in_one_launch(case):
+    """kv_mmr_select_compact: the admission sequence and the compacted rows are bit-identical to
+    kv_mmr_select followed by kv_compact_cache on the same scores (256 and 512 candidates in
+    bf16, fp32 keys with and without the kept tail)."""
+    import torch
+    from paper_2609_30738_amd import _lib, api
+    tail = None
+    if case == "mistral_layer":
+        wl = workloads.mistral_layer()
+    elif case == "pass_8k_B128_scaled":
+        wl = workloads.mistral_pass_8k(budget=128, n_layers=3, L=4096)
+    else:
+        wl = workloads.tiny_f32()
+        tail = 0 if case == "tiny_f32_no_tail" else None
+    keep = wl.w if tail is None else tail
+    print(f"[gpu case] select+compact {case}", flush=True)
+    packed = workloads.draw_packed(wl)
+    import bench
+    lam1, lam2 = bench.lambdas(wl)
+    inp = api.upload(wl.dtype, wl.h_q, wl.h_kv, wl.d, wl.w, packed.q_win, packed.k, packed.v,
+                     packed.lens, packed.tok_off, lam1, lam2)
+    out = api.allocate(inp, wl.budget, 4, keep)
+    b = inp.batch
+    _lib.window_mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
+                         out.sigma, out.ws)
+    _lib.mmr_select(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2, wl.budget, 4, keep,
+                    out.sel_idx, None, None, None, out.ws)
+    _lib.compact_cache(b, inp.k, inp.v, out.sel_idx, wl.budget, keep, out.k_out, out.v_out)
+    sel2, k2, v2 = (torch.full_like(out.sel_idx, -7), torch.zeros_like(out.k_out),
+                    torch.zeros_like(out.v_out))
+    _lib.mmr_select_compact(b, out.mu, out.sigma, inp.k, inp.v, inp.lambda1, inp.lambda2,
+                            wl.budget, 4, keep, sel2, k2, v2, out.ws)
+    torch.cuda.synchronize()
+    assert torch.equal(sel2, out.sel_idx)
+    assert torch.equal(k2.view(torch.int16 if k2.element_size() == 2 else torch.int32),
+                       out.k_out.view(torch.int16 if k2.element_size() == 2 else torch.int32))
+    assert torch.equal(v2.view(torch.int16 if v2.element_size() == 2 else torch.int32),
+                       out.v_out.view(torch.int16 if v2.element_size() == 2 else torch.int32))
