@@ -92,10 +92,11 @@ const char* kv_strerror(int status);
 /* ABI version, currently 1. */
 int kv_version(void);
 
-/* Bytes of device workspace the calls below need for this batch (kv_window_scores,
- * kv_window_mu_sigma and kv_mmr_select; kv_mu_sigma and kv_compact_cache need none).  Returns 0
- * for invalid arguments.  The workspace must be 256-byte aligned; its contents need no
- * initialisation and are not preserved between calls. */
+/* Bytes of device workspace the calls below need for this batch (kv_window_scores and
+ * kv_window_mu_sigma; kv_mmr_select, kv_mmr_select_ex and kv_mmr_select_compact take a workspace
+ * argument but stage everything in on-chip memory, and kv_mu_sigma and kv_compact_cache need
+ * none).  Returns 0 for invalid arguments.  The workspace must be 256-byte aligned; its contents
+ * need no initialisation and are not preserved between calls. */
 size_t kv_workspace_bytes(const kv_problem* pr, int32_t budget, int32_t cand_mult,
                           int32_t keep_tail);
 
