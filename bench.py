@@ -473,6 +473,7 @@ def main() -> None:
         "pass_frac_of_hbm_peak": round(ab["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "breakdown_ms": {n: round(float(v), 4) for n, v in zip(names, mean_part)},
         "step_ms_min_max": [round(float(step_ms.min()), 4), round(float(step_ms.max()), 4)],
+        "step_ms_median": round(float(np.median(step_ms)), 4),
         "wall_s_timed_loop": round(wall, 3),
         "cache_flush": f"{args.flush} of 512 MiB before every timed step",
         "per_layer_schedule_ms": {"total": round(lay_score + lay_rest, 4),
