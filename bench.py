@@ -233,7 +233,8 @@ def main() -> None:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=20,
+                    help="untimed steps first: the step time settles over the first 10-20 passes")
     ap.add_argument("--workload", default=WORKLOADS[0], choices=WORKLOADS)
     ap.add_argument("--cpu-layers", type=int, default=20,
                     help="layers of the oracle sample for the CPU baseline (0: skip)")
@@ -474,6 +475,7 @@ def main() -> None:
         "breakdown_ms": {n: round(float(v), 4) for n, v in zip(names, mean_part)},
         "step_ms_min_max": [round(float(step_ms.min()), 4), round(float(step_ms.max()), 4)],
         "step_ms_median": round(float(np.median(step_ms)), 4),
+        "step_ms_each": [round(float(x), 4) for x in step_ms],
         "wall_s_timed_loop": round(wall, 3),
         "cache_flush": f"{args.flush} of 512 MiB before every timed step",
         "per_layer_schedule_ms": {"total": round(lay_score + lay_rest, 4),
