@@ -173,6 +173,8 @@ class GreedyTrace:
     runner_up: List[Optional[int]]
     runner_up_score: List[float]
     corr: dict                   # final corr(i, S) over the candidates (fp32), by position
+    best_corr: List[float] = dataclasses.field(default_factory=list)       # corr of the winner
+    runner_up_corr: List[float] = dataclasses.field(default_factory=list)  # and of the runner-up
 
 
 def greedy_mmr(s_tilde: np.ndarray, k_unit: np.ndarray, cand: List[int], lam2: float,
@@ -208,6 +210,8 @@ def greedy_mmr(s_tilde: np.ndarray, k_unit: np.ndarray, cand: List[int], lam2: f
         trace.score.append(best_v)
         trace.runner_up.append(second)
         trace.runner_up_score.append(second_v)
+        trace.best_corr.append(float(corr[best]))
+        trace.runner_up_corr.append(float(corr[second]) if second is not None else 0.0)
         rest = [i for i in cand if i not in taken]
         if rest:
             cos = (k_unit[rest] @ k_unit[best]).astype(np.float32)
@@ -243,6 +247,7 @@ class HeadResult:
     s: np.ndarray          # fp32 base scores over [0, n_cand)
     s_tilde: np.ndarray    # fp32 normalised scores over [0, n_cand)
     boundary_gap: Optional[tuple]  # (s of the last kept candidate, s of the first excluded)
+    boundary_pos: Optional[tuple] = None  # their positions
 
 
 @dataclasses.dataclass
@@ -272,14 +277,15 @@ def select_head(mu_g: np.ndarray, sigma_g: np.ndarray, k_g: np.ndarray, lam1: fl
     s_t = normalised_scores(s, n_cand)
     n_keep = candidate_count(n_cand, budget, cand_mult)
     cand = top_candidates(s, n_cand, n_keep)
-    gap = None
+    gap = pos = None
     if n_keep < n_cand:
         ranked = sorted(range(n_cand), key=lambda i: (-float(s[i]), i))
         gap = (float(s[ranked[n_keep - 1]]), float(s[ranked[n_keep]]))
+        pos = (ranked[n_keep - 1], ranked[n_keep])
     k_unit = np.zeros_like(k_g)
     k_unit[cand] = unit_keys(k_g[cand])
     trace = greedy_mmr(s_t, k_unit, cand, lam2, budget)
-    return HeadResult(cand, trace, s, s_t, gap)
+    return HeadResult(cand, trace, s, s_t, gap, pos)
 
 
 def evict_problem(q_win, k, v, dtype: str, scale: float, lam1: float, lam2: float, budget: int,

@@ -25,7 +25,11 @@ Recipe (per problem = one (sequence, layer), seed ``[config_id, sequence, layer]
     noise;
   * regions are placed at random, non-overlapping offsets in [1, L - W);
   * values are random bf16 numbers (random sign and mantissa, exponent 2^-7..2^2): they are only ever
-    gathered, never used in arithmetic.
+    gathered, never used in arithmetic;
+  * optionally, given positions of given kv heads are re-drawn after planting: their keys are
+    replaced by fresh bulk keys N(0, 1) / sqrt(d) from the seed
+    ``[config_id, sequence, layer, 1000 + kv_head, position, n]`` (n counts earlier re-draws of the
+    same position).  The positions come from the caller; this module only draws.
 
 Decode over compacted caches (draw_decode): queries, keys, values and the new token's key/value
 ~ N(0, 1), a few rows of every block's keys scaled by 4 (dominant rows), scale 1/sqrt(d).
@@ -37,7 +41,7 @@ from __future__ import annotations
 import concurrent.futures
 import dataclasses
 import os
-from typing import List, Optional, Sequence, Tuple
+from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
@@ -69,6 +73,7 @@ class Layout:
     passage_len: int = 128
     passage_alpha: Tuple[float, float] = (0.5, 2.0)
     cluster_density: Optional[float] = None  # if set, n_clusters = floor(density * L / size)
+    noise_rel: float = NOISE_REL  # relative noise of cluster members and passage copies (0: exact)
 
 
 @dataclasses.dataclass
@@ -250,7 +255,7 @@ def _planted_keys(rng, q_group: np.ndarray, scale: float, L: int, w: int, lay: L
             base = c(alphas[ci]) * (u + 2.0 * xi[ci])
             rms = np.linalg.norm(base) / np.sqrt(d)
             m = lay.cluster_size
-            k[starts[ci]:starts[ci] + m] = base + NOISE_REL * rms * rng.standard_normal((m, d))
+            k[starts[ci]:starts[ci] + m] = base + lay.noise_rel * rms * rng.standard_normal((m, d))
     if lay.n_passages:
         alphas = np.linspace(lay.passage_alpha[0], lay.passage_alpha[1], lay.n_passages)
         for pi in range(lay.n_passages):
@@ -261,7 +266,7 @@ def _planted_keys(rng, q_group: np.ndarray, scale: float, L: int, w: int, lay: L
             s0 = starts[n_clusters + 2 * pi]
             s1 = starts[n_clusters + 2 * pi + 1]
             k[s0:s0 + n] = toks
-            k[s1:s1 + n] = toks + NOISE_REL * rms * rng.standard_normal((n, d))
+            k[s1:s1 + n] = toks + lay.noise_rel * rms * rng.standard_normal((n, d))
 
 
 def _random_values(rng: np.random.Generator, shape, out: Optional[np.ndarray] = None) -> np.ndarray:
@@ -289,10 +294,13 @@ class ProblemInputs:
 
 
 def draw_problem(wl: Workload, p: int, k_out: Optional[np.ndarray] = None,
-                 v_out: Optional[np.ndarray] = None) -> ProblemInputs:
+                 v_out: Optional[np.ndarray] = None,
+                 redraw: Optional[Dict[int, Sequence[int]]] = None) -> ProblemInputs:
     """Draw the inputs of problem p (deterministic in (config_id, sequence, layer)).
 
-    k_out / v_out (optional, [h_kv, L, d] in the stored dtype) receive K and V directly."""
+    k_out / v_out (optional, [h_kv, L, d] in the stored dtype) receive K and V directly.  redraw
+    (optional): {kv_head: [position, ...]} keys to replace by fresh bulk keys after planting, in
+    list order (a position listed twice is re-drawn twice)."""
     s, layer = wl.seq_of(p), wl.layer_of(p)
     L = int(wl.seq_lens[s])
     rng = np.random.default_rng([wl.config_id, s, layer])
@@ -309,6 +317,16 @@ def draw_problem(wl: Workload, p: int, k_out: Optional[np.ndarray] = None,
     for g in range(h_kv):
         qg = q[g * g_sz:(g + 1) * g_sz].reshape(-1, d).astype(np.float64)
         _planted_keys(rng, qg, wl.scale, L, w, lay, n_clusters, k[g])
+    for g, positions in (redraw or {}).items():
+        count: Dict[int, int] = {}
+        for pos in positions:
+            pos = int(pos)
+            if not 0 <= pos < L:
+                raise ValueError(f"re-drawn position {pos} outside [0, {L})")
+            n = count.get(pos, 0)
+            count[pos] = n + 1
+            r2 = np.random.default_rng([wl.config_id, s, layer, 1000 + int(g), pos, n])
+            k[int(g), pos] = r2.standard_normal(d, dtype=np.float32) / np.float32(np.sqrt(d))
     if wl.dtype == F32:
         v = rng.standard_normal((h_kv, L, d), dtype=np.float32)
         if k_out is not None:
@@ -334,9 +352,11 @@ class PackedInputs:
 
 
 def draw_packed(wl: Workload, problems: Optional[Sequence[int]] = None,
-                threads: Optional[int] = None) -> PackedInputs:
+                threads: Optional[int] = None,
+                redraw: Optional[Dict[int, Dict[int, Sequence[int]]]] = None) -> PackedInputs:
     """Draw and pack the given problems (default: all) of a workload (problems are independent
-    and drawn in parallel threads; the result does not depend on the thread count)."""
+    and drawn in parallel threads; the result does not depend on the thread count).  redraw:
+    {problem: {kv_head: [position, ...]}}, see draw_problem."""
     probs = list(range(wl.n_prob)) if problems is None else list(problems)
     lens = np.asarray([wl.seq_lens[wl.seq_of(p)] for p in probs], dtype=np.int32)
     off = np.zeros(len(probs), dtype=np.int64)
@@ -353,7 +373,7 @@ def draw_packed(wl: Workload, problems: Optional[Sequence[int]] = None,
         base = int(off[j]) * wl.h_kv * wl.d
         shape = (wl.h_kv, int(lens[j]), wl.d)
         pi = draw_problem(wl, probs[j], k[base:base + n].reshape(shape),
-                          v[base:base + n].reshape(shape))
+                          v[base:base + n].reshape(shape), (redraw or {}).get(probs[j]))
         q[j] = pi.q_win
 
     workers = max(1, min(len(probs), threads if threads else min(16, os.cpu_count() or 1)))

@@ -1,12 +1,22 @@
 """Comparison of GPU results with the CPU oracle.
 
-Statistics (row max/sum, attention, mu, sigma, corr) are compared element by element within the
-fp32 tolerances below.  Selections are integer results decided by fp32 arithmetic: where the
-oracle's decision has a clear margin over its runner-up the GPU must make the same decision; at a
-near-tie (margin within the fp32 error of the scores) several answers are correct, so the GPU's
-choice and every later step are checked for validity instead: each admitted position must be an
-(approximate) argmax of s~ + lambda2 corr given the positions admitted before it, recomputed by
-the oracle's own functions.
+Statistics (row max/sum, attention, mu, sigma) are compared element by element within the fp32
+tolerances below; every candidate's corr and every step's score are compared with the oracle's
+values for the same admission history.
+
+Selections are integer results decided by fp32 arithmetic (R23).  Per kv head:
+  * the candidate set (top C of s, section 3.2): identical to the oracle's where the oracle's margin
+    at the cut is certified (tests/certify.py); otherwise (a cut through the flat bulk of the
+    scores) the sets may differ only by tokens whose base scores lie within the fp32 error of the
+    cut value, which is checked;
+  * the greedy admissions (Eq. (5)): the oracle's greedy is run on the GPU's candidate set (the
+    oracle's own trace when the sets are equal) and its margins certified; a certified greedy
+    must be reproduced exactly, in admission order (with lambda2 = 0, where only the set is
+    decided, the set exactly and the order step by step within the score tolerance).  An
+    uncertified greedy is replayed: each admitted position must be an argmax of s~ + lambda2 corr
+    within the score tolerance, given the GPU's own earlier admissions;
+  * sel_score and cand_corr are compared with the oracle's values for the GPU's own admission
+    sequence, and the compacted rows with the rows at the GPU's own selection, byte for byte.
 """
 from __future__ import annotations
 
@@ -16,32 +26,54 @@ from typing import List, Optional, Sequence
 import numpy as np
 
 from oracle import evict
+from tests import certify
 
-# fp32 error model of the GPU path: statistics within 1e-5 relative (sigma with a floor of
-# 1e-6 mu, since sigma is formed from values of size mu), cosines within 2e-6 absolute, and the
-# scores built from them within the sum of their parts.
+# fp32 error model of the GPU path (the comparator of the scope table: 1e-5 relative in fp32):
+# mu to 1e-5 relative; sigma to 1e-5 relative plus 1e-6 mu, since sigma is formed from values of
+# size mu and fp32 rounding of those values alone moves sigma by ~1e-6 mu; corr to 1e-5 relative
+# plus 1e-6 absolute.  A per-step score s~ + lambda2 corr is a sum of two terms with their own
+# errors: s~ = s / max s is a ratio of two base scores, each within 1e-5 of its value, hence within
+# 2e-5 |s~|, and lambda2 corr within |lambda2| (1e-5 |corr| + 1e-6); the bound is taken on the terms
+# (the score itself can be far smaller than either where they cancel), plus 1e-6 for its rounding.
 MU_RTOL = 1e-5
 SIGMA_RTOL = 1e-5
 SIGMA_MU_FLOOR = 1e-6
 STAT_ATOL_FRAC = 1e-12   # of the largest mean in the head
-CORR_ATOL = 2e-6
-SCORE_RTOL = 2e-5        # relative error of s~ (mu and sigma to 1e-5, plus the normaliser)
-SCORE_PER_LAMBDA = 2 * CORR_ATOL  # error of lambda2 * corr per unit |lambda2|
-BOUNDARY_RTOL = 2e-5     # relative error of a base score
+CORR_RTOL = 1e-5
+CORR_ATOL = 1e-6
+SCORE_RTOL = 2e-5        # of |s~|
+SCORE_ATOL = 1e-6
+BOUNDARY_RTOL = 2e-5     # relative error of a base score at a cut through the bulk
+# replay of an uncertified greedy: two candidates' scores may swap within the sum of their errors
+PAIR_RTOL = 2e-5
+PAIR_PER_LAMBDA = 4e-6
 
 
 def pair_tol(st_a: float, st_b: float, lam2: float) -> float:
     """How far apart the fp32 scores s~ + lambda2 corr of two candidates may be and still swap."""
-    return SCORE_RTOL * (abs(st_a) + abs(st_b)) + SCORE_PER_LAMBDA * abs(lam2)
+    return PAIR_RTOL * (abs(st_a) + abs(st_b)) + PAIR_PER_LAMBDA * abs(lam2)
 
 
-def score_tol(st: float, lam2: float) -> float:
-    """Error bound of one candidate's score."""
-    return SCORE_RTOL * abs(st) + 0.5 * SCORE_PER_LAMBDA * abs(lam2)
+@dataclasses.dataclass
+class ErrStats:
+    """Largest observed errors: mu and sigma relative (sigma where sigma > 1e-3 mu), corr
+    absolute, per-step score as a fraction of its tolerance."""
+    mu_rel: float = 0.0
+    sigma_rel: float = 0.0
+    corr_abs: float = 0.0
+    score_tol_frac: float = 0.0
+
+    def merge(self, o: "ErrStats") -> None:
+        for f in dataclasses.fields(self):
+            setattr(self, f.name, max(getattr(self, f.name), getattr(o, f.name)))
+
+    def text(self) -> str:
+        return (f"max-err mu={self.mu_rel:.2g}rel sigma={self.sigma_rel:.2g}rel "
+                f"corr={self.corr_abs:.2g}abs score={self.score_tol_frac:.2g}xtol")
 
 
 def assert_mu_sigma(mu: np.ndarray, sigma: np.ndarray, ref_mu: np.ndarray, ref_sigma: np.ndarray,
-                    where: str) -> None:
+                    where: str, err: Optional[ErrStats] = None) -> None:
     floor = STAT_ATOL_FRAC * float(ref_mu.max())
     mu_err = np.abs(mu - ref_mu)
     bad = mu_err > MU_RTOL * np.abs(ref_mu) + floor
@@ -51,6 +83,13 @@ def assert_mu_sigma(mu: np.ndarray, sigma: np.ndarray, ref_mu: np.ndarray, ref_s
     bad = sg_err > SIGMA_RTOL * np.abs(ref_sigma) + SIGMA_MU_FLOOR * np.abs(ref_mu) + floor
     assert not bad.any(), (f"{where}: sigma mismatch at {np.flatnonzero(bad)[:8]} "
                            f"gpu {sigma[bad][:4]} ref {ref_sigma[bad][:4]}")
+    if err is not None:
+        nz = ref_mu > 0
+        if nz.any():
+            err.mu_rel = max(err.mu_rel, float((mu_err[nz] / ref_mu[nz]).max()))
+        nz = ref_sigma > 1e-3 * ref_mu
+        if nz.any():
+            err.sigma_rel = max(err.sigma_rel, float((sg_err[nz] / ref_sigma[nz]).max()))
 
 
 def assert_row_stats(row_max, row_sum, ref_max, ref_sum, where: str) -> None:
@@ -61,29 +100,42 @@ def assert_row_stats(row_max, row_sum, ref_max, ref_sum, where: str) -> None:
 @dataclasses.dataclass
 class SelectionReport:
     steps: int
-    exact_steps: int           # steps identical to the oracle before any divergence
-    near_ties: int             # oracle steps whose margin is within the score tolerance
-    diverged_at: Optional[int]
+    identical_steps: int        # steps identical to the reference trace before any divergence
+    certified: bool             # the oracle certified both the cut and the greedy (stored inputs)
     candidates_equal: bool
-    divergence_margin: Optional[float] = None  # oracle margin at the divergence, relative to s~
+    set_equal: bool             # admitted set identical to the oracle's
+    greedy_certified: bool      # the reference greedy (on the GPU's candidates) is certified
+    boundary: str
+    err: ErrStats = dataclasses.field(default_factory=ErrStats)
 
 
-def _valid_replay(h: evict.HeadResult, k_unit: np.ndarray, cand: Sequence[int], lam2: float,
-                  sel: Sequence[int], start: int, where: str) -> None:
-    """Check sel[start:] step by step against the oracle's scores given sel[:t]."""
+@dataclasses.dataclass
+class Replay:
+    scores: List[float]  # the oracle's fp32 score of each GPU admission, given the GPU's history
+    corr: dict           # each candidate's corr when admitted, else after the last step
+
+
+def replay(h: evict.HeadResult, k_unit: np.ndarray, cand: Sequence[int], lam2: float,
+           sel: Sequence[int], check_from: Optional[int], where: str) -> Replay:
+    """The oracle's scores along the GPU's admission sequence; from step check_from on (None: no
+    check) every admission must be an argmax within the pair tolerance."""
     lam = float(np.float32(lam2))
     cand = np.asarray(sorted(cand))
     pos = {int(c): j for j, c in enumerate(cand)}
     s_t = np.array([h.s_tilde[c] for c in cand], dtype=np.float64)
     corr = np.zeros(len(cand), dtype=np.float32)
     taken = np.zeros(len(cand), dtype=bool)
+    out_scores = []
+    corr_at = {}
     for t, j in enumerate(sel):
         j = int(j)
         assert j in pos, f"{where}: step {t} admitted {j}, not a candidate"
         jj = pos[j]
         assert not taken[jj], f"{where}: step {t} admitted {j} twice"
-        if t >= start:
-            score = (s_t + lam * corr.astype(np.float64)).astype(np.float32).astype(np.float64)
+        score = (s_t + lam * corr.astype(np.float64)).astype(np.float32).astype(np.float64)
+        out_scores.append(float(score[jj]))
+        corr_at[j] = float(corr[jj])
+        if check_from is not None and t >= check_from:
             score[taken] = -np.inf
             bi = int(np.argmax(score))
             tol = pair_tol(s_t[jj], s_t[bi], lam2)
@@ -94,49 +146,93 @@ def _valid_replay(h: evict.HeadResult, k_unit: np.ndarray, cand: Sequence[int], 
         cos = (k_unit[cand] @ k_unit[j]).astype(np.float32)
         upd = ~taken & (cos > corr)
         corr[upd] = cos[upd]
+    for c, j in pos.items():
+        if c not in corr_at:
+            corr_at[c] = float(corr[j])
+    return Replay(out_scores, corr_at)
+
+
+def check_candidates(h: evict.HeadResult, cand: Sequence[int], where: str) -> bool:
+    """GPU candidate positions against the oracle's; returns whether they are equal (a difference is
+    allowed only among near-ties at the cut)."""
+    assert len(cand) == len(h.candidates), f"{where}: candidate count {len(cand)}"
+    if list(cand) == list(h.candidates):
+        return True
+    assert h.boundary_gap is not None, f"{where}: candidate sets differ without a cut"
+    s_c = h.boundary_gap[0]
+    for i in set(cand) ^ set(h.candidates):
+        assert abs(float(h.s[i]) - s_c) <= BOUNDARY_RTOL * abs(s_c), (
+            f"{where}: candidate {i} (s={h.s[i]:.9g}) differs away from the cut {s_c:.9g}")
+    return False
 
 
 def check_selection(h: evict.HeadResult, k_head: np.ndarray, lam2: float, sel: Sequence[int],
-                    cand: Optional[Sequence[int]] = None, where: str = "") -> SelectionReport:
-    """Compare one head's GPU admissions (admission order) with the oracle's HeadResult.
+                    cand: Sequence[int], budget: int, certified: bool, dtype: str,
+                    sel_score: Optional[np.ndarray] = None, cand_corr: Optional[np.ndarray] = None,
+                    where: str = "") -> SelectionReport:
+    """One head's GPU selection against the oracle (see the module docstring).
 
-    k_head: the head's keys in float64 [L, d].  cand: GPU candidate positions (optional).
-    """
+    k_head: the head's stored keys [L, d]; cand: the GPU's candidate positions (ascending);
+    certified: the oracle certified this head's cut and greedy on these inputs, so the GPU must
+    reproduce the oracle exactly.  sel_score / cand_corr (optional): the GPU's outputs for them."""
     sel = [int(x) for x in sel]
-    ora = h.trace.selected
-    margins = [a - b for a, b in zip(h.trace.score, h.trace.runner_up_score)]
-    tols = [pair_tol(h.s_tilde[a], h.s_tilde[b] if b is not None else 0.0, lam2)
-            for a, b in zip(ora, h.trace.runner_up)]
-    near = sum(1 for m, tl in zip(margins, tols) if m <= tl)
-    cand_equal = True
-    use_cand = h.candidates
-    if cand is not None:
-        cand = sorted(int(c) for c in cand if c >= 0)
-        assert len(cand) == len(h.candidates), f"{where}: candidate count {len(cand)}"
-        if cand != h.candidates:
-            cand_equal = False
-            # differences are only allowed among near-tied scores at the top-C boundary
-            assert h.boundary_gap is not None, f"{where}: candidate sets differ without a boundary"
-            s_c = h.boundary_gap[0]
-            diff = set(cand) ^ set(h.candidates)
-            for i in diff:
-                assert abs(float(h.s[i]) - s_c) <= BOUNDARY_RTOL * abs(s_c), (
-                    f"{where}: candidate {i} (s={h.s[i]:.9g}) differs away from the boundary "
-                    f"{s_c:.9g}")
-            use_cand = cand
-    div = next((t for t, (a, b) in enumerate(zip(sel, ora)) if a != b), None)
-    if div is None and cand_equal:
-        assert len(sel) == len(ora)
-        return SelectionReport(len(sel), len(sel), near, None, True)
-    start = 0 if not cand_equal else div
-    rel = None
+    cand = [int(c) for c in cand]
+    cand_equal = check_candidates(h, cand, where)
+    if certified:
+        assert cand_equal, f"{where}: certified head, candidate set differs from the oracle's"
+    kd = evict.decode(k_head, dtype)
+    k_unit = np.zeros_like(kd)
+    k_unit[cand] = evict.unit_keys(kd[cand])
     if cand_equal:
-        assert margins[div] <= tols[div], (
-            f"{where}: step {div} admitted {sel[div]} but the oracle admits {ora[div]} by a margin "
-            f"{margins[div]:.3g} > {tols[div]:.3g}")
-        rel = margins[div] / max(abs(float(h.s_tilde[ora[div]])), 1e-30)
-    k_unit = np.zeros_like(k_head)
-    k_unit[use_cand] = evict.unit_keys(k_head[use_cand])
-    _valid_replay(h, k_unit, use_cand, lam2, sel, start, where)
-    return SelectionReport(len(sel), div if div is not None else len(sel), near, div, cand_equal,
-                           rel)
+        ref = h.trace
+    else:
+        ref = evict.greedy_mmr(h.s_tilde, k_unit, cand, lam2, budget)
+    g_stat, _, _, _ = certify.certify_greedy(h, k_head, lam2, dtype, ref, cand)
+    g_cert = g_stat == "certified"
+    lam0 = float(np.float32(lam2)) == 0.0
+    if certified:
+        assert g_cert, f"{where}: certified head, greedy margins not certified"
+    div = next((t for t, (a, b) in enumerate(zip(sel, ref.selected)) if a != b), None)
+    if g_cert and not lam0:
+        assert div is None and len(sel) == len(ref.selected), (
+            f"{where}: certified greedy, GPU admits {sel[div] if div is not None else sel} at step "
+            f"{div}, oracle {ref.selected[div] if div is not None else ref.selected}")
+    if g_cert and lam0:
+        assert set(sel) == set(ref.selected), f"{where}: certified set differs"
+    check_from = None if (g_cert and not lam0) else 0
+    rp = replay(h, k_unit, cand, lam2, sel, check_from, where)
+    err = ErrStats()
+    if sel_score is not None:
+        ref_sc = np.asarray(rp.scores)
+        d = np.abs(np.asarray(sel_score, dtype=np.float64) - ref_sc)
+        st_sel = np.array([abs(float(h.s_tilde[j])) for j in sel])
+        corr_sel = np.array([abs(rp.corr[j]) for j in sel])
+        lam = abs(float(np.float32(lam2)))
+        tol = SCORE_RTOL * st_sel + lam * (CORR_RTOL * corr_sel + CORR_ATOL) + SCORE_ATOL
+        bad = d > tol
+        assert not bad.any(), (f"{where}: sel_score at steps {np.flatnonzero(bad)[:8]}: "
+                               f"{np.asarray(sel_score)[bad][:4]} vs {ref_sc[bad][:4]}")
+        if d.size:
+            err.score_tol_frac = float((d / tol).max())
+    if cand_corr is not None:
+        ref_c = np.array([rp.corr[c] for c in cand])
+        d = np.abs(np.asarray(cand_corr, dtype=np.float64) - ref_c)
+        bad = d > CORR_RTOL * np.abs(ref_c) + CORR_ATOL
+        assert not bad.any(), (f"{where}: cand_corr at {np.flatnonzero(bad)[:8]}: "
+                               f"{np.asarray(cand_corr)[bad][:4]} vs {ref_c[bad][:4]}")
+        err.corr_abs = float(d.max()) if d.size else 0.0
+    return SelectionReport(len(sel), div if div is not None else len(sel), certified, cand_equal,
+                           set(sel) == set(h.trace.selected), g_cert, "", err)
+
+
+def summarize(reports: List[SelectionReport]) -> str:
+    steps = sum(r.steps for r in reports)
+    ident = sum(r.identical_steps for r in reports)
+    err = ErrStats()
+    for r in reports:
+        err.merge(r.err)
+    return (f"heads={len(reports)} certified-heads={sum(r.certified for r in reports)} "
+            f"identical-candidate-sets={sum(r.candidates_equal for r in reports)} "
+            f"identical-selected-sets={sum(r.set_equal for r in reports)} "
+            f"greedy-certified={sum(r.greedy_certified for r in reports)} "
+            f"steps={steps} identical-to-reference={ident} | {err.text()}")

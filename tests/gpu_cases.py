@@ -1,25 +1,23 @@
 """Shared driver of the GPU parity tests: draw a workload, run it through the C ABI, run the oracle
-on the same inputs (all problems and heads, or a sample), and compare."""
+on the same inputs (every problem and head, or a chosen subset, in parallel processes), and compare.
+"""
 from __future__ import annotations
 
+import concurrent.futures
 import dataclasses
 import sys
 from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
-from oracle import evict, profiles
+from oracle import evict
 from paper_2609_30738_amd import _lib, api, workloads
-from tests import compare
+from tests import certified_cases, certify, compare
 
 
 def layer_lambdas(wl: workloads.Workload, problems: Sequence[int]) -> Tuple[np.ndarray, np.ndarray]:
     """Per-problem fp32 coefficients from the oracle's own profile evaluation."""
-    l1 = profiles.layer_lambdas(wl.lam1.family, wl.lam1.params, wl.n_layers)
-    l2 = profiles.layer_lambdas(wl.lam2.family, wl.lam2.params, wl.n_layers)
-    lam1 = np.array([l1[wl.layer_of(p)] for p in problems], dtype=np.float32)
-    lam2 = np.array([l2[wl.layer_of(p)] for p in problems], dtype=np.float32)
-    return lam1, lam2
+    return certify.layer_lambdas(wl, problems)
 
 
 @dataclasses.dataclass
@@ -30,13 +28,13 @@ class GpuRun:
     lam1: np.ndarray
     lam2: np.ndarray
     budget: int
-    cand_mult: int
+    opts: certify.Options
     keep_tail: int
     host: Dict[str, np.ndarray]
-    pool: int = 1
-    w_mu: float = 1.0
-    sigma_rows: str = "group_mean"
+    redraw: certify.Redraw
+    case: Optional[str] = None  # certified case name (its inputs carry the stored re-draws)
     budgets: Optional[np.ndarray] = None  # per-problem budgets (budget is then the row stride)
+    custom: bool = False  # inputs given by the caller (not reproducible from the seeds)
 
     def budget_of(self, j: int) -> int:
         return self.budget if self.budgets is None else int(self.budgets[j])
@@ -46,16 +44,22 @@ def run_gpu(wl: workloads.Workload, problems: Optional[Sequence[int]] = None, *,
             want_attn: bool = False, cand_mult: int = 4, keep_tail: Optional[int] = None,
             budget: Optional[int] = None, packed: Optional[workloads.PackedInputs] = None,
             pool: int = 1, w_mu: float = 1.0, sigma_rows: str = "group_mean",
-            budgets: Optional[Sequence[int]] = None) -> GpuRun:
+            budgets: Optional[Sequence[int]] = None, redraw: Optional[certify.Redraw] = None,
+            case: Optional[str] = None, timed: bool = False) -> GpuRun:
+    """One pass through the C ABI.  timed=True runs the benchmark's calls (kv_window_mu_sigma, then
+    kv_mmr_select_compact: sel_idx, k_out, v_out) and, on the same mu / sigma, kv_mmr_select with
+    its optional outputs (sel_score, cand_idx, cand_corr, and its own sel_idx as sel_idx_plain)."""
     import torch
     probs = list(range(wl.n_prob)) if problems is None else list(problems)
-    print(f"[gpu case] {wl.name} problems={len(probs)} fused={fused} attn={want_attn} "
-          f"cand_mult={cand_mult} keep_tail={keep_tail} pool={pool} w_mu={w_mu} "
+    print(f"[gpu case] {case or wl.name} problems={len(probs)} fused={fused} timed={timed} "
+          f"attn={want_attn} cand_mult={cand_mult} keep_tail={keep_tail} pool={pool} w_mu={w_mu} "
           f"sigma_rows={sigma_rows} budgets={None if budgets is None else list(budgets)}",
           flush=True)
     sys.stdout.flush()
+    red = redraw or {}
+    custom = packed is not None
     if packed is None:
-        packed = workloads.draw_packed(wl, probs)
+        packed = workloads.draw_packed(wl, probs, redraw=red)
     lam1, lam2 = layer_lambdas(wl, probs)
     B = wl.budget if budget is None else budget
     bud = None
@@ -66,17 +70,43 @@ def run_gpu(wl: workloads.Workload, problems: Optional[Sequence[int]] = None, *,
     inp = api.upload(wl.dtype, wl.h_q, wl.h_kv, wl.d, wl.w, packed.q_win, packed.k, packed.v,
                      packed.lens, packed.tok_off, lam1, lam2)
     out = api.allocate(inp, B, cand_mult, tail, want_candidates=True, want_attn=want_attn)
-    api.run_pass(inp, out, B, cand_mult, tail, fused=fused, pool=pool, w_mu=w_mu,
-                 sigma_rows=sigma_rows,
-                 budgets=None if bud is None else _lib.Budgets(bud, inp.k.device))
+    b = inp.batch
+    extra = {}
+    if timed:
+        _lib.window_mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
+                             out.sigma, out.ws)
+        _lib.mmr_select_compact(b, out.mu, out.sigma, inp.k, inp.v, inp.lambda1, inp.lambda2, B,
+                                cand_mult, tail, out.sel_idx, out.k_out, out.v_out, out.ws)
+        plain = torch.empty_like(out.sel_idx)
+        _lib.mmr_select(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2, B, cand_mult, tail,
+                        plain, out.sel_score, out.cand_idx, out.cand_corr, out.ws)
+        extra["sel_idx_plain"] = plain
+    else:
+        api.run_pass(inp, out, B, cand_mult, tail, fused=fused, pool=pool, w_mu=w_mu,
+                     sigma_rows=sigma_rows,
+                     budgets=None if bud is None else _lib.Budgets(bud, inp.k.device))
     torch.cuda.synchronize()
     host = {name: api.to_host_bits(getattr(out, name)) for name in
             ("row_max", "row_sum", "mu", "sigma", "sel_idx", "sel_score", "cand_idx", "cand_corr",
              "k_out", "v_out")}
+    for name, t in extra.items():
+        host[name] = api.to_host_bits(t)
     if want_attn:
         host["attn"] = api.to_host_bits(out.attn)
-    return GpuRun(wl, probs, packed, lam1, lam2, B, cand_mult, tail, host, pool, w_mu, sigma_rows,
-                  bud)
+    opts = certify.Options(cand_mult=cand_mult, keep_tail=keep_tail, pool=pool, w_mu=w_mu,
+                           sigma_all_rows=sigma_rows == "all_rows",
+                           budgets=None if bud is None else tuple(int(x) for x in bud))
+    return GpuRun(wl, probs, packed, lam1, lam2, B, opts, tail, host, red, case, bud, custom)
+
+
+def run_case(name: str, problems: Optional[Sequence[int]] = None, **kw) -> GpuRun:
+    """A certified case (tests/certified_cases.py) with its stored re-draws and options."""
+    wl = certified_cases.workload(name)
+    o = certified_cases.options(name)
+    red = certified_cases.load_redraw(name)
+    return run_gpu(wl, problems, cand_mult=o.cand_mult, keep_tail=o.keep_tail, pool=o.pool,
+                   w_mu=o.w_mu, sigma_rows="all_rows" if o.sigma_all_rows else "group_mean",
+                   budgets=o.budgets, redraw=red, case=name, **kw)
 
 
 def problem_arrays(run: GpuRun, j: int):
@@ -90,19 +120,46 @@ def problem_arrays(run: GpuRun, j: int):
     return run.packed.q_win[j], k, v
 
 
-def check_problem(run: GpuRun, j: int, heads: Optional[Sequence[int]] = None,
-                  check_compaction: bool = True) -> List[compare.SelectionReport]:
+def _oracle_task(args):
+    wl, p, j, lam1, lam2, opts, red_p, want_attn, arrays = args
+    if arrays is None:
+        pi = workloads.draw_problem(wl, p, redraw=red_p)
+        q, k = pi.q_win, pi.k
+    else:
+        q, k = arrays
+    budget = wl.budget if opts.budgets is None else int(opts.budgets[j])
+    return j, evict.evict_problem(q, k, None, wl.dtype, wl.scale, lam1, lam2, budget,
+                                  opts.cand_mult, opts.keep_tail, want_attn=want_attn,
+                                  pool=opts.pool, w_mu=opts.w_mu,
+                                  sigma_all_rows=opts.sigma_all_rows)
+
+
+def oracle_results(run: GpuRun, js: Sequence[int], workers: Optional[int] = None):
+    """The oracle on problems js of the run (indices into run.problems), in parallel processes that
+    draw their own inputs (the same seeds and re-draws as the run), or are handed the run's arrays
+    when the caller built the inputs.  {j: ProblemResult}."""
+    want_attn = "attn" in run.host
+    args = [(run.wl, run.problems[j], j, float(run.lam1[j]), float(run.lam2[j]), run.opts,
+             run.redraw.get(run.problems[j]), want_attn,
+             problem_arrays(run, j)[:2] if run.custom else None) for j in js]
+    workers = min(workers or certify.default_workers(), len(args))
+    if workers <= 1:
+        return dict(_oracle_task(a) for a in args)
+    with certify._pool(workers) as ex:
+        return dict(ex.map(_oracle_task, args))
+
+
+def check_problem(run: GpuRun, j: int, res: Optional[evict.ProblemResult] = None,
+                  heads: Optional[Sequence[int]] = None) -> List[compare.SelectionReport]:
     """Compare problem j of a GPU run with the oracle; returns the selection reports."""
     wl = run.wl
     q, k, v = problem_arrays(run, j)
     L = int(run.packed.lens[j])
     heads = list(range(wl.h_kv)) if heads is None else list(heads)
-    where = f"{wl.name} p={run.problems[j]}"
+    where = f"{run.case or wl.name} p={run.problems[j]}"
     Bp = run.budget_of(j)
-    res = evict.evict_problem(q, k, None, wl.dtype, wl.scale, float(run.lam1[j]),
-                              float(run.lam2[j]), Bp, run.cand_mult, run.keep_tail,
-                              heads=heads, want_attn="attn" in run.host, pool=run.pool,
-                              w_mu=run.w_mu, sigma_all_rows=run.sigma_rows == "all_rows")
+    if res is None:
+        res = oracle_results(run, [j], workers=1)[j]
     H = run.host
     rows = wl.h_q * wl.w
     compare.assert_row_stats(H["row_max"][j * rows:(j + 1) * rows].reshape(wl.h_q, wl.w),
@@ -111,58 +168,65 @@ def check_problem(run: GpuRun, j: int, heads: Optional[Sequence[int]] = None,
     tok = int(run.packed.tok_off[j])
     mu = H["mu"][tok * wl.h_kv:(tok + L) * wl.h_kv].reshape(wl.h_kv, L)
     sg = H["sigma"][tok * wl.h_kv:(tok + L) * wl.h_kv].reshape(wl.h_kv, L)
+    errs = {}
     for g in heads:
-        compare.assert_mu_sigma(mu[g], sg[g], res.mu[g], res.sigma[g], f"{where} g={g}")
+        errs[g] = compare.ErrStats()
+        compare.assert_mu_sigma(mu[g], sg[g], res.mu[g], res.sigma[g], f"{where} g={g}", errs[g])
     if "attn" in H:
         a = H["attn"][tok * wl.h_q * wl.w:(tok + L) * wl.h_q * wl.w].reshape(wl.h_q, wl.w, L)
         np.testing.assert_allclose(a, res.attn, rtol=1e-5, atol=1e-12, err_msg=f"{where}: attn")
         assert np.all(a[res.attn == 0] == 0), f"{where}: masked attention must be exactly 0"
-    kd = evict.decode(k, wl.dtype)
+    kb = k.view(np.uint16) if wl.dtype == workloads.BF16 else k
     reports = []
     B = run.budget
     stride = H["cand_idx"].size // (len(run.problems) * wl.h_kv)
+    rows_out = Bp + run.keep_tail  # rows written; the block's stride is B + keep_tail
     for g in heads:
-        o = (j * wl.h_kv + g)
+        o = j * wl.h_kv + g
+        hr = res.heads[g]
+        # the oracle's margins on these inputs decide whether the GPU must match it exactly
+        hc = certify.certify_head(hr, kb[g], float(run.lam2[j]), wl.dtype,
+                                  redrawn=certify.HEAD_REDRAW_CAP + 1)
         assert np.all(H["sel_idx"][o * B + Bp:(o + 1) * B] == -1), f"{where} g={g}: padding"
-        assert np.all(H["sel_score"][o * B + Bp:(o + 1) * B] == 0), f"{where} g={g}: padding"
         sel = H["sel_idx"][o * B:o * B + Bp]
         cand = H["cand_idx"][o * stride:(o + 1) * stride]
-        hr = res.heads[g]
-        rep = compare.check_selection(hr, kd[g], float(run.lam2[j]), sel, cand, f"{where} g={g}")
+        live = cand[cand >= 0]
+        assert np.all(cand[len(live):] == -1) and np.all(np.diff(live) > 0), f"{where} g={g}: cand"
+        if "sel_idx_plain" in H:
+            assert np.array_equal(H["sel_idx_plain"][o * B:o * B + Bp], sel), (
+                f"{where} g={g}: kv_mmr_select and kv_mmr_select_compact disagree")
+        else:
+            assert np.all(H["sel_score"][o * B + Bp:(o + 1) * B] == 0), f"{where} g={g}: padding"
+        rep = compare.check_selection(
+            hr, kb[g], float(run.lam2[j]), sel, live, Bp, hc.ok, wl.dtype,
+            sel_score=H["sel_score"][o * B:o * B + Bp],
+            cand_corr=H["cand_corr"][o * stride:o * stride + len(live)], where=f"{where} g={g}")
+        rep.err.merge(errs[g])
+        rep.boundary = hc.boundary
         reports.append(rep)
-        if rep.diverged_at is None and rep.candidates_equal:
-            ss = H["sel_score"][o * B:o * B + Bp]
-            tol = [compare.score_tol(float(hr.s_tilde[i]), float(run.lam2[j])) for i in sel]
-            bad = np.abs(ss - np.asarray(hr.trace.score)) > np.asarray(tol)
-            assert not bad.any(), (f"{where} g={g}: sel_score at steps {np.flatnonzero(bad)[:8]}: "
-                                   f"{ss[bad][:4]} vs {np.asarray(hr.trace.score)[bad][:4]}")
-            corr = H["cand_corr"][o * stride:o * stride + len(hr.candidates)]
-            ref = np.array([float(hr.trace.corr[c]) for c in hr.candidates])
-            np.testing.assert_allclose(corr, ref, rtol=1e-5, atol=compare.CORR_ATOL,
-                                       err_msg=f"{where} g={g}: corr")
-            assert np.all(cand[len(hr.candidates):] == -1)
-        if check_compaction and rep.diverged_at is None and rep.candidates_equal:
-            # same admissions as the oracle: the compacted rows must be the oracle's, byte for byte
-            rows_out = Bp + run.keep_tail  # rows written; the block's stride is B + keep_tail
-            keep = evict.kept_positions(hr.trace.selected, L, run.keep_tail)
-            base = o * (B + run.keep_tail) * wl.d
-            ko = H["k_out"][base:base + rows_out * wl.d].reshape(rows_out, wl.d)
-            vo = H["v_out"][base:base + rows_out * wl.d].reshape(rows_out, wl.d)
-            np.testing.assert_array_equal(ko, evict.compact_rows(k[g], keep),
-                                          err_msg=f"{where} g={g}: compacted K")
-            np.testing.assert_array_equal(vo, evict.compact_rows(v[g], keep),
-                                          err_msg=f"{where} g={g}: compacted V")
+        # the compacted rows are the rows at the GPU's own selection, byte for byte; where the
+        # selected set is the oracle's, they are the oracle's compaction
+        keep = evict.kept_positions([int(x) for x in sel], L, run.keep_tail)
+        base = o * (B + run.keep_tail) * wl.d
+        ko = H["k_out"][base:base + rows_out * wl.d].reshape(rows_out, wl.d)
+        vo = H["v_out"][base:base + rows_out * wl.d].reshape(rows_out, wl.d)
+        np.testing.assert_array_equal(ko, evict.compact_rows(k[g], keep),
+                                      err_msg=f"{where} g={g}: compacted K")
+        np.testing.assert_array_equal(vo, evict.compact_rows(v[g], keep),
+                                      err_msg=f"{where} g={g}: compacted V")
+    return reports
+
+
+def check_all(run: GpuRun, js: Optional[Sequence[int]] = None, heads=None,
+              workers: Optional[int] = None) -> List[compare.SelectionReport]:
+    """Compare problems js (default: all) of a run, the oracle computed in parallel."""
+    js = list(range(len(run.problems))) if js is None else list(js)
+    res = oracle_results(run, js, workers)
+    reports = []
+    for j in js:
+        reports += check_problem(run, j, res[j], heads)
     return reports
 
 
 def summarize(reports: List[compare.SelectionReport]) -> str:
-    steps = sum(r.steps for r in reports)
-    exact = sum(r.exact_steps for r in reports)
-    div = [r for r in reports if r.diverged_at is not None]
-    near = sum(r.near_ties for r in reports)
-    cert = sum(1 for r in reports if r.near_ties == 0)
-    worst = max((r.divergence_margin for r in div if r.divergence_margin is not None),
-                default=None)
-    return (f"heads={len(reports)} fully-certified-heads={cert} steps={steps} "
-            f"identical-to-oracle={exact} near-ties(oracle)={near} diverged-heads={len(div)}"
-            + (f" largest-relative-margin-at-divergence={worst:.2g}" if worst is not None else ""))
+    return compare.summarize(reports)

@@ -12,34 +12,78 @@ from tests import gpu_cases
 pytestmark = pytest.mark.gpu
 
 
-def _all(run, heads=None):
-    reports = []
-    for j in range(len(run.problems)):
-        reports += gpu_cases.check_problem(run, j, heads)
+def _all(run, heads=None, certified=False):
+    """Compare every problem of a run with the oracle; certified=True: every head's inputs are
+    margin-certified, so every head must reproduce the oracle exactly."""
+    reports = gpu_cases.check_all(run, heads=heads)
     print("  ", gpu_cases.summarize(reports), flush=True)
+    if certified:
+        assert all(r.certified for r in reports), gpu_cases.summarize(reports)
+        assert all(r.identical_steps == r.steps for r in reports)
     return reports
 
 
 def test_tiny_f32_unfused_with_attention():
-    """fp32 path, 2 query heads on 1 kv head, d=64, W=8 (general window reduction)."""
-    reports = _all(gpu_cases.run_gpu(workloads.tiny_f32(), want_attn=True))
-    assert all(r.candidates_equal for r in reports)
+    """fp32 path, 2 query heads on 1 kv head, d=64, W=8 (general window reduction); certified."""
+    _all(gpu_cases.run_case("tiny_f32", want_attn=True), certified=True)
 
 
 def test_tiny_f32_fused_exact_greedy_over_all_candidates():
-    """cand_mult = 0: the greedy runs over every prefix position."""
-    _all(gpu_cases.run_gpu(workloads.tiny_f32(), fused=True, cand_mult=0))
+    """cand_mult = 0: the greedy runs over every prefix position; certified."""
+    _all(gpu_cases.run_case("tiny_f32_all_candidates", fused=True), certified=True)
 
 
-@pytest.mark.parametrize("keep_tail", [0, 3])
-def test_tiny_f32_keep_tail(keep_tail):
-    _all(gpu_cases.run_gpu(workloads.tiny_f32(), keep_tail=keep_tail))
+@pytest.mark.parametrize("case", ["tiny_f32_no_tail", "tiny_f32_tail3"])
+def test_tiny_f32_keep_tail(case):
+    _all(gpu_cases.run_case(case), certified=True)
 
 
 def test_mistral_layer_unfused():
-    """One Mistral-7B layer, bf16, L=4096, W=32, B=64, lambda1=0.3, lambda2=-0.8."""
-    reports = _all(gpu_cases.run_gpu(workloads.mistral_layer()))
-    assert sum(r.exact_steps for r in reports) >= 0.9 * sum(r.steps for r in reports)
+    """One Mistral-7B layer, bf16, L=4096, W=32, B=64, lambda1=0.3, lambda2=-0.8; certified inputs,
+    so every admission is the oracle's."""
+    _all(gpu_cases.run_case("mistral_layer"), certified=True)
+
+
+def test_mistral_layer_timed_calls():
+    """The benchmark's calls (kv_window_mu_sigma, kv_mmr_select_compact) on certified inputs."""
+    _all(gpu_cases.run_case("mistral_layer", timed=True), certified=True)
+
+
+def test_exact_duplicate_keys_ties_to_lower_position():
+    """Clusters of bitwise identical keys: exact ties at the candidate cut and in the greedy argmax
+    are decided by the lower position on both sides (R10), through the default and the benchmark
+    calls."""
+    for timed in (False, True):
+        _all(gpu_cases.run_case("exact_duplicates", fused=True, timed=timed), certified=True)
+
+
+def test_nonfinite_inputs_keep_indices_valid():
+    """NaN and Inf planted in keys and in window queries (results unspecified, R21): every call
+    succeeds, and every selection is B distinct candidate positions."""
+    wl = workloads.mistral_layer()
+    wl.seq_lens = [3000]
+    wl.n_seq = 1
+    pk = workloads.draw_packed(wl)
+    L, d, G = 3000, wl.d, wl.h_q // wl.h_kv
+    k = pk.k.reshape(wl.h_kv, L, d)
+    nan, inf, ninf = np.uint16(0x7FC0), np.uint16(0x7F80), np.uint16(0xFF80)
+    k[0, 100] = nan                 # a NaN key row
+    k[1, 200, :5] = inf             # a key with infinite entries
+    k[2, 300:310] = ninf            # ten keys of -inf entries
+    k[3, :, 7] = nan                # a NaN component in every key of a head
+    pk.q_win[0, 5 * G, 3] = nan     # a NaN window query of kv head 5's group
+    pk.q_win[0, 6 * G + 1, :] = inf  # an infinite window query of kv head 6's group
+    for fused in (True, False):
+        run = gpu_cases.run_gpu(wl, fused=fused, packed=pk)
+        for timed in (False, True):
+            if timed:
+                run = gpu_cases.run_gpu(wl, packed=pk, timed=True)
+            B = run.budget
+            sel = run.host["sel_idx"].reshape(wl.h_kv, B)
+            for g in range(wl.h_kv):
+                s = sel[g]
+                assert len(set(s.tolist())) == B, f"g={g}: repeated positions {s}"
+                assert np.all((s >= 0) & (s < L - wl.w)), f"g={g}: out of range {s}"
 
 
 def test_mistral_layer_fused_with_attention_short_context():
@@ -52,21 +96,18 @@ def test_mistral_layer_fused_with_attention_short_context():
 @pytest.mark.parametrize("budget", [32, 64, 128])
 def test_segments_profile_budget_sweep_scaled(budget):
     """Three-segment lambda2 over 3 layers (one per segment), L=2048, B in {32, 64, 128}."""
-    wl = workloads.mistral_pass_8k(budget=budget, n_layers=3, L=2048)
-    _all(gpu_cases.run_gpu(wl, fused=True))
+    _all(gpu_cases.run_case(f"segments_scaled_B{budget}", fused=True))
 
 
 def test_curve_profile_scaled():
-    """Quadratic lambda2 profile with passages repeated twice, 4 layers of L=6000."""
-    wl = workloads.mistral_pass_32k(n_layers=4, L=6000, n_clusters=16, n_passages=4)
-    _all(gpu_cases.run_gpu(wl, fused=True))
+    """Quadratic lambda2 profile with passages repeated twice, 4 layers of L=6000; certified."""
+    _all(gpu_cases.run_case("curve_scaled", fused=True), certified=True)
 
 
 @pytest.mark.parametrize("run", ["dispersion_only", "redundancy_only", "both"])
 def test_ragged_batch_scaled(run):
     """Three sequences of different lengths x 2 layers, B=128, the three term-ablation runs."""
-    wl = workloads.ragged_batch(run, n_seq=3, n_layers=2, len_range=(700, 3100))
-    _all(gpu_cases.run_gpu(wl, fused=True))
+    _all(gpu_cases.run_case(f"ragged_scaled_{run}", fused=True))
 
 
 def _plant_rising_keys(wl, pk, plants):
@@ -134,11 +175,10 @@ def test_max_pooled_scores_fp32_keep_all():
     _all(gpu_cases.run_gpu(workloads.tiny_f32(), fused=True, keep_tail=0, pool=5))
 
 
-@pytest.mark.parametrize("lam_run", ["dispersion_only", "both"])
-def test_mean_free_score(lam_run):
+@pytest.mark.parametrize("case", ["mean_free_dispersion_only", "mean_free"])
+def test_mean_free_score(case):
     """w_mu = 0: the score without the mean term (dispersion and redundancy only)."""
-    wl = workloads.ragged_batch(lam_run, n_seq=2, n_layers=2, len_range=(700, 3100))
-    _all(gpu_cases.run_gpu(wl, fused=True, w_mu=0.0))
+    _all(gpu_cases.run_case(case, fused=True))
 
 
 def test_mean_free_max_pooled_unfused():
@@ -152,19 +192,14 @@ def test_mean_free_max_pooled_unfused():
 def test_dispersion_over_all_group_rows(fused):
     """KV_SIGMA_ALL_ROWS, 4 query heads per kv head: streaming pass 2 (fused) and the generic
     w = 32 kernel with the attention output (unfused), L = 3000."""
-    wl = workloads.mistral_layer()
-    wl.seq_lens = [3000]
-    _all(gpu_cases.run_gpu(wl, fused=fused, want_attn=not fused, sigma_rows="all_rows"))
+    _all(gpu_cases.run_case("sigma_all_rows", fused=fused, want_attn=not fused), certified=True)
 
 
 @pytest.mark.parametrize("sigma_rows", ["group_mean", "all_rows"])
 def test_three_query_heads_per_kv_head(sigma_rows):
     """G = 3 (w = 32): 96 window rows in four 32-row blocks, the last one padding; generic
     kernels, both dispersion readings, L = 2100."""
-    wl = workloads.mistral_layer()
-    wl.h_q, wl.h_kv = 12, 4
-    wl.seq_lens = [2100]
-    _all(gpu_cases.run_gpu(wl, fused=True, sigma_rows=sigma_rows))
+    _all(gpu_cases.run_case(f"g3_{sigma_rows}", fused=True), certified=True)
 
 
 def test_dispersion_over_all_group_rows_general_window():
@@ -177,12 +212,11 @@ def test_depth_decreasing_budgets():
     3), two sequences x 4 layers of L = 3000 and 2200: ragged greedy lengths, candidate counts and
     compacted blocks, padded steps."""
     from oracle import budgets
-    wl = workloads.mistral_pass_8k(n_layers=4, L=3000)
-    wl.n_seq, wl.seq_lens = 2, [3000, 2200]
+    from tests import certified_cases
     sched = budgets.pyramid_budgets(64, 4, 20.0)
     assert sched == [125, 85, 43, 3]
-    per_prob = [sched[wl.layer_of(p)] for p in range(wl.n_prob)]
-    _all(gpu_cases.run_gpu(wl, fused=True, budgets=per_prob))
+    assert certified_cases.options("depth_budgets").budgets == tuple(sched * 2)
+    _all(gpu_cases.run_case("depth_budgets", fused=True))
 
 
 def test_depth_decreasing_budgets_fp32_with_options():

@@ -207,8 +207,8 @@ def test_normalised_scores_bounds_and_ranking():
 
 
 def test_normaliser_clamped_positive():
-    """All base scores non-positive: the denominator is clamped to a positive value (R7), so the
-    order is preserved and nothing divides by zero."""
+    """All base scores non-positive: the normaliser falls back to its positive floor (R7), so the
+    order is preserved and nothing divides by zero (section 3.2, Eq. (5))."""
     s = np.array([-3e-4, -1e-4, 0.0, -2e-4], dtype=np.float32)
     st_ = evict.normalised_scores(s, 4)
     assert np.all(np.isfinite(st_))
@@ -291,8 +291,8 @@ def test_greedy_matches_bruteforce(seed, n, budget, lam2):
 
 
 def test_greedy_zero_lambdas_is_top_b_by_mean():
-    """lambda1 = lambda2 = 0 recovers the baseline ranking: the B tokens with the largest mean
-    attention, admitted in descending order of mu (section 3.2; SnapKV/PyramidKV point)."""
+    """lambda1 = lambda2 = 0 reduces the score to mean attention alone: the B tokens with the
+    largest mu, admitted in descending order of mu (section 3.2, Eq. (5))."""
     rng = np.random.default_rng(17)
     mu = rng.random(300) * 1e-3
     sg = rng.random(300) * 1e-3
