@@ -35,7 +35,9 @@ KV_PROFILE_CURVE = 2
 PROFILE_FAMILIES = {"global": KV_PROFILE_GLOBAL, "segments": KV_PROFILE_SEGMENTS,
                     "curve": KV_PROFILE_CURVE}
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvevict.so")
+# KVEVICT_LIB selects another build of the same library (the host-sanitized one of the CPU tests)
+LIB_PATH = os.environ.get("KVEVICT_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                         "libkvevict.so")
 
 SYMBOLS = ("kv_strerror", "kv_version", "kv_workspace_bytes", "kv_candidate_stride",
            "kv_window_scores", "kv_mu_sigma", "kv_mu_sigma_ex", "kv_window_mu_sigma",

@@ -137,7 +137,8 @@ int mmr_select_impl(const kv_problem* pr, const float* mu, const float* sigma, c
   if (!mu || !sigma || !k || !lambda1 || !lambda2 || !sel_idx) return KV_ERR_NULL;
   if (!aligned16(k)) return KV_ERR_ARG;
   if (k_out && (!aligned16(v) || !aligned16(k_out) || !aligned16(v_out))) return KV_ERR_ARG;
-  if (cand_mult < 0) return KV_ERR_ARG;
+  // the kernels form cand_mult * B_p in 32-bit arithmetic (B_p <= budget)
+  if (cand_mult < 0 || (int64_t)cand_mult * budget > INT32_MAX) return KV_ERR_ARG;
   const int32_t pool = opts ? opts->pool : 1;
   const float w_mu = opts ? opts->w_mu : 1.f;
   const int32_t* b_host = opts ? opts->budget_host : nullptr;

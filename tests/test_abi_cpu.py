@@ -123,6 +123,9 @@ def test_budget_and_candidate_checks():
     assert mmr_select(pr.ref(), keep_tail=-1) == _lib.KV_ERR_ARG
     assert mmr_select(pr.ref(), keep_tail=100) == _lib.KV_ERR_ARG
     assert mmr_select(pr.ref(), cand_mult=-1) == _lib.KV_ERR_ARG
+    # cand_mult * budget beyond 32 bits (e.g. INT32_MAX meant as 'all') is rejected, not wrapped
+    assert mmr_select(pr.ref(), budget=64, cand_mult=2**31 - 1) == _lib.KV_ERR_ARG
+    assert mmr_select(pr.ref(), budget=2, cand_mult=2**30) == _lib.KV_ERR_ARG
     assert mmr_select(pr.ref(), budget=64, cand_mult=0) == _lib.KV_ERR_SHAPE  # 4064 > 512
     assert mmr_select(pr.ref(), budget=64, cand_mult=16) == _lib.KV_ERR_SHAPE  # 1024 > 512
     assert compact(pr.ref(), budget=69) == _lib.KV_ERR_BUDGET
