@@ -11,12 +11,19 @@
 //   2. the candidate set P: every score above the threshold plus the lowest positions among those
 //      equal to it, compacted in ascending position order (ballot ranks inside a wave, LDS prefix
 //      across waves);
-//   3. B greedy steps.  Thread t owns candidates t, t + NT, ...: it keeps their keys in registers,
-//      their normalised score s~, running max-cosine and admitted flag.  Each step updates the
-//      running maxima against the last admitted key (read from an LDS copy of the candidate keys),
-//      forms s~ + lambda2 * corr, and finds the (score, lowest slot) maximum: a DPP / permlane
-//      maximum and a ballot inside each wave, then one barrier; the per-wave winners are
-//      double-buffered so that one barrier per step suffices.
+//   3. B greedy steps, in one of two ways:
+//      - Gram (when the upper triangle of the C x C dot-product matrix of the candidate keys fits in
+//        LDS: C <= 256 for d = 128): the dot products k_i . k_j of every candidate pair are formed
+//        once with MFMA tiles (each wave a 32 x 32 block, operands gathered straight from the key
+//        rows) into the LDS triangle, 1/|k_i| from its diagonal; then ONE wave runs every step,
+//        each lane holding up to four candidates' s~, running max-cosine and admitted flag: a step
+//        reads one triangle entry per candidate against the last admitted slot and takes a DPP /
+//        permlane maximum, with no barrier;
+//      - rows (larger C): thread t owns candidates t, t + NT, ... and keeps their keys in
+//        registers; each step updates the running maxima against the last admitted key (read from
+//        an LDS copy of the candidate keys), forms s~ + lambda2 * corr, and finds the (score,
+//        lowest slot) maximum: a DPP / permlane maximum and a ballot inside each wave, then one
+//        barrier; the per-wave winners are double-buffered so that one barrier per step suffices.
 #include <float.h>
 
 #include <algorithm>
@@ -32,6 +39,13 @@ namespace {
 constexpr int kMaxCandBytes = 131072;        // LDS copy of the candidate keys
 constexpr int kMaxStagedKeyBytes = 139264;  // LDS copy of every candidate's score key (34816)
 constexpr size_t kLdsBytes = 163840;        // LDS of one CU
+constexpr int kGramMaxCand = 256;           // candidates of the Gram greedy (4 per lane of a wave)
+constexpr int kGramSlots = kGramMaxCand / 64;
+
+// Entries of the upper triangle (diagonal included) of a C x C matrix, and the index of (i, j),
+// i <= j, row by row.
+__host__ __device__ constexpr size_t tri_entries(int c) { return (size_t)c * (c + 1) / 2; }
+__device__ __forceinline__ int tri_index(int i, int j, int c) { return (i * (2 * c - i + 1)) / 2 + (j - i); }
 
 __device__ __forceinline__ uint32_t order_key(float x) {
   const uint32_t u = __float_as_uint(x);
@@ -196,6 +210,164 @@ template <int NW> struct SelectShared {
   int sel_need;
 };
 
+// Append the positions of the lanes where `pred` holds to out[] at slots taken from *counter
+// (one LDS atomic per wave); the order of the appended entries is unspecified.
+template <typename F>
+__device__ __forceinline__ void wave_append(bool pred, uint32_t* counter, int lane, F&& write) {
+  const uint64_t m = __ballot(pred);
+  if (m == 0) return;
+  const int leader = __ffsll((unsigned long long)m) - 1;
+  uint32_t base = 0;
+  if (lane == leader) base = atomicAdd(counter, (uint32_t)__popcll(m));
+  base = __builtin_amdgcn_readlane(base, leader);
+  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  if (pred) write(base + (uint32_t)__popcll(m & below));
+}
+
+// Ascending bitonic sort of v[0, n2) (n2 a power of two) by the NT threads; starts and ends with
+// the workgroup synchronised.
+template <typename V>
+__device__ __forceinline__ void bitonic_sort(V* v, int n2, int tid, int nt) {
+  for (int size = 2; size <= n2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = tid; i < n2; i += nt) {
+        const int j = i ^ stride;
+        if (j > i) {
+          const bool up = (i & size) == 0;
+          const V a = v[i], b = v[j];
+          if ((a > b) == up) {
+            v[i] = b;
+            v[j] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+constexpr int kFastBins = 2048;  // 11-bit digit
+constexpr int kListCap = 1024;   // members of the cut's bin ranked exactly
+
+// The candidate positions (C of the n_cand staged keys, the largest keys, ties to the lower
+// position) in ascending order into cpos, when the bin of the C-th largest key under an 11-bit
+// digit holds at most kListCap keys; returns false (having written nothing the general path
+// reads) otherwise.  Uses the radix histograms' space; starts and ends synchronised.
+template <int NW>
+__device__ bool fast_candidates(SelectShared<NW>& sh, const uint32_t* skeys, int32_t* cpos,
+                                int n_cand, int C, int tid, int lane, int wave) {
+  constexpr int NT = NW * 64;
+  static_assert(NT * 2 == kFastBins, "two bins per thread");
+  static_assert(sizeof(sh.hist) >= kFastBins * 4 + kListCap * 8, "histogram and list space");
+  uint32_t* h = &sh.hist[0][0];
+  uint64_t* list = reinterpret_cast<uint64_t*>(h + kFastBins);
+  for (int i = tid; i < kFastBins; i += NT) h[i] = 0u;
+  if (tid < 2) sh.wave_cnt[0][tid] = 0u;  // append counters: candidates above the bin, list
+  __syncthreads();
+  for (int i0 = 0; i0 < n_cand; i0 += 4 * NT) {
+    uint32_t kk[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int i = i0 + q * NT + tid;
+      kk[q] = i < n_cand ? skeys[i] : 0u;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) wave_hist_add(h, kk[q] >> 21, i0 + q * NT + tid < n_cand);
+  }
+  __syncthreads();
+  // suffix sums over the bins (larger bins = larger keys): thread t owns bins 2t, 2t + 1
+  const uint32_t c0 = h[2 * tid], c1 = h[2 * tid + 1];
+  uint32_t suf = c0 + c1;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t o = __shfl_down(suf, off, 64);
+    if (lane + off < 64) suf += o;
+  }
+  if (lane == 0) sh.scan[wave] = suf;
+  __syncthreads();
+  uint32_t above = 0;
+  for (int v = wave + 1; v < NW; ++v) above += sh.scan[v];
+  const uint32_t gt_hi = suf - (c0 + c1) + above;  // keys in bins above 2t + 1
+  const uint32_t gt_lo = gt_hi + c1;               // keys in bins above 2t
+  if (gt_hi < (uint32_t)C && gt_hi + c1 >= (uint32_t)C) {
+    sh.sel_threshold = 2 * tid + 1;
+    sh.sel_need = C - (int)gt_hi;
+    sh.wave_cnt[1][0] = c1;
+  }
+  if (gt_lo < (uint32_t)C && gt_lo + c0 >= (uint32_t)C) {
+    sh.sel_threshold = 2 * tid;
+    sh.sel_need = C - (int)gt_lo;
+    sh.wave_cnt[1][0] = c0;
+  }
+  __syncthreads();
+  const uint32_t bin = sh.sel_threshold;
+  const int need = sh.sel_need;
+  const int members = (int)sh.wave_cnt[1][0];
+  if (members > kListCap) return false;
+  // every key above the bin is a candidate (C - need of them, any order); the bin's members go
+  // to the list as (~key, position): ascending order is the key descending, then the position
+  for (int i0 = 0; i0 < n_cand; i0 += 4 * NT) {
+    uint32_t kk[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int i = i0 + q * NT + tid;
+      kk[q] = i < n_cand ? skeys[i] : 0u;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int i = i0 + q * NT + tid;
+      const bool in = i < n_cand;
+      wave_append(in && (kk[q] >> 21) > bin, &sh.wave_cnt[0][0], lane,
+                  [&](uint32_t slot) { cpos[slot] = i; });
+      wave_append(in && (kk[q] >> 21) == bin, &sh.wave_cnt[0][1], lane,
+                  [&](uint32_t slot) { list[slot] = ((uint64_t)(~kk[q]) << 32) | (uint32_t)i; });
+    }
+  }
+  int n2 = 1;
+  while (n2 < members) n2 <<= 1;
+  for (int i = members + tid; i < n2; i += NT) list[i] = ~0ull;
+  __syncthreads();
+  bitonic_sort(list, n2, tid, NT);
+  // the candidates in ascending position order: a bitmap over the positions (the histogram's
+  // space, free again: n_cand <= kMaxStagedKeyBytes / 4 positions), then each thread writes the
+  // set positions of its words at its offset
+  uint32_t* bits = h;
+  constexpr int kWords = kMaxStagedKeyBytes / 4 / 32;
+  static_assert(kWords * 4 <= kFastBins * 4, "bitmap space");
+  const int words = (n_cand + 31) / 32;
+  for (int w = tid; w < words; w += NT) bits[w] = 0u;
+  __syncthreads();
+  for (int t = tid; t < C; t += NT) {
+    const int pos = t < C - need ? cpos[t] : (int32_t)(uint32_t)list[t - (C - need)];
+    atomicOr(&bits[pos >> 5], 1u << (pos & 31));
+  }
+  __syncthreads();
+  // words [per * tid, per * tid + per) belong to thread tid
+  const int per = (words + NT - 1) / NT;
+  uint32_t cnt = 0;
+  for (int w = per * tid; w < min(words, per * tid + per); ++w) cnt += __popc(bits[w]);
+  uint32_t incl = cnt;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t o = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += o;
+  }
+  if (lane == 63) sh.scan[wave] = incl;
+  __syncthreads();
+  uint32_t out = incl - cnt;
+  for (int v = 0; v < wave; ++v) out += sh.scan[v];
+  for (int w = per * tid; w < min(words, per * tid + per); ++w) {
+    uint32_t m = bits[w];
+    while (m) {
+      const int b = __ffs(m) - 1;
+      cpos[out++] = 32 * w + b;
+      m &= m - 1;
+    }
+  }
+  __syncthreads();
+  return true;
+}
+
 // Compaction after the selection (k_out == nullptr: none); K, V, outputs as 16-byte vectors.
 struct CompactOut {
   const uint4* k;
@@ -207,7 +379,7 @@ struct CompactOut {
 
 }  // namespace
 
-template <int DT, int D, int NT, int CPT, bool STAGED>
+template <int DT, int D, int NT, int CPT, bool STAGED, bool GRAM>
 __global__ __launch_bounds__(NT) void mmr_select_kernel(
     const float* __restrict__ mu, const float* __restrict__ sigma,
     const typename Elem<DT>::T* __restrict__ k, const int32_t* __restrict__ lens,
@@ -220,8 +392,9 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
   constexpr int kThreads = NT, kWaves = NT / 64;
   static_assert(NT >= 256, "one thread per histogram bin");
   __shared__ SelectShared<kWaves> sh;
-  // dynamic LDS: [max_cand] positions, [max_cand] 1/|k|, then a region that first holds the
-  // order-preserving keys of every candidate score (STAGED) and then the candidates' key rows
+  // dynamic LDS: [max_cand] positions, [max_cand] 1/|k|, [max_cand] s~ (Gram greedy), then a region
+  // that first holds the order-preserving keys of every candidate score (STAGED) and then the
+  // candidates' key rows or (GRAM) the triangle of their dot products
   extern __shared__ __align__(16) unsigned char dyn[];
   const int g = blockIdx.x % h_kv, p = blockIdx.x / h_kv;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -236,7 +409,8 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
   const float lam1 = lambda1[p], lam2 = lambda2[p];
   int32_t* cpos = reinterpret_cast<int32_t*>(dyn);
   float* cinv = reinterpret_cast<float*>(dyn + (size_t)max_cand * 4);
-  unsigned char* region = dyn + (((size_t)max_cand * 8 + 15) & ~(size_t)15);
+  float* cst = reinterpret_cast<float*>(dyn + (size_t)max_cand * 8);
+  unsigned char* region = dyn + (((size_t)max_cand * 12 + 15) & ~(size_t)15);
   uint32_t* skeys = reinterpret_cast<uint32_t*>(region);
   T* ckeys = reinterpret_cast<T*>(region);
   const bool take_all = (C >= n_cand);
@@ -329,10 +503,20 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
     if (lane == 0) sh.wave_max[wave] = wm;
   }
 
+  // ---- 1a. fast front end (staged keys, 1024 threads): one 11-bit histogram of the keys finds
+  //      the bin of the C-th largest; every key above that bin is a candidate, and the bin's own
+  //      members (a few hundred where salient tokens set the cut) are sorted exactly, by key and then
+  //      position, in LDS.  The candidates are then sorted by position.  A bin too full for the
+  //      list (a cut through the flat bulk of the scores) takes the general path below.
+  bool fast_done = false;
+  if constexpr (STAGED && NT == 1024) {
+    if (!take_all) fast_done = fast_candidates<kWaves>(sh, skeys, cpos, n_cand, C, tid, lane, wave);
+  }
+
   // ---- 1. the C-th largest key: most-significant-digit radix select ---------------------------
   uint32_t prefix = 0, pmask = 0;
   int need = C;
-  for (int pass = 0; pass < (take_all ? 0 : 4); ++pass) {
+  for (int pass = 0; pass < (take_all || fast_done ? 0 : 4); ++pass) {
     const int shift = 24 - 8 * pass;
     for (int i = tid; i < kWaves * 256; i += kThreads) (&sh.hist[0][0])[i] = 0u;
     __syncthreads();
@@ -391,7 +575,7 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
 
   // ---- 2. candidate positions in ascending order ----------------------------------------------
   // key > threshold: taken; key == threshold: the `need` lowest positions are taken.
-  {
+  if (!fast_done) {
     const uint32_t thr = prefix;
     const int per_wave = (n_cand + kWaves - 1) / kWaves;
     const int w0 = wave * per_wave, w1 = min(n_cand, w0 + per_wave);
@@ -450,102 +634,310 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
   __syncthreads();  // the staged score keys are dead from here on: the region takes key rows
 
   // ---- 3. greedy admission -------------------------------------------------------------------
-  KeyRow<DT, D> key[CPT];
-  float st[CPT], corr[CPT], inv[CPT];
-  bool admitted[CPT];
-#pragma unroll
-  for (int q = 0; q < CPT; ++q) {
-    const int c = tid + q * kThreads;
-    admitted[q] = c >= C;  // slots beyond C never compete
-    corr[q] = 0.f;
-    st[q] = 0.f;
-    inv[q] = 0.f;
-    if (c < C) {
-      const int pos = cpos[c];
-      key[q].load(kg + (size_t)pos * D);
-      key[q].store(ckeys + (size_t)c * D);
-      const float n2 = key[q].sq_norm();
-      inv[q] = n2 > 0.f ? 1.f / sqrtf(n2) : 0.f;  // a zero key has cosine 0 to everything
-      cinv[c] = inv[q];
-      float sv = fmaf(lam1, sg_g[pos], w_mu * mu_g[pos]);
-      for (int j = max(0, pos - pool_h); j <= min(n_cand - 1, pos + pool_h); ++j)
-        sv = fmaxf(sv, fmaf(lam1, sg_g[j], w_mu * mu_g[j]));
-      st[q] = sv / den;
-    }
-  }
-  __syncthreads();
-
-  int last = -1;
-  float last_inv = 0.f;
   // the greedy trace (admitted slot and score key per step) reuses the radix histograms: at most
   // C <= 2 NT steps (2 NT = 128 NW words each)
   uint32_t* trace_slot = &sh.hist[0][0];
   uint32_t* trace_key = &sh.hist[0][0] + kWaves * 128;
-  // only the waves that own candidate slots take part; the others just keep step with the
-  // barrier (sleeping there instead of taking issue slots from the live waves)
-  const int live_waves = min(kWaves, (C + 63) / 64);
-  const bool live = wave < live_waves;
-  for (int t = 0; t < bp; ++t) {
-    if (live) {
-      float my_score = -INFINITY;  // admitted slots rank below every live score
-      int my_slot = 0x7FFFFFFF;
+  int last = -1;
+  if constexpr (GRAM) {
+    static_assert(DT == kDtBf16, "the Gram greedy takes bf16 keys");
+    float* gram = reinterpret_cast<float*>(region);
+    const int l32 = lane & 31, half = lane >> 5;
+    // s~ of every candidate (its base score, pooled as in phase 0, over the normaliser)
+    for (int c = tid; c < C; c += kThreads) {
+      const int pos = cpos[c];
+      float sv = fmaf(lam1, sg_g[pos], w_mu * mu_g[pos]);
+      for (int j = max(0, pos - pool_h); j <= min(n_cand - 1, pos + pool_h); ++j)
+        sv = fmaxf(sv, fmaf(lam1, sg_g[j], w_mu * mu_g[j]));
+      cst[c] = sv / den;
+    }
+    // Dot products of every pair of candidate keys, k_i . k_j, in 32 x 32 blocks (I, J), I <= J
+    // (block b of a wave: b-th of wave, wave + NW, ...), accumulated over the head dimension 16
+    // elements at a time: each 16-element slice of every candidate row is staged in LDS (the radix
+    // histograms' space, two slices in turn) and feeds one MFMA step of every block.  Each thread
+    // loads its 16-byte piece of every slice up front, so the key rows cross the memory system once
+    // with all loads in flight.
+    constexpr int kSlices = D / 16, kMaxBlk = 3;
+    const int nb = (C + 31) / 32;
+    const int n_blocks = nb * (nb + 1) / 2;
+    static_assert(kWaves * kMaxBlk >= (kGramMaxCand / 32) * (kGramMaxCand / 32 + 1) / 2, "blocks");
+    uint16_t* slice = reinterpret_cast<uint16_t*>(&sh.hist[0][0]);  // [2][kGramMaxCand][16]
+    static_assert(sizeof(sh.hist) >= 2 * kGramMaxCand * 16 * sizeof(uint16_t), "slice buffers");
+    const int piece_row = tid >> 1, piece_half = tid & 1;  // thread's 8-element piece of a slice
+    const bool has_piece = piece_row < C;
+    bf16x8_t pieces[kSlices];
+    {
+      const uint16_t* src = kg + (size_t)cpos[has_piece ? piece_row : 0] * D + 8 * piece_half;
+#pragma unroll
+      for (int sl = 0; sl < kSlices; ++sl)
+        pieces[sl] = *reinterpret_cast<const bf16x8_t*>(src + 16 * sl);
+      // |k|^2 of the row: this thread's half, then the other half from the neighbouring lane
+      typedef __bf16 __attribute__((ext_vector_type(2))) bf2;
+      float n2 = 0.f;
+#pragma unroll
+      for (int sl = 0; sl < kSlices; ++sl) {
+        const auto w = __builtin_bit_cast(uint4, pieces[sl]);
+        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          n2 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf2, ws[u]), __builtin_bit_cast(bf2, ws[u]), n2, false);
+      }
+      n2 += __shfl_xor(n2, 1, 64);
+      if (has_piece && piece_half == 0) cinv[piece_row] = n2 > 0.f ? 1.f / sqrtf(n2) : 0.f;
+    }
+    int blk_i[kMaxBlk], blk_j[kMaxBlk];
+#pragma unroll
+    for (int u = 0; u < kMaxBlk; ++u) {
+      int I = 0, rem = wave + u * kWaves;
+      while (I < nb && rem >= nb - I) {
+        rem -= nb - I;
+        ++I;
+      }
+      blk_i[u] = I;  // I == nb: no block
+      blk_j[u] = I + rem;
+    }
+    f32x16_t acc[kMaxBlk];
+#pragma unroll
+    for (int u = 0; u < kMaxBlk; ++u)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[u][r] = 0.f;
+#pragma unroll
+    for (int sl = 0; sl < kSlices; ++sl) {
+      uint16_t* buf = slice + (sl & 1) * kGramMaxCand * 16;
+      if (has_piece)
+        *reinterpret_cast<bf16x8_t*>(buf + piece_row * 16 + 8 * piece_half) = pieces[sl];
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < kMaxBlk; ++u) {
+        if (blk_i[u] < nb) {
+          const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(
+              buf + min(32 * blk_i[u] + l32, C - 1) * 16 + 8 * half);
+          const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(
+              buf + min(32 * blk_j[u] + l32, C - 1) * 16 + 8 * half);
+          acc[u] = mfma_step(a, b, acc[u]);
+        }
+      }
+      // the other buffer is written next: its readers (slice sl - 1) are done, the barrier above
+    }
+    // the triangle holds the cosines (k_i . k_j / |k_i|) / |k_j|, i <= j (a zero key has 1 / |k| = 0,
+    // hence cosine 0 to everything; a non-finite product counts as cosine 0)
+#pragma unroll
+    for (int u = 0; u < kMaxBlk; ++u) {
+      if (blk_i[u] < nb) {
+        const int j = 32 * blk_j[u] + l32;
+        const float inv_j = cinv[min(j, C - 1)];
+#pragma unroll
+        for (int jj = 0; jj < 16; ++jj) {
+          const int i = 32 * blk_i[u] + acc_row(jj, lane);
+          if (i < C && j < C && i <= j) {
+            const float cs = acc[u][jj] * cinv[i] * inv_j;
+            gram[tri_index(i, j, C)] = __builtin_isfinite(cs) ? cs : 0.f;
+          }
+        }
+      }
+    }
+    (void)n_blocks;
+    __syncthreads();
+    if (wave == 0) {
+      // One wave runs every step: lane l holds candidate slots l, l + 64, l + 128, l + 192, their
+      // s~ (-inf once admitted or for slots beyond C) and running max-cosine.  The cosine of
+      // slots (i, j), i <= j, is at row_off(i) + j of the triangle.  s~ and the cosines are
+      // finite after the clamps below, so a live score is finite and an admitted one -inf.
+      auto row_off = [&](int i) { return (i * (2 * C - i + 1)) / 2 - i; };
+      float st[kGramSlots], corr[kGramSlots];
+      int cq[kGramSlots], offq[kGramSlots];
+#pragma unroll
+      for (int q = 0; q < kGramSlots; ++q) {
+        const int c = lane + 64 * q;
+        cq[q] = min(c, C - 1);
+        offq[q] = row_off(cq[q]);
+        // a NaN or -inf score still ranks above the admitted slots (as the lowest finite one)
+        st[q] = c < C ? fmaxf(cst[c], -FLT_MAX) : -INFINITY;
+        corr[q] = 0.f;
+      }
+      float* corr_adm = cst;  // s~ has been read: the slot of s~ keeps the corr at admission
+      for (int t = 0; t < bp; ++t) {
+        // the cosines against the last admitted slot, every read in flight at once (slots past C
+        // read a valid entry that is not used)
+        if (last >= 0) {
+          const int off_last = row_off(last);
+          float gv[kGramSlots];
+#pragma unroll
+          for (int q = 0; q < kGramSlots; ++q)
+            gv[q] = gram[cq[q] <= last ? offq[q] + last : off_last + cq[q]];
+#pragma unroll
+          for (int q = 0; q < kGramSlots; ++q) corr[q] = __builtin_elementwise_maximum(corr[q], gv[q]);
+        }
+        float my_score = -INFINITY;
+        int my_slot = 0x7FFFFFFF;
+#pragma unroll
+        for (int q = 0; q < kGramSlots; ++q) {
+          const float sc = fmaf(lam2, corr[q], st[q]);
+          const bool better = sc > my_score;  // q ascending: ties keep the lower slot
+          my_score = better ? sc : my_score;
+          my_slot = better ? lane + 64 * q : my_slot;
+        }
+        const uint64_t b = wave_best<false>(my_score, my_slot);
+        last = __builtin_amdgcn_readfirstlane(min(max(unpack_slot(b), 0), C - 1));  // bp <= C
+        const int q_last = last >> 6;
+        if (lane == (last & 63)) {
+#pragma unroll
+          for (int q = 0; q < kGramSlots; ++q)
+            if (q == q_last) {
+              st[q] = -INFINITY;
+              corr_adm[last] = corr[q];
+            }
+        }
+        if (lane == 0) {  // the step's record; written out after the last step
+          trace_slot[t] = (uint32_t)last;
+          trace_key[t] = (uint32_t)(b >> 32);
+        }
+      }
+      if (cand_idx || cand_corr) {
+        // corr after the last step includes the last admitted key; an admitted slot reports its
+        // corr at admission
+        const size_t o = ((size_t)p * h_kv + g) * cand_stride;
+        const int off_last = row_off(last);
+#pragma unroll
+        for (int q = 0; q < kGramSlots; ++q) {
+          const int c = lane + 64 * q;
+          if (c < C) {
+            const bool adm = st[q] == -INFINITY;
+            const float gl = gram[cq[q] <= last ? offq[q] + last : off_last + cq[q]];
+            corr[q] = adm ? corr_adm[c] : __builtin_elementwise_maximum(corr[q], gl);
+          }
+          if (c < cand_stride) {
+            if (cand_idx) cand_idx[o + c] = c < C ? cpos[c] : -1;
+            if (cand_corr) cand_corr[o + c] = c < C ? corr[q] : 0.f;
+          }
+        }
+      }
+    }
+    if (cand_idx || cand_corr) {
+      const size_t o = ((size_t)p * h_kv + g) * cand_stride;
+      for (int c = kGramSlots * 64 + tid; c < cand_stride; c += kThreads) {
+        if (cand_idx) cand_idx[o + c] = -1;
+        if (cand_corr) cand_corr[o + c] = 0.f;
+      }
+    }
+    __syncthreads();
+  } else {
+    KeyRow<DT, D> key[CPT];
+    float st[CPT], corr[CPT], inv[CPT];
+    bool admitted[CPT];
+#pragma unroll
+    for (int q = 0; q < CPT; ++q) {
+      const int c = tid + q * kThreads;
+      admitted[q] = c >= C;  // slots beyond C never compete
+      corr[q] = 0.f;
+      st[q] = 0.f;
+      inv[q] = 0.f;
+      if (c < C) {
+        const int pos = cpos[c];
+        key[q].load(kg + (size_t)pos * D);
+        key[q].store(ckeys + (size_t)c * D);
+        const float n2 = key[q].sq_norm();
+        inv[q] = n2 > 0.f ? 1.f / sqrtf(n2) : 0.f;  // a zero key has cosine 0 to everything
+        cinv[c] = inv[q];
+        float sv = fmaf(lam1, sg_g[pos], w_mu * mu_g[pos]);
+        for (int j = max(0, pos - pool_h); j <= min(n_cand - 1, pos + pool_h); ++j)
+          sv = fmaxf(sv, fmaf(lam1, sg_g[j], w_mu * mu_g[j]));
+        st[q] = sv / den;
+      }
+    }
+    __syncthreads();
+
+    float last_inv = 0.f;
+    // only the waves that own candidate slots take part; the others just keep step with the
+    // barrier (sleeping there instead of taking issue slots from the live waves)
+    const int live_waves = min(kWaves, (C + 63) / 64);
+    const bool live = wave < live_waves;
+    for (int t = 0; t < bp; ++t) {
+      if (live) {
+        float my_score = -INFINITY;  // admitted slots rank below every live score
+        int my_slot = 0x7FFFFFFF;
+#pragma unroll
+        for (int q = 0; q < CPT; ++q) {
+          if (!admitted[q]) {
+            if (last >= 0) {
+              const float cs = key[q].dot_lds(ckeys + (size_t)last * D) * inv[q] * last_inv;
+              corr[q] = fmaxf(corr[q], cs);
+            }
+            float sc = fmaf(lam2, corr[q], st[q]);
+            if (!(sc > -INFINITY)) sc = -FLT_MAX;  // NaN or -inf still ranks above admitted slots
+            if (sc > my_score) {  // q ascending: ties keep the lower slot
+              my_score = sc;
+              my_slot = tid + q * kThreads;
+            }
+          }
+        }
+        const uint64_t wbest = wave_best<CPT == 1>(my_score, my_slot);
+        // the wave's best slot is owned by one of its lanes (slot = tid + q NT): its 1 / |k| rides
+        // along, so that no lookup follows the barrier
+        const int bslot = unpack_slot(wbest);
+        float binv = 0.f;
+#pragma unroll
+        for (int q = 0; q < CPT; ++q) {
+          const uint32_t v = __builtin_amdgcn_readlane(__float_as_uint(inv[q]), bslot & 63);
+          if ((bslot - q * kThreads) >> 6 == wave) binv = __uint_as_float(v);
+        }
+        if (lane == 0)
+          sh.best[t & 1][wave] = make_uint4((uint32_t)wbest, (uint32_t)(wbest >> 32), __float_as_uint(binv), 0u);
+      }
+      __syncthreads();
+      if (live) {
+        // the live waves' records (score key, slot, 1 / |k|), four reads in flight at a time
+        uint64_t b = 0;
+        float bi = 0.f;
+        for (int v0 = 0; v0 < live_waves; v0 += 4) {
+          // records past the live waves are read (v0 + 3 < NW) but never win
+          uint4 r[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) r[u] = sh.best[t & 1][v0 + u];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const uint64_t o = v0 + u < live_waves ? ((uint64_t)r[u].y << 32) | r[u].x : 0ull;
+            if (o > b) {
+              b = o;
+              bi = __uint_as_float(r[u].z);
+            }
+          }
+        }
+        last = min(max(unpack_slot(b), 0), C - 1);  // always a live slot: bp <= C
+#pragma unroll
+        for (int q = 0; q < CPT; ++q)
+          if (tid + q * kThreads == last) admitted[q] = true;
+        last_inv = bi;
+        if (tid == 0) {  // the step's record; written out after the last step
+          trace_slot[t] = (uint32_t)last;
+          trace_key[t] = (uint32_t)(b >> 32);
+        }
+      }
+    }
+    if (cand_idx || cand_corr) {
+      // corr after the last step includes the last admitted key
 #pragma unroll
       for (int q = 0; q < CPT; ++q) {
         if (!admitted[q]) {
-          if (last >= 0) {
-            const float cs = key[q].dot_lds(ckeys + (size_t)last * D) * inv[q] * last_inv;
-            corr[q] = fmaxf(corr[q], cs);
-          }
-          float sc = fmaf(lam2, corr[q], st[q]);
-          if (!(sc > -INFINITY)) sc = -FLT_MAX;  // NaN or -inf still ranks above admitted slots
-          if (sc > my_score) {  // q ascending: ties keep the lower slot
-            my_score = sc;
-            my_slot = tid + q * kThreads;
-          }
+          const float cs = key[q].dot_lds(ckeys + (size_t)last * D) * inv[q] * last_inv;
+          corr[q] = fmaxf(corr[q], cs);
         }
       }
-      const uint64_t wbest = wave_best<CPT == 1>(my_score, my_slot);
-      // the wave's best slot is owned by one of its lanes (slot = tid + q NT): its 1 / |k| rides
-      // along, so that no lookup follows the barrier
-      const int bslot = unpack_slot(wbest);
-      float binv = 0.f;
+      const size_t o = ((size_t)p * h_kv + g) * cand_stride;
 #pragma unroll
       for (int q = 0; q < CPT; ++q) {
-        const uint32_t v = __builtin_amdgcn_readlane(__float_as_uint(inv[q]), bslot & 63);
-        if ((bslot - q * kThreads) >> 6 == wave) binv = __uint_as_float(v);
-      }
-      if (lane == 0)
-        sh.best[t & 1][wave] = make_uint4((uint32_t)wbest, (uint32_t)(wbest >> 32), __float_as_uint(binv), 0u);
-    }
-    __syncthreads();
-    if (live) {
-      // the live waves' records (score key, slot, 1 / |k|), four reads in flight at a time
-      uint64_t b = 0;
-      float bi = 0.f;
-      for (int v0 = 0; v0 < live_waves; v0 += 4) {
-        // records past the live waves are read (v0 + 3 < NW) but never win
-        uint4 r[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) r[u] = sh.best[t & 1][v0 + u];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const uint64_t o = v0 + u < live_waves ? ((uint64_t)r[u].y << 32) | r[u].x : 0ull;
-          if (o > b) {
-            b = o;
-            bi = __uint_as_float(r[u].z);
-          }
+        const int c = tid + q * kThreads;
+        if (c < cand_stride) {
+          if (cand_idx) cand_idx[o + c] = c < C ? cpos[c] : -1;
+          if (cand_corr) cand_corr[o + c] = c < C ? corr[q] : 0.f;
         }
       }
-      last = min(max(unpack_slot(b), 0), C - 1);  // always a live slot: bp <= C
-#pragma unroll
-      for (int q = 0; q < CPT; ++q)
-        if (tid + q * kThreads == last) admitted[q] = true;
-      last_inv = bi;
-      if (tid == 0) {  // the step's record; written out after the last step
-        trace_slot[t] = (uint32_t)last;
-        trace_key[t] = (uint32_t)(b >> 32);
+      for (int c = tid + CPT * kThreads; c < cand_stride; c += kThreads) {
+        if (cand_idx) cand_idx[o + c] = -1;
+        if (cand_corr) cand_corr[o + c] = 0.f;
       }
     }
+
   }
   __syncthreads();
   for (int t = tid; t < bp; t += kThreads) {
@@ -557,36 +949,11 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
       sel_score[o] = __uint_as_float(u);
     }
   }
-
   // steps beyond this problem's budget: padding
   for (int t = bp + tid; t < budget; t += kThreads) {
     const size_t o = ((size_t)p * h_kv + g) * budget + t;
     sel_idx[o] = -1;
     if (sel_score) sel_score[o] = 0.f;
-  }
-
-  if (cand_idx || cand_corr) {
-    // corr after the last step includes the last admitted key
-#pragma unroll
-    for (int q = 0; q < CPT; ++q) {
-      if (!admitted[q]) {
-        const float cs = key[q].dot_lds(ckeys + (size_t)last * D) * inv[q] * last_inv;
-        corr[q] = fmaxf(corr[q], cs);
-      }
-    }
-    const size_t o = ((size_t)p * h_kv + g) * cand_stride;
-#pragma unroll
-    for (int q = 0; q < CPT; ++q) {
-      const int c = tid + q * kThreads;
-      if (c < cand_stride) {
-        if (cand_idx) cand_idx[o + c] = c < C ? cpos[c] : -1;
-        if (cand_corr) cand_corr[o + c] = c < C ? corr[q] : 0.f;
-      }
-    }
-    for (int c = tid + CPT * kThreads; c < cand_stride; c += kThreads) {
-      if (cand_idx) cand_idx[o + c] = -1;
-      if (cand_corr) cand_corr[o + c] = 0.f;
-    }
   }
 
   if (co.k_out) {
@@ -614,13 +981,15 @@ int select_max_candidates(int d, int elem_bytes) {
 }
 
 namespace {
-template <int DT, int D, int NT, int CPT, bool STAGED>
-hipError_t select_launch(const Shape& s, const SelectArgs& a, hipStream_t st) {
+// Bytes of dynamic LDS before the region: positions, 1 / |k| and s~ of max_cand candidates.
+size_t lds_head(int max_cand) { return ((size_t)max_cand * 12 + 15) & ~(size_t)15; }
+
+template <int DT, int D, int NT, int CPT, bool STAGED, bool GRAM>
+hipError_t select_launch(const Shape& s, const SelectArgs& a, size_t body, hipStream_t st) {
   using T = typename Elem<DT>::T;
-  const size_t region = std::max((size_t)a.max_cand * D * sizeof(T),
-                                 STAGED ? (size_t)a.max_cand_all * 4 : (size_t)0);
-  const size_t dyn = (((size_t)a.max_cand * 8 + 15) & ~(size_t)15) + region;
-  auto kern = mmr_select_kernel<DT, D, NT, CPT, STAGED>;
+  const size_t region = std::max(body, STAGED ? (size_t)a.max_cand_all * 4 : (size_t)0);
+  const size_t dyn = lds_head(a.max_cand) + region;
+  auto kern = mmr_select_kernel<DT, D, NT, CPT, STAGED, GRAM>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
   if (e != hipSuccess) return e;
@@ -634,17 +1003,17 @@ hipError_t select_launch(const Shape& s, const SelectArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Score keys are staged in LDS when every problem's candidates fit next to the key rows (and the
-// whole workgroup's LDS stays within the 160 KiB of a CU).
-template <int DT, int D, int NT, int CPT>
+// Score keys are staged in LDS when every problem's candidates fit next to the key rows or the
+// Gram triangle (and the whole workgroup's LDS stays within the 160 KiB of a CU).
+template <int DT, int D, int NT, int CPT, bool GRAM>
 hipError_t select_dispatch(const Shape& s, const SelectArgs& a, hipStream_t st) {
   using T = typename Elem<DT>::T;
-  const size_t rows = (size_t)a.max_cand * D * sizeof(T);
-  const size_t staged = (((size_t)a.max_cand * 8 + 15) & ~(size_t)15) +
-                        std::max(rows, (size_t)a.max_cand_all * 4) + sizeof(SelectShared<NT / 64>);
+  const size_t body = GRAM ? tri_entries(a.max_cand) * 4 : (size_t)a.max_cand * D * sizeof(T);
+  const size_t staged = lds_head(a.max_cand) + std::max(body, (size_t)a.max_cand_all * 4) +
+                        sizeof(SelectShared<NT / 64>);
   if ((size_t)a.max_cand_all * 4 <= (size_t)kMaxStagedKeyBytes && staged <= kLdsBytes)
-    return select_launch<DT, D, NT, CPT, true>(s, a, st);
-  return select_launch<DT, D, NT, CPT, false>(s, a, st);
+    return select_launch<DT, D, NT, CPT, true, GRAM>(s, a, body, st);
+  return select_launch<DT, D, NT, CPT, false, GRAM>(s, a, body, st);
 }
 
 template <int DT, int D>
@@ -653,16 +1022,17 @@ hipError_t select_cpt(const Shape& s, const SelectArgs& a, hipStream_t st) {
   if constexpr (DT == kDtBf16) {
     // bf16 key rows fit the registers of 16 waves: one candidate per thread of 1024
     static_assert(kMaxCand <= 1024, "one candidate per thread");
-    return select_dispatch<DT, D, 1024, 1>(s, a, st);
+    if (a.max_cand <= kGramMaxCand) return select_dispatch<DT, D, 1024, 1, true>(s, a, st);
+    return select_dispatch<DT, D, 1024, 1, false>(s, a, st);
   } else {
     // only the candidates-per-thread counts that the LDS key copy allows are instantiated
     constexpr int kNT = 256;
     const int cpt = (a.max_cand + kNT - 1) / kNT;
-    if (cpt <= 1) return select_dispatch<DT, D, kNT, 1>(s, a, st);
+    if (cpt <= 1) return select_dispatch<DT, D, kNT, 1, false>(s, a, st);
     if constexpr (kMaxCand > kNT) {
-      if (cpt <= 2) return select_dispatch<DT, D, kNT, 2>(s, a, st);
+      if (cpt <= 2) return select_dispatch<DT, D, kNT, 2, false>(s, a, st);
     }
-    if constexpr (kMaxCand > 2 * kNT) return select_dispatch<DT, D, kNT, 4>(s, a, st);
+    if constexpr (kMaxCand > 2 * kNT) return select_dispatch<DT, D, kNT, 4, false>(s, a, st);
     return hipErrorInvalidValue;
   }
 }
