@@ -16,7 +16,8 @@
  *   - A "problem" is one layer of one sequence.  A batch holds n_prob problems; problem p has
  *     context length L_p and its keys/values start at packed token offset tok_off[p].
  *   - Every tensor pointer is a caller-owned DEVICE pointer unless its name ends in _host.  The
- *     library never allocates or frees device memory; scratch comes from the caller's workspace.
+ *     library never allocates or frees device memory; scratch comes from the caller's workspace
+ *     (kv_window_mu_sigma_noalloc: from a static device array of the library instead).
  *   - Calls are asynchronous: after host-side validation they enqueue kernels on `stream` (a
  *     hipStream_t passed as void*, NULL = default stream) and return.  Device faults surface at the
  *     caller's next synchronisation.
@@ -61,6 +62,7 @@ extern "C" {
 #define KV_ERR_WORKSPACE (-5) /* workspace smaller than kv_workspace_bytes() asks for           */
 #define KV_ERR_LAUNCH (-6)    /* a HIP launch or device query failed                            */
 #define KV_ERR_ARG (-7)       /* any other invalid argument (n_prob, profile family, params)    */
+#define KV_ERR_SCRATCH (-8)   /* the batch needs more than KV_NOALLOC_SCRATCH_BYTES of scratch  */
 
 /* ---- element types --------------------------------------------------------------------------- */
 #define KV_F32 0
@@ -135,6 +137,19 @@ int kv_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float sc
 int kv_window_mu_sigma(const kv_problem* pr, const void* q_win, const void* k, float scale,
                        float* row_max, float* row_sum, float* mu, float* sigma, void* ws,
                        size_t ws_bytes, void* stream);
+
+/* kv_window_mu_sigma_ex for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): same arguments without the
+ * workspace, same kernels, same results bit for bit.  The library's own static scratch of
+ * KV_NOALLOC_SCRATCH_BYTES per GPU (held from the first call on that GPU until the process ends)
+ * takes the workspace's place; nothing is allocated or freed, by the library or any routine it
+ * calls.  A batch whose workspace (kv_workspace_bytes) exceeds it returns KV_ERR_SCRATCH and
+ * launches nothing.  Every call on one GPU shares that GPU's scratch: calls that overlap on one GPU
+ * (on different streams, or from different threads) race, and must be ordered by the caller. */
+#define KV_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+int kv_window_mu_sigma_noalloc(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                               int32_t sigma_rows, float* row_max, float* row_sum, float* mu,
+                               float* sigma, void* stream);
 
 /* Which window values the dispersion sigma of kv_mu_sigma_ex / kv_window_mu_sigma_ex runs over.
  * The paper defines Eq. (3) for one attention head and does not say how the G query heads that

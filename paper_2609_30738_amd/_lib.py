@@ -21,6 +21,8 @@ KV_ERR_BUDGET = -4
 KV_ERR_WORKSPACE = -5
 KV_ERR_LAUNCH = -6
 KV_ERR_ARG = -7
+KV_ERR_SCRATCH = -8
+KV_NOALLOC_SCRATCH_BYTES = 16 << 20
 
 KV_SIGMA_GROUP_MEAN = 0
 KV_SIGMA_ALL_ROWS = 1
@@ -41,7 +43,8 @@ LIB_PATH = os.environ.get("KVEVICT_LIB") or os.path.join(os.path.dirname(os.path
 
 SYMBOLS = ("kv_strerror", "kv_version", "kv_workspace_bytes", "kv_candidate_stride",
            "kv_window_scores", "kv_mu_sigma", "kv_mu_sigma_ex", "kv_window_mu_sigma",
-           "kv_window_mu_sigma_ex", "kv_mmr_select", "kv_mmr_select_ex", "kv_mmr_select_compact",
+           "kv_window_mu_sigma_ex", "kv_window_mu_sigma_noalloc", "kv_mmr_select",
+           "kv_mmr_select_ex", "kv_mmr_select_compact",
            "kv_compact_cache", "kv_compact_cache_ex", "kv_decode_workspace_bytes",
            "kv_decode_attention", "kv_pyramid_budgets", "kv_depth_profile")
 
@@ -96,6 +99,8 @@ def lib() -> ctypes.CDLL:
         h.kv_mu_sigma_ex.argtypes = [pr, vp, vp, ctypes.c_float, vp, vp, i32, vp, vp, vp, vp]
         h.kv_window_mu_sigma_ex.argtypes = [pr, vp, vp, ctypes.c_float, i32, vp, vp, vp, vp, vp,
                                             sz, vp]
+        h.kv_window_mu_sigma_noalloc.argtypes = [pr, vp, vp, ctypes.c_float, i32, vp, vp, vp, vp,
+                                                 vp]
         h.kv_mmr_select.argtypes = [pr, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, sz,
                                     vp]
         h.kv_mmr_select_compact.argtypes = [pr, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp,
@@ -112,7 +117,8 @@ def lib() -> ctypes.CDLL:
         h.kv_depth_profile.argtypes = [i32, ctypes.POINTER(ctypes.c_double), i32, i32,
                                        ctypes.POINTER(ctypes.c_float)]
         for name in ("kv_window_scores", "kv_mu_sigma", "kv_mu_sigma_ex", "kv_window_mu_sigma",
-                     "kv_window_mu_sigma_ex", "kv_mmr_select", "kv_mmr_select_ex",
+                     "kv_window_mu_sigma_ex", "kv_window_mu_sigma_noalloc", "kv_mmr_select",
+                     "kv_mmr_select_ex",
                      "kv_compact_cache", "kv_compact_cache_ex", "kv_decode_attention",
                      "kv_pyramid_budgets", "kv_depth_profile"):
             getattr(h, name).restype = ctypes.c_int
@@ -258,6 +264,15 @@ def window_mu_sigma_ex(batch: Batch, q_win, k, scale: float, sigma_rows, row_max
                                        _ptr(mu), _ptr(sigma), _ptr(ws),
                                        0 if ws is None else ws.numel() * ws.element_size(),
                                        _stream(stream)), "kv_window_mu_sigma_ex")
+
+
+def window_mu_sigma_noalloc(batch: Batch, q_win, k, scale: float, row_max, row_sum, mu, sigma,
+                            sigma_rows="group_mean", stream=None) -> None:
+    """kv_window_mu_sigma_noalloc (no workspace: the library's static scratch)."""
+    _check(lib().kv_window_mu_sigma_noalloc(batch.ref(), _ptr(q_win), _ptr(k), float(scale),
+                                            _sigma_rows(sigma_rows), _ptr(row_max),
+                                            _ptr(row_sum), _ptr(mu), _ptr(sigma),
+                                            _stream(stream)), "kv_window_mu_sigma_noalloc")
 
 
 def mmr_select(batch: Batch, mu, sigma, k, lambda1, lambda2, budget: int, cand_mult: int,

@@ -192,6 +192,7 @@ const char* kv_strerror(int status) {
     case KV_ERR_WORKSPACE: return "workspace too small or misaligned";
     case KV_ERR_LAUNCH: return "HIP launch failed";
     case KV_ERR_ARG: return "invalid argument";
+    case KV_ERR_SCRATCH: return "batch needs more scratch than KV_NOALLOC_SCRATCH_BYTES";
     default: return "unknown status";
   }
 }
@@ -316,6 +317,21 @@ int kv_window_mu_sigma_ex(const kv_problem* pr, const void* q_win, const void* k
   if (st != KV_OK) return st;
   return launch_status(kv::launch_mu_sigma(s, q_win, k, scale, row_max, row_sum, mu, sigma,
                                            nullptr, all, hs));
+}
+
+int kv_window_mu_sigma_noalloc(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                               int32_t sigma_rows, float* row_max, float* row_sum, float* mu,
+                               float* sigma, void* stream) {
+  static_assert(KV_NOALLOC_SCRATCH_BYTES == kv::kNoAllocScratchBytes, "scratch size");
+  kv::Shape s;
+  const int st = check_problem(pr, &s);
+  if (st != KV_OK) return st;
+  if (window_ws_bytes(pr, s) > kv::kNoAllocScratchBytes) return KV_ERR_SCRATCH;
+  void* ws = nullptr;
+  if (!q_win || !k || !row_max || !row_sum || !mu || !sigma) return KV_ERR_NULL;
+  if (kv::noalloc_scratch(&ws) != hipSuccess) return KV_ERR_LAUNCH;
+  return kv_window_mu_sigma_ex(pr, q_win, k, scale, sigma_rows, row_max, row_sum, mu, sigma, ws,
+                               kv::kNoAllocScratchBytes, stream);
 }
 
 int kv_mmr_select(const kv_problem* pr, const float* mu, const float* sigma, const void* k,

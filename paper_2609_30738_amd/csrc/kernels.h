@@ -112,6 +112,11 @@ hipError_t launch_compact(const Shape& s, const void* k, const void* v, const in
                           int budget, const int32_t* budgets, int keep_tail, int out_rows,
                           void* k_out, void* v_out, hipStream_t stream);
 
+// The static scratch of the entry point that allocates nothing (noalloc.hip): its device address
+// on the current device, looked up on the first call per device.
+constexpr size_t kNoAllocScratchBytes = (size_t)16 << 20;
+hipError_t noalloc_scratch(void** ptr);
+
 // Decode attention over a compacted cache (decode.hip).
 struct DecodeArgs {
   const void* q;      // [n_prob][h_q][d]

@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_version_and_strerror():
     assert _lib.version() == 1
-    for code in range(-7, 1):
+    for code in range(-8, 1):
         assert _lib.strerror(code) and _lib.strerror(code) != "unknown status"
     assert _lib.strerror(-99) == "unknown status"
 
@@ -303,3 +303,19 @@ def test_select_compact_checks():
     assert lib.kv_mmr_select_compact(*args(mu=None)) == _lib.KV_ERR_NULL
     assert lib.kv_mmr_select_compact(*args(v=ctypes.c_void_p(258))) == _lib.KV_ERR_ARG
     assert lib.kv_mmr_select_compact(*args(budget=0)) == _lib.KV_ERR_BUDGET
+
+
+def test_no_alloc_entry_validates_and_bounds_its_scratch():
+    """kv_window_mu_sigma_noalloc: a batch whose workspace exceeds the static scratch is rejected
+    with KV_ERR_SCRATCH before anything else runs; other argument errors as in kv_window_mu_sigma."""
+    lib = _lib.lib()
+    big = HostProblem(dtype=_lib.KV_F32, h_q=8, h_kv=8, d=128, w=8, lens=(32768,) * 512)
+    assert lib.kv_workspace_bytes(big.ref(), 64, 4, 8) > _lib.KV_NOALLOC_SCRATCH_BYTES
+    assert lib.kv_window_mu_sigma_noalloc(big.ref(), P, P, 0.088, 0, P, P, P, P,
+                                          NULL) == _lib.KV_ERR_SCRATCH
+    pr = HostProblem()
+    assert lib.kv_workspace_bytes(pr.ref(), 64, 4, 32) <= _lib.KV_NOALLOC_SCRATCH_BYTES
+    assert lib.kv_window_mu_sigma_noalloc(pr.ref(), NULL, P, 0.088, 0, P, P, P, P,
+                                          NULL) == _lib.KV_ERR_NULL
+    assert lib.kv_window_mu_sigma_noalloc(None, P, P, 0.088, 0, P, P, P, P, NULL) == _lib.KV_ERR_NULL
+
