@@ -136,26 +136,52 @@ def measured_traffic(kernel: str, workload: str):
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(wl, packed_layers, n_layers_sample: int) -> dict:
-    """The CPU oracle, as it stands, on a bounded sample (the first layers), scaled to ms/pass."""
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:  # pragma: no cover
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, packed_layers, single_thread_layers: int) -> dict:
+    """The CPU oracle, as it stands: the whole pass (every layer) with its BLAS on every host
+    thread, then the first layers single-threaded, scaled to the pass."""
     from oracle import evict, profiles
     lam1 = profiles.layer_lambdas(wl.lam1.family, wl.lam1.params, wl.n_layers)
     lam2 = profiles.layer_lambdas(wl.lam2.family, wl.lam2.params, wl.n_layers)
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
+        threadpool_limits = None
         threads = os.cpu_count() or 1
-    t0 = time.perf_counter()
-    for j, (q, k, v) in enumerate(packed_layers[:n_layers_sample]):
-        layer = wl.layer_of(j)
-        evict.evict_problem(q, k, v, wl.dtype, wl.scale, lam1[layer], lam2[layer], wl.budget)
-    dt = time.perf_counter() - t0
-    per_pass_ms = dt / n_layers_sample * wl.n_prob * 1e3
-    return {"value": round(per_pass_ms, 1), "unit": "ms", "cores": int(threads),
+
+    def run(layers):
+        t0 = time.perf_counter()
+        for j, (q, k, v) in enumerate(layers):
+            layer = wl.layer_of(j)
+            evict.evict_problem(q, k, v, wl.dtype, wl.scale, lam1[layer], lam2[layer], wl.budget)
+        return time.perf_counter() - t0
+
+    full_s = run(packed_layers)
+    line = {"value": round(full_s * 1e3, 1), "unit": "ms", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"{n_layers_sample} of {wl.n_prob} layers of {wl.name} "
-                      f"({dt:.1f} s), scaled to the full pass"}
+            "sample": f"the whole pass: all {len(packed_layers)} layers of {wl.name}, "
+                      f"BLAS on {threads} threads",
+            "host_cpus": os.cpu_count(), "cpu_model": cpu_model()}
+    if single_thread_layers > 0 and threadpool_limits is not None:
+        n1 = min(single_thread_layers, len(packed_layers))
+        with threadpool_limits(1):
+            one_s = run(packed_layers[:n1])
+        line["single_thread"] = {"value": round(one_s / n1 * len(packed_layers) * 1e3, 1),
+                                 "unit": "ms", "cores": 1,
+                                 "sample": f"{n1} of {len(packed_layers)} layers ({one_s:.1f} s), "
+                                           "scaled to the pass"}
+    return line
 
 
 def copy_probe(torch, mib: int) -> None:
@@ -236,8 +262,16 @@ def main() -> None:
     ap.add_argument("--warmup", type=int, default=20,
                     help="untimed steps first: the step time settles over the first 10-20 passes")
     ap.add_argument("--workload", default=WORKLOADS[0], choices=WORKLOADS)
-    ap.add_argument("--cpu-layers", type=int, default=20,
-                    help="layers of the oracle sample for the CPU baseline (0: skip)")
+    ap.add_argument("--cpu-baseline", type=int, default=1,
+                    help="1: time the CPU oracle on the whole pass (all host threads) and on "
+                         "--cpu-single-layers layers single-threaded; 0: skip")
+    ap.add_argument("--cpu-single-layers", type=int, default=8,
+                    help="layers of the single-threaded oracle sample")
+    ap.add_argument("--settle-ms", type=float, default=0.0,
+                    help="untimed passes before the warm-up, for at least this long (0: none). "
+                         "From idle the engine clock ramps up over the first 20-30 passes; after "
+                         "a few hundred ms of back-to-back passes the pass time turns bimodal "
+                         "(0.82 / 0.91 ms) as the power management steps the clock")
     ap.add_argument("--flush", choices=("read", "write"), default="read",
                     help="how the last-level cache is emptied before each timed step")
     ap.add_argument("--unfused", action="store_true",
@@ -307,12 +341,25 @@ def main() -> None:
     def new_events():
         return [torch.cuda.Event(enable_timing=True) for _ in range(3)]
 
+    # optional settle phase (off by default): from idle the engine clock ramps up over the first
+    # 20-30 passes (a fixed bf16 GEMM between passes runs ~17 % faster after them), while a few
+    # hundred ms of back-to-back passes make the pass time bimodal under the power management
+    settle_passes, t_settle = 0, time.perf_counter()
+    while args.settle_ms > 0 and (settle_passes < 20 or
+                                  (time.perf_counter() - t_settle) * 1e3 < args.settle_ms):
+        flush()
+        step(new_events())
+        settle_passes += 1
+        if settle_passes % 10 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    settle_ms = (time.perf_counter() - t_settle) * 1e3
     for _ in range(args.warmup):
         flush()
         step(new_events())
     torch.cuda.synchronize()
-    print(f"# inputs drawn and uploaded in {gen_s:.1f} s; warmup done", file=sys.stderr,
-          flush=True)
+    print(f"# inputs drawn and uploaded in {gen_s:.1f} s; settled ({settle_passes} passes, "
+          f"{settle_ms:.0f} ms) and warmed up", file=sys.stderr, flush=True)
 
     all_events = []
     torch.cuda.synchronize()
@@ -478,6 +525,7 @@ def main() -> None:
         "step_ms_each": [round(float(x), 4) for x in step_ms],
         "wall_s_timed_loop": round(wall, 3),
         "cache_flush": f"{args.flush} of 512 MiB before every timed step",
+        "settle": {"passes": settle_passes, "ms": round(settle_ms, 1)},
         "per_layer_schedule_ms": {"total": round(lay_score + lay_rest, 4),
                                   "scoring (32 launches of kv_window_mu_sigma)": round(lay_score, 4),
                                   "select+compact (batched)": round(lay_rest, 4)},
@@ -504,15 +552,21 @@ def main() -> None:
         "roofline": dominant,
         "roofline_passes": passes,
     }
-    if args.cpu_layers > 0:
+    # the device work is complete and its buffers released before the host-side baseline (and
+    # before the interpreter exits: no device memory or event outlives the run)
+    torch.cuda.synchronize()
+    del all_events, layer_events
+    inp = out = None
+    torch.cuda.empty_cache()
+    if args.cpu_baseline:
         layers = []
-        for j in range(min(args.cpu_layers, wl.n_prob)):
+        for j in range(wl.n_prob):
             L = int(packed.lens[j])
             off = int(packed.tok_off[j]) * wl.h_kv * wl.d
             n = L * wl.h_kv * wl.d
             layers.append((packed.q_win[j], packed.k[off:off + n].reshape(wl.h_kv, L, wl.d),
                            packed.v[off:off + n].reshape(wl.h_kv, L, wl.d)))
-        line["cpu_baseline"] = cpu_baseline(wl, layers, len(layers))
+        line["cpu_baseline"] = cpu_baseline(wl, layers, args.cpu_single_layers)
     print(json.dumps(line), flush=True)
 
 

@@ -9,6 +9,9 @@ The paper does not print the schedule.  Reading (R26), after PyramidKV's arithme
   b(l)  = B_max - l (B_max - B_min) / (n_layers - 1)       (exact rational; b = B for one layer)
 and the integer budget rounds b(l) away from B (up above B, down below it).  b(l) + b(n-1-l) = 2 B,
 so the rounded pair still sums to 2 B and the total is exactly n_layers * B.
+
+Parity unpinned: the schedule is a reading (R26); the tests pin this function to its own
+arithmetic (a hand-worked case, the exact total, monotone decrease, symmetry), not to the paper.
 """
 from __future__ import annotations
 

@@ -30,6 +30,11 @@ Readings of points the paper leaves open (each used below where it applies):
   R12 a zero key has a zero unit vector (its cosine to anything is 0).
   R14 selections are reported in admission order; the compacted cache holds the kept positions in
       ascending order followed by the kept tail.
+
+Parity unpinned: R1 (how the query heads of a group enter mu and sigma; token_statistics) and R6
+(the size and placement of max_pool) are readings the paper does not fix.  The tests pin both
+functions to their own definitions (library mean / stdev, scipy's maximum filter), not to the
+paper.
 """
 from __future__ import annotations
 
