@@ -197,44 +197,44 @@ def copy_probe(torch, mib: int) -> None:
 
 
 def config_passes(torch, args) -> None:
-    """One JSON line per workload of the other configurations: the same batched pass (scoring,
-    selection, compaction), timed the same way (cache read-flushed before every step, HIP events),
-    with its algorithmic bytes per second.  The ragged batch times its three coefficient runs over
-    one scoring."""
+    """One JSON line per workload of the other configurations: the same batched pass (scoring with
+    the base scores formed inside it, then selection and compaction), timed the same way (cache
+    read-flushed before every step, HIP events), with its algorithmic bytes per second.  The ragged
+    batch's three coefficient runs differ in lambda1 as well, so each is a pass of its own."""
     from paper_2609_30738_amd import _lib, api, workloads as W
     flush_buf = torch.ones(128 << 20, dtype=torch.float32, device="cuda")
     cases = [W.mistral_layer()] + [W.mistral_pass_8k(b) for b in (32, 64, 128)]
     ragged = [W.ragged_batch(r) for r in ("dispersion_only", "redundancy_only", "both")]
     stream = torch.cuda.current_stream()
 
-    def run(wl, packed, lam_runs):
+    def run(wl, packed):
         inp = api.upload(wl.dtype, wl.h_q, wl.h_kv, wl.d, wl.w, packed.q_win, packed.k, packed.v,
-                         packed.lens, packed.tok_off, *lam_runs[0])
+                         packed.lens, packed.tok_off, *lambdas(wl))
         out = api.allocate(inp, wl.budget)
         b = inp.batch
-        lam_dev = [(torch.from_numpy(np.asarray(l1, np.float32)).cuda(),
-                    torch.from_numpy(np.asarray(l2, np.float32)).cuda()) for l1, l2 in lam_runs]
+        score = torch.empty_like(out.mu)
+        wsb = _lib.base_scores_workspace_bytes(b)
+        ws_sc = torch.empty(wsb, dtype=torch.uint8, device="cuda") if wsb else None
         rows = []
         for it in range(args.warmup + args.steps):
             flush_buf.amax()
-            evs = [torch.cuda.Event(enable_timing=True) for _ in range(2 + len(lam_dev))]
+            evs = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
             evs[0].record(stream)
-            _lib.window_mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
-                                 out.sigma, out.ws)
+            _lib.window_base_scores(b, inp.q_win, inp.k, inp.scale, inp.lambda1, out.row_max,
+                                    out.row_sum, score, ws=ws_sc)
             evs[1].record(stream)
-            for r, (l1, l2) in enumerate(lam_dev):
-                _lib.mmr_select_compact(b, out.mu, out.sigma, inp.k, inp.v, l1, l2, wl.budget, 4,
-                                        wl.w, out.sel_idx, out.k_out, out.v_out, out.ws)
-                evs[2 + r].record(stream)
+            _lib.mmr_select_scored(b, score, inp.k, inp.v, inp.lambda2, wl.budget, 4, wl.w,
+                                   out.sel_idx, k_out=out.k_out, v_out=out.v_out)
+            evs[2].record(stream)
             if it >= args.warmup:
                 rows.append(evs)
         torch.cuda.synchronize()
-        t = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(len(e) - 1)] for e in rows])
+        t = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(2)] for e in rows])
         return t.mean(axis=0), algorithmic_bytes(wl)
 
     for wl in cases:
         packed = W.draw_packed(wl)
-        parts, ab = run(wl, packed, [lambdas(wl)])
+        parts, ab = run(wl, packed)
         ms = float(parts.sum())
         print(json.dumps({"config": wl.name, "ms_per_pass": round(ms, 4),
                           "scoring_ms": round(float(parts[0]), 4),
@@ -242,17 +242,17 @@ def config_passes(torch, args) -> None:
                           "algorithmic_bytes": ab["total"],
                           "GBps": round(ab["total"] / (ms * 1e-3) / 1e9, 1)}), flush=True)
     packed = W.draw_packed(ragged[0])  # the three runs share their inputs
-    parts, ab = run(ragged[0], packed, [lambdas(wl) for wl in ragged])
+    per_run = {}
+    for wl in ragged:
+        parts, ab = run(wl, packed)
+        ms = float(parts.sum())
+        per_run[wl.name.rsplit("_B128_", 1)[-1]] = {
+            "ms_per_pass": round(ms, 4), "scoring_ms": round(float(parts[0]), 4),
+            "select_compact_ms": round(float(parts[1]), 4),
+            "GBps": round(ab["total"] / (ms * 1e-3) / 1e9, 1)}
     print(json.dumps({"config": ragged[0].name.replace("_dispersion_only", ""),
                       "total_tokens_per_layer": int(packed.lens.sum() // ragged[0].n_layers),
-                      "scoring_ms": round(float(parts[0]), 4),
-                      "select_compact_ms_per_run": {r: round(float(x), 4) for r, x in
-                                                    zip(("dispersion_only", "redundancy_only",
-                                                         "both"), parts[1:])},
-                      "ms_per_pass_both": round(float(parts[0] + parts[3]), 4),
-                      "algorithmic_bytes": ab["total"],
-                      "GBps_both": round(ab["total"] / (float(parts[0] + parts[3]) * 1e-3) / 1e9, 1)}),
-          flush=True)
+                      "algorithmic_bytes": ab["total"], "runs": per_run}), flush=True)
 
 
 def main() -> None:
@@ -274,6 +274,9 @@ def main() -> None:
                          "(0.82 / 0.91 ms) as the power management steps the clock")
     ap.add_argument("--flush", choices=("read", "write"), default="read",
                     help="how the last-level cache is emptied before each timed step")
+    ap.add_argument("--mu-sigma-path", action="store_true",
+                    help="time kv_window_mu_sigma + kv_mmr_select_compact (mu and sigma through "
+                         "HBM) instead of kv_window_base_scores + kv_mmr_select_scored")
     ap.add_argument("--unfused", action="store_true",
                     help="time kv_window_scores + kv_mu_sigma instead of kv_window_mu_sigma")
     ap.add_argument("--configs", action="store_true",
@@ -321,8 +324,29 @@ def main() -> None:
             flush_buf.amax()
     stream = torch.cuda.current_stream()
     b = inp.batch
+    # the base score of every key: the timed pass's intermediate
+    score = torch.empty_like(out.mu)
+    ws_sc_bytes = _lib.base_scores_workspace_bytes(b)
+    ws_sc = torch.empty(ws_sc_bytes, dtype=torch.uint8, device="cuda") if ws_sc_bytes else None
+    mu_sigma_path = args.mu_sigma_path or args.unfused
 
     names = ["scoring", "select + compact"]
+
+    def scored_scoring():
+        _lib.window_base_scores(b, inp.q_win, inp.k, inp.scale, inp.lambda1, out.row_max,
+                                out.row_sum, score, ws=ws_sc)
+
+    def scored_select():
+        _lib.mmr_select_scored(b, score, inp.k, inp.v, inp.lambda2, wl.budget, 4, wl.w,
+                               out.sel_idx, k_out=out.k_out, v_out=out.v_out)
+
+    def ms_scoring():
+        _lib.window_mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
+                             out.sigma, out.ws)
+
+    def ms_select():
+        _lib.mmr_select_compact(b, out.mu, out.sigma, inp.k, inp.v, inp.lambda1, inp.lambda2,
+                                wl.budget, 4, wl.w, out.sel_idx, out.k_out, out.v_out, out.ws)
 
     def step(evs):
         evs[0].record(stream)
@@ -330,12 +354,15 @@ def main() -> None:
             _lib.window_scores(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.ws)
             _lib.mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
                           out.sigma)
+        elif mu_sigma_path:
+            ms_scoring()
         else:
-            _lib.window_mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum,
-                                 out.mu, out.sigma, out.ws)
+            scored_scoring()
         evs[1].record(stream)
-        _lib.mmr_select_compact(b, out.mu, out.sigma, inp.k, inp.v, inp.lambda1, inp.lambda2,
-                                wl.budget, 4, wl.w, out.sel_idx, out.k_out, out.v_out, out.ws)
+        if mu_sigma_path:
+            ms_select()
+        else:
+            scored_select()
         evs[2].record(stream)
 
     def new_events():
@@ -388,6 +415,12 @@ def main() -> None:
         torch.cuda.synchronize()
         t = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(len(calls))] for e in rows_])
         return [float(x) for x in t.mean(axis=0)]
+
+    # the other path on the same inputs: mu and sigma through HBM, then the selection from them
+    if mu_sigma_path:
+        alt_scoring, alt_select = timed(scored_scoring, scored_select)
+    else:
+        alt_scoring, alt_select = timed(ms_scoring, ms_select)
 
     # per kernel: the two scoring passes through their own entry points, events between them
     # (warm-up first: a kernel's first launch also loads its code); with one segment per unit,
@@ -456,16 +489,26 @@ def main() -> None:
     layer_batches = [_lib.Batch(wl.dtype, wl.h_q, wl.h_kv, wl.d, wl.w, [int(b.lens_host[p])],
                                 [int(b.tok_off_host[p])]) for p in range(b.n_prob)]
     rows = wl.h_q * wl.w
+    ws_lay_bytes = max(_lib.base_scores_workspace_bytes(lb) for lb in layer_batches)
+    ws_lay = torch.empty(max(ws_lay_bytes, 256), dtype=torch.uint8, device="cuda")
 
     def layered_step(evs):
         evs[0].record(stream)
         for p, lb in enumerate(layer_batches):
-            _lib.window_mu_sigma(lb, inp.q_win[p], inp.k, inp.scale,
-                                 out.row_max[p * rows:(p + 1) * rows],
-                                 out.row_sum[p * rows:(p + 1) * rows], out.mu, out.sigma, out.ws)
+            if mu_sigma_path:
+                _lib.window_mu_sigma(lb, inp.q_win[p], inp.k, inp.scale,
+                                     out.row_max[p * rows:(p + 1) * rows],
+                                     out.row_sum[p * rows:(p + 1) * rows], out.mu, out.sigma,
+                                     out.ws)
+            else:
+                _lib.window_base_scores(lb, inp.q_win[p], inp.k, inp.scale, inp.lambda1[p:p + 1],
+                                        out.row_max[p * rows:(p + 1) * rows],
+                                        out.row_sum[p * rows:(p + 1) * rows], score, ws=ws_lay)
         evs[1].record(stream)
-        _lib.mmr_select_compact(b, out.mu, out.sigma, inp.k, inp.v, inp.lambda1, inp.lambda2,
-                                wl.budget, 4, wl.w, out.sel_idx, out.k_out, out.v_out, out.ws)
+        if mu_sigma_path:
+            ms_select()
+        else:
+            scored_select()
         evs[2].record(stream)
 
     layer_events = []
@@ -485,11 +528,11 @@ def main() -> None:
     mean_part = per.mean(axis=0)
     ab = algorithmic_bytes(wl)
     flops = mfma_flops(wl)
-    # The dominant kernel is the scoring kernel of the timed pass (kv_window_mu_sigma with every
-    # unit one segment: both passes of a unit in one workgroup).  What the method must move for it
-    # is K and Q_W once; its second read of K and its outputs (row statistics, mu and sigma) are
-    # overhead of the design, and show in `traffic`.  roofline_passes gives the same view of the
-    # two passes run as separate launches.
+    # The dominant kernel is the scoring kernel of the timed pass (kv_window_base_scores with every
+    # unit one segment: both passes of a unit in one workgroup, the base scores formed in the
+    # second).  What the method must move for it is K and Q_W once; its second read of K and its
+    # outputs (row statistics and base scores) are overhead of the design, and show in
+    # `traffic`.  roofline_passes gives the same view of the two passes run as separate launches.
     def roofline(kernel, alg, kms):
         achieved = alg / (kms * 1e-3) / 1e9
         return {"kernel": kernel, "bound": "hbm", "achieved": round(achieved, 1),
@@ -526,14 +569,28 @@ def main() -> None:
         "wall_s_timed_loop": round(wall, 3),
         "cache_flush": f"{args.flush} of 512 MiB before every timed step",
         "settle": {"passes": settle_passes, "ms": round(settle_ms, 1)},
+        "pass": ("kv_window_scores + kv_mu_sigma, kv_mmr_select_compact" if args.unfused else
+                 "kv_window_mu_sigma, kv_mmr_select_compact" if mu_sigma_path else
+                 "kv_window_base_scores, kv_mmr_select_scored (compacting)"),
+        "other_path_ms": {("kv_window_base_scores" if mu_sigma_path else "kv_window_mu_sigma"):
+                          round(alt_scoring, 4),
+                          ("kv_mmr_select_scored (compacting)" if mu_sigma_path else
+                           "kv_mmr_select_compact"): round(alt_select, 4),
+                          "total": round(alt_scoring + alt_select, 4)},
         "per_layer_schedule_ms": {"total": round(lay_score + lay_rest, 4),
-                                  "scoring (32 launches of kv_window_mu_sigma)": round(lay_score, 4),
+                                  ("scoring (32 launches of kv_window_mu_sigma)" if mu_sigma_path
+                                   else "scoring (32 launches of kv_window_base_scores)"):
+                                  round(lay_score, 4),
                                   "select+compact (batched)": round(lay_rest, 4)},
         "per_kernel_ms": {("stats_stream + mu_sigma_stream (unfused)" if args.unfused else
-                           "window_stream (kv_window_mu_sigma)"): round(float(mean_part[0]), 4),
+                           "window_stream (kv_window_mu_sigma)" if mu_sigma_path else
+                           "window_stream, base-score mode (kv_window_base_scores)"):
+                          round(float(mean_part[0]), 4),
                           "stats_stream (kv_window_scores)": round(k_stats, 4),
                           "mu_sigma_stream (kv_mu_sigma)": round(k_mu, 4),
-                          "mmr_select_compact (kv_mmr_select_compact)": round(float(mean_part[1]), 4),
+                          ("mmr_select_compact (kv_mmr_select_compact)" if mu_sigma_path else
+                           "mmr_select_compact, scored (kv_mmr_select_scored)"):
+                          round(float(mean_part[1]), 4),
                           "mmr_select (kv_mmr_select)": round(k_sel, 4),
                           "compact (kv_compact_cache)": round(k_cmp, 4)},
         "options_ms": {"kv_window_mu_sigma_ex (sigma over all G*W rows)": round(v_all, 4),
@@ -556,7 +613,7 @@ def main() -> None:
     # before the interpreter exits: no device memory or event outlives the run)
     torch.cuda.synchronize()
     del all_events, layer_events
-    inp = out = None
+    inp = out = score = ws_sc = ws_lay = None
     torch.cuda.empty_cache()
     if args.cpu_baseline:
         layers = []

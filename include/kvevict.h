@@ -173,6 +173,26 @@ int kv_window_mu_sigma_ex(const kv_problem* pr, const void* q_win, const void* k
                           int32_t sigma_rows, float* row_max, float* row_sum, float* mu,
                           float* sigma, void* ws, size_t ws_bytes, void* stream);
 
+/* Window statistics and base scores in one call (section 3.1, Eq. (1), (3); section 3.2, Eq. (5)):
+ * row_max / row_sum as from kv_window_mu_sigma_ex with the same sigma_rows, and for every key i of
+ * every problem p and kv head
+ *   score[i] = fmaf(lambda1[p], sigma[i], w_mu * mu[i])   (fp32, one rounding of the fma)
+ * bit for bit what kv_window_mu_sigma_ex's mu and sigma give, without those two arrays.  score has
+ * the layout of mu (problem p at tok_off[p]*h_kv, [h_kv][L_p], fp32, 16-byte aligned).
+ * lambda1: [n_prob] fp32 device.  w_mu: finite (1 for the paper's score).
+ * For bf16 batches (w = 32, d in {64, 128}, G in {1, 2, 4}, scale > 0) the scores are formed
+ * inside the window kernel's second pass, which then writes one array instead of two; with every
+ * (problem, kv head) scored by one workgroup no workspace is needed.  Otherwise, and when the
+ * one-launch path cannot run, mu and sigma go through the workspace
+ * (kv_base_scores_workspace_bytes).  Calls that overlap on one workspace race. */
+int kv_window_base_scores(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                          const float* lambda1, float w_mu, int32_t sigma_rows, float* row_max,
+                          float* row_sum, float* score, void* ws, size_t ws_bytes, void* stream);
+
+/* Bytes of device workspace kv_window_base_scores needs for this batch with scale > 0 (0 if none;
+ * 256-byte alignment).  Returns 0 for invalid arguments as well. */
+size_t kv_base_scores_workspace_bytes(const kv_problem* pr);
+
 /* Greedy diversity-aware selection (Eq. (2), (4), (5); section 3.2), per problem p and kv head g:
  *   candidates i in [0, n_cand), n_cand = L_p - keep_tail (the last keep_tail positions are always
  *   kept and never compete);
@@ -243,6 +263,20 @@ int kv_mmr_select_compact(const kv_problem* pr, const float* mu, const float* si
                           const void* v, const float* lambda1, const float* lambda2,
                           int32_t budget, int32_t cand_mult, int32_t keep_tail, int32_t* sel_idx,
                           void* k_out, void* v_out, void* ws, size_t ws_bytes, void* stream);
+
+/* kv_mmr_select_ex, optionally followed by kv_compact_cache_ex's compaction in the same launch,
+ * with the base scores given (section 3.2, Eq. (2), (4), (5)): score as from kv_window_base_scores
+ * (16-byte aligned) takes the place of fmaf(lambda1[p], sigma, w_mu * mu), so that with the score
+ * of the same mu, sigma, lambda1 and w_mu every output equals kv_mmr_select_ex's bit for bit.
+ * opts (nullable) as in kv_mmr_select_ex, its w_mu unused.  With k_out and v_out (both or
+ * neither; v then required) the compaction is kv_mmr_select_compact's: budget <= 8192, rows of
+ * [n_prob][h_kv][budget + keep_tail][d], the first B_p rows of a block from the selection.
+ * sel_score, cand_idx, cand_corr nullable as in kv_mmr_select.  Needs no workspace. */
+int kv_mmr_select_scored(const kv_problem* pr, const float* score, const void* k, const void* v,
+                         const float* lambda2, int32_t budget, int32_t cand_mult, int32_t keep_tail,
+                         const kv_select_opts* opts, int32_t* sel_idx, float* sel_score,
+                         int32_t* cand_idx, float* cand_corr, void* k_out, void* v_out,
+                         void* stream);
 
 /* kv_compact_cache with per-problem budgets and a chosen block size (budget_host / budget_dev as
  * in kv_select_opts; both NULL with out_rows = 0 is exactly kv_compact_cache).  The block of every

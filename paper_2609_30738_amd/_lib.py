@@ -43,8 +43,9 @@ LIB_PATH = os.environ.get("KVEVICT_LIB") or os.path.join(os.path.dirname(os.path
 
 SYMBOLS = ("kv_strerror", "kv_version", "kv_workspace_bytes", "kv_candidate_stride",
            "kv_window_scores", "kv_mu_sigma", "kv_mu_sigma_ex", "kv_window_mu_sigma",
-           "kv_window_mu_sigma_ex", "kv_window_mu_sigma_noalloc", "kv_mmr_select",
-           "kv_mmr_select_ex", "kv_mmr_select_compact",
+           "kv_window_mu_sigma_ex", "kv_window_mu_sigma_noalloc", "kv_window_base_scores",
+           "kv_base_scores_workspace_bytes", "kv_mmr_select", "kv_mmr_select_ex",
+           "kv_mmr_select_compact", "kv_mmr_select_scored",
            "kv_compact_cache", "kv_compact_cache_ex", "kv_decode_workspace_bytes",
            "kv_decode_attention", "kv_pyramid_budgets", "kv_depth_profile")
 
@@ -101,6 +102,12 @@ def lib() -> ctypes.CDLL:
                                             sz, vp]
         h.kv_window_mu_sigma_noalloc.argtypes = [pr, vp, vp, ctypes.c_float, i32, vp, vp, vp, vp,
                                                  vp]
+        h.kv_window_base_scores.argtypes = [pr, vp, vp, ctypes.c_float, vp, ctypes.c_float, i32,
+                                            vp, vp, vp, vp, sz, vp]
+        h.kv_base_scores_workspace_bytes.argtypes = [pr]
+        h.kv_base_scores_workspace_bytes.restype = sz
+        h.kv_mmr_select_scored.argtypes = [pr, vp, vp, vp, vp, i32, i32, i32,
+                                           ctypes.POINTER(KvSelectOpts), vp, vp, vp, vp, vp, vp, vp]
         h.kv_mmr_select.argtypes = [pr, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, sz,
                                     vp]
         h.kv_mmr_select_compact.argtypes = [pr, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp,
@@ -117,8 +124,9 @@ def lib() -> ctypes.CDLL:
         h.kv_depth_profile.argtypes = [i32, ctypes.POINTER(ctypes.c_double), i32, i32,
                                        ctypes.POINTER(ctypes.c_float)]
         for name in ("kv_window_scores", "kv_mu_sigma", "kv_mu_sigma_ex", "kv_window_mu_sigma",
-                     "kv_window_mu_sigma_ex", "kv_window_mu_sigma_noalloc", "kv_mmr_select",
-                     "kv_mmr_select_ex",
+                     "kv_window_mu_sigma_ex", "kv_window_mu_sigma_noalloc",
+                     "kv_window_base_scores", "kv_mmr_select", "kv_mmr_select_ex",
+                     "kv_mmr_select_scored",
                      "kv_compact_cache", "kv_compact_cache_ex", "kv_decode_attention",
                      "kv_pyramid_budgets", "kv_depth_profile"):
             getattr(h, name).restype = ctypes.c_int
@@ -275,6 +283,41 @@ def window_mu_sigma_noalloc(batch: Batch, q_win, k, scale: float, row_max, row_s
                                             _stream(stream)), "kv_window_mu_sigma_noalloc")
 
 
+def base_scores_workspace_bytes(batch: Batch) -> int:
+    return int(lib().kv_base_scores_workspace_bytes(batch.ref()))
+
+
+def window_base_scores(batch: Batch, q_win, k, scale: float, lambda1, row_max, row_sum, score,
+                       w_mu: float = 1.0, sigma_rows="group_mean", ws=None, stream=None) -> None:
+    """kv_window_base_scores."""
+    _check(lib().kv_window_base_scores(batch.ref(), _ptr(q_win), _ptr(k), float(scale),
+                                       _ptr(lambda1), float(w_mu), _sigma_rows(sigma_rows),
+                                       _ptr(row_max), _ptr(row_sum), _ptr(score), _ptr(ws),
+                                       0 if ws is None else ws.numel() * ws.element_size(),
+                                       _stream(stream)), "kv_window_base_scores")
+
+
+def _select_opts(pool, w_mu, budgets):
+    if pool is None and w_mu is None and budgets is None:
+        return None
+    bh, bd = budgets.pointers() if budgets is not None else (None, None)
+    return ctypes.byref(KvSelectOpts(1 if pool is None else int(pool),
+                                     1.0 if w_mu is None else float(w_mu), bh, bd))
+
+
+def mmr_select_scored(batch: Batch, score, k, v, lambda2, budget: int, cand_mult: int,
+                      keep_tail: int, sel_idx, sel_score=None, cand_idx=None, cand_corr=None,
+                      k_out=None, v_out=None, pool: Optional[int] = None,
+                      budgets: Optional[Budgets] = None, stream=None) -> None:
+    """kv_mmr_select_scored; with k_out / v_out the compaction runs in the same launch."""
+    _check(lib().kv_mmr_select_scored(batch.ref(), _ptr(score), _ptr(k), _ptr(v), _ptr(lambda2),
+                                      int(budget), int(cand_mult),
+                                      int(keep_tail), _select_opts(pool, None, budgets),
+                                      _ptr(sel_idx), _ptr(sel_score), _ptr(cand_idx),
+                                      _ptr(cand_corr), _ptr(k_out), _ptr(v_out),
+                                      _stream(stream)), "kv_mmr_select_scored")
+
+
 def mmr_select(batch: Batch, mu, sigma, k, lambda1, lambda2, budget: int, cand_mult: int,
                keep_tail: int, sel_idx, sel_score=None, cand_idx=None, cand_corr=None, ws=None,
                stream=None) -> None:
@@ -301,11 +344,7 @@ def mmr_select_ex(batch: Batch, mu, sigma, k, lambda1, lambda2, budget: int, can
                   budgets: Optional[Budgets] = None, stream=None) -> None:
     """kv_mmr_select_ex; options are passed as NULL when pool, w_mu and budgets are all None.
     With `budgets`, `budget` is the row stride of sel_idx / sel_score."""
-    opts = None
-    if pool is not None or w_mu is not None or budgets is not None:
-        bh, bd = budgets.pointers() if budgets is not None else (None, None)
-        opts = ctypes.byref(KvSelectOpts(1 if pool is None else int(pool),
-                                         1.0 if w_mu is None else float(w_mu), bh, bd))
+    opts = _select_opts(pool, w_mu, budgets)
     _check(lib().kv_mmr_select_ex(batch.ref(), _ptr(mu), _ptr(sigma), _ptr(k), _ptr(lambda1),
                                   _ptr(lambda2), int(budget), int(cand_mult), int(keep_tail), opts,
                                   _ptr(sel_idx), _ptr(sel_score), _ptr(cand_idx),

@@ -125,16 +125,40 @@ size_t window_ws_bytes(const kv_problem* pr, const kv::Shape& s) {
   return align_up(b);
 }
 
-// Selection, and with k_out / v_out the compaction of the selected rows, in one launch.
-int mmr_select_impl(const kv_problem* pr, const float* mu, const float* sigma, const void* k,
-                    const void* v, const float* lambda1, const float* lambda2, int32_t budget,
+// Tokens of the batch: sum_p L_p (the rows of mu, sigma and the scores per kv head).
+int64_t total_tokens(const kv_problem* pr) {
+  int64_t t = 0;
+  for (int p = 0; p < pr->n_prob; ++p) t += pr->len_host[p];
+  return t;
+}
+
+// Whether kv_window_base_scores forms the scores inside the window kernel's second pass (bf16
+// streaming shapes with every unit one segment), or from mu / sigma in the workspace.
+bool scores_in_window_pass(const kv_problem* pr, const kv::Shape& s, float scale) {
+  return kv::stream_shape_ok(s, scale) && stream_plan_of(pr, s).max_segs == 1;
+}
+
+// Workspace of kv_window_base_scores: none for the fused path (with fused_ok, for a positive
+// scale), else the window paths' part and rows of mu and sigma.
+size_t base_scores_ws_bytes(const kv_problem* pr, const kv::Shape& s, bool fused_ok = true) {
+  if (fused_ok && scores_in_window_pass(pr, s, 1.f)) return 0;
+  const size_t keys = (size_t)total_tokens(pr) * pr->h_kv;
+  return window_ws_bytes(pr, s) + 2 * align_up(keys * sizeof(float));
+}
+
+// Selection, and with k_out / v_out the compaction of the selected rows, in one launch; base
+// scores from mu / sigma, or given (score).
+int mmr_select_impl(const kv_problem* pr, const float* mu, const float* sigma, const float* score,
+                    const void* k, const void* v,
+                    const float* lambda1, const float* lambda2, int32_t budget,
                     int32_t cand_mult, int32_t keep_tail, const kv_select_opts* opts,
                     int32_t* sel_idx, float* sel_score, int32_t* cand_idx, float* cand_corr,
                     void* k_out, void* v_out, void* stream) {
   kv::Shape s;
   int st = check_problem(pr, &s);
   if (st != KV_OK) return st;
-  if (!mu || !sigma || !k || !lambda1 || !lambda2 || !sel_idx) return KV_ERR_NULL;
+  if (!score && (!mu || !sigma || !lambda1)) return KV_ERR_NULL;
+  if (!k || !lambda2 || !sel_idx) return KV_ERR_NULL;
   if (!aligned16(k)) return KV_ERR_ARG;
   if (k_out && (!aligned16(v) || !aligned16(k_out) || !aligned16(v_out))) return KV_ERR_ARG;
   // the kernels form cand_mult * B_p in 32-bit arithmetic (B_p <= budget)
@@ -154,6 +178,7 @@ int mmr_select_impl(const kv_problem* pr, const float* mu, const float* sigma, c
   kv::SelectArgs a;
   a.mu = mu;
   a.sigma = sigma;
+  a.score = score;
   a.k = k;
   a.lambda1 = lambda1;
   a.lambda2 = lambda2;
@@ -334,6 +359,52 @@ int kv_window_mu_sigma_noalloc(const kv_problem* pr, const void* q_win, const vo
                                kv::kNoAllocScratchBytes, stream);
 }
 
+size_t kv_base_scores_workspace_bytes(const kv_problem* pr) {
+  kv::Shape s;
+  if (check_problem(pr, &s) != KV_OK) return 0;
+  return base_scores_ws_bytes(pr, s);
+}
+
+int kv_window_base_scores(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                          const float* lambda1, float w_mu, int32_t sigma_rows, float* row_max,
+                          float* row_sum, float* score, void* ws, size_t ws_bytes, void* stream) {
+  kv::Shape s;
+  int st = check_problem(pr, &s);
+  if (st != KV_OK) return st;
+  if (!q_win || !k || !lambda1 || !row_max || !row_sum || !score) return KV_ERR_NULL;
+  if (!aligned16(q_win) || !aligned16(k) || !aligned16(score)) return KV_ERR_ARG;
+  if (!std::isfinite(scale) || !std::isfinite(w_mu)) return KV_ERR_ARG;
+  if (sigma_rows != KV_SIGMA_GROUP_MEAN && sigma_rows != KV_SIGMA_ALL_ROWS) return KV_ERR_ARG;
+  const bool fused = scores_in_window_pass(pr, s, scale);
+  const size_t need = fused ? 0 : base_scores_ws_bytes(pr, s, false);
+  if (need > 0 && (ws_bytes < need || !ws || (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1))))
+    return KV_ERR_WORKSPACE;
+  const bool all = sigma_rows == KV_SIGMA_ALL_ROWS;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (fused)
+    return launch_status(kv::launch_stream_window_scores(s, stream_plan_of(pr, s), q_win, k, scale,
+                                                         lambda1, w_mu, row_max, row_sum, score,
+                                                         all, hs));
+  const size_t win = window_ws_bytes(pr, s);
+  if (kv::stream_shape_ok(s, scale)) {
+    // several segments per unit: the one-launch path in base-score mode when the grid fits
+    const kv::ScoreMode sm{score, lambda1, w_mu};
+    bool launched = false;
+    st = launch_status(kv::launch_stream_window_coop(s, stream_plan_of(pr, s), q_win, k, scale, ws,
+                                                     row_max, row_sum, nullptr, nullptr, all,
+                                                     spin_limit(), hs, &launched, &sm));
+    if (st != KV_OK || launched) return st;
+  }
+  // mu / sigma into the workspace after the window paths' own part, then the scores from them
+  const size_t keys = (size_t)total_tokens(pr) * pr->h_kv;
+  float* mu = reinterpret_cast<float*>(static_cast<char*>(ws) + win);
+  float* sigma = reinterpret_cast<float*>(static_cast<char*>(ws) + win + align_up(keys * sizeof(float)));
+  st = kv_window_mu_sigma_ex(pr, q_win, k, scale, sigma_rows, row_max, row_sum, mu, sigma, ws, win,
+                             stream);
+  if (st != KV_OK) return st;
+  return launch_status(kv::launch_base_scores(s, mu, sigma, lambda1, w_mu, score, hs));
+}
+
 int kv_mmr_select(const kv_problem* pr, const float* mu, const float* sigma, const void* k,
                   const float* lambda1, const float* lambda2, int32_t budget, int32_t cand_mult,
                   int32_t keep_tail, int32_t* sel_idx, float* sel_score, int32_t* cand_idx,
@@ -349,8 +420,9 @@ int kv_mmr_select_ex(const kv_problem* pr, const float* mu, const float* sigma, 
                      size_t ws_bytes, void* stream) {
   (void)ws;
   (void)ws_bytes;
-  return mmr_select_impl(pr, mu, sigma, k, nullptr, lambda1, lambda2, budget, cand_mult, keep_tail,
-                         opts, sel_idx, sel_score, cand_idx, cand_corr, nullptr, nullptr, stream);
+  return mmr_select_impl(pr, mu, sigma, nullptr, k, nullptr, lambda1, lambda2, budget, cand_mult,
+                         keep_tail, opts, sel_idx, sel_score, cand_idx, cand_corr, nullptr, nullptr,
+                         stream);
 }
 
 int kv_mmr_select_compact(const kv_problem* pr, const float* mu, const float* sigma, const void* k,
@@ -360,8 +432,23 @@ int kv_mmr_select_compact(const kv_problem* pr, const float* mu, const float* si
   (void)ws;
   (void)ws_bytes;
   if (!v || !k_out || !v_out) return KV_ERR_NULL;
-  return mmr_select_impl(pr, mu, sigma, k, v, lambda1, lambda2, budget, cand_mult, keep_tail,
-                         nullptr, sel_idx, nullptr, nullptr, nullptr, k_out, v_out, stream);
+  return mmr_select_impl(pr, mu, sigma, nullptr, k, v, lambda1, lambda2, budget, cand_mult,
+                         keep_tail, nullptr, sel_idx, nullptr, nullptr, nullptr, k_out, v_out,
+                         stream);
+}
+
+int kv_mmr_select_scored(const kv_problem* pr, const float* score, const void* k, const void* v,
+                         const float* lambda2, int32_t budget,
+                         int32_t cand_mult, int32_t keep_tail, const kv_select_opts* opts,
+                         int32_t* sel_idx, float* sel_score, int32_t* cand_idx, float* cand_corr,
+                         void* k_out, void* v_out, void* stream) {
+  if (!score) return KV_ERR_NULL;
+  if (!aligned16(score)) return KV_ERR_ARG;
+  if ((k_out != nullptr) != (v_out != nullptr)) return KV_ERR_NULL;
+  if (k_out && !v) return KV_ERR_NULL;
+  return mmr_select_impl(pr, nullptr, nullptr, score, k, v, nullptr, lambda2, budget, cand_mult,
+                         keep_tail, opts, sel_idx, sel_score, cand_idx, cand_corr, k_out, v_out,
+                         stream);
 }
 
 int kv_compact_cache(const kv_problem* pr, const void* k, const void* v, const int32_t* sel_idx,

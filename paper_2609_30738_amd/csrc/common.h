@@ -92,6 +92,27 @@ __device__ __forceinline__ f32x16_t mfma_tile(const Frags<DT, D>& a, const Frags
   return acc;
 }
 
+// Order-preserving 32-bit key of a float: a larger key means a larger value (-0 below +0; NaNs
+// with the sign bit clear above +inf, with it set below -inf).
+__device__ __forceinline__ uint32_t order_key(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Add one to hist[digit] (LDS) for every active lane.  The digit of the first active lane is
+// counted with one ballot and a single LDS add (the common case: most scores share their leading
+// digits); lanes with other digits use LDS atomics, which handle scattered digits without
+// conflicts.  Every lane of the wave must call it.
+__device__ __forceinline__ void wave_hist_add(uint32_t* hist, uint32_t digit, bool active) {
+  const uint64_t act = __ballot(active);
+  if (act == 0) return;
+  const int leader = __ffsll((unsigned long long)act) - 1;
+  const uint32_t dl = __builtin_amdgcn_readlane(digit, leader);
+  const uint64_t same = __ballot(active && digit == dl);
+  if ((int)(threadIdx.x & 63) == leader) atomicAdd(&hist[dl], (uint32_t)__popcll(same));
+  if (active && digit != dl) atomicAdd(&hist[digit], 1u);
+}
+
 // Value of the lane l ^ 32 (the other K-half / the other 16 accumulator rows).
 __device__ __forceinline__ float swap_halves(float x) {
   return __shfl_xor(x, 32, 64);

@@ -66,14 +66,31 @@ hipError_t launch_stream_mu_sigma(const Shape& s, const StreamPlan& plan, const 
 hipError_t launch_stream_window(const Shape& s, const StreamPlan& plan, const void* q_win,
                                 const void* k, float scale, float* row_max, float* row_sum,
                                 float* mu, float* sigma, bool sigma_all, hipStream_t stream);
+// Both passes in one launch, every unit one segment, in base-score mode: row_max / row_sum, and
+// per key s = fma(lambda1[p], sigma, w_mu mu) into score instead of mu / sigma.
+hipError_t launch_stream_window_scores(const Shape& s, const StreamPlan& plan, const void* q_win,
+                                       const void* k, float scale, const float* lambda1,
+                                       float w_mu, float* row_max, float* row_sum, float* score,
+                                       bool sigma_all, hipStream_t stream);
+// Base scores s = fma(lambda1[p], sigma, w_mu mu) of every key from mu / sigma rows (for batches
+// that take the other window paths).
+hipError_t launch_base_scores(const Shape& s, const float* mu, const float* sigma,
+                              const float* lambda1, float w_mu, float* score, hipStream_t stream);
 // Both passes in one launch when units span several segments: partials and per-unit arrival
 // counters in ws; a workgroup polls at most spin_limit times for its unit's other segments before
 // it computes their partials itself.  Sets *launched = false (and launches nothing) if the grid
 // does not fit the chip at once; the caller then takes the two-launch path.
+// With sm (base-score mode) the second pass stores scores instead of mu / sigma.
+struct ScoreMode {
+  float* score;
+  const float* lambda1;
+  float w_mu;
+};
 hipError_t launch_stream_window_coop(const Shape& s, const StreamPlan& plan, const void* q_win,
                                      const void* k, float scale, void* ws, float* row_max,
                                      float* row_sum, float* mu, float* sigma, bool sigma_all,
-                                     uint32_t spin_limit, hipStream_t stream, bool* launched);
+                                     uint32_t spin_limit, hipStream_t stream, bool* launched,
+                                     const ScoreMode* sm = nullptr);
 constexpr uint32_t kDefaultSpinLimit = 4096;  // polls (each a device-coherent load and a short sleep)
 // row_max / row_sum from chunk partials [n_units][max_chunks][rows_pad] of chunk_keys keys each.
 hipError_t launch_combine_partials(const Shape& s, const void* part, int chunk_keys,
@@ -83,6 +100,8 @@ hipError_t launch_combine_partials(const Shape& s, const void* part, int chunk_k
 struct SelectArgs {
   const float* mu;
   const float* sigma;
+  // base scores given instead of mu / sigma (then lambda1 and w_mu are unused)
+  const float* score = nullptr;
   const void* k;
   const float* lambda1;
   const float* lambda2;

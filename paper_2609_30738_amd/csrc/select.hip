@@ -47,24 +47,6 @@ constexpr int kGramSlots = kGramMaxCand / 64;
 __host__ __device__ constexpr size_t tri_entries(int c) { return (size_t)c * (c + 1) / 2; }
 __device__ __forceinline__ int tri_index(int i, int j, int c) { return (i * (2 * c - i + 1)) / 2 + (j - i); }
 
-__device__ __forceinline__ uint32_t order_key(float x) {
-  const uint32_t u = __float_as_uint(x);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
-// Add one to hist[digit] for every active lane.  The digit of the first active lane is counted
-// with one ballot and a single LDS add (the common case: most scores share their leading digits);
-// lanes with other digits use LDS atomics, which handle scattered digits without conflicts.
-__device__ __forceinline__ void wave_hist_add(uint32_t* hist, uint32_t digit, bool active) {
-  const uint64_t act = __ballot(active);
-  if (act == 0) return;
-  const int leader = __ffsll((unsigned long long)act) - 1;
-  const uint32_t dl = __builtin_amdgcn_readlane(digit, leader);
-  const uint64_t same = __ballot(active && digit == dl);
-  if ((int)(threadIdx.x & 63) == leader) atomicAdd(&hist[dl], (uint32_t)__popcll(same));
-  if (active && digit != dl) atomicAdd(&hist[digit], 1u);
-}
-
 // (score, slot) packed so that a larger value means a larger score, then a lower slot.
 __device__ __forceinline__ uint64_t pack_best(float score, int slot) {
   return ((uint64_t)order_key(score) << 32) | (uint32_t)(0x7FFFFFFF - slot);
@@ -247,6 +229,7 @@ __device__ __forceinline__ void bitonic_sort(V* v, int n2, int tid, int nt) {
 }
 
 constexpr int kFastBins = 2048;  // 11-bit digit
+constexpr int kFastShift = 21;
 constexpr int kListCap = 1024;   // members of the cut's bin ranked exactly
 
 // The candidate positions (C of the n_cand staged keys, the largest keys, ties to the lower
@@ -272,7 +255,7 @@ __device__ bool fast_candidates(SelectShared<NW>& sh, const uint32_t* skeys, int
       kk[q] = i < n_cand ? skeys[i] : 0u;
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) wave_hist_add(h, kk[q] >> 21, i0 + q * NT + tid < n_cand);
+    for (int q = 0; q < 4; ++q) wave_hist_add(h, kk[q] >> kFastShift, i0 + q * NT + tid < n_cand);
   }
   __syncthreads();
   // suffix sums over the bins (larger bins = larger keys): thread t owns bins 2t, 2t + 1
@@ -317,9 +300,9 @@ __device__ bool fast_candidates(SelectShared<NW>& sh, const uint32_t* skeys, int
     for (int q = 0; q < 4; ++q) {
       const int i = i0 + q * NT + tid;
       const bool in = i < n_cand;
-      wave_append(in && (kk[q] >> 21) > bin, &sh.wave_cnt[0][0], lane,
+      wave_append(in && (kk[q] >> kFastShift) > bin, &sh.wave_cnt[0][0], lane,
                   [&](uint32_t slot) { cpos[slot] = i; });
-      wave_append(in && (kk[q] >> 21) == bin, &sh.wave_cnt[0][1], lane,
+      wave_append(in && (kk[q] >> kFastShift) == bin, &sh.wave_cnt[0][1], lane,
                   [&](uint32_t slot) { list[slot] = ((uint64_t)(~kk[q]) << 32) | (uint32_t)i; });
     }
   }
@@ -382,6 +365,7 @@ struct CompactOut {
 template <int DT, int D, int NT, int CPT, bool STAGED, bool GRAM>
 __global__ __launch_bounds__(NT) void mmr_select_kernel(
     const float* __restrict__ mu, const float* __restrict__ sigma,
+    const float* __restrict__ score,
     const typename Elem<DT>::T* __restrict__ k, const int32_t* __restrict__ lens,
     const int64_t* __restrict__ tok_off, const float* __restrict__ lambda1,
     const float* __restrict__ lambda2, int pool_h, float w_mu, int h_kv, int budget,
@@ -405,8 +389,13 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
   const size_t base = (size_t)tok_off[p] * h_kv + (size_t)g * L;
   const float* mu_g = mu + base;
   const float* sg_g = sigma + base;
+  const float lam1 = lambda1 ? lambda1[p] : 0.f, lam2 = lambda2[p];  // no lambda1 with scores given
+  const float* sc_g = score ? score + base : nullptr;  // base scores given: mu / sigma unused
+  // base score of candidate position i
+  auto base_score = [&](int i) -> float {
+    return sc_g ? sc_g[i] : fmaf(lam1, sg_g[i], w_mu * mu_g[i]);
+  };
   const T* kg = k + base * D;
-  const float lam1 = lambda1[p], lam2 = lambda2[p];
   int32_t* cpos = reinterpret_cast<int32_t*>(dyn);
   float* cinv = reinterpret_cast<float*>(dyn + (size_t)max_cand * 4);
   float* cst = reinterpret_cast<float*>(dyn + (size_t)max_cand * 8);
@@ -415,41 +404,51 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
   T* ckeys = reinterpret_cast<T*>(region);
   const bool take_all = (C >= n_cand);
 
-  // ---- 0. base scores s_i = mu_i + lambda1 sigma_i (one rounding) and their maximum -----------
+  // ---- 0. base scores s_i = mu_i + lambda1 sigma_i (one rounding, or given) and their maximum -
   float local_max = -INFINITY;
   if constexpr (STAGED) {
-    // mu / sigma rows start at a multiple of 4 floats only if base is; stage element-wise until
-    // the first aligned index, then 4 per lane with several loads in flight
+    // the rows start at a multiple of 4 floats only if base is; stage element-wise until the
+    // first aligned index, then 4 per lane with several loads in flight
     const int head = (int)((4 - (base & 3)) & 3) < n_cand ? (int)((4 - (base & 3)) & 3) : n_cand;
     if (tid < head) {
-      const float sv = fmaf(lam1, sg_g[tid], w_mu * mu_g[tid]);
+      const float sv = base_score(tid);
       local_max = fmaxf(local_max, sv);
       skeys[tid] = order_key(sv);
     }
     const int n4 = (n_cand - head) / 4;
-    const float4* mu4 = reinterpret_cast<const float4*>(mu_g + head);
-    const float4* sg4 = reinterpret_cast<const float4*>(sg_g + head);
-#pragma unroll 4
-    for (int v = tid; v < n4; v += kThreads) {
-      const float4 m = mu4[v], sgv = sg4[v];
-      const float s0 = fmaf(lam1, sgv.x, w_mu * m.x), s1 = fmaf(lam1, sgv.y, w_mu * m.y);
-      const float s2 = fmaf(lam1, sgv.z, w_mu * m.z), s3 = fmaf(lam1, sgv.w, w_mu * m.w);
+    auto stage4 = [&](int v, float s0, float s1, float s2, float s3) {
       local_max = fmaxf(fmaxf(local_max, fmaxf(s0, s1)), fmaxf(s2, s3));
       const int i = head + 4 * v;
       skeys[i] = order_key(s0);
       skeys[i + 1] = order_key(s1);
       skeys[i + 2] = order_key(s2);
       skeys[i + 3] = order_key(s3);
+    };
+    if (sc_g) {
+      const float4* sc4 = reinterpret_cast<const float4*>(sc_g + head);
+#pragma unroll 4
+      for (int v = tid; v < n4; v += kThreads) {
+        const float4 sv = sc4[v];
+        stage4(v, sv.x, sv.y, sv.z, sv.w);
+      }
+    } else {
+      const float4* mu4 = reinterpret_cast<const float4*>(mu_g + head);
+      const float4* sg4 = reinterpret_cast<const float4*>(sg_g + head);
+#pragma unroll 4
+      for (int v = tid; v < n4; v += kThreads) {
+        const float4 m = mu4[v], sgv = sg4[v];
+        stage4(v, fmaf(lam1, sgv.x, w_mu * m.x), fmaf(lam1, sgv.y, w_mu * m.y),
+               fmaf(lam1, sgv.z, w_mu * m.z), fmaf(lam1, sgv.w, w_mu * m.w));
+      }
     }
     for (int i = head + 4 * n4 + tid; i < n_cand; i += kThreads) {
-      const float sv = fmaf(lam1, sg_g[i], w_mu * mu_g[i]);
+      const float sv = base_score(i);
       local_max = fmaxf(local_max, sv);
       skeys[i] = order_key(sv);
     }
     __syncthreads();
   } else {
-    for (int i = tid; i < n_cand; i += kThreads)
-      local_max = fmaxf(local_max, fmaf(lam1, sg_g[i], w_mu * mu_g[i]));
+    for (int i = tid; i < n_cand; i += kThreads) local_max = fmaxf(local_max, base_score(i));
   }
   // Max-pooling keeps the largest score of the window, whose key is also the largest key.
   if constexpr (STAGED) {
@@ -489,11 +488,10 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
     if constexpr (STAGED) {
       return skeys[i];
     } else {
-      uint32_t kmax = order_key(fmaf(lam1, sg_g[i], w_mu * mu_g[i]));
+      uint32_t kmax = order_key(base_score(i));
       if (pool_h > 0) {
         const int j1 = min(n_cand - 1, i + pool_h);
-        for (int j = max(0, i - pool_h); j <= j1; ++j)
-          kmax = max(kmax, order_key(fmaf(lam1, sg_g[j], w_mu * mu_g[j])));
+        for (int j = max(0, i - pool_h); j <= j1; ++j) kmax = max(kmax, order_key(base_score(j)));
       }
       return kmax;
     }
@@ -646,9 +644,9 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
     // s~ of every candidate (its base score, pooled as in phase 0, over the normaliser)
     for (int c = tid; c < C; c += kThreads) {
       const int pos = cpos[c];
-      float sv = fmaf(lam1, sg_g[pos], w_mu * mu_g[pos]);
+      float sv = base_score(pos);
       for (int j = max(0, pos - pool_h); j <= min(n_cand - 1, pos + pool_h); ++j)
-        sv = fmaxf(sv, fmaf(lam1, sg_g[j], w_mu * mu_g[j]));
+        sv = fmaxf(sv, base_score(j));
       cst[c] = sv / den;
     }
     // Dot products of every pair of candidate keys, k_i . k_j, in 32 x 32 blocks (I, J), I <= J
@@ -839,9 +837,9 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
         const float n2 = key[q].sq_norm();
         inv[q] = n2 > 0.f ? 1.f / sqrtf(n2) : 0.f;  // a zero key has cosine 0 to everything
         cinv[c] = inv[q];
-        float sv = fmaf(lam1, sg_g[pos], w_mu * mu_g[pos]);
+        float sv = base_score(pos);
         for (int j = max(0, pos - pool_h); j <= min(n_cand - 1, pos + pool_h); ++j)
-          sv = fmaxf(sv, fmaf(lam1, sg_g[j], w_mu * mu_g[j]));
+          sv = fmaxf(sv, base_score(j));
         st[q] = sv / den;
       }
     }
@@ -994,7 +992,8 @@ hipError_t select_launch(const Shape& s, const SelectArgs& a, size_t body, hipSt
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
   if (e != hipSuccess) return e;
   kern<<<dim3((unsigned)(s.n_prob * s.h_kv)), NT, dyn, st>>>(
-      a.mu, a.sigma, static_cast<const T*>(a.k), s.lens, s.tok_off, a.lambda1, a.lambda2,
+      a.mu, a.sigma, a.score, static_cast<const T*>(a.k), s.lens, s.tok_off,
+      a.lambda1, a.lambda2,
       a.pool / 2, a.w_mu, s.h_kv,
       a.budget, a.budgets, a.cand_mult, a.keep_tail, a.cand_stride, a.max_cand, a.sel_idx, a.sel_score,
       a.cand_idx, a.cand_corr,

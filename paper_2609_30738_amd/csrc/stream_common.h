@@ -63,6 +63,11 @@ struct StreamArgs {
   float* mu;
   float* sigma;
   int sigma_all;          // pass 2: dispersion over all G x 32 (head, row) values
+  // base-score mode of pass 2: s = fma(lambda1[p], sigma, w_mu mu) per key into `score` instead
+  // of mu / sigma
+  float* score;
+  const float* lambda1;
+  float w_mu;
 };
 
 template <int D, int NB> struct SGeo {

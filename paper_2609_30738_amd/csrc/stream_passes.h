@@ -97,17 +97,34 @@ __device__ __forceinline__ float2 merge_waves(const float2* red, int row) {
   return v;
 }
 
+// One mu or sigma value to HBM with the device-scope store policy (sc1).  These 128-byte pieces
+// trickle out between the key loads of a stream that keeps HBM busy; on MI355X the default policy
+// costs about 0.03 ms more per 2 GiB pass (the values are the same).  The store is counted by the
+// explicit vmcnt waits of the key stream like any other vector memory operation.
+__device__ __forceinline__ void store_stat(float* dst, float v) {
+  asm volatile("global_store_dword %0, %1, off sc1" ::"v"(dst), "v"(v) : "memory");
+}
+
+// Output of pass 2 in base-score mode: the unit's score row and the base-score parameters.
+struct ScoreOut {
+  float* score_u;
+  float lam1, w_mu;
+};
+
 // Pass 2 over the wave's tiles of a segment: logits again with keys as the MFMA N dimension (a
 // lane holds one key), a = 2^(t - b) with the row normalisers b = M + log2 Z read from bsh, summed
 // over the group's heads, then the mean and the two-pass sample variance over the 32 window rows,
 // stored as mu / sigma (mu_u, sigma_u: the unit's rows).  With ALL the variance runs over all
 // G x 32 (head, row) values: every head's mean and squared deviations over its 32 rows, merged
-// across heads with the pairwise update of Chan, Golub and LeVeque.
-template <int D, int NB, bool ALL, int NW, int S>
+// across heads with the pairwise update of Chan, Golub and LeVeque.  With SC the key's base score
+// s = fma(lam1, sigma, w_mu mu) (section 3.2, Eq. (5)) is stored instead, with the same rounding
+// as a score formed later from the stored mu and sigma.
+template <int D, int NB, bool ALL, int NW, int S, bool SC = false>
 __device__ __forceinline__ void mu_sigma_tiles(const KeyStream<D, NB, NW, S>& ks,
                                                const bf16x8_t (&q)[NB][D / 16], const float* bsh,
                                                int my_tiles, int k1, int L, float c, float inv_g,
-                                               float* mu_u, float* sigma_u, int l32, int half) {
+                                               float* mu_u, float* sigma_u, int l32, int half,
+                                               ScoreOut so = {}) {
   constexpr int NS = D / 16;
   auto tile = [&](const bf16x8_t (&kt)[NS], int t0, auto masked) __attribute__((always_inline)) {
     const int key = t0 + l32;
@@ -173,7 +190,13 @@ __device__ __forceinline__ void mu_sigma_tiles(const KeyStream<D, NB, NW, S>& ks
       }
       var = sum_halves((vp[0] + vp[1]) + (vp[2] + vp[3])) * (1.f / 31.f);
     }
-    if (key < k1) (half == 0 ? mu_u : sigma_u)[key] = half == 0 ? mean : __builtin_amdgcn_sqrtf(var);
+    if constexpr (SC) {
+      // both halves hold the key's mean and variance; half 0 stores
+      const float sv = fmaf(so.lam1, __builtin_amdgcn_sqrtf(var), so.w_mu * mean);
+      if (half == 0 && key < k1) store_stat(so.score_u + key, sv);
+    } else {
+      if (key < k1) store_stat((half == 0 ? mu_u : sigma_u) + key, half == 0 ? mean : __builtin_amdgcn_sqrtf(var));
+    }
   };
 
   for (int j = 0; j < my_tiles; ++j) {

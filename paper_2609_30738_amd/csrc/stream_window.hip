@@ -3,13 +3,17 @@
 // row statistics are complete when its own pass 1 ends, so its pass 2 follows at once, with the
 // queries still in registers and the first key tiles of pass 2 loaded while the waves' statistics
 // are merged; no workgroup waits for any other.  The per-segment loops are in stream_passes.h.
+//
+// In base-score mode (SC) pass 2 keeps mu and sigma in registers and stores only each key's base
+// score (section 3.2, Eq. (5)): half the bytes, which trickle out between the key loads of a
+// stream that keeps HBM busy, and the selection reads one array instead of two.
 #include "stream_passes.h"
 
 namespace kv {
 namespace stream {
 namespace {
 
-template <int D, int NB, bool ALL, int NW, int S>
+template <int D, int NB, bool ALL, int NW, int S, bool SC>
 __global__ __launch_bounds__(NW * 64, 1) void window_stream_kernel(StreamArgs a) {
   using Gm = SGeo<D, NB>;
   constexpr int R = Gm::R, NS = Gm::NS;
@@ -48,8 +52,14 @@ __global__ __launch_bounds__(NW * 64, 1) void window_stream_kernel(StreamArgs a)
     bsh[threadIdx.x] = v.x + __builtin_log2f(v.y);  // b = M + log2 Z, base 2
   }
   __syncthreads();
-  mu_sigma_tiles<D, NB, ALL, NW, S>(ks, q, bsh, my_tiles, L, L, c, inv_g, a.mu + stat_base,
-                                    a.sigma + stat_base, l32, half);
+  if constexpr (SC) {
+    const ScoreOut so{a.score + stat_base, a.lambda1[p], a.w_mu};
+    mu_sigma_tiles<D, NB, ALL, NW, S, true>(ks, q, bsh, my_tiles, L, L, c, inv_g, nullptr, nullptr,
+                                            l32, half, so);
+  } else {
+    mu_sigma_tiles<D, NB, ALL, NW, S>(ks, q, bsh, my_tiles, L, L, c, inv_g, a.mu + stat_base,
+                                      a.sigma + stat_base, l32, half);
+  }
   wait_vmem<0>();  // no load into the ring may outlive the workgroup
   // the row statistics, merged again from the same entries in the same order
   if (threadIdx.x < R) {
@@ -63,8 +73,13 @@ __global__ __launch_bounds__(NW * 64, 1) void window_stream_kernel(StreamArgs a)
 template <int D, int NB> struct WindowLaunch {
   static hipError_t run(const Shape& s, const StreamArgs& args, hipStream_t st) {
     const dim3 grid(1, s.h_kv, s.n_prob);
-    if (args.sigma_all) window_stream_kernel<D, NB, true, kWaves, 2><<<grid, kThreads, 0, st>>>(args);
-    else window_stream_kernel<D, NB, false, kWaves, 2><<<grid, kThreads, 0, st>>>(args);
+    if (args.score) {
+      if (args.sigma_all) window_stream_kernel<D, NB, true, kWaves, 2, true><<<grid, kThreads, 0, st>>>(args);
+      else window_stream_kernel<D, NB, false, kWaves, 2, true><<<grid, kThreads, 0, st>>>(args);
+    } else {
+      if (args.sigma_all) window_stream_kernel<D, NB, true, kWaves, 2, false><<<grid, kThreads, 0, st>>>(args);
+      else window_stream_kernel<D, NB, false, kWaves, 2, false><<<grid, kThreads, 0, st>>>(args);
+    }
     return hipGetLastError();
   }
 };
@@ -82,6 +97,21 @@ hipError_t launch_stream_window(const Shape& s, const StreamPlan& plan, const vo
   a.mu = mu;
   a.sigma = sigma;
   a.sigma_all = sigma_all ? 1 : 0;
+  return stream::launch_for_shape<stream::WindowLaunch>(s, a, stream);
+}
+
+hipError_t launch_stream_window_scores(const Shape& s, const StreamPlan& plan, const void* q_win,
+                                       const void* k, float scale, const float* lambda1,
+                                       float w_mu, float* row_max, float* row_sum, float* score,
+                                       bool sigma_all, hipStream_t stream) {
+  if (plan.max_segs != 1 || !score) return hipErrorInvalidValue;
+  stream::StreamArgs a = stream::base_args(s, plan, q_win, k, scale);
+  a.row_max_out = row_max;
+  a.row_sum_out = row_sum;
+  a.sigma_all = sigma_all ? 1 : 0;
+  a.score = score;
+  a.lambda1 = lambda1;
+  a.w_mu = w_mu;
   return stream::launch_for_shape<stream::WindowLaunch>(s, a, stream);
 }
 

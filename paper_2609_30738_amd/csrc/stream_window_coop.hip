@@ -26,7 +26,9 @@ __device__ __forceinline__ float2 load_partial(const float2* src) {
                                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
 }
 
-template <int D, int NB, bool ALL, int NW, int S>
+// In base-score mode (SC) pass 2 stores each key's base score instead of mu and sigma (see
+// stream_window.hip).
+template <int D, int NB, bool ALL, int NW, int S, bool SC>
 __global__ __launch_bounds__(NW * 64, 1) void window_coop_kernel(StreamArgs a, uint32_t* arrive,
                                                                  uint32_t spin_limit) {
   using Gm = SGeo<D, NB>;
@@ -59,6 +61,7 @@ __global__ __launch_bounds__(NW * 64, 1) void window_coop_kernel(StreamArgs a, u
 
   KeyStream<D, NB, NW, S> ks{ring[wave], kg, k0, k1, wave, lane};
   const int my_tiles = tiles_of(k0, k1);
+
   bf16x8_t q[NB][NS];
   load_queries<D, NB>(q, a.q_win + ((size_t)p * a.h_q + (size_t)g * G) * 32 * D, l32, half);
   ks.prologue(my_tiles);
@@ -137,8 +140,14 @@ __global__ __launch_bounds__(NW * 64, 1) void window_coop_kernel(StreamArgs a, u
     }
   }
   __syncthreads();
-  mu_sigma_tiles<D, NB, ALL, NW, S>(ks, q, bsh, my_tiles, k1, L, c, inv_g, a.mu + stat_base,
-                                    a.sigma + stat_base, l32, half);
+  if constexpr (SC) {
+    const ScoreOut so{a.score + stat_base, a.lambda1[p], a.w_mu};
+    mu_sigma_tiles<D, NB, ALL, NW, S, true>(ks, q, bsh, my_tiles, k1, L, c, inv_g, nullptr, nullptr,
+                                            l32, half, so);
+  } else {
+    mu_sigma_tiles<D, NB, ALL, NW, S>(ks, q, bsh, my_tiles, k1, L, c, inv_g, a.mu + stat_base,
+                                      a.sigma + stat_base, l32, half);
+  }
   wait_vmem<0>();  // no load into the ring may outlive the workgroup
 }
 
@@ -151,11 +160,14 @@ __global__ void zero_words_kernel(uint32_t* w, int n) {
 // the chip at once (then no workgroup normally waits long); `launched` tells the caller whether it
 // ran.
 template <int D, int NB> struct CoopLaunch {
+  template <bool ALL, bool SC> static const void* kernel() {
+    return reinterpret_cast<const void*>(window_coop_kernel<D, NB, ALL, kWaves, 2, SC>);
+  }
   static hipError_t run(const Shape& s, StreamArgs args, uint32_t* arrive, uint32_t spin_limit,
                         hipStream_t st, bool* launched) {
-    const void* kern = args.sigma_all
-        ? reinterpret_cast<const void*>(window_coop_kernel<D, NB, true, kWaves, 2>)
-        : reinterpret_cast<const void*>(window_coop_kernel<D, NB, false, kWaves, 2>);
+    const bool sc = args.score != nullptr;
+    const void* kern = args.sigma_all ? (sc ? kernel<true, true>() : kernel<true, false>())
+                                      : (sc ? kernel<false, true>() : kernel<false, false>());
     int dev = 0, n_cu = 0, per_cu = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e == hipSuccess) e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
@@ -168,10 +180,13 @@ template <int D, int NB> struct CoopLaunch {
     }
     const int n_units = s.n_prob * s.h_kv;
     zero_words_kernel<<<(n_units + 255) / 256, 256, 0, st>>>(arrive, n_units);
-    if (args.sigma_all)
-      window_coop_kernel<D, NB, true, kWaves, 2><<<grid, kThreads, 0, st>>>(args, arrive, spin_limit);
-    else
-      window_coop_kernel<D, NB, false, kWaves, 2><<<grid, kThreads, 0, st>>>(args, arrive, spin_limit);
+    if (args.sigma_all) {
+      if (sc) window_coop_kernel<D, NB, true, kWaves, 2, true><<<grid, kThreads, 0, st>>>(args, arrive, spin_limit);
+      else window_coop_kernel<D, NB, true, kWaves, 2, false><<<grid, kThreads, 0, st>>>(args, arrive, spin_limit);
+    } else {
+      if (sc) window_coop_kernel<D, NB, false, kWaves, 2, true><<<grid, kThreads, 0, st>>>(args, arrive, spin_limit);
+      else window_coop_kernel<D, NB, false, kWaves, 2, false><<<grid, kThreads, 0, st>>>(args, arrive, spin_limit);
+    }
     e = hipGetLastError();
     *launched = e == hipSuccess;
     return e;
@@ -184,7 +199,8 @@ template <int D, int NB> struct CoopLaunch {
 hipError_t launch_stream_window_coop(const Shape& s, const StreamPlan& plan, const void* q_win,
                                      const void* k, float scale, void* ws, float* row_max,
                                      float* row_sum, float* mu, float* sigma, bool sigma_all,
-                                     uint32_t spin_limit, hipStream_t stream, bool* launched) {
+                                     uint32_t spin_limit, hipStream_t stream, bool* launched,
+                                     const ScoreMode* sm) {
   *launched = false;
   stream::StreamArgs a = stream::base_args(s, plan, q_win, k, scale);
   a.part = static_cast<float2*>(ws);
@@ -193,6 +209,11 @@ hipError_t launch_stream_window_coop(const Shape& s, const StreamPlan& plan, con
   a.mu = mu;
   a.sigma = sigma;
   a.sigma_all = sigma_all ? 1 : 0;
+  if (sm) {
+    a.score = sm->score;
+    a.lambda1 = sm->lambda1;
+    a.w_mu = sm->w_mu;
+  }
   uint32_t* arrive = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + stream_counter_offset(s, plan));
   const int G = s.group();
   using namespace stream;

@@ -21,6 +21,7 @@ Selections are integer results decided by fp32 arithmetic (R23).  Per kv head:
 from __future__ import annotations
 
 import dataclasses
+from fractions import Fraction
 from typing import List, Optional, Sequence
 
 import numpy as np
@@ -47,6 +48,47 @@ BOUNDARY_RTOL = 2e-5     # relative error of a base score at a cut through the b
 # replay of an uncertified greedy: two candidates' scores may swap within the sum of their errors
 PAIR_RTOL = 2e-5
 PAIR_PER_LAMBDA = 4e-6
+
+
+def order_key(x: np.ndarray) -> np.ndarray:
+    """Order-preserving uint32 key of fp32 values (larger value, larger key), as the kernels form it:
+    the complemented word for a set sign bit, else the word with the sign bit set."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    return np.where(u & np.uint32(0x80000000), ~u, u | np.uint32(0x80000000))
+
+
+def _round_f32_exact(x: Fraction) -> np.float32:
+    """The fp32 value nearest to the rational x, ties to an even significand."""
+    r = np.float32(float(x))
+    best, best_d = None, None
+    for c in (np.nextafter(r, np.float32(-np.inf)), r, np.nextafter(r, np.float32(np.inf))):
+        if not np.isfinite(c):
+            continue
+        d = abs(Fraction(float(c)) - x)
+        if best is None or d < best_d or (d == best_d and int(c.view(np.uint32)) % 2 == 0):
+            best, best_d = c, d
+    return best
+
+
+def assert_fma_f32(got: np.ndarray, a: float, b: np.ndarray, c: np.ndarray, where: str) -> None:
+    """got == fp32(a * b + c) with one rounding, bit for bit (a, b, c fp32).  The exact product of
+    two fp32 values fits a float64, so a float64 sum rounded to fp32 is the fused result except
+    where the sum itself rounds next to an fp32 rounding boundary; every element where that
+    evaluation disagrees is decided in exact rational arithmetic."""
+    a32 = np.float32(a)
+    b32 = np.asarray(b, dtype=np.float32)
+    c32 = np.asarray(c, dtype=np.float32)
+    got = np.asarray(got, dtype=np.float32)
+    fin = np.isfinite(b32) & np.isfinite(c32)
+    with np.errstate(over="ignore", invalid="ignore"):
+        approx = (np.float64(a32) * b32.astype(np.float64) + c32.astype(np.float64)).astype(np.float32)
+    same = (got.view(np.uint32) == approx.view(np.uint32)) | (np.isnan(got) & np.isnan(approx))
+    for i in np.flatnonzero(~same & fin):
+        want = _round_f32_exact(Fraction(float(a32)) * Fraction(float(b32[i])) + Fraction(float(c32[i])))
+        assert got[i].view(np.uint32) == want.view(np.uint32), (
+            f"{where}[{i}]: {got[i]!r} is not fma({a32!r}, {b32[i]!r}, {c32[i]!r}) = {want!r}")
+    bad = ~same & ~fin
+    assert not bad.any(), f"{where}: non-finite inputs give {got[bad][:4]} instead of {approx[bad][:4]}"
 
 
 def pair_tol(st_a: float, st_b: float, lam2: float) -> float:

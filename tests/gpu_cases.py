@@ -46,9 +46,11 @@ def run_gpu(wl: workloads.Workload, problems: Optional[Sequence[int]] = None, *,
             pool: int = 1, w_mu: float = 1.0, sigma_rows: str = "group_mean",
             budgets: Optional[Sequence[int]] = None, redraw: Optional[certify.Redraw] = None,
             case: Optional[str] = None, timed: bool = False) -> GpuRun:
-    """One pass through the C ABI.  timed=True runs the benchmark's calls (kv_window_mu_sigma, then
-    kv_mmr_select_compact: sel_idx, k_out, v_out) and, on the same mu / sigma, kv_mmr_select with
-    its optional outputs (sel_score, cand_idx, cand_corr, and its own sel_idx as sel_idx_plain)."""
+    """One pass through the C ABI.  timed=True runs the benchmark's calls (kv_window_base_scores,
+    then kv_mmr_select_scored with the compaction: row_max, row_sum, score, sel_idx, k_out, v_out)
+    and, on the same inputs, kv_window_mu_sigma_ex and kv_mmr_select_ex with the optional outputs
+    (mu, sigma, sel_score, cand_idx, cand_corr; their row statistics and sel_idx as row_max_plain,
+    row_sum_plain, sel_idx_plain)."""
     import torch
     probs = list(range(wl.n_prob)) if problems is None else list(problems)
     print(f"[gpu case] {case or wl.name} problems={len(probs)} fused={fused} timed={timed} "
@@ -73,14 +75,25 @@ def run_gpu(wl: workloads.Workload, problems: Optional[Sequence[int]] = None, *,
     b = inp.batch
     extra = {}
     if timed:
-        _lib.window_mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
-                             out.sigma, out.ws)
-        _lib.mmr_select_compact(b, out.mu, out.sigma, inp.k, inp.v, inp.lambda1, inp.lambda2, B,
-                                cand_mult, tail, out.sel_idx, out.k_out, out.v_out, out.ws)
+        dev = inp.k.device
+        budgets_dev = None if bud is None else _lib.Budgets(bud, dev)
+        score = torch.empty_like(out.mu)
+        wsb = _lib.base_scores_workspace_bytes(b)
+        ws_sc = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
+        _lib.window_base_scores(b, inp.q_win, inp.k, inp.scale, inp.lambda1, out.row_max,
+                                out.row_sum, score, w_mu=w_mu, sigma_rows=sigma_rows,
+                                ws=ws_sc if wsb > 0 else None)
+        _lib.mmr_select_scored(b, score, inp.k, inp.v, inp.lambda2, B, cand_mult, tail,
+                               out.sel_idx, k_out=out.k_out, v_out=out.v_out, pool=pool,
+                               budgets=budgets_dev)
         plain = torch.empty_like(out.sel_idx)
-        _lib.mmr_select(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2, B, cand_mult, tail,
-                        plain, out.sel_score, out.cand_idx, out.cand_corr, out.ws)
-        extra["sel_idx_plain"] = plain
+        rm, rs = torch.empty_like(out.row_max), torch.empty_like(out.row_sum)
+        _lib.window_mu_sigma_ex(b, inp.q_win, inp.k, inp.scale, sigma_rows, rm, rs, out.mu,
+                                out.sigma, out.ws)
+        _lib.mmr_select_ex(b, out.mu, out.sigma, inp.k, inp.lambda1, inp.lambda2, B, cand_mult,
+                           tail, plain, out.sel_score, out.cand_idx, out.cand_corr, out.ws,
+                           pool=pool, w_mu=w_mu, budgets=budgets_dev)
+        extra.update(sel_idx_plain=plain, row_max_plain=rm, row_sum_plain=rs, score=score)
     else:
         api.run_pass(inp, out, B, cand_mult, tail, fused=fused, pool=pool, w_mu=w_mu,
                      sigma_rows=sigma_rows,
@@ -168,6 +181,17 @@ def check_problem(run: GpuRun, j: int, res: Optional[evict.ProblemResult] = None
     tok = int(run.packed.tok_off[j])
     mu = H["mu"][tok * wl.h_kv:(tok + L) * wl.h_kv].reshape(wl.h_kv, L)
     sg = H["sigma"][tok * wl.h_kv:(tok + L) * wl.h_kv].reshape(wl.h_kv, L)
+    if "score" in H:
+        # the timed path's row statistics and base scores are those of the mu / sigma path, bit
+        # for bit
+        for name in ("row_max", "row_sum"):
+            assert np.array_equal(H[name][j * rows:(j + 1) * rows].view(np.uint32),
+                                  H[name + "_plain"][j * rows:(j + 1) * rows].view(np.uint32)), (
+                f"{where}: {name} of kv_window_base_scores and kv_window_mu_sigma_ex differ")
+        sc = H["score"][tok * wl.h_kv:(tok + L) * wl.h_kv].reshape(wl.h_kv, L)
+        for g in heads:
+            compare.assert_fma_f32(sc[g], float(run.lam1[j]), sg[g], np.float32(run.opts.w_mu) * mu[g],
+                                   f"{where} g={g}: score")
     errs = {}
     for g in heads:
         errs[g] = compare.ErrStats()
@@ -194,7 +218,7 @@ def check_problem(run: GpuRun, j: int, res: Optional[evict.ProblemResult] = None
         assert np.all(cand[len(live):] == -1) and np.all(np.diff(live) > 0), f"{where} g={g}: cand"
         if "sel_idx_plain" in H:
             assert np.array_equal(H["sel_idx_plain"][o * B:o * B + Bp], sel), (
-                f"{where} g={g}: kv_mmr_select and kv_mmr_select_compact disagree")
+                f"{where} g={g}: kv_mmr_select_ex and kv_mmr_select_scored disagree")
         else:
             assert np.all(H["sel_score"][o * B + Bp:(o + 1) * B] == 0), f"{where} g={g}: padding"
         rep = compare.check_selection(

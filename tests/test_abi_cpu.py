@@ -319,3 +319,55 @@ def test_no_alloc_entry_validates_and_bounds_its_scratch():
                                           NULL) == _lib.KV_ERR_NULL
     assert lib.kv_window_mu_sigma_noalloc(None, P, P, 0.088, 0, P, P, P, P, NULL) == _lib.KV_ERR_NULL
 
+
+
+def test_base_scores_checks():
+    """kv_window_base_scores: workspace only when mu / sigma must go through it, argument checks
+    before any launch."""
+    lib = _lib.lib()
+    pr = HostProblem()  # 4096 keys per (problem, kv head): several segments per unit
+    need = lib.kv_base_scores_workspace_bytes(pr.ref())
+    assert need > lib.kv_workspace_bytes(pr.ref(), 64, 4, 32) and need % 256 == 0
+    # every (layer, kv head) of a 32 x 32k batch is one workgroup's: scores in the window kernel
+    assert lib.kv_base_scores_workspace_bytes(HostProblem(lens=(32768,) * 32).ref()) == 0
+    assert lib.kv_base_scores_workspace_bytes(
+        HostProblem(dtype=_lib.KV_F32, lens=(32768,) * 32).ref()) > 0
+    assert lib.kv_base_scores_workspace_bytes(HostProblem(d=96).ref()) == 0
+    nan = float("nan")
+
+    def call(**kw):
+        return lib.kv_window_base_scores(
+            pr.ref(), kw.get("q", P), kw.get("k", P), kw.get("scale", 0.088), kw.get("lam1", P),
+            kw.get("w_mu", 1.0), kw.get("rows", 0), kw.get("rm", P), P, kw.get("score", P),
+            kw.get("ws", P), kw.get("ws_bytes", 0), NULL)
+    odd = ctypes.c_void_p(BUF.ctypes.data + 4)
+    assert lib.kv_window_base_scores(None, P, P, 0.088, P, 1.0, 0, P, P, P, P, need,
+                                     NULL) == _lib.KV_ERR_NULL
+    for kw in (dict(q=NULL), dict(lam1=NULL), dict(rm=NULL), dict(score=NULL)):
+        assert call(**kw) == _lib.KV_ERR_NULL, kw
+    for kw in (dict(score=odd), dict(k=odd), dict(scale=nan), dict(w_mu=nan), dict(rows=2)):
+        assert call(ws_bytes=need, **kw) == _lib.KV_ERR_ARG, kw
+    assert call(ws_bytes=need - 1) == _lib.KV_ERR_WORKSPACE
+    assert call(ws=NULL, ws_bytes=need) == _lib.KV_ERR_WORKSPACE
+
+
+def test_select_scored_checks():
+    """kv_mmr_select_scored validates like kv_mmr_select_ex, with the scores in place of mu /
+    sigma / lambda1, and k_out / v_out both or neither."""
+    lib = _lib.lib()
+    pr = HostProblem(lens=(4096,))
+
+    def call(**kw):
+        return lib.kv_mmr_select_scored(
+            pr.ref(), kw.get("score", P), kw.get("k", P), kw.get("v", P), kw.get("lam2", P),
+            kw.get("budget", 64), kw.get("cand_mult", 4), 32, None, kw.get("sel", P), None, None,
+            None, kw.get("k_out", P), kw.get("v_out", P), NULL)
+    for kw in (dict(score=NULL), dict(sel=NULL), dict(lam2=NULL), dict(k=NULL),
+               dict(k_out=NULL), dict(v_out=NULL), dict(v=NULL)):
+        assert call(**kw) == _lib.KV_ERR_NULL, kw
+    assert call(budget=0) == _lib.KV_ERR_BUDGET
+    assert call(budget=4096) == _lib.KV_ERR_BUDGET
+    assert call(cand_mult=-1) == _lib.KV_ERR_ARG
+    assert call(cand_mult=1 << 30) == _lib.KV_ERR_ARG
+    assert call(k=ctypes.c_void_p(BUF.ctypes.data + 4)) == _lib.KV_ERR_ARG
+    assert call(score=ctypes.c_void_p(BUF.ctypes.data + 4)) == _lib.KV_ERR_ARG

@@ -408,3 +408,54 @@ def test_select_and_compact_in_one_launch(case):
                        out.k_out.view(torch.int16 if k2.element_size() == 2 else torch.int32))
     assert torch.equal(v2.view(torch.int16 if v2.element_size() == 2 else torch.int32),
                        out.v_out.view(torch.int16 if v2.element_size() == 2 else torch.int32))
+
+
+# ------------------------------------------------------------------------------------------------
+# The benchmark's calls (kv_window_base_scores, then kv_mmr_select_scored with the compaction) with
+# every scoring option and on every window path: fp32 batches take mu / sigma through the
+# workspace and the base-score kernel, units in several segments the one-launch cooperative kernel
+# (or, when its grid does not fit, the two-launch path), whole-unit workgroups the fused kernel.
+# Each run also checks the scores bit for bit against the mu / sigma path's (tests/gpu_cases.py).
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("case,certified", [
+    ("tiny_f32", True), ("tiny_f32_tail3", True), ("sigma_all_rows", True),
+    ("g3_group_mean", True), ("g3_all_rows", True), ("curve_scaled", True),
+    ("mean_free", False), ("depth_budgets", False)])
+def test_scored_calls_with_options(case, certified):
+    _all(gpu_cases.run_case(case, timed=True), certified=certified)
+
+
+def test_scored_calls_max_pooled():
+    """Pooling in the selection from given scores."""
+    wl = workloads.ragged_batch("both", n_seq=2, n_layers=2, len_range=(700, 3100))
+    wl.budget = 64
+    _all(gpu_cases.run_gpu(wl, pool=7, timed=True))
+
+
+@pytest.mark.parametrize("h_q,h_kv,d", STREAM_SHAPES)
+def test_scored_calls_stream_shapes(h_q, h_kv, d):
+    """Every streaming head layout and head size, one segment per unit (scores formed in the fused
+    kernel) and several (in the cooperative kernel)."""
+    n_prob = 256 // h_kv
+    one = _shape_workload(h_q, h_kv, d, 2, n_prob // 2, [1024, 777])
+    assert _one_segment_per_unit(one)
+    _all(gpu_cases.run_gpu(one, timed=True))
+    _all(gpu_cases.run_gpu(_shape_workload(h_q, h_kv, d, 2, 2, [3000, 2100]), timed=True))
+
+
+def test_scored_calls_late_segments_and_second_launch(monkeypatch):
+    """Base scores from the cooperative kernel's waiting-workgroup path (poll limit 0) equal the
+    default path's bit for bit; a batch whose cooperative grid does not fit the chip forms them
+    from mu / sigma in the workspace."""
+    wl = workloads.mistral_layer()
+    monkeypatch.delenv("KVEVICT_SPIN_LIMIT", raising=False)
+    ref = gpu_cases.run_gpu(wl, timed=True)
+    monkeypatch.setenv("KVEVICT_SPIN_LIMIT", "0")
+    run = gpu_cases.run_gpu(wl, timed=True)
+    for name in ("row_max", "row_sum", "score", "sel_idx", "k_out", "v_out"):
+        assert np.array_equal(run.host[name], ref.host[name]), name
+    _all(run)
+    monkeypatch.delenv("KVEVICT_SPIN_LIMIT", raising=False)
+    big = _shape_workload(32, 8, 128, 3, 8, [5000, 5000, 5000], budget=32)
+    _all(gpu_cases.run_gpu(big, timed=True))
