@@ -228,6 +228,28 @@ __device__ __forceinline__ void bitonic_sort(V* v, int n2, int tid, int nt) {
   }
 }
 
+// Add one to hist[digit] (LDS) for every active lane, with few colliding atomics where most keys
+// share one bin (the bulk of the scores, which holds about three in four keys of the workloads
+// here): the wave's `hot` digit (the largest bin of its earlier calls) is counted with one ballot
+// and one atomic, then the digit of the first lane left likewise, and only the lanes left after
+// that add one each.  Every lane of the wave must call it; `hot` is wave-uniform.
+__device__ __forceinline__ void wave_hist_add_hot(uint32_t* hist, uint32_t digit, bool active,
+                                                  uint32_t& hot, int lane) {
+  uint64_t rem = __ballot(active);
+  if (rem == 0) return;
+  const uint64_t s1 = __ballot(active && digit == hot);
+  if (s1 != 0 && lane == __ffsll((unsigned long long)s1) - 1) atomicAdd(&hist[hot], (uint32_t)__popcll(s1));
+  rem &= ~s1;
+  if (rem == 0) return;
+  const int leader = __ffsll((unsigned long long)rem) - 1;
+  const uint32_t dl = __builtin_amdgcn_readlane(digit, leader);
+  const uint64_t s2 = __ballot(digit == dl) & rem;
+  if (lane == leader) atomicAdd(&hist[dl], (uint32_t)__popcll(s2));
+  rem &= ~s2;
+  if (__popcll(s2) > __popcll(s1)) hot = dl;
+  if ((rem >> lane) & 1ull) atomicAdd(&hist[digit], 1u);
+}
+
 constexpr int kFastBins = 2048;  // 11-bit digit
 constexpr int kFastShift = 21;
 constexpr int kListCap = 1024;   // members of the cut's bin ranked exactly
@@ -247,6 +269,7 @@ __device__ bool fast_candidates(SelectShared<NW>& sh, const uint32_t* skeys, int
   for (int i = tid; i < kFastBins; i += NT) h[i] = 0u;
   if (tid < 2) sh.wave_cnt[0][tid] = 0u;  // append counters: candidates above the bin, list
   __syncthreads();
+  uint32_t hot = ~0u;  // no digit yet
   for (int i0 = 0; i0 < n_cand; i0 += 4 * NT) {
     uint32_t kk[4];
 #pragma unroll
@@ -255,7 +278,8 @@ __device__ bool fast_candidates(SelectShared<NW>& sh, const uint32_t* skeys, int
       kk[q] = i < n_cand ? skeys[i] : 0u;
     }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) wave_hist_add(h, kk[q] >> kFastShift, i0 + q * NT + tid < n_cand);
+    for (int q = 0; q < 4; ++q)
+      wave_hist_add_hot(h, kk[q] >> kFastShift, i0 + q * NT + tid < n_cand, hot, lane);
   }
   __syncthreads();
   // suffix sums over the bins (larger bins = larger keys): thread t owns bins 2t, 2t + 1
