@@ -1,22 +1,21 @@
 """Benchmark of one eviction pass over a whole batch on one MI355X.
 
 A step is the full hot path over every layer of the workload: window row statistics, per-token
-mean/dispersion, greedy selection and cache compaction (kv_window_mu_sigma, then
-kv_mmr_select_compact: the selection and the compaction in one launch, with the results of
-kv_mmr_select followed by kv_compact_cache), with every input already resident in HBM.  Default workload: 32 layers of a
-Mistral-7B-shaped cache (32 query / 8 kv heads, d=128, bf16), L=32768, W=32, B=64, quadratic
-lambda2 depth profile.
+mean/dispersion and base score, the candidate cut, greedy selection and cache compaction, with
+every input already resident in HBM.  The timed pass is kv_window_candidates (the row statistics
+and each unit's candidate set from one launch that reads the keys once in full and revisits only
+the tiles whose score bound reaches the candidate cut) followed by kv_mmr_select_candidates (the
+greedy and the compaction in one launch).  Default workload: 32 layers of a Mistral-7B-shaped
+cache (32 query / 8 kv heads, d=128, bf16), L=32768, W=32, B=64, quadratic lambda2 depth profile.
 
 Before every timed step a 512 MiB buffer is read (outside the timed region) so that no part of
 the 2 GiB key cache is served from the 256 MB last-level cache.  Each step is timed with HIP
-events on the launch stream, per entry point and in total (`value`: the whole batch in one launch
-per entry point).  A second timed loop runs the scoring
-as its two separate entry points (kv_window_scores: the first streaming pass over the keys, which
-writes the row statistics itself at this size; kv_mu_sigma: the second pass) so that each kernel's duration
-is measured live; the roofline entry describes the scoring kernel of the timed pass (both passes
-of a unit in one workgroup, the dominant kernel), roofline_passes the two passes run separately.  A third loop
-times the per-layer schedule: the scoring launched once per layer, then one batched selection and
-compaction.  One JSON line is printed.
+events on the launch stream, per entry point and in total.  Further timed loops run, on the same
+inputs, the other scoring routes (base scores through HBM; mu and sigma through HBM; the two
+streaming passes as separate launches, so that each kernel's duration is measured live), the
+selection options, a decode step, and the per-layer schedule (the scoring launched once per
+layer, then one batched selection and compaction).  The roofline entry describes the scoring
+kernel of the timed pass (the dominant kernel).  One JSON line is printed.
 """
 from __future__ import annotations
 
@@ -34,6 +33,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, published
+PATHS = ("candidates", "scored", "mu_sigma", "unfused")
 WORKLOADS = ("mistral32_L32768_W32_B64", "mistral32_L8192_W32_B64", "mistral_layer_L4096_W32_B64")
 
 
@@ -84,6 +84,7 @@ def mfma_flops(wl) -> float:
 
 # sources that define each profiled kernel: its traffic record stays valid while they are unchanged
 KERNEL_SOURCES = {
+    "window_prune": ("stream_prune.hip", "stream_passes.h", "stream_common.h", "common.h"),
     "window_stream": ("stream_window.hip", "stream_passes.h", "stream_common.h", "common.h"),
     "stats_stream": ("stream_stats.hip", "stream_passes.h", "stream_common.h", "common.h"),
     "mu_sigma_stream": ("stream_mu_sigma.hip", "stream_passes.h", "stream_common.h", "common.h"),
@@ -197,10 +198,11 @@ def copy_probe(torch, mib: int) -> None:
 
 
 def config_passes(torch, args) -> None:
-    """One JSON line per workload of the other configurations: the same batched pass (scoring with
-    the base scores formed inside it, then selection and compaction), timed the same way (cache
-    read-flushed before every step, HIP events), with its algorithmic bytes per second.  The ragged
-    batch's three coefficient runs differ in lambda1 as well, so each is a pass of its own."""
+    """One JSON line per workload of the other configurations: the same batched pass
+    (kv_window_candidates, then kv_mmr_select_candidates with the compaction), timed the same way
+    (cache read-flushed before every step, HIP events), with its algorithmic bytes per second, and
+    the scored route (kv_window_base_scores, kv_mmr_select_scored) beside it.  The ragged batch's
+    three coefficient runs differ in lambda1 as well, so each is a pass of its own."""
     from paper_2609_30738_amd import _lib, api, workloads as W
     flush_buf = torch.ones(128 << 20, dtype=torch.float32, device="cuda")
     cases = [W.mistral_layer()] + [W.mistral_pass_8k(b) for b in (32, 64, 128)]
@@ -215,41 +217,62 @@ def config_passes(torch, args) -> None:
         score = torch.empty_like(out.mu)
         wsb = _lib.base_scores_workspace_bytes(b)
         ws_sc = torch.empty(wsb, dtype=torch.uint8, device="cuda") if wsb else None
-        rows = []
-        for it in range(args.warmup + args.steps):
-            flush_buf.amax()
-            evs = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-            evs[0].record(stream)
+        wcb = _lib.candidates_workspace_bytes(b, wl.budget, 4, wl.w)
+        ws_c = torch.empty(wcb, dtype=torch.uint8, device="cuda")
+
+        def cand():
+            _lib.window_candidates(b, inp.q_win, inp.k, inp.scale, inp.lambda1, wl.budget, 4,
+                                   wl.w, out.row_max, out.row_sum, ws_c)
+
+        def cand_sel():
+            _lib.mmr_select_candidates(b, ws_c, inp.k, inp.v, inp.lambda2, wl.budget, 4, wl.w,
+                                       out.sel_idx, k_out=out.k_out, v_out=out.v_out)
+
+        def scored():
             _lib.window_base_scores(b, inp.q_win, inp.k, inp.scale, inp.lambda1, out.row_max,
                                     out.row_sum, score, ws=ws_sc)
-            evs[1].record(stream)
+
+        def scored_sel():
             _lib.mmr_select_scored(b, score, inp.k, inp.v, inp.lambda2, wl.budget, 4, wl.w,
                                    out.sel_idx, k_out=out.k_out, v_out=out.v_out)
-            evs[2].record(stream)
-            if it >= args.warmup:
-                rows.append(evs)
-        torch.cuda.synchronize()
-        t = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(2)] for e in rows])
-        return t.mean(axis=0), algorithmic_bytes(wl)
+        res = []
+        for calls in ((cand, cand_sel), (scored, scored_sel)):
+            rows = []
+            for it in range(args.warmup + args.steps):
+                flush_buf.amax()
+                evs = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+                evs[0].record(stream)
+                calls[0]()
+                evs[1].record(stream)
+                calls[1]()
+                evs[2].record(stream)
+                if it >= args.warmup:
+                    rows.append(evs)
+            torch.cuda.synchronize()
+            res.append(np.array([[e[i].elapsed_time(e[i + 1]) for i in range(2)]
+                                 for e in rows]).mean(axis=0))
+        return res[0], float(res[1].sum()), algorithmic_bytes(wl)
 
     for wl in cases:
         packed = W.draw_packed(wl)
-        parts, ab = run(wl, packed)
+        parts, scored_ms, ab = run(wl, packed)
         ms = float(parts.sum())
         print(json.dumps({"config": wl.name, "ms_per_pass": round(ms, 4),
                           "scoring_ms": round(float(parts[0]), 4),
                           "select_compact_ms": round(float(parts[1]), 4),
                           "algorithmic_bytes": ab["total"],
-                          "GBps": round(ab["total"] / (ms * 1e-3) / 1e9, 1)}), flush=True)
+                          "GBps": round(ab["total"] / (ms * 1e-3) / 1e9, 1),
+                          "scored_route_ms": round(scored_ms, 4)}), flush=True)
     packed = W.draw_packed(ragged[0])  # the three runs share their inputs
     per_run = {}
     for wl in ragged:
-        parts, ab = run(wl, packed)
+        parts, scored_ms, ab = run(wl, packed)
         ms = float(parts.sum())
         per_run[wl.name.rsplit("_B128_", 1)[-1]] = {
             "ms_per_pass": round(ms, 4), "scoring_ms": round(float(parts[0]), 4),
             "select_compact_ms": round(float(parts[1]), 4),
-            "GBps": round(ab["total"] / (ms * 1e-3) / 1e9, 1)}
+            "GBps": round(ab["total"] / (ms * 1e-3) / 1e9, 1),
+            "scored_route_ms": round(scored_ms, 4)}
     print(json.dumps({"config": ragged[0].name.replace("_dispersion_only", ""),
                       "total_tokens_per_layer": int(packed.lens.sum() // ragged[0].n_layers),
                       "algorithmic_bytes": ab["total"], "runs": per_run}), flush=True)
@@ -274,11 +297,12 @@ def main() -> None:
                          "(0.82 / 0.91 ms) as the power management steps the clock")
     ap.add_argument("--flush", choices=("read", "write"), default="read",
                     help="how the last-level cache is emptied before each timed step")
-    ap.add_argument("--mu-sigma-path", action="store_true",
-                    help="time kv_window_mu_sigma + kv_mmr_select_compact (mu and sigma through "
-                         "HBM) instead of kv_window_base_scores + kv_mmr_select_scored")
-    ap.add_argument("--unfused", action="store_true",
-                    help="time kv_window_scores + kv_mu_sigma instead of kv_window_mu_sigma")
+    ap.add_argument("--path", choices=PATHS, default=PATHS[0],
+                    help="the timed pass: candidates = kv_window_candidates + "
+                         "kv_mmr_select_candidates; scored = kv_window_base_scores + "
+                         "kv_mmr_select_scored (base scores through HBM); mu_sigma = "
+                         "kv_window_mu_sigma + kv_mmr_select_compact (mu and sigma through HBM); "
+                         "unfused = kv_window_scores + kv_mu_sigma, then kv_mmr_select_compact")
     ap.add_argument("--configs", action="store_true",
                     help="only time the pass on the other workloads (one layer, the 8k sweep over B, "
                          "the ragged batch), one JSON line each")
@@ -324,13 +348,25 @@ def main() -> None:
             flush_buf.amax()
     stream = torch.cuda.current_stream()
     b = inp.batch
-    # the base score of every key: the timed pass's intermediate
+    # the candidate lists of the timed pass, and the base score of every key for the scored route
+    ws_c_bytes = _lib.candidates_workspace_bytes(b, wl.budget, 4, wl.w)
+    if ws_c_bytes == 0:
+        raise SystemExit("kv_candidates_workspace_bytes rejected the workload")
+    ws_c = torch.empty(ws_c_bytes, dtype=torch.uint8, device="cuda")
     score = torch.empty_like(out.mu)
     ws_sc_bytes = _lib.base_scores_workspace_bytes(b)
     ws_sc = torch.empty(ws_sc_bytes, dtype=torch.uint8, device="cuda") if ws_sc_bytes else None
-    mu_sigma_path = args.mu_sigma_path or args.unfused
+    mu_sigma_path = args.path in ("mu_sigma", "unfused")
 
     names = ["scoring", "select + compact"]
+
+    def cand_scoring():
+        _lib.window_candidates(b, inp.q_win, inp.k, inp.scale, inp.lambda1, wl.budget, 4, wl.w,
+                               out.row_max, out.row_sum, ws_c)
+
+    def cand_select():
+        _lib.mmr_select_candidates(b, ws_c, inp.k, inp.v, inp.lambda2, wl.budget, 4, wl.w,
+                                   out.sel_idx, k_out=out.k_out, v_out=out.v_out)
 
     def scored_scoring():
         _lib.window_base_scores(b, inp.q_win, inp.k, inp.scale, inp.lambda1, out.row_max,
@@ -348,21 +384,24 @@ def main() -> None:
         _lib.mmr_select_compact(b, out.mu, out.sigma, inp.k, inp.v, inp.lambda1, inp.lambda2,
                                 wl.budget, 4, wl.w, out.sel_idx, out.k_out, out.v_out, out.ws)
 
+    def unfused_scoring():
+        _lib.window_scores(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.ws)
+        _lib.mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu, out.sigma)
+
+    routes = {"candidates": (cand_scoring, cand_select,
+                             "kv_window_candidates", "kv_mmr_select_candidates (compacting)"),
+              "scored": (scored_scoring, scored_select,
+                         "kv_window_base_scores", "kv_mmr_select_scored (compacting)"),
+              "mu_sigma": (ms_scoring, ms_select, "kv_window_mu_sigma", "kv_mmr_select_compact"),
+              "unfused": (unfused_scoring, ms_select, "kv_window_scores + kv_mu_sigma",
+                          "kv_mmr_select_compact")}
+    run_scoring, run_select, scoring_name, select_name = routes[args.path]
+
     def step(evs):
         evs[0].record(stream)
-        if args.unfused:
-            _lib.window_scores(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.ws)
-            _lib.mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu,
-                          out.sigma)
-        elif mu_sigma_path:
-            ms_scoring()
-        else:
-            scored_scoring()
+        run_scoring()
         evs[1].record(stream)
-        if mu_sigma_path:
-            ms_select()
-        else:
-            scored_select()
+        run_select()
         evs[2].record(stream)
 
     def new_events():
@@ -416,11 +455,14 @@ def main() -> None:
         t = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(len(calls))] for e in rows_])
         return [float(x) for x in t.mean(axis=0)]
 
-    # the other path on the same inputs: mu and sigma through HBM, then the selection from them
-    if mu_sigma_path:
-        alt_scoring, alt_select = timed(scored_scoring, scored_select)
-    else:
-        alt_scoring, alt_select = timed(ms_scoring, ms_select)
+    # the other routes on the same inputs (the unfused one is covered by the per-kernel loop)
+    other_routes = {}
+    for name in ("candidates", "scored", "mu_sigma"):
+        if name != args.path:
+            f_sc, f_sel, n_sc, n_sel = routes[name]
+            t_sc, t_sel = timed(f_sc, f_sel)
+            other_routes[name] = {n_sc: round(t_sc, 4), n_sel: round(t_sel, 4),
+                                  "total": round(t_sc + t_sel, 4)}
 
     # per kernel: the two scoring passes through their own entry points, events between them
     # (warm-up first: a kernel's first launch also loads its code); with one segment per unit,
@@ -539,8 +581,10 @@ def main() -> None:
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": measured_traffic(kernel, wl.name),
                 "algorithmic_bytes_per_launch": alg, "ms_per_launch": round(kms, 4)}
-    dominant = roofline("stats_stream+mu_sigma_stream" if args.unfused else "window_stream",
-                        ab["scoring"], float(mean_part[0]))
+    dominant_kernel = {"candidates": "window_prune", "scored": "window_stream",
+                       "mu_sigma": "window_stream",
+                       "unfused": "stats_stream+mu_sigma_stream"}[args.path]
+    dominant = roofline(dominant_kernel, ab["scoring"], float(mean_part[0]))
     passes = [roofline("stats_stream", ab["scoring"], k_stats),
               roofline("mu_sigma_stream", ab["scoring"], k_mu)]
     line = {
@@ -569,28 +613,17 @@ def main() -> None:
         "wall_s_timed_loop": round(wall, 3),
         "cache_flush": f"{args.flush} of 512 MiB before every timed step",
         "settle": {"passes": settle_passes, "ms": round(settle_ms, 1)},
-        "pass": ("kv_window_scores + kv_mu_sigma, kv_mmr_select_compact" if args.unfused else
-                 "kv_window_mu_sigma, kv_mmr_select_compact" if mu_sigma_path else
-                 "kv_window_base_scores, kv_mmr_select_scored (compacting)"),
-        "other_path_ms": {("kv_window_base_scores" if mu_sigma_path else "kv_window_mu_sigma"):
-                          round(alt_scoring, 4),
-                          ("kv_mmr_select_scored (compacting)" if mu_sigma_path else
-                           "kv_mmr_select_compact"): round(alt_select, 4),
-                          "total": round(alt_scoring + alt_select, 4)},
+        "pass": f"{scoring_name}, {select_name}",
+        "other_routes_ms": other_routes,
         "per_layer_schedule_ms": {"total": round(lay_score + lay_rest, 4),
                                   ("scoring (32 launches of kv_window_mu_sigma)" if mu_sigma_path
                                    else "scoring (32 launches of kv_window_base_scores)"):
                                   round(lay_score, 4),
                                   "select+compact (batched)": round(lay_rest, 4)},
-        "per_kernel_ms": {("stats_stream + mu_sigma_stream (unfused)" if args.unfused else
-                           "window_stream (kv_window_mu_sigma)" if mu_sigma_path else
-                           "window_stream, base-score mode (kv_window_base_scores)"):
-                          round(float(mean_part[0]), 4),
+        "per_kernel_ms": {f"{dominant_kernel} ({scoring_name})": round(float(mean_part[0]), 4),
                           "stats_stream (kv_window_scores)": round(k_stats, 4),
                           "mu_sigma_stream (kv_mu_sigma)": round(k_mu, 4),
-                          ("mmr_select_compact (kv_mmr_select_compact)" if mu_sigma_path else
-                           "mmr_select_compact, scored (kv_mmr_select_scored)"):
-                          round(float(mean_part[1]), 4),
+                          f"mmr_select ({select_name})": round(float(mean_part[1]), 4),
                           "mmr_select (kv_mmr_select)": round(k_sel, 4),
                           "compact (kv_compact_cache)": round(k_cmp, 4)},
         "options_ms": {"kv_window_mu_sigma_ex (sigma over all G*W rows)": round(v_all, 4),
@@ -613,7 +646,7 @@ def main() -> None:
     # before the interpreter exits: no device memory or event outlives the run)
     torch.cuda.synchronize()
     del all_events, layer_events
-    inp = out = score = ws_sc = ws_lay = None
+    inp = out = score = ws_sc = ws_lay = ws_c = None
     torch.cuda.empty_cache()
     if args.cpu_baseline:
         layers = []

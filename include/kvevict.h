@@ -278,6 +278,43 @@ int kv_mmr_select_scored(const kv_problem* pr, const float* score, const void* k
                          int32_t* cand_idx, float* cand_corr, void* k_out, void* v_out,
                          void* stream);
 
+/* Window statistics and the candidate set P of the selection in one call (section 3.1, Eq. (1),
+ * (3); section 3.2, Eq. (4), (5)): row_max / row_sum as from kv_window_base_scores with the same
+ * sigma_rows, and, in the workspace (ws, ws_bytes >= kv_candidates_workspace_bytes, 256-byte
+ * aligned), for every problem p and kv head g the C_p = min(cand_mult * B_p, n_cand) candidates of
+ * kv_mmr_select_ex (the largest base scores s_i = fmaf(lambda1[p], sigma_i, w_mu * mu_i) over
+ * i < n_cand = L_p - keep_tail, ties to the lower position) with their scores, and the normaliser
+ * max(max_i s_i, 1e-12), so that kv_mmr_select_candidates can run the greedy without the score
+ * array.  The layout of the workspace is private to these two calls; it stays valid until the
+ * next call that writes it.  budget, cand_mult, keep_tail and opts (pool must be 1, else
+ * KV_ERR_ARG; w_mu and the per-problem budgets as in kv_mmr_select_ex) must be the values later
+ * given to kv_mmr_select_candidates.  lambda1: [n_prob] fp32 device.
+ * For bf16 batches that kv_window_base_scores scores inside the window kernel's second pass, with
+ * cand_mult > 0, C_p <= 448 and L_p <= 65535, the candidates are kept inside that pass (one list
+ * per wave, merged by the selection) and no score is stored; otherwise the scores go through the
+ * workspace and the selection kernel's first phases cut the candidates from them.  Calls that
+ * overlap on one workspace race. */
+int kv_window_candidates(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                         const float* lambda1, int32_t sigma_rows, int32_t budget,
+                         int32_t cand_mult, int32_t keep_tail, const kv_select_opts* opts,
+                         float* row_max, float* row_sum, void* ws, size_t ws_bytes, void* stream);
+
+/* Bytes of device workspace kv_window_candidates needs for this batch and these selection
+ * arguments with scale > 0 (256-byte alignment).  Returns 0 for invalid arguments. */
+size_t kv_candidates_workspace_bytes(const kv_problem* pr, int32_t budget, int32_t cand_mult,
+                                     int32_t keep_tail, const kv_select_opts* opts);
+
+/* The greedy of kv_mmr_select_scored, and optionally its compaction, from the candidates that
+ * kv_window_candidates left in the workspace (section 3.2, Eq. (2), (4)): with the same budget,
+ * cand_mult, keep_tail and opts, every output equals kv_mmr_select_scored's given the score of
+ * kv_window_base_scores, bit for bit (sel_idx, sel_score, cand_idx, cand_corr, k_out, v_out;
+ * nullability, layouts and limits as there).  The workspace is only read. */
+int kv_mmr_select_candidates(const kv_problem* pr, const void* ws, size_t ws_bytes, const void* k,
+                             const void* v, const float* lambda2, int32_t budget,
+                             int32_t cand_mult, int32_t keep_tail, const kv_select_opts* opts,
+                             int32_t* sel_idx, float* sel_score, int32_t* cand_idx,
+                             float* cand_corr, void* k_out, void* v_out, void* stream);
+
 /* kv_compact_cache with per-problem budgets and a chosen block size (budget_host / budget_dev as
  * in kv_select_opts; both NULL with out_rows = 0 is exactly kv_compact_cache).  The block of every
  * (problem, kv head) in k_out / v_out has out_rows rows (0: budget + keep_tail; otherwise at least

@@ -45,7 +45,8 @@ SYMBOLS = ("kv_strerror", "kv_version", "kv_workspace_bytes", "kv_candidate_stri
            "kv_window_scores", "kv_mu_sigma", "kv_mu_sigma_ex", "kv_window_mu_sigma",
            "kv_window_mu_sigma_ex", "kv_window_mu_sigma_noalloc", "kv_window_base_scores",
            "kv_base_scores_workspace_bytes", "kv_mmr_select", "kv_mmr_select_ex",
-           "kv_mmr_select_compact", "kv_mmr_select_scored",
+           "kv_mmr_select_compact", "kv_mmr_select_scored", "kv_window_candidates",
+           "kv_candidates_workspace_bytes", "kv_mmr_select_candidates",
            "kv_compact_cache", "kv_compact_cache_ex", "kv_decode_workspace_bytes",
            "kv_decode_attention", "kv_pyramid_budgets", "kv_depth_profile")
 
@@ -108,6 +109,14 @@ def lib() -> ctypes.CDLL:
         h.kv_base_scores_workspace_bytes.restype = sz
         h.kv_mmr_select_scored.argtypes = [pr, vp, vp, vp, vp, i32, i32, i32,
                                            ctypes.POINTER(KvSelectOpts), vp, vp, vp, vp, vp, vp, vp]
+        h.kv_window_candidates.argtypes = [pr, vp, vp, ctypes.c_float, vp, i32, i32, i32, i32,
+                                           ctypes.POINTER(KvSelectOpts), vp, vp, vp, sz, vp]
+        h.kv_candidates_workspace_bytes.argtypes = [pr, i32, i32, i32,
+                                                    ctypes.POINTER(KvSelectOpts)]
+        h.kv_candidates_workspace_bytes.restype = sz
+        h.kv_mmr_select_candidates.argtypes = [pr, vp, sz, vp, vp, vp, i32, i32, i32,
+                                               ctypes.POINTER(KvSelectOpts), vp, vp, vp, vp, vp,
+                                               vp, vp]
         h.kv_mmr_select.argtypes = [pr, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, sz,
                                     vp]
         h.kv_mmr_select_compact.argtypes = [pr, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp,
@@ -126,7 +135,7 @@ def lib() -> ctypes.CDLL:
         for name in ("kv_window_scores", "kv_mu_sigma", "kv_mu_sigma_ex", "kv_window_mu_sigma",
                      "kv_window_mu_sigma_ex", "kv_window_mu_sigma_noalloc",
                      "kv_window_base_scores", "kv_mmr_select", "kv_mmr_select_ex",
-                     "kv_mmr_select_scored",
+                     "kv_mmr_select_scored", "kv_window_candidates", "kv_mmr_select_candidates",
                      "kv_compact_cache", "kv_compact_cache_ex", "kv_decode_attention",
                      "kv_pyramid_budgets", "kv_depth_profile"):
             getattr(h, name).restype = ctypes.c_int
@@ -316,6 +325,44 @@ def mmr_select_scored(batch: Batch, score, k, v, lambda2, budget: int, cand_mult
                                       _ptr(sel_idx), _ptr(sel_score), _ptr(cand_idx),
                                       _ptr(cand_corr), _ptr(k_out), _ptr(v_out),
                                       _stream(stream)), "kv_mmr_select_scored")
+
+
+def candidates_workspace_bytes(batch: Batch, budget: int, cand_mult: int, keep_tail: int,
+                               w_mu: Optional[float] = None,
+                               budgets: Optional[Budgets] = None) -> int:
+    return int(lib().kv_candidates_workspace_bytes(batch.ref(), int(budget), int(cand_mult),
+                                                   int(keep_tail),
+                                                   _select_opts(None, w_mu, budgets)))
+
+
+def window_candidates(batch: Batch, q_win, k, scale: float, lambda1, budget: int, cand_mult: int,
+                      keep_tail: int, row_max, row_sum, ws, w_mu: Optional[float] = None,
+                      budgets: Optional[Budgets] = None, sigma_rows="group_mean",
+                      stream=None) -> None:
+    """kv_window_candidates: row statistics out, the candidates into ws (see
+    candidates_workspace_bytes) for mmr_select_candidates with the same selection arguments."""
+    _check(lib().kv_window_candidates(batch.ref(), _ptr(q_win), _ptr(k), float(scale),
+                                      _ptr(lambda1), _sigma_rows(sigma_rows), int(budget),
+                                      int(cand_mult), int(keep_tail),
+                                      _select_opts(None, w_mu, budgets), _ptr(row_max),
+                                      _ptr(row_sum), _ptr(ws),
+                                      0 if ws is None else ws.numel() * ws.element_size(),
+                                      _stream(stream)), "kv_window_candidates")
+
+
+def mmr_select_candidates(batch: Batch, ws, k, v, lambda2, budget: int, cand_mult: int,
+                          keep_tail: int, sel_idx, sel_score=None, cand_idx=None, cand_corr=None,
+                          k_out=None, v_out=None, w_mu: Optional[float] = None,
+                          budgets: Optional[Budgets] = None, stream=None) -> None:
+    """kv_mmr_select_candidates; with k_out / v_out the compaction runs in the same launch."""
+    _check(lib().kv_mmr_select_candidates(batch.ref(), _ptr(ws),
+                                          0 if ws is None else ws.numel() * ws.element_size(),
+                                          _ptr(k), _ptr(v), _ptr(lambda2), int(budget),
+                                          int(cand_mult), int(keep_tail),
+                                          _select_opts(None, w_mu, budgets), _ptr(sel_idx),
+                                          _ptr(sel_score), _ptr(cand_idx), _ptr(cand_corr),
+                                          _ptr(k_out), _ptr(v_out), _stream(stream)),
+           "kv_mmr_select_candidates")
 
 
 def mmr_select(batch: Batch, mu, sigma, k, lambda1, lambda2, budget: int, cand_mult: int,

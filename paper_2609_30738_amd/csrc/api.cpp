@@ -146,19 +146,56 @@ size_t base_scores_ws_bytes(const kv_problem* pr, const kv::Shape& s, bool fused
   return window_ws_bytes(pr, s) + 2 * align_up(keys * sizeof(float));
 }
 
+// Candidate lists of kv_window_candidates: kCandListCount lists of `stride` 8-byte entries per
+// (problem, kv head).
+size_t cand_lists_bytes(const kv_problem* pr, int stride) {
+  return align_up((size_t)pr->n_prob * pr->h_kv * kv::kCandListCount * stride * sizeof(uint64_t));
+}
+
+// Whether kv_window_candidates forms the candidate lists inside the window kernel's second pass:
+// every unit one segment of a streaming shape, units of at most kCandMaxLen keys, at most kCandMaxC
+// candidates (cand_mult > 0).
+bool cands_in_window_pass(const kv_problem* pr, const kv::Shape& s, float scale, int32_t cand_mult,
+                          int stride) {
+  return scores_in_window_pass(pr, s, scale) && cand_mult > 0 && stride <= kv::kCandMaxC &&
+         s.max_len <= kv::kCandMaxLen;
+}
+
+// Workspace of kv_window_candidates: the lists and the units' normalisers, and without the fused
+// path the scores and what kv_window_base_scores needs after them.
+size_t cand_ws_bytes(const kv_problem* pr, const kv::Shape& s, int stride, bool fused) {
+  const size_t head = cand_lists_bytes(pr, stride) + align_up((size_t)pr->n_prob * pr->h_kv * sizeof(float));
+  if (fused) return head;
+  return head + align_up((size_t)total_tokens(pr) * pr->h_kv * sizeof(float)) +
+         base_scores_ws_bytes(pr, s, false);
+}
+
 // Selection, and with k_out / v_out the compaction of the selected rows, in one launch; base
 // scores from mu / sigma, or given (score).
-int mmr_select_impl(const kv_problem* pr, const float* mu, const float* sigma, const float* score,
-                    const void* k, const void* v,
-                    const float* lambda1, const float* lambda2, int32_t budget,
+// Where the selection's base scores come from: mu / sigma (with lambda1), given scores, or the
+// candidate lists of kv_window_candidates; with cut_out only the candidate cut runs (lists out).
+struct ScoreSource {
+  const float* mu = nullptr;
+  const float* sigma = nullptr;
+  const float* lambda1 = nullptr;
+  const float* score = nullptr;
+  const uint64_t* cand_in = nullptr;
+  const float* cand_in_max = nullptr;
+  uint64_t* cut_out = nullptr;
+  float* cut_max = nullptr;
+  int list_stride = 0;
+};
+
+int mmr_select_impl(const kv_problem* pr, const ScoreSource& src, const void* k, const void* v,
+                    const float* lambda2, int32_t budget,
                     int32_t cand_mult, int32_t keep_tail, const kv_select_opts* opts,
                     int32_t* sel_idx, float* sel_score, int32_t* cand_idx, float* cand_corr,
                     void* k_out, void* v_out, void* stream) {
   kv::Shape s;
   int st = check_problem(pr, &s);
   if (st != KV_OK) return st;
-  if (!score && (!mu || !sigma || !lambda1)) return KV_ERR_NULL;
-  if (!k || !lambda2 || !sel_idx) return KV_ERR_NULL;
+  if (!src.score && !src.cand_in && (!src.mu || !src.sigma || !src.lambda1)) return KV_ERR_NULL;
+  if (!k || (!src.cut_out && (!lambda2 || !sel_idx))) return KV_ERR_NULL;
   if (!aligned16(k)) return KV_ERR_ARG;
   if (k_out && (!aligned16(v) || !aligned16(k_out) || !aligned16(v_out))) return KV_ERR_ARG;
   // the kernels form cand_mult * B_p in 32-bit arithmetic (B_p <= budget)
@@ -175,12 +212,18 @@ int mmr_select_impl(const kv_problem* pr, const float* mu, const float* sigma, c
   if (k_out && budget > kMaxCompactBudget) return KV_ERR_BUDGET;
   const int max_cand = max_candidates(pr, budget, cand_mult, keep_tail, b_host);
   if (max_cand > kv::select_max_candidates(pr->d, elem_bytes(pr->dtype))) return KV_ERR_SHAPE;
+  if ((src.cand_in || src.cut_out) && pool != 1) return KV_ERR_ARG;  // lists hold unpooled scores
   kv::SelectArgs a;
-  a.mu = mu;
-  a.sigma = sigma;
-  a.score = score;
+  a.mu = src.mu;
+  a.sigma = src.sigma;
+  a.score = src.score;
+  a.cand_in = src.cand_in;
+  a.cand_in_max = src.cand_in_max;
+  a.cut_out = src.cut_out;
+  a.cut_max = src.cut_max;
+  a.list_stride = src.list_stride;
   a.k = k;
-  a.lambda1 = lambda1;
+  a.lambda1 = src.lambda1;
   a.lambda2 = lambda2;
   a.pool = pool;
   a.w_mu = w_mu;
@@ -420,9 +463,12 @@ int kv_mmr_select_ex(const kv_problem* pr, const float* mu, const float* sigma, 
                      size_t ws_bytes, void* stream) {
   (void)ws;
   (void)ws_bytes;
-  return mmr_select_impl(pr, mu, sigma, nullptr, k, nullptr, lambda1, lambda2, budget, cand_mult,
-                         keep_tail, opts, sel_idx, sel_score, cand_idx, cand_corr, nullptr, nullptr,
-                         stream);
+  ScoreSource src;
+  src.mu = mu;
+  src.sigma = sigma;
+  src.lambda1 = lambda1;
+  return mmr_select_impl(pr, src, k, nullptr, lambda2, budget, cand_mult, keep_tail, opts, sel_idx,
+                         sel_score, cand_idx, cand_corr, nullptr, nullptr, stream);
 }
 
 int kv_mmr_select_compact(const kv_problem* pr, const float* mu, const float* sigma, const void* k,
@@ -432,9 +478,12 @@ int kv_mmr_select_compact(const kv_problem* pr, const float* mu, const float* si
   (void)ws;
   (void)ws_bytes;
   if (!v || !k_out || !v_out) return KV_ERR_NULL;
-  return mmr_select_impl(pr, mu, sigma, nullptr, k, v, lambda1, lambda2, budget, cand_mult,
-                         keep_tail, nullptr, sel_idx, nullptr, nullptr, nullptr, k_out, v_out,
-                         stream);
+  ScoreSource src;
+  src.mu = mu;
+  src.sigma = sigma;
+  src.lambda1 = lambda1;
+  return mmr_select_impl(pr, src, k, v, lambda2, budget, cand_mult, keep_tail, nullptr, sel_idx,
+                         nullptr, nullptr, nullptr, k_out, v_out, stream);
 }
 
 int kv_mmr_select_scored(const kv_problem* pr, const float* score, const void* k, const void* v,
@@ -446,9 +495,105 @@ int kv_mmr_select_scored(const kv_problem* pr, const float* score, const void* k
   if (!aligned16(score)) return KV_ERR_ARG;
   if ((k_out != nullptr) != (v_out != nullptr)) return KV_ERR_NULL;
   if (k_out && !v) return KV_ERR_NULL;
-  return mmr_select_impl(pr, nullptr, nullptr, score, k, v, nullptr, lambda2, budget, cand_mult,
-                         keep_tail, opts, sel_idx, sel_score, cand_idx, cand_corr, k_out, v_out,
-                         stream);
+  ScoreSource src;
+  src.score = score;
+  return mmr_select_impl(pr, src, k, v, lambda2, budget, cand_mult, keep_tail, opts, sel_idx,
+                         sel_score, cand_idx, cand_corr, k_out, v_out, stream);
+}
+
+size_t kv_candidates_workspace_bytes(const kv_problem* pr, int32_t budget, int32_t cand_mult,
+                                     int32_t keep_tail, const kv_select_opts* opts) {
+  kv::Shape s;
+  if (check_problem(pr, &s) != KV_OK) return 0;
+  const int32_t* b_host = opts ? opts->budget_host : nullptr;
+  if (cand_mult < 0 || budget < 1 || check_budget(pr, budget, keep_tail, b_host != nullptr) != KV_OK)
+    return 0;
+  if (opts && opts->pool != 1) return 0;
+  const int stride = max_candidates(pr, budget, cand_mult, keep_tail, b_host);
+  if (stride > kv::select_max_candidates(pr->d, elem_bytes(pr->dtype))) return 0;
+  return cand_ws_bytes(pr, s, stride, cands_in_window_pass(pr, s, 1.f, cand_mult, stride));
+}
+
+int kv_window_candidates(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                         const float* lambda1, int32_t sigma_rows, int32_t budget,
+                         int32_t cand_mult, int32_t keep_tail, const kv_select_opts* opts,
+                         float* row_max, float* row_sum, void* ws, size_t ws_bytes, void* stream) {
+  kv::Shape s;
+  int st = check_problem(pr, &s);
+  if (st != KV_OK) return st;
+  if (!q_win || !k || !lambda1 || !row_max || !row_sum) return KV_ERR_NULL;
+  if (!aligned16(q_win) || !aligned16(k)) return KV_ERR_ARG;
+  if (!std::isfinite(scale)) return KV_ERR_ARG;
+  if (sigma_rows != KV_SIGMA_GROUP_MEAN && sigma_rows != KV_SIGMA_ALL_ROWS) return KV_ERR_ARG;
+  if (cand_mult < 0 || (int64_t)cand_mult * budget > INT32_MAX) return KV_ERR_ARG;
+  const int32_t pool = opts ? opts->pool : 1;
+  const float w_mu = opts ? opts->w_mu : 1.f;
+  const int32_t* b_host = opts ? opts->budget_host : nullptr;
+  const int32_t* b_dev = opts ? opts->budget_dev : nullptr;
+  if (pool != 1 || !std::isfinite(w_mu)) return KV_ERR_ARG;
+  st = check_budget(pr, budget, keep_tail, b_host != nullptr || b_dev != nullptr);
+  if (st != KV_OK) return st;
+  st = check_budgets(pr, budget, keep_tail, b_host, b_dev);
+  if (st != KV_OK) return st;
+  const int stride = max_candidates(pr, budget, cand_mult, keep_tail, b_host);
+  if (stride > kv::select_max_candidates(pr->d, elem_bytes(pr->dtype))) return KV_ERR_SHAPE;
+  const bool fused = cands_in_window_pass(pr, s, scale, cand_mult, stride);
+  const size_t need = cand_ws_bytes(pr, s, stride, fused);
+  if (ws_bytes < need || !ws || (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1)))
+    return KV_ERR_WORKSPACE;
+  const bool all = sigma_rows == KV_SIGMA_ALL_ROWS;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  char* base = static_cast<char*>(ws);
+  const size_t n_units = (size_t)pr->n_prob * pr->h_kv;
+  uint64_t* lists = reinterpret_cast<uint64_t*>(base);
+  float* cmax = reinterpret_cast<float*>(base + cand_lists_bytes(pr, stride));
+  if (fused)
+    return launch_status(kv::launch_stream_window_cands(s, stream_plan_of(pr, s), q_win, k, scale,
+                                                        lambda1, w_mu, budget, b_dev, cand_mult,
+                                                        keep_tail, row_max, row_sum, lists, cmax,
+                                                        stride, all, hs));
+  // the scores into the workspace, then the candidate cut of the selection kernel
+  const size_t head = cand_lists_bytes(pr, stride) + align_up(n_units * sizeof(float));
+  float* score = reinterpret_cast<float*>(base + head);
+  const size_t score_bytes = align_up((size_t)total_tokens(pr) * pr->h_kv * sizeof(float));
+  st = kv_window_base_scores(pr, q_win, k, scale, lambda1, w_mu, sigma_rows, row_max, row_sum,
+                             score, base + head + score_bytes, ws_bytes - head - score_bytes,
+                             stream);
+  if (st != KV_OK) return st;
+  ScoreSource src;
+  src.score = score;
+  src.cut_out = lists;
+  src.cut_max = cmax;
+  src.list_stride = stride;
+  return mmr_select_impl(pr, src, k, nullptr, nullptr, budget, cand_mult, keep_tail, opts, nullptr,
+                         nullptr, nullptr, nullptr, nullptr, nullptr, stream);
+}
+
+int kv_mmr_select_candidates(const kv_problem* pr, const void* ws, size_t ws_bytes, const void* k,
+                             const void* v, const float* lambda2, int32_t budget,
+                             int32_t cand_mult, int32_t keep_tail, const kv_select_opts* opts,
+                             int32_t* sel_idx, float* sel_score, int32_t* cand_idx,
+                             float* cand_corr, void* k_out, void* v_out, void* stream) {
+  kv::Shape s;
+  int st = check_problem(pr, &s);
+  if (st != KV_OK) return st;
+  if ((k_out != nullptr) != (v_out != nullptr)) return KV_ERR_NULL;
+  if (k_out && !v) return KV_ERR_NULL;
+  if (cand_mult < 0) return KV_ERR_ARG;
+  const int32_t* b_host = opts ? opts->budget_host : nullptr;
+  st = check_budget(pr, budget, keep_tail, b_host != nullptr);
+  if (st != KV_OK) return st;
+  const int stride = max_candidates(pr, budget, cand_mult, keep_tail, b_host);
+  const size_t lists = cand_lists_bytes(pr, stride);
+  if (ws_bytes < lists + align_up((size_t)pr->n_prob * pr->h_kv * sizeof(float)) || !ws ||
+      (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1)))
+    return KV_ERR_WORKSPACE;
+  ScoreSource src;
+  src.cand_in = static_cast<const uint64_t*>(ws);
+  src.cand_in_max = reinterpret_cast<const float*>(static_cast<const char*>(ws) + lists);
+  src.list_stride = stride;
+  return mmr_select_impl(pr, src, k, v, lambda2, budget, cand_mult, keep_tail, opts, sel_idx,
+                         sel_score, cand_idx, cand_corr, k_out, v_out, stream);
 }
 
 int kv_compact_cache(const kv_problem* pr, const void* k, const void* v, const int32_t* sel_idx,

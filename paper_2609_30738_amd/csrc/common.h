@@ -99,6 +99,18 @@ __device__ __forceinline__ uint32_t order_key(float x) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// The float whose order key is k (the inverse of order_key, bit for bit).
+__device__ __forceinline__ float key_float(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
+
+// Candidate entry: the order key of a base score and its position; a larger entry means a larger
+// score, then a lower position (the selection's order and tie rule).  0 is no entry.
+__device__ __forceinline__ uint64_t cand_entry(uint32_t okey, uint32_t pos) {
+  return ((uint64_t)okey << 32) | (uint32_t)(0xFFFFFFFFu - pos);
+}
+__device__ __forceinline__ uint32_t cand_entry_pos(uint64_t e) { return 0xFFFFFFFFu - (uint32_t)e; }
+
 // Add one to hist[digit] (LDS) for every active lane.  The digit of the first active lane is
 // counted with one ballot and a single LDS add (the common case: most scores share their leading
 // digits); lanes with other digits use LDS atomics, which handle scattered digits without
@@ -111,6 +123,28 @@ __device__ __forceinline__ void wave_hist_add(uint32_t* hist, uint32_t digit, bo
   const uint64_t same = __ballot(active && digit == dl);
   if ((int)(threadIdx.x & 63) == leader) atomicAdd(&hist[dl], (uint32_t)__popcll(same));
   if (active && digit != dl) atomicAdd(&hist[digit], 1u);
+}
+
+// Ascending bitonic sort of v[0, n2) (n2 a power of two) by the nt threads of the workgroup; starts and ends with
+// the workgroup synchronised.
+template <typename V>
+__device__ __forceinline__ void bitonic_sort(V* v, int n2, int tid, int nt) {
+  for (int size = 2; size <= n2; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = tid; i < n2; i += nt) {
+        const int j = i ^ stride;
+        if (j > i) {
+          const bool up = (i & size) == 0;
+          const V a = v[i], b = v[j];
+          if ((a > b) == up) {
+            v[i] = b;
+            v[j] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
 }
 
 // Value of the lane l ^ 32 (the other K-half / the other 16 accumulator rows).

@@ -72,6 +72,22 @@ hipError_t launch_stream_window_scores(const Shape& s, const StreamPlan& plan, c
                                        const void* k, float scale, const float* lambda1,
                                        float w_mu, float* row_max, float* row_sum, float* score,
                                        bool sigma_all, hipStream_t stream);
+// Window statistics and the candidate set in one launch, every unit one segment (candidate mode,
+// stream_prune.hip): row_max / row_sum, and per unit the candidate lists
+// [n_units][kCandListCount][cand_stride] of (order key of the score, position) entries packed as
+// key << 32 | (0xFFFFFFFF - position) (0: none) whose union holds the unit's C_p best entries, and
+// cand_max [n_units], the largest base score over the candidate positions clamped at 1e-12.  The
+// keys are read once in full; the second pass revisits only the tiles whose score bound reaches
+// the unit's cut.  Units of at most kCandMaxLen keys and C_p <= kCandMaxC.
+constexpr int kCandListCount = 8;
+constexpr int kCandMaxC = 288;
+constexpr int kCandMaxLen = 32768;
+hipError_t launch_stream_window_cands(const Shape& s, const StreamPlan& plan, const void* q_win,
+                                      const void* k, float scale, const float* lambda1, float w_mu,
+                                      int budget, const int32_t* budgets, int cand_mult,
+                                      int keep_tail, float* row_max, float* row_sum,
+                                      uint64_t* cand_out, float* cand_max, int cand_stride,
+                                      bool sigma_all, hipStream_t stream);
 // Base scores s = fma(lambda1[p], sigma, w_mu mu) of every key from mu / sigma rows (for batches
 // that take the other window paths).
 hipError_t launch_base_scores(const Shape& s, const float* mu, const float* sigma,
@@ -102,6 +118,14 @@ struct SelectArgs {
   const float* sigma;
   // base scores given instead of mu / sigma (then lambda1 and w_mu are unused)
   const float* score = nullptr;
+  // candidate lists given instead (cand_in, cand_in_max: as launch_stream_window_cands writes
+  // them, list_stride entries per list; no pooling), or, with cut_out, only the candidate cut:
+  // each unit's C candidates as list 0 of its lists and its normaliser into cut_max
+  const uint64_t* cand_in = nullptr;
+  const float* cand_in_max = nullptr;
+  uint64_t* cut_out = nullptr;
+  float* cut_max = nullptr;
+  int list_stride = 0;
   const void* k;
   const float* lambda1;
   const float* lambda2;

@@ -206,28 +206,6 @@ __device__ __forceinline__ void wave_append(bool pred, uint32_t* counter, int la
   if (pred) write(base + (uint32_t)__popcll(m & below));
 }
 
-// Ascending bitonic sort of v[0, n2) (n2 a power of two) by the NT threads; starts and ends with
-// the workgroup synchronised.
-template <typename V>
-__device__ __forceinline__ void bitonic_sort(V* v, int n2, int tid, int nt) {
-  for (int size = 2; size <= n2; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int i = tid; i < n2; i += nt) {
-        const int j = i ^ stride;
-        if (j > i) {
-          const bool up = (i & size) == 0;
-          const V a = v[i], b = v[j];
-          if ((a > b) == up) {
-            v[i] = b;
-            v[j] = a;
-          }
-        }
-      }
-      __syncthreads();
-    }
-  }
-}
-
 // Add one to hist[digit] (LDS) for every active lane, with few colliding atomics where most keys
 // share one bin (the bulk of the scores, which holds about three in four keys of the workloads
 // here): the wave's `hot` digit (the largest bin of its earlier calls) is counted with one ballot
@@ -389,7 +367,9 @@ struct CompactOut {
 template <int DT, int D, int NT, int CPT, bool STAGED, bool GRAM>
 __global__ __launch_bounds__(NT) void mmr_select_kernel(
     const float* __restrict__ mu, const float* __restrict__ sigma,
-    const float* __restrict__ score,
+    const float* __restrict__ score, const uint64_t* __restrict__ cand_in,
+    const float* __restrict__ cand_in_max, uint64_t* __restrict__ cut_out,
+    float* __restrict__ cut_max, int list_stride,
     const typename Elem<DT>::T* __restrict__ k, const int32_t* __restrict__ lens,
     const int64_t* __restrict__ tok_off, const float* __restrict__ lambda1,
     const float* __restrict__ lambda2, int pool_h, float w_mu, int h_kv, int budget,
@@ -413,7 +393,8 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
   const size_t base = (size_t)tok_off[p] * h_kv + (size_t)g * L;
   const float* mu_g = mu + base;
   const float* sg_g = sigma + base;
-  const float lam1 = lambda1 ? lambda1[p] : 0.f, lam2 = lambda2[p];  // no lambda1 with scores given
+  // no lambda1 with scores given, no lambda2 for the candidate cut alone
+  const float lam1 = lambda1 ? lambda1[p] : 0.f, lam2 = lambda2 ? lambda2[p] : 0.f;
   const float* sc_g = score ? score + base : nullptr;  // base scores given: mu / sigma unused
   // base score of candidate position i
   auto base_score = [&](int i) -> float {
@@ -427,6 +408,36 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
   uint32_t* skeys = reinterpret_cast<uint32_t*>(region);
   T* ckeys = reinterpret_cast<T*>(region);
   const bool take_all = (C >= n_cand);
+  float den = 0.f;
+  if (cand_in) {
+    // ---- 0-2 from candidate lists: the units' kCandListCount lists hold the C best entries
+    //      (order key of the score, position) among them; sort them all, keep the C largest, and
+    //      put those in position order (their scores: the keys' floats)
+    const uint64_t* src = cand_in + (size_t)blockIdx.x * kCandListCount * list_stride;
+    const int n_in = kCandListCount * list_stride;
+    int n2 = 1;
+    while (n2 < n_in) n2 <<= 1;
+    uint64_t* ent = reinterpret_cast<uint64_t*>(region);
+    for (int i = tid; i < n2; i += kThreads) ent[i] = i < n_in ? src[i] : 0ull;  // 0: no entry
+    __syncthreads();
+    bitonic_sort(ent, n2, tid, kThreads);  // ascending: the best last
+    int nc2 = 1;
+    while (nc2 < C) nc2 <<= 1;
+    // the C best, re-keyed by position, into the front: n2 >= kCandListCount C > nc2 + C, so the
+    // entries read here and the slots written do not overlap
+    for (int i = tid; i < nc2; i += kThreads) {
+      const uint64_t e = i < C ? ent[n2 - 1 - i] : 0ull;
+      ent[i] = i < C ? ((uint64_t)cand_entry_pos(e) << 32) | (uint32_t)(e >> 32) : ~0ull;
+    }
+    __syncthreads();
+    bitonic_sort(ent, nc2, tid, kThreads);  // by position
+    for (int i = tid; i < C; i += kThreads) {
+      cpos[i] = (int32_t)(ent[i] >> 32);
+      cst[i] = key_float((uint32_t)ent[i]);
+    }
+    den = cand_in_max[blockIdx.x];
+    __syncthreads();
+  } else {
 
   // ---- 0. base scores s_i = mu_i + lambda1 sigma_i (one rounding, or given) and their maximum -
   float local_max = -INFINITY;
@@ -590,7 +601,7 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
     __syncthreads();
   }
   __syncthreads();
-  float den = sh.wave_max[0];
+  den = sh.wave_max[0];
 #pragma unroll
   for (int v = 1; v < kWaves; ++v) den = fmaxf(den, sh.wave_max[v]);
   den = fmaxf(den, 1e-12f);
@@ -653,6 +664,17 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
       }
     }
   }
+  __syncthreads();
+  if (cut_out) {
+    // the candidate list of a unit for the selection from lists: list 0 holds the C candidates,
+    // the others nothing
+    uint64_t* dst = cut_out + (size_t)blockIdx.x * kCandListCount * list_stride;
+    for (int i = tid; i < kCandListCount * list_stride; i += kThreads)
+      dst[i] = i < C ? cand_entry(order_key(base_score(cpos[i])), (uint32_t)cpos[i]) : 0ull;
+    if (tid == 0) cut_max[blockIdx.x] = den;
+    return;
+  }
+  }  // phases 0-2
   __syncthreads();  // the staged score keys are dead from here on: the region takes key rows
 
   // ---- 3. greedy admission -------------------------------------------------------------------
@@ -668,9 +690,14 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
     // s~ of every candidate (its base score, pooled as in phase 0, over the normaliser)
     for (int c = tid; c < C; c += kThreads) {
       const int pos = cpos[c];
-      float sv = base_score(pos);
-      for (int j = max(0, pos - pool_h); j <= min(n_cand - 1, pos + pool_h); ++j)
-        sv = fmaxf(sv, base_score(j));
+      float sv;
+      if (cand_in) {
+        sv = cst[c];  // the entry's score (no pooling with candidate lists)
+      } else {
+        sv = base_score(pos);
+        for (int j = max(0, pos - pool_h); j <= min(n_cand - 1, pos + pool_h); ++j)
+          sv = fmaxf(sv, base_score(j));
+      }
       cst[c] = sv / den;
     }
     // Dot products of every pair of candidate keys, k_i . k_j, in 32 x 32 blocks (I, J), I <= J
@@ -861,9 +888,14 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
         const float n2 = key[q].sq_norm();
         inv[q] = n2 > 0.f ? 1.f / sqrtf(n2) : 0.f;  // a zero key has cosine 0 to everything
         cinv[c] = inv[q];
-        float sv = base_score(pos);
-        for (int j = max(0, pos - pool_h); j <= min(n_cand - 1, pos + pool_h); ++j)
-          sv = fmaxf(sv, base_score(j));
+        float sv;
+        if (cand_in) {
+          sv = cst[c];  // the entry's score (no pooling with candidate lists)
+        } else {
+          sv = base_score(pos);
+          for (int j = max(0, pos - pool_h); j <= min(n_cand - 1, pos + pool_h); ++j)
+            sv = fmaxf(sv, base_score(j));
+        }
         st[q] = sv / den;
       }
     }
@@ -1009,14 +1041,22 @@ size_t lds_head(int max_cand) { return ((size_t)max_cand * 12 + 15) & ~(size_t)1
 template <int DT, int D, int NT, int CPT, bool STAGED, bool GRAM>
 hipError_t select_launch(const Shape& s, const SelectArgs& a, size_t body, hipStream_t st) {
   using T = typename Elem<DT>::T;
-  const size_t region = std::max(body, STAGED ? (size_t)a.max_cand_all * 4 : (size_t)0);
+  size_t lists = 0;  // the merge of candidate lists: a power of two of entries
+  if (a.cand_in) {
+    size_t n2 = 1;
+    while (n2 < (size_t)kCandListCount * a.list_stride) n2 <<= 1;
+    lists = n2 * sizeof(uint64_t);
+  }
+  const size_t region =
+      std::max(std::max(body, STAGED ? (size_t)a.max_cand_all * 4 : (size_t)0), lists);
   const size_t dyn = lds_head(a.max_cand) + region;
   auto kern = mmr_select_kernel<DT, D, NT, CPT, STAGED, GRAM>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
   if (e != hipSuccess) return e;
   kern<<<dim3((unsigned)(s.n_prob * s.h_kv)), NT, dyn, st>>>(
-      a.mu, a.sigma, a.score, static_cast<const T*>(a.k), s.lens, s.tok_off,
+      a.mu, a.sigma, a.score, a.cand_in, a.cand_in_max, a.cut_out, a.cut_max, a.list_stride,
+      static_cast<const T*>(a.k), s.lens, s.tok_off,
       a.lambda1, a.lambda2,
       a.pool / 2, a.w_mu, s.h_kv,
       a.budget, a.budgets, a.cand_mult, a.keep_tail, a.cand_stride, a.max_cand, a.sel_idx, a.sel_score,

@@ -68,7 +68,19 @@ struct StreamArgs {
   float* score;
   const float* lambda1;
   float w_mu;
+  // candidate mode of pass 2 (every unit one segment): per unit the waves' candidate lists,
+  // [n_units][kCandLists][cand_stride] entries (0: none), and the maximum base score over the
+  // candidate positions clamped at 1e-12 (the selection's normaliser); C_p = min(cand_mult B_p,
+  // L_p - keep_tail), B_p = budgets[p] or budget
+  uint64_t* cand_out;
+  float* cand_max;
+  int cand_stride;
+  int budget, cand_mult, keep_tail;
+  const int32_t* budgets;
 };
+
+constexpr int kCandLists = kWaves;  // candidate lists per unit: one per wave of the fused kernel
+static_assert(kCandLists == kCandListCount, "candidate list count");
 
 template <int D, int NB> struct SGeo {
   static constexpr int R = NB * 32;          // window rows of a unit (G heads x 32)
@@ -100,6 +112,11 @@ __device__ __forceinline__ float sum_halves(float x) {  // x + x of lane ^ 32
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+__device__ __forceinline__ float max_halves(float x) {  // max(x, x of lane ^ 32)
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 // s_waitcnt vmcnt(later NDMA + (stores ? TS : 0)) for a run-time later in [0, 3]
 template <int NDMA, int TS>
 __device__ __forceinline__ void wait_vmem_tiles(int later, bool stores) {
@@ -128,8 +145,14 @@ template <int D, int NB, int NW, int S> struct KeyStream {
   uint16_t* ring;       // this wave's S tiles
   const uint16_t* kg;   // keys of the unit
   int k0, k1, wave, lane;
+  // nullptr: tile j of the wave is the segment's tile j NW + wave; otherwise order[j NW + wave]
+  // (LDS) names it
+  const uint16_t* order = nullptr;
 
-  __device__ int tile_key(int j) const { return k0 + (j * NW + wave) * kTileKeys; }
+  __device__ int tile_key(int j) const {
+    const int t = order ? (int)order[j * NW + wave] : j * NW + wave;
+    return k0 + t * kTileKeys;
+  }
 
   // tile j into its slot; rows past the segment end re-read its last key
   __device__ __forceinline__ void issue(int j) const {

@@ -97,6 +97,128 @@ __device__ __forceinline__ float2 merge_waves(const float2* red, int row) {
   return v;
 }
 
+// Score bounds of pass 1 in candidate mode (stream_prune.hip).  For each tile, with the running
+// normaliser b' <= b of every window row (the larger of the lane's own running log-sum-exp over
+// its keys and the workgroup's total at the last checkpoint), every key of the tile has
+//   a[h][r] = 2^(t - b) <= 2^(tmax[h][r] - b') =: a'[h][r]   (tmax: the tile's largest logit),
+// hence mu <= (1 / 32) sum_r abar'[r] (abar' = mean over the G heads) and, since a variance is at
+// most the mean square, sigma <= sqrt(sum_r abar'[r]^2 / 31) (sum_{h,r} a'^2 / (32 G - 1) for the
+// dispersion over all rows).  The bound of s = w_mu mu + lambda1 sigma (section 3.2, Eq. (5))
+// takes the positive parts of w_mu and lambda1, widened by kBoundSlack for the rounding of both
+// passes and kept above kBoundFloor.  A tile with a masked key gets +inf (always revisited).
+constexpr int kCkptTiles = 4;                       // tiles per wave between checkpoints
+constexpr float kBoundSlack = 1.00390625f;          // 1 + 2^-8
+constexpr float kBoundFloor = 0x1p-100f;
+struct Bound {
+  float* ub;       // [n_tiles] LDS: bound of tile i of the unit
+  float2* red;     // [NW][R] LDS: the waves' (m, z) at a checkpoint
+  float* tot_l;    // [R] LDS: the workgroup's log-sum-exp per row at the last checkpoint
+  float wmu_p, lam1_p;  // positive parts of w_mu and lambda1
+  float inv_g, inv_n1;  // 1 / G; 1 / 31 or 1 / (32 G - 1)
+};
+
+// Pass 1 of candidate mode over a whole unit (k1 = L): the statistics of stats_tiles and, per
+// tile, its score bound into bd.ub.  Every kCkptTiles tiles, while every wave still has tiles
+// (j + 1 < min_tiles), the waves merge their running statistics into bd.tot_l (two barriers).
+template <int D, int NB, bool ALL, int NW, int S>
+__device__ __forceinline__ void stats_bound_tiles(const KeyStream<D, NB, NW, S>& ks,
+                                                  const bf16x8_t (&q)[NB][D / 16], int my_tiles,
+                                                  int min_tiles, int L, float c, int l32, int half,
+                                                  float (&m_run)[NB], float (&z_run)[NB],
+                                                  const Bound& bd) {
+  constexpr int NS = D / 16, R = NB * 32;
+  const int lane = threadIdx.x & 63;
+  float tot[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    m_run[b] = -INFINITY;
+    z_run[b] = 0.f;
+    tot[b] = -INFINITY;
+  }
+  const int kedge = L - 31;
+  for (int j = 0; j < my_tiles; ++j) {
+    bf16x8_t kt[NS];
+    ks.template next<0>(kt, j, my_tiles, l32, half);
+    const int t0 = ks.tile_key(j);
+    const int tile = j * NW + ks.wave;
+    if (t0 + 31 < kedge) {
+      float tmax[NB];
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const f32x16_t d = chain<NS>(kt, q[b]);
+        float mx = fmax3(fmax3(fmax3(d[0], d[1], d[2]), d[3], d[4]), d[5], d[6]);
+        mx = fmax3(fmax3(mx, d[7], d[8]), d[9], d[10]);
+        mx = fmax3(fmax3(mx, d[11], d[12]), d[13], d[14]);
+        tmax[b] = __builtin_elementwise_maximum(mx, d[15]);
+        const float mn = __builtin_elementwise_maximum(m_run[b], tmax[b] * c);
+        const float keep = __builtin_amdgcn_exp2f(m_run[b] - mn);  // 0 on the lane's first tile
+        float ex[16];
+#pragma unroll
+        for (int jj = 0; jj < 16; ++jj) ex[jj] = __builtin_amdgcn_exp2f(fmaf(d[jj], c, -mn));
+        float zs[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) zs[u] = (ex[4 * u] + ex[4 * u + 1]) + (ex[4 * u + 2] + ex[4 * u + 3]);
+        z_run[b] = fmaf(z_run[b], keep, (zs[0] + zs[1]) + (zs[2] + zs[3]));
+        m_run[b] = mn;
+      }
+      float p1 = 0.f, p2 = 0.f;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const float tm = max_halves(tmax[b]) * c;
+        const float own = m_run[b] + __builtin_amdgcn_logf(z_run[b]);
+        const float a = __builtin_amdgcn_exp2f(tm - fmaxf(own, tot[b]));
+        p1 += a;
+        if constexpr (ALL) p2 = fmaf(a, a, p2);
+      }
+      p1 *= bd.inv_g;
+      if constexpr (!ALL) p2 = p1 * p1;
+#pragma unroll
+      for (int off = 1; off < 32; off <<= 1) {  // over the 32 rows of each half
+        p1 += __shfl_xor(p1, off, 64);
+        p2 += __shfl_xor(p2, off, 64);
+      }
+      if (lane == 0)
+        bd.ub[tile] = fmaf(fmaf(bd.lam1_p, __builtin_sqrtf(p2 * bd.inv_n1),
+                                bd.wmu_p * (p1 * (1.f / 32.f))),
+                           kBoundSlack, kBoundFloor);
+    } else {
+      // the guarded path of stats_tiles (k1 = L)
+      const int thr = L - 32 + l32 - t0 - 4 * half;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        f32x16_t d = chain<NS>(kt, q[b]);
+#pragma unroll
+        for (int jj = 0; jj < 16; ++jj)
+          if (8 * (jj >> 2) + (jj & 3) > thr) d[jj] = -INFINITY;
+        float mx = d[0];
+#pragma unroll
+        for (int jj = 1; jj < 16; ++jj) mx = fmaxf(mx, d[jj]);
+        const float mn = fmaxf(m_run[b], mx * c);
+        if (mn != -INFINITY) {
+          const float keep = m_run[b] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[b] - mn);
+          float z = z_run[b] * keep;
+#pragma unroll
+          for (int jj = 0; jj < 16; ++jj) z += __builtin_amdgcn_exp2f(fmaf(d[jj], c, -mn));
+          z_run[b] = z;
+          m_run[b] = mn;
+        }
+      }
+      if (lane == 0) bd.ub[tile] = INFINITY;
+    }
+    if ((j + 1) % kCkptTiles == 0 && j + 1 < min_tiles) {
+      stats_to_lds<NB>(m_run, z_run, bd.red + ks.wave * R, l32, half);
+      __syncthreads();
+      if ((int)threadIdx.x < R) {
+        const float2 v = merge_waves<NW, R>(bd.red, threadIdx.x);
+        bd.tot_l[threadIdx.x] = v.x + __builtin_amdgcn_logf(v.y);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int b = 0; b < NB; ++b) tot[b] = bd.tot_l[b * 32 + l32];
+    }
+  }
+}
+
 // One mu or sigma value to HBM with the device-scope store policy (sc1).  These 128-byte pieces
 // trickle out between the key loads of a stream that keeps HBM busy; on MI355X the default policy
 // costs about 0.03 ms more per 2 GiB pass (the values are the same).  The store is counted by the
@@ -111,20 +233,195 @@ struct ScoreOut {
   float lam1, w_mu;
 };
 
+// What pass 2 writes per key: mu and sigma, the base score, or nothing (candidate mode: the key's
+// base score only enters the wave's candidate list below).
+enum PassOut { kOutMuSigma = 0, kOutScore = 1, kOutCand = 2 };
+
+// Candidate list of one wave in the second pass of candidate mode.  The unit's candidate set is
+// the C keys with the largest base scores, ties to the lower position (section 3.2, the top-4B
+// restriction); it is the top C of the union of every wave's own top C.  A wave keeps, in LDS,
+// every key whose entry (order key of its score, position) beats the C-th best entry among the
+// wave's earlier keys (a lower bound of the unit's final cut) and a bound shared by the waves, and
+// when the list fills it sorts the list in registers and keeps the best C.
+constexpr int kCandCap = 320;              // entries per wave: 1920 bytes of LDS
+constexpr int kCandMax = kCandCap - 32;    // largest C (a tile appends at most 32 entries)
+static_assert(kCandMax == kCandMaxC, "the host's limit on C");
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
+  const uint32_t lo = __shfl_xor((uint32_t)v, m, 64), hi = __shfl_xor((uint32_t)(v >> 32), m, 64);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Descending bitonic sort of 512 entries held by one wave, 8 per lane (entry lane * 8 + i in v[i]).
+__device__ __forceinline__ void wave_sort_desc_512(uint64_t (&v)[8], int lane) {
+#pragma unroll
+  for (int k = 2; k <= 512; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      if (j >= 8) {
+        // partner in lane ^ (j / 8), same register
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const uint64_t o = shfl_xor_u64(v[i], j >> 3);
+          const int idx = lane * 8 + i;
+          // blocks with (idx & k) == 0 end descending; the pair's lower index keeps the larger
+          const bool take_max = ((idx & j) == 0) == ((idx & k) == 0);
+          v[i] = take_max ? (o > v[i] ? o : v[i]) : (o < v[i] ? o : v[i]);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          if ((i & j) == 0) {
+            const int p = i | j;
+            const bool desc = ((lane * 8 + i) & k) == 0;
+            const uint64_t a = v[i], b = v[p];
+            const bool sw = desc ? (a < b) : (a > b);
+            v[i] = sw ? b : a;
+            v[p] = sw ? a : b;
+          }
+        }
+      }
+    }
+  }
+}
+
+struct CandList {
+  uint32_t* okey;  // [kCandCap] LDS: order key of the entry's score
+  uint16_t* pos;   // [kCandCap] LDS: its position (units of at most 65535 keys)
+  int C;           // the unit's candidate count, 1..kCandMax
+  int n;           // entries held (wave-uniform)
+  uint64_t thr;    // once `bounded`, an entry must be larger than this one
+  bool bounded;
+  float smax;      // the lane's running maximum of its candidate positions' scores (NaN ignored)
+
+  // Sort the held entries and keep the best C (n > C).
+  __device__ __forceinline__ void compact(int lane) {
+    uint64_t v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int idx = lane * 8 + i;
+      v[i] = idx < n ? cand_entry(okey[idx], pos[idx]) : 0ull;  // real entries are > 0
+    }
+    wave_sort_desc_512(v, lane);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int idx = lane * 8 + i;
+      if (idx < C) {
+        okey[idx] = (uint32_t)(v[i] >> 32);
+        pos[idx] = (uint16_t)cand_entry_pos(v[i]);
+      }
+    }
+    // the C-th best entry: register (C - 1) % 8 of lane (C - 1) / 8
+    uint64_t t = v[0];
+#pragma unroll
+    for (int i = 1; i < 8; ++i)
+      if (((C - 1) & 7) == i) t = v[i];
+    const int src = (C - 1) >> 3;
+    // (readlane returns int: both halves go through uint32_t, or the low one sign-extends)
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((uint32_t)(t >> 32), src);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((uint32_t)t, src);
+    thr = ((uint64_t)hi << 32) | lo;
+    bounded = true;
+    n = C;
+  }
+
+  // One key per lane of half 0 (valid: a candidate position); every lane of the wave calls it.
+  __device__ __forceinline__ void add(float sv, int key, bool valid, int lane) {
+    if (valid) smax = fmaxf(smax, sv);
+    const uint32_t ok = order_key(sv);
+    const bool in = valid && (!bounded || cand_entry(ok, (uint32_t)key) > thr);
+    const uint64_t m = __ballot(in);
+    if (m != 0ull) {
+      // entries of the lanes below this one
+      const int slot = n + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                           __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      if (in) {
+        okey[slot] = ok;
+        pos[slot] = (uint16_t)key;
+      }
+      n += (int)__popcll(m);
+      if (n > kCandMax) compact(lane);
+    }
+  }
+};
+
+// Shared state of the second pass of candidate mode (stream_prune.hip), which revisits the unit's
+// tiles in decreasing order of their score bound and stops at the first tile whose bound is below
+// the unit's cut: the order key of the C-th best base score among the keys evaluated so far,
+// rounded down to its bin of an LDS histogram of those keys (a lower bound of the final cut, so
+// no key left out can be among the C best).
+constexpr int kPruneShift = 21;                     // histogram bin = order key >> kPruneShift
+constexpr int kPruneBins = 1 << (32 - kPruneShift);
+struct Prune {
+  CandList cl;           // the wave's candidate list
+  const float* ubs;      // [n_tiles] LDS: score bound of the i-th tile of the order
+  uint32_t* hist;        // [kPruneBins] LDS: evaluated candidate keys per bin
+  uint32_t* cut;         // LDS: the unit's current cut (an order key; 0: none yet)
+  uint32_t* top_bin;     // LDS: a bin at or above every nonempty one
+  int n_cand;
+
+  // The wave's next tile is worth evaluating (its bound is not below the cut).
+  __device__ __forceinline__ bool wanted(int idx) const {
+    const uint32_t c = __builtin_amdgcn_readfirstlane(*cut);
+    const uint32_t u = __builtin_amdgcn_readfirstlane(order_key(ubs[idx]));
+    return u >= c;
+  }
+
+  // The evaluated candidate keys of a tile (one per lane of half 0) into the histogram and the
+  // list; the list takes only keys at or above the cut.
+  __device__ __forceinline__ void add(float sv, int key, bool valid, int lane) {
+    const uint32_t ok = order_key(sv);
+    wave_hist_add(hist, ok >> kPruneShift, valid);
+    uint32_t hb = valid ? ok >> kPruneShift : 0u;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) hb = max(hb, (uint32_t)__shfl_xor((int)hb, off, 64));
+    if (lane == 0) atomicMax(top_bin, hb);
+    const uint32_t c = __builtin_amdgcn_readfirstlane(*cut);
+    cl.add(sv, key, valid && ok >= c, lane);
+  }
+
+  // Raise the cut to the lower edge of the bin that holds the C-th best evaluated key (the
+  // histogram as this wave sees it: counts only grow, so a stale view gives a lower cut).
+  __device__ __forceinline__ void update_cut(int lane) {
+    int b0 = (int)__builtin_amdgcn_readfirstlane(*top_bin);
+    uint32_t cum = 0;
+    for (; b0 >= 0; b0 -= 64) {
+      const int b = b0 - lane;
+      uint32_t pre = b >= 0 ? hist[b] : 0u;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t o = (uint32_t)__shfl_up((int)pre, off, 64);
+        if (lane >= off) pre += o;
+      }
+      const uint64_t hit = __ballot(cum + pre >= (uint32_t)cl.C);
+      if (hit) {
+        const int bin = b0 - (__ffsll((unsigned long long)hit) - 1);
+        if (lane == 0) atomicMax(cut, (uint32_t)bin << kPruneShift);
+        return;
+      }
+      cum += (uint32_t)__builtin_amdgcn_readlane((int)pre, 63);
+    }
+  }
+};
+
 // Pass 2 over the wave's tiles of a segment: logits again with keys as the MFMA N dimension (a
 // lane holds one key), a = 2^(t - b) with the row normalisers b = M + log2 Z read from bsh, summed
 // over the group's heads, then the mean and the two-pass sample variance over the 32 window rows,
 // stored as mu / sigma (mu_u, sigma_u: the unit's rows).  With ALL the variance runs over all
 // G x 32 (head, row) values: every head's mean and squared deviations over its 32 rows, merged
-// across heads with the pairwise update of Chan, Golub and LeVeque.  With SC the key's base score
-// s = fma(lam1, sigma, w_mu mu) (section 3.2, Eq. (5)) is stored instead, with the same rounding
-// as a score formed later from the stored mu and sigma.
-template <int D, int NB, bool ALL, int NW, int S, bool SC = false>
+// across heads with the pairwise update of Chan, Golub and LeVeque.  With OUT = kOutScore the
+// key's base score s = fma(lam1, sigma, w_mu mu) (section 3.2, Eq. (5)) is stored instead, with the
+// same rounding as a score formed later from the stored mu and sigma; with OUT = kOutCand the
+// score goes to the candidate state `pr` (keys below n_cand), nothing is stored, and the wave
+// stops at its first tile that pr no longer wants.
+template <int D, int NB, bool ALL, int NW, int S, int OUT = kOutMuSigma>
 __device__ __forceinline__ void mu_sigma_tiles(const KeyStream<D, NB, NW, S>& ks,
                                                const bf16x8_t (&q)[NB][D / 16], const float* bsh,
                                                int my_tiles, int k1, int L, float c, float inv_g,
                                                float* mu_u, float* sigma_u, int l32, int half,
-                                               ScoreOut so = {}) {
+                                               ScoreOut so = {}, Prune* pr = nullptr) {
+  constexpr int kStores = OUT == kOutCand ? 0 : 1;  // global stores per tile (the waits count them)
+  const int lane = threadIdx.x & 63;
   constexpr int NS = D / 16;
   auto tile = [&](const bf16x8_t (&kt)[NS], int t0, auto masked) __attribute__((always_inline)) {
     const int key = t0 + l32;
@@ -190,21 +487,29 @@ __device__ __forceinline__ void mu_sigma_tiles(const KeyStream<D, NB, NW, S>& ks
       }
       var = sum_halves((vp[0] + vp[1]) + (vp[2] + vp[3])) * (1.f / 31.f);
     }
-    if constexpr (SC) {
-      // both halves hold the key's mean and variance; half 0 stores
+    if constexpr (OUT == kOutScore) {
+      // both halves hold the key's mean and variance; half 0 stores (every tile has a key < k1,
+      // so the store the waits count is issued)
       const float sv = fmaf(so.lam1, __builtin_amdgcn_sqrtf(var), so.w_mu * mean);
       if (half == 0 && key < k1) store_stat(so.score_u + key, sv);
+    } else if constexpr (OUT == kOutCand) {
+      const float sv = fmaf(so.lam1, __builtin_amdgcn_sqrtf(var), so.w_mu * mean);
+      pr->add(sv, key, half == 0 && key < pr->n_cand, lane);
     } else {
       if (key < k1) store_stat((half == 0 ? mu_u : sigma_u) + key, half == 0 ? mean : __builtin_amdgcn_sqrtf(var));
     }
   };
 
   for (int j = 0; j < my_tiles; ++j) {
+    if constexpr (OUT == kOutCand) {
+      if (!pr->wanted(j * NW + ks.wave)) break;
+    }
     bf16x8_t kt[NS];
-    ks.template next<1>(kt, j, my_tiles, l32, half);  // one mu / sigma store per tile
+    ks.template next<kStores>(kt, j, my_tiles, l32, half);  // stores per tile in flight
     const int t0 = ks.tile_key(j);
     if (t0 + 31 > L - 32) tile(kt, t0, std::true_type{});
     else tile(kt, t0, std::false_type{});
+    if constexpr (OUT == kOutCand) pr->update_cut(lane);
   }
 }
 

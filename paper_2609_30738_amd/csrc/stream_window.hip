@@ -4,19 +4,21 @@
 // queries still in registers and the first key tiles of pass 2 loaded while the waves' statistics
 // are merged; no workgroup waits for any other.  The per-segment loops are in stream_passes.h.
 //
-// In base-score mode (SC) pass 2 keeps mu and sigma in registers and stores only each key's base
-// score (section 3.2, Eq. (5)): half the bytes, which trickle out between the key loads of a
-// stream that keeps HBM busy, and the selection reads one array instead of two.
+// In base-score mode (OUT = kOutScore) pass 2 keeps mu and sigma in registers and stores only
+// each key's base score (section 3.2, Eq. (5)): half the bytes, which trickle out between the key
+// loads of a stream that keeps HBM busy, and the selection reads one array instead of two.  The
+// candidate mode, which stores nothing per key, has its own kernel (stream_prune.hip).
 #include "stream_passes.h"
 
 namespace kv {
 namespace stream {
 namespace {
 
-template <int D, int NB, bool ALL, int NW, int S, bool SC>
+template <int D, int NB, bool ALL, int NW, int S, int OUT>
 __global__ __launch_bounds__(NW * 64, 1) void window_stream_kernel(StreamArgs a) {
   using Gm = SGeo<D, NB>;
   constexpr int R = Gm::R, NS = Gm::NS;
+  static_assert(OUT != kOutCand, "candidate mode: stream_prune.hip");
   __shared__ __align__(16) uint16_t ring[NW][S * Gm::TE];
   __shared__ float2 red[NW][R];
   __shared__ __align__(16) float bsh[R];
@@ -52,10 +54,10 @@ __global__ __launch_bounds__(NW * 64, 1) void window_stream_kernel(StreamArgs a)
     bsh[threadIdx.x] = v.x + __builtin_log2f(v.y);  // b = M + log2 Z, base 2
   }
   __syncthreads();
-  if constexpr (SC) {
+  if constexpr (OUT == kOutScore) {
     const ScoreOut so{a.score + stat_base, a.lambda1[p], a.w_mu};
-    mu_sigma_tiles<D, NB, ALL, NW, S, true>(ks, q, bsh, my_tiles, L, L, c, inv_g, nullptr, nullptr,
-                                            l32, half, so);
+    mu_sigma_tiles<D, NB, ALL, NW, S, kOutScore>(ks, q, bsh, my_tiles, L, L, c, inv_g, nullptr,
+                                                 nullptr, l32, half, so);
   } else {
     mu_sigma_tiles<D, NB, ALL, NW, S>(ks, q, bsh, my_tiles, L, L, c, inv_g, a.mu + stat_base,
                                       a.sigma + stat_base, l32, half);
@@ -74,11 +76,11 @@ template <int D, int NB> struct WindowLaunch {
   static hipError_t run(const Shape& s, const StreamArgs& args, hipStream_t st) {
     const dim3 grid(1, s.h_kv, s.n_prob);
     if (args.score) {
-      if (args.sigma_all) window_stream_kernel<D, NB, true, kWaves, 2, true><<<grid, kThreads, 0, st>>>(args);
-      else window_stream_kernel<D, NB, false, kWaves, 2, true><<<grid, kThreads, 0, st>>>(args);
+      if (args.sigma_all) window_stream_kernel<D, NB, true, kWaves, 2, kOutScore><<<grid, kThreads, 0, st>>>(args);
+      else window_stream_kernel<D, NB, false, kWaves, 2, kOutScore><<<grid, kThreads, 0, st>>>(args);
     } else {
-      if (args.sigma_all) window_stream_kernel<D, NB, true, kWaves, 2, false><<<grid, kThreads, 0, st>>>(args);
-      else window_stream_kernel<D, NB, false, kWaves, 2, false><<<grid, kThreads, 0, st>>>(args);
+      if (args.sigma_all) window_stream_kernel<D, NB, true, kWaves, 2, kOutMuSigma><<<grid, kThreads, 0, st>>>(args);
+      else window_stream_kernel<D, NB, false, kWaves, 2, kOutMuSigma><<<grid, kThreads, 0, st>>>(args);
     }
     return hipGetLastError();
   }

@@ -142,7 +142,7 @@ __global__ __launch_bounds__(NW * 64, 1) void window_coop_kernel(StreamArgs a, u
   __syncthreads();
   if constexpr (SC) {
     const ScoreOut so{a.score + stat_base, a.lambda1[p], a.w_mu};
-    mu_sigma_tiles<D, NB, ALL, NW, S, true>(ks, q, bsh, my_tiles, k1, L, c, inv_g, nullptr, nullptr,
+    mu_sigma_tiles<D, NB, ALL, NW, S, kOutScore>(ks, q, bsh, my_tiles, k1, L, c, inv_g, nullptr, nullptr,
                                             l32, half, so);
   } else {
     mu_sigma_tiles<D, NB, ALL, NW, S>(ks, q, bsh, my_tiles, k1, L, c, inv_g, a.mu + stat_base,

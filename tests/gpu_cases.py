@@ -46,11 +46,14 @@ def run_gpu(wl: workloads.Workload, problems: Optional[Sequence[int]] = None, *,
             pool: int = 1, w_mu: float = 1.0, sigma_rows: str = "group_mean",
             budgets: Optional[Sequence[int]] = None, redraw: Optional[certify.Redraw] = None,
             case: Optional[str] = None, timed: bool = False) -> GpuRun:
-    """One pass through the C ABI.  timed=True runs the benchmark's calls (kv_window_base_scores,
-    then kv_mmr_select_scored with the compaction: row_max, row_sum, score, sel_idx, k_out, v_out)
-    and, on the same inputs, kv_window_mu_sigma_ex and kv_mmr_select_ex with the optional outputs
-    (mu, sigma, sel_score, cand_idx, cand_corr; their row statistics and sel_idx as row_max_plain,
-    row_sum_plain, sel_idx_plain)."""
+    """One pass through the C ABI.  timed=True runs the benchmark's calls (kv_window_candidates,
+    then kv_mmr_select_candidates with the compaction: row_max, row_sum, sel_idx, k_out, v_out;
+    where the candidate path does not apply, pool > 1 or too many candidates,
+    kv_window_base_scores and kv_mmr_select_scored take its place) and, on the same inputs,
+    kv_mmr_select_candidates again with the optional outputs (cands_*), kv_window_base_scores and
+    kv_mmr_select_scored (score, *_scored), and kv_window_mu_sigma_ex and kv_mmr_select_ex with the
+    optional outputs (mu, sigma, sel_score, cand_idx, cand_corr; their row statistics and sel_idx
+    as row_max_plain, row_sum_plain, sel_idx_plain)."""
     import torch
     probs = list(range(wl.n_prob)) if problems is None else list(problems)
     print(f"[gpu case] {case or wl.name} problems={len(probs)} fused={fused} timed={timed} "
@@ -80,12 +83,36 @@ def run_gpu(wl: workloads.Workload, problems: Optional[Sequence[int]] = None, *,
         score = torch.empty_like(out.mu)
         wsb = _lib.base_scores_workspace_bytes(b)
         ws_sc = torch.empty(max(wsb, 256), dtype=torch.uint8, device=dev)
-        _lib.window_base_scores(b, inp.q_win, inp.k, inp.scale, inp.lambda1, out.row_max,
-                                out.row_sum, score, w_mu=w_mu, sigma_rows=sigma_rows,
-                                ws=ws_sc if wsb > 0 else None)
-        _lib.mmr_select_scored(b, score, inp.k, inp.v, inp.lambda2, B, cand_mult, tail,
-                               out.sel_idx, k_out=out.k_out, v_out=out.v_out, pool=pool,
-                               budgets=budgets_dev)
+        wcb = _lib.candidates_workspace_bytes(b, B, cand_mult, tail, w_mu=w_mu,
+                                              budgets=budgets_dev) if pool == 1 else 0
+        if wcb > 0:
+            ws_c = torch.empty(wcb, dtype=torch.uint8, device=dev)
+            _lib.window_candidates(b, inp.q_win, inp.k, inp.scale, inp.lambda1, B, cand_mult, tail,
+                                   out.row_max, out.row_sum, ws_c, w_mu=w_mu, budgets=budgets_dev,
+                                   sigma_rows=sigma_rows)
+            _lib.mmr_select_candidates(b, ws_c, inp.k, inp.v, inp.lambda2, B, cand_mult, tail,
+                                       out.sel_idx, k_out=out.k_out, v_out=out.v_out,
+                                       budgets=budgets_dev)
+            full = {n: torch.empty_like(getattr(out, n))
+                    for n in ("sel_idx", "sel_score", "cand_idx", "cand_corr")}
+            _lib.mmr_select_candidates(b, ws_c, inp.k, None, inp.lambda2, B, cand_mult, tail,
+                                       full["sel_idx"], full["sel_score"], full["cand_idx"],
+                                       full["cand_corr"], budgets=budgets_dev)
+            extra.update({"cands_" + n: x for n, x in full.items()})
+            rm_s, rs_s = torch.empty_like(out.row_max), torch.empty_like(out.row_sum)
+            sel_s = torch.empty_like(out.sel_idx)
+            _lib.window_base_scores(b, inp.q_win, inp.k, inp.scale, inp.lambda1, rm_s, rs_s, score,
+                                    w_mu=w_mu, sigma_rows=sigma_rows, ws=ws_sc if wsb > 0 else None)
+            _lib.mmr_select_scored(b, score, inp.k, None, inp.lambda2, B, cand_mult, tail, sel_s,
+                                   pool=pool, budgets=budgets_dev)
+            extra.update(row_max_scored=rm_s, row_sum_scored=rs_s, sel_idx_scored=sel_s)
+        else:
+            _lib.window_base_scores(b, inp.q_win, inp.k, inp.scale, inp.lambda1, out.row_max,
+                                    out.row_sum, score, w_mu=w_mu, sigma_rows=sigma_rows,
+                                    ws=ws_sc if wsb > 0 else None)
+            _lib.mmr_select_scored(b, score, inp.k, inp.v, inp.lambda2, B, cand_mult, tail,
+                                   out.sel_idx, k_out=out.k_out, v_out=out.v_out, pool=pool,
+                                   budgets=budgets_dev)
         plain = torch.empty_like(out.sel_idx)
         rm, rs = torch.empty_like(out.row_max), torch.empty_like(out.row_sum)
         _lib.window_mu_sigma_ex(b, inp.q_win, inp.k, inp.scale, sigma_rows, rm, rs, out.mu,
@@ -185,9 +212,12 @@ def check_problem(run: GpuRun, j: int, res: Optional[evict.ProblemResult] = None
         # the timed path's row statistics and base scores are those of the mu / sigma path, bit
         # for bit
         for name in ("row_max", "row_sum"):
-            assert np.array_equal(H[name][j * rows:(j + 1) * rows].view(np.uint32),
-                                  H[name + "_plain"][j * rows:(j + 1) * rows].view(np.uint32)), (
-                f"{where}: {name} of kv_window_base_scores and kv_window_mu_sigma_ex differ")
+            for other in ("_plain", "_scored"):
+                if name + other in H:
+                    assert np.array_equal(
+                        H[name][j * rows:(j + 1) * rows].view(np.uint32),
+                        H[name + other][j * rows:(j + 1) * rows].view(np.uint32)), (
+                        f"{where}: {name} of the timed calls and {name + other} differ")
         sc = H["score"][tok * wl.h_kv:(tok + L) * wl.h_kv].reshape(wl.h_kv, L)
         for g in heads:
             compare.assert_fma_f32(sc[g], float(run.lam1[j]), sg[g], np.float32(run.opts.w_mu) * mu[g],
@@ -218,7 +248,20 @@ def check_problem(run: GpuRun, j: int, res: Optional[evict.ProblemResult] = None
         assert np.all(cand[len(live):] == -1) and np.all(np.diff(live) > 0), f"{where} g={g}: cand"
         if "sel_idx_plain" in H:
             assert np.array_equal(H["sel_idx_plain"][o * B:o * B + Bp], sel), (
-                f"{where} g={g}: kv_mmr_select_ex and kv_mmr_select_scored disagree")
+                f"{where} g={g}: kv_mmr_select_ex and the timed selection disagree")
+        if "sel_idx_scored" in H:
+            assert np.array_equal(H["sel_idx_scored"][o * B:(o + 1) * B],
+                                  H["sel_idx"][o * B:(o + 1) * B]), (
+                f"{where} g={g}: kv_mmr_select_scored and kv_mmr_select_candidates disagree")
+        if "cands_sel_idx" in H:
+            # the optional outputs from candidate lists are kv_mmr_select_ex's, bit for bit
+            for n, lo, hi in (("sel_idx", o * B, (o + 1) * B), ("sel_score", o * B, (o + 1) * B),
+                              ("cand_idx", o * stride, (o + 1) * stride),
+                              ("cand_corr", o * stride, (o + 1) * stride)):
+                ref_n = "sel_idx_plain" if n == "sel_idx" else n
+                assert np.array_equal(H["cands_" + n][lo:hi].view(np.uint32),
+                                      H[ref_n][lo:hi].view(np.uint32)), (
+                    f"{where} g={g}: {n} of kv_mmr_select_candidates and kv_mmr_select_ex differ")
         else:
             assert np.all(H["sel_score"][o * B + Bp:(o + 1) * B] == 0), f"{where} g={g}: padding"
         rep = compare.check_selection(

@@ -371,3 +371,78 @@ def test_select_scored_checks():
     assert call(cand_mult=1 << 30) == _lib.KV_ERR_ARG
     assert call(k=ctypes.c_void_p(BUF.ctypes.data + 4)) == _lib.KV_ERR_ARG
     assert call(score=ctypes.c_void_p(BUF.ctypes.data + 4)) == _lib.KV_ERR_ARG
+
+
+def test_candidates_checks():
+    """kv_window_candidates / kv_mmr_select_candidates: a workspace of candidate lists (and of the
+    scores when the window pass cannot keep the lists), argument checks before any launch."""
+    lib = _lib.lib()
+    big = HostProblem(lens=(32768,) * 32)  # 256 units, each one workgroup of the window kernel
+    units = 32 * 8
+
+    def lists(stride):
+        return units * 8 * stride * 8  # 8 lists of `stride` 8-byte entries per unit
+
+    norm = (units * 4 + 255) // 256 * 256
+    scores = 32 * 32768 * 8 * 4
+    assert lib.kv_candidates_workspace_bytes(big.ref(), 64, 4, 32, None) == lists(256) + norm
+    # 512 candidates exceed a wave's list: the scores go through the workspace
+    assert lib.kv_candidates_workspace_bytes(big.ref(), 128, 4, 32, None) >= (
+        lists(512) + norm + scores)
+    f32 = HostProblem(dtype=_lib.KV_F32, lens=(32768,) * 32)
+    assert lib.kv_candidates_workspace_bytes(f32.ref(), 64, 4, 32, None) >= (
+        lists(256) + norm + scores)
+    # cand_mult = 0 (every position a candidate) exceeds the selection's limit; so does pooling
+    assert lib.kv_candidates_workspace_bytes(big.ref(), 64, 0, 32, None) == 0
+    pool3 = _lib.KvSelectOpts(3, 1.0, None, None)
+    assert lib.kv_candidates_workspace_bytes(big.ref(), 64, 4, 32, ctypes.byref(pool3)) == 0
+    assert lib.kv_candidates_workspace_bytes(big.ref(), 0, 4, 32, None) == 0
+
+    pr = HostProblem(lens=(4096,))
+    need = lib.kv_candidates_workspace_bytes(pr.ref(), 64, 4, 32, None)
+    assert need > 0 and need % 256 == 0
+    ws = np.zeros((need + 512) // 4, dtype=np.float32)
+    wsp = ctypes.c_void_p(ws.ctypes.data + (-ws.ctypes.data) % 256)
+    nan = float("nan")
+    bh = np.full(1, 64, dtype=np.int32)
+    half_budgets = _lib.KvSelectOpts(1, 1.0, bh.ctypes.data, None)  # host budgets only
+    w_nan = _lib.KvSelectOpts(1, nan, None, None)
+
+    def window(**kw):
+        opts = kw.get("opts")
+        return lib.kv_window_candidates(
+            kw.get("pr", pr.ref()), kw.get("q", P), kw.get("k", P), kw.get("scale", 0.088),
+            kw.get("lam1", P), kw.get("rows", 0), kw.get("budget", 64), kw.get("cand_mult", 4), 32,
+            None if opts is None else ctypes.byref(opts), kw.get("rm", P), kw.get("rs", P),
+            kw.get("ws", wsp), kw.get("ws_bytes", need), NULL)
+    assert window(pr=None) == _lib.KV_ERR_NULL
+    for kw in (dict(q=NULL), dict(k=NULL), dict(lam1=NULL), dict(rm=NULL), dict(rs=NULL),
+               dict(opts=half_budgets)):
+        assert window(**kw) == _lib.KV_ERR_NULL, kw
+    for kw in (dict(k=ctypes.c_void_p(BUF.ctypes.data + 4)), dict(scale=nan), dict(rows=2),
+               dict(cand_mult=-1), dict(cand_mult=1 << 30), dict(opts=pool3), dict(opts=w_nan)):
+        assert window(**kw) == _lib.KV_ERR_ARG, kw
+    assert window(budget=0) == _lib.KV_ERR_BUDGET
+    assert window(budget=4096) == _lib.KV_ERR_BUDGET
+    assert window(cand_mult=0) == _lib.KV_ERR_SHAPE  # 4064 candidates
+    assert window(ws_bytes=need - 1) == _lib.KV_ERR_WORKSPACE
+    assert window(ws=NULL) == _lib.KV_ERR_WORKSPACE
+    assert window(ws=ctypes.c_void_p(wsp.value + 16)) == _lib.KV_ERR_WORKSPACE
+
+    def select(**kw):
+        opts = kw.get("opts")
+        return lib.kv_mmr_select_candidates(
+            pr.ref(), kw.get("ws", wsp), kw.get("ws_bytes", need), kw.get("k", P), kw.get("v", P),
+            kw.get("lam2", P), kw.get("budget", 64), kw.get("cand_mult", 4), 32,
+            None if opts is None else ctypes.byref(opts), kw.get("sel", P), None, None, None,
+            kw.get("k_out", P), kw.get("v_out", P), NULL)
+    for kw in (dict(sel=NULL), dict(lam2=NULL), dict(k=NULL), dict(k_out=NULL),
+               dict(v_out=NULL), dict(v=NULL)):
+        assert select(**kw) == _lib.KV_ERR_NULL, kw
+    assert select(opts=pool3) == _lib.KV_ERR_ARG
+    assert select(cand_mult=-1) == _lib.KV_ERR_ARG
+    assert select(budget=0) == _lib.KV_ERR_BUDGET
+    assert select(budget=4096) == _lib.KV_ERR_BUDGET
+    # the selection reads only the lists and the normalisers: 8 units x 8 lists x 256 entries
+    assert select(ws_bytes=8 * 8 * 256 * 8 + 256 - 1) == _lib.KV_ERR_WORKSPACE
+    assert select(ws=NULL) == _lib.KV_ERR_WORKSPACE

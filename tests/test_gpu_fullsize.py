@@ -1,7 +1,8 @@
 """GPU parity at the full workload sizes, in the benchmark's launch configuration (every layer of
-every sequence in one batch; kv_window_mu_sigma, then kv_mmr_select_compact, plus kv_mmr_select on
-the same mu / sigma for its optional outputs), against the oracle on every problem and kv head (the
-ragged batch: every problem of two whole sequences).  Inputs carry their stored margin
+every sequence in one batch; kv_window_candidates, then kv_mmr_select_candidates with the
+compaction, and on the same inputs the other scoring routes and kv_mmr_select_ex for the optional
+outputs), against the oracle on every problem and kv head (the ragged batch: every problem of two
+whole sequences).  Inputs carry their stored margin
 certification (tests/certify.py): a head whose cut and greedy the oracle certifies must reproduce
 the oracle exactly; the summary line reports how many are.
 
