@@ -125,10 +125,12 @@ size_t window_ws_bytes(const kv_problem* pr, const kv::Shape& s) {
   return align_up(b);
 }
 
-// Tokens of the batch: sum_p L_p (the rows of mu, sigma and the scores per kv head).
-int64_t total_tokens(const kv_problem* pr) {
+// Token rows that per-token arrays of the batch span (mu, sigma and the scores per kv head):
+// max_p tok_off[p] + L_p, which is sum_p L_p for packed offsets.  Arrays in the workspace are
+// sized by it, so offsets with gaps cannot reach past them.
+int64_t token_extent(const kv_problem* pr) {
   int64_t t = 0;
-  for (int p = 0; p < pr->n_prob; ++p) t += pr->len_host[p];
+  for (int p = 0; p < pr->n_prob; ++p) t = std::max<int64_t>(t, pr->tok_off_host[p] + pr->len_host[p]);
   return t;
 }
 
@@ -142,7 +144,7 @@ bool scores_in_window_pass(const kv_problem* pr, const kv::Shape& s, float scale
 // scale), else the window paths' part and rows of mu and sigma.
 size_t base_scores_ws_bytes(const kv_problem* pr, const kv::Shape& s, bool fused_ok = true) {
   if (fused_ok && scores_in_window_pass(pr, s, 1.f)) return 0;
-  const size_t keys = (size_t)total_tokens(pr) * pr->h_kv;
+  const size_t keys = (size_t)token_extent(pr) * pr->h_kv;
   return window_ws_bytes(pr, s) + 2 * align_up(keys * sizeof(float));
 }
 
@@ -161,12 +163,14 @@ bool cands_in_window_pass(const kv_problem* pr, const kv::Shape& s, float scale,
          s.max_len <= kv::kCandMaxLen;
 }
 
-// Workspace of kv_window_candidates: the lists and the units' normalisers, and without the fused
-// path the scores and what kv_window_base_scores needs after them.
+// Workspace of kv_window_candidates: the lists and the units' normalisers, then with the fused
+// path the tile codes of its first pass, without it the scores and what kv_window_base_scores needs
+// after them.
 size_t cand_ws_bytes(const kv_problem* pr, const kv::Shape& s, int stride, bool fused) {
   const size_t head = cand_lists_bytes(pr, stride) + align_up((size_t)pr->n_prob * pr->h_kv * sizeof(float));
-  if (fused) return head;
-  return head + align_up((size_t)total_tokens(pr) * pr->h_kv * sizeof(float)) +
+  if (fused)
+    return head + align_up((size_t)pr->n_prob * pr->h_kv * kv::cand_code_stride(s) * sizeof(uint32_t));
+  return head + align_up((size_t)token_extent(pr) * pr->h_kv * sizeof(float)) +
          base_scores_ws_bytes(pr, s, false);
 }
 
@@ -439,7 +443,7 @@ int kv_window_base_scores(const kv_problem* pr, const void* q_win, const void* k
     if (st != KV_OK || launched) return st;
   }
   // mu / sigma into the workspace after the window paths' own part, then the scores from them
-  const size_t keys = (size_t)total_tokens(pr) * pr->h_kv;
+  const size_t keys = (size_t)token_extent(pr) * pr->h_kv;
   float* mu = reinterpret_cast<float*>(static_cast<char*>(ws) + win);
   float* sigma = reinterpret_cast<float*>(static_cast<char*>(ws) + win + align_up(keys * sizeof(float)));
   st = kv_window_mu_sigma_ex(pr, q_win, k, scale, sigma_rows, row_max, row_sum, mu, sigma, ws, win,
@@ -547,15 +551,15 @@ int kv_window_candidates(const kv_problem* pr, const void* q_win, const void* k,
   const size_t n_units = (size_t)pr->n_prob * pr->h_kv;
   uint64_t* lists = reinterpret_cast<uint64_t*>(base);
   float* cmax = reinterpret_cast<float*>(base + cand_lists_bytes(pr, stride));
-  if (fused)
-    return launch_status(kv::launch_stream_window_cands(s, stream_plan_of(pr, s), q_win, k, scale,
-                                                        lambda1, w_mu, budget, b_dev, cand_mult,
-                                                        keep_tail, row_max, row_sum, lists, cmax,
-                                                        stride, all, hs));
-  // the scores into the workspace, then the candidate cut of the selection kernel
   const size_t head = cand_lists_bytes(pr, stride) + align_up(n_units * sizeof(float));
+  if (fused)
+    return launch_status(kv::launch_stream_window_cands(
+        s, stream_plan_of(pr, s), q_win, k, scale, lambda1, w_mu, budget, b_dev, cand_mult,
+        keep_tail, row_max, row_sum, lists, cmax, stride, reinterpret_cast<uint32_t*>(base + head),
+        all, hs));
+  // the scores into the workspace, then the candidate cut of the selection kernel
   float* score = reinterpret_cast<float*>(base + head);
-  const size_t score_bytes = align_up((size_t)total_tokens(pr) * pr->h_kv * sizeof(float));
+  const size_t score_bytes = align_up((size_t)token_extent(pr) * pr->h_kv * sizeof(float));
   st = kv_window_base_scores(pr, q_win, k, scale, lambda1, w_mu, sigma_rows, row_max, row_sum,
                              score, base + head + score_bytes, ws_bytes - head - score_bytes,
                              stream);

@@ -78,16 +78,18 @@ hipError_t launch_stream_window_scores(const Shape& s, const StreamPlan& plan, c
 // key << 32 | (0xFFFFFFFF - position) (0: none) whose union holds the unit's C_p best entries, and
 // cand_max [n_units], the largest base score over the candidate positions clamped at 1e-12.  The
 // keys are read once in full; the second pass revisits only the tiles whose score bound reaches
-// the unit's cut.  Units of at most kCandMaxLen keys and C_p <= kCandMaxC.
+// the unit's cut.  codes: scratch of n_units * cand_code_stride(s) words (the first pass's tile
+// codes).  Units of at most kCandMaxLen keys and C_p <= kCandMaxC.
 constexpr int kCandListCount = 8;
 constexpr int kCandMaxC = 288;
 constexpr int kCandMaxLen = 32768;
+int cand_code_stride(const Shape& s);
 hipError_t launch_stream_window_cands(const Shape& s, const StreamPlan& plan, const void* q_win,
                                       const void* k, float scale, const float* lambda1, float w_mu,
                                       int budget, const int32_t* budgets, int cand_mult,
                                       int keep_tail, float* row_max, float* row_sum,
                                       uint64_t* cand_out, float* cand_max, int cand_stride,
-                                      bool sigma_all, hipStream_t stream);
+                                      uint32_t* codes, bool sigma_all, hipStream_t stream);
 // Base scores s = fma(lambda1[p], sigma, w_mu mu) of every key from mu / sigma rows (for batches
 // that take the other window paths).
 hipError_t launch_base_scores(const Shape& s, const float* mu, const float* sigma,

@@ -77,6 +77,9 @@ struct StreamArgs {
   int cand_stride;
   int budget, cand_mult, keep_tail;
   const int32_t* budgets;
+  // candidate mode, pass 1: per unit code_stride words of tile codes (32 words per tile)
+  uint32_t* codes;
+  int code_stride;
 };
 
 constexpr int kCandLists = kWaves;  // candidate lists per unit: one per wave of the fused kernel

@@ -9,15 +9,26 @@
 namespace kv {
 namespace stream {
 
+// Per-tile hook of pass 1 that does nothing (the plain statistics).
+struct NoTileHook {
+  static constexpr int kStores = 0;  // vector memory stores the hook issues per tile
+  template <int NB>
+  __device__ __forceinline__ void interior(int, const float (&)[NB]) const {}
+  __device__ __forceinline__ void guarded(int) const {}
+};
+
 // Pass 1 over the wave's tiles of a segment [k0, k1) of a unit with L keys: for every head, the
 // running maximum m of t = logit * c and the sum z of 2^(t - m) over the keys the lane's window
 // row sees (online softmax; base 2).  Interior tiles run without masks or branches; a tile with a
 // masked key (the causal triangle of the window, keys past the segment end) takes a guarded path.
-template <int D, int NB, int NW, int S>
+// After each tile the hook sees the tile's index in the segment and, for an interior tile, the
+// lane's largest logit (unscaled) of every head over its 16 keys; it issues Hook::kStores vector
+// memory stores per tile, which the stream's waits count.
+template <int D, int NB, int NW, int S, class Hook = NoTileHook>
 __device__ __forceinline__ void stats_tiles(const KeyStream<D, NB, NW, S>& ks,
                                             const bf16x8_t (&q)[NB][D / 16], int my_tiles, int k1,
                                             int L, float c, int l32, int half, float (&m_run)[NB],
-                                            float (&z_run)[NB]) {
+                                            float (&z_run)[NB], const Hook& hook = Hook{}) {
   constexpr int NS = D / 16;
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
@@ -28,16 +39,18 @@ __device__ __forceinline__ void stats_tiles(const KeyStream<D, NB, NW, S>& ks,
   const int kedge = min(k1, L - 31);
   for (int j = 0; j < my_tiles; ++j) {
     bf16x8_t kt[NS];
-    ks.template next<0>(kt, j, my_tiles, l32, half);
+    ks.template next<Hook::kStores>(kt, j, my_tiles, l32, half);
     const int t0 = ks.tile_key(j);
     if (t0 + 31 < kedge) {
+      float tmax[NB];
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
         const f32x16_t d = chain<NS>(kt, q[b]);
         float mx = fmax3(fmax3(fmax3(d[0], d[1], d[2]), d[3], d[4]), d[5], d[6]);
         mx = fmax3(fmax3(mx, d[7], d[8]), d[9], d[10]);
         mx = fmax3(fmax3(mx, d[11], d[12]), d[13], d[14]);
-        const float mn = __builtin_elementwise_maximum(m_run[b], __builtin_elementwise_maximum(mx, d[15]) * c);
+        tmax[b] = __builtin_elementwise_maximum(mx, d[15]);
+        const float mn = __builtin_elementwise_maximum(m_run[b], tmax[b] * c);
         const float keep = __builtin_amdgcn_exp2f(m_run[b] - mn);  // 0 on the lane's first tile
         float ex[16];
 #pragma unroll
@@ -48,6 +61,7 @@ __device__ __forceinline__ void stats_tiles(const KeyStream<D, NB, NW, S>& ks,
         z_run[b] = fmaf(z_run[b], keep, (zs[0] + zs[1]) + (zs[2] + zs[3]));
         m_run[b] = mn;
       }
+      hook.template interior<NB>(j * NW + ks.wave, tmax);
     } else {
       // window row l32 of every head sees keys <= L - 32 + l32; keys >= k1 belong to the next
       // segment.  The key of register jj is t0 + 4 half + 8 (jj / 4) + (jj % 4).
@@ -71,6 +85,7 @@ __device__ __forceinline__ void stats_tiles(const KeyStream<D, NB, NW, S>& ks,
           m_run[b] = mn;
         }
       }
+      hook.guarded(j * NW + ks.wave);
     }
   }
 }
@@ -95,128 +110,6 @@ __device__ __forceinline__ float2 merge_waves(const float2* red, int row) {
 #pragma unroll
   for (int w = 1; w < NW; ++w) merge_mz(v.x, v.y, red[w * R + row].x, red[w * R + row].y);
   return v;
-}
-
-// Score bounds of pass 1 in candidate mode (stream_prune.hip).  For each tile, with the running
-// normaliser b' <= b of every window row (the larger of the lane's own running log-sum-exp over
-// its keys and the workgroup's total at the last checkpoint), every key of the tile has
-//   a[h][r] = 2^(t - b) <= 2^(tmax[h][r] - b') =: a'[h][r]   (tmax: the tile's largest logit),
-// hence mu <= (1 / 32) sum_r abar'[r] (abar' = mean over the G heads) and, since a variance is at
-// most the mean square, sigma <= sqrt(sum_r abar'[r]^2 / 31) (sum_{h,r} a'^2 / (32 G - 1) for the
-// dispersion over all rows).  The bound of s = w_mu mu + lambda1 sigma (section 3.2, Eq. (5))
-// takes the positive parts of w_mu and lambda1, widened by kBoundSlack for the rounding of both
-// passes and kept above kBoundFloor.  A tile with a masked key gets +inf (always revisited).
-constexpr int kCkptTiles = 4;                       // tiles per wave between checkpoints
-constexpr float kBoundSlack = 1.00390625f;          // 1 + 2^-8
-constexpr float kBoundFloor = 0x1p-100f;
-struct Bound {
-  float* ub;       // [n_tiles] LDS: bound of tile i of the unit
-  float2* red;     // [NW][R] LDS: the waves' (m, z) at a checkpoint
-  float* tot_l;    // [R] LDS: the workgroup's log-sum-exp per row at the last checkpoint
-  float wmu_p, lam1_p;  // positive parts of w_mu and lambda1
-  float inv_g, inv_n1;  // 1 / G; 1 / 31 or 1 / (32 G - 1)
-};
-
-// Pass 1 of candidate mode over a whole unit (k1 = L): the statistics of stats_tiles and, per
-// tile, its score bound into bd.ub.  Every kCkptTiles tiles, while every wave still has tiles
-// (j + 1 < min_tiles), the waves merge their running statistics into bd.tot_l (two barriers).
-template <int D, int NB, bool ALL, int NW, int S>
-__device__ __forceinline__ void stats_bound_tiles(const KeyStream<D, NB, NW, S>& ks,
-                                                  const bf16x8_t (&q)[NB][D / 16], int my_tiles,
-                                                  int min_tiles, int L, float c, int l32, int half,
-                                                  float (&m_run)[NB], float (&z_run)[NB],
-                                                  const Bound& bd) {
-  constexpr int NS = D / 16, R = NB * 32;
-  const int lane = threadIdx.x & 63;
-  float tot[NB];
-#pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    m_run[b] = -INFINITY;
-    z_run[b] = 0.f;
-    tot[b] = -INFINITY;
-  }
-  const int kedge = L - 31;
-  for (int j = 0; j < my_tiles; ++j) {
-    bf16x8_t kt[NS];
-    ks.template next<0>(kt, j, my_tiles, l32, half);
-    const int t0 = ks.tile_key(j);
-    const int tile = j * NW + ks.wave;
-    if (t0 + 31 < kedge) {
-      float tmax[NB];
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const f32x16_t d = chain<NS>(kt, q[b]);
-        float mx = fmax3(fmax3(fmax3(d[0], d[1], d[2]), d[3], d[4]), d[5], d[6]);
-        mx = fmax3(fmax3(mx, d[7], d[8]), d[9], d[10]);
-        mx = fmax3(fmax3(mx, d[11], d[12]), d[13], d[14]);
-        tmax[b] = __builtin_elementwise_maximum(mx, d[15]);
-        const float mn = __builtin_elementwise_maximum(m_run[b], tmax[b] * c);
-        const float keep = __builtin_amdgcn_exp2f(m_run[b] - mn);  // 0 on the lane's first tile
-        float ex[16];
-#pragma unroll
-        for (int jj = 0; jj < 16; ++jj) ex[jj] = __builtin_amdgcn_exp2f(fmaf(d[jj], c, -mn));
-        float zs[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) zs[u] = (ex[4 * u] + ex[4 * u + 1]) + (ex[4 * u + 2] + ex[4 * u + 3]);
-        z_run[b] = fmaf(z_run[b], keep, (zs[0] + zs[1]) + (zs[2] + zs[3]));
-        m_run[b] = mn;
-      }
-      float p1 = 0.f, p2 = 0.f;
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const float tm = max_halves(tmax[b]) * c;
-        const float own = m_run[b] + __builtin_amdgcn_logf(z_run[b]);
-        const float a = __builtin_amdgcn_exp2f(tm - fmaxf(own, tot[b]));
-        p1 += a;
-        if constexpr (ALL) p2 = fmaf(a, a, p2);
-      }
-      p1 *= bd.inv_g;
-      if constexpr (!ALL) p2 = p1 * p1;
-#pragma unroll
-      for (int off = 1; off < 32; off <<= 1) {  // over the 32 rows of each half
-        p1 += __shfl_xor(p1, off, 64);
-        p2 += __shfl_xor(p2, off, 64);
-      }
-      if (lane == 0)
-        bd.ub[tile] = fmaf(fmaf(bd.lam1_p, __builtin_sqrtf(p2 * bd.inv_n1),
-                                bd.wmu_p * (p1 * (1.f / 32.f))),
-                           kBoundSlack, kBoundFloor);
-    } else {
-      // the guarded path of stats_tiles (k1 = L)
-      const int thr = L - 32 + l32 - t0 - 4 * half;
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        f32x16_t d = chain<NS>(kt, q[b]);
-#pragma unroll
-        for (int jj = 0; jj < 16; ++jj)
-          if (8 * (jj >> 2) + (jj & 3) > thr) d[jj] = -INFINITY;
-        float mx = d[0];
-#pragma unroll
-        for (int jj = 1; jj < 16; ++jj) mx = fmaxf(mx, d[jj]);
-        const float mn = fmaxf(m_run[b], mx * c);
-        if (mn != -INFINITY) {
-          const float keep = m_run[b] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[b] - mn);
-          float z = z_run[b] * keep;
-#pragma unroll
-          for (int jj = 0; jj < 16; ++jj) z += __builtin_amdgcn_exp2f(fmaf(d[jj], c, -mn));
-          z_run[b] = z;
-          m_run[b] = mn;
-        }
-      }
-      if (lane == 0) bd.ub[tile] = INFINITY;
-    }
-    if ((j + 1) % kCkptTiles == 0 && j + 1 < min_tiles) {
-      stats_to_lds<NB>(m_run, z_run, bd.red + ks.wave * R, l32, half);
-      __syncthreads();
-      if ((int)threadIdx.x < R) {
-        const float2 v = merge_waves<NW, R>(bd.red, threadIdx.x);
-        bd.tot_l[threadIdx.x] = v.x + __builtin_amdgcn_logf(v.y);
-      }
-      __syncthreads();
-#pragma unroll
-      for (int b = 0; b < NB; ++b) tot[b] = bd.tot_l[b * 32 + l32];
-    }
-  }
 }
 
 // One mu or sigma value to HBM with the device-scope store policy (sc1).  These 128-byte pieces

@@ -2,19 +2,22 @@
 // keys once in full (section 3.1, Eq. (1), Eq. (3); section 3.2, Eq. (5) and the top-4B
 // restriction).
 //
-// Pass 1 streams every key tile, as in stream_window.hip, and also bounds the base score of every
-// key of each tile from above with the running softmax normalisers known at that point (Bound,
-// stream_passes.h).  After the row normalisers b are complete, the tiles are sorted by their
-// bounds and pass 2 evaluates the exact base scores tile by tile in that order, wave w taking
-// positions w, w + 8, ... of the order.  The evaluated keys of the candidate range go into an LDS
-// histogram and the waves' candidate lists (Prune, CandList); the histogram gives a lower bound of
-// the unit's cut (the C-th best score), and a wave stops at its first tile whose bound lies below
-// it: every key of the tiles left out scores below the cut.  Scores are formed by the same code as
-// in the other window kernels, so each evaluated key's score is the one kv_window_base_scores
-// writes, bit for bit; the candidate lists therefore hold exactly the unit's C best entries.
+// Pass 1 streams every key tile, as in stream_window.hip, and also records, per tile and per
+// (head, window row), the tile's largest logit as a one-byte code below the tile's largest logit
+// (TileCodes; 128 bytes per tile in the workspace).  Once the row normalisers b are complete, these
+// codes bound the base score of every key of each tile from above (tile_bound).  The tiles are
+// then ordered by their bounds (a counting sort into bins of 1/16 of an octave below the largest
+// bound, each tile standing for its bin's upper edge) and pass 2 evaluates the exact base scores
+// tile by tile in that order, wave w taking positions w, w + 8, ... of the order.  The evaluated
+// keys of the candidate range go into an LDS histogram and the waves' candidate lists (Prune,
+// CandList); the histogram gives a lower bound of the unit's cut (the C-th best score), and a wave
+// stops at its first tile whose bound lies below it: every key of the tiles left out scores below
+// the cut.  Scores are formed by the same code as in the other window kernels, so each evaluated
+// key's score is the one kv_window_base_scores writes, bit for bit; the candidate lists therefore
+// hold exactly the unit's C best entries.
 //
-// On the 32-layer Mistral-shaped pass at L = 32768 (C = 256) pass 2 revisits about one tile in
-// six; pass 1 is a plain stream of the keys.
+// On the 32-layer Mistral-shaped pass at L = 32768 (C = 256) the bounds leave about one tile in
+// twenty to pass 2.
 #include "stream_passes.h"
 
 namespace kv {
@@ -22,25 +25,123 @@ namespace stream {
 namespace {
 
 constexpr int kPruneMaxTiles = kCandMaxLen / kTileKeys;
+// Order of the tiles for pass 2: bin 0 holds the tiles with a masked key (bound +inf), bin k >= 1
+// the tiles whose bound lies within ((k - 1) / 16, k / 16] octaves below the largest finite bound
+// (the last bin: everything further below).
+constexpr int kOrderBins = 1024;
+constexpr float kBinsPerOctave = 16.f;
+// Bounds are widened by kBoundSlack for the rounding of both passes (logits formed in another
+// MFMA operand order, approximate exp2 / log2) and kept above kBoundFloor.
+constexpr float kBoundSlack = 1.00390625f;  // 1 + 2^-8
+constexpr float kBoundFloor = 0x1p-100f;
+constexpr float kCodeStep = 0.125f;          // code units: 1/8 of a factor of two
+
+// Pass-1 hook of candidate mode: per tile, the largest t = logit * c of every (head, window row) as
+// the number of 1/8-steps it lies below the tile's largest t (rounded down, at most 255), one byte
+// per head of the row's word in the unit's code rows, and the tile's largest t into ref[tile]
+// (LDS); a tile with a masked key gets ref = +inf (always revisited).  Both halves of the wave hold
+// the same row maxima after the exchange, so every lane stores its row's word (one store per tile).
+template <int NBH> struct TileCodes {
+  static constexpr int kStores = 1;
+  uint32_t* codes;  // tile i at codes + 32 i: word r = window row r, byte b = head b (255 unused)
+  float* ref;       // [n_tiles] LDS
+  float c;
+  int l32, lane;
+
+  template <int NB>
+  __device__ __forceinline__ void interior(int tile, const float (&tmax)[NB]) const {
+    static_assert(NB == NBH, "head count");
+    float tm[NB];
+    float r = -INFINITY;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      tm[b] = max_halves(tmax[b]) * c;
+      r = __builtin_elementwise_maximum(r, tm[b]);
+    }
+#pragma unroll
+    for (int off = 1; off < 32; off <<= 1) r = __builtin_elementwise_maximum(r, __shfl_xor(r, off, 64));
+    uint32_t w = 0xFFFFFFFFu;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const float steps = (r - tm[b]) * (1.f / kCodeStep);  // >= 0; NaN gives 255
+      const uint32_t code = steps < 255.f ? (uint32_t)steps : 255u;
+      w = (w & ~(0xFFu << (8 * b))) | (code << (8 * b));
+    }
+    store_word(codes + 32 * tile + l32, w);
+    if (lane == 0) ref[tile] = r;
+  }
+  __device__ __forceinline__ void guarded(int tile) const {
+    store_word(codes + 32 * tile + l32, 0xFFFFFFFFu);
+    if (lane == 0) ref[tile] = INFINITY;
+  }
+  __device__ __forceinline__ static void store_word(uint32_t* dst, uint32_t v) {
+    asm volatile("global_store_dword %0, %1, off sc1" ::"v"(dst), "v"(v) : "memory");
+  }
+};
+
+// Upper bound of the base score s = w_mu mu + lambda1 sigma (section 3.2, Eq. (5)) of every key of
+// a tile from its codes (row r of head h: t <= ref - code / 8) and the final row normalisers b:
+// a[h][r] = 2^(t - b[h][r]) <= a'[h][r], hence mu <= (1 / 32) sum_r abar'[r] (abar': mean over the
+// G heads) and, since a variance is at most the mean square, sigma <= sqrt(sum_r abar'[r]^2 / 31)
+// (sum_{h,r} a'^2 / (32 G - 1) for the dispersion over all rows).  The positive parts of w_mu and
+// lambda1 enter.
+template <int NB, bool ALL>
+__device__ __forceinline__ float tile_bound(const uint32_t* codes_t, float ref, const float* bsh,
+                                            float wmu_p, float lam1_p, float inv_g) {
+  const uint4* src = reinterpret_cast<const uint4*>(codes_t);
+  float p1 = 0.f, p2 = 0.f;
+#pragma unroll 2
+  for (int v = 0; v < 8; ++v) {
+    const uint4 w4 = src[v];
+    const uint32_t ws[4] = {w4.x, w4.y, w4.z, w4.w};
+    float arow[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const float4 bv = *reinterpret_cast<const float4*>(bsh + b * 32 + 4 * v);
+      const float bb[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float code = (float)((ws[e] >> (8 * b)) & 0xFFu);
+        const float a = __builtin_amdgcn_exp2f(fmaf(code, -kCodeStep, ref) - bb[e]);
+        arow[e] += a;
+        if constexpr (ALL) p2 = fmaf(a, a, p2);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      p1 += arow[e];
+      if constexpr (!ALL) {
+        const float ab = arow[e] * inv_g;
+        p2 = fmaf(ab, ab, p2);
+      }
+    }
+  }
+  constexpr float inv_n1 = ALL ? 1.f / (float)(NB * 32 - 1) : 1.f / 31.f;
+  const float mu_b = p1 * inv_g * (1.f / 32.f);
+  return fmaf(fmaf(lam1_p, __builtin_sqrtf(p2 * inv_n1), wmu_p * mu_b), kBoundSlack, kBoundFloor);
+}
 
 template <int D, int NB, bool ALL, int NW, int S>
 __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) {
   using Gm = SGeo<D, NB>;
   constexpr int R = Gm::R, NS = Gm::NS, NT = NW * 64;
   constexpr int kRedWords = NW * R * 2;
+  constexpr int kTilesPerThread = kPruneMaxTiles / NT;
   static_assert(NW == kCandLists, "one candidate list per wave");
-  static_assert((size_t)NW * S * Gm::TE * 2 >= (size_t)kPruneMaxTiles * 8, "the sort fits the ring");
+  static_assert(kPruneMaxTiles % NT == 0, "whole tiles per thread");
+  static_assert(NW * kCandCap >= 2 * kOrderBins, "the bin counts and offsets fit the lists");
   __shared__ __align__(16) uint16_t ring[NW][S * Gm::TE];
-  // the waves' statistics in pass 1, the histogram of evaluated scores in pass 2
+  // the waves' statistics after pass 1, the histogram of evaluated scores in pass 2
   __shared__ __align__(16) uint32_t red_hist[kRedWords > kPruneBins ? kRedWords : kPruneBins];
   __shared__ __align__(16) float bsh[R];
-  __shared__ float tot_l[R];
+  // pass 1: the tile's largest t; from the order on: the bound of the i-th tile of the order
   __shared__ float ub[kPruneMaxTiles];
   __shared__ uint16_t order[kPruneMaxTiles];
+  // the waves' candidate lists (before pass 2: the bin counts and offsets of the order)
   __shared__ uint32_t c_okey[NW * kCandCap];
   __shared__ uint16_t c_pos[NW * kCandCap];
   __shared__ float c_max[NW];
-  __shared__ uint32_t cut, top_bin;
+  __shared__ uint32_t cut, top_bin, bmax_bits, n_eval;
 
   const int g = blockIdx.y, p = blockIdx.z;
   const int L = a.lens[p];
@@ -52,6 +153,7 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   const float lam1 = a.lambda1[p];
   const size_t stat_base = (size_t)a.tok_off[p] * a.h_kv + (size_t)g * L;
   float2* red = reinterpret_cast<float2*>(red_hist);
+  uint32_t* codes_u = a.codes + ((size_t)p * a.h_kv + g) * a.code_stride;
 
   const uint16_t* kg = a.k + stat_base * D;
   KeyStream<D, NB, NW, S> ks{ring[wave], kg, 0, L, wave, lane};
@@ -62,13 +164,17 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   ks.prologue(my_tiles);
   hold_until_loaded<D, NB>(q);
 
-  // ---- pass 1: statistics and tile bounds
+  // ---- pass 1: statistics and tile codes
   float m_run[NB], z_run[NB];
-  const Bound bd{ub, red, tot_l, fmaxf(a.w_mu, 0.f), fmaxf(lam1, 0.f), inv_g,
-                 ALL ? 1.f / (float)(NB * 32 - 1) : 1.f / 31.f};
-  stats_bound_tiles<D, NB, ALL, NW, S>(ks, q, my_tiles, n_tiles / NW, L, c, l32, half, m_run,
-                                       z_run, bd);
+  stats_tiles<D, NB, NW, S>(ks, q, my_tiles, L, L, c, l32, half, m_run, z_run,
+                            TileCodes<NB>{codes_u, ub, c, l32, lane});
+  wait_vmem<0>();  // this wave's code stores have landed (other waves read them below)
   stats_to_lds<NB>(m_run, z_run, red + wave * R, l32, half);
+  if (tid == 0) {
+    cut = 0u;
+    top_bin = 0u;
+    bmax_bits = 0u;
+  }
   __syncthreads();
   if (tid < R) {
     const float2 v = merge_waves<NW, R>(red, tid);
@@ -77,38 +183,98 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
     a.row_max_out[ri] = v.x * kLn2;
     a.row_sum_out[ri] = v.y;
   }
-  // ---- the tiles in decreasing order of their bounds, sorted in the ring (every load of pass 1
-  //      has landed and been read: its last wait is vmcnt(0))
-  int n2 = 1;
-  while (n2 < n_tiles) n2 <<= 1;
-  uint64_t* se = reinterpret_cast<uint64_t*>(&ring[0][0]);
-  __syncthreads();  // the statistics are read from red; the ring is idle
-  for (int i = tid; i < n2; i += NT)
-    se[i] = i < n_tiles ? ((uint64_t)order_key(ub[i]) << 32) | (uint32_t)(0xFFFF - i) : 0ull;
+  __syncthreads();  // the normalisers are complete; red is free
+
+  // ---- bounds of the thread's tiles tid + u NT (-inf: no candidate key, never revisited)
+  uint32_t* cnt = c_okey;                // [kOrderBins] tiles per bin
+  uint32_t* off = c_okey + kOrderBins;   // [kOrderBins] first position of each bin, then a cursor
   for (int i = tid; i < kPruneBins; i += NT) red_hist[i] = 0u;
-  if (tid == 0) {
-    cut = 0u;
-    top_bin = 0u;
+  for (int i = tid; i < kOrderBins; i += NT) cnt[i] = 0u;
+  const int n_cand = L - a.keep_tail;
+  const float wmu_p = fmaxf(a.w_mu, 0.f), lam1_p = fmaxf(lam1, 0.f);
+  float bnd[kTilesPerThread];
+  float lmax = 0.f;  // largest finite bound (bounds are positive)
+#pragma unroll
+  for (int u = 0; u < kTilesPerThread; ++u) {
+    const int i = tid + u * NT;
+    bnd[u] = -INFINITY;
+    if (i < n_tiles && i * kTileKeys < n_cand) {
+      const float r = ub[i];
+      float bd = INFINITY;
+      if (r < INFINITY) bd = tile_bound<NB, ALL>(codes_u + 32 * i, r, bsh, wmu_p, lam1_p, inv_g);
+      if (!(bd == bd)) bd = INFINITY;  // NaN inputs: revisit
+      bnd[u] = bd;
+      if (bd < INFINITY) lmax = fmaxf(lmax, bd);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) lmax = fmaxf(lmax, __shfl_xor(lmax, o, 64));
+  if (lane == 0) atomicMax(&bmax_bits, __float_as_uint(lmax));  // positive floats order as integers
+  __syncthreads();
+  const float bmax = __uint_as_float(bmax_bits);
+  const float lg_max = __builtin_amdgcn_logf(bmax);  // log2; only used when a finite bound exists
+  int bin[kTilesPerThread];
+#pragma unroll
+  for (int u = 0; u < kTilesPerThread; ++u) {
+    bin[u] = -1;
+    if (bnd[u] == INFINITY) {
+      bin[u] = 0;
+    } else if (bnd[u] > 0.f) {
+      // bins counted down from the largest bound, rounded towards the larger bound (the bin's
+      // upper edge stays above every bound in it despite the rounding of log2)
+      const float x = (lg_max - __builtin_amdgcn_logf(bnd[u])) * kBinsPerOctave - (1.f / 64.f);
+      bin[u] = 1 + (int)fminf(fmaxf(x, 0.f), (float)(kOrderBins - 2));
+    }
+    if (bin[u] >= 0) atomicAdd(&cnt[bin[u]], 1u);
   }
   __syncthreads();
-  bitonic_sort(se, n2, tid, NT);  // ascending
-  for (int i = tid; i < n_tiles; i += NT) {
-    const uint64_t e = se[n2 - 1 - i];
-    order[i] = (uint16_t)(0xFFFF - (uint32_t)e);
-    ub[i] = key_float((uint32_t)(e >> 32));
+  if (wave == 0) {
+    // exclusive scan of the counts: lane l holds bins 16 l .. 16 l + 15
+    constexpr int PB = kOrderBins / 64;
+    uint32_t v[PB];
+    uint32_t s = 0;
+#pragma unroll
+    for (int k = 0; k < PB; ++k) {
+      v[k] = cnt[lane * PB + k];
+      s += v[k];
+    }
+    uint32_t incl = s;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t t = (uint32_t)__shfl_up((int)incl, o, 64);
+      if (lane >= o) incl += t;
+    }
+    uint32_t run = incl - s;
+#pragma unroll
+    for (int k = 0; k < PB; ++k) {
+      off[lane * PB + k] = run;
+      run += v[k];
+    }
+    if (lane == 63) n_eval = incl;
   }
-  __syncthreads();  // the order is complete and the ring is free again
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < kTilesPerThread; ++u) {
+    if (bin[u] >= 0) {
+      const uint32_t pos = atomicAdd(&off[bin[u]], 1u);
+      order[pos] = (uint16_t)(tid + u * NT);
+      ub[pos] = bin[u] == 0 ? INFINITY
+                            : bmax * __builtin_amdgcn_exp2f(-(float)(bin[u] - 1) * (1.f / kBinsPerOctave));
+    }
+  }
+  __syncthreads();  // the order is complete; the lists and the ring are free
 
   // ---- pass 2: exact scores of the wanted tiles
-  const int n_cand = L - a.keep_tail;
+  const int n_ord = (int)n_eval;
   const int bp = a.budgets ? a.budgets[p] : a.budget;
   const int C = min(a.cand_mult * bp, n_cand);
+  const int my_tiles2 = n_ord > wave ? (n_ord - wave + NW - 1) / NW : 0;
   KeyStream<D, NB, NW, S> ks2{ring[wave], kg, 0, L, wave, lane, order};
-  ks2.prologue(my_tiles);
+  ks2.prologue(my_tiles2);
   Prune pr{CandList{c_okey + wave * kCandCap, c_pos + wave * kCandCap, C, 0, 0ull, false, -INFINITY},
            ub, red_hist, &cut, &top_bin, n_cand};
   const ScoreOut so{nullptr, lam1, a.w_mu};
-  mu_sigma_tiles<D, NB, ALL, NW, S, kOutCand>(ks2, q, bsh, my_tiles, L, L, c, inv_g, nullptr,
+  mu_sigma_tiles<D, NB, ALL, NW, S, kOutCand>(ks2, q, bsh, my_tiles2, L, L, c, inv_g, nullptr,
                                               nullptr, l32, half, so, &pr);
   wait_vmem<0>();  // no load into the ring may outlive the workgroup (a stopped wave has some)
   CandList& cl = pr.cl;
@@ -119,7 +285,7 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
     dst[i] = i < cl.n ? cand_entry(cl.okey[i], cl.pos[i]) : 0ull;
   float m = cl.smax;
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
   if (lane == 0) c_max[wave] = m;
   __syncthreads();
   if (tid == 0) {
@@ -142,13 +308,17 @@ template <int D, int NB> struct PruneLaunch {
 }  // namespace
 }  // namespace stream
 
+int cand_code_stride(const Shape& s) {
+  return (s.max_len + stream::kTileKeys - 1) / stream::kTileKeys * 32;
+}
+
 hipError_t launch_stream_window_cands(const Shape& s, const StreamPlan& plan, const void* q_win,
                                       const void* k, float scale, const float* lambda1, float w_mu,
                                       int budget, const int32_t* budgets, int cand_mult,
                                       int keep_tail, float* row_max, float* row_sum,
                                       uint64_t* cand_out, float* cand_max, int cand_stride,
-                                      bool sigma_all, hipStream_t stream) {
-  if (plan.max_segs != 1 || !cand_out || !cand_max || s.max_len > kCandMaxLen)
+                                      uint32_t* codes, bool sigma_all, hipStream_t stream) {
+  if (plan.max_segs != 1 || !cand_out || !cand_max || !codes || s.max_len > kCandMaxLen)
     return hipErrorInvalidValue;
   stream::StreamArgs a = stream::base_args(s, plan, q_win, k, scale);
   a.row_max_out = row_max;
@@ -163,6 +333,8 @@ hipError_t launch_stream_window_cands(const Shape& s, const StreamPlan& plan, co
   a.budgets = budgets;
   a.cand_mult = cand_mult;
   a.keep_tail = keep_tail;
+  a.codes = codes;
+  a.code_stride = cand_code_stride(s);
   return stream::launch_for_shape<stream::PruneLaunch>(s, a, stream);
 }
 

@@ -385,7 +385,9 @@ def test_candidates_checks():
 
     norm = (units * 4 + 255) // 256 * 256
     scores = 32 * 32768 * 8 * 4
-    assert lib.kv_candidates_workspace_bytes(big.ref(), 64, 4, 32, None) == lists(256) + norm
+    codes = units * (32768 // 32) * 128  # the first pass's tile codes: 128 bytes per 32 keys
+    assert lib.kv_candidates_workspace_bytes(big.ref(), 64, 4, 32, None) == (
+        lists(256) + norm + codes)
     # 512 candidates exceed a wave's list: the scores go through the workspace
     assert lib.kv_candidates_workspace_bytes(big.ref(), 128, 4, 32, None) >= (
         lists(512) + norm + scores)
