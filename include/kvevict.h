@@ -290,10 +290,11 @@ int kv_mmr_select_scored(const kv_problem* pr, const float* score, const void* k
  * KV_ERR_ARG; w_mu and the per-problem budgets as in kv_mmr_select_ex) must be the values later
  * given to kv_mmr_select_candidates.  lambda1: [n_prob] fp32 device.
  * For bf16 batches that kv_window_base_scores scores inside the window kernel's second pass, with
- * cand_mult > 0, C_p <= 288 and L_p <= 32768, the candidates are kept inside that pass (one list
- * per wave, merged by the selection) and no score is stored; otherwise the scores go through the
- * workspace and the selection kernel's first phases cut the candidates from them.  Calls that
- * overlap on one workspace race. */
+ * cand_mult > 0, C_p <= 288 and L_p <= 32768, the keys are read once in full, the candidates
+ * are cut inside that launch (a second pass revisits only the 32-key tiles whose score bound
+ * reaches the cut) and no score is stored; otherwise the scores go through the workspace and the
+ * selection kernel's first phases cut the candidates from them.  Calls that overlap on one
+ * workspace race. */
 int kv_window_candidates(const kv_problem* pr, const void* q_win, const void* k, float scale,
                          const float* lambda1, int32_t sigma_rows, int32_t budget,
                          int32_t cand_mult, int32_t keep_tail, const kv_select_opts* opts,

@@ -148,10 +148,10 @@ size_t base_scores_ws_bytes(const kv_problem* pr, const kv::Shape& s, bool fused
   return window_ws_bytes(pr, s) + 2 * align_up(keys * sizeof(float));
 }
 
-// Candidate lists of kv_window_candidates: kCandListCount lists of `stride` 8-byte entries per
-// (problem, kv head).
+// Candidate lists of kv_window_candidates: one list of `stride` 8-byte entries per (problem, kv
+// head).
 size_t cand_lists_bytes(const kv_problem* pr, int stride) {
-  return align_up((size_t)pr->n_prob * pr->h_kv * kv::kCandListCount * stride * sizeof(uint64_t));
+  return align_up((size_t)pr->n_prob * pr->h_kv * stride * sizeof(uint64_t));
 }
 
 // Whether kv_window_candidates forms the candidate lists inside the window kernel's second pass:

@@ -73,14 +73,13 @@ hipError_t launch_stream_window_scores(const Shape& s, const StreamPlan& plan, c
                                        float w_mu, float* row_max, float* row_sum, float* score,
                                        bool sigma_all, hipStream_t stream);
 // Window statistics and the candidate set in one launch, every unit one segment (candidate mode,
-// stream_prune.hip): row_max / row_sum, and per unit the candidate lists
-// [n_units][kCandListCount][cand_stride] of (order key of the score, position) entries packed as
-// key << 32 | (0xFFFFFFFF - position) (0: none) whose union holds the unit's C_p best entries, and
-// cand_max [n_units], the largest base score over the candidate positions clamped at 1e-12.  The
+// stream_prune.hip): row_max / row_sum, and per unit the candidate list [n_units][cand_stride] of
+// (order key of the score, position) entries packed as key << 32 | (0xFFFFFFFF - position): the
+// unit's C_p best entries in ascending position order, then zeros; and cand_max [n_units], the
+// largest base score over the candidate positions clamped at 1e-12.  The
 // keys are read once in full; the second pass revisits only the tiles whose score bound reaches
 // the unit's cut.  codes: scratch of n_units * cand_code_stride(s) words (the first pass's tile
 // codes).  Units of at most kCandMaxLen keys and C_p <= kCandMaxC.
-constexpr int kCandListCount = 8;
 constexpr int kCandMaxC = 288;
 constexpr int kCandMaxLen = 32768;
 int cand_code_stride(const Shape& s);
@@ -120,9 +119,9 @@ struct SelectArgs {
   const float* sigma;
   // base scores given instead of mu / sigma (then lambda1 and w_mu are unused)
   const float* score = nullptr;
-  // candidate lists given instead (cand_in, cand_in_max: as launch_stream_window_cands writes
-  // them, list_stride entries per list; no pooling), or, with cut_out, only the candidate cut:
-  // each unit's C candidates as list 0 of its lists and its normaliser into cut_max
+  // a candidate list given instead (cand_in, cand_in_max: as launch_stream_window_cands writes
+  // them, list_stride entries per unit; no pooling), or, with cut_out, only the candidate cut:
+  // each unit's C candidates in the same form and its normaliser into cut_max
   const uint64_t* cand_in = nullptr;
   const float* cand_in_max = nullptr;
   uint64_t* cut_out = nullptr;

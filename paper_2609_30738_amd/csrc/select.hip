@@ -410,30 +410,13 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
   const bool take_all = (C >= n_cand);
   float den = 0.f;
   if (cand_in) {
-    // ---- 0-2 from candidate lists: the units' kCandListCount lists hold the C best entries
-    //      (order key of the score, position) among them; sort them all, keep the C largest, and
-    //      put those in position order (their scores: the keys' floats)
-    const uint64_t* src = cand_in + (size_t)blockIdx.x * kCandListCount * list_stride;
-    const int n_in = kCandListCount * list_stride;
-    int n2 = 1;
-    while (n2 < n_in) n2 <<= 1;
-    uint64_t* ent = reinterpret_cast<uint64_t*>(region);
-    for (int i = tid; i < n2; i += kThreads) ent[i] = i < n_in ? src[i] : 0ull;  // 0: no entry
-    __syncthreads();
-    bitonic_sort(ent, n2, tid, kThreads);  // ascending: the best last
-    int nc2 = 1;
-    while (nc2 < C) nc2 <<= 1;
-    // the C best, re-keyed by position, into the front: n2 >= kCandListCount C > nc2 + C, so the
-    // entries read here and the slots written do not overlap
-    for (int i = tid; i < nc2; i += kThreads) {
-      const uint64_t e = i < C ? ent[n2 - 1 - i] : 0ull;
-      ent[i] = i < C ? ((uint64_t)cand_entry_pos(e) << 32) | (uint32_t)(e >> 32) : ~0ull;
-    }
-    __syncthreads();
-    bitonic_sort(ent, nc2, tid, kThreads);  // by position
+    // ---- 0-2 from a candidate list: the unit's C candidates (order key of the score, position)
+    //      in ascending position order
+    const uint64_t* src = cand_in + (size_t)blockIdx.x * list_stride;
     for (int i = tid; i < C; i += kThreads) {
-      cpos[i] = (int32_t)(ent[i] >> 32);
-      cst[i] = key_float((uint32_t)ent[i]);
+      const uint64_t e = src[i];
+      cpos[i] = (int32_t)cand_entry_pos(e);
+      cst[i] = key_float((uint32_t)(e >> 32));
     }
     den = cand_in_max[blockIdx.x];
     __syncthreads();
@@ -666,10 +649,10 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
   }
   __syncthreads();
   if (cut_out) {
-    // the candidate list of a unit for the selection from lists: list 0 holds the C candidates,
-    // the others nothing
-    uint64_t* dst = cut_out + (size_t)blockIdx.x * kCandListCount * list_stride;
-    for (int i = tid; i < kCandListCount * list_stride; i += kThreads)
+    // the candidate list of a unit for the selection from a list: the C candidates in position
+    // order, then nothing
+    uint64_t* dst = cut_out + (size_t)blockIdx.x * list_stride;
+    for (int i = tid; i < list_stride; i += kThreads)
       dst[i] = i < C ? cand_entry(order_key(base_score(cpos[i])), (uint32_t)cpos[i]) : 0ull;
     if (tid == 0) cut_max[blockIdx.x] = den;
     return;
@@ -1041,14 +1024,7 @@ size_t lds_head(int max_cand) { return ((size_t)max_cand * 12 + 15) & ~(size_t)1
 template <int DT, int D, int NT, int CPT, bool STAGED, bool GRAM>
 hipError_t select_launch(const Shape& s, const SelectArgs& a, size_t body, hipStream_t st) {
   using T = typename Elem<DT>::T;
-  size_t lists = 0;  // the merge of candidate lists: a power of two of entries
-  if (a.cand_in) {
-    size_t n2 = 1;
-    while (n2 < (size_t)kCandListCount * a.list_stride) n2 <<= 1;
-    lists = n2 * sizeof(uint64_t);
-  }
-  const size_t region =
-      std::max(std::max(body, STAGED ? (size_t)a.max_cand_all * 4 : (size_t)0), lists);
+  const size_t region = std::max(body, STAGED ? (size_t)a.max_cand_all * 4 : (size_t)0);
   const size_t dyn = lds_head(a.max_cand) + region;
   auto kern = mmr_select_kernel<DT, D, NT, CPT, STAGED, GRAM>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),

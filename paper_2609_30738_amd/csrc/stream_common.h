@@ -68,10 +68,10 @@ struct StreamArgs {
   float* score;
   const float* lambda1;
   float w_mu;
-  // candidate mode of pass 2 (every unit one segment): per unit the waves' candidate lists,
-  // [n_units][kCandLists][cand_stride] entries (0: none), and the maximum base score over the
-  // candidate positions clamped at 1e-12 (the selection's normaliser); C_p = min(cand_mult B_p,
-  // L_p - keep_tail), B_p = budgets[p] or budget
+  // candidate mode of pass 2 (every unit one segment): per unit the candidate list,
+  // [n_units][cand_stride] entries (the C_p candidates in position order, then 0), and the maximum
+  // base score over the candidate positions clamped at 1e-12 (the selection's normaliser);
+  // C_p = min(cand_mult B_p, L_p - keep_tail), B_p = budgets[p] or budget
   uint64_t* cand_out;
   float* cand_max;
   int cand_stride;
@@ -83,7 +83,6 @@ struct StreamArgs {
 };
 
 constexpr int kCandLists = kWaves;  // candidate lists per unit: one per wave of the fused kernel
-static_assert(kCandLists == kCandListCount, "candidate list count");
 
 template <int D, int NB> struct SGeo {
   static constexpr int R = NB * 32;          // window rows of a unit (G heads x 32)

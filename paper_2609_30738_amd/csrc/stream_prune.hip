@@ -121,6 +121,37 @@ __device__ __forceinline__ float tile_bound(const uint32_t* codes_t, float ref, 
   return fmaf(fmaf(lam1_p, __builtin_sqrtf(p2 * inv_n1), wmu_p * mu_b), kBoundSlack, kBoundFloor);
 }
 
+// Bitmap words over the candidate positions of a unit (one bit per position).
+constexpr int kBitmapWords = kCandMaxLen / 32;
+
+// The bin (order key >> kPruneShift) of the C-th largest entry counted in hist, scanning down from
+// top (a bin at or above every nonempty one), into *cut_bin, and the number of entries in the bins
+// above it into *above.  One wave; hist holds at least C entries.
+__device__ __forceinline__ void find_cut_bin(const uint32_t* hist, uint32_t top, int C, int lane,
+                                             uint32_t* cut_bin, uint32_t* above) {
+  uint32_t cum = 0;
+  for (int b0 = (int)top; b0 >= 0; b0 -= 64) {
+    const int b = b0 - lane;
+    const uint32_t own = b >= 0 ? hist[b] : 0u;
+    uint32_t pre = own;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t t = (uint32_t)__shfl_up((int)pre, o, 64);
+      if (lane >= o) pre += t;
+    }
+    const uint64_t hit = __ballot(cum + pre >= (uint32_t)C);
+    if (hit) {
+      const int hl = __ffsll((unsigned long long)hit) - 1;
+      if (lane == hl) {
+        *cut_bin = (uint32_t)b;
+        *above = cum + pre - own;
+      }
+      return;
+    }
+    cum += (uint32_t)__builtin_amdgcn_readlane((int)pre, 63);
+  }
+}
+
 template <int D, int NB, bool ALL, int NW, int S>
 __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) {
   using Gm = SGeo<D, NB>;
@@ -130,6 +161,9 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   static_assert(NW == kCandLists, "one candidate list per wave");
   static_assert(kPruneMaxTiles % NT == 0, "whole tiles per thread");
   static_assert(NW * kCandCap >= 2 * kOrderBins, "the bin counts and offsets fit the lists");
+  static_assert(sizeof(uint16_t) * NW * S * Gm::TE >= 4 * kBitmapWords + 8 * NW * kCandCap,
+                "the bitmap and the cut bin's entries fit the ring");
+  static_assert(kPruneBins >= kBitmapWords, "the word prefixes fit the histogram");
   __shared__ __align__(16) uint16_t ring[NW][S * Gm::TE];
   // the waves' statistics after pass 1, the histogram of evaluated scores in pass 2
   __shared__ __align__(16) uint32_t red_hist[kRedWords > kPruneBins ? kRedWords : kPruneBins];
@@ -142,6 +176,7 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   __shared__ uint16_t c_pos[NW * kCandCap];
   __shared__ float c_max[NW];
   __shared__ uint32_t cut, top_bin, bmax_bits, n_eval;
+  __shared__ uint64_t cut_entry;
 
   const int g = blockIdx.y, p = blockIdx.z;
   const int L = a.lens[p];
@@ -278,16 +313,99 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
                                               nullptr, l32, half, so, &pr);
   wait_vmem<0>();  // no load into the ring may outlive the workgroup (a stopped wave has some)
   CandList& cl = pr.cl;
-  // the wave's best C (all of its entries when it holds no more), then zeros
-  if (cl.n > C) cl.compact(lane);
-  uint64_t* dst = a.cand_out + (((size_t)p * a.h_kv + g) * kCandLists + wave) * a.cand_stride;
-  for (int i = lane; i < a.cand_stride; i += 64)
-    dst[i] = i < cl.n ? cand_entry(cl.okey[i], cl.pos[i]) : 0ull;
+  if (cl.n > C) cl.compact(lane);  // the wave's best C
   float m = cl.smax;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
   if (lane == 0) c_max[wave] = m;
+
+  // ---- the unit's candidates: the C largest entries of the waves' lists (entries are distinct:
+  //      every position is evaluated by one wave at most), written in ascending position order
+  uint32_t* bm = reinterpret_cast<uint32_t*>(&ring[0][0]);              // position bitmap
+  uint64_t* gb = reinterpret_cast<uint64_t*>(&ring[0][0]) + kBitmapWords / 2;  // the cut bin's entries
+  const int n_words = (n_cand + 31) >> 5;
+  __syncthreads();  // every list is final; the ring and the pass-2 histogram are free
+  for (int i = tid; i < kPruneBins; i += NT) red_hist[i] = 0u;
+  for (int i = tid; i < n_words; i += NT) bm[i] = 0u;
+  if (tid == 0) {
+    n_eval = 0u;  // from here: entries of the cut bin
+    cut = 0u;
+    bmax_bits = 0u;
+    cut_entry = ~0ull;
+  }
   __syncthreads();
+  const int n_mine = cl.n;  // wave-uniform
+  const uint32_t* okw = cl.okey;
+  const uint16_t* pw = cl.pos;
+  for (int i0 = 0; i0 < n_mine; i0 += 64) {
+    const int i = i0 + lane;
+    wave_hist_add(red_hist, i < n_mine ? okw[i] >> kPruneShift : 0u, i < n_mine);
+  }
+  __syncthreads();
+  if (wave == 0) find_cut_bin(red_hist, top_bin, C, lane, &cut, &bmax_bits);
+  __syncthreads();
+  const uint32_t cbin = cut, above = bmax_bits;  // the C-th entry's bin; entries in higher bins
+  for (int i0 = 0; i0 < n_mine; i0 += 64) {
+    const int i = i0 + lane;
+    if (i < n_mine && (okw[i] >> kPruneShift) == cbin)
+      gb[atomicAdd(&n_eval, 1u)] = cand_entry(okw[i], pw[i]);
+  }
+  __syncthreads();
+  // the (C - above)-th largest entry of the cut bin, by counting the larger ones
+  const int n_bin = (int)n_eval, need = C - (int)above;
+  for (int i = tid; i < n_bin; i += NT) {
+    const uint64_t e = gb[i];
+    int larger = 0;
+    for (int j = 0; j < n_bin; ++j) larger += gb[j] > e ? 1 : 0;
+    if (larger == need - 1) cut_entry = e;
+  }
+  __syncthreads();
+  const uint64_t t_entry = cut_entry;  // the C-th largest entry: the candidates are the entries >= it
+  for (int i0 = 0; i0 < n_mine; i0 += 64) {
+    const int i = i0 + lane;
+    if (i < n_mine && cand_entry(okw[i], pw[i]) >= t_entry)
+      atomicOr(&bm[pw[i] >> 5], 1u << (pw[i] & 31));
+  }
+  __syncthreads();
+  uint32_t* wpre = red_hist;  // candidates in the bitmap words before each word
+  if (wave == 0) {
+    constexpr int PW = kBitmapWords / 64;
+    uint32_t v[PW];
+    uint32_t sum = 0;
+#pragma unroll
+    for (int k = 0; k < PW; ++k) {
+      const int w = lane * PW + k;
+      v[k] = w < n_words ? (uint32_t)__popc(bm[w]) : 0u;
+      sum += v[k];
+    }
+    uint32_t incl = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t t = (uint32_t)__shfl_up((int)incl, o, 64);
+      if (lane >= o) incl += t;
+    }
+    uint32_t run = incl - sum;
+#pragma unroll
+    for (int k = 0; k < PW; ++k) {
+      wpre[lane * PW + k] = run;
+      run += v[k];
+    }
+  }
+  __syncthreads();
+  uint64_t* dst = a.cand_out + ((size_t)p * a.h_kv + g) * a.cand_stride;
+  for (int i0 = 0; i0 < n_mine; i0 += 64) {
+    const int i = i0 + lane;
+    if (i < n_mine) {
+      const uint64_t e = cand_entry(okw[i], pw[i]);
+      if (e >= t_entry) {
+        const int ps = pw[i];
+        const uint32_t below = bm[ps >> 5] & ((1u << (ps & 31)) - 1u);
+        const uint32_t rank = wpre[ps >> 5] + (uint32_t)__popc(below);
+        if (rank < (uint32_t)C) dst[rank] = e;  // exactly C entries are >= t_entry
+      }
+    }
+  }
+  for (int i = C + tid; i < a.cand_stride; i += NT) dst[i] = 0ull;
   if (tid == 0) {
     float d = c_max[0];
 #pragma unroll

@@ -381,7 +381,7 @@ def test_candidates_checks():
     units = 32 * 8
 
     def lists(stride):
-        return units * 8 * stride * 8  # 8 lists of `stride` 8-byte entries per unit
+        return units * stride * 8  # one list of `stride` 8-byte entries per unit
 
     norm = (units * 4 + 255) // 256 * 256
     scores = 32 * 32768 * 8 * 4
@@ -445,6 +445,6 @@ def test_candidates_checks():
     assert select(cand_mult=-1) == _lib.KV_ERR_ARG
     assert select(budget=0) == _lib.KV_ERR_BUDGET
     assert select(budget=4096) == _lib.KV_ERR_BUDGET
-    # the selection reads only the lists and the normalisers: 8 units x 8 lists x 256 entries
-    assert select(ws_bytes=8 * 8 * 256 * 8 + 256 - 1) == _lib.KV_ERR_WORKSPACE
+    # the selection reads only the lists and the normalisers: 8 units x 256 entries
+    assert select(ws_bytes=8 * 256 * 8 + 256 - 1) == _lib.KV_ERR_WORKSPACE
     assert select(ws=NULL) == _lib.KV_ERR_WORKSPACE

@@ -475,7 +475,7 @@ def test_candidate_lists_cut_back_during_the_pass(h_q, h_kv, d, lens, budget, ca
     assert wl.n_prob * wl.h_kv == 256 and _one_segment_per_unit(wl)
     b = _lib.Batch(wl.dtype, h_q, h_kv, d, wl.w, wl.lens, device="cpu")
     C = cand_mult * budget
-    lists = 256 * 8 * C * 8
+    lists = 256 * C * 8
     codes = 256 * ((max(lens) + 31) // 32) * 128  # 128 bytes per tile of the longest unit
     # the lists are formed in the window pass: the workspace holds them, the normalisers and the
     # first pass's tile codes only
