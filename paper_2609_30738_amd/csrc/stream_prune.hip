@@ -45,7 +45,7 @@ template <int NBH> struct TileCodes {
   static constexpr int kStores = 1;
   uint32_t* codes;  // tile i at codes + 32 i: word r = window row r, byte b = head b (255 unused)
   float* ref;       // [n_tiles] LDS
-  float c;
+  float c;          // softmax scale * log2(e)
   int l32, lane;
 
   template <int NB>
@@ -58,8 +58,7 @@ template <int NBH> struct TileCodes {
       tm[b] = max_halves(tmax[b]) * c;
       r = __builtin_elementwise_maximum(r, tm[b]);
     }
-#pragma unroll
-    for (int off = 1; off < 32; off <<= 1) r = __builtin_elementwise_maximum(r, __shfl_xor(r, off, 64));
+    r = max32_f(r);  // the tile's largest t: the same in every lane
     uint32_t w = 0xFFFFFFFFu;
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
