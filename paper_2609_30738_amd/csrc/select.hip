@@ -40,6 +40,7 @@ constexpr int kMaxCandBytes = 131072;        // LDS copy of the candidate keys
 constexpr int kMaxStagedKeyBytes = 139264;  // LDS copy of every candidate's score key (34816)
 constexpr size_t kLdsBytes = 163840;        // LDS of one CU
 constexpr int kGramMaxCand = 256;           // candidates of the Gram greedy (4 per lane of a wave)
+constexpr int kMaxSlotWords = 64;           // bitmap words over the candidate slots (C <= 2048)
 constexpr int kGramSlots = kGramMaxCand / 64;
 
 // Entries of the upper triangle (diagonal included) of a C x C matrix, and the index of (i, j),
@@ -787,7 +788,6 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
         st[q] = c < C ? fmaxf(cst[c], -FLT_MAX) : -INFINITY;
         corr[q] = 0.f;
       }
-      float* corr_adm = cst;  // s~ has been read: the slot of s~ keeps the corr at admission
       for (int t = 0; t < bp; ++t) {
         // the cosines against the last admitted slot, every read in flight at once (slots past C
         // read a valid entry that is not used)
@@ -811,23 +811,26 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
         }
         const uint64_t b = wave_best<false>(my_score, my_slot);
         last = __builtin_amdgcn_readfirstlane(min(max(unpack_slot(b), 0), C - 1));  // bp <= C
-        const int q_last = last >> 6;
-        if (lane == (last & 63)) {
 #pragma unroll
-          for (int q = 0; q < kGramSlots; ++q)
-            if (q == q_last) {
-              st[q] = -INFINITY;
-              corr_adm[last] = corr[q];
-            }
-        }
-        if (lane == 0) {  // the step's record; written out after the last step
-          trace_slot[t] = (uint32_t)last;
-          trace_key[t] = (uint32_t)(b >> 32);
-        }
+        for (int q = 0; q < kGramSlots; ++q) st[q] = lane + 64 * q == last ? -INFINITY : st[q];
+        // the step's record, written out after the last step (every lane stores the same value)
+        trace_slot[t] = (uint32_t)last;
+        trace_key[t] = (uint32_t)(b >> 32);
       }
       if (cand_idx || cand_corr) {
-        // corr after the last step includes the last admitted key; an admitted slot reports its
-        // corr at admission
+        // an admitted slot reports its corr at admission: the largest of 0 and its cosines to the
+        // slots admitted before it (the same maximum the steps formed); the slot of s~ keeps it
+        float* corr_adm = cst;
+        for (int t = lane; t < bp; t += 64) {
+          const int si = (int)trace_slot[t];
+          float m = 0.f;
+          for (int u = 0; u < t; ++u) {
+            const int su = (int)trace_slot[u];
+            m = __builtin_elementwise_maximum(m, gram[si < su ? row_off(si) + su : row_off(su) + si]);
+          }
+          corr_adm[si] = m;
+        }
+        // corr after the last step includes the last admitted key
         const size_t o = ((size_t)p * h_kv + g) * cand_stride;
         const int off_last = row_off(last);
 #pragma unroll
@@ -994,15 +997,37 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
   }
 
   if (co.k_out) {
-    // the unit's compacted rows: the admitted positions sorted in the key-row region (dead once
-    // the last candidate has read it), then the rows copied as in compact.hip
-    int32_t* srt = reinterpret_cast<int32_t*>(region);
-    int n2 = 1;
-    while (n2 < bp) n2 <<= 1;
+    // the unit's compacted rows: the admitted positions in ascending order, then the rows copied
+    // as in compact.hip.  The candidates are in position order, so the admitted slots in ascending
+    // order give the positions in ascending order: a bitmap over the slots and the prefix counts of
+    // its words rank them (in the key-row region, dead once the last candidate has read it).
+    static_assert(kMaxSlotWords <= 64, "one bitmap word per lane of a wave");
+    uint32_t* bits = reinterpret_cast<uint32_t*>(region);
+    uint32_t* pre = bits + kMaxSlotWords;
+    int32_t* srt = reinterpret_cast<int32_t*>(pre + kMaxSlotWords);
+    const int words = (C + 31) >> 5;
     __syncthreads();
-    for (int i = tid; i < n2; i += kThreads) srt[i] = i < bp ? cpos[trace_slot[i]] : INT_MAX;
+    for (int w = tid; w < words; w += kThreads) bits[w] = 0u;
     __syncthreads();
-    sort_positions(srt, n2, tid, kThreads);
+    for (int t = tid; t < bp; t += kThreads)
+      atomicOr(&bits[trace_slot[t] >> 5], 1u << (trace_slot[t] & 31));
+    __syncthreads();
+    if (wave == 0) {
+      const uint32_t v = lane < words ? (uint32_t)__popc(bits[lane]) : 0u;
+      uint32_t incl = v;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t o = (uint32_t)__shfl_up((int)incl, off, 64);
+        if (lane >= off) incl += o;
+      }
+      if (lane < words) pre[lane] = incl - v;
+    }
+    __syncthreads();
+    for (int t = tid; t < bp; t += kThreads) {
+      const uint32_t sl = trace_slot[t];
+      srt[pre[sl >> 5] + (uint32_t)__popc(bits[sl >> 5] & ((1u << (sl & 31)) - 1u))] = cpos[sl];
+    }
+    __syncthreads();
     constexpr int kRowVecs = D * (int)sizeof(T) / 16;
     copy_kept_rows(co.k, co.v, srt, bp, keep_tail, L, kRowVecs, base * kRowVecs,
                    ((size_t)p * h_kv + g) * co.out_rows * kRowVecs, co.k_out, co.v_out, tid,
@@ -1024,7 +1049,10 @@ size_t lds_head(int max_cand) { return ((size_t)max_cand * 12 + 15) & ~(size_t)1
 template <int DT, int D, int NT, int CPT, bool STAGED, bool GRAM>
 hipError_t select_launch(const Shape& s, const SelectArgs& a, size_t body, hipStream_t st) {
   using T = typename Elem<DT>::T;
-  const size_t region = std::max(body, STAGED ? (size_t)a.max_cand_all * 4 : (size_t)0);
+  // the region also holds the compaction's slot bitmap, its word prefixes and the positions
+  const size_t region =
+      std::max(std::max(body, STAGED ? (size_t)a.max_cand_all * 4 : (size_t)0),
+               (size_t)(2 * kMaxSlotWords + a.max_cand) * 4);
   const size_t dyn = lds_head(a.max_cand) + region;
   auto kern = mmr_select_kernel<DT, D, NT, CPT, STAGED, GRAM>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),

@@ -164,10 +164,11 @@ template <int D, int NB, int NW, int S> struct KeyStream {
   // (LDS) names it
   const uint16_t* order = nullptr;
 
-  __device__ int tile_key(int j) const {
-    const int t = order ? (int)order[j * NW + wave] : j * NW + wave;
-    return k0 + t * kTileKeys;
+  // the segment's tile index of the wave's tile j
+  __device__ int tile_index(int j) const {
+    return order ? (int)order[j * NW + wave] : j * NW + wave;
   }
+  __device__ int tile_key(int j) const { return k0 + tile_index(j) * kTileKeys; }
 
   // tile j into its slot; rows past the segment end re-read its last key
   __device__ __forceinline__ void issue(int j) const {

@@ -61,7 +61,7 @@ __device__ __forceinline__ void stats_tiles(const KeyStream<D, NB, NW, S>& ks,
         z_run[b] = fmaf(z_run[b], keep, (zs[0] + zs[1]) + (zs[2] + zs[3]));
         m_run[b] = mn;
       }
-      hook.template interior<NB>(j * NW + ks.wave, tmax);
+      hook.template interior<NB>(ks.tile_index(j), tmax);
     } else {
       // window row l32 of every head sees keys <= L - 32 + l32; keys >= k1 belong to the next
       // segment.  The key of register jj is t0 + 4 half + 8 (jj / 4) + (jj % 4).
@@ -85,7 +85,7 @@ __device__ __forceinline__ void stats_tiles(const KeyStream<D, NB, NW, S>& ks,
           m_run[b] = mn;
         }
       }
-      hook.guarded(j * NW + ks.wave);
+      hook.guarded(ks.tile_index(j));
     }
   }
 }
