@@ -132,6 +132,19 @@ __device__ __forceinline__ float max32_f(float v) {
   return __builtin_elementwise_maximum(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
 }
 
+// inclusive prefix sum over the 64 lanes in lane order: steps of 1, 2, 4 and 8 lanes within each
+// row of 16 (DPP row shifts, lanes shifted in from outside the row read 0), then the last lane of
+// each row added to the rows after it (DPP row broadcasts)
+__device__ __forceinline__ uint32_t wave_inclusive_sum(uint32_t x) {
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x111, 0xF, 0xF, true);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x112, 0xF, 0xF, true);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x114, 0xF, 0xF, true);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x118, 0xF, 0xF, true);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x142, 0xA, 0xF, false);  // row_bcast:15 into rows 1, 3
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x143, 0xC, 0xF, false);  // row_bcast:31 into rows 2, 3
+  return x;
+}
+
 // s_waitcnt vmcnt(later NDMA + (stores ? TS : 0)) for a run-time later in [0, 3]
 template <int NDMA, int TS>
 __device__ __forceinline__ void wait_vmem_tiles(int later, bool stores) {

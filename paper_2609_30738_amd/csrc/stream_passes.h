@@ -250,7 +250,7 @@ struct Prune {
   const float* ubs;      // [n_tiles] LDS: score bound of the i-th tile of the order
   uint32_t* hist;        // [kPruneBins] LDS: evaluated candidate keys per bin
   uint32_t* cut;         // LDS: the unit's current cut (an order key; 0: none yet)
-  uint32_t* top_bin;     // LDS: a bin at or above every nonempty one
+  int top_bin;           // where the cut's scan starts: the bin of the largest finite tile bound
   int n_cand;
 
   // The wave's next tile is worth evaluating (its bound is not below the cut).
@@ -265,27 +265,18 @@ struct Prune {
   __device__ __forceinline__ void add(float sv, int key, bool valid, int lane) {
     const uint32_t ok = order_key(sv);
     wave_hist_add(hist, ok >> kPruneShift, valid);
-    uint32_t hb = valid ? ok >> kPruneShift : 0u;
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) hb = max(hb, (uint32_t)__shfl_xor((int)hb, off, 64));
-    if (lane == 0) atomicMax(top_bin, hb);
     const uint32_t c = __builtin_amdgcn_readfirstlane(*cut);
     cl.add(sv, key, valid && ok >= c, lane);
   }
 
-  // Raise the cut to the lower edge of the bin that holds the C-th best evaluated key (the
-  // histogram as this wave sees it: counts only grow, so a stale view gives a lower cut).
+  // Raise the cut to the lower edge of the bin that holds the C-th best evaluated key among the
+  // bins from top_bin down (the histogram as this wave sees it: counts only grow, so a stale view,
+  // like keys above top_bin left out, gives a lower cut).
   __device__ __forceinline__ void update_cut(int lane) {
-    int b0 = (int)__builtin_amdgcn_readfirstlane(*top_bin);
     uint32_t cum = 0;
-    for (; b0 >= 0; b0 -= 64) {
+    for (int b0 = top_bin; b0 >= 0; b0 -= 64) {
       const int b = b0 - lane;
-      uint32_t pre = b >= 0 ? hist[b] : 0u;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const uint32_t o = (uint32_t)__shfl_up((int)pre, off, 64);
-        if (lane >= off) pre += o;
-      }
+      const uint32_t pre = wave_inclusive_sum(b >= 0 ? hist[b] : 0u);
       const uint64_t hit = __ballot(cum + pre >= (uint32_t)cl.C);
       if (hit) {
         const int bin = b0 - (__ffsll((unsigned long long)hit) - 1);

@@ -132,12 +132,7 @@ __device__ __forceinline__ void find_cut_bin(const uint32_t* hist, uint32_t top,
   for (int b0 = (int)top; b0 >= 0; b0 -= 64) {
     const int b = b0 - lane;
     const uint32_t own = b >= 0 ? hist[b] : 0u;
-    uint32_t pre = own;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const uint32_t t = (uint32_t)__shfl_up((int)pre, o, 64);
-      if (lane >= o) pre += t;
-    }
+    const uint32_t pre = wave_inclusive_sum(own);
     const uint64_t hit = __ballot(cum + pre >= (uint32_t)C);
     if (hit) {
       const int hl = __ffsll((unsigned long long)hit) - 1;
@@ -206,7 +201,6 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   stats_to_lds<NB>(m_run, z_run, red + wave * R, l32, half);
   if (tid == 0) {
     cut = 0u;
-    top_bin = 0u;
     bmax_bits = 0u;
   }
   __syncthreads();
@@ -305,8 +299,11 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   const int my_tiles2 = n_ord > wave ? (n_ord - wave + NW - 1) / NW : 0;
   KeyStream<D, NB, NW, S> ks2{ring[wave], kg, 0, L, wave, lane, order};
   ks2.prologue(my_tiles2);
+  // the cut's scan starts at the bin of the largest finite bound: scores above it (in tiles with a
+  // masked key) are left out of the scan, which only lowers the cut
+  const int scan_top = bmax > 0.f ? (int)(order_key(bmax) >> kPruneShift) : kPruneBins - 1;
   Prune pr{CandList{c_okey + wave * kCandCap, c_pos + wave * kCandCap, C, 0, 0ull, false, -INFINITY},
-           ub, red_hist, &cut, &top_bin, n_cand};
+           ub, red_hist, &cut, scan_top, n_cand};
   const ScoreOut so{nullptr, lam1, a.w_mu};
   mu_sigma_tiles<D, NB, ALL, NW, S, kOutCand>(ks2, q, bsh, my_tiles2, L, L, c, inv_g, nullptr,
                                               nullptr, l32, half, so, &pr);
@@ -329,6 +326,7 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   if (tid == 0) {
     n_eval = 0u;  // from here: entries of the cut bin
     cut = 0u;
+    top_bin = 0u;
     bmax_bits = 0u;
     cut_entry = ~0ull;
   }
@@ -336,10 +334,16 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   const int n_mine = cl.n;  // wave-uniform
   const uint32_t* okw = cl.okey;
   const uint16_t* pw = cl.pos;
+  uint32_t my_top = 0u;
   for (int i0 = 0; i0 < n_mine; i0 += 64) {
     const int i = i0 + lane;
-    wave_hist_add(red_hist, i < n_mine ? okw[i] >> kPruneShift : 0u, i < n_mine);
+    const uint32_t bin_i = i < n_mine ? okw[i] >> kPruneShift : 0u;
+    wave_hist_add(red_hist, bin_i, i < n_mine);
+    my_top = max(my_top, bin_i);
   }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) my_top = max(my_top, (uint32_t)__shfl_xor((int)my_top, o, 64));
+  if (lane == 0) atomicMax(&top_bin, my_top);
   __syncthreads();
   if (wave == 0) find_cut_bin(red_hist, top_bin, C, lane, &cut, &bmax_bits);
   __syncthreads();
