@@ -290,7 +290,7 @@ int kv_mmr_select_scored(const kv_problem* pr, const float* score, const void* k
  * KV_ERR_ARG; w_mu and the per-problem budgets as in kv_mmr_select_ex) must be the values later
  * given to kv_mmr_select_candidates.  lambda1: [n_prob] fp32 device.
  * For bf16 batches that kv_window_base_scores scores inside the window kernel's second pass, with
- * cand_mult > 0, C_p <= 288 and L_p <= 32768, the keys are read once in full, the candidates
+ * cand_mult > 0 and L_p <= 32768, the keys are read once in full, the candidates
  * are cut inside that launch (a second pass revisits only the 32-key tiles whose score bound
  * reaches the cut) and no score is stored; otherwise the scores go through the workspace and the
  * selection kernel's first phases cut the candidates from them.  Calls that overlap on one

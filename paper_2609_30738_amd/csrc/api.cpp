@@ -154,13 +154,11 @@ size_t cand_lists_bytes(const kv_problem* pr, int stride) {
   return align_up((size_t)pr->n_prob * pr->h_kv * stride * sizeof(uint64_t));
 }
 
-// Whether kv_window_candidates forms the candidate lists inside the window kernel's second pass:
-// every unit one segment of a streaming shape, units of at most kCandMaxLen keys, at most kCandMaxC
-// candidates (cand_mult > 0).
-bool cands_in_window_pass(const kv_problem* pr, const kv::Shape& s, float scale, int32_t cand_mult,
-                          int stride) {
-  return scores_in_window_pass(pr, s, scale) && cand_mult > 0 && stride <= kv::kCandMaxC &&
-         s.max_len <= kv::kCandMaxLen;
+// Whether kv_window_candidates forms the candidate lists inside the window kernel: every unit one
+// segment of a streaming shape, units of at most kCandMaxLen keys, cand_mult > 0 (the caller has
+// checked the candidate count against the selection's limit).
+bool cands_in_window_pass(const kv_problem* pr, const kv::Shape& s, float scale, int32_t cand_mult) {
+  return scores_in_window_pass(pr, s, scale) && cand_mult > 0 && s.max_len <= kv::kCandMaxLen;
 }
 
 // Workspace of kv_window_candidates: the lists and the units' normalisers, then with the fused
@@ -515,7 +513,7 @@ size_t kv_candidates_workspace_bytes(const kv_problem* pr, int32_t budget, int32
   if (opts && opts->pool != 1) return 0;
   const int stride = max_candidates(pr, budget, cand_mult, keep_tail, b_host);
   if (stride > kv::select_max_candidates(pr->d, elem_bytes(pr->dtype))) return 0;
-  return cand_ws_bytes(pr, s, stride, cands_in_window_pass(pr, s, 1.f, cand_mult, stride));
+  return cand_ws_bytes(pr, s, stride, cands_in_window_pass(pr, s, 1.f, cand_mult));
 }
 
 int kv_window_candidates(const kv_problem* pr, const void* q_win, const void* k, float scale,
@@ -541,7 +539,7 @@ int kv_window_candidates(const kv_problem* pr, const void* q_win, const void* k,
   if (st != KV_OK) return st;
   const int stride = max_candidates(pr, budget, cand_mult, keep_tail, b_host);
   if (stride > kv::select_max_candidates(pr->d, elem_bytes(pr->dtype))) return KV_ERR_SHAPE;
-  const bool fused = cands_in_window_pass(pr, s, scale, cand_mult, stride);
+  const bool fused = cands_in_window_pass(pr, s, scale, cand_mult);
   const size_t need = cand_ws_bytes(pr, s, stride, fused);
   if (ws_bytes < need || !ws || (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1)))
     return KV_ERR_WORKSPACE;

@@ -79,8 +79,7 @@ hipError_t launch_stream_window_scores(const Shape& s, const StreamPlan& plan, c
 // largest base score over the candidate positions clamped at 1e-12.  The
 // keys are read once in full; the second pass revisits only the tiles whose score bound reaches
 // the unit's cut.  codes: scratch of n_units * cand_code_stride(s) words (the first pass's tile
-// codes).  Units of at most kCandMaxLen keys and C_p <= kCandMaxC.
-constexpr int kCandMaxC = 288;
+// codes, then the evaluated keys' scores).  Units of at most kCandMaxLen keys.
 constexpr int kCandMaxLen = 32768;
 int cand_code_stride(const Shape& s);
 hipError_t launch_stream_window_cands(const Shape& s, const StreamPlan& plan, const void* q_win,

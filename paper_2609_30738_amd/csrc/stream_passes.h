@@ -126,132 +126,28 @@ struct ScoreOut {
   float lam1, w_mu;
 };
 
-// What pass 2 writes per key: mu and sigma, the base score, or nothing (candidate mode: the key's
-// base score only enters the wave's candidate list below).
+// What pass 2 writes per key: mu and sigma, the base score, or (candidate mode) the base score of
+// the keys of the tiles it evaluates, which also enter the unit's histogram of scores below.
 enum PassOut { kOutMuSigma = 0, kOutScore = 1, kOutCand = 2 };
-
-// Candidate list of one wave in the second pass of candidate mode.  The unit's candidate set is
-// the C keys with the largest base scores, ties to the lower position (section 3.2, the top-4B
-// restriction); it is the top C of the union of every wave's own top C.  A wave keeps, in LDS,
-// every key whose entry (order key of its score, position) beats the C-th best entry among the
-// wave's earlier keys (a lower bound of the unit's final cut) and a bound shared by the waves, and
-// when the list fills it sorts the list in registers and keeps the best C.
-constexpr int kCandCap = 320;              // entries per wave: 1920 bytes of LDS
-constexpr int kCandMax = kCandCap - 32;    // largest C (a tile appends at most 32 entries)
-static_assert(kCandMax == kCandMaxC, "the host's limit on C");
-
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
-  const uint32_t lo = __shfl_xor((uint32_t)v, m, 64), hi = __shfl_xor((uint32_t)(v >> 32), m, 64);
-  return ((uint64_t)hi << 32) | lo;
-}
-
-// Descending bitonic sort of 512 entries held by one wave, 8 per lane (entry lane * 8 + i in v[i]).
-__device__ __forceinline__ void wave_sort_desc_512(uint64_t (&v)[8], int lane) {
-#pragma unroll
-  for (int k = 2; k <= 512; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      if (j >= 8) {
-        // partner in lane ^ (j / 8), same register
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const uint64_t o = shfl_xor_u64(v[i], j >> 3);
-          const int idx = lane * 8 + i;
-          // blocks with (idx & k) == 0 end descending; the pair's lower index keeps the larger
-          const bool take_max = ((idx & j) == 0) == ((idx & k) == 0);
-          v[i] = take_max ? (o > v[i] ? o : v[i]) : (o < v[i] ? o : v[i]);
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          if ((i & j) == 0) {
-            const int p = i | j;
-            const bool desc = ((lane * 8 + i) & k) == 0;
-            const uint64_t a = v[i], b = v[p];
-            const bool sw = desc ? (a < b) : (a > b);
-            v[i] = sw ? b : a;
-            v[p] = sw ? a : b;
-          }
-        }
-      }
-    }
-  }
-}
-
-struct CandList {
-  uint32_t* okey;  // [kCandCap] LDS: order key of the entry's score
-  uint16_t* pos;   // [kCandCap] LDS: its position (units of at most 65535 keys)
-  int C;           // the unit's candidate count, 1..kCandMax
-  int n;           // entries held (wave-uniform)
-  uint64_t thr;    // once `bounded`, an entry must be larger than this one
-  bool bounded;
-  float smax;      // the lane's running maximum of its candidate positions' scores (NaN ignored)
-
-  // Sort the held entries and keep the best C (n > C).
-  __device__ __forceinline__ void compact(int lane) {
-    uint64_t v[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int idx = lane * 8 + i;
-      v[i] = idx < n ? cand_entry(okey[idx], pos[idx]) : 0ull;  // real entries are > 0
-    }
-    wave_sort_desc_512(v, lane);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int idx = lane * 8 + i;
-      if (idx < C) {
-        okey[idx] = (uint32_t)(v[i] >> 32);
-        pos[idx] = (uint16_t)cand_entry_pos(v[i]);
-      }
-    }
-    // the C-th best entry: register (C - 1) % 8 of lane (C - 1) / 8
-    uint64_t t = v[0];
-#pragma unroll
-    for (int i = 1; i < 8; ++i)
-      if (((C - 1) & 7) == i) t = v[i];
-    const int src = (C - 1) >> 3;
-    // (readlane returns int: both halves go through uint32_t, or the low one sign-extends)
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((uint32_t)(t >> 32), src);
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((uint32_t)t, src);
-    thr = ((uint64_t)hi << 32) | lo;
-    bounded = true;
-    n = C;
-  }
-
-  // One key per lane of half 0 (valid: a candidate position); every lane of the wave calls it.
-  __device__ __forceinline__ void add(float sv, int key, bool valid, int lane) {
-    if (valid) smax = fmaxf(smax, sv);
-    const uint32_t ok = order_key(sv);
-    const bool in = valid && (!bounded || cand_entry(ok, (uint32_t)key) > thr);
-    const uint64_t m = __ballot(in);
-    if (m != 0ull) {
-      // entries of the lanes below this one
-      const int slot = n + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                                           __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-      if (in) {
-        okey[slot] = ok;
-        pos[slot] = (uint16_t)key;
-      }
-      n += (int)__popcll(m);
-      if (n > kCandMax) compact(lane);
-    }
-  }
-};
 
 // Shared state of the second pass of candidate mode (stream_prune.hip), which revisits the unit's
 // tiles in decreasing order of their score bound and stops at the first tile whose bound is below
 // the unit's cut: the order key of the C-th best base score among the keys evaluated so far,
 // rounded down to its bin of an LDS histogram of those keys (a lower bound of the final cut, so
-// no key left out can be among the C best).
+// no key left out can be among the C best).  Every evaluated key's base score is stored at
+// score_u[key] (section 3.2, the top-4B restriction: the candidate set is cut from them after the
+// pass).
 constexpr int kPruneShift = 21;                     // histogram bin = order key >> kPruneShift
 constexpr int kPruneBins = 1 << (32 - kPruneShift);
 struct Prune {
-  CandList cl;           // the wave's candidate list
   const float* ubs;      // [n_tiles] LDS: score bound of the i-th tile of the order
   uint32_t* hist;        // [kPruneBins] LDS: evaluated candidate keys per bin
   uint32_t* cut;         // LDS: the unit's current cut (an order key; 0: none yet)
+  float* score_u;        // the unit's score row (the evaluated keys only)
   int top_bin;           // where the cut's scan starts: the bin of the largest finite tile bound
-  int n_cand;
+  int n_cand, C;
+  float smax;            // the lane's largest score over candidate positions (NaN ignored)
+  int evaluated;         // tiles this wave evaluated
 
   // The wave's next tile is worth evaluating (its bound is not below the cut).
   __device__ __forceinline__ bool wanted(int idx) const {
@@ -261,12 +157,10 @@ struct Prune {
   }
 
   // The evaluated candidate keys of a tile (one per lane of half 0) into the histogram and the
-  // list; the list takes only keys at or above the cut.
-  __device__ __forceinline__ void add(float sv, int key, bool valid, int lane) {
-    const uint32_t ok = order_key(sv);
-    wave_hist_add(hist, ok >> kPruneShift, valid);
-    const uint32_t c = __builtin_amdgcn_readfirstlane(*cut);
-    cl.add(sv, key, valid && ok >= c, lane);
+  // running maximum (the store of the score is the caller's).
+  __device__ __forceinline__ void add(float sv, bool valid) {
+    if (valid) smax = fmaxf(smax, sv);
+    wave_hist_add(hist, order_key(sv) >> kPruneShift, valid);
   }
 
   // Raise the cut to the lower edge of the bin that holds the C-th best evaluated key among the
@@ -277,7 +171,7 @@ struct Prune {
     for (int b0 = top_bin; b0 >= 0; b0 -= 64) {
       const int b = b0 - lane;
       const uint32_t pre = wave_inclusive_sum(b >= 0 ? hist[b] : 0u);
-      const uint64_t hit = __ballot(cum + pre >= (uint32_t)cl.C);
+      const uint64_t hit = __ballot(cum + pre >= (uint32_t)C);
       if (hit) {
         const int bin = b0 - (__ffsll((unsigned long long)hit) - 1);
         if (lane == 0) atomicMax(cut, (uint32_t)bin << kPruneShift);
@@ -296,15 +190,15 @@ struct Prune {
 // across heads with the pairwise update of Chan, Golub and LeVeque.  With OUT = kOutScore the
 // key's base score s = fma(lam1, sigma, w_mu mu) (section 3.2, Eq. (5)) is stored instead, with the
 // same rounding as a score formed later from the stored mu and sigma; with OUT = kOutCand the
-// score goes to the candidate state `pr` (keys below n_cand), nothing is stored, and the wave
-// stops at its first tile that pr no longer wants.
+// score is also stored (at pr->score_u) and counted by the candidate state `pr` (keys below
+// n_cand), and the wave stops at its first tile that pr no longer wants.
 template <int D, int NB, bool ALL, int NW, int S, int OUT = kOutMuSigma>
 __device__ __forceinline__ void mu_sigma_tiles(const KeyStream<D, NB, NW, S>& ks,
                                                const bf16x8_t (&q)[NB][D / 16], const float* bsh,
                                                int my_tiles, int k1, int L, float c, float inv_g,
                                                float* mu_u, float* sigma_u, int l32, int half,
                                                ScoreOut so = {}, Prune* pr = nullptr) {
-  constexpr int kStores = OUT == kOutCand ? 0 : 1;  // global stores per tile (the waits count them)
+  constexpr int kStores = 1;  // global stores per tile (the waits count them)
   const int lane = threadIdx.x & 63;
   constexpr int NS = D / 16;
   auto tile = [&](const bf16x8_t (&kt)[NS], int t0, auto masked) __attribute__((always_inline)) {
@@ -378,13 +272,15 @@ __device__ __forceinline__ void mu_sigma_tiles(const KeyStream<D, NB, NW, S>& ks
       if (half == 0 && key < k1) store_stat(so.score_u + key, sv);
     } else if constexpr (OUT == kOutCand) {
       const float sv = fmaf(so.lam1, __builtin_amdgcn_sqrtf(var), so.w_mu * mean);
-      pr->add(sv, key, half == 0 && key < pr->n_cand, lane);
+      pr->add(sv, half == 0 && key < pr->n_cand);
+      if (half == 0 && key < k1) store_stat(pr->score_u + key, sv);
     } else {
       if (key < k1) store_stat((half == 0 ? mu_u : sigma_u) + key, half == 0 ? mean : __builtin_amdgcn_sqrtf(var));
     }
   };
 
-  for (int j = 0; j < my_tiles; ++j) {
+  int j = 0;
+  for (; j < my_tiles; ++j) {
     if constexpr (OUT == kOutCand) {
       if (!pr->wanted(j * NW + ks.wave)) break;
     }
@@ -395,6 +291,7 @@ __device__ __forceinline__ void mu_sigma_tiles(const KeyStream<D, NB, NW, S>& ks
     else tile(kt, t0, std::false_type{});
     if constexpr (OUT == kOutCand) pr->update_cut(lane);
   }
+  if constexpr (OUT == kOutCand) pr->evaluated = j;
 }
 
 }  // namespace stream

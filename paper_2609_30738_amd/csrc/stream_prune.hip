@@ -9,12 +9,13 @@
 // then ordered by their bounds (a counting sort into bins of 1/16 of an octave below the largest
 // bound, each tile standing for its bin's upper edge) and pass 2 evaluates the exact base scores
 // tile by tile in that order, wave w taking positions w, w + 8, ... of the order.  The evaluated
-// keys of the candidate range go into an LDS histogram and the waves' candidate lists (Prune,
-// CandList); the histogram gives a lower bound of the unit's cut (the C-th best score), and a wave
-// stops at its first tile whose bound lies below it: every key of the tiles left out scores below
-// the cut.  Scores are formed by the same code as in the other window kernels, so each evaluated
-// key's score is the one kv_window_base_scores writes, bit for bit; the candidate lists therefore
-// hold exactly the unit's C best entries.
+// keys of the candidate range go into an LDS histogram (Prune), which gives a lower bound of the
+// unit's cut (the C-th best score), and a wave stops at its first tile whose bound lies below it:
+// every key of the tiles left out scores below the cut.  The evaluated scores are stored over the
+// tiles' codes; after the pass the C-th largest (score, position) entry among them is found digit
+// by digit, and the C candidates are written in position order.  Scores are formed by the same
+// code as in the other window kernels, so each evaluated key's score is the one
+// kv_window_base_scores writes, bit for bit, and the candidates are exactly the unit's C best.
 //
 // On the 32-layer Mistral-shaped pass at L = 32768 (C = 256) the bounds leave about one tile in
 // twenty to pass 2.
@@ -122,6 +123,8 @@ __device__ __forceinline__ float tile_bound(const uint32_t* codes_t, float ref, 
 
 // Bitmap words over the candidate positions of a unit (one bit per position).
 constexpr int kBitmapWords = kCandMaxLen / 32;
+// Entries that share every digit found so far and are ranked directly (by counting).
+constexpr int kRankDirect = 512;
 
 // The bin (order key >> kPruneShift) of the C-th largest entry counted in hist, scanning down from
 // top (a bin at or above every nonempty one), into *cut_bin, and the number of entries in the bins
@@ -152,11 +155,10 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   constexpr int R = Gm::R, NS = Gm::NS, NT = NW * 64;
   constexpr int kRedWords = NW * R * 2;
   constexpr int kTilesPerThread = kPruneMaxTiles / NT;
-  static_assert(NW == kCandLists, "one candidate list per wave");
   static_assert(kPruneMaxTiles % NT == 0, "whole tiles per thread");
-  static_assert(NW * kCandCap >= 2 * kOrderBins, "the bin counts and offsets fit the lists");
-  static_assert(sizeof(uint16_t) * NW * S * Gm::TE >= 4 * kBitmapWords + 8 * NW * kCandCap,
-                "the bitmap and the cut bin's entries fit the ring");
+  static_assert(NT % kTileKeys == 0, "whole tiles per visit");
+  static_assert(sizeof(uint16_t) * NW * S * Gm::TE >= 4 * kBitmapWords + 8 * kRankDirect,
+                "the bitmap and the ranked group fit the ring");
   static_assert(kPruneBins >= kBitmapWords, "the word prefixes fit the histogram");
   __shared__ __align__(16) uint16_t ring[NW][S * Gm::TE];
   // the waves' statistics after pass 1, the histogram of evaluated scores in pass 2
@@ -165,11 +167,11 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   // pass 1: the tile's largest t; from the order on: the bound of the i-th tile of the order
   __shared__ float ub[kPruneMaxTiles];
   __shared__ uint16_t order[kPruneMaxTiles];
-  // the waves' candidate lists (before pass 2: the bin counts and offsets of the order)
-  __shared__ uint32_t c_okey[NW * kCandCap];
-  __shared__ uint16_t c_pos[NW * kCandCap];
+  // the bin counts and offsets of the order
+  __shared__ uint32_t bins[2 * kOrderBins];
   __shared__ float c_max[NW];
-  __shared__ uint32_t cut, top_bin, bmax_bits, n_eval;
+  __shared__ uint32_t ev[NW];
+  __shared__ uint32_t cut, bmax_bits, n_eval;
   __shared__ uint64_t cut_entry;
 
   const int g = blockIdx.y, p = blockIdx.z;
@@ -214,8 +216,8 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   __syncthreads();  // the normalisers are complete; red is free
 
   // ---- bounds of the thread's tiles tid + u NT (-inf: no candidate key, never revisited)
-  uint32_t* cnt = c_okey;                // [kOrderBins] tiles per bin
-  uint32_t* off = c_okey + kOrderBins;   // [kOrderBins] first position of each bin, then a cursor
+  uint32_t* cnt = bins;                  // [kOrderBins] tiles per bin
+  uint32_t* off = bins + kOrderBins;     // [kOrderBins] first position of each bin, then a cursor
   for (int i = tid; i < kPruneBins; i += NT) red_hist[i] = 0u;
   for (int i = tid; i < kOrderBins; i += NT) cnt[i] = 0u;
   const int n_cand = L - a.keep_tail;
@@ -292,83 +294,109 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   }
   __syncthreads();  // the order is complete; the lists and the ring are free
 
-  // ---- pass 2: exact scores of the wanted tiles
+  // ---- pass 2: exact scores of the wanted tiles, stored over their codes
   const int n_ord = (int)n_eval;
   const int bp = a.budgets ? a.budgets[p] : a.budget;
   const int C = min(a.cand_mult * bp, n_cand);
   const int my_tiles2 = n_ord > wave ? (n_ord - wave + NW - 1) / NW : 0;
   KeyStream<D, NB, NW, S> ks2{ring[wave], kg, 0, L, wave, lane, order};
   ks2.prologue(my_tiles2);
+  float* score_u = reinterpret_cast<float*>(codes_u);  // a tile's codes are dead once bounded
   // the cut's scan starts at the bin of the largest finite bound: scores above it (in tiles with a
   // masked key) are left out of the scan, which only lowers the cut
   const int scan_top = bmax > 0.f ? (int)(order_key(bmax) >> kPruneShift) : kPruneBins - 1;
-  Prune pr{CandList{c_okey + wave * kCandCap, c_pos + wave * kCandCap, C, 0, 0ull, false, -INFINITY},
-           ub, red_hist, &cut, scan_top, n_cand};
+  Prune pr{ub, red_hist, &cut, score_u, scan_top, n_cand, C, -INFINITY, 0};
   const ScoreOut so{nullptr, lam1, a.w_mu};
   mu_sigma_tiles<D, NB, ALL, NW, S, kOutCand>(ks2, q, bsh, my_tiles2, L, L, c, inv_g, nullptr,
                                               nullptr, l32, half, so, &pr);
-  wait_vmem<0>();  // no load into the ring may outlive the workgroup (a stopped wave has some)
-  CandList& cl = pr.cl;
-  if (cl.n > C) cl.compact(lane);  // the wave's best C
-  float m = cl.smax;
+  wait_vmem<0>();  // the score stores have landed; no load into the ring outlives the workgroup
+  float m = pr.smax;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-  if (lane == 0) c_max[wave] = m;
+  if (lane == 0) {
+    c_max[wave] = m;
+    ev[wave] = (uint32_t)pr.evaluated;
+  }
 
-  // ---- the unit's candidates: the C largest entries of the waves' lists (entries are distinct:
-  //      every position is evaluated by one wave at most), written in ascending position order
-  uint32_t* bm = reinterpret_cast<uint32_t*>(&ring[0][0]);              // position bitmap
-  uint64_t* gb = reinterpret_cast<uint64_t*>(&ring[0][0]) + kBitmapWords / 2;  // the cut bin's entries
-  const int n_words = (n_cand + 31) >> 5;
-  __syncthreads();  // every list is final; the ring and the pass-2 histogram are free
-  for (int i = tid; i < kPruneBins; i += NT) red_hist[i] = 0u;
-  for (int i = tid; i < n_words; i += NT) bm[i] = 0u;
+  // ---- the unit's candidates: the C largest entries (order key of the score, position) among
+  //      the evaluated keys, written in ascending position order.  The C-th largest entry is
+  //      found digit by digit (11 bits at a time, most significant first): the histogram of the
+  //      pass gives the first digit; each further digit counts the evaluated entries that share
+  //      the digits found so far, until few enough remain to rank them directly.
+  __syncthreads();  // the scores, the histogram and every wave's tile count are final
+  if (wave == 0) find_cut_bin(red_hist, kPruneBins - 1, C, lane, &cut, &bmax_bits);
+  __syncthreads();
+  int max_ev = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) max_ev = max(max_ev, (int)ev[w]);
+  const int n_pos = min(n_ord, max_ev * NW);  // order positions at or after this one: not evaluated
+  // visit every evaluated key once: fn(entry) for keys of the candidate range
+  auto for_each_entry = [&](auto fn) __attribute__((always_inline)) {
+    for (int p0 = 0; p0 < n_pos; p0 += NT / kTileKeys) {
+      const int pos = p0 + tid / kTileKeys;
+      if (pos < n_pos && (pos / NW) < (int)ev[pos % NW]) {
+        const int key = (int)order[pos] * kTileKeys + (tid % kTileKeys);
+        if (key < n_cand) {
+          // device-coherent load: the line may still sit in this CU's vector cache with the
+          // tile's codes, read before the score was stored over them
+          const float sc = __uint_as_float(__hip_atomic_load(
+              reinterpret_cast<uint32_t*>(score_u + key), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+          fn(cand_entry(order_key(sc), (uint32_t)key), key);
+        }
+      }
+    }
+  };
+  uint64_t prefix = (uint64_t)cut << (64 - (32 - kPruneShift));  // the digits found so far
+  int pbits = 32 - kPruneShift;                                   // their count
+  int need = C - (int)bmax_bits;  // how many entries of the group the candidates still take
+  uint32_t group = red_hist[cut];
+  while (group > (uint32_t)kRankDirect && pbits < 64) {
+    const int dbits = min(32 - kPruneShift, 64 - pbits);
+    const int shift = 64 - pbits - dbits;
+    __syncthreads();  // the last digit's readers are done with the histogram
+    for (int i = tid; i < kPruneBins; i += NT) red_hist[i] = 0u;
+    __syncthreads();
+    for_each_entry([&](uint64_t e, int) {
+      if ((e >> (64 - pbits)) == (prefix >> (64 - pbits)))
+        atomicAdd(&red_hist[(uint32_t)(e >> shift) & ((1u << dbits) - 1u)], 1u);
+    });
+    __syncthreads();
+    if (wave == 0) find_cut_bin(red_hist, (1 << dbits) - 1, need, lane, &cut, &bmax_bits);
+    __syncthreads();
+    prefix |= (uint64_t)cut << shift;
+    pbits += dbits;
+    need -= (int)bmax_bits;
+    group = red_hist[cut];
+  }
+  // the group: at most kRankDirect entries (or one, once every digit is found); its need-th
+  // largest entry is the C-th largest overall, found by counting the larger ones
+  uint64_t* gb = reinterpret_cast<uint64_t*>(&ring[0][0]) + kBitmapWords / 2;
   if (tid == 0) {
-    n_eval = 0u;  // from here: entries of the cut bin
-    cut = 0u;
-    top_bin = 0u;
-    bmax_bits = 0u;
+    n_eval = 0u;
     cut_entry = ~0ull;
   }
   __syncthreads();
-  const int n_mine = cl.n;  // wave-uniform
-  const uint32_t* okw = cl.okey;
-  const uint16_t* pw = cl.pos;
-  uint32_t my_top = 0u;
-  for (int i0 = 0; i0 < n_mine; i0 += 64) {
-    const int i = i0 + lane;
-    const uint32_t bin_i = i < n_mine ? okw[i] >> kPruneShift : 0u;
-    wave_hist_add(red_hist, bin_i, i < n_mine);
-    my_top = max(my_top, bin_i);
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) my_top = max(my_top, (uint32_t)__shfl_xor((int)my_top, o, 64));
-  if (lane == 0) atomicMax(&top_bin, my_top);
+  for_each_entry([&](uint64_t e, int) {
+    if ((e >> (64 - pbits)) == (prefix >> (64 - pbits)) && n_eval < (uint32_t)kRankDirect)
+      gb[min(atomicAdd(&n_eval, 1u), (uint32_t)kRankDirect - 1u)] = e;
+  });
   __syncthreads();
-  if (wave == 0) find_cut_bin(red_hist, top_bin, C, lane, &cut, &bmax_bits);
-  __syncthreads();
-  const uint32_t cbin = cut, above = bmax_bits;  // the C-th entry's bin; entries in higher bins
-  for (int i0 = 0; i0 < n_mine; i0 += 64) {
-    const int i = i0 + lane;
-    if (i < n_mine && (okw[i] >> kPruneShift) == cbin)
-      gb[atomicAdd(&n_eval, 1u)] = cand_entry(okw[i], pw[i]);
-  }
-  __syncthreads();
-  // the (C - above)-th largest entry of the cut bin, by counting the larger ones
-  const int n_bin = (int)n_eval, need = C - (int)above;
-  for (int i = tid; i < n_bin; i += NT) {
+  const int n_grp = min((int)n_eval, kRankDirect);
+  for (int i = tid; i < n_grp; i += NT) {
     const uint64_t e = gb[i];
     int larger = 0;
-    for (int j = 0; j < n_bin; ++j) larger += gb[j] > e ? 1 : 0;
+    for (int j = 0; j < n_grp; ++j) larger += gb[j] > e ? 1 : 0;
     if (larger == need - 1) cut_entry = e;
   }
+  // the candidates (the entries >= the C-th largest) in a bitmap over the positions
+  uint32_t* bm = reinterpret_cast<uint32_t*>(&ring[0][0]);
+  const int n_words = (n_cand + 31) >> 5;
+  for (int i = tid; i < n_words; i += NT) bm[i] = 0u;
   __syncthreads();
-  const uint64_t t_entry = cut_entry;  // the C-th largest entry: the candidates are the entries >= it
-  for (int i0 = 0; i0 < n_mine; i0 += 64) {
-    const int i = i0 + lane;
-    if (i < n_mine && cand_entry(okw[i], pw[i]) >= t_entry)
-      atomicOr(&bm[pw[i] >> 5], 1u << (pw[i] & 31));
-  }
+  const uint64_t t_entry = cut_entry;
+  for_each_entry([&](uint64_t e, int key) {
+    if (e >= t_entry) atomicOr(&bm[key >> 5], 1u << (key & 31));
+  });
   __syncthreads();
   uint32_t* wpre = red_hist;  // candidates in the bitmap words before each word
   if (wave == 0) {
@@ -381,13 +409,7 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
       v[k] = w < n_words ? (uint32_t)__popc(bm[w]) : 0u;
       sum += v[k];
     }
-    uint32_t incl = sum;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const uint32_t t = (uint32_t)__shfl_up((int)incl, o, 64);
-      if (lane >= o) incl += t;
-    }
-    uint32_t run = incl - sum;
+    uint32_t run = wave_inclusive_sum(sum) - sum;
 #pragma unroll
     for (int k = 0; k < PW; ++k) {
       wpre[lane * PW + k] = run;
@@ -396,18 +418,13 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   }
   __syncthreads();
   uint64_t* dst = a.cand_out + ((size_t)p * a.h_kv + g) * a.cand_stride;
-  for (int i0 = 0; i0 < n_mine; i0 += 64) {
-    const int i = i0 + lane;
-    if (i < n_mine) {
-      const uint64_t e = cand_entry(okw[i], pw[i]);
-      if (e >= t_entry) {
-        const int ps = pw[i];
-        const uint32_t below = bm[ps >> 5] & ((1u << (ps & 31)) - 1u);
-        const uint32_t rank = wpre[ps >> 5] + (uint32_t)__popc(below);
-        if (rank < (uint32_t)C) dst[rank] = e;  // exactly C entries are >= t_entry
-      }
+  for_each_entry([&](uint64_t e, int key) {
+    if (e >= t_entry) {
+      const uint32_t below = bm[key >> 5] & ((1u << (key & 31)) - 1u);
+      const uint32_t rank = wpre[key >> 5] + (uint32_t)__popc(below);
+      if (rank < (uint32_t)C) dst[rank] = e;  // exactly C entries are >= t_entry
     }
-  }
+  });
   for (int i = C + tid; i < a.cand_stride; i += NT) dst[i] = 0ull;
   if (tid == 0) {
     float d = c_max[0];

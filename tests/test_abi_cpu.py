@@ -374,8 +374,9 @@ def test_select_scored_checks():
 
 
 def test_candidates_checks():
-    """kv_window_candidates / kv_mmr_select_candidates: a workspace of candidate lists (and of the
-    scores when the window pass cannot keep the lists), argument checks before any launch."""
+    """kv_window_candidates / kv_mmr_select_candidates: a workspace of candidate lists and of the
+    window kernel's tile codes (or of the scores when the window kernel cannot cut the candidates
+    itself), argument checks before any launch."""
     lib = _lib.lib()
     big = HostProblem(lens=(32768,) * 32)  # 256 units, each one workgroup of the window kernel
     units = 32 * 8
@@ -388,9 +389,10 @@ def test_candidates_checks():
     codes = units * (32768 // 32) * 128  # the first pass's tile codes: 128 bytes per 32 keys
     assert lib.kv_candidates_workspace_bytes(big.ref(), 64, 4, 32, None) == (
         lists(256) + norm + codes)
-    # 512 candidates exceed a wave's list: the scores go through the workspace
-    assert lib.kv_candidates_workspace_bytes(big.ref(), 128, 4, 32, None) >= (
-        lists(512) + norm + scores)
+    # 512 candidates: the same layout
+    assert lib.kv_candidates_workspace_bytes(big.ref(), 128, 4, 32, None) == (
+        lists(512) + norm + codes)
+    # fp32 caches have no streaming window kernel: the scores go through the workspace
     f32 = HostProblem(dtype=_lib.KV_F32, lens=(32768,) * 32)
     assert lib.kv_candidates_workspace_bytes(f32.ref(), 64, 4, 32, None) >= (
         lists(256) + norm + scores)

@@ -463,14 +463,16 @@ def test_scored_calls_late_segments_and_second_launch(monkeypatch):
 
 @pytest.mark.parametrize("h_q,h_kv,d,lens,budget,cand_mult", [
     (8, 8, 64, [8192, 8161], 16, 4), (8, 8, 64, [8192, 8161], 37, 3),
-    (8, 8, 64, [8192, 8161], 72, 4), (32, 8, 128, [4096, 4065], 37, 3)])
-def test_candidate_lists_cut_back_during_the_pass(h_q, h_kv, d, lens, budget, cand_mult):
-    """256 units of one segment each, 4065 to 8192 keys: the candidate kernel codes every tile's
-    row maxima in pass 1, bounds the tiles' scores once the normalisers are known and revisits
-    tiles in decreasing order of their bounds until the cut passes them; a wave's candidate list
-    fills and is cut back to its C best (C = 64, 111 and 288, the largest: the C-th entry in each
-    of the register slots of its lane).  The selection from the lists equals kv_mmr_select_ex's,
-    every output bit for bit, and the oracle's."""
+    (8, 8, 64, [8192, 8161], 72, 4), (8, 8, 64, [8192, 8161], 128, 4),
+    (32, 8, 128, [4096, 4065], 37, 3), (32, 8, 128, [4096, 4065], 96, 4)])
+def test_candidates_cut_in_the_window_kernel(h_q, h_kv, d, lens, budget, cand_mult):
+    """256 units of one segment each, 4065 to 8192 keys, 2 % planted keys, so that for C above
+    their count the cut falls in the bulk: the candidate kernel codes every tile's row maxima in
+    pass 1, bounds the
+    tiles' scores once the normalisers are known, revisits tiles in decreasing order of their
+    bounds until the cut passes them, and finds the C-th largest of the evaluated entries digit by
+    digit (C = 64, 111, 288, 512 and 384).  The selection from its candidates equals
+    kv_mmr_select_ex's, every output bit for bit, and the oracle's."""
     wl = _shape_workload(h_q, h_kv, d, 2, 16, lens, budget=budget)
     assert wl.n_prob * wl.h_kv == 256 and _one_segment_per_unit(wl)
     b = _lib.Batch(wl.dtype, h_q, h_kv, d, wl.w, wl.lens, device="cpu")
