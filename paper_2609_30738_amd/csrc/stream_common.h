@@ -183,18 +183,43 @@ template <int D, int NB, int NW, int S> struct KeyStream {
   }
   __device__ int tile_key(int j) const { return k0 + tile_index(j) * kTileKeys; }
 
+  // Byte offset, within a tile, of the 16-byte chunk that load instruction i of this lane fetches
+  // (the chunk that lands at the lane's LDS slot 64 i + lane).  Four consecutive rows per
+  // instruction at d = 128, so the swizzle repeats every four instructions and the offset of
+  // instruction i is that of i mod 4 plus 4 KiB per four; at d = 64 it is that of 0 plus 1 KiB
+  // per instruction.
+  __device__ static int chunk_off(int i, int lane) {
+    const int pos = 64 * i + lane;  // LDS chunk slot written by this lane
+    const int row = pos / Gm::CH;
+    const int ch = (pos % Gm::CH) ^ (row % Gm::CH);
+    return (row * D + ch * 8) * (int)sizeof(uint16_t);
+  }
+  static constexpr int kOffRegs = Gm::NDMA < 4 ? Gm::NDMA : 4;
+
   // tile j into its slot; rows past the segment end re-read its last key
   __device__ __forceinline__ void issue(int j) const {
     const int t0 = tile_key(j);
     uint16_t* dst = ring + (j & (S - 1)) * Gm::TE;
+    if (t0 + kTileKeys <= k1) {
+      // a whole tile: a wave-uniform base and per-lane offsets that do not change from tile to
+      // tile (aux 2: non-temporal, the keys are read once per pass)
+      const char* base = reinterpret_cast<const char*>(kg + (size_t)t0 * D);
+      int off[kOffRegs];
 #pragma unroll
-    for (int i = 0; i < Gm::NDMA; ++i) {
-      const int pos = 64 * i + lane;  // LDS chunk slot written by this lane
-      const int row = pos / Gm::CH;
-      const int ch = (pos % Gm::CH) ^ (row % Gm::CH);
-      const uint16_t* src = kg + (size_t)min(t0 + row, k1 - 1) * D + ch * 8;
-      // aux 2: non-temporal (the keys are read once per pass)
-      __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)(dst + i * 512), 16, 0, 2);
+      for (int i = 0; i < kOffRegs; ++i) off[i] = chunk_off(i, lane);
+#pragma unroll
+      for (int i = 0; i < Gm::NDMA; ++i)
+        __builtin_amdgcn_global_load_lds((gptr_t)(base + (i / 4) * 4096 + off[i % 4]),
+                                         (lptr_t)(dst + i * 512), 16, 0, 2);
+    } else {
+#pragma unroll
+      for (int i = 0; i < Gm::NDMA; ++i) {
+        const int pos = 64 * i + lane;
+        const int row = pos / Gm::CH;
+        const int ch = (pos % Gm::CH) ^ (row % Gm::CH);
+        const uint16_t* src = kg + (size_t)min(t0 + row, k1 - 1) * D + ch * 8;
+        __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)(dst + i * 512), 16, 0, 2);
+      }
     }
   }
 

@@ -157,10 +157,12 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   constexpr int kTilesPerThread = kPruneMaxTiles / NT;
   static_assert(kPruneMaxTiles % NT == 0, "whole tiles per thread");
   static_assert(NT % kTileKeys == 0, "whole tiles per visit");
-  static_assert(sizeof(uint16_t) * NW * S * Gm::TE >= 4 * kBitmapWords + 8 * kRankDirect,
-                "the bitmap and the ranked group fit the ring");
+  static_assert(2 * kOrderBins >= kBitmapWords + 2 * kRankDirect,
+                "the bitmap and the ranked group fit the order's bins");
   static_assert(kPruneBins >= kBitmapWords, "the word prefixes fit the histogram");
-  __shared__ __align__(16) uint16_t ring[NW][S * Gm::TE];
+  // the waves' key rings; after the second pass, the order keys of the evaluated scores
+  constexpr int kRingElems = NW * S * Gm::TE > 2 * kCandMaxLen ? NW * S * Gm::TE : 2 * kCandMaxLen;
+  __shared__ __align__(16) uint16_t ring[kRingElems];
   // the waves' statistics after pass 1, the histogram of evaluated scores in pass 2
   __shared__ __align__(16) uint32_t red_hist[kRedWords > kPruneBins ? kRedWords : kPruneBins];
   __shared__ __align__(16) float bsh[R];
@@ -187,7 +189,7 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   uint32_t* codes_u = a.codes + ((size_t)p * a.h_kv + g) * a.code_stride;
 
   const uint16_t* kg = a.k + stat_base * D;
-  KeyStream<D, NB, NW, S> ks{ring[wave], kg, 0, L, wave, lane};
+  KeyStream<D, NB, NW, S> ks{ring + wave * S * Gm::TE, kg, 0, L, wave, lane};
   const int n_tiles = (L + kTileKeys - 1) / kTileKeys;
   const int my_tiles = n_tiles > wave ? (n_tiles - wave + NW - 1) / NW : 0;
   bf16x8_t q[NB][NS];
@@ -292,14 +294,14 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
                             : bmax * __builtin_amdgcn_exp2f(-(float)(bin[u] - 1) * (1.f / kBinsPerOctave));
     }
   }
-  __syncthreads();  // the order is complete; the lists and the ring are free
+  __syncthreads();  // the order is complete; the ring is free
 
   // ---- pass 2: exact scores of the wanted tiles, stored over their codes
   const int n_ord = (int)n_eval;
   const int bp = a.budgets ? a.budgets[p] : a.budget;
   const int C = min(a.cand_mult * bp, n_cand);
   const int my_tiles2 = n_ord > wave ? (n_ord - wave + NW - 1) / NW : 0;
-  KeyStream<D, NB, NW, S> ks2{ring[wave], kg, 0, L, wave, lane, order};
+  KeyStream<D, NB, NW, S> ks2{ring + wave * S * Gm::TE, kg, 0, L, wave, lane, order};
   ks2.prologue(my_tiles2);
   float* score_u = reinterpret_cast<float*>(codes_u);  // a tile's codes are dead once bounded
   // the cut's scan starts at the bin of the largest finite bound: scores above it (in tiles with a
@@ -330,19 +332,28 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
 #pragma unroll
   for (int w = 0; w < NW; ++w) max_ev = max(max_ev, (int)ev[w]);
   const int n_pos = min(n_ord, max_ev * NW);  // order positions at or after this one: not evaluated
-  // visit every evaluated key once: fn(entry) for keys of the candidate range
+  // the order keys of the evaluated scores, copied once into the ring (free after the pass) at
+  // [order position][key in tile]; the passes below visit them there
+  uint32_t* okc = reinterpret_cast<uint32_t*>(ring);
+  for (int p0 = 0; p0 < n_pos; p0 += NT / kTileKeys) {
+    const int pos = p0 + tid / kTileKeys;
+    if (pos < n_pos && (pos / NW) < (int)ev[pos % NW]) {
+      const int key = (int)order[pos] * kTileKeys + (tid % kTileKeys);
+      // device-coherent load: the line may still sit in this CU's vector cache with the tile's
+      // codes, read before the score was stored over them
+      if (key < n_cand)
+        okc[pos * kTileKeys + tid % kTileKeys] = order_key(__uint_as_float(__hip_atomic_load(
+            reinterpret_cast<uint32_t*>(score_u + key), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)));
+    }
+  }
+  __syncthreads();
+  // visit every evaluated key of the candidate range once: fn(entry, key)
   auto for_each_entry = [&](auto fn) __attribute__((always_inline)) {
     for (int p0 = 0; p0 < n_pos; p0 += NT / kTileKeys) {
       const int pos = p0 + tid / kTileKeys;
       if (pos < n_pos && (pos / NW) < (int)ev[pos % NW]) {
         const int key = (int)order[pos] * kTileKeys + (tid % kTileKeys);
-        if (key < n_cand) {
-          // device-coherent load: the line may still sit in this CU's vector cache with the
-          // tile's codes, read before the score was stored over them
-          const float sc = __uint_as_float(__hip_atomic_load(
-              reinterpret_cast<uint32_t*>(score_u + key), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-          fn(cand_entry(order_key(sc), (uint32_t)key), key);
-        }
+        if (key < n_cand) fn(cand_entry(okc[pos * kTileKeys + tid % kTileKeys], (uint32_t)key), key);
       }
     }
   };
@@ -370,7 +381,7 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   }
   // the group: at most kRankDirect entries (or one, once every digit is found); its need-th
   // largest entry is the C-th largest overall, found by counting the larger ones
-  uint64_t* gb = reinterpret_cast<uint64_t*>(&ring[0][0]) + kBitmapWords / 2;
+  uint64_t* gb = reinterpret_cast<uint64_t*>(bins + kBitmapWords);
   if (tid == 0) {
     n_eval = 0u;
     cut_entry = ~0ull;
@@ -389,7 +400,7 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
     if (larger == need - 1) cut_entry = e;
   }
   // the candidates (the entries >= the C-th largest) in a bitmap over the positions
-  uint32_t* bm = reinterpret_cast<uint32_t*>(&ring[0][0]);
+  uint32_t* bm = bins;
   const int n_words = (n_cand + 31) >> 5;
   for (int i = tid; i < n_words; i += NT) bm[i] = 0u;
   __syncthreads();
