@@ -2,10 +2,10 @@
 
 A step is the full hot path over every layer of the workload: window row statistics, per-token
 mean/dispersion and base score, the candidate cut, greedy selection and cache compaction, with
-every input already resident in HBM.  The timed pass is kv_window_candidates (the row statistics
-and each unit's candidate set from one launch that reads the keys once in full and revisits only
-the tiles whose score bound reaches the candidate cut) followed by kv_mmr_select_candidates (the
-greedy and the compaction in one launch).  Default workload: 32 layers of a Mistral-7B-shaped
+every input already resident in HBM.  The timed pass is kv_evict_pass: one launch in which each
+(layer, kv head) unit's workgroup forms the row statistics and the unit's candidate set (reading
+the keys once in full and revisiting only the tiles whose score bound reaches the candidate cut),
+then runs the greedy on the candidates and compacts the kept rows.  Default workload: 32 layers of a Mistral-7B-shaped
 cache (32 query / 8 kv heads, d=128, bf16), L=32768, W=32, B=64, quadratic lambda2 depth profile.
 
 Before every timed step a 512 MiB buffer is read (outside the timed region) so that no part of
@@ -14,8 +14,9 @@ events on the launch stream, per entry point and in total.  Further timed loops 
 inputs, the other scoring routes (base scores through HBM; mu and sigma through HBM; the two
 streaming passes as separate launches, so that each kernel's duration is measured live), the
 selection options, a decode step, and the per-layer schedule (the scoring launched once per
-layer, then one batched selection and compaction).  The roofline entry describes the scoring
-kernel of the timed pass (the dominant kernel).  One JSON line is printed.
+layer, then one batched selection and compaction).  The roofline entry describes the kernel of
+the timed pass (the dominant kernel; with the evict path the only one).  One JSON line is
+printed.
 """
 from __future__ import annotations
 
@@ -33,7 +34,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, published
-PATHS = ("candidates", "scored", "mu_sigma", "unfused")
+PATHS = ("evict", "candidates", "scored", "mu_sigma", "unfused")
 WORKLOADS = ("mistral32_L32768_W32_B64", "mistral32_L8192_W32_B64", "mistral_layer_L4096_W32_B64")
 
 
@@ -84,7 +85,8 @@ def mfma_flops(wl) -> float:
 
 # sources that define each profiled kernel: its traffic record stays valid while they are unchanged
 KERNEL_SOURCES = {
-    "window_prune": ("stream_prune.hip", "stream_passes.h", "stream_common.h", "common.h"),
+    "window_prune": ("stream_prune.hip", "select_gram.h", "compact_rows.h", "stream_passes.h",
+                     "stream_common.h", "common.h"),
     "window_stream": ("stream_window.hip", "stream_passes.h", "stream_common.h", "common.h"),
     "stats_stream": ("stream_stats.hip", "stream_passes.h", "stream_common.h", "common.h"),
     "mu_sigma_stream": ("stream_mu_sigma.hip", "stream_passes.h", "stream_common.h", "common.h"),
@@ -197,11 +199,17 @@ def copy_probe(torch, mib: int) -> None:
     print(json.dumps({"copy_probe_bytes": n, "launches": 3}), flush=True)
 
 
+def per_mean_of(events, n):
+    """Mean ms between consecutive events of each recorded step."""
+    return np.array([[e[i].elapsed_time(e[i + 1]) for i in range(n)] for e in events]).mean(axis=0)
+
+
 def config_passes(torch, args) -> None:
     """One JSON line per workload of the other configurations: the same batched pass
-    (kv_window_candidates, then kv_mmr_select_candidates with the compaction), timed the same way
-    (cache read-flushed before every step, HIP events), with its algorithmic bytes per second, and
-    the scored route (kv_window_base_scores, kv_mmr_select_scored) beside it.  The ragged batch's
+    (kv_evict_pass with the compaction), timed the same way (cache read-flushed before every step,
+    HIP events), with its algorithmic bytes per second, and beside it the two calls it stands for
+    (kv_window_candidates, then kv_mmr_select_candidates) and the scored route
+    (kv_window_base_scores, kv_mmr_select_scored).  The ragged batch's
     three coefficient runs differ in lambda1 as well, so each is a pass of its own."""
     from paper_2609_30738_amd import _lib, api, workloads as W
     flush_buf = torch.ones(128 << 20, dtype=torch.float32, device="cuda")
@@ -220,6 +228,11 @@ def config_passes(torch, args) -> None:
         wcb = _lib.candidates_workspace_bytes(b, wl.budget, 4, wl.w)
         ws_c = torch.empty(wcb, dtype=torch.uint8, device="cuda")
 
+        def evict():
+            _lib.evict_pass(b, inp.q_win, inp.k, inp.v, inp.scale, inp.lambda1, inp.lambda2,
+                            wl.budget, 4, wl.w, out.row_max, out.row_sum, out.sel_idx, ws_c,
+                            k_out=out.k_out, v_out=out.v_out)
+
         def cand():
             _lib.window_candidates(b, inp.q_win, inp.k, inp.scale, inp.lambda1, wl.budget, 4,
                                    wl.w, out.row_max, out.row_sum, ws_c)
@@ -236,43 +249,38 @@ def config_passes(torch, args) -> None:
             _lib.mmr_select_scored(b, score, inp.k, inp.v, inp.lambda2, wl.budget, 4, wl.w,
                                    out.sel_idx, k_out=out.k_out, v_out=out.v_out)
         res = []
-        for calls in ((cand, cand_sel), (scored, scored_sel)):
+        for calls in ((evict,), (cand, cand_sel), (scored, scored_sel)):
             rows = []
             for it in range(args.warmup + args.steps):
                 flush_buf.amax()
-                evs = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+                evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
                 evs[0].record(stream)
-                calls[0]()
-                evs[1].record(stream)
-                calls[1]()
-                evs[2].record(stream)
+                for i, fn in enumerate(calls):
+                    fn()
+                    evs[i + 1].record(stream)
                 if it >= args.warmup:
                     rows.append(evs)
             torch.cuda.synchronize()
-            res.append(np.array([[e[i].elapsed_time(e[i + 1]) for i in range(2)]
-                                 for e in rows]).mean(axis=0))
-        return res[0], float(res[1].sum()), algorithmic_bytes(wl)
+            res.append(per_mean_of(rows, len(calls)))
+        return float(res[0][0]), res[1], float(res[2].sum()), algorithmic_bytes(wl)
+
+    def entry(ms, two, scored_ms, ab):
+        return {"ms_per_pass": round(ms, 4), "GBps": round(ab["total"] / (ms * 1e-3) / 1e9, 1),
+                "two_calls_ms": {"kv_window_candidates": round(float(two[0]), 4),
+                                 "kv_mmr_select_candidates (compacting)": round(float(two[1]), 4),
+                                 "total": round(float(two.sum()), 4)},
+                "scored_route_ms": round(scored_ms, 4)}
 
     for wl in cases:
         packed = W.draw_packed(wl)
-        parts, scored_ms, ab = run(wl, packed)
-        ms = float(parts.sum())
-        print(json.dumps({"config": wl.name, "ms_per_pass": round(ms, 4),
-                          "scoring_ms": round(float(parts[0]), 4),
-                          "select_compact_ms": round(float(parts[1]), 4),
-                          "algorithmic_bytes": ab["total"],
-                          "GBps": round(ab["total"] / (ms * 1e-3) / 1e9, 1),
-                          "scored_route_ms": round(scored_ms, 4)}), flush=True)
+        ms, two, scored_ms, ab = run(wl, packed)
+        print(json.dumps({"config": wl.name, "algorithmic_bytes": ab["total"],
+                          **entry(ms, two, scored_ms, ab)}), flush=True)
     packed = W.draw_packed(ragged[0])  # the three runs share their inputs
     per_run = {}
     for wl in ragged:
-        parts, scored_ms, ab = run(wl, packed)
-        ms = float(parts.sum())
-        per_run[wl.name.rsplit("_B128_", 1)[-1]] = {
-            "ms_per_pass": round(ms, 4), "scoring_ms": round(float(parts[0]), 4),
-            "select_compact_ms": round(float(parts[1]), 4),
-            "GBps": round(ab["total"] / (ms * 1e-3) / 1e9, 1),
-            "scored_route_ms": round(scored_ms, 4)}
+        ms, two, scored_ms, ab = run(wl, packed)
+        per_run[wl.name.rsplit("_B128_", 1)[-1]] = entry(ms, two, scored_ms, ab)
     print(json.dumps({"config": ragged[0].name.replace("_dispersion_only", ""),
                       "total_tokens_per_layer": int(packed.lens.sum() // ragged[0].n_layers),
                       "algorithmic_bytes": ab["total"], "runs": per_run}), flush=True)
@@ -298,8 +306,8 @@ def main() -> None:
     ap.add_argument("--flush", choices=("read", "write"), default="read",
                     help="how the last-level cache is emptied before each timed step")
     ap.add_argument("--path", choices=PATHS, default=PATHS[0],
-                    help="the timed pass: candidates = kv_window_candidates + "
-                         "kv_mmr_select_candidates; scored = kv_window_base_scores + "
+                    help="the timed pass: evict = kv_evict_pass (one launch); candidates = "
+                         "kv_window_candidates + kv_mmr_select_candidates; scored = kv_window_base_scores + "
                          "kv_mmr_select_scored (base scores through HBM); mu_sigma = "
                          "kv_window_mu_sigma + kv_mmr_select_compact (mu and sigma through HBM); "
                          "unfused = kv_window_scores + kv_mu_sigma, then kv_mmr_select_compact")
@@ -358,7 +366,10 @@ def main() -> None:
     ws_sc = torch.empty(ws_sc_bytes, dtype=torch.uint8, device="cuda") if ws_sc_bytes else None
     mu_sigma_path = args.path in ("mu_sigma", "unfused")
 
-    names = ["scoring", "select + compact"]
+    def evict_pass():
+        _lib.evict_pass(b, inp.q_win, inp.k, inp.v, inp.scale, inp.lambda1, inp.lambda2,
+                        wl.budget, 4, wl.w, out.row_max, out.row_sum, out.sel_idx, ws_c,
+                        k_out=out.k_out, v_out=out.v_out)
 
     def cand_scoring():
         _lib.window_candidates(b, inp.q_win, inp.k, inp.scale, inp.lambda1, wl.budget, 4, wl.w,
@@ -388,24 +399,26 @@ def main() -> None:
         _lib.window_scores(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.ws)
         _lib.mu_sigma(b, inp.q_win, inp.k, inp.scale, out.row_max, out.row_sum, out.mu, out.sigma)
 
-    routes = {"candidates": (cand_scoring, cand_select,
-                             "kv_window_candidates", "kv_mmr_select_candidates (compacting)"),
-              "scored": (scored_scoring, scored_select,
-                         "kv_window_base_scores", "kv_mmr_select_scored (compacting)"),
-              "mu_sigma": (ms_scoring, ms_select, "kv_window_mu_sigma", "kv_mmr_select_compact"),
-              "unfused": (unfused_scoring, ms_select, "kv_window_scores + kv_mu_sigma",
-                          "kv_mmr_select_compact")}
-    run_scoring, run_select, scoring_name, select_name = routes[args.path]
+    # each route: its entry points in order, (name, call); the breakdown times each call
+    routes = {"evict": [("kv_evict_pass (compacting)", evict_pass)],
+              "candidates": [("kv_window_candidates", cand_scoring),
+                             ("kv_mmr_select_candidates (compacting)", cand_select)],
+              "scored": [("kv_window_base_scores", scored_scoring),
+                         ("kv_mmr_select_scored (compacting)", scored_select)],
+              "mu_sigma": [("kv_window_mu_sigma", ms_scoring), ("kv_mmr_select_compact", ms_select)],
+              "unfused": [("kv_window_scores + kv_mu_sigma", unfused_scoring),
+                          ("kv_mmr_select_compact", ms_select)]}
+    calls = routes[args.path]
+    names = [n for n, _ in calls]
 
     def step(evs):
         evs[0].record(stream)
-        run_scoring()
-        evs[1].record(stream)
-        run_select()
-        evs[2].record(stream)
+        for i, (_, fn) in enumerate(calls):
+            fn()
+            evs[i + 1].record(stream)
 
     def new_events():
-        return [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        return [torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
 
     # optional settle phase (off by default): from idle the engine clock ramps up over the first
     # 20-30 passes (a fixed bf16 GEMM between passes runs ~17 % faster after them), while a few
@@ -457,12 +470,14 @@ def main() -> None:
 
     # the other routes on the same inputs (the unfused one is covered by the per-kernel loop)
     other_routes = {}
-    for name in ("candidates", "scored", "mu_sigma"):
+    for name in ("evict", "candidates", "scored", "mu_sigma"):
         if name != args.path:
-            f_sc, f_sel, n_sc, n_sel = routes[name]
-            t_sc, t_sel = timed(f_sc, f_sel)
-            other_routes[name] = {n_sc: round(t_sc, 4), n_sel: round(t_sel, 4),
-                                  "total": round(t_sc + t_sel, 4)}
+            t = timed(*[fn for _, fn in routes[name]])
+            other_routes[name] = {n: round(x, 4) for (n, _), x in zip(routes[name], t)}
+            other_routes[name]["total"] = round(sum(t), 4)
+    # the candidates route's two launches, from the timed pass or from the loop above
+    cand_ms = (list(per_mean_of(all_events, len(calls))) if args.path == "candidates"
+               else [other_routes["candidates"][n] for n, _ in routes["candidates"]])
 
     # per kernel: the two scoring passes through their own entry points, events between them
     # (warm-up first: a kernel's first launch also loads its code); with one segment per unit,
@@ -564,27 +579,29 @@ def main() -> None:
     lay = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(2)] for e in layer_events])
     lay_score, lay_rest = (float(x) for x in lay.mean(axis=0))
 
-    per = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(2)] for e in all_events])
+    per = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(len(calls))] for e in all_events])
     step_ms = per.sum(axis=1)
     ms = float(step_ms.mean())
     mean_part = per.mean(axis=0)
     ab = algorithmic_bytes(wl)
     flops = mfma_flops(wl)
-    # The dominant kernel is the scoring kernel of the timed pass (kv_window_base_scores with every
-    # unit one segment: both passes of a unit in one workgroup, the base scores formed in the
-    # second).  What the method must move for it is K and Q_W once; its second read of K and its
-    # outputs (row statistics and base scores) are overhead of the design, and show in
-    # `traffic`.  roofline_passes gives the same view of the two passes run as separate launches.
+    # The dominant kernel is the first kernel of the timed pass: with the evict path the one launch
+    # of window_prune_kernel that scores, cuts, selects and compacts (what the method must move
+    # for it: K and Q_W once, the kept rows of K and V read and written, the indices), otherwise
+    # the scoring kernel (K and Q_W once).  Its revisits of K and its workspace traffic are
+    # overhead of the design and show in `traffic`.  roofline_passes gives the same view of the two
+    # streaming passes run as separate launches.
     def roofline(kernel, alg, kms):
         achieved = alg / (kms * 1e-3) / 1e9
         return {"kernel": kernel, "bound": "hbm", "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": measured_traffic(kernel, wl.name),
                 "algorithmic_bytes_per_launch": alg, "ms_per_launch": round(kms, 4)}
-    dominant_kernel = {"candidates": "window_prune", "scored": "window_stream",
-                       "mu_sigma": "window_stream",
+    dominant_kernel = {"evict": "window_prune", "candidates": "window_prune",
+                       "scored": "window_stream", "mu_sigma": "window_stream",
                        "unfused": "stats_stream+mu_sigma_stream"}[args.path]
-    dominant = roofline(dominant_kernel, ab["scoring"], float(mean_part[0]))
+    dominant = roofline(dominant_kernel, ab["total"] if args.path == "evict" else ab["scoring"],
+                        float(mean_part[0]))
     passes = [roofline("stats_stream", ab["scoring"], k_stats),
               roofline("mu_sigma_stream", ab["scoring"], k_mu)]
     line = {
@@ -613,17 +630,18 @@ def main() -> None:
         "wall_s_timed_loop": round(wall, 3),
         "cache_flush": f"{args.flush} of 512 MiB before every timed step",
         "settle": {"passes": settle_passes, "ms": round(settle_ms, 1)},
-        "pass": f"{scoring_name}, {select_name}",
+        "pass": ", ".join(names),
         "other_routes_ms": other_routes,
         "per_layer_schedule_ms": {"total": round(lay_score + lay_rest, 4),
                                   ("scoring (32 launches of kv_window_mu_sigma)" if mu_sigma_path
                                    else "scoring (32 launches of kv_window_base_scores)"):
                                   round(lay_score, 4),
                                   "select+compact (batched)": round(lay_rest, 4)},
-        "per_kernel_ms": {f"{dominant_kernel} ({scoring_name})": round(float(mean_part[0]), 4),
+        "per_kernel_ms": {f"{dominant_kernel} ({names[0]})": round(float(mean_part[0]), 4),
+                          "window_prune (kv_window_candidates)": round(cand_ms[0], 4),
                           "stats_stream (kv_window_scores)": round(k_stats, 4),
                           "mu_sigma_stream (kv_mu_sigma)": round(k_mu, 4),
-                          f"mmr_select ({select_name})": round(float(mean_part[1]), 4),
+                          "mmr_select (kv_mmr_select_candidates (compacting))": round(cand_ms[1], 4),
                           "mmr_select (kv_mmr_select)": round(k_sel, 4),
                           "compact (kv_compact_cache)": round(k_cmp, 4)},
         "options_ms": {"kv_window_mu_sigma_ex (sigma over all G*W rows)": round(v_all, 4),

@@ -316,6 +316,23 @@ int kv_mmr_select_candidates(const kv_problem* pr, const void* ws, size_t ws_byt
                              int32_t* sel_idx, float* sel_score, int32_t* cand_idx,
                              float* cand_corr, void* k_out, void* v_out, void* stream);
 
+/* The whole eviction pass of a batch in one call (sections 3.1 and 3.2, Eq. (1)-(5)): exactly
+ * kv_window_candidates followed by kv_mmr_select_candidates on the same workspace with the same
+ * budget, cand_mult, keep_tail and opts (cand_idx / cand_corr not offered): row_max, row_sum,
+ * sel_idx, sel_score (nullable) and, with k_out and v_out (both or neither; v then required), the
+ * compacted cache, bit for bit as the two calls give them, and the workspace (ws, ws_bytes >=
+ * kv_candidates_workspace_bytes) left holding the candidates.  Arguments, layouts, limits and
+ * error codes as in the two calls; nothing is launched when either would refuse its arguments.
+ * Where the window kernel cuts the candidates (bf16, L_p <= 32768, see kv_window_candidates) and
+ * every C_p = min(cand_mult * B_p, n_cand) <= 256, each (problem, kv head) unit's workgroup runs
+ * the greedy and the compaction right after its cut, in the same launch; otherwise the two calls
+ * run in turn.  Calls that overlap on one workspace race. */
+int kv_evict_pass(const kv_problem* pr, const void* q_win, const void* k, const void* v,
+                  float scale, const float* lambda1, const float* lambda2, int32_t sigma_rows,
+                  int32_t budget, int32_t cand_mult, int32_t keep_tail, const kv_select_opts* opts,
+                  float* row_max, float* row_sum, int32_t* sel_idx, float* sel_score, void* k_out,
+                  void* v_out, void* ws, size_t ws_bytes, void* stream);
+
 /* kv_compact_cache with per-problem budgets and a chosen block size (budget_host / budget_dev as
  * in kv_select_opts; both NULL with out_rows = 0 is exactly kv_compact_cache).  The block of every
  * (problem, kv head) in k_out / v_out has out_rows rows (0: budget + keep_tail; otherwise at least

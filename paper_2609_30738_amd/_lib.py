@@ -46,7 +46,7 @@ SYMBOLS = ("kv_strerror", "kv_version", "kv_workspace_bytes", "kv_candidate_stri
            "kv_window_mu_sigma_ex", "kv_window_mu_sigma_noalloc", "kv_window_base_scores",
            "kv_base_scores_workspace_bytes", "kv_mmr_select", "kv_mmr_select_ex",
            "kv_mmr_select_compact", "kv_mmr_select_scored", "kv_window_candidates",
-           "kv_candidates_workspace_bytes", "kv_mmr_select_candidates",
+           "kv_candidates_workspace_bytes", "kv_mmr_select_candidates", "kv_evict_pass",
            "kv_compact_cache", "kv_compact_cache_ex", "kv_decode_workspace_bytes",
            "kv_decode_attention", "kv_pyramid_budgets", "kv_depth_profile")
 
@@ -117,6 +117,9 @@ def lib() -> ctypes.CDLL:
         h.kv_mmr_select_candidates.argtypes = [pr, vp, sz, vp, vp, vp, i32, i32, i32,
                                                ctypes.POINTER(KvSelectOpts), vp, vp, vp, vp, vp,
                                                vp, vp]
+        h.kv_evict_pass.argtypes = [pr, vp, vp, vp, ctypes.c_float, vp, vp, i32, i32, i32, i32,
+                                    ctypes.POINTER(KvSelectOpts), vp, vp, vp, vp, vp, vp, vp, sz,
+                                    vp]
         h.kv_mmr_select.argtypes = [pr, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, sz,
                                     vp]
         h.kv_mmr_select_compact.argtypes = [pr, vp, vp, vp, vp, vp, vp, i32, i32, i32, vp, vp, vp,
@@ -136,7 +139,7 @@ def lib() -> ctypes.CDLL:
                      "kv_window_mu_sigma_ex", "kv_window_mu_sigma_noalloc",
                      "kv_window_base_scores", "kv_mmr_select", "kv_mmr_select_ex",
                      "kv_mmr_select_scored", "kv_window_candidates", "kv_mmr_select_candidates",
-                     "kv_compact_cache", "kv_compact_cache_ex", "kv_decode_attention",
+                     "kv_evict_pass", "kv_compact_cache", "kv_compact_cache_ex", "kv_decode_attention",
                      "kv_pyramid_budgets", "kv_depth_profile"):
             getattr(h, name).restype = ctypes.c_int
         _LIB = h
@@ -363,6 +366,21 @@ def mmr_select_candidates(batch: Batch, ws, k, v, lambda2, budget: int, cand_mul
                                           _ptr(sel_score), _ptr(cand_idx), _ptr(cand_corr),
                                           _ptr(k_out), _ptr(v_out), _stream(stream)),
            "kv_mmr_select_candidates")
+
+
+def evict_pass(batch: Batch, q_win, k, v, scale: float, lambda1, lambda2, budget: int,
+               cand_mult: int, keep_tail: int, row_max, row_sum, sel_idx, ws, sel_score=None,
+               k_out=None, v_out=None, w_mu: Optional[float] = None,
+               budgets: Optional[Budgets] = None, sigma_rows="group_mean", stream=None) -> None:
+    """kv_evict_pass: window_candidates then mmr_select_candidates (with k_out / v_out the
+    compaction), in one launch where the window kernel cuts the candidates and C <= 256."""
+    _check(lib().kv_evict_pass(batch.ref(), _ptr(q_win), _ptr(k), _ptr(v), float(scale),
+                               _ptr(lambda1), _ptr(lambda2), _sigma_rows(sigma_rows), int(budget),
+                               int(cand_mult), int(keep_tail), _select_opts(None, w_mu, budgets),
+                               _ptr(row_max), _ptr(row_sum), _ptr(sel_idx), _ptr(sel_score),
+                               _ptr(k_out), _ptr(v_out), _ptr(ws),
+                               0 if ws is None else ws.numel() * ws.element_size(),
+                               _stream(stream)), "kv_evict_pass")
 
 
 def mmr_select(batch: Batch, mu, sigma, k, lambda1, lambda2, budget: int, cand_mult: int,

@@ -248,6 +248,66 @@ int mmr_select_impl(const kv_problem* pr, const ScoreSource& src, const void* k,
   return launch_status(kv::launch_mmr_select(s, a, static_cast<hipStream_t>(stream)));
 }
 
+// kv_window_candidates; with sel (the caller has checked that the window kernel cuts the
+// candidates, every C_p <= kCandSelectMax, and the selection's arguments) the selection of each
+// unit follows its cut in the same launch.
+int window_candidates_impl(const kv_problem* pr, const void* q_win, const void* k, float scale,
+                           const float* lambda1, int32_t sigma_rows, int32_t budget,
+                           int32_t cand_mult, int32_t keep_tail, const kv_select_opts* opts,
+                           float* row_max, float* row_sum, void* ws, size_t ws_bytes,
+                           const kv::CandSelect* sel, void* stream) {
+  kv::Shape s;
+  int st = check_problem(pr, &s);
+  if (st != KV_OK) return st;
+  if (!q_win || !k || !lambda1 || !row_max || !row_sum) return KV_ERR_NULL;
+  if (!aligned16(q_win) || !aligned16(k)) return KV_ERR_ARG;
+  if (!std::isfinite(scale)) return KV_ERR_ARG;
+  if (sigma_rows != KV_SIGMA_GROUP_MEAN && sigma_rows != KV_SIGMA_ALL_ROWS) return KV_ERR_ARG;
+  if (cand_mult < 0 || (int64_t)cand_mult * budget > INT32_MAX) return KV_ERR_ARG;
+  const int32_t pool = opts ? opts->pool : 1;
+  const float w_mu = opts ? opts->w_mu : 1.f;
+  const int32_t* b_host = opts ? opts->budget_host : nullptr;
+  const int32_t* b_dev = opts ? opts->budget_dev : nullptr;
+  if (pool != 1 || !std::isfinite(w_mu)) return KV_ERR_ARG;
+  st = check_budget(pr, budget, keep_tail, b_host != nullptr || b_dev != nullptr);
+  if (st != KV_OK) return st;
+  st = check_budgets(pr, budget, keep_tail, b_host, b_dev);
+  if (st != KV_OK) return st;
+  const int stride = max_candidates(pr, budget, cand_mult, keep_tail, b_host);
+  if (stride > kv::select_max_candidates(pr->d, elem_bytes(pr->dtype))) return KV_ERR_SHAPE;
+  const bool fused = cands_in_window_pass(pr, s, scale, cand_mult);
+  const size_t need = cand_ws_bytes(pr, s, stride, fused);
+  if (ws_bytes < need || !ws || (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1)))
+    return KV_ERR_WORKSPACE;
+  const bool all = sigma_rows == KV_SIGMA_ALL_ROWS;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  char* base = static_cast<char*>(ws);
+  const size_t n_units = (size_t)pr->n_prob * pr->h_kv;
+  uint64_t* lists = reinterpret_cast<uint64_t*>(base);
+  float* cmax = reinterpret_cast<float*>(base + cand_lists_bytes(pr, stride));
+  const size_t head = cand_lists_bytes(pr, stride) + align_up(n_units * sizeof(float));
+  if (fused)
+    return launch_status(kv::launch_stream_window_cands(
+        s, stream_plan_of(pr, s), q_win, k, scale, lambda1, w_mu, budget, b_dev, cand_mult,
+        keep_tail, row_max, row_sum, lists, cmax, stride, reinterpret_cast<uint32_t*>(base + head),
+        all, sel, hs));
+  if (sel) return KV_ERR_ARG;  // the selection follows the cut only in the window kernel
+  // the scores into the workspace, then the candidate cut of the selection kernel
+  float* score = reinterpret_cast<float*>(base + head);
+  const size_t score_bytes = align_up((size_t)token_extent(pr) * pr->h_kv * sizeof(float));
+  st = kv_window_base_scores(pr, q_win, k, scale, lambda1, w_mu, sigma_rows, row_max, row_sum,
+                             score, base + head + score_bytes, ws_bytes - head - score_bytes,
+                             stream);
+  if (st != KV_OK) return st;
+  ScoreSource src;
+  src.score = score;
+  src.cut_out = lists;
+  src.cut_max = cmax;
+  src.list_stride = stride;
+  return mmr_select_impl(pr, src, k, nullptr, nullptr, budget, cand_mult, keep_tail, opts, nullptr,
+                         nullptr, nullptr, nullptr, nullptr, nullptr, stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -520,55 +580,8 @@ int kv_window_candidates(const kv_problem* pr, const void* q_win, const void* k,
                          const float* lambda1, int32_t sigma_rows, int32_t budget,
                          int32_t cand_mult, int32_t keep_tail, const kv_select_opts* opts,
                          float* row_max, float* row_sum, void* ws, size_t ws_bytes, void* stream) {
-  kv::Shape s;
-  int st = check_problem(pr, &s);
-  if (st != KV_OK) return st;
-  if (!q_win || !k || !lambda1 || !row_max || !row_sum) return KV_ERR_NULL;
-  if (!aligned16(q_win) || !aligned16(k)) return KV_ERR_ARG;
-  if (!std::isfinite(scale)) return KV_ERR_ARG;
-  if (sigma_rows != KV_SIGMA_GROUP_MEAN && sigma_rows != KV_SIGMA_ALL_ROWS) return KV_ERR_ARG;
-  if (cand_mult < 0 || (int64_t)cand_mult * budget > INT32_MAX) return KV_ERR_ARG;
-  const int32_t pool = opts ? opts->pool : 1;
-  const float w_mu = opts ? opts->w_mu : 1.f;
-  const int32_t* b_host = opts ? opts->budget_host : nullptr;
-  const int32_t* b_dev = opts ? opts->budget_dev : nullptr;
-  if (pool != 1 || !std::isfinite(w_mu)) return KV_ERR_ARG;
-  st = check_budget(pr, budget, keep_tail, b_host != nullptr || b_dev != nullptr);
-  if (st != KV_OK) return st;
-  st = check_budgets(pr, budget, keep_tail, b_host, b_dev);
-  if (st != KV_OK) return st;
-  const int stride = max_candidates(pr, budget, cand_mult, keep_tail, b_host);
-  if (stride > kv::select_max_candidates(pr->d, elem_bytes(pr->dtype))) return KV_ERR_SHAPE;
-  const bool fused = cands_in_window_pass(pr, s, scale, cand_mult);
-  const size_t need = cand_ws_bytes(pr, s, stride, fused);
-  if (ws_bytes < need || !ws || (reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1)))
-    return KV_ERR_WORKSPACE;
-  const bool all = sigma_rows == KV_SIGMA_ALL_ROWS;
-  hipStream_t hs = static_cast<hipStream_t>(stream);
-  char* base = static_cast<char*>(ws);
-  const size_t n_units = (size_t)pr->n_prob * pr->h_kv;
-  uint64_t* lists = reinterpret_cast<uint64_t*>(base);
-  float* cmax = reinterpret_cast<float*>(base + cand_lists_bytes(pr, stride));
-  const size_t head = cand_lists_bytes(pr, stride) + align_up(n_units * sizeof(float));
-  if (fused)
-    return launch_status(kv::launch_stream_window_cands(
-        s, stream_plan_of(pr, s), q_win, k, scale, lambda1, w_mu, budget, b_dev, cand_mult,
-        keep_tail, row_max, row_sum, lists, cmax, stride, reinterpret_cast<uint32_t*>(base + head),
-        all, hs));
-  // the scores into the workspace, then the candidate cut of the selection kernel
-  float* score = reinterpret_cast<float*>(base + head);
-  const size_t score_bytes = align_up((size_t)token_extent(pr) * pr->h_kv * sizeof(float));
-  st = kv_window_base_scores(pr, q_win, k, scale, lambda1, w_mu, sigma_rows, row_max, row_sum,
-                             score, base + head + score_bytes, ws_bytes - head - score_bytes,
-                             stream);
-  if (st != KV_OK) return st;
-  ScoreSource src;
-  src.score = score;
-  src.cut_out = lists;
-  src.cut_max = cmax;
-  src.list_stride = stride;
-  return mmr_select_impl(pr, src, k, nullptr, nullptr, budget, cand_mult, keep_tail, opts, nullptr,
-                         nullptr, nullptr, nullptr, nullptr, nullptr, stream);
+  return window_candidates_impl(pr, q_win, k, scale, lambda1, sigma_rows, budget, cand_mult,
+                                keep_tail, opts, row_max, row_sum, ws, ws_bytes, nullptr, stream);
 }
 
 int kv_mmr_select_candidates(const kv_problem* pr, const void* ws, size_t ws_bytes, const void* k,
@@ -596,6 +609,39 @@ int kv_mmr_select_candidates(const kv_problem* pr, const void* ws, size_t ws_byt
   src.list_stride = stride;
   return mmr_select_impl(pr, src, k, v, lambda2, budget, cand_mult, keep_tail, opts, sel_idx,
                          sel_score, cand_idx, cand_corr, k_out, v_out, stream);
+}
+
+int kv_evict_pass(const kv_problem* pr, const void* q_win, const void* k, const void* v,
+                  float scale, const float* lambda1, const float* lambda2, int32_t sigma_rows,
+                  int32_t budget, int32_t cand_mult, int32_t keep_tail, const kv_select_opts* opts,
+                  float* row_max, float* row_sum, int32_t* sel_idx, float* sel_score, void* k_out,
+                  void* v_out, void* ws, size_t ws_bytes, void* stream) {
+  kv::Shape s;
+  int st = check_problem(pr, &s);
+  if (st != KV_OK) return st;
+  // the selection's own checks first: nothing runs unless both calls would
+  if (!lambda2 || !sel_idx) return KV_ERR_NULL;
+  if ((k_out != nullptr) != (v_out != nullptr)) return KV_ERR_NULL;
+  if (k_out && !v) return KV_ERR_NULL;
+  if (k_out && (!aligned16(v) || !aligned16(k_out) || !aligned16(v_out))) return KV_ERR_ARG;
+  if (k_out && budget > kMaxCompactBudget) return KV_ERR_BUDGET;
+  if (cand_mult < 0 || (int64_t)cand_mult * budget > INT32_MAX) return KV_ERR_ARG;
+  const int32_t* b_host = opts ? opts->budget_host : nullptr;
+  const int32_t* b_dev = opts ? opts->budget_dev : nullptr;
+  st = check_budget(pr, budget, keep_tail, b_host != nullptr || b_dev != nullptr);
+  if (st != KV_OK) return st;
+  const int stride = max_candidates(pr, budget, cand_mult, keep_tail, b_host);
+  if (pr->dtype == KV_BF16 && cands_in_window_pass(pr, s, scale, cand_mult) &&
+      stride <= kv::kCandSelectMax) {
+    kv::CandSelect sel{lambda2, sel_idx, sel_score, v, k_out, v_out, budget + keep_tail};
+    return window_candidates_impl(pr, q_win, k, scale, lambda1, sigma_rows, budget, cand_mult,
+                                  keep_tail, opts, row_max, row_sum, ws, ws_bytes, &sel, stream);
+  }
+  st = kv_window_candidates(pr, q_win, k, scale, lambda1, sigma_rows, budget, cand_mult,
+                            keep_tail, opts, row_max, row_sum, ws, ws_bytes, stream);
+  if (st != KV_OK) return st;
+  return kv_mmr_select_candidates(pr, ws, ws_bytes, k, v, lambda2, budget, cand_mult, keep_tail,
+                                  opts, sel_idx, sel_score, nullptr, nullptr, k_out, v_out, stream);
 }
 
 int kv_compact_cache(const kv_problem* pr, const void* k, const void* v, const int32_t* sel_idx,

@@ -80,14 +80,29 @@ hipError_t launch_stream_window_scores(const Shape& s, const StreamPlan& plan, c
 // keys are read once in full; the second pass revisits only the tiles whose score bound reaches
 // the unit's cut.  codes: scratch of n_units * cand_code_stride(s) words (the first pass's tile
 // codes, then the evaluated keys' scores).  Units of at most kCandMaxLen keys.
+// With sel, each unit's workgroup then runs the selection on its list (every C_p <= 256, bf16): the
+// greedy of the selection kernel's Gram path, with sel_idx / sel_score ([n_prob][h_kv][budget],
+// sel_score nullable) and, with k_out, the compaction (k_out / v_out [n_prob][h_kv][out_rows][D],
+// both or neither, v required) as the selection kernel writes them from the same list.
 constexpr int kCandMaxLen = 32768;
+constexpr int kCandSelectMax = 256;  // candidates per unit of the selection in the window launch
+struct CandSelect {
+  const float* lambda2;
+  int32_t* sel_idx;
+  float* sel_score;
+  const void* v;
+  void* k_out;
+  void* v_out;
+  int out_rows;
+};
 int cand_code_stride(const Shape& s);
 hipError_t launch_stream_window_cands(const Shape& s, const StreamPlan& plan, const void* q_win,
                                       const void* k, float scale, const float* lambda1, float w_mu,
                                       int budget, const int32_t* budgets, int cand_mult,
                                       int keep_tail, float* row_max, float* row_sum,
                                       uint64_t* cand_out, float* cand_max, int cand_stride,
-                                      uint32_t* codes, bool sigma_all, hipStream_t stream);
+                                      uint32_t* codes, bool sigma_all, const CandSelect* sel,
+                                      hipStream_t stream);
 // Base scores s = fma(lambda1[p], sigma, w_mu mu) of every key from mu / sigma rows (for batches
 // that take the other window paths).
 hipError_t launch_base_scores(const Shape& s, const float* mu, const float* sigma,

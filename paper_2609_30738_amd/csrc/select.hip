@@ -12,13 +12,11 @@
 //      equal to it, compacted in ascending position order (ballot ranks inside a wave, LDS prefix
 //      across waves);
 //   3. B greedy steps, in one of two ways:
-//      - Gram (when the upper triangle of the C x C dot-product matrix of the candidate keys fits in
-//        LDS: C <= 256 for d = 128): the dot products k_i . k_j of every candidate pair are formed
-//        once with MFMA tiles (each wave a 32 x 32 block, operands gathered straight from the key
-//        rows) into the LDS triangle, 1/|k_i| from its diagonal; then ONE wave runs every step,
-//        each lane holding up to four candidates' s~, running max-cosine and admitted flag: a step
-//        reads one triangle entry per candidate against the last admitted slot and takes a DPP /
-//        permlane maximum, with no barrier;
+//      - Gram (bf16, C <= 256; select_gram.h): the candidates' key rows are staged in LDS, the
+//        cosines of every candidate pair formed once with MFMA tiles into a strict upper triangle
+//        in LDS; then ONE wave runs every step, each lane holding up to four candidates' s~ and
+//        running max-cosine: a step reads one triangle entry per candidate against the last
+//        admitted slot and takes a DPP / permlane maximum, with no barrier;
 //      - rows (larger C): thread t owns candidates t, t + NT, ... and keeps their keys in
 //        registers; each step updates the running maxima against the last admitted key (read from
 //        an LDS copy of the candidate keys), forms s~ + lambda2 * corr, and finds the (score,
@@ -31,6 +29,7 @@
 #include "common.h"
 #include "compact_rows.h"
 #include "kernels.h"
+#include "select_gram.h"
 
 namespace kv {
 
@@ -39,14 +38,7 @@ namespace {
 constexpr int kMaxCandBytes = 131072;        // LDS copy of the candidate keys
 constexpr int kMaxStagedKeyBytes = 139264;  // LDS copy of every candidate's score key (34816)
 constexpr size_t kLdsBytes = 163840;        // LDS of one CU
-constexpr int kGramMaxCand = 256;           // candidates of the Gram greedy (4 per lane of a wave)
 constexpr int kMaxSlotWords = 64;           // bitmap words over the candidate slots (C <= 2048)
-constexpr int kGramSlots = kGramMaxCand / 64;
-
-// Entries of the upper triangle (diagonal included) of a C x C matrix, and the index of (i, j),
-// i <= j, row by row.
-__host__ __device__ constexpr size_t tri_entries(int c) { return (size_t)c * (c + 1) / 2; }
-__device__ __forceinline__ int tri_index(int i, int j, int c) { return (i * (2 * c - i + 1)) / 2 + (j - i); }
 
 // (score, slot) packed so that a larger value means a larger score, then a lower slot.
 __device__ __forceinline__ uint64_t pack_best(float score, int slot) {
@@ -669,8 +661,6 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
   int last = -1;
   if constexpr (GRAM) {
     static_assert(DT == kDtBf16, "the Gram greedy takes bf16 keys");
-    float* gram = reinterpret_cast<float*>(region);
-    const int l32 = lane & 31, half = lane >> 5;
     // s~ of every candidate (its base score, pooled as in phase 0, over the normaliser)
     for (int c = tid; c < C; c += kThreads) {
       const int pos = cpos[c];
@@ -684,139 +674,14 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
       }
       cst[c] = sv / den;
     }
-    // Dot products of every pair of candidate keys, k_i . k_j, in 32 x 32 blocks (I, J), I <= J
-    // (block b of a wave: b-th of wave, wave + NW, ...), accumulated over the head dimension 16
-    // elements at a time: each 16-element slice of every candidate row is staged in LDS (the radix
-    // histograms' space, two slices in turn) and feeds one MFMA step of every block.  Each thread
-    // loads its 16-byte piece of every slice up front, so the key rows cross the memory system once
-    // with all loads in flight.
-    constexpr int kSlices = D / 16, kMaxBlk = 3;
-    const int nb = (C + 31) / 32;
-    const int n_blocks = nb * (nb + 1) / 2;
-    static_assert(kWaves * kMaxBlk >= (kGramMaxCand / 32) * (kGramMaxCand / 32 + 1) / 2, "blocks");
-    uint16_t* slice = reinterpret_cast<uint16_t*>(&sh.hist[0][0]);  // [2][kGramMaxCand][16]
-    static_assert(sizeof(sh.hist) >= 2 * kGramMaxCand * 16 * sizeof(uint16_t), "slice buffers");
-    const int piece_row = tid >> 1, piece_half = tid & 1;  // thread's 8-element piece of a slice
-    const bool has_piece = piece_row < C;
-    bf16x8_t pieces[kSlices];
-    {
-      const uint16_t* src = kg + (size_t)cpos[has_piece ? piece_row : 0] * D + 8 * piece_half;
-#pragma unroll
-      for (int sl = 0; sl < kSlices; ++sl)
-        pieces[sl] = *reinterpret_cast<const bf16x8_t*>(src + 16 * sl);
-      // |k|^2 of the row: this thread's half, then the other half from the neighbouring lane
-      typedef __bf16 __attribute__((ext_vector_type(2))) bf2;
-      float n2 = 0.f;
-#pragma unroll
-      for (int sl = 0; sl < kSlices; ++sl) {
-        const auto w = __builtin_bit_cast(uint4, pieces[sl]);
-        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          n2 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf2, ws[u]), __builtin_bit_cast(bf2, ws[u]), n2, false);
-      }
-      n2 += __shfl_xor(n2, 1, 64);
-      if (has_piece && piece_half == 0) cinv[piece_row] = n2 > 0.f ? 1.f / sqrtf(n2) : 0.f;
-    }
-    int blk_i[kMaxBlk], blk_j[kMaxBlk];
-#pragma unroll
-    for (int u = 0; u < kMaxBlk; ++u) {
-      int I = 0, rem = wave + u * kWaves;
-      while (I < nb && rem >= nb - I) {
-        rem -= nb - I;
-        ++I;
-      }
-      blk_i[u] = I;  // I == nb: no block
-      blk_j[u] = I + rem;
-    }
-    f32x16_t acc[kMaxBlk];
-#pragma unroll
-    for (int u = 0; u < kMaxBlk; ++u)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[u][r] = 0.f;
-#pragma unroll
-    for (int sl = 0; sl < kSlices; ++sl) {
-      uint16_t* buf = slice + (sl & 1) * kGramMaxCand * 16;
-      if (has_piece)
-        *reinterpret_cast<bf16x8_t*>(buf + piece_row * 16 + 8 * piece_half) = pieces[sl];
-      __syncthreads();
-#pragma unroll
-      for (int u = 0; u < kMaxBlk; ++u) {
-        if (blk_i[u] < nb) {
-          const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(
-              buf + min(32 * blk_i[u] + l32, C - 1) * 16 + 8 * half);
-          const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(
-              buf + min(32 * blk_j[u] + l32, C - 1) * 16 + 8 * half);
-          acc[u] = mfma_step(a, b, acc[u]);
-        }
-      }
-      // the other buffer is written next: its readers (slice sl - 1) are done, the barrier above
-    }
-    // the triangle holds the cosines (k_i . k_j / |k_i|) / |k_j|, i <= j (a zero key has 1 / |k| = 0,
-    // hence cosine 0 to everything; a non-finite product counts as cosine 0)
-#pragma unroll
-    for (int u = 0; u < kMaxBlk; ++u) {
-      if (blk_i[u] < nb) {
-        const int j = 32 * blk_j[u] + l32;
-        const float inv_j = cinv[min(j, C - 1)];
-#pragma unroll
-        for (int jj = 0; jj < 16; ++jj) {
-          const int i = 32 * blk_i[u] + acc_row(jj, lane);
-          if (i < C && j < C && i <= j) {
-            const float cs = acc[u][jj] * cinv[i] * inv_j;
-            gram[tri_index(i, j, C)] = __builtin_isfinite(cs) ? cs : 0.f;
-          }
-        }
-      }
-    }
-    (void)n_blocks;
-    __syncthreads();
+    gram::cosines<D, kWaves>(kg, cpos, C, cinv, region, tid);
+    const float* tri = reinterpret_cast<const float*>(region) + 1;
     if (wave == 0) {
-      // One wave runs every step: lane l holds candidate slots l, l + 64, l + 128, l + 192, their
-      // s~ (-inf once admitted or for slots beyond C) and running max-cosine.  The cosine of
-      // slots (i, j), i <= j, is at row_off(i) + j of the triangle.  s~ and the cosines are
-      // finite after the clamps below, so a live score is finite and an admitted one -inf.
-      auto row_off = [&](int i) { return (i * (2 * C - i + 1)) / 2 - i; };
-      float st[kGramSlots], corr[kGramSlots];
-      int cq[kGramSlots], offq[kGramSlots];
-#pragma unroll
-      for (int q = 0; q < kGramSlots; ++q) {
-        const int c = lane + 64 * q;
-        cq[q] = min(c, C - 1);
-        offq[q] = row_off(cq[q]);
-        // a NaN or -inf score still ranks above the admitted slots (as the lowest finite one)
-        st[q] = c < C ? fmaxf(cst[c], -FLT_MAX) : -INFINITY;
-        corr[q] = 0.f;
-      }
-      for (int t = 0; t < bp; ++t) {
-        // the cosines against the last admitted slot, every read in flight at once (slots past C
-        // read a valid entry that is not used)
-        if (last >= 0) {
-          const int off_last = row_off(last);
-          float gv[kGramSlots];
-#pragma unroll
-          for (int q = 0; q < kGramSlots; ++q)
-            gv[q] = gram[cq[q] <= last ? offq[q] + last : off_last + cq[q]];
-#pragma unroll
-          for (int q = 0; q < kGramSlots; ++q) corr[q] = __builtin_elementwise_maximum(corr[q], gv[q]);
-        }
-        float my_score = -INFINITY;
-        int my_slot = 0x7FFFFFFF;
-#pragma unroll
-        for (int q = 0; q < kGramSlots; ++q) {
-          const float sc = fmaf(lam2, corr[q], st[q]);
-          const bool better = sc > my_score;  // q ascending: ties keep the lower slot
-          my_score = better ? sc : my_score;
-          my_slot = better ? lane + 64 * q : my_slot;
-        }
-        const uint64_t b = wave_best<false>(my_score, my_slot);
-        last = __builtin_amdgcn_readfirstlane(min(max(unpack_slot(b), 0), C - 1));  // bp <= C
-#pragma unroll
-        for (int q = 0; q < kGramSlots; ++q) st[q] = lane + 64 * q == last ? -INFINITY : st[q];
-        // the step's record, written out after the last step (every lane stores the same value)
-        trace_slot[t] = (uint32_t)last;
-        trace_key[t] = (uint32_t)(b >> 32);
-      }
+      gram::Greedy gr;
+      gr.init(cst, C, lane);
+      if (sel_score) gr.run<true>(tri, C, bp, lam2, lane, trace_slot, trace_key);
+      else gr.run<false>(tri, C, bp, lam2, lane, trace_slot, trace_key);
+      last = gr.last;
       if (cand_idx || cand_corr) {
         // an admitted slot reports its corr at admission: the largest of 0 and its cosines to the
         // slots admitted before it (the same maximum the steps formed); the slot of s~ keeps it
@@ -826,31 +691,32 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
           float m = 0.f;
           for (int u = 0; u < t; ++u) {
             const int su = (int)trace_slot[u];
-            m = __builtin_elementwise_maximum(m, gram[si < su ? row_off(si) + su : row_off(su) + si]);
+            m = __builtin_elementwise_maximum(m, tri[gram::row_off(min(si, su), C) + max(si, su)]);
           }
           corr_adm[si] = m;
         }
         // corr after the last step includes the last admitted key
         const size_t o = ((size_t)p * h_kv + g) * cand_stride;
-        const int off_last = row_off(last);
+        float gl[gram::kSlots];
+        gr.cos_to(tri, last, C, gl);
 #pragma unroll
-        for (int q = 0; q < kGramSlots; ++q) {
+        for (int q = 0; q < gram::kSlots; ++q) {
           const int c = lane + 64 * q;
+          float cr = 0.f;
           if (c < C) {
-            const bool adm = st[q] == -INFINITY;
-            const float gl = gram[cq[q] <= last ? offq[q] + last : off_last + cq[q]];
-            corr[q] = adm ? corr_adm[c] : __builtin_elementwise_maximum(corr[q], gl);
+            const bool adm = gr.st[q] == -INFINITY;
+            cr = adm ? corr_adm[c] : __builtin_elementwise_maximum(gr.corr[q], gl[q]);
           }
           if (c < cand_stride) {
             if (cand_idx) cand_idx[o + c] = c < C ? cpos[c] : -1;
-            if (cand_corr) cand_corr[o + c] = c < C ? corr[q] : 0.f;
+            if (cand_corr) cand_corr[o + c] = cr;
           }
         }
       }
     }
     if (cand_idx || cand_corr) {
       const size_t o = ((size_t)p * h_kv + g) * cand_stride;
-      for (int c = kGramSlots * 64 + tid; c < cand_stride; c += kThreads) {
+      for (int c = gram::kSlots * 64 + tid; c < cand_stride; c += kThreads) {
         if (cand_idx) cand_idx[o + c] = -1;
         if (cand_corr) cand_corr[o + c] = 0.f;
       }
@@ -1075,7 +941,7 @@ hipError_t select_launch(const Shape& s, const SelectArgs& a, size_t body, hipSt
 template <int DT, int D, int NT, int CPT, bool GRAM>
 hipError_t select_dispatch(const Shape& s, const SelectArgs& a, hipStream_t st) {
   using T = typename Elem<DT>::T;
-  const size_t body = GRAM ? tri_entries(a.max_cand) * 4 : (size_t)a.max_cand * D * sizeof(T);
+  const size_t body = GRAM ? gram::region_bytes<D>(a.max_cand) : (size_t)a.max_cand * D * sizeof(T);
   const size_t staged = lds_head(a.max_cand) + std::max(body, (size_t)a.max_cand_all * 4) +
                         sizeof(SelectShared<NT / 64>);
   if ((size_t)a.max_cand_all * 4 <= (size_t)kMaxStagedKeyBytes && staged <= kLdsBytes)
@@ -1089,7 +955,7 @@ hipError_t select_cpt(const Shape& s, const SelectArgs& a, hipStream_t st) {
   if constexpr (DT == kDtBf16) {
     // bf16 key rows fit the registers of 16 waves: one candidate per thread of 1024
     static_assert(kMaxCand <= 1024, "one candidate per thread");
-    if (a.max_cand <= kGramMaxCand) return select_dispatch<DT, D, 1024, 1, true>(s, a, st);
+    if (a.max_cand <= gram::kMaxCand) return select_dispatch<DT, D, 1024, 1, true>(s, a, st);
     return select_dispatch<DT, D, 1024, 1, false>(s, a, st);
   } else {
     // only the candidates-per-thread counts that the LDS key copy allows are instantiated

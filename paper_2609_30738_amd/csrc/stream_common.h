@@ -80,6 +80,16 @@ struct StreamArgs {
   // candidate mode, pass 1: per unit code_stride words of tile codes (32 words per tile)
   uint32_t* codes;
   int code_stride;
+  // candidate mode with the selection in the same launch (sel_idx != nullptr, every C_p <= 256):
+  // the greedy's outputs as from the selection kernel, [n_prob][h_kv][budget], and with k_out the
+  // compacted rows of K and V, [n_prob][h_kv][out_rows][D]
+  const float* lambda2;
+  int32_t* sel_idx;
+  float* sel_score;
+  const uint16_t* v;
+  uint16_t* k_out;
+  uint16_t* v_out;
+  int out_rows;
 };
 
 constexpr int kCandLists = kWaves;  // candidate lists per unit: one per wave of the fused kernel
@@ -176,6 +186,9 @@ template <int D, int NB, int NW, int S> struct KeyStream {
   // nullptr: tile j of the wave is the segment's tile j NW + wave; otherwise order[j NW + wave]
   // (LDS) names it
   const uint16_t* order = nullptr;
+  // loads that stay in the caches (a second visit of a few tiles whose keys are read again soon);
+  // otherwise non-temporal (aux 2: each key read once per pass)
+  bool keep = false;
 
   // the segment's tile index of the wave's tile j
   __device__ int tile_index(int j) const {
@@ -202,23 +215,26 @@ template <int D, int NB, int NW, int S> struct KeyStream {
     uint16_t* dst = ring + (j & (S - 1)) * Gm::TE;
     if (t0 + kTileKeys <= k1) {
       // a whole tile: a wave-uniform base and per-lane offsets that do not change from tile to
-      // tile (aux 2: non-temporal, the keys are read once per pass)
+      // tile
       const char* base = reinterpret_cast<const char*>(kg + (size_t)t0 * D);
       int off[kOffRegs];
 #pragma unroll
       for (int i = 0; i < kOffRegs; ++i) off[i] = chunk_off(i, lane);
 #pragma unroll
-      for (int i = 0; i < Gm::NDMA; ++i)
-        __builtin_amdgcn_global_load_lds((gptr_t)(base + (i / 4) * 4096 + off[i % 4]),
-                                         (lptr_t)(dst + i * 512), 16, 0, 2);
+      for (int i = 0; i < Gm::NDMA; ++i) {
+        const gptr_t src = (gptr_t)(base + (i / 4) * 4096 + off[i % 4]);
+        if (keep) __builtin_amdgcn_global_load_lds(src, (lptr_t)(dst + i * 512), 16, 0, 0);
+        else __builtin_amdgcn_global_load_lds(src, (lptr_t)(dst + i * 512), 16, 0, 2);
+      }
     } else {
 #pragma unroll
       for (int i = 0; i < Gm::NDMA; ++i) {
         const int pos = 64 * i + lane;
         const int row = pos / Gm::CH;
         const int ch = (pos % Gm::CH) ^ (row % Gm::CH);
-        const uint16_t* src = kg + (size_t)min(t0 + row, k1 - 1) * D + ch * 8;
-        __builtin_amdgcn_global_load_lds((gptr_t)src, (lptr_t)(dst + i * 512), 16, 0, 2);
+        const gptr_t src = (gptr_t)(kg + (size_t)min(t0 + row, k1 - 1) * D + ch * 8);
+        if (keep) __builtin_amdgcn_global_load_lds(src, (lptr_t)(dst + i * 512), 16, 0, 0);
+        else __builtin_amdgcn_global_load_lds(src, (lptr_t)(dst + i * 512), 16, 0, 2);
       }
     }
   }

@@ -19,6 +19,7 @@
 //
 // On the 32-layer Mistral-shaped pass at L = 32768 (C = 256) the bounds leave about one tile in
 // twenty to pass 2.
+#include "select_gram.h"
 #include "stream_passes.h"
 
 namespace kv {
@@ -149,7 +150,7 @@ __device__ __forceinline__ void find_cut_bin(const uint32_t* hist, uint32_t top,
   }
 }
 
-template <int D, int NB, bool ALL, int NW, int S>
+template <int D, int NB, bool ALL, int NW, int S, bool SEL>
 __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) {
   using Gm = SGeo<D, NB>;
   constexpr int R = Gm::R, NS = Gm::NS, NT = NW * 64;
@@ -163,6 +164,9 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   // the waves' key rings; after the second pass, the order keys of the evaluated scores
   constexpr int kRingElems = NW * S * Gm::TE > 2 * kCandMaxLen ? NW * S * Gm::TE : 2 * kCandMaxLen;
   __shared__ __align__(16) uint16_t ring[kRingElems];
+  static_assert(!SEL || gram::region_bytes<D>(gram::kMaxCand) <= sizeof(ring),
+                "the staged key rows and the cosine triangle fit the ring");
+  static_assert(!SEL || 4 * gram::kMaxCand <= kPruneMaxTiles, "the slot arrays fit the bounds");
   // the waves' statistics after pass 1, the histogram of evaluated scores in pass 2
   __shared__ __align__(16) uint32_t red_hist[kRedWords > kPruneBins ? kRedWords : kPruneBins];
   __shared__ __align__(16) float bsh[R];
@@ -301,7 +305,8 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   const int bp = a.budgets ? a.budgets[p] : a.budget;
   const int C = min(a.cand_mult * bp, n_cand);
   const int my_tiles2 = n_ord > wave ? (n_ord - wave + NW - 1) / NW : 0;
-  KeyStream<D, NB, NW, S> ks2{ring + wave * S * Gm::TE, kg, 0, L, wave, lane, order};
+  // the second visit keeps its tiles in the caches: the selection reads the candidates' rows next
+  KeyStream<D, NB, NW, S> ks2{ring + wave * S * Gm::TE, kg, 0, L, wave, lane, order, true};
   ks2.prologue(my_tiles2);
   float* score_u = reinterpret_cast<float*>(codes_u);  // a tile's codes are dead once bounded
   // the cut's scan starts at the bin of the largest finite bound: scores above it (in tiles with a
@@ -429,27 +434,74 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   }
   __syncthreads();
   uint64_t* dst = a.cand_out + ((size_t)p * a.h_kv + g) * a.cand_stride;
+  // with the selection: the candidates' positions and scores by slot, their 1 / |k|, the greedy's
+  // trace (the bounds are dead after pass 2; the ranked group's space after the cut)
+  int32_t* cpos_l = reinterpret_cast<int32_t*>(ub);
+  float* cst_l = ub + gram::kMaxCand;
+  float* cinv_l = ub + 2 * gram::kMaxCand;
+  uint32_t* trace_slot = reinterpret_cast<uint32_t*>(ub + 3 * gram::kMaxCand);
+  uint32_t* trace_key = bins + kBitmapWords;
   for_each_entry([&](uint64_t e, int key) {
     if (e >= t_entry) {
       const uint32_t below = bm[key >> 5] & ((1u << (key & 31)) - 1u);
       const uint32_t rank = wpre[key >> 5] + (uint32_t)__popc(below);
-      if (rank < (uint32_t)C) dst[rank] = e;  // exactly C entries are >= t_entry
+      if (rank < (uint32_t)C) {  // exactly C entries are >= t_entry
+        dst[rank] = e;
+        if constexpr (SEL) {
+          cpos_l[rank] = key;
+          cst_l[rank] = key_float((uint32_t)(e >> 32));
+        }
+      }
     }
   });
   for (int i = C + tid; i < a.cand_stride; i += NT) dst[i] = 0ull;
-  if (tid == 0) {
-    float d = c_max[0];
+  float den = c_max[0];
 #pragma unroll
-    for (int w = 1; w < NW; ++w) d = fmaxf(d, c_max[w]);
-    a.cand_max[(size_t)p * a.h_kv + g] = fmaxf(d, 1e-12f);
+  for (int w = 1; w < NW; ++w) den = fmaxf(den, c_max[w]);
+  den = fmaxf(den, 1e-12f);
+  if (tid == 0) a.cand_max[(size_t)p * a.h_kv + g] = den;
+  if constexpr (SEL) {
+    // ---- the selection of the unit (section 3.2, Eq. (2), (4)) from its C candidates, as the
+    //      selection kernel runs it on the list just written: s~ = score / normaliser, the cosine
+    //      triangle in the ring, the greedy on wave 0, then the outputs and the compaction
+    __syncthreads();  // the slot arrays are complete; the ring's score keys are dead
+    for (int c2 = tid; c2 < C; c2 += NT) cst_l[c2] = cst_l[c2] / den;
+    gram::cosines<D, NW>(kg, cpos_l, C, cinv_l, reinterpret_cast<unsigned char*>(ring), tid);
+    const float* tri = reinterpret_cast<const float*>(ring) + 1;
+    if (wave == 0) {
+      gram::Greedy gr;
+      gr.init(cst_l, C, lane);
+      if (a.sel_score) gr.run<true>(tri, C, bp, a.lambda2[p], lane, trace_slot, trace_key);
+      else gr.run<false>(tri, C, bp, a.lambda2[p], lane, trace_slot, trace_key);
+    }
+    __syncthreads();
+    const size_t so0 = ((size_t)p * a.h_kv + g) * a.budget;
+    for (int t = tid; t < a.budget; t += NT) {
+      a.sel_idx[so0 + t] = t < bp ? cpos_l[trace_slot[t]] : -1;
+      if (a.sel_score) a.sel_score[so0 + t] = t < bp ? key_float(trace_key[t]) : 0.f;
+    }
+    if (a.k_out) {
+      int32_t* srt = reinterpret_cast<int32_t*>(ring);  // the triangle is dead
+      gram::admitted_in_order(trace_slot, cpos_l, bp, red_hist, srt, tid, NT);
+      constexpr int kRowVecs = D * 2 / 16;
+      copy_kept_rows(reinterpret_cast<const uint4*>(a.k), reinterpret_cast<const uint4*>(a.v), srt,
+                     bp, a.keep_tail, L, kRowVecs, stat_base * kRowVecs,
+                     ((size_t)p * a.h_kv + g) * a.out_rows * kRowVecs,
+                     reinterpret_cast<uint4*>(a.k_out), reinterpret_cast<uint4*>(a.v_out), tid, NT);
+    }
   }
 }
 
 template <int D, int NB> struct PruneLaunch {
   static hipError_t run(const Shape& s, const StreamArgs& args, hipStream_t st) {
     const dim3 grid(1, s.h_kv, s.n_prob);
-    if (args.sigma_all) window_prune_kernel<D, NB, true, kWaves, 2><<<grid, kThreads, 0, st>>>(args);
-    else window_prune_kernel<D, NB, false, kWaves, 2><<<grid, kThreads, 0, st>>>(args);
+    if (args.sel_idx) {
+      if (args.sigma_all) window_prune_kernel<D, NB, true, kWaves, 2, true><<<grid, kThreads, 0, st>>>(args);
+      else window_prune_kernel<D, NB, false, kWaves, 2, true><<<grid, kThreads, 0, st>>>(args);
+    } else {
+      if (args.sigma_all) window_prune_kernel<D, NB, true, kWaves, 2, false><<<grid, kThreads, 0, st>>>(args);
+      else window_prune_kernel<D, NB, false, kWaves, 2, false><<<grid, kThreads, 0, st>>>(args);
+    }
     return hipGetLastError();
   }
 };
@@ -466,8 +518,11 @@ hipError_t launch_stream_window_cands(const Shape& s, const StreamPlan& plan, co
                                       int budget, const int32_t* budgets, int cand_mult,
                                       int keep_tail, float* row_max, float* row_sum,
                                       uint64_t* cand_out, float* cand_max, int cand_stride,
-                                      uint32_t* codes, bool sigma_all, hipStream_t stream) {
+                                      uint32_t* codes, bool sigma_all, const CandSelect* sel,
+                                      hipStream_t stream) {
   if (plan.max_segs != 1 || !cand_out || !cand_max || !codes || s.max_len > kCandMaxLen)
+    return hipErrorInvalidValue;
+  if (sel && (!sel->lambda2 || !sel->sel_idx || (sel->k_out && (!sel->v || !sel->v_out))))
     return hipErrorInvalidValue;
   stream::StreamArgs a = stream::base_args(s, plan, q_win, k, scale);
   a.row_max_out = row_max;
@@ -484,6 +539,15 @@ hipError_t launch_stream_window_cands(const Shape& s, const StreamPlan& plan, co
   a.keep_tail = keep_tail;
   a.codes = codes;
   a.code_stride = cand_code_stride(s);
+  if (sel) {
+    a.lambda2 = sel->lambda2;
+    a.sel_idx = sel->sel_idx;
+    a.sel_score = sel->sel_score;
+    a.v = static_cast<const uint16_t*>(sel->v);
+    a.k_out = static_cast<uint16_t*>(sel->k_out);
+    a.v_out = static_cast<uint16_t*>(sel->v_out);
+    a.out_rows = sel->out_rows;
+  }
   return stream::launch_for_shape<stream::PruneLaunch>(s, a, stream);
 }
 

@@ -46,11 +46,14 @@ def run_gpu(wl: workloads.Workload, problems: Optional[Sequence[int]] = None, *,
             pool: int = 1, w_mu: float = 1.0, sigma_rows: str = "group_mean",
             budgets: Optional[Sequence[int]] = None, redraw: Optional[certify.Redraw] = None,
             case: Optional[str] = None, timed: bool = False) -> GpuRun:
-    """One pass through the C ABI.  timed=True runs the benchmark's calls (kv_window_candidates,
-    then kv_mmr_select_candidates with the compaction: row_max, row_sum, sel_idx, k_out, v_out;
+    """One pass through the C ABI.  timed=True runs the benchmark's call (kv_evict_pass with the
+    compaction: row_max, row_sum, sel_idx, k_out, v_out, and its sel_score as evict_sel_score;
     where the candidate path does not apply, pool > 1 or too many candidates,
-    kv_window_base_scores and kv_mmr_select_scored take its place) and, on the same inputs,
-    kv_mmr_select_candidates again with the optional outputs (cands_*), kv_window_base_scores and
+    kv_window_base_scores and kv_mmr_select_scored take its place) and, on the same inputs, the two
+    calls it stands for on a workspace of their own (kv_window_candidates, then
+    kv_mmr_select_candidates with the compaction: twocall_*, and the candidate lists of both
+    workspaces as evict_lists / twocall_lists), kv_mmr_select_candidates again with the optional
+    outputs (cands_*), kv_window_base_scores and
     kv_mmr_select_scored (score, *_scored), and kv_window_mu_sigma_ex and kv_mmr_select_ex with the
     optional outputs (mu, sigma, sel_score, cand_idx, cand_corr; their row statistics and sel_idx
     as row_max_plain, row_sum_plain, sel_idx_plain)."""
@@ -87,12 +90,24 @@ def run_gpu(wl: workloads.Workload, problems: Optional[Sequence[int]] = None, *,
                                               budgets=budgets_dev) if pool == 1 else 0
         if wcb > 0:
             ws_c = torch.empty(wcb, dtype=torch.uint8, device=dev)
+            ev_score = torch.empty_like(out.sel_score)
+            _lib.evict_pass(b, inp.q_win, inp.k, inp.v, inp.scale, inp.lambda1, inp.lambda2, B,
+                            cand_mult, tail, out.row_max, out.row_sum, out.sel_idx, ws_c,
+                            sel_score=ev_score, k_out=out.k_out, v_out=out.v_out, w_mu=w_mu,
+                            budgets=budgets_dev, sigma_rows=sigma_rows)
+            ws_t = torch.empty(wcb, dtype=torch.uint8, device=dev)
+            two = {n: torch.empty_like(getattr(out, n))
+                   for n in ("row_max", "row_sum", "sel_idx", "k_out", "v_out")}
             _lib.window_candidates(b, inp.q_win, inp.k, inp.scale, inp.lambda1, B, cand_mult, tail,
-                                   out.row_max, out.row_sum, ws_c, w_mu=w_mu, budgets=budgets_dev,
-                                   sigma_rows=sigma_rows)
-            _lib.mmr_select_candidates(b, ws_c, inp.k, inp.v, inp.lambda2, B, cand_mult, tail,
-                                       out.sel_idx, k_out=out.k_out, v_out=out.v_out,
+                                   two["row_max"], two["row_sum"], ws_t, w_mu=w_mu,
+                                   budgets=budgets_dev, sigma_rows=sigma_rows)
+            _lib.mmr_select_candidates(b, ws_t, inp.k, inp.v, inp.lambda2, B, cand_mult, tail,
+                                       two["sel_idx"], k_out=two["k_out"], v_out=two["v_out"],
                                        budgets=budgets_dev)
+            extra.update({n + "_twocall": x for n, x in two.items()})
+            lb = _list_bytes(wl, packed, B if bud is None else bud, cand_mult, tail)
+            extra.update(evict_sel_score=ev_score, evict_lists=ws_c[:lb], twocall_lists=ws_t[:lb])
+            ws_c = ws_t
             full = {n: torch.empty_like(getattr(out, n))
                     for n in ("sel_idx", "sel_score", "cand_idx", "cand_corr")}
             _lib.mmr_select_candidates(b, ws_c, inp.k, None, inp.lambda2, B, cand_mult, tail,
@@ -137,6 +152,15 @@ def run_gpu(wl: workloads.Workload, problems: Optional[Sequence[int]] = None, *,
                            sigma_all_rows=sigma_rows == "all_rows",
                            budgets=None if bud is None else tuple(int(x) for x in bud))
     return GpuRun(wl, probs, packed, lam1, lam2, B, opts, tail, host, red, case, bud, custom)
+
+
+def _list_bytes(wl, packed, budgets, cand_mult: int, tail: int) -> int:
+    """Bytes of the candidate lists at the start of kv_window_candidates' workspace: a list of
+    max_p C_p 8-byte entries per (problem, kv head) unit."""
+    n = len(packed.lens)
+    bp = np.broadcast_to(np.asarray(budgets, dtype=np.int64), (n,))
+    c = max(min(cand_mult * int(bp[j]), int(packed.lens[j]) - tail) for j in range(n))
+    return n * wl.h_kv * c * 8
 
 
 def run_case(name: str, problems: Optional[Sequence[int]] = None, **kw) -> GpuRun:
@@ -212,7 +236,7 @@ def check_problem(run: GpuRun, j: int, res: Optional[evict.ProblemResult] = None
         # the timed path's row statistics and base scores are those of the mu / sigma path, bit
         # for bit
         for name in ("row_max", "row_sum"):
-            for other in ("_plain", "_scored"):
+            for other in ("_plain", "_scored", "_twocall"):
                 if name + other in H:
                     assert np.array_equal(
                         H[name][j * rows:(j + 1) * rows].view(np.uint32),
@@ -249,6 +273,18 @@ def check_problem(run: GpuRun, j: int, res: Optional[evict.ProblemResult] = None
         if "sel_idx_plain" in H:
             assert np.array_equal(H["sel_idx_plain"][o * B:o * B + Bp], sel), (
                 f"{where} g={g}: kv_mmr_select_ex and the timed selection disagree")
+        if "sel_idx_twocall" in H:
+            # kv_evict_pass is the two calls, bit for bit (its sel_score against the second
+            # call's optional-output run); the compacted blocks' written rows
+            blk = o * (B + run.keep_tail) * wl.d
+            for n, lo, hi in (("sel_idx", o * B, (o + 1) * B),
+                              ("k_out", blk, blk + rows_out * wl.d),
+                              ("v_out", blk, blk + rows_out * wl.d)):
+                assert np.array_equal(H[n][lo:hi], H[n + "_twocall"][lo:hi]), (
+                    f"{where} g={g}: {n} of kv_evict_pass and of the two calls differ")
+            assert np.array_equal(H["evict_sel_score"][o * B:(o + 1) * B].view(np.uint32),
+                                  H["cands_sel_score"][o * B:(o + 1) * B].view(np.uint32)), (
+                f"{where} g={g}: sel_score of kv_evict_pass and kv_mmr_select_candidates differ")
         if "sel_idx_scored" in H:
             assert np.array_equal(H["sel_idx_scored"][o * B:(o + 1) * B],
                                   H["sel_idx"][o * B:(o + 1) * B]), (
@@ -288,6 +324,10 @@ def check_all(run: GpuRun, js: Optional[Sequence[int]] = None, heads=None,
               workers: Optional[int] = None) -> List[compare.SelectionReport]:
     """Compare problems js (default: all) of a run, the oracle computed in parallel."""
     js = list(range(len(run.problems))) if js is None else list(js)
+    if "evict_lists" in run.host:
+        # kv_evict_pass leaves the candidates in its workspace as kv_window_candidates does
+        assert np.array_equal(run.host["evict_lists"], run.host["twocall_lists"]), (
+            "candidate lists of kv_evict_pass and kv_window_candidates differ")
     res = oracle_results(run, js, workers)
     reports = []
     for j in js:

@@ -450,3 +450,48 @@ def test_candidates_checks():
     # the selection reads only the lists and the normalisers: 8 units x 256 entries
     assert select(ws_bytes=8 * 256 * 8 + 256 - 1) == _lib.KV_ERR_WORKSPACE
     assert select(ws=NULL) == _lib.KV_ERR_WORKSPACE
+
+
+def test_evict_pass_checks():
+    """kv_evict_pass refuses every argument that kv_window_candidates or kv_mmr_select_candidates
+    refuses, with the same code and before any launch (the workspace is that of
+    kv_window_candidates)."""
+    lib = _lib.lib()
+    for lens in ((4096,), (32768,) * 32):  # the two calls in turn; one launch (C = 256)
+        pr = HostProblem(lens=lens)
+        need = lib.kv_candidates_workspace_bytes(pr.ref(), 64, 4, 32, None)
+        assert need > 0
+        ws = np.zeros((need + 512) // 4, dtype=np.float32) if len(lens) == 1 else None
+        wsp = ctypes.c_void_p(ws.ctypes.data + (-ws.ctypes.data) % 256) if ws is not None else P
+        nan = float("nan")
+        pool3 = _lib.KvSelectOpts(3, 1.0, None, None)
+        w_nan = _lib.KvSelectOpts(1, nan, None, None)
+        bh = np.full(len(lens), 64, dtype=np.int32)
+        host_only = _lib.KvSelectOpts(1, 1.0, bh.ctypes.data, None)
+
+        def evict(**kw):
+            opts = kw.get("opts")
+            return lib.kv_evict_pass(
+                kw.get("pr", pr.ref()), kw.get("q", P), kw.get("k", P), kw.get("v", P),
+                kw.get("scale", 0.088), kw.get("lam1", P), kw.get("lam2", P), kw.get("rows", 0),
+                kw.get("budget", 64), kw.get("cand_mult", 4), 32,
+                None if opts is None else ctypes.byref(opts), kw.get("rm", P), kw.get("rs", P),
+                kw.get("sel", P), kw.get("score", NULL), kw.get("k_out", P), kw.get("v_out", P),
+                kw.get("ws", wsp), kw.get("ws_bytes", need), NULL)
+        assert evict(pr=None) == _lib.KV_ERR_NULL
+        for kw in (dict(q=NULL), dict(k=NULL), dict(lam1=NULL), dict(lam2=NULL), dict(rm=NULL),
+                   dict(rs=NULL), dict(sel=NULL), dict(k_out=NULL), dict(v_out=NULL),
+                   dict(v=NULL), dict(opts=host_only)):
+            assert evict(**kw) == _lib.KV_ERR_NULL, (lens[0], kw)
+        odd = ctypes.c_void_p(BUF.ctypes.data + 4)
+        for kw in (dict(k=odd), dict(q=odd), dict(v=odd), dict(k_out=odd), dict(v_out=odd),
+                   dict(scale=nan), dict(rows=2), dict(cand_mult=-1), dict(cand_mult=1 << 30),
+                   dict(opts=pool3), dict(opts=w_nan)):
+            assert evict(**kw) == _lib.KV_ERR_ARG, (lens[0], kw)
+        assert evict(budget=0) == _lib.KV_ERR_BUDGET
+        assert evict(budget=lens[0]) == _lib.KV_ERR_BUDGET
+        assert evict(cand_mult=0) == _lib.KV_ERR_SHAPE
+        if ws is not None:
+            assert evict(ws_bytes=need - 1) == _lib.KV_ERR_WORKSPACE
+            assert evict(ws=NULL) == _lib.KV_ERR_WORKSPACE
+            assert evict(ws=ctypes.c_void_p(wsp.value + 16)) == _lib.KV_ERR_WORKSPACE
