@@ -298,11 +298,11 @@ def main() -> None:
                          "--cpu-single-layers layers single-threaded; 0: skip")
     ap.add_argument("--cpu-single-layers", type=int, default=8,
                     help="layers of the single-threaded oracle sample")
-    ap.add_argument("--settle-ms", type=float, default=0.0,
-                    help="untimed passes before the warm-up, for at least this long (0: none). "
-                         "From idle the engine clock ramps up over the first 20-30 passes; after "
-                         "a few hundred ms of back-to-back passes the pass time turns bimodal "
-                         "(0.82 / 0.91 ms) as the power management steps the clock")
+    ap.add_argument("--settle-ms", type=float, default=30.0,
+                    help="untimed passes before the warm-up: at least 20 and for at least this "
+                         "long (0: none).  From idle the engine clock ramps up over the first "
+                         "20-40 passes, so that a short warm-up leaves the first timed steps "
+                         "slower than the rest")
     ap.add_argument("--flush", choices=("read", "write"), default="read",
                     help="how the last-level cache is emptied before each timed step")
     ap.add_argument("--path", choices=PATHS, default=PATHS[0],
@@ -420,9 +420,8 @@ def main() -> None:
     def new_events():
         return [torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
 
-    # optional settle phase (off by default): from idle the engine clock ramps up over the first
-    # 20-30 passes (a fixed bf16 GEMM between passes runs ~17 % faster after them), while a few
-    # hundred ms of back-to-back passes make the pass time bimodal under the power management
+    # settle phase (--settle-ms, 30 ms by default; reported as "settle"): from idle the engine
+    # clock ramps up over the first 20-40 passes, which a warm-up of a few steps does not cover
     settle_passes, t_settle = 0, time.perf_counter()
     while args.settle_ms > 0 and (settle_passes < 20 or
                                   (time.perf_counter() - t_settle) * 1e3 < args.settle_ms):

@@ -91,18 +91,27 @@ __device__ __forceinline__ void cosines(const uint16_t* __restrict__ kg, const i
     n2 += __shfl_xor(n2, 1, 64);
     if (h == 0) cinv[r] = n2 > 0.f ? 1.f / sqrtf(n2) : 0.f;
   }
-  // the dot products of blocks (I, J), I <= J, block b of the row-major enumeration on wave b % NW
-  const int nb = (C + 31) / 32;
+  // the dot products of blocks (I, J), I <= J: each wave takes a run of consecutive blocks of the
+  // row-major enumeration (mostly one block row, so that the A operand is read once per slice)
+  const int nb = (C + 31) / 32, n_blk = nb * (nb + 1) / 2;
+  const int per = n_blk / NW, extra = n_blk % NW;
+  const int first = wave * per + min(wave, extra), count = per + (wave < extra ? 1 : 0);
   int blk_i[kBlk], blk_j[kBlk];
-#pragma unroll
-  for (int u = 0; u < kBlk; ++u) {
-    int I = 0, rem = wave + u * NW;
+  {
+    int I = 0, rem = first;
     while (I < nb && rem >= nb - I) {
       rem -= nb - I;
       ++I;
     }
-    blk_i[u] = I;  // I == nb: no block
-    blk_j[u] = I + rem;
+#pragma unroll
+    for (int u = 0; u < kBlk; ++u) {
+      blk_i[u] = u < count ? I : nb;  // nb: no block
+      blk_j[u] = I + rem;
+      if (++rem >= nb - I) {
+        ++I;
+        rem = 0;
+      }
+    }
   }
   f32x16_t acc[kBlk];
 #pragma unroll
@@ -111,13 +120,19 @@ __device__ __forceinline__ void cosines(const uint16_t* __restrict__ kg, const i
     for (int r = 0; r < 16; ++r) acc[u][r] = 0.f;
 #pragma unroll
   for (int sl = 0; sl < kSlices; ++sl) {
+    bf16x8_t a = bf16x8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    int a_row = -1;  // the block row whose fragment `a` holds (wave-uniform)
 #pragma unroll
     for (int u = 0; u < kBlk; ++u) {
       if (blk_i[u] < nb) {
-        const bf16x8_t a =
-            *reinterpret_cast<const bf16x8_t*>(at(min(32 * blk_i[u] + l32, C - 1), 2 * sl + half));
+        if (blk_i[u] != a_row) {
+          a = *reinterpret_cast<const bf16x8_t*>(at(min(32 * blk_i[u] + l32, C - 1), 2 * sl + half));
+          a_row = blk_i[u];
+        }
         const bf16x8_t b =
-            *reinterpret_cast<const bf16x8_t*>(at(min(32 * blk_j[u] + l32, C - 1), 2 * sl + half));
+            blk_j[u] == blk_i[u]
+                ? a
+                : *reinterpret_cast<const bf16x8_t*>(at(min(32 * blk_j[u] + l32, C - 1), 2 * sl + half));
         acc[u] = mfma_step(a, b, acc[u]);
       }
     }
@@ -129,28 +144,39 @@ __device__ __forceinline__ void cosines(const uint16_t* __restrict__ kg, const i
   for (int u = 0; u < kBlk; ++u) {
     if (blk_i[u] < nb) {
       // register jj holds row i = i0 + 8 (jj / 4) + jj % 4 of column j; row_off(i + 1) =
-      // row_off(i) + C - 2 - i
+      // row_off(i) + C - 2 - i.  cinv is read up to 32 nb - 1 (past C: values not used).
       const int j = 32 * blk_j[u] + l32;
       const int i0 = 32 * blk_i[u] + 4 * half;
-      const bool diag = blk_i[u] == blk_j[u];
-      const float inv_j = cinv[min(j, C - 1)];
+      const float inv_j = cinv[j];
       float inv_i[16];
 #pragma unroll
-      for (int jj = 0; jj < 16; ++jj) inv_i[jj] = cinv[min(i0 + 8 * (jj >> 2) + (jj & 3), C - 1)];
-      // a lane without an entry (i >= j in a diagonal block, j >= C) stores to its own word
-      // past the triangle
-      const int spare = C * (C - 1) / 2 + lane;
+      for (int jj = 0; jj < 16; ++jj) inv_i[jj] = cinv[i0 + 8 * (jj >> 2) + (jj & 3)];
+      if (blk_i[u] < blk_j[u] && 32 * blk_j[u] + 32 <= C) {
+        // a whole block above the diagonal: every register is an entry
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int ir = i0 + 8 * r;
-        int idx = row_off(ir, C) + j;
+        for (int r = 0; r < 4; ++r) {
+          const int ir = i0 + 8 * r;
+          int idx = row_off(ir, C) + j;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int jj = 4 * r + e;
-          const float cs = acc[u][jj] * inv_i[jj] * inv_j;
-          const bool live = j < C && (!diag || ir + e < j);
-          tri[live ? idx : spare] = __builtin_isfinite(cs) ? cs : 0.f;
-          idx += C - 2 - (ir + e);
+          for (int e = 0; e < 4; ++e) {
+            const float cs = acc[u][4 * r + e] * inv_i[4 * r + e] * inv_j;
+            tri[idx] = __builtin_isfinite(cs) ? cs : 0.f;
+            idx += C - 2 - (ir + e);
+          }
+        }
+      } else {
+        // a lane without an entry (i >= j, j >= C) stores to its own word past the triangle
+        const int spare = C * (C - 1) / 2 + lane;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int ir = i0 + 8 * r;
+          int idx = row_off(ir, C) + j;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float cs = acc[u][4 * r + e] * inv_i[4 * r + e] * inv_j;
+            tri[j < C && ir + e < j ? idx : spare] = __builtin_isfinite(cs) ? cs : 0.f;
+            idx += C - 2 - (ir + e);
+          }
         }
       }
     }

@@ -158,6 +158,7 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   constexpr int kTilesPerThread = kPruneMaxTiles / NT;
   static_assert(kPruneMaxTiles % NT == 0, "whole tiles per thread");
   static_assert(NT % kTileKeys == 0, "whole tiles per visit");
+  static_assert(kTileKeys == 32, "a half-wave visits the keys of one tile");
   static_assert(2 * kOrderBins >= kBitmapWords + 2 * kRankDirect,
                 "the bitmap and the ranked group fit the order's bins");
   static_assert(kPruneBins >= kBitmapWords, "the word prefixes fit the histogram");
@@ -385,34 +386,71 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
     group = red_hist[cut];
   }
   // the group: at most kRankDirect entries (or one, once every digit is found); its need-th
-  // largest entry is the C-th largest overall, found by counting the larger ones
+  // largest entry is the C-th largest overall, found by counting the larger ones.  A half-wave
+  // visits the 32 keys of one evaluated tile: the group is appended by ballot, the candidates'
+  // bits of a tile are a ballot too.
   uint64_t* gb = reinterpret_cast<uint64_t*>(bins + kBitmapWords);
+  uint32_t* bm = bins;          // the candidates in a bitmap over the positions (word = tile)
+  uint32_t* gcnt = red_hist;    // [kRankDirect] entries of the group larger than each member
+  const int n_words = (n_cand + 31) >> 5;
   if (tid == 0) {
     n_eval = 0u;
     cut_entry = ~0ull;
   }
-  __syncthreads();
-  for_each_entry([&](uint64_t e, int) {
-    if ((e >> (64 - pbits)) == (prefix >> (64 - pbits)) && n_eval < (uint32_t)kRankDirect)
-      gb[min(atomicAdd(&n_eval, 1u), (uint32_t)kRankDirect - 1u)] = e;
-  });
+  __syncthreads();  // every thread has read the group's size from the histogram
+  for (int i = tid; i < kRankDirect; i += NT) gcnt[i] = 0u;
+  for (int i = tid; i < n_words; i += NT) bm[i] = 0u;
+  // entry of this thread's key in visit p0 (0: none)
+  auto entry_at = [&](int p0, int* tile) __attribute__((always_inline)) -> uint64_t {
+    const int pos = p0 + tid / kTileKeys;
+    *tile = -1;
+    if (pos < n_pos && (pos / NW) < (int)ev[pos % NW]) {
+      *tile = (int)order[pos];
+      const int key = *tile * kTileKeys + (tid % kTileKeys);
+      if (key < n_cand) return cand_entry(okc[pos * kTileKeys + tid % kTileKeys], (uint32_t)key);
+    }
+    return 0ull;
+  };
+  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  for (int p0 = 0; p0 < n_pos; p0 += NT / kTileKeys) {
+    int tile;
+    const uint64_t e = entry_at(p0, &tile);
+    const bool in = e != 0ull && (e >> (64 - pbits)) == (prefix >> (64 - pbits));
+    const uint64_t m = __ballot(in);
+    if (m) {
+      const int leader = __ffsll((unsigned long long)m) - 1;
+      uint32_t base = 0;
+      if (lane == leader) base = atomicAdd(&n_eval, (uint32_t)__popcll(m));
+      base = __builtin_amdgcn_readlane(base, leader);
+      const uint32_t at_ = base + (uint32_t)__popcll(m & below);
+      if (in && at_ < (uint32_t)kRankDirect) gb[at_] = e;
+    }
+  }
   __syncthreads();
   const int n_grp = min((int)n_eval, kRankDirect);
-  for (int i = tid; i < n_grp; i += NT) {
-    const uint64_t e = gb[i];
-    int larger = 0;
-    for (int j = 0; j < n_grp; ++j) larger += gb[j] > e ? 1 : 0;
-    if (larger == need - 1) cut_entry = e;
+  {
+    // member i against a share of the group: thread t takes member t % n_grp and share t / n_grp
+    const int parts = n_grp > 0 ? max(1, NT / n_grp) : 1;
+    if (tid < parts * n_grp) {
+      const int i = tid % n_grp, part = tid / n_grp;
+      const int j0 = part * n_grp / parts, j1 = (part + 1) * n_grp / parts;
+      const uint64_t e = gb[i];
+      uint32_t larger = 0;
+      for (int j = j0; j < j1; ++j) larger += gb[j] > e ? 1u : 0u;
+      if (larger) atomicAdd(&gcnt[i], larger);
+    }
   }
-  // the candidates (the entries >= the C-th largest) in a bitmap over the positions
-  uint32_t* bm = bins;
-  const int n_words = (n_cand + 31) >> 5;
-  for (int i = tid; i < n_words; i += NT) bm[i] = 0u;
+  __syncthreads();
+  for (int i = tid; i < n_grp; i += NT)
+    if (gcnt[i] == (uint32_t)(need - 1)) cut_entry = gb[i];
   __syncthreads();
   const uint64_t t_entry = cut_entry;
-  for_each_entry([&](uint64_t e, int key) {
-    if (e >= t_entry) atomicOr(&bm[key >> 5], 1u << (key & 31));
-  });
+  for (int p0 = 0; p0 < n_pos; p0 += NT / kTileKeys) {
+    int tile;
+    const uint64_t e = entry_at(p0, &tile);
+    const uint64_t m = __ballot(e != 0ull && e >= t_entry);
+    if ((tid & (kTileKeys - 1)) == 0 && tile >= 0) bm[tile] = (uint32_t)(m >> (lane & 32));
+  }
   __syncthreads();
   uint32_t* wpre = red_hist;  // candidates in the bitmap words before each word
   if (wave == 0) {
@@ -468,11 +506,37 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
     for (int c2 = tid; c2 < C; c2 += NT) cst_l[c2] = cst_l[c2] / den;
     gram::cosines<D, NW>(kg, cpos_l, C, cinv_l, reinterpret_cast<unsigned char*>(ring), tid);
     const float* tri = reinterpret_cast<const float*>(ring) + 1;
+    constexpr int kRowVecs = D * 2 / 16;  // 16-byte vectors of a key row
+    const uint4* k4 = reinterpret_cast<const uint4*>(a.k);
+    const uint4* v4 = reinterpret_cast<const uint4*>(a.v);
+    const size_t src0 = stat_base * kRowVecs;
+    const size_t dst0 = ((size_t)p * a.h_kv + g) * a.out_rows * kRowVecs;
     if (wave == 0) {
       gram::Greedy gr;
       gr.init(cst_l, C, lane);
       if (a.sel_score) gr.run<true>(tri, C, bp, a.lambda2[p], lane, trace_slot, trace_key);
       else gr.run<false>(tri, C, bp, a.lambda2[p], lane, trace_slot, trace_key);
+    } else if (a.k_out) {
+      // meanwhile the other waves copy the kept tail (rows bp .. bp + keep_tail - 1 of the block)
+      // and fetch the candidates' value rows into the caches for the compaction below
+      const int t1 = tid - 64, nt1 = NT - 64;
+      for (int e = t1; e < a.keep_tail * kRowVecs; e += nt1) {
+        const int r = e / kRowVecs, cv = e % kRowVecs;
+        const size_t sidx = src0 + (size_t)(L - a.keep_tail + r) * kRowVecs + cv;
+        const size_t didx = dst0 + (size_t)(bp + r) * kRowVecs + cv;
+        reinterpret_cast<uint4*>(a.k_out)[didx] = k4[sidx];
+        reinterpret_cast<uint4*>(a.v_out)[didx] = v4[sidx];
+      }
+      for (int c2 = t1; c2 < C; c2 += nt1) {
+        // one load per 128-byte line of the row
+        const uint4* row = v4 + src0 + (size_t)cpos_l[c2] * kRowVecs;
+#pragma unroll
+        for (int l = 0; l < kRowVecs; l += 8) {
+          uint32_t x;
+          asm volatile("global_load_dword %0, %1, off" : "=v"(x) : "v"(row + l) : "memory");
+        }
+      }
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     }
     __syncthreads();
     const size_t so0 = ((size_t)p * a.h_kv + g) * a.budget;
@@ -481,12 +545,10 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
       if (a.sel_score) a.sel_score[so0 + t] = t < bp ? key_float(trace_key[t]) : 0.f;
     }
     if (a.k_out) {
+      // the admitted rows (the tail is copied)
       int32_t* srt = reinterpret_cast<int32_t*>(ring);  // the triangle is dead
       gram::admitted_in_order(trace_slot, cpos_l, bp, red_hist, srt, tid, NT);
-      constexpr int kRowVecs = D * 2 / 16;
-      copy_kept_rows(reinterpret_cast<const uint4*>(a.k), reinterpret_cast<const uint4*>(a.v), srt,
-                     bp, a.keep_tail, L, kRowVecs, stat_base * kRowVecs,
-                     ((size_t)p * a.h_kv + g) * a.out_rows * kRowVecs,
+      copy_kept_rows(k4, v4, srt, bp, 0, L, kRowVecs, src0, dst0,
                      reinterpret_cast<uint4*>(a.k_out), reinterpret_cast<uint4*>(a.v_out), tid, NT);
     }
   }
