@@ -527,16 +527,16 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
         reinterpret_cast<uint4*>(a.k_out)[didx] = k4[sidx];
         reinterpret_cast<uint4*>(a.v_out)[didx] = v4[sidx];
       }
+      // one dword per 128-byte line of each row, loaded straight into LDS words that nothing
+      // reads (the histogram, cleared before its next use below)
+      uint32_t* sink = red_hist + 64 * (wave & 7);
       for (int c2 = t1; c2 < C; c2 += nt1) {
-        // one load per 128-byte line of the row
         const uint4* row = v4 + src0 + (size_t)cpos_l[c2] * kRowVecs;
 #pragma unroll
-        for (int l = 0; l < kRowVecs; l += 8) {
-          uint32_t x;
-          asm volatile("global_load_dword %0, %1, off" : "=v"(x) : "v"(row + l) : "memory");
-        }
+        for (int l = 0; l < kRowVecs; l += 8)
+          __builtin_amdgcn_global_load_lds((gptr_t)(row + l), (lptr_t)sink, 4, 0, 0);
       }
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      wait_vmem<0>();
     }
     __syncthreads();
     const size_t so0 = ((size_t)p * a.h_kv + g) * a.budget;
