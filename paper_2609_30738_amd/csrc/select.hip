@@ -679,8 +679,8 @@ __global__ __launch_bounds__(NT) void mmr_select_kernel(
     if (wave == 0) {
       gram::Greedy gr;
       gr.init(cst, C, lane);
-      if (sel_score) gr.run<true>(tri, C, bp, lam2, lane, trace_slot, trace_key);
-      else gr.run<false>(tri, C, bp, lam2, lane, trace_slot, trace_key);
+      if (sel_score) gr.run_for<true>(tri, C, bp, lam2, lane, trace_slot, trace_key);
+      else gr.run_for<false>(tri, C, bp, lam2, lane, trace_slot, trace_key);
       last = gr.last;
       if (cand_idx || cand_corr) {
         // an admitted slot reports its corr at admission: the largest of 0 and its cosines to the

@@ -220,12 +220,11 @@ struct Greedy {
   // slot that holds it (one ballot per slot group q, whose lanes hold slots 64 q + lane), then
   // its s~ cleared and the cosines to it read for the next step (group q below the admitted
   // slot's group: every lane's slot lies before it, so the entry is in its column; groups above:
-  // in its row; its own group: by lane).  The first 64 records stay in lanes of two registers
-  // until the end.
-  template <bool KEYS>
+  // in its row; its own group: by lane).  Without CHECK (|lam2| <= 1e30: a live score
+  // fmaf(lam2, corr <= 1, s~ >= -FLT_MAX) stays finite) the test for a live slot is left out.
+  template <bool KEYS, bool CHECK>
   __device__ __forceinline__ void run(const float* tri, int C, int bp, float lam2, int lane,
                                       uint32_t* trace_slot, uint32_t* trace_key) {
-    uint32_t tv_slot = 0u, tv_key = 0u;
     float gv[kSlots];
     for (int t = 0; t < bp; ++t) {
       if (t > 0) {
@@ -240,7 +239,7 @@ struct Greedy {
                                                      __builtin_elementwise_maximum(sc[2], sc[3]));
       const float wm = wave_max_to_uniform(lm);
       int slot = C - 1;  // no live slot left (every score -inf or NaN)
-      if (wm > -INFINITY) {
+      if (!CHECK || wm > -INFINITY) {
         uint64_t m = __ballot(sc[0] == wm);
         int q = 0;
 #pragma unroll
@@ -253,15 +252,9 @@ struct Greedy {
         slot = 64 * q + (__ffsll((unsigned long long)m) - 1);
       }
       last = __builtin_amdgcn_readfirstlane(slot);
-      uint32_t key = 0u;
-      if constexpr (KEYS) key = wm_key(wm, sc);
-      if (t < 64) {
-        tv_slot = lane == t ? (uint32_t)last : tv_slot;
-        if constexpr (KEYS) tv_key = lane == t ? key : tv_key;
-      } else {
-        trace_slot[t] = (uint32_t)last;
-        if constexpr (KEYS) trace_key[t] = key;
-      }
+      // the step's record (every lane stores the same value)
+      trace_slot[t] = (uint32_t)last;
+      if constexpr (KEYS) trace_key[t] = wm_key(wm, sc);
       // slot `last` leaves the race; the cosines of every slot to it for the next step
       const int ql = last >> 6, ll = last & 63;
 #pragma unroll
@@ -277,10 +270,13 @@ struct Greedy {
         }
       }
     }
-    if (lane < bp) {
-      trace_slot[lane] = tv_slot;
-      if constexpr (KEYS) trace_key[lane] = tv_key;
-    }
+  }
+  // run<KEYS, CHECK> with CHECK decided by lam2
+  template <bool KEYS>
+  __device__ __forceinline__ void run_for(const float* tri, int C, int bp, float lam2, int lane,
+                                          uint32_t* trace_slot, uint32_t* trace_key) {
+    if (__builtin_fabsf(lam2) <= 1e30f) run<KEYS, false>(tri, C, bp, lam2, lane, trace_slot, trace_key);
+    else run<KEYS, true>(tri, C, bp, lam2, lane, trace_slot, trace_key);
   }
 
   // The order key of the step's score: the largest score of the wave; a largest score of zero is

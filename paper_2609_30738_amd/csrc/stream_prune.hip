@@ -332,24 +332,28 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
   //      pass gives the first digit; each further digit counts the evaluated entries that share
   //      the digits found so far, until few enough remain to rank them directly.
   __syncthreads();  // the scores, the histogram and every wave's tile count are final
-  if (wave == 0) find_cut_bin(red_hist, kPruneBins - 1, C, lane, &cut, &bmax_bits);
-  __syncthreads();
   int max_ev = 0;
 #pragma unroll
   for (int w = 0; w < NW; ++w) max_ev = max(max_ev, (int)ev[w]);
   const int n_pos = min(n_ord, max_ev * NW);  // order positions at or after this one: not evaluated
   // the order keys of the evaluated scores, copied once into the ring (free after the pass) at
-  // [order position][key in tile]; the passes below visit them there
+  // [order position][key in tile] by waves 1.. while wave 0 finds the first digit of the cut; the
+  // passes below visit them there
   uint32_t* okc = reinterpret_cast<uint32_t*>(ring);
-  for (int p0 = 0; p0 < n_pos; p0 += NT / kTileKeys) {
-    const int pos = p0 + tid / kTileKeys;
-    if (pos < n_pos && (pos / NW) < (int)ev[pos % NW]) {
-      const int key = (int)order[pos] * kTileKeys + (tid % kTileKeys);
-      // device-coherent load: the line may still sit in this CU's vector cache with the tile's
-      // codes, read before the score was stored over them
-      if (key < n_cand)
-        okc[pos * kTileKeys + tid % kTileKeys] = order_key(__uint_as_float(__hip_atomic_load(
-            reinterpret_cast<uint32_t*>(score_u + key), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)));
+  if (wave == 0) {
+    find_cut_bin(red_hist, kPruneBins - 1, C, lane, &cut, &bmax_bits);
+  } else {
+    constexpr int kVisit = (NT - 64) / kTileKeys;  // tiles per visit
+    for (int p0 = 0; p0 < n_pos; p0 += kVisit) {
+      const int pos = p0 + (tid - 64) / kTileKeys;
+      if (pos < n_pos && (pos / NW) < (int)ev[pos % NW]) {
+        const int key = (int)order[pos] * kTileKeys + (tid % kTileKeys);
+        // device-coherent load: the line may still sit in this CU's vector cache with the tile's
+        // codes, read before the score was stored over them
+        if (key < n_cand)
+          okc[pos * kTileKeys + tid % kTileKeys] = order_key(__uint_as_float(__hip_atomic_load(
+              reinterpret_cast<uint32_t*>(score_u + key), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)));
+      }
     }
   }
   __syncthreads();
@@ -514,8 +518,8 @@ __global__ __launch_bounds__(NW * 64, 1) void window_prune_kernel(StreamArgs a) 
     if (wave == 0) {
       gram::Greedy gr;
       gr.init(cst_l, C, lane);
-      if (a.sel_score) gr.run<true>(tri, C, bp, a.lambda2[p], lane, trace_slot, trace_key);
-      else gr.run<false>(tri, C, bp, a.lambda2[p], lane, trace_slot, trace_key);
+      if (a.sel_score) gr.run_for<true>(tri, C, bp, a.lambda2[p], lane, trace_slot, trace_key);
+      else gr.run_for<false>(tri, C, bp, a.lambda2[p], lane, trace_slot, trace_key);
     } else if (a.k_out) {
       // meanwhile the other waves copy the kept tail (rows bp .. bp + keep_tail - 1 of the block)
       // and fetch the candidates' value rows into the caches for the compaction below
