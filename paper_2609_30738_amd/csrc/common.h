@@ -152,6 +152,28 @@ __device__ __forceinline__ float swap_halves(float x) {
   return __shfl_xor(x, 32, 64);
 }
 
+// The largest value over the 64 lanes (quiet NaNs are ignored: NaN only if every lane holds NaN),
+// as a uniform value: maxima within rows of 16 lanes, then across rows with row broadcasts into
+// lane 63, each step one v_max_f32 with a DPP source (two wait states before each, for the VGPR it
+// reads).
+__device__ __forceinline__ float wave_max_uniform(float v) {
+  asm("s_nop 1\n\t"
+      "v_max_f32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\t"
+      "v_max_f32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\t"
+      "v_max_f32_dpp %0, %0, %0 row_ror:4 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\t"
+      "v_max_f32_dpp %0, %0, %0 row_ror:8 row_mask:0xf bank_mask:0xf\n\t"
+      "s_nop 1\n\t"
+      "v_max_f32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n\t"
+      "s_nop 1\n\t"
+      "v_max_f32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n\t"
+      "s_nop 1"
+      : "+v"(v));
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__float_as_uint(v), 63));
+}
+
 // Online-softmax pair merge in base-2 units: (m, z) represents z * 2^m.
 __device__ __forceinline__ void merge_mz(float& m, float& z, float m2, float z2) {
   float mn = fmaxf(m, m2);

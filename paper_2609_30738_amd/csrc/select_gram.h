@@ -237,7 +237,7 @@ struct Greedy {
       static_assert(kSlots == 4, "four slot groups");
       const float lm = __builtin_elementwise_maximum(__builtin_elementwise_maximum(sc[0], sc[1]),
                                                      __builtin_elementwise_maximum(sc[2], sc[3]));
-      const float wm = wave_max_to_uniform(lm);
+      const float wm = wave_max_uniform(lm);
       int slot = C - 1;  // no live slot left (every score -inf or NaN)
       if (!CHECK || wm > -INFINITY) {
         uint64_t m = __ballot(sc[0] == wm);
@@ -295,26 +295,6 @@ struct Greedy {
     return order_key(wm);
   }
 
-  // The largest value over the 64 lanes (NaN only if every lane holds NaN), as a uniform value:
-  // maxima within rows of 16 lanes, then across rows with row broadcasts into lane 63, each step
-  // one v_max_f32 with a DPP source (two wait states before each, for the VGPR it reads).
-  __device__ __forceinline__ static float wave_max_to_uniform(float v) {
-    asm("s_nop 1\n\t"
-        "v_max_f32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
-        "s_nop 1\n\t"
-        "v_max_f32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
-        "s_nop 1\n\t"
-        "v_max_f32_dpp %0, %0, %0 row_ror:4 row_mask:0xf bank_mask:0xf\n\t"
-        "s_nop 1\n\t"
-        "v_max_f32_dpp %0, %0, %0 row_ror:8 row_mask:0xf bank_mask:0xf\n\t"
-        "s_nop 1\n\t"
-        "v_max_f32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n\t"
-        "s_nop 1\n\t"
-        "v_max_f32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n\t"
-        "s_nop 1"
-        : "+v"(v));
-    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__float_as_uint(v), 63));
-  }
 };
 
 // The positions of the admitted slots (trace_slot[0, bp), slots < C <= kMaxCand) in ascending

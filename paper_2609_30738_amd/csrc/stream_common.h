@@ -129,19 +129,6 @@ __device__ __forceinline__ float max_halves(float x) {  // max(x, x of lane ^ 32
   return __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
-// maximum over each 32-lane half of the wave (every lane of a half gets it): DPP within rows of 16
-// lanes, then the two rows of the half
-__device__ __forceinline__ float max32_f(float v) {
-#define KV_DPPF(x, CTRL) __uint_as_float(__builtin_amdgcn_mov_dpp(__float_as_uint(x), CTRL, 0xF, 0xF, true))
-  v = __builtin_elementwise_maximum(v, KV_DPPF(v, 0xB1));   // quad_perm [1,0,3,2]
-  v = __builtin_elementwise_maximum(v, KV_DPPF(v, 0x4E));   // quad_perm [2,3,0,1]
-  v = __builtin_elementwise_maximum(v, KV_DPPF(v, 0x124));  // row_ror:4
-  v = __builtin_elementwise_maximum(v, KV_DPPF(v, 0x128));  // row_ror:8
-#undef KV_DPPF
-  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __builtin_elementwise_maximum(__uint_as_float(r16[0]), __uint_as_float(r16[1]));
-}
-
 // inclusive prefix sum over the 64 lanes in lane order: steps of 1, 2, 4 and 8 lanes within each
 // row of 16 (DPP row shifts, lanes shifted in from outside the row read 0), then the last lane of
 // each row added to the rows after it (DPP row broadcasts)

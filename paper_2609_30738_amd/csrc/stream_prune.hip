@@ -39,13 +39,17 @@ constexpr float kBoundFloor = 0x1p-100f;
 constexpr float kCodeStep = 0.125f;          // code units: 1/8 of a factor of two
 
 // Pass-1 hook of candidate mode: per tile, the largest t = logit * c of every (head, window row) as
-// the number of 1/8-steps it lies below the tile's largest t (rounded down, at most 255), one byte
-// per head of the row's word in the unit's code rows, and the tile's largest t into ref[tile]
-// (LDS); a tile with a masked key gets ref = +inf (always revisited).  Both halves of the wave hold
-// the same row maxima after the exchange, so every lane stores its row's word (one store per tile).
+// the number of 1/8-steps it lies below the tile's largest t (rounded down, one less where the
+// exact number is an odd integer; at most 255), one byte per head of the row's word in the unit's
+// code rows, and the tile's largest t into ref[tile] (LDS); a tile with a masked key gets
+// ref = +inf and a tile with a NaN logit ref = NaN (both always revisited).  The row maxima of two
+// heads are merged across the wave's halves in one exchange, leaving head k in lanes 0-31 and head
+// k + NB / 2 in lanes 32-63, so each lane stores the bytes of its row's word that belong to its
+// heads (one store per tile).
 template <int NBH> struct TileCodes {
   static constexpr int kStores = 1;
-  uint32_t* codes;  // tile i at codes + 32 i: word r = window row r, byte b = head b (255 unused)
+  static_assert(NBH == 1 || NBH == 2 || NBH == 4, "one, two or four query heads per key head");
+  uint32_t* codes;  // tile i at codes + 32 i: word r = window row r, byte b < NB = head b
   float* ref;       // [n_tiles] LDS
   float c;          // softmax scale * log2(e)
   int l32, lane;
@@ -53,22 +57,31 @@ template <int NBH> struct TileCodes {
   template <int NB>
   __device__ __forceinline__ void interior(int tile, const float (&tmax)[NB]) const {
     static_assert(NB == NBH, "head count");
-    float tm[NB];
-    float r = -INFINITY;
+    constexpr int NP = NB == 4 ? 2 : 1;  // heads per lane after the exchange
+    float tm[NP];  // row maxima of t over the tile's 32 keys
+    if constexpr (NB == 1) {
+      tm[0] = max_halves(tmax[0]) * c;
+    } else {
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      tm[b] = max_halves(tmax[b]) * c;
-      r = __builtin_elementwise_maximum(r, tm[b]);
+      for (int k = 0; k < NP; ++k) {
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(tmax[k]),
+                                                        __float_as_uint(tmax[k + NB / 2]), false, false);
+        tm[k] = __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1])) * c;
+      }
     }
-    r = max32_f(r);  // the tile's largest t: the same in every lane
-    uint32_t w = 0xFFFFFFFFu;
+    const float m = NP == 2 ? __builtin_elementwise_maximum(tm[0], tm[NP - 1]) : tm[0];
+    float r = wave_max_uniform(m);  // the tile's largest t
+    if (__ballot(m != m)) r = __builtin_nanf("");
+    // code: the steps (r - t) * 8 less half a step, rounded to nearest (even) and saturated to
+    // [0, 255] by v_cvt_pk_u8_f32: never above the exact number of steps (NaN gives 0)
+    uint32_t w = 0u;
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const float steps = (r - tm[b]) * (1.f / kCodeStep);  // >= 0; NaN gives 255
-      const uint32_t code = steps < 255.f ? (uint32_t)steps : 255u;
-      w = (w & ~(0xFFu << (8 * b))) | (code << (8 * b));
-    }
-    store_word(codes + 32 * tile + l32, w);
+    for (int k = 0; k < NP; ++k)
+      w = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(r - tm[k], 1.f / kCodeStep, -0.5f), (uint32_t)k, w);
+    char* dst = reinterpret_cast<char*>(codes + 32 * tile + l32);
+    if constexpr (NB == 4) store_u16(dst + 2 * (lane >> 5), w);
+    else if constexpr (NB == 2) store_u8(dst + (lane >> 5), w);
+    else store_u8(dst, w);
     if (lane == 0) ref[tile] = r;
   }
   __device__ __forceinline__ void guarded(int tile) const {
@@ -77,6 +90,12 @@ template <int NBH> struct TileCodes {
   }
   __device__ __forceinline__ static void store_word(uint32_t* dst, uint32_t v) {
     asm volatile("global_store_dword %0, %1, off sc1" ::"v"(dst), "v"(v) : "memory");
+  }
+  __device__ __forceinline__ static void store_u16(char* dst, uint32_t v) {
+    asm volatile("global_store_short %0, %1, off sc1" ::"v"(dst), "v"(v) : "memory");
+  }
+  __device__ __forceinline__ static void store_u8(char* dst, uint32_t v) {
+    asm volatile("global_store_byte %0, %1, off sc1" ::"v"(dst), "v"(v) : "memory");
   }
 };
 
